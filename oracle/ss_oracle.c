@@ -1,0 +1,441 @@
+/*
+ * Oracle for the GMG what-if simulator -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Written from the paper (SliceScheduler, arXiv 2608.15762):
+ *   - transfer estimator, Sec. 3.3.1: t = alpha * size + c per accelerator pair,
+ *     taken in integer form as lat[k] + ceil(bytes / bw[k]) per link class k;
+ *   - simulator construction, Sec. 3.3.2: an op is ready when its local
+ *     predecessors have completed and the outputs of remote predecessors have
+ *     arrived; a queue runs at most one op at a time; completion = start +
+ *     operator estimate; ready and executing ops determine the tensors
+ *     resident in HBM;
+ *   - event-driven simulation and what-if, Sec. 3.3.3: advance every queue,
+ *     score a placement from completion-time statistics;
+ *   - selection, Sec. 3.4.2 and Alg. 1: discard placements that run out of
+ *     memory, keep the one with the smallest average completion time.
+ *
+ * Readings where the paper is silent (each is listed in the design notes):
+ *   - an op runs non-preemptively inside ONE idle slice of its device; after
+ *     the last finite slice a device is free forever (open tail);
+ *   - contract A serves each device's ops in index order (index order is the
+ *     priority order of the GMG); the ready-time dispatch of Sec. 3.3.2 is
+ *     the SSO_READY_ORDER variant;
+ *   - a transfer is pure latency starting at the producer's finish, one per
+ *     (tensor, destination device), shared by all consumers there;
+ *   - memory: an op's output occupies its device from the op's start until the
+ *     later of its last local consumer's finish and its last outgoing
+ *     transfer's arrival; a remote copy occupies the destination from the
+ *     transfer's start (the producer's finish; the receive buffer exists
+ *     before the data moves, Sec. 3.5.2) until its last consumer there
+ *     finishes; outputs without consumers stay resident; intervals are
+ *     half-open; a device violates when its peak exceeds its capacity.
+ *
+ * Parity: pinned by closed forms, bounds, brute force and hand-worked cases in
+ * the CPU test-suite (no printed worked example exists in the paper).
+ */
+#include "ss_oracle.h"
+
+#include <stdlib.h>
+#include <string.h>
+
+/* ---------------------------------------------------------------- estimators */
+
+/* Transfer estimator X(u, s, t): zero on the same device, else
+ * lat + ceil(out_bytes[u] / bw) of the (s, t) link class (Sec. 3.3.1). */
+static int64_t transfer_time(const sso_gmg *g, int64_t u, int64_t s, int64_t t) {
+  if (s == t) return 0;
+  const int k = g->link_class[s * g->n_dev + t];
+  const int64_t bytes = g->out_bytes[u];
+  const int64_t bw = g->bw[k];
+  return g->lat[k] + (bytes + bw - 1) / bw;
+}
+
+/* Operator estimator: duration of op v on device d (per device class). */
+static int64_t op_duration(const sso_gmg *g, int64_t v, int64_t d) {
+  return g->dur[v * g->n_class + g->dev_class[d]];
+}
+
+/* Earliest s >= t such that [s, s + w) lies inside one idle slice of device d.
+ * Slices are sorted; the start max(t, a_k) does not decrease with k, so the
+ * first slice that can hold the op gives the earliest start. */
+static int64_t earliest_fit(const sso_gmg *g, int64_t d, int64_t t, int64_t w) {
+  for (int64_t k = g->slice_ptr[d]; k < g->slice_ptr[d + 1]; ++k) {
+    const int64_t a = g->slice_begin[k], e = g->slice_end[k];
+    const int64_t s = t > a ? t : a;
+    if (s + w <= e) return s;
+  }
+  return -1; /* not reached: the last slice of every device is open */
+}
+
+/* Ready time: the later of the request's release (and t0 = 0) and, over every
+ * predecessor u, its finish plus the transfer of its output to v's device. */
+static int64_t ready_time(const sso_gmg *g, const uint8_t *place, const int64_t *fin, int64_t v) {
+  int64_t r = g->release[g->op_req[v]];
+  if (r < 0) r = 0;
+  for (int64_t e = g->pred_ptr[v]; e < g->pred_ptr[v + 1]; ++e) {
+    const int64_t u = g->pred_idx[e];
+    const int64_t arrive = fin[u] + transfer_time(g, u, place[u], place[v]);
+    if (arrive > r) r = arrive;
+  }
+  return r;
+}
+
+/* ---------------------------------------------------------------- successors */
+
+typedef struct {
+  int64_t *ptr; /* [n_ops+1] */
+  int64_t *idx; /* ascending within each op */
+} succ_csr;
+
+static int build_succ(const sso_gmg *g, succ_csr *s) {
+  const int64_t N = g->n_ops, E = g->pred_ptr[N];
+  s->ptr = (int64_t *)calloc((size_t)N + 1, sizeof(int64_t));
+  s->idx = (int64_t *)malloc(((size_t)E + 1) * sizeof(int64_t));
+  int64_t *fill = (int64_t *)calloc((size_t)N + 1, sizeof(int64_t));
+  if (!s->ptr || !s->idx || !fill) {
+    free(s->ptr); free(s->idx); free(fill);
+    return -1;
+  }
+  for (int64_t e = 0; e < E; ++e) s->ptr[g->pred_idx[e] + 1]++;
+  for (int64_t v = 0; v < N; ++v) s->ptr[v + 1] += s->ptr[v];
+  /* visiting consumers v in increasing order keeps each list ascending */
+  for (int64_t v = 0; v < N; ++v)
+    for (int64_t e = g->pred_ptr[v]; e < g->pred_ptr[v + 1]; ++e) {
+      const int64_t u = g->pred_idx[e];
+      s->idx[s->ptr[u] + fill[u]++] = v;
+    }
+  free(fill);
+  return 0;
+}
+
+static void free_succ(succ_csr *s) { free(s->ptr); free(s->idx); }
+
+/* ---------------------------------------------------------------- schedules */
+
+/* Contract A: ops in index order; each starts at the earliest fit at or after
+ * max(ready, the device's previous finish); one op at a time per device. */
+static void schedule_index_order(const sso_gmg *g, const uint8_t *place, int64_t *clock, int64_t *st,
+                                 int64_t *fin) {
+  for (int64_t d = 0; d < g->n_dev; ++d) clock[d] = 0;
+  for (int64_t v = 0; v < g->n_ops; ++v) {
+    const int64_t d = place[v];
+    const int64_t w = op_duration(g, v, d);
+    const int64_t ready = ready_time(g, place, fin, v);
+    const int64_t t = ready > clock[d] ? ready : clock[d];
+    st[v] = earliest_fit(g, d, t, w);
+    fin[v] = st[v] + w;
+    clock[d] = fin[v];
+  }
+}
+
+/* binary min-heap of (ready, op) pairs */
+typedef struct { int64_t ready, op; } ready_item;
+
+static int item_less(ready_item a, ready_item b) {
+  return a.ready < b.ready || (a.ready == b.ready && a.op < b.op);
+}
+
+static void heap_push(ready_item *h, int64_t *n, ready_item x) {
+  int64_t i = (*n)++;
+  h[i] = x;
+  while (i > 0) {
+    const int64_t p = (i - 1) / 2;
+    if (!item_less(h[i], h[p])) break;
+    ready_item t = h[i]; h[i] = h[p]; h[p] = t;
+    i = p;
+  }
+}
+
+static ready_item heap_pop(ready_item *h, int64_t *n) {
+  ready_item top = h[0];
+  h[0] = h[--(*n)];
+  int64_t i = 0;
+  for (;;) {
+    const int64_t l = 2 * i + 1, r = l + 1;
+    int64_t m = i;
+    if (l < *n && item_less(h[l], h[m])) m = l;
+    if (r < *n && item_less(h[r], h[m])) m = r;
+    if (m == i) break;
+    ready_item t = h[i]; h[i] = h[m]; h[m] = t;
+    i = m;
+  }
+  return top;
+}
+
+/* Ready-order variant: repeatedly dispatch the op with the earliest ready
+ * time among those whose predecessors are all scheduled (ties to the lower
+ * index), then place it on its device exactly as contract A does. */
+static int schedule_ready_order(const sso_gmg *g, const uint8_t *place, const succ_csr *sc, int64_t *clock,
+                                int64_t *st, int64_t *fin) {
+  const int64_t N = g->n_ops;
+  int64_t *missing = (int64_t *)malloc(((size_t)N + 1) * sizeof(int64_t));
+  ready_item *heap = (ready_item *)malloc(((size_t)N + 1) * sizeof(ready_item));
+  if (!missing || !heap) { free(missing); free(heap); return -1; }
+  int64_t hn = 0;
+  for (int64_t d = 0; d < g->n_dev; ++d) clock[d] = 0;
+  for (int64_t v = 0; v < N; ++v) {
+    missing[v] = g->pred_ptr[v + 1] - g->pred_ptr[v];
+    if (missing[v] == 0) heap_push(heap, &hn, (ready_item){ready_time(g, place, fin, v), v});
+  }
+  while (hn > 0) {
+    const ready_item it = heap_pop(heap, &hn);
+    const int64_t v = it.op, d = place[v];
+    const int64_t w = op_duration(g, v, d);
+    const int64_t t = it.ready > clock[d] ? it.ready : clock[d];
+    st[v] = earliest_fit(g, d, t, w);
+    fin[v] = st[v] + w;
+    clock[d] = fin[v];
+    for (int64_t e = sc->ptr[v]; e < sc->ptr[v + 1]; ++e) {
+      const int64_t x = sc->idx[e];
+      if (--missing[x] == 0) heap_push(heap, &hn, (ready_item){ready_time(g, place, fin, x), x});
+    }
+  }
+  free(missing);
+  free(heap);
+  return 0;
+}
+
+/* ---------------------------------------------------------------- memory */
+
+typedef struct { int64_t dev, lo, hi, bytes; } interval;
+
+/* Residency intervals of one scheduled candidate (see the memory reading in
+ * the file header).  Returns the count, or -1 on allocation failure. */
+static int64_t residency_intervals(const sso_gmg *g, const uint8_t *place, const succ_csr *sc, const int64_t *st,
+                                   const int64_t *fin, interval **out) {
+  const int64_t N = g->n_ops;
+  int64_t cap = N + sc->ptr[N] + 1, n = 0;
+  interval *iv = (interval *)malloc((size_t)cap * sizeof(interval));
+  if (!iv) return -1;
+  for (int64_t v = 0; v < N; ++v) {
+    const int64_t d = place[v];
+    const int64_t b = g->out_bytes[v];
+    const int64_t s0 = sc->ptr[v], s1 = sc->ptr[v + 1];
+    /* own output on d: from v's start until every local consumer has finished
+     * and every outgoing transfer has arrived; kept forever without consumers */
+    int64_t free_at = SSO_INF;
+    if (s1 > s0) {
+      free_at = fin[v];
+      for (int64_t e = s0; e < s1; ++e) {
+        const int64_t x = sc->idx[e], dx = place[x];
+        const int64_t t = (dx == d) ? fin[x] : fin[v] + transfer_time(g, v, d, dx);
+        if (t > free_at) free_at = t;
+      }
+    }
+    iv[n++] = (interval){d, st[v], free_at, b};
+    /* one remote copy per destination device, from v's finish until the last
+     * consumer on that device finishes */
+    for (int64_t e = s0; e < s1; ++e) {
+      const int64_t dx = place[sc->idx[e]];
+      if (dx == d) continue;
+      int seen = 0;
+      for (int64_t e2 = s0; e2 < e; ++e2)
+        if (place[sc->idx[e2]] == dx) seen = 1;
+      if (seen) continue;
+      int64_t last = 0;
+      for (int64_t e2 = s0; e2 < s1; ++e2)
+        if (place[sc->idx[e2]] == dx && fin[sc->idx[e2]] > last) last = fin[sc->idx[e2]];
+      iv[n++] = (interval){dx, fin[v], last, b};
+    }
+  }
+  *out = iv;
+  return n;
+}
+
+typedef struct { int64_t time; int64_t is_alloc; int64_t delta; } mem_event;
+
+static int event_cmp(const void *pa, const void *pb) {
+  const mem_event *a = (const mem_event *)pa, *b = (const mem_event *)pb;
+  if (a->time != b->time) return a->time < b->time ? -1 : 1;
+  /* at equal times frees come first: intervals are half-open */
+  if (a->is_alloc != b->is_alloc) return a->is_alloc < b->is_alloc ? -1 : 1;
+  return 0;
+}
+
+/* peak[d] = max over time of the bytes live on d; sweep over sorted endpoints */
+static int peak_by_sweep(const sso_gmg *g, const interval *iv, int64_t n, int64_t *peak) {
+  mem_event *ev = (mem_event *)malloc(((size_t)2 * n + 1) * sizeof(mem_event));
+  if (!ev) return -1;
+  for (int64_t d = 0; d < g->n_dev; ++d) {
+    int64_t m = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      if (iv[i].dev != d) continue;
+      ev[m++] = (mem_event){iv[i].lo, 1, iv[i].bytes};
+      if (iv[i].hi != SSO_INF) ev[m++] = (mem_event){iv[i].hi, 0, -iv[i].bytes};
+    }
+    qsort(ev, (size_t)m, sizeof(mem_event), event_cmp);
+    int64_t live = 0, best = 0;
+    for (int64_t i = 0; i < m; ++i) {
+      live += ev[i].delta;
+      if (live > best) best = live;
+    }
+    peak[d] = best;
+  }
+  free(ev);
+  return 0;
+}
+
+/* peak[d] = max over allocation instants t of sum of bytes with lo <= t < hi */
+static void peak_by_pairs(const sso_gmg *g, const interval *iv, int64_t n, int64_t *peak) {
+  for (int64_t d = 0; d < g->n_dev; ++d) peak[d] = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t t = iv[i].lo;
+    int64_t live = 0;
+    for (int64_t j = 0; j < n; ++j)
+      if (iv[j].dev == iv[i].dev && iv[j].lo <= t && t < iv[j].hi) live += iv[j].bytes;
+    if (live > peak[iv[i].dev]) peak[iv[i].dev] = live;
+  }
+}
+
+/* ---------------------------------------------------------------- what-if */
+
+static int valid_placement(const sso_gmg *g, const uint8_t *place) {
+  for (int64_t v = 0; v < g->n_ops; ++v)
+    if (place[v] >= g->n_dev) return 0;
+  return 1;
+}
+
+static int simulate_with(const sso_gmg *g, const succ_csr *sc, const uint8_t *place, int dispatch, int64_t *st,
+                         int64_t *fin, int64_t *clock, int64_t *peak_buf, int64_t *makespan, int64_t *peak,
+                         uint8_t *violation, int64_t *slack, int64_t *sumfin) {
+  const int64_t N = g->n_ops, D = g->n_dev, R = g->n_req;
+  if (!valid_placement(g, place)) {
+    /* a placement naming a device outside the set is not simulated */
+    *makespan = INT64_MAX;
+    *sumfin = INT64_MAX;
+    *violation = 4;
+    if (peak) for (int64_t d = 0; d < D; ++d) peak[d] = 0;
+    if (slack) for (int64_t r = 0; r < R; ++r) slack[r] = INT64_MIN;
+    return 0;
+  }
+  if (dispatch == SSO_READY_ORDER) {
+    if (schedule_ready_order(g, place, sc, clock, st, fin) != 0) return -1;
+  } else {
+    schedule_index_order(g, place, clock, st, fin);
+  }
+  /* completion-time statistics (Sec. 3.3.3): makespan from t0 = 0, per-request
+   * completion (its release when it has no ops) against its deadline, and the
+   * sum of finish times (average completion time times N, Sec. 3.4.2) */
+  int64_t ms = 0, sum = 0;
+  for (int64_t v = 0; v < N; ++v) {
+    if (fin[v] > ms) ms = fin[v];
+    sum += fin[v];
+  }
+  *makespan = ms;
+  *sumfin = sum;
+  if (slack) {
+    for (int64_t r = 0; r < R; ++r) slack[r] = g->release[r];
+    for (int64_t v = 0; v < N; ++v)
+      if (fin[v] > slack[g->op_req[v]]) slack[g->op_req[v]] = fin[v];
+    for (int64_t r = 0; r < R; ++r) slack[r] = g->deadline[r] - slack[r];
+  }
+  interval *iv = 0;
+  const int64_t n = residency_intervals(g, place, sc, st, fin, &iv);
+  if (n < 0) return -1;
+  const int rc = peak_by_sweep(g, iv, n, peak_buf);
+  free(iv);
+  if (rc != 0) return -1;
+  uint8_t viol = 0;
+  for (int64_t d = 0; d < D; ++d)
+    if (peak_buf[d] > g->cap[d]) viol = 1;
+  *violation = viol;
+  if (peak) memcpy(peak, peak_buf, (size_t)D * sizeof(int64_t));
+  return 0;
+}
+
+typedef struct {
+  int64_t *st, *fin, *clock, *peak;
+} work_bufs;
+
+static int alloc_work(const sso_gmg *g, work_bufs *w) {
+  w->st = (int64_t *)malloc(((size_t)g->n_ops + 1) * sizeof(int64_t));
+  w->fin = (int64_t *)malloc(((size_t)g->n_ops + 1) * sizeof(int64_t));
+  w->clock = (int64_t *)malloc(((size_t)g->n_dev + 1) * sizeof(int64_t));
+  w->peak = (int64_t *)malloc(((size_t)g->n_dev + 1) * sizeof(int64_t));
+  return (w->st && w->fin && w->clock && w->peak) ? 0 : -1;
+}
+
+static void free_work(work_bufs *w) { free(w->st); free(w->fin); free(w->clock); free(w->peak); }
+
+int sso_simulate_one(const sso_gmg *g, const uint8_t *place, int dispatch, int64_t *st, int64_t *fin,
+                     int64_t *makespan, int64_t *peak, uint8_t *violation, int64_t *slack, int64_t *sumfin) {
+  succ_csr sc;
+  work_bufs w;
+  if (build_succ(g, &sc) != 0) return -1;
+  if (alloc_work(g, &w) != 0) { free_succ(&sc); free_work(&w); return -1; }
+  const int rc = simulate_with(g, &sc, place, dispatch, w.st, w.fin, w.clock, w.peak, makespan, peak, violation,
+                               slack, sumfin);
+  if (rc == 0 && valid_placement(g, place)) {
+    if (st) memcpy(st, w.st, (size_t)g->n_ops * sizeof(int64_t));
+    if (fin) memcpy(fin, w.fin, (size_t)g->n_ops * sizeof(int64_t));
+  }
+  free_work(&w);
+  free_succ(&sc);
+  return rc;
+}
+
+int sso_simulate_batch(const sso_gmg *g, const uint8_t *places, int64_t B, int dispatch, int64_t *makespan,
+                       int64_t *peak, uint8_t *violation, int64_t *slack, int64_t *sumfin) {
+  succ_csr sc;
+  work_bufs w;
+  if (build_succ(g, &sc) != 0) return -1;
+  if (alloc_work(g, &w) != 0) { free_succ(&sc); free_work(&w); return -1; }
+  int rc = 0;
+  for (int64_t b = 0; b < B && rc == 0; ++b)
+    rc = simulate_with(g, &sc, places + b * g->n_ops, dispatch, w.st, w.fin, w.clock, w.peak, &makespan[b],
+                       peak ? peak + b * g->n_dev : 0, &violation[b], slack ? slack + b * g->n_req : 0,
+                       &sumfin[b]);
+  free_work(&w);
+  free_succ(&sc);
+  return rc;
+}
+
+static int peak_common(const sso_gmg *g, const uint8_t *place, const int64_t *st, const int64_t *fin,
+                       int64_t *peak, int pairwise) {
+  succ_csr sc;
+  if (build_succ(g, &sc) != 0) return -1;
+  interval *iv = 0;
+  const int64_t n = residency_intervals(g, place, &sc, st, fin, &iv);
+  free_succ(&sc);
+  if (n < 0) return -1;
+  int rc = 0;
+  if (pairwise)
+    peak_by_pairs(g, iv, n, peak);
+  else
+    rc = peak_by_sweep(g, iv, n, peak);
+  free(iv);
+  return rc;
+}
+
+int sso_peak_sweep(const sso_gmg *g, const uint8_t *place, const int64_t *st, const int64_t *fin, int64_t *peak) {
+  return peak_common(g, place, st, fin, peak, 0);
+}
+
+int sso_peak_pairwise(const sso_gmg *g, const uint8_t *place, const int64_t *st, const int64_t *fin,
+                      int64_t *peak) {
+  return peak_common(g, place, st, fin, peak, 1);
+}
+
+/* Alg. 1: record feasible candidates, return the best.  Feasible = no memory
+ * violation and a valid placement; optionally also no missed deadline.  Best =
+ * smallest key (sum of finish times = N x average completion time, or the
+ * makespan), ties to the lower candidate index. */
+void sso_select_best(int64_t B, int64_t n_req, const uint8_t *violation, const int64_t *key, const int64_t *slack,
+                     int require_sla, int64_t *best_idx, int64_t *best_key) {
+  int64_t bi = -1, bk = INT64_MAX;
+  for (int64_t b = 0; b < B; ++b) {
+    if (violation[b] != 0) continue;
+    if (require_sla) {
+      int ok = 1;
+      for (int64_t r = 0; r < n_req; ++r)
+        if (slack[b * n_req + r] < 0) ok = 0;
+      if (!ok) continue;
+    }
+    if (bi < 0 || key[b] < bk) {
+      bi = b;
+      bk = key[b];
+    }
+  }
+  *best_idx = bi;
+  *best_key = bk;
+}
