@@ -1,0 +1,172 @@
+/*
+ * ss.h -- C ABI of the MI355X what-if simulator over the Global Mapping Graph.
+ *
+ * The method is SliceScheduler's global simulator (arXiv 2608.15762,
+ * Sec. 3.3) driven by the parallel candidate loop of its incremental
+ * scheduling algorithm (Alg. 1, Sec. 3.4): a GMG snapshot (Sec. 3.2) plus a
+ * batch of candidate placements goes in; per candidate the simulated
+ * makespan, per-device peak memory, a violation verdict and per-request SLA
+ * slack come out, and the best feasible candidate is selected.
+ *
+ * Every entry point returns SS_OK (0) or a negative SS_ERR_* code and never
+ * throws; ss_last_error() gives a message for the calling thread's last
+ * failure.  All times are int64 microseconds and all sizes int64 bytes.
+ */
+#ifndef SS_H
+#define SS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SS_OK 0
+#define SS_ERR_INVALID_ARG (-1)  /* null pointer, negative count, unknown flag or layout */
+#define SS_ERR_INVALID_GMG (-2)  /* the snapshot breaks a rule listed under ss_gmg_desc */
+#define SS_ERR_OOM (-3)          /* host or device allocation failed */
+#define SS_ERR_DEVICE (-4)       /* a HIP call or kernel launch failed */
+#define SS_ERR_UNSUPPORTED (-5)  /* valid input beyond this build's limits (see ss_gmg_desc) */
+
+#define SS_TIME_INF INT64_MAX    /* end of a device's last (open) idle slice */
+
+#define SS_LAYOUT_ROW_MAJOR 0    /* placements[b * n_ops + v] = device of op v in candidate b */
+
+#define SS_VIOLATION_MEMORY 0x1  /* some device's peak memory exceeds its capacity */
+#define SS_VIOLATION_INVALID 0x4 /* the placement names a device id >= n_dev; not simulated */
+
+#define SS_SELECT_REQUIRE_SLA 0x1 /* feasible also requires every request's slack >= 0 */
+
+typedef struct ss_gmg ss_gmg;
+
+/*
+ * A GMG snapshot (Sec. 3.2): the Shape DAG of the operators to place, their
+ * estimator outputs, and the Accelerator Set with its pre-existing load.
+ * All pointers are HOST pointers; ss_gmg_load copies what it needs, so the
+ * caller may free them when it returns.
+ *
+ *   n_ops N        operators; index order is a topological order and is the
+ *                  dispatch priority of every device queue (Sec. 3.3.2).
+ *   pred_ptr[N+1], pred_idx[E]  predecessor CSR: the data dependencies of op v
+ *                  are pred_idx[pred_ptr[v] .. pred_ptr[v+1]), strictly
+ *                  increasing and each < v; pred_ptr[0] = 0.
+ *   op_req[N]      request of each op, in [0, n_req).
+ *   dur[N][n_class] operator estimator (Sec. 3.3.1): duration of op v on a
+ *                  device of class c, >= 1.
+ *   out_bytes[N]   size of op v's output tensor (Sec. 3.2 metadata), >= 0.
+ *   dev_class[D]   class of each device, in [0, n_class).  1 <= D <= 255.
+ *   link_class[D][D] link class of each ordered device pair (diagonal
+ *                  ignored), in [0, n_link).
+ *   bw[K], lat[K]  transfer estimator t = alpha*size + c per link class
+ *                  (Sec. 3.3.1) in integer form lat + ceil(bytes / bw);
+ *                  bw >= 1 byte/us, lat >= 0.
+ *   slice_ptr[D+1], slice_begin[], slice_end[]  idle slices of device d are
+ *                  [slice_begin[k], slice_end[k]) for k in
+ *                  [slice_ptr[d], slice_ptr[d+1]): at least one, begin >= 0,
+ *                  begin < end, end <= next begin, every end finite except the
+ *                  last, which is SS_TIME_INF (the device is free from then on).
+ *                  At most 65535 slices per device.
+ *   cap[D]         memory available to the simulated tensors on each device.
+ *   release[R], deadline[R]  per-request arrival (>= 0) and absolute SLA
+ *                  deadline (|deadline| < 2^62).
+ *
+ * The loader also rejects snapshots whose time horizon could overflow:
+ * H = max_d last-slice start + max_r release + sum_v max_c dur[v][c]
+ *     + sum_v (outdeg(v) + 1) * max_k (lat[k] + ceil(out_bytes[v] / bw[k]))
+ * must stay below 2^62, N * H below 2^63, and sum_v out_bytes[v] * (D + 1)
+ * below 2^63.
+ */
+typedef struct ss_gmg_desc {
+  int64_t n_ops, n_edges, n_dev, n_class, n_link, n_req;
+  const int32_t *pred_ptr;
+  const int32_t *pred_idx;
+  const int32_t *op_req;
+  const int64_t *dur;
+  const int64_t *out_bytes;
+  const int32_t *dev_class;
+  const uint8_t *link_class;
+  const int64_t *bw;
+  const int64_t *lat;
+  const int64_t *slice_ptr;
+  const int64_t *slice_begin;
+  const int64_t *slice_end;
+  const int64_t *cap;
+  const int64_t *release;
+  const int64_t *deadline;
+} ss_gmg_desc;
+
+/*
+ * Validate a snapshot (rules above), precompute its transfer table and
+ * successor lists, and stage it in the memory of the CURRENT HIP device
+ * (once per GMG; Sec. 3.3.2 builds the simulator from the snapshot).
+ * On success *out owns the staged copy until ss_gmg_free.  A loaded GMG is
+ * read-only and may be used by concurrent calls on any streams of that device.
+ * Errors: SS_ERR_INVALID_ARG, SS_ERR_INVALID_GMG, SS_ERR_OOM, SS_ERR_DEVICE.
+ */
+int ss_gmg_load(const ss_gmg_desc *desc, ss_gmg **out);
+
+/* Release a GMG (synchronises the device first).  NULL is a no-op. */
+void ss_gmg_free(ss_gmg *g);
+
+/* Sizes of a loaded GMG; any output pointer may be NULL. */
+int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req);
+
+/*
+ * What-if simulation of B candidate placements at once (Sec. 3.3.3 and the
+ * "in parallel" candidate loop of Alg. 1).  For each candidate b:
+ *   - ops run in index order on their devices, one at a time, each starting
+ *     at the earliest instant >= max(ready time, the device's previous
+ *     finish) at which it fits entirely inside one idle slice; the ready time
+ *     is the later of the request's release and, over the predecessors, their
+ *     finish plus the transfer estimate when they ran on another device
+ *     (Sec. 3.3.2);
+ *   - memory: an op's output occupies its device from the op's start until
+ *     its last local consumer finishes and its last outgoing transfer has
+ *     arrived (forever if it has no consumer); each (output, remote device)
+ *     pair holds one copy there from the producer's finish until the last
+ *     consumer on that device finishes; peak = the maximum over time of the
+ *     bytes resident on a device (half-open intervals) (Sec. 3.3.2, 3.5.2).
+ * Outputs (DEVICE pointers, caller-owned, row-major):
+ *   out_makespan[B]      latest finish time (t0 = 0)              (required)
+ *   out_peak_mem[B][D]   per-device peak bytes                    (nullable)
+ *   out_violation[B]     SS_VIOLATION_* bits, 0 = feasible        (required)
+ *   out_sla_slack[B][R]  deadline[r] - completion of request r (its release
+ *                        when it has no ops); may be negative     (nullable)
+ *   out_sumfin[B]        sum of finish times = N x the average completion
+ *                        time that Sec. 3.4.2 minimises           (nullable)
+ * A candidate naming a device >= n_dev is not simulated: violation =
+ * SS_VIOLATION_INVALID, makespan = sumfin = INT64_MAX, peak = 0 and slack =
+ * INT64_MIN.  This is a per-candidate result, not a call error.
+ * placements: DEVICE pointer, uint8 [B][n_ops] for SS_LAYOUT_ROW_MAJOR.
+ * The call is asynchronous on hip_stream (NULL = the null stream); inputs must
+ * stay valid and outputs are defined once that stream has been synchronised.
+ * It allocates stream-ordered scratch on hip_stream for the duration of the
+ * work.  B = 0 is a no-op.  Results are bit-identical to a sequential CPU
+ * evaluation of the same rules.
+ * Errors: SS_ERR_INVALID_ARG, SS_ERR_OOM, SS_ERR_DEVICE, SS_ERR_UNSUPPORTED.
+ */
+int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int64_t B, int layout, int64_t *out_makespan,
+                      int64_t *out_peak_mem, uint8_t *out_violation, int64_t *out_sla_slack, int64_t *out_sumfin,
+                      void *hip_stream);
+
+/*
+ * Best-candidate selection of Alg. 1 / Sec. 3.4.2: discard infeasible
+ * candidates (violation != 0, and with SS_SELECT_REQUIRE_SLA also any
+ * negative slack), then take the smallest key, ties to the lowest index.
+ * key is out_sumfin (the average-completion objective) or out_makespan.
+ * violation[B], key[B], sla_slack[B][n_req] (needed only with
+ * SS_SELECT_REQUIRE_SLA) are DEVICE pointers; out_best is a DEVICE int64[2]
+ * receiving {index or -1, key or INT64_MAX}.  Asynchronous on hip_stream.
+ * Errors: SS_ERR_INVALID_ARG, SS_ERR_OOM, SS_ERR_DEVICE.
+ */
+int ss_select_best(const ss_gmg *g, const uint8_t *violation, const int64_t *key, const int64_t *sla_slack,
+                   int64_t B, int flags, int64_t *out_best, void *hip_stream);
+
+/* Message for the calling thread's most recent failed call ("" if none). */
+const char *ss_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SS_H */

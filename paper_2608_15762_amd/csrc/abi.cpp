@@ -1,0 +1,57 @@
+// C ABI entry points: argument checks, error reporting, dispatch to the
+// kernel drivers.  The GMG loader lives in gmg_load.cpp.
+#include <string>
+
+#include "ss_internal.h"
+
+namespace {
+thread_local std::string g_last_error;
+
+int check_device(const ss_gmg *g) {
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return ss_set_error(SS_ERR_DEVICE, "hipGetDevice failed");
+  if (cur != g->device)
+    return ss_set_error(SS_ERR_INVALID_ARG, "the current HIP device is not the one the GMG was loaded on");
+  return SS_OK;
+}
+}  // namespace
+
+int ss_set_error(int code, const std::string &msg) {
+  g_last_error = msg;
+  return code;
+}
+
+void ss_clear_error() { g_last_error.clear(); }
+
+extern "C" const char *ss_last_error(void) { return g_last_error.c_str(); }
+
+extern "C" int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int64_t B, int layout,
+                                 int64_t *out_makespan, int64_t *out_peak_mem, uint8_t *out_violation,
+                                 int64_t *out_sla_slack, int64_t *out_sumfin, void *hip_stream) {
+  ss_clear_error();
+  if (!g) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: g is NULL");
+  if (B < 0) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: B < 0");
+  if (layout != SS_LAYOUT_ROW_MAJOR) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: unknown layout");
+  if (B == 0) return SS_OK;
+  if (!out_makespan || !out_violation)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: out_makespan and out_violation are required");
+  if (!placements && g->n_ops > 0) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: placements is NULL");
+  const int rc = check_device(g);
+  if (rc != SS_OK) return rc;
+  return ss_run_simulate(g, placements, B, out_makespan, out_peak_mem, out_violation, out_sla_slack, out_sumfin,
+                         static_cast<hipStream_t>(hip_stream));
+}
+
+extern "C" int ss_select_best(const ss_gmg *g, const uint8_t *violation, const int64_t *key,
+                              const int64_t *sla_slack, int64_t B, int flags, int64_t *out_best, void *hip_stream) {
+  ss_clear_error();
+  if (!g || !out_best) return ss_set_error(SS_ERR_INVALID_ARG, "ss_select_best: g and out_best are required");
+  if (B < 0 || (flags & ~SS_SELECT_REQUIRE_SLA))
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_select_best: B < 0 or unknown flag");
+  const int require_sla = (flags & SS_SELECT_REQUIRE_SLA) && g->n_req > 0;
+  if (B > 0 && (!violation || !key || (require_sla && !sla_slack)))
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_select_best: violation, key (and slack with REQUIRE_SLA) required");
+  const int rc = check_device(g);
+  if (rc != SS_OK) return rc;
+  return ss_run_select(g, violation, key, sla_slack, B, require_sla, out_best, static_cast<hipStream_t>(hip_stream));
+}

@@ -1,0 +1,231 @@
+// GMG snapshot loader: validation, load-time precompute and one-time staging
+// of the snapshot in device memory (the simulator is built once per GMG,
+// Sec. 3.3.2; the per-candidate work happens in simulate.hip).
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <sstream>
+#include <vector>
+
+#include "ss_internal.h"
+
+namespace {
+
+using i128 = __int128;
+constexpr i128 kTimeLimit = (i128)1 << 62;
+constexpr i128 kSumLimit = (i128)1 << 63;
+
+struct Packer {
+  std::vector<unsigned char> host;
+  size_t add(const void *src, size_t bytes) {
+    size_t off = (host.size() + 255) & ~size_t(255);
+    host.resize(off + bytes);
+    if (bytes && src) std::memcpy(host.data() + off, src, bytes);
+    return off;
+  }
+  template <class T>
+  size_t add(const std::vector<T> &v) {
+    return add(v.data(), v.size() * sizeof(T));
+  }
+};
+
+int bad(const std::string &msg) { return ss_set_error(SS_ERR_INVALID_GMG, "invalid GMG: " + msg); }
+
+}  // namespace
+
+extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
+  ss_clear_error();
+  if (!out) return ss_set_error(SS_ERR_INVALID_ARG, "ss_gmg_load: out is NULL");
+  *out = nullptr;
+  if (!d) return ss_set_error(SS_ERR_INVALID_ARG, "ss_gmg_load: desc is NULL");
+  const int64_t N = d->n_ops, E = d->n_edges, D = d->n_dev, C = d->n_class, K = d->n_link, R = d->n_req;
+  if (N < 0 || E < 0 || N >= INT32_MAX || E >= INT32_MAX) return bad("n_ops and n_edges must be in [0, 2^31-1)");
+  if (D < 1 || D > 255) return bad("n_dev must be in [1, 255]");
+  if (C < 1 || C > INT32_MAX || K < 1 || K > 256 || R < 0 || R >= INT32_MAX) return bad("bad n_class, n_link or n_req");
+  if (N > 0 && R < 1) return bad("ops need at least one request");
+  if (!d->pred_ptr || (E > 0 && !d->pred_idx) || (N > 0 && (!d->op_req || !d->dur || !d->out_bytes)) ||
+      !d->dev_class || !d->link_class || !d->bw || !d->lat || !d->slice_ptr || !d->slice_begin || !d->slice_end ||
+      !d->cap || (R > 0 && (!d->release || !d->deadline)))
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_gmg_load: a required array is NULL");
+
+  try {
+    // ------------------------------------------------------------------ DAG
+    if (d->pred_ptr[0] != 0 || d->pred_ptr[N] != E) return bad("pred_ptr must start at 0 and end at n_edges");
+    for (int64_t v = 0; v < N; ++v)
+      if (d->pred_ptr[v + 1] < d->pred_ptr[v] || d->pred_ptr[v + 1] > E) return bad("pred_ptr must be non-decreasing");
+    std::vector<int32_t> outdeg(N, 0);
+    for (int64_t v = 0; v < N; ++v) {
+      const int64_t a = d->pred_ptr[v], b = d->pred_ptr[v + 1];
+      if (b < a) return bad("pred_ptr must be non-decreasing");
+      for (int64_t e = a; e < b; ++e) {
+        const int64_t u = d->pred_idx[e];
+        if (u < 0 || u >= v) {
+          std::ostringstream m;
+          m << "edge " << u << " -> " << v << " breaks the topological index order";
+          return bad(m.str());
+        }
+        if (e > a && u <= d->pred_idx[e - 1]) return bad("predecessors of an op must be strictly increasing");
+        outdeg[u]++;
+      }
+      if (d->op_req[v] < 0 || d->op_req[v] >= R) return bad("op_req out of range");
+      for (int64_t c = 0; c < C; ++c)
+        if (d->dur[v * C + c] < 1) return bad("durations must be >= 1");
+      if (d->out_bytes[v] < 0) return bad("out_bytes must be >= 0");
+    }
+    // ------------------------------------------------------------ devices
+    for (int64_t x = 0; x < D; ++x)
+      if (d->dev_class[x] < 0 || d->dev_class[x] >= C) return bad("dev_class out of range");
+    for (int64_t s = 0; s < D; ++s)
+      for (int64_t t = 0; t < D; ++t)
+        if (s != t && d->link_class[s * D + t] >= K) return bad("link_class out of range");
+    for (int64_t k = 0; k < K; ++k)
+      if (d->bw[k] < 1 || d->lat[k] < 0) return bad("bandwidth must be >= 1 and latency >= 0");
+    if (d->slice_ptr[0] != 0) return bad("slice_ptr must start at 0");
+    int64_t max_slices = 0;
+    i128 last_start = 0;
+    for (int64_t x = 0; x < D; ++x) {
+      const int64_t a = d->slice_ptr[x], b = d->slice_ptr[x + 1];
+      if (b <= a) return bad("every device needs at least one idle slice");
+      if (b - a > 65535) return ss_set_error(SS_ERR_UNSUPPORTED, "more than 65535 idle slices on one device");
+      max_slices = std::max(max_slices, b - a);
+      for (int64_t k = a; k < b; ++k) {
+        const int64_t s0 = d->slice_begin[k], s1 = d->slice_end[k];
+        if (s0 < 0 || s0 >= s1) return bad("idle slices need 0 <= begin < end");
+        if (k + 1 < b && (s1 == SS_TIME_INF || s1 > d->slice_begin[k + 1]))
+          return bad("idle slices must be sorted, disjoint and finite except the last");
+        if (k + 1 == b && s1 != SS_TIME_INF) return bad("the last idle slice of a device must be open (SS_TIME_INF)");
+      }
+      last_start = std::max<i128>(last_start, d->slice_begin[b - 1]);
+    }
+    for (int64_t x = 0; x < D; ++x)
+      if (d->cap[x] < 0) return bad("capacity must be >= 0");
+    i128 max_rel = 0;
+    for (int64_t r = 0; r < R; ++r) {
+      if (d->release[r] < 0) return bad("release times must be >= 0");
+      if (d->deadline[r] >= ((int64_t)1 << 62) || d->deadline[r] <= -((int64_t)1 << 62))
+        return bad("deadline magnitude must be below 2^62");
+      max_rel = std::max<i128>(max_rel, d->release[r]);
+    }
+
+    // ------------------------------------------- precompute + overflow bound
+    std::vector<int64_t> xfer((size_t)N * K);
+    i128 horizon = last_start + max_rel, bytes_total = 0;
+    for (int64_t v = 0; v < N; ++v) {
+      int64_t wmax = 0, xmax = 0;
+      for (int64_t c = 0; c < C; ++c) wmax = std::max(wmax, d->dur[v * C + c]);
+      for (int64_t k = 0; k < K; ++k) {
+        const i128 x = (i128)d->lat[k] + ((i128)d->out_bytes[v] + d->bw[k] - 1) / d->bw[k];
+        if (x >= kTimeLimit) return bad("transfer estimate overflows the time horizon");
+        xfer[v * K + k] = (int64_t)x;
+        xmax = std::max<int64_t>(xmax, (int64_t)x);
+      }
+      horizon += (i128)wmax + (i128)(outdeg[v] + 1) * xmax;
+      bytes_total += d->out_bytes[v];
+      if (horizon >= kTimeLimit) return bad("time horizon bound reaches 2^62");
+      if (bytes_total * (D + 1) >= kSumLimit) return bad("total tensor bytes times (n_dev + 1) reaches 2^63");
+    }
+    if (horizon * (i128)std::max<int64_t>(N, 1) >= kSumLimit) return bad("n_ops times the horizon reaches 2^63");
+
+    // successor CSR, ascending within each op
+    std::vector<int32_t> succ_ptr(N + 1, 0), succ_idx(E), fill(N, 0);
+    for (int64_t v = 0; v < N; ++v) succ_ptr[v + 1] = succ_ptr[v] + outdeg[v];
+    for (int64_t v = 0; v < N; ++v)
+      for (int64_t e = d->pred_ptr[v]; e < d->pred_ptr[v + 1]; ++e) {
+        const int32_t u = d->pred_idx[e];
+        succ_idx[succ_ptr[u] + fill[u]++] = (int32_t)v;
+      }
+    std::vector<int32_t> pred_ptr(d->pred_ptr, d->pred_ptr + N + 1), slice_ptr(D + 1);
+    for (int64_t x = 0; x <= D; ++x) slice_ptr[x] = (int32_t)d->slice_ptr[x];
+    const int64_t S = d->slice_ptr[D];
+    if (S >= INT32_MAX) return ss_set_error(SS_ERR_UNSUPPORTED, "too many idle slices in total");
+
+    // ------------------------------------------------------------- staging
+    Packer pk;
+    const size_t o_pred_ptr = pk.add(pred_ptr);
+    const size_t o_pred_idx = pk.add(d->pred_idx, E * sizeof(int32_t));
+    const size_t o_succ_ptr = pk.add(succ_ptr);
+    const size_t o_succ_idx = pk.add(succ_idx);
+    const size_t o_op_req = pk.add(d->op_req, N * sizeof(int32_t));
+    const size_t o_dev_class = pk.add(d->dev_class, D * sizeof(int32_t));
+    const size_t o_slice_ptr = pk.add(slice_ptr);
+    const size_t o_dur = pk.add(d->dur, N * C * sizeof(int64_t));
+    const size_t o_bytes = pk.add(d->out_bytes, N * sizeof(int64_t));
+    const size_t o_xfer = pk.add(xfer);
+    const size_t o_sb = pk.add(d->slice_begin, S * sizeof(int64_t));
+    const size_t o_se = pk.add(d->slice_end, S * sizeof(int64_t));
+    const size_t o_cap = pk.add(d->cap, D * sizeof(int64_t));
+    const size_t o_rel = pk.add(d->release, R * sizeof(int64_t));
+    const size_t o_dl = pk.add(d->deadline, R * sizeof(int64_t));
+    const size_t o_link = pk.add(d->link_class, D * D);
+    pk.add(nullptr, 256);  // tail padding
+
+    ss_gmg *g = new ss_gmg();
+    if (hipGetDevice(&g->device) != hipSuccess) {
+      delete g;
+      return ss_set_error(SS_ERR_DEVICE, "hipGetDevice failed");
+    }
+    if (hipMalloc(&g->dev_mem, pk.host.size()) != hipSuccess) {
+      delete g;
+      return ss_set_error(SS_ERR_OOM, "hipMalloc of the staged GMG failed");
+    }
+    if (hipMemcpy(g->dev_mem, pk.host.data(), pk.host.size(), hipMemcpyHostToDevice) != hipSuccess) {
+      (void)hipFree(g->dev_mem);
+      delete g;
+      return ss_set_error(SS_ERR_DEVICE, "hipMemcpy of the staged GMG failed");
+    }
+    auto *base = static_cast<unsigned char *>(g->dev_mem);
+    GmgView &V = g->view;
+    V.n_ops = (int32_t)N;
+    V.n_dev = (int32_t)D;
+    V.n_class = (int32_t)C;
+    V.n_link = (int32_t)K;
+    V.n_req = (int32_t)R;
+    V.pred_ptr = reinterpret_cast<const int32_t *>(base + o_pred_ptr);
+    V.pred_idx = reinterpret_cast<const int32_t *>(base + o_pred_idx);
+    V.succ_ptr = reinterpret_cast<const int32_t *>(base + o_succ_ptr);
+    V.succ_idx = reinterpret_cast<const int32_t *>(base + o_succ_idx);
+    V.op_req = reinterpret_cast<const int32_t *>(base + o_op_req);
+    V.dev_class = reinterpret_cast<const int32_t *>(base + o_dev_class);
+    V.slice_ptr = reinterpret_cast<const int32_t *>(base + o_slice_ptr);
+    V.dur = reinterpret_cast<const int64_t *>(base + o_dur);
+    V.out_bytes = reinterpret_cast<const int64_t *>(base + o_bytes);
+    V.xfer = reinterpret_cast<const int64_t *>(base + o_xfer);
+    V.slice_begin = reinterpret_cast<const int64_t *>(base + o_sb);
+    V.slice_end = reinterpret_cast<const int64_t *>(base + o_se);
+    V.cap = reinterpret_cast<const int64_t *>(base + o_cap);
+    V.release = reinterpret_cast<const int64_t *>(base + o_rel);
+    V.deadline = reinterpret_cast<const int64_t *>(base + o_dl);
+    V.link_class = reinterpret_cast<const uint8_t *>(base + o_link);
+    g->n_ops = N;
+    g->n_edges = E;
+    g->n_dev = D;
+    g->n_class = C;
+    g->n_link = K;
+    g->n_req = R;
+    g->max_slices = max_slices;
+    *out = g;
+    return SS_OK;
+  } catch (const std::bad_alloc &) {
+    return ss_set_error(SS_ERR_OOM, "host allocation failed while loading the GMG");
+  }
+}
+
+extern "C" void ss_gmg_free(ss_gmg *g) {
+  if (!g) return;
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(g->device);
+  (void)hipDeviceSynchronize();
+  (void)hipFree(g->dev_mem);
+  (void)hipSetDevice(prev);
+  delete g;
+}
+
+extern "C" int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req) {
+  ss_clear_error();
+  if (!g) return ss_set_error(SS_ERR_INVALID_ARG, "ss_gmg_info: g is NULL");
+  if (n_ops) *n_ops = g->n_ops;
+  if (n_dev) *n_dev = g->n_dev;
+  if (n_req) *n_req = g->n_req;
+  return SS_OK;
+}

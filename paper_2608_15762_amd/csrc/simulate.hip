@@ -1,0 +1,392 @@
+// Batched what-if simulation kernels for gfx950 (one HIP source, no other targets).
+//
+// schedule_kernel: one lane per candidate.  The lane walks the ops in index
+//   order (the dispatch priority of every device queue) and computes each op's
+//   ready time, its earliest fit into an idle slice of its device after the
+//   device's previous finish, and its finish time (Sec. 3.3.2-3.3.3).  The
+//   per-candidate device clocks and slice cursors live in LDS laid out
+//   [device][lane], so the 64 lanes of a wave hit 64 distinct banks whatever
+//   device each one touches.  Op-indexed GMG data is the same for every lane
+//   (all lanes are at the same op), so it is read with wave-uniform loads.
+//   Finish times go to a per-chunk scratch row for the memory pass.
+//
+// memory_kernel: one wave per candidate.  It groups the candidate's ops by
+//   device, then for each device builds the endpoints of the residency
+//   intervals resident there (own outputs and remote copies, Sec. 3.3.2),
+//   sorts them in LDS by (time, free-before-allocate) with a bitonic network
+//   and takes the maximum prefix sum of the byte deltas: the device's peak.
+//   A device with more endpoints than fit in LDS uses the same code on a
+//   per-workgroup global buffer.
+#include <climits>
+
+#include "ss_internal.h"
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kMemCap = 2048;                     // endpoints of one device sorted in LDS
+constexpr int64_t kFinBudget = int64_t(16) << 30; // bytes of finish-time scratch per chunk
+constexpr int kMemBlocksPerCU = 4;
+
+__device__ __forceinline__ int64_t imax(int64_t a, int64_t b) { return a > b ? a : b; }
+
+// ------------------------------------------------------------------ schedule
+__global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const uint8_t *__restrict__ P,
+                                                         int64_t nb, int64_t *__restrict__ fin,
+                                                         int64_t *__restrict__ comp, int64_t *__restrict__ makespan,
+                                                         int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
+                                                         uint8_t *__restrict__ violation) {
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = G.n_class, K = G.n_link;
+  const int lane = threadIdx.x;
+  int64_t *clk = reinterpret_cast<int64_t *>(lds_raw);                        // [D][64]
+  uint16_t *cur = reinterpret_cast<uint16_t *>(lds_raw + (size_t)D * kWave * 8);  // [D][64]
+  const int64_t c = (int64_t)blockIdx.x * kWave + lane;
+  if (c >= nb) return;
+  const uint8_t *prow = P + c * N;
+  int64_t *frow = fin + c * N;
+  for (int d = 0; d < D; ++d) {
+    clk[d * kWave + lane] = 0;
+    cur[d * kWave + lane] = 0;
+  }
+  for (int r = 0; r < R; ++r) comp[(int64_t)r * nb + c] = G.release[r];
+
+  bool invalid = false;
+  int64_t ms = 0, sum = 0;
+  for (int v = 0; v < N; ++v) {
+    int d = prow[v];
+    if (d >= D) {  // not a device of the set: finish the walk on device 0, report sentinels
+      invalid = true;
+      d = 0;
+    }
+    const int64_t w = G.dur[(int64_t)v * C + G.dev_class[d]];
+    const int r = G.op_req[v];
+    // ready: release, and every predecessor's finish plus its transfer
+    int64_t ready = G.release[r];
+    const int e1 = G.pred_ptr[v + 1];
+    for (int e = G.pred_ptr[v]; e < e1; ++e) {
+      const int u = G.pred_idx[e];
+      int64_t t = frow[u];
+      int du = prow[u];
+      if (du >= D) du = 0;
+      if (du != d) t += G.xfer[(int64_t)u * K + G.link_class[du * D + d]];
+      ready = imax(ready, t);
+    }
+    // one op at a time: not before the device's previous finish; then the
+    // first idle slice that holds [s, s + w) (the cursor only moves forward)
+    const int slot = d * kWave + lane;
+    const int64_t t = imax(ready, clk[slot]);
+    const int sbase = G.slice_ptr[d];
+    int k = cur[slot];
+    int64_t s;
+    for (;;) {
+      const int64_t a = G.slice_begin[sbase + k], e = G.slice_end[sbase + k];
+      s = imax(t, a);
+      if (s + w <= e) break;
+      ++k;
+    }
+    cur[slot] = (uint16_t)k;
+    const int64_t f = s + w;
+    frow[v] = f;
+    clk[slot] = f;
+    ms = imax(ms, f);
+    sum += f;
+    int64_t *cr = comp + (int64_t)r * nb + c;
+    *cr = imax(*cr, f);
+  }
+  if (invalid) {
+    makespan[c] = INT64_MAX;
+    if (sumfin) sumfin[c] = INT64_MAX;
+    if (slack)
+      for (int r = 0; r < R; ++r) slack[c * R + r] = INT64_MIN;
+    violation[c] = SS_VIOLATION_INVALID;
+  } else {
+    makespan[c] = ms;
+    if (sumfin) sumfin[c] = sum;
+    if (slack)
+      for (int r = 0; r < R; ++r) slack[c * R + r] = G.deadline[r] - comp[(int64_t)r * nb + c];
+    violation[c] = 0;
+  }
+}
+
+// ------------------------------------------------------------------ memory
+// Interval endpoints contributed by op y placed on device e: its own output
+// (allocated at its start, freed when its last local consumer has finished and
+// its last outgoing transfer has arrived; never for an op without consumers)
+// and, for every remote predecessor whose last consumer on e is y, that
+// predecessor's copy on e (allocated at the predecessor's finish, freed at y's
+// finish).  Key = 2 * time + (1 for an allocation), so frees sort first at
+// equal times (half-open intervals).  Zero-byte tensors contribute nothing.
+template <bool kWrite, class KP, class VP>
+__device__ int op_events(const GmgView &G, const uint8_t *prow, const int64_t *frow, int y, int e, KP keys,
+                         VP vals, int w) {
+  const int C = G.n_class, K = G.n_link, D = G.n_dev;
+  int n = 0;
+  const int64_t fy = frow[y];
+  const int64_t by = G.out_bytes[y];
+  if (by > 0) {
+    if (kWrite) {
+      keys[w] = 2 * (fy - G.dur[(int64_t)y * C + G.dev_class[e]]) + 1;
+      vals[w] = by;
+    }
+    ++n;
+    const int x0 = G.succ_ptr[y], x1 = G.succ_ptr[y + 1];
+    if (x1 > x0) {
+      if (kWrite) {
+        int64_t F = fy;
+        for (int q = x0; q < x1; ++q) {
+          const int x = G.succ_idx[q];
+          const int dx = prow[x];
+          const int64_t t = (dx == e) ? frow[x] : fy + G.xfer[(int64_t)y * K + G.link_class[e * D + dx]];
+          F = imax(F, t);
+        }
+        keys[w + n] = 2 * F;
+        vals[w + n] = -by;
+      }
+      ++n;
+    }
+  }
+  const int p1 = G.pred_ptr[y + 1];
+  for (int q = G.pred_ptr[y]; q < p1; ++q) {
+    const int u = G.pred_idx[q];
+    if (prow[u] == e) continue;
+    const int64_t bu = G.out_bytes[u];
+    if (bu == 0) continue;
+    bool last = true;  // no consumer of u on e after y?
+    const int s0 = G.succ_ptr[u];
+    for (int s = G.succ_ptr[u + 1] - 1; s >= s0; --s) {
+      const int x = G.succ_idx[s];
+      if (x <= y) break;
+      if (prow[x] == e) {
+        last = false;
+        break;
+      }
+    }
+    if (!last) continue;
+    if (kWrite) {
+      keys[w + n] = 2 * frow[u] + 1;
+      vals[w + n] = bu;
+      keys[w + n + 1] = 2 * fy;
+      vals[w + n + 1] = -bu;
+    }
+    n += 2;
+  }
+  return n;
+}
+
+template <class KP, class VP>
+__device__ __forceinline__ void compare_swap(KP keys, VP vals, int i, int l) {
+  const int64_t ki = keys[i], kl = keys[l];
+  if (kl < ki) {
+    const int64_t vi = vals[i], vl = vals[l];
+    keys[i] = kl;
+    keys[l] = ki;
+    vals[i] = vl;
+    vals[l] = vi;
+  }
+}
+
+// Ascending bitonic sort of n (key, value) pairs by one wave.  Every
+// comparator puts the smaller key at the lower index, so the virtual padding
+// up to the next power of two (keys = +inf) never moves and pairs that reach
+// into it are skipped.
+template <class KP, class VP>
+__device__ void sort_pairs(KP keys, VP vals, int n, int lane) {
+  if (n < 2) return;
+  int lg = 0;
+  while ((1 << lg) < n) ++lg;
+  const int half_total = 1 << (lg - 1);
+  for (int kb = 1; kb <= lg; ++kb) {
+    const int k = 1 << kb, hmask = (k >> 1) - 1;
+    for (int q = lane; q < half_total; q += kWave) {
+      const int base = (q >> (kb - 1)) << kb, off = q & hmask;
+      const int l = base + k - 1 - off;
+      if (l < n) compare_swap(keys, vals, base + off, l);
+    }
+    __syncthreads();
+    for (int jb = kb - 2; jb >= 0; --jb) {
+      const int j = 1 << jb;
+      for (int q = lane; q < half_total; q += kWave) {
+        const int i = ((q >> jb) << (jb + 1)) + (q & (j - 1));
+        if (i + j < n) compare_swap(keys, vals, i, i + j);
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// Maximum over prefixes of the sorted deltas (= peak live bytes, >= 0).
+template <class VP>
+__device__ int64_t max_prefix_sum(VP vals, int n, int lane) {
+  int64_t carry = 0, best = 0;
+  for (int base = 0; base < n; base += kWave) {
+    const int i = base + lane;
+    int64_t s = i < n ? vals[i] : 0;
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int64_t y = __shfl_up(s, o, kWave);
+      if (lane >= o) s += y;
+    }
+    s += carry;
+    int64_t m = i < n ? s : INT64_MIN;
+    for (int o = kWave / 2; o >= 1; o >>= 1) m = imax(m, __shfl_xor(m, o, kWave));
+    best = imax(best, m);
+    carry = __shfl(s, kWave - 1, kWave);
+  }
+  return best;
+}
+
+__device__ __forceinline__ int wave_exclusive_scan(int x, int lane, int *total) {
+  int s = x;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(s, o, kWave);
+    if (lane >= o) s += y;
+  }
+  *total = __shfl(s, kWave - 1, kWave);
+  return s - x;
+}
+
+__global__ __launch_bounds__(kWave) void memory_kernel(const GmgView G, const uint8_t *__restrict__ P, int64_t nb,
+                                                       const int64_t *__restrict__ fin, int32_t *__restrict__ bydev_all,
+                                                       int64_t *__restrict__ gkeys_all,
+                                                       int64_t *__restrict__ gvals_all, int64_t slot_cap,
+                                                       int64_t *__restrict__ peak, uint8_t *__restrict__ violation) {
+  __shared__ int64_t skeys[kMemCap];
+  __shared__ int64_t svals[kMemCap];
+  __shared__ int32_t start[257];
+  __shared__ int32_t fillp[256];
+  const int D = G.n_dev, N = G.n_ops;
+  const int lane = threadIdx.x;
+  int32_t *bydev = bydev_all + (int64_t)blockIdx.x * N;
+  int64_t *gkeys = gkeys_all + (int64_t)blockIdx.x * slot_cap;
+  int64_t *gvals = gvals_all + (int64_t)blockIdx.x * slot_cap;
+  for (int64_t c = blockIdx.x; c < nb; c += gridDim.x) {
+    const uint8_t *prow = P + c * N;
+    const int64_t *frow = fin + c * N;
+    if (violation[c] & SS_VIOLATION_INVALID) {
+      if (peak)
+        for (int d = lane; d < D; d += kWave) peak[c * D + d] = 0;
+      continue;
+    }
+    // group the ops by device (order inside a device is irrelevant: the
+    // endpoints are sorted afterwards)
+    for (int d = lane; d <= D; d += kWave) start[d] = 0;
+    __syncthreads();
+    for (int v = lane; v < N; v += kWave) atomicAdd(&start[prow[v]], 1);
+    __syncthreads();
+    if (lane == 0) {
+      int s = 0;
+      for (int d = 0; d < D; ++d) {
+        const int t = start[d];
+        start[d] = s;
+        fillp[d] = s;
+        s += t;
+      }
+      start[D] = s;
+    }
+    __syncthreads();
+    for (int v = lane; v < N; v += kWave) bydev[atomicAdd(&fillp[prow[v]], 1)] = v;
+    __syncthreads();
+
+    uint8_t viol = 0;
+    for (int e = 0; e < D; ++e) {
+      const int lo = start[e], hi = start[e + 1];
+      int64_t pk = 0;
+      if (hi > lo) {
+        int mine = 0;
+        for (int q = lo + lane; q < hi; q += kWave)
+          mine += op_events<false>(G, prow, frow, bydev[q], e, (int64_t *)nullptr, (int64_t *)nullptr, 0);
+        int total;
+        int w = wave_exclusive_scan(mine, lane, &total);
+        if (total <= kMemCap) {
+          for (int q = lo + lane; q < hi; q += kWave) w += op_events<true>(G, prow, frow, bydev[q], e, skeys, svals, w);
+          __syncthreads();
+          sort_pairs(skeys, svals, total, lane);
+          pk = max_prefix_sum(svals, total, lane);
+        } else {
+          for (int q = lo + lane; q < hi; q += kWave) w += op_events<true>(G, prow, frow, bydev[q], e, gkeys, gvals, w);
+          __syncthreads();
+          sort_pairs(gkeys, gvals, total, lane);
+          pk = max_prefix_sum(gvals, total, lane);
+        }
+        __syncthreads();
+      }
+      if (peak && lane == 0) peak[c * D + e] = pk;
+      if (pk > G.cap[e]) viol = SS_VIOLATION_MEMORY;
+    }
+    if (lane == 0) violation[c] = viol;
+    __syncthreads();
+  }
+}
+
+int hip_fail(hipError_t err, const char *what) {
+  return ss_set_error(err == hipErrorOutOfMemory ? SS_ERR_OOM : SS_ERR_DEVICE,
+                      std::string(what) + ": " + hipGetErrorString(err));
+}
+
+}  // namespace
+
+int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
+                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream) {
+  const GmgView &G = g->view;
+  const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req;
+  const int64_t slot_cap = 2 * (N + E) + 2;
+  if (slot_cap >= INT32_MAX) return ss_set_error(SS_ERR_UNSUPPORTED, "n_ops + n_edges too large for the memory pass");
+  const size_t sched_lds = (size_t)D * kWave * (sizeof(int64_t) + sizeof(uint16_t));
+  int cus = 0;
+  hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, g->device);
+  if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
+  size_t lds_max = 0;
+  {
+    int v = 0;
+    err = hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, g->device);
+    if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
+    lds_max = (size_t)v;
+  }
+  if (sched_lds > lds_max) return ss_set_error(SS_ERR_UNSUPPORTED, "device state of the schedule pass exceeds LDS");
+  err = hipFuncSetAttribute(reinterpret_cast<const void *>(&schedule_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
+  if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
+
+  int64_t chunk = kFinBudget / std::max<int64_t>(1, N * 8);
+  chunk = std::max<int64_t>(kWave, chunk / kWave * kWave);
+  chunk = std::min<int64_t>(chunk, B);
+  const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kMemBlocksPerCU, chunk));
+
+  auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
+  const size_t sz_fin = align((size_t)chunk * N * 8 + 8);
+  const size_t sz_comp = align((size_t)chunk * R * 8 + 8);
+  const size_t sz_bydev = align((size_t)nslots * N * 4 + 4);
+  const size_t sz_ev = align((size_t)nslots * slot_cap * 8);
+  void *scratch = nullptr;
+  err = hipMallocAsync(&scratch, sz_fin + sz_comp + sz_bydev + 2 * sz_ev, stream);
+  if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of simulation scratch");
+  auto *base = static_cast<unsigned char *>(scratch);
+  auto *fin = reinterpret_cast<int64_t *>(base);
+  auto *comp = reinterpret_cast<int64_t *>(base + sz_fin);
+  auto *bydev = reinterpret_cast<int32_t *>(base + sz_fin + sz_comp);
+  auto *gkeys = reinterpret_cast<int64_t *>(base + sz_fin + sz_comp + sz_bydev);
+  auto *gvals = reinterpret_cast<int64_t *>(base + sz_fin + sz_comp + sz_bydev + sz_ev);
+
+  int rc = SS_OK;
+  for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
+    const int64_t nb = std::min(chunk, B - b0);
+    const uint8_t *Pc = P + b0 * N;
+    hipLaunchKernelGGL(schedule_kernel, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), sched_lds, stream,
+                       G, Pc, nb, fin, comp, makespan + b0, sumfin ? sumfin + b0 : nullptr,
+                       slack ? slack + b0 * R : nullptr, violation + b0);
+    err = hipGetLastError();
+    if (err != hipSuccess) {
+      rc = hip_fail(err, "schedule_kernel launch");
+      break;
+    }
+    const int64_t grid = std::min<int64_t>(nb, nslots);
+    hipLaunchKernelGGL(memory_kernel, dim3((unsigned)grid), dim3(kWave), 0, stream, G, Pc, nb,
+                       static_cast<const int64_t *>(fin), bydev, gkeys, gvals, slot_cap,
+                       peak ? peak + b0 * D : nullptr, violation + b0);
+    err = hipGetLastError();
+    if (err != hipSuccess) rc = hip_fail(err, "memory_kernel launch");
+  }
+  err = hipFreeAsync(scratch, stream);
+  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
+  return rc;
+}

@@ -1,0 +1,42 @@
+// Internal declarations of the simulator library (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+
+#include "ss.h"
+
+// Device-resident GMG, passed by value to every kernel.  Times and sizes are
+// int64; indices int32 (the loader enforces N, E < 2^31).
+struct GmgView {
+  int32_t n_ops, n_dev, n_class, n_link, n_req;
+  const int32_t *pred_ptr, *pred_idx;  // predecessor CSR
+  const int32_t *succ_ptr, *succ_idx;  // successor CSR, ascending within an op
+  const int32_t *op_req, *dev_class, *slice_ptr;
+  const int64_t *dur;        // [N][n_class]
+  const int64_t *out_bytes;  // [N]
+  const int64_t *xfer;       // [N][n_link]: lat[k] + ceil(out_bytes[v] / bw[k])
+  const int64_t *slice_begin, *slice_end;
+  const int64_t *cap, *release, *deadline;
+  const uint8_t *link_class;  // [D][D]
+};
+
+struct ss_gmg {
+  int device = 0;
+  int64_t n_ops = 0, n_edges = 0, n_dev = 0, n_class = 0, n_link = 0, n_req = 0;
+  int64_t max_slices = 0;  // largest slice count of any device
+  void *dev_mem = nullptr;
+  GmgView view{};
+};
+
+// Record an error message for ss_last_error() and return the code.
+int ss_set_error(int code, const std::string &msg);
+void ss_clear_error();
+
+// Kernel drivers (simulate.hip / select.hip).  Arguments are already checked.
+int ss_run_simulate(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
+                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream);
+int ss_run_select(const ss_gmg *g, const uint8_t *violation, const int64_t *key, const int64_t *slack, int64_t B,
+                  int require_sla, int64_t *out_best, hipStream_t stream);

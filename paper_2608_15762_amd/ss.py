@@ -1,0 +1,155 @@
+"""Python binding of libss.so (the C ABI in include/ss.h).
+
+Argument marshalling only: every step of the simulation runs in the HIP
+kernels behind the C ABI.  PyTorch provides device memory and streams.  There
+is no fallback: if the library is missing or cannot load, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libss.so")
+
+SS_OK = 0
+ERRORS = {-1: "SS_ERR_INVALID_ARG", -2: "SS_ERR_INVALID_GMG", -3: "SS_ERR_OOM", -4: "SS_ERR_DEVICE",
+          -5: "SS_ERR_UNSUPPORTED"}
+SS_LAYOUT_ROW_MAJOR = 0
+SS_VIOLATION_MEMORY = 0x1
+SS_VIOLATION_INVALID = 0x4
+SS_SELECT_REQUIRE_SLA = 0x1
+EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "ss_select_best", "ss_last_error")
+
+_lib = None
+_lock = threading.Lock()
+
+
+class SSError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class _Desc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in ("n_ops", "n_edges", "n_dev", "n_class", "n_link", "n_req")] + \
+               [(n, ctypes.c_void_p) for n in ("pred_ptr", "pred_idx", "op_req", "dur", "out_bytes", "dev_class",
+                                               "link_class", "bw", "lat", "slice_ptr", "slice_begin", "slice_end",
+                                               "cap", "release", "deadline")]
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2608_15762_amd/build.py")
+            L = ctypes.CDLL(LIB_PATH)
+            P, I64 = ctypes.c_void_p, ctypes.c_int64
+            L.ss_gmg_load.argtypes = [ctypes.POINTER(_Desc), ctypes.POINTER(ctypes.c_void_p)]
+            L.ss_gmg_load.restype = ctypes.c_int
+            L.ss_gmg_free.argtypes = [P]
+            L.ss_gmg_free.restype = None
+            L.ss_gmg_info.argtypes = [P, P, P, P]
+            L.ss_simulate_batch.argtypes = [P, P, I64, ctypes.c_int, P, P, P, P, P, P]
+            L.ss_simulate_batch.restype = ctypes.c_int
+            L.ss_select_best.argtypes = [P, P, P, P, I64, ctypes.c_int, P, P]
+            L.ss_select_best.restype = ctypes.c_int
+            L.ss_last_error.argtypes = []
+            L.ss_last_error.restype = ctypes.c_char_p
+            _lib = L
+    return _lib
+
+
+def _check(rc):
+    if rc != SS_OK:
+        raise SSError(rc, lib().ss_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream_ptr(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Gmg:
+    """A GMG snapshot staged on the current HIP device (ss_gmg_load)."""
+
+    def __init__(self, g):
+        keep = {}
+
+        def arr(name, dtype):
+            a = np.ascontiguousarray(getattr(g, name), dtype)
+            keep[name] = a
+            return a.ctypes.data
+
+        d = _Desc(int(g.n_ops), int(g.pred_ptr[-1]), int(g.n_dev), int(g.n_class), int(g.n_link), int(g.n_req),
+                  arr("pred_ptr", np.int32), arr("pred_idx", np.int32), arr("op_req", np.int32),
+                  arr("dur", np.int64), arr("out_bytes", np.int64), arr("dev_class", np.int32),
+                  arr("link_class", np.uint8), arr("bw", np.int64), arr("lat", np.int64),
+                  arr("slice_ptr", np.int64), arr("slice_begin", np.int64), arr("slice_end", np.int64),
+                  arr("cap", np.int64), arr("release", np.int64), arr("deadline", np.int64))
+        h = ctypes.c_void_p()
+        _check(lib().ss_gmg_load(ctypes.byref(d), ctypes.byref(h)))
+        self.handle = h
+        self.n_ops, self.n_dev, self.n_req = int(g.n_ops), int(g.n_dev), int(g.n_req)
+
+    def info(self):
+        n = [ctypes.c_int64() for _ in range(3)]
+        _check(lib().ss_gmg_info(self.handle, *[ctypes.byref(x) for x in n]))
+        return tuple(x.value for x in n)
+
+    def free(self):
+        if self.handle:
+            lib().ss_gmg_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def simulate_batch_into(g: Gmg, placements, makespan, violation, peak=None, slack=None, sumfin=None,
+                        stream=None):
+    """ss_simulate_batch on caller-provided torch CUDA tensors (row-major)."""
+    B = placements.shape[0]
+    assert placements.dtype.is_floating_point is False and placements.element_size() == 1
+    assert placements.is_contiguous() and placements.shape == (B, g.n_ops)
+    _check(lib().ss_simulate_batch(g.handle, _ptr(placements), B, SS_LAYOUT_ROW_MAJOR, _ptr(makespan), _ptr(peak),
+                                   _ptr(violation), _ptr(slack), _ptr(sumfin), _stream_ptr(stream)))
+
+
+def simulate_batch(g: Gmg, placements, want_peak=True, want_slack=True, want_sumfin=True, stream=None) -> dict:
+    """Allocate outputs on placements' device and run ss_simulate_batch."""
+    import torch
+    B = placements.shape[0]
+    dev = placements.device
+    out = dict(makespan=torch.empty(B, dtype=torch.int64, device=dev),
+               violation=torch.empty(B, dtype=torch.uint8, device=dev),
+               peak=torch.empty((B, g.n_dev), dtype=torch.int64, device=dev) if want_peak else None,
+               slack=torch.empty((B, g.n_req), dtype=torch.int64, device=dev) if want_slack else None,
+               sumfin=torch.empty(B, dtype=torch.int64, device=dev) if want_sumfin else None)
+    simulate_batch_into(g, placements, out["makespan"], out["violation"], out["peak"], out["slack"], out["sumfin"],
+                        stream)
+    return out
+
+
+def select_best(g: Gmg, violation, key, slack=None, require_sla=False, out=None, stream=None):
+    """ss_select_best; returns a device int64[2] tensor {index or -1, key}."""
+    import torch
+    B = violation.shape[0]
+    if out is None:
+        out = torch.empty(2, dtype=torch.int64, device=violation.device)
+    _check(lib().ss_select_best(g.handle, _ptr(violation), _ptr(key), _ptr(slack), B,
+                                SS_SELECT_REQUIRE_SLA if require_sla else 0, _ptr(out), _stream_ptr(stream)))
+    return out

@@ -294,7 +294,7 @@ def make_gmg(n_dev, kinds, edges, op_req, dur, out_bytes, slices, cap, release, 
     for v in range(N):
         pred_ptr[v + 1] = pred_ptr[v] + len(preds[v])
     pred_idx = np.array([u for v in range(N) for u in sorted(preds[v])], np.int32)
-    dur_arr = np.asarray(dur, np.int64).reshape(N, -1)
+    dur_arr = np.asarray(dur, np.int64).reshape(N, -1) if N else np.zeros((0, 1), np.int64)
     D = n_dev
     if link_class is None:
         link_class = np.zeros((D, D), np.uint8)

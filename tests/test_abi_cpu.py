@@ -1,0 +1,110 @@
+"""The C-ABI library on a machine without a GPU: it loads, exports every
+entry point include/ss.h declares, and its loader rejects malformed GMG
+snapshots before touching the device."""
+import copy
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_15762_amd import ss, synth
+from paper_2608_15762_amd.synth import TIME_INF, make_gmg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names |= set(re.findall(r"\b(ss_[a-z_]+)\s*\(", text))
+    return names
+
+
+def test_library_exports_every_declared_entry_point():
+    L = ss.lib()
+    names = declared_functions()
+    assert names == set(ss.EXPORTED)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_null_arguments():
+    L = ss.lib()
+    h = ctypes.c_void_p()
+    assert L.ss_gmg_load(None, ctypes.byref(h)) == -1
+    assert L.ss_simulate_batch(None, None, 0, 0, None, None, None, None, None, None) == -1
+    assert L.ss_select_best(None, None, None, None, 0, 0, None, None) == -1
+    assert L.ss_gmg_info(None, None, None, None) == -1
+    assert b"NULL" in L.ss_last_error()
+    L.ss_gmg_free(None)
+
+
+def good():
+    return make_gmg(2, ["op"] * 3, [(0, 1), (1, 2)], [0, 0, 0], [[2], [3], [4]], [10, 20, 30],
+                    [[(0, 5), (9, TIME_INF)], [(0, TIME_INF)]], [100, 100], [0], [50], bw=[10], lat=[1])
+
+
+def load_rc(g):
+    try:
+        h = ss.Gmg(g)
+        h.free()
+        return 0
+    except ss.SSError as e:
+        return e.code
+
+
+def test_valid_snapshot_passes_validation():
+    # without a GPU the loader gets as far as the device (SS_ERR_DEVICE); with one it loads
+    assert load_rc(good()) in (0, -4)
+
+
+def _mut(fn):
+    g = copy.deepcopy(good())
+    fn(g)
+    return g
+
+
+BAD = {
+    "non_topological_edge": lambda g: g.pred_idx.__setitem__(1, 2),
+    "duplicate_pred": lambda g: (setattr(g, "pred_ptr", np.array([0, 0, 1, 3], np.int32)),
+                                 setattr(g, "pred_idx", np.array([0, 1, 1], np.int32))),
+    "zero_duration": lambda g: g.dur.__setitem__((1, 0), 0),
+    "negative_bytes": lambda g: g.out_bytes.__setitem__(0, -1),
+    "zero_bandwidth": lambda g: g.bw.__setitem__(0, 0),
+    "negative_latency": lambda g: g.lat.__setitem__(0, -1),
+    "no_open_tail": lambda g: g.slice_end.__setitem__(2, 1000),
+    "overlapping_slices": lambda g: g.slice_end.__setitem__(0, 10),
+    "empty_slice": lambda g: g.slice_end.__setitem__(0, 0),
+    "open_slice_not_last": lambda g: g.slice_end.__setitem__(0, TIME_INF),
+    "negative_slice_start": lambda g: g.slice_begin.__setitem__(0, -3),
+    "link_class_out_of_range": lambda g: g.link_class.__setitem__((0, 1), 1),
+    "dev_class_out_of_range": lambda g: g.dev_class.__setitem__(1, 1),
+    "op_req_out_of_range": lambda g: g.op_req.__setitem__(0, 1),
+    "negative_release": lambda g: g.release.__setitem__(0, -1),
+    "huge_deadline": lambda g: g.deadline.__setitem__(0, 1 << 62),
+    "negative_cap": lambda g: g.cap.__setitem__(0, -1),
+    "horizon_overflow": lambda g: g.slice_begin.__setitem__(1, 1 << 62),
+    "bytes_overflow": lambda g: g.out_bytes.__setitem__(0, 1 << 62),
+}
+
+
+@pytest.mark.parametrize("name", sorted(BAD))
+def test_loader_rejects_malformed_snapshot(name):
+    g = _mut(BAD[name])
+    assert load_rc(g) == -2, name
+
+
+def test_loader_rejects_too_many_devices():
+    g = synth.random_gmg(0, n_ops=4, n_dev=3)
+    g.n_dev = 256
+    assert load_rc(g) == -2
+
+
+def test_last_error_is_per_call():
+    assert load_rc(_mut(BAD["zero_duration"])) == -2
+    assert b"duration" in ss.lib().ss_last_error()

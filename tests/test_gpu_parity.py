@@ -1,0 +1,169 @@
+"""Parity of the HIP path (through the C ABI) with the oracle, element by element.
+
+Integer results, so the bar is bit-exact on every output.  Inputs are the
+seeded workloads and random small GMGs; the oracle never sees GPU output.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_15762_amd import ss, synth
+from paper_2608_15762_amd.synth import TIME_INF, make_gmg
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+FIELDS = ("makespan", "peak", "violation", "slack", "sumfin")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    ss.lib()
+    return torch.device("cuda:0")
+
+
+def gpu_run(h, P, dev, **kw):
+    Pt = torch.from_numpy(np.ascontiguousarray(P)).to(dev)
+    out = ss.simulate_batch(h, Pt, **kw)
+    torch.cuda.synchronize()
+    return {k: (None if v is None else v.cpu().numpy()) for k, v in out.items()}
+
+
+def assert_same(gpu, ref, idx=None, label=""):
+    for f in FIELDS:
+        if gpu.get(f) is None:
+            continue
+        a = gpu[f] if idx is None else gpu[f][idx]
+        b = ref[f]
+        if not np.array_equal(a, b):
+            bad = np.argwhere(a != b)[:5]
+            pytest.fail(f"{label}: {f} differs at {bad.tolist()}: gpu {a[tuple(bad[0])]} oracle {b[tuple(bad[0])]}")
+
+
+@pytest.mark.parametrize("cid,nb", [(0, 256), (1, 1000), (2, 300), (3, 130), (4, 20)])
+def test_config_parity(dev, cid, nb):
+    print(f"config {cid}: {nb} candidates", flush=True)
+    g = synth.build_gmg(cid)
+    P = synth.placements(g, cid, 0, nb)
+    ref = oracle.simulate_batch(g, P, n_threads=8)
+    got = gpu_run(ss.Gmg(g), P, dev)
+    assert_same(got, ref, label=f"config {cid}")
+
+
+FUZZ = [dict(n_ops=n, n_dev=D, n_req=R, n_slices=S, n_class=C, n_link=K, rel_max=rel, zero_bytes_p=zb,
+             cap_scale=cs, slice_scale=ss_)
+        for n, D, R, S, C, K, rel, zb, cs, ss_ in [
+            (1, 1, 1, 0, 1, 1, 0, 0.0, None, 60), (7, 2, 1, 2, 1, 1, 0, 0.1, 500, 60),
+            (30, 3, 2, 4, 2, 2, 5, 0.2, 2000, 40), (64, 5, 3, 3, 1, 3, 0, 0.0, 3000, 100),
+            (65, 4, 4, 6, 3, 2, 20, 0.3, 1500, 30), (200, 7, 2, 8, 2, 3, 9, 0.1, 5000, 80),
+            (129, 16, 5, 5, 1, 2, 0, 0.05, 4000, 50), (333, 9, 6, 12, 2, 2, 50, 0.1, 20000, 200)]]
+
+
+@pytest.mark.parametrize("seed", range(len(FUZZ)))
+def test_fuzz_parity(dev, seed):
+    kw = FUZZ[seed]
+    print(f"fuzz {seed}: {kw}", flush=True)
+    g = synth.random_gmg(seed, **kw)
+    st = synth.Stream(seed + 12345)
+    B = 197
+    P = np.array([[st.uniform_int(0, g.n_dev - 1) for _ in range(g.n_ops)] for _ in range(B)], np.uint8)
+    for b in range(0, B, 17):  # some candidates name a device outside the set
+        P[b, st.uniform_int(0, g.n_ops - 1)] = g.n_dev + st.uniform_int(0, 255 - g.n_dev)
+    ref = oracle.simulate_batch(g, P)
+    got = gpu_run(ss.Gmg(g), P, dev)
+    assert_same(got, ref, label=f"fuzz {seed}")
+    assert (got["violation"] == 4).sum() >= 1
+
+
+def test_nullable_outputs_and_empty_batch(dev):
+    g = synth.build_gmg(0)
+    h = ss.Gmg(g)
+    P = synth.placements(g, 0, 0, 70)
+    ref = oracle.simulate_batch(g, P)
+    got = gpu_run(h, P, dev, want_peak=False, want_slack=False, want_sumfin=False)
+    assert np.array_equal(got["makespan"], ref["makespan"]) and np.array_equal(got["violation"], ref["violation"])
+    empty = gpu_run(h, np.zeros((0, g.n_ops), np.uint8), dev)
+    assert empty["makespan"].shape == (0,)
+
+
+def test_zero_ops_gmg(dev):
+    g = make_gmg(3, [], [], [], np.zeros((0, 1), np.int64), [], [[(0, TIME_INF)]] * 3, [5, 5, 5], [4], [10])
+    P = np.zeros((5, 0), np.uint8)
+    ref = oracle.simulate_batch(g, P)
+    got = gpu_run(ss.Gmg(g), P, dev)
+    assert_same(got, ref, label="zero ops")
+    assert got["slack"].tolist() == [[6]] * 5
+
+
+def test_max_devices(dev):
+    g = synth.random_gmg(7, n_ops=300, n_dev=255, n_req=3, n_slices=3, n_link=2, cap_scale=3000)
+    st = synth.Stream(99)
+    P = np.array([[st.uniform_int(0, 255) for _ in range(g.n_ops)] for _ in range(130)], np.uint8)
+    ref = oracle.simulate_batch(g, P)
+    got = gpu_run(ss.Gmg(g), P, dev)
+    assert_same(got, ref, label="255 devices")
+
+
+def test_crowded_device_uses_global_sort_buffer(dev):
+    """All 2,052 ops of the 4-tenant workload on one device: > 2,048 endpoints."""
+    g = synth.build_gmg(2)
+    P = np.zeros((6, g.n_ops), np.uint8)
+    P[1:] = synth.placements(g, 2, 0, 5)
+    P[2, : g.n_ops // 2] = 3
+    ref = oracle.simulate_batch(g, P)
+    got = gpu_run(ss.Gmg(g), P, dev)
+    assert_same(got, ref, label="crowded")
+
+
+# ------------------------------------------------------------------ selection
+def gpu_select(h, viol, key, slack, require_sla, dev):
+    out = ss.select_best(h, torch.from_numpy(viol).to(dev), torch.from_numpy(key).to(dev),
+                         None if slack is None else torch.from_numpy(slack).to(dev), require_sla)
+    torch.cuda.synchronize()
+    return tuple(out.cpu().tolist())
+
+
+def test_select_best_on_tight_memory_workload(dev):
+    g = synth.build_gmg(3)
+    h = ss.Gmg(g)
+    P = synth.placements(g, 3, 0, 2000)
+    got = gpu_run(h, P, dev)
+    ref = oracle.simulate_batch(g, P, n_threads=8)
+    assert_same(got, ref, label="config 3 x 2000")
+    assert 0 < (ref["violation"] == 1).sum() < 2000
+    for key in ("sumfin", "makespan"):
+        for sla in (False, True):
+            exp = oracle.select_best(ref["violation"], ref[key], ref["slack"], sla)
+            assert gpu_select(h, got["violation"], got[key], got["slack"], sla, dev) == exp
+
+
+@pytest.mark.parametrize("B", [0, 1, 255, 256, 257, 100_003, 3_000_001])
+def test_select_best_ties_and_sizes(dev, B):
+    g = synth.random_gmg(1, n_ops=4, n_dev=2, n_req=2)
+    h = ss.Gmg(g)
+    rng = np.random.default_rng(B)
+    key = rng.integers(0, 50, B).astype(np.int64)  # many ties
+    viol = (rng.random(B) < 0.3).astype(np.uint8) * rng.choice(np.array([1, 4], np.uint8), B)
+    slack = rng.integers(-3, 100, (B, 2)).astype(np.int64)
+    for sla in (False, True):
+        exp = oracle.select_best(viol, key, slack, sla)
+        assert gpu_select(h, viol, key, slack, sla, dev) == exp
+    none = gpu_select(h, np.ones(B, np.uint8), key, slack, False, dev)
+    assert none == (-1, 2 ** 63 - 1)
+
+
+# ------------------------------------------------------------------ full-size batches
+@pytest.mark.parametrize("cid,n_sample", [(1, 256), (2, 64), (3, 32)])
+def test_full_batch_sampled_parity(dev, cid, n_sample):
+    """The whole batch of a workload in one call (the configuration the
+    benchmark times), checked against the oracle on sampled candidates."""
+    g = synth.build_gmg(cid)
+    B = synth.CONFIGS[cid].n_cand
+    print(f"config {cid}: full batch of {B}", flush=True)
+    P = synth.placements(g, cid, 0, B)
+    got = gpu_run(ss.Gmg(g), P, dev)
+    rng = np.random.default_rng(cid)
+    idx = np.unique(np.concatenate([[0, B - 1], rng.choice(B, n_sample, replace=False)]))
+    ref = oracle.simulate_batch(g, P[idx], n_threads=8)
+    assert_same(got, ref, idx=idx, label=f"config {cid} full")
