@@ -1,0 +1,194 @@
+"""Benchmark of the batched what-if simulator on one MI355X.
+
+One step = the whole hot path over one batch: ss_simulate_batch on every
+candidate of the workload (schedule, memory peak, verdicts, slack) followed by
+ss_select_best.  Placements are generated and staged in HBM before timing.
+
+Prints one JSON line.  The default workload is the cluster-scale one (50,000
+ops of 16 tenants on 128 simulated devices, 1,048,576 candidates).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "candidate placements simulated/sec (+ op-evals/sec, % HBM roofline), 1 GPU"
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=4, help="workload id 0-4 (4 = cluster scale)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--gen-chunk", type=int, default=32768, help="candidates generated per host chunk")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def stage_placements(torch, synth, g, cid, B, dev, chunk):
+    """Generate the candidate batch on the host in chunks and copy it into one
+    device tensor [B, N] (row-major uint8)."""
+    N = g.n_ops
+    P = torch.empty((B, N), dtype=torch.uint8, device=dev)
+    chunk = max(1, min(chunk, B))
+    bufs = [torch.empty((chunk, N), dtype=torch.uint8, pin_memory=True) for _ in range(2)]
+    events = [None, None]
+    base = None
+    rec = synth.CONFIGS[cid].placement
+    if rec["mode_even"] == 1 or rec["mode_odd"] == 1:
+        base = synth.base_placement(g, cid)
+    for i, b0 in enumerate(range(0, B, chunk)):
+        nb = min(chunk, B - b0)
+        k = i % 2
+        if events[k] is not None:
+            events[k].synchronize()
+        synth.placements(g, cid, b0, nb, out=bufs[k].numpy()[:nb], base=base)
+        P[b0:b0 + nb].copy_(bufs[k][:nb], non_blocking=True)
+        events[k] = torch.cuda.Event()
+        events[k].record()
+    torch.cuda.synchronize()
+    return P
+
+
+def sample_rows(synth, g, cid, idx):
+    """Placements of the candidates idx (the same seeded rows the GPU batch holds)."""
+    rec = synth.CONFIGS[cid].placement
+    base = synth.base_placement(g, cid) if (rec["mode_even"] == 1 or rec["mode_odd"] == 1) else None
+    out = np.empty((len(idx), g.n_ops), np.uint8)
+    for i, b in enumerate(idx):
+        synth.placements(g, cid, int(b), 1, out=out[i:i + 1], base=base, n_threads=1)
+    return out
+
+
+def cpu_baseline(g, cid, B, seconds, got):
+    """The oracle, as it stands, on a bounded evenly spaced sample of the same
+    batch, on the host's cores; its results are also compared with the GPU's."""
+    import oracle
+    from paper_2608_15762_amd import synth
+
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    og = oracle.OracleGmg(g)
+    pilot = sample_rows(synth, g, cid, np.linspace(0, B - 1, 9).astype(np.int64))
+    oracle.simulate_batch(og, pilot[:1], n_threads=1)  # first call pays one-time costs
+    t0 = time.perf_counter()
+    oracle.simulate_batch(og, pilot[1:], n_threads=1)
+    per = (time.perf_counter() - t0) / (len(pilot) - 1)
+    n = int(max(threads, min(B, 65536, seconds * threads / max(per, 1e-9))))
+    idx = np.unique(np.linspace(0, B - 1, n).astype(np.int64))
+    log(f"oracle: {per * 1e3:.2f} ms per candidate on one core; timing {len(idx)} candidates on {threads} threads")
+    P = sample_rows(synth, g, cid, idx)
+    t0 = time.perf_counter()
+    ref = oracle.simulate_batch(og, P, n_threads=threads)
+    wall = time.perf_counter() - t0
+    mism = 0
+    for f in ("makespan", "peak", "violation", "slack", "sumfin"):
+        a = got[f][idx]
+        mism += int((a != ref[f]).reshape(len(idx), -1).any(axis=1).sum())
+    log(f"oracle: {len(idx) / wall:.1f} candidates/s; {mism} candidates differ from the GPU")
+    return dict(value=len(idx) / wall, unit="candidates/s", cores=threads, kind="oracle",
+                sample=f"{len(idx)} evenly spaced candidates of the same batch (indices 0..{B - 1}), "
+                       f"{threads} threads, {wall:.1f} s wall",
+                op_evals_per_s=len(idx) * g.n_ops / wall), dict(checked=int(len(idx)), mismatching_candidates=mism)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the candidate batch shards "
+              "across GPUs by contiguous ranges but no multi-GPU run is part of this build.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2608_15762_amd import ss, synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    cid = args.workload
+    cfg = synth.CONFIGS[cid]
+    g = synth.build_gmg(cid)
+    B, N, D, R = cfg.n_cand, g.n_ops, g.n_dev, g.n_req
+    log(f"workload {cfg.name}: N={N} E={g.n_edges} D={D} R={R} B={B}")
+    h = ss.Gmg(g)
+    t0 = time.perf_counter()
+    P = stage_placements(torch, synth, g, cid, B, dev, args.gen_chunk)
+    log(f"staged {B * N / 1e9:.2f} GB of placements in HBM in {time.perf_counter() - t0:.1f} s")
+    out = dict(makespan=torch.empty(B, dtype=torch.int64, device=dev),
+               violation=torch.empty(B, dtype=torch.uint8, device=dev),
+               peak=torch.empty((B, D), dtype=torch.int64, device=dev),
+               slack=torch.empty((B, R), dtype=torch.int64, device=dev),
+               sumfin=torch.empty(B, dtype=torch.int64, device=dev))
+    best = torch.empty(2, dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        ss.simulate_batch_into(h, P, out["makespan"], out["violation"], out["peak"], out["slack"], out["sumfin"],
+                               stream=stream)
+        ss.select_best(h, out["violation"], out["sumfin"], out=best, stream=stream)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"warmup step {i + 1}/{args.warmup} done")
+    ss.kernel_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step()
+        torch.cuda.synchronize()
+        log(f"timed step {i + 1}/{args.steps} done ({(time.perf_counter() - t0) / (i + 1) * 1e3:.1f} ms/step)")
+    elapsed = time.perf_counter() - t0
+    kernels = {}
+    for k, name in ss.KERNEL_NAMES.items():
+        n, ms = ss.kernel_time(k)
+        kernels[name] = dict(launches=n, total_ms=round(ms, 3), avg_ms=round(ms / max(n, 1), 4))
+    ss.kernel_timing(False)
+
+    value = B * args.steps / elapsed
+    bytes_per_cand = N + 8 + 8 * D + 1 + 8 * R + 8  # placements in; makespan, peak, violation, slack, sumfin out
+    dom = max(("schedule_kernel", "memory_kernel"), key=lambda k: kernels[k]["total_ms"])
+    launches_per_step = max(1, kernels[dom]["launches"] // args.steps)
+    cand_per_launch = B / launches_per_step
+    achieved = bytes_per_cand * cand_per_launch / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
+    result = {
+        "metric": METRIC, "value": round(value, 1), "unit": "candidates/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 2), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
+        "config": {"workload": cfg.name, "n_ops": N, "n_edges": g.n_edges, "n_dev": D, "n_req": R,
+                   "candidates": B, "idle_slices_per_device": cfg.n_slices},
+        "op_evals_per_s": round(value * N, 1),
+        "path_hbm_frac": round(value * bytes_per_cand / (HBM_PEAK_GBS * 1e9), 6),
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6), "traffic": None,
+                     "bytes_per_candidate": bytes_per_cand, "candidates_per_launch": cand_per_launch},
+        "kernels": kernels,
+    }
+    torch.cuda.synchronize()
+    bi, bk = best.cpu().tolist()
+    result["best"] = {"index": bi, "sumfin": bk}
+    if not args.no_cpu_baseline:
+        got = {k: v.cpu().numpy() for k, v in out.items()}
+        log("running the oracle CPU baseline")
+        cb, par = cpu_baseline(g, cid, B, args.cpu_seconds, got)
+        result["cpu_baseline"] = cb
+        result["parity_sample"] = par
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

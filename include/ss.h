@@ -162,6 +162,20 @@ int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int64_t B, int
 int ss_select_best(const ss_gmg *g, const uint8_t *violation, const int64_t *key, const int64_t *sla_slack,
                    int64_t B, int flags, int64_t *out_best, void *hip_stream);
 
+/*
+ * Kernel timing, for benchmarks.  While enabled (process-wide), every kernel
+ * that ss_simulate_batch and ss_select_best launch is bracketed by a HIP
+ * event pair recorded on the caller's stream.  ss_kernel_time waits for the
+ * recorded events of one kernel kind, returns how many launches there were
+ * and their summed duration in milliseconds, and forgets them.  Disabling
+ * drops unread records.  Errors: SS_ERR_INVALID_ARG, SS_ERR_DEVICE.
+ */
+#define SS_KERNEL_SCHEDULE 0     /* per-candidate list schedule (one lane per candidate) */
+#define SS_KERNEL_MEMORY 1       /* per-device peak memory (one wave per candidate) */
+#define SS_KERNEL_SELECT 2       /* best-candidate reduction (both passes) */
+int ss_kernel_timing(int enable);
+int ss_kernel_time(int kernel, int64_t *launches, double *total_ms);
+
 /* Message for the calling thread's most recent failed call ("" if none). */
 const char *ss_last_error(void);
 

@@ -1,11 +1,28 @@
 // C ABI entry points: argument checks, error reporting, dispatch to the
 // kernel drivers.  The GMG loader lives in gmg_load.cpp.
+#include <atomic>
+#include <mutex>
 #include <string>
+#include <vector>
 
 #include "ss_internal.h"
 
+struct SsTimingRec {
+  int kernel;
+  hipEvent_t start, stop;
+};
+
 namespace {
 thread_local std::string g_last_error;
+std::atomic<int> g_timing_on{0};
+std::mutex g_timing_mu;
+std::vector<SsTimingRec *> g_timing;
+
+void drop_record(SsTimingRec *r) {
+  (void)hipEventDestroy(r->start);
+  (void)hipEventDestroy(r->stop);
+  delete r;
+}
 
 int check_device(const ss_gmg *g) {
   int cur = -1;
@@ -54,4 +71,63 @@ extern "C" int ss_select_best(const ss_gmg *g, const uint8_t *violation, const i
   const int rc = check_device(g);
   if (rc != SS_OK) return rc;
   return ss_run_select(g, violation, key, sla_slack, B, require_sla, out_best, static_cast<hipStream_t>(hip_stream));
+}
+
+SsTimingRec *ss_timing_start(int kernel, hipStream_t stream) {
+  if (!g_timing_on.load()) return nullptr;
+  auto *r = new SsTimingRec{kernel, nullptr, nullptr};
+  if (hipEventCreate(&r->start) != hipSuccess || hipEventCreate(&r->stop) != hipSuccess ||
+      hipEventRecord(r->start, stream) != hipSuccess) {
+    drop_record(r);
+    return nullptr;
+  }
+  return r;
+}
+
+void ss_timing_stop(SsTimingRec *r, hipStream_t stream) {
+  if (!r) return;
+  if (hipEventRecord(r->stop, stream) != hipSuccess) {
+    drop_record(r);
+    return;
+  }
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  g_timing.push_back(r);
+}
+
+extern "C" int ss_kernel_timing(int enable) {
+  ss_clear_error();
+  g_timing_on.store(enable ? 1 : 0);
+  if (!enable) {
+    std::lock_guard<std::mutex> lk(g_timing_mu);
+    for (auto *r : g_timing) drop_record(r);
+    g_timing.clear();
+  }
+  return SS_OK;
+}
+
+extern "C" int ss_kernel_time(int kernel, int64_t *launches, double *total_ms) {
+  ss_clear_error();
+  if (!launches || !total_ms || kernel < SS_KERNEL_SCHEDULE || kernel > SS_KERNEL_SELECT)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_kernel_time: bad kernel id or NULL output");
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  int64_t n = 0;
+  double ms = 0.0;
+  int rc = SS_OK;
+  std::vector<SsTimingRec *> keep;
+  for (auto *r : g_timing) {
+    if (r->kernel != kernel) {
+      keep.push_back(r);
+      continue;
+    }
+    float t = 0.f;
+    if (hipEventSynchronize(r->stop) != hipSuccess || hipEventElapsedTime(&t, r->start, r->stop) != hipSuccess)
+      rc = ss_set_error(SS_ERR_DEVICE, "ss_kernel_time: reading a timing event failed");
+    ms += t;
+    ++n;
+    drop_record(r);
+  }
+  g_timing.swap(keep);
+  *launches = n;
+  *total_ms = ms;
+  return rc;
 }

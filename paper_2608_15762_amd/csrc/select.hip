@@ -86,6 +86,7 @@ int ss_run_select(const ss_gmg *g, const uint8_t *violation, const int64_t *key,
   hipError_t err = hipMallocAsync(&part, (size_t)nblk * 2 * sizeof(int64_t), stream);
   if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of selection scratch");
   int rc = SS_OK;
+  SsTimingRec *t_sel = ss_timing_start(SS_KERNEL_SELECT, stream);
   hipLaunchKernelGGL(select_partial, dim3(nblk), dim3(kThreads), 0, stream, violation, key, slack, g->n_req, B,
                      require_sla, static_cast<int64_t *>(part));
   err = hipGetLastError();
@@ -96,6 +97,7 @@ int ss_run_select(const ss_gmg *g, const uint8_t *violation, const int64_t *key,
     err = hipGetLastError();
     if (err != hipSuccess) rc = hip_fail(err, "select_final launch");
   }
+  ss_timing_stop(t_sel, stream);
   err = hipFreeAsync(part, stream);
   if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
   return rc;

@@ -371,19 +371,23 @@ int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makes
   for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
     const int64_t nb = std::min(chunk, B - b0);
     const uint8_t *Pc = P + b0 * N;
+    SsTimingRec *t_sched = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
     hipLaunchKernelGGL(schedule_kernel, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), sched_lds, stream,
                        G, Pc, nb, fin, comp, makespan + b0, sumfin ? sumfin + b0 : nullptr,
                        slack ? slack + b0 * R : nullptr, violation + b0);
     err = hipGetLastError();
+    ss_timing_stop(t_sched, stream);
     if (err != hipSuccess) {
       rc = hip_fail(err, "schedule_kernel launch");
       break;
     }
     const int64_t grid = std::min<int64_t>(nb, nslots);
+    SsTimingRec *t_mem = ss_timing_start(SS_KERNEL_MEMORY, stream);
     hipLaunchKernelGGL(memory_kernel, dim3((unsigned)grid), dim3(kWave), 0, stream, G, Pc, nb,
                        static_cast<const int64_t *>(fin), bydev, gkeys, gvals, slot_cap,
                        peak ? peak + b0 * D : nullptr, violation + b0);
     err = hipGetLastError();
+    ss_timing_stop(t_mem, stream);
     if (err != hipSuccess) rc = hip_fail(err, "memory_kernel launch");
   }
   err = hipFreeAsync(scratch, stream);

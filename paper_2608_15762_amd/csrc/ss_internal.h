@@ -35,6 +35,12 @@ struct ss_gmg {
 int ss_set_error(int code, const std::string &msg);
 void ss_clear_error();
 
+// Optional per-kernel event timing (abi.cpp): returns a started record or
+// nullptr when timing is off; ss_timing_stop closes it on the same stream.
+struct SsTimingRec;
+SsTimingRec *ss_timing_start(int kernel, hipStream_t stream);
+void ss_timing_stop(SsTimingRec *rec, hipStream_t stream);
+
 // Kernel drivers (simulate.hip / select.hip).  Arguments are already checked.
 int ss_run_simulate(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
                     uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream);

@@ -22,7 +22,10 @@ SS_LAYOUT_ROW_MAJOR = 0
 SS_VIOLATION_MEMORY = 0x1
 SS_VIOLATION_INVALID = 0x4
 SS_SELECT_REQUIRE_SLA = 0x1
-EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "ss_select_best", "ss_last_error")
+EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "ss_select_best", "ss_kernel_timing",
+            "ss_kernel_time", "ss_last_error")
+SS_KERNEL_SCHEDULE, SS_KERNEL_MEMORY, SS_KERNEL_SELECT = 0, 1, 2
+KERNEL_NAMES = {0: "schedule_kernel", 1: "memory_kernel", 2: "select"}
 
 _lib = None
 _lock = threading.Lock()
@@ -59,6 +62,10 @@ def lib():
             L.ss_simulate_batch.restype = ctypes.c_int
             L.ss_select_best.argtypes = [P, P, P, P, I64, ctypes.c_int, P, P]
             L.ss_select_best.restype = ctypes.c_int
+            L.ss_kernel_timing.argtypes = [ctypes.c_int]
+            L.ss_kernel_timing.restype = ctypes.c_int
+            L.ss_kernel_time.argtypes = [ctypes.c_int, P, P]
+            L.ss_kernel_time.restype = ctypes.c_int
             L.ss_last_error.argtypes = []
             L.ss_last_error.restype = ctypes.c_char_p
             _lib = L
@@ -153,3 +160,15 @@ def select_best(g: Gmg, violation, key, slack=None, require_sla=False, out=None,
     _check(lib().ss_select_best(g.handle, _ptr(violation), _ptr(key), _ptr(slack), B,
                                 SS_SELECT_REQUIRE_SLA if require_sla else 0, _ptr(out), _stream_ptr(stream)))
     return out
+
+
+def kernel_timing(enable: bool) -> None:
+    """Turn per-kernel HIP event timing on or off (process-wide)."""
+    _check(lib().ss_kernel_timing(1 if enable else 0))
+
+
+def kernel_time(kernel: int) -> tuple[int, float]:
+    """(launches, summed milliseconds) recorded for one kernel kind since the last read."""
+    n, ms = ctypes.c_int64(), ctypes.c_double()
+    _check(lib().ss_kernel_time(kernel, ctypes.byref(n), ctypes.byref(ms)))
+    return n.value, ms.value
