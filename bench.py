@@ -34,6 +34,7 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--gen-chunk", type=int, default=32768, help="candidates generated per host chunk")
+    ap.add_argument("--candidates", type=int, default=0, help="first N candidates only (default: the whole batch)")
     return ap.parse_args()
 
 
@@ -123,6 +124,8 @@ def main():
     cfg = synth.CONFIGS[cid]
     g = synth.build_gmg(cid)
     B, N, D, R = cfg.n_cand, g.n_ops, g.n_dev, g.n_req
+    if args.candidates > 0:
+        B = min(B, args.candidates)
     log(f"workload {cfg.name}: N={N} E={g.n_edges} D={D} R={R} B={B}")
     h = ss.Gmg(g)
     t0 = time.perf_counter()

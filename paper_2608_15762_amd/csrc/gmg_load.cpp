@@ -139,6 +139,21 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     const int64_t S = d->slice_ptr[D];
     if (S >= INT32_MAX) return ss_set_error(SS_ERR_UNSUPPORTED, "too many idle slices in total");
 
+    // 32-bit time path: every time the simulation can produce is <= horizon
+    const bool time32 = horizon < (i128)UINT32_MAX && N <= 65535;
+    std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32;
+    if (time32) {
+      dur32.assign(d->dur, d->dur + N * C);
+      xfer32.assign(xfer.begin(), xfer.end());
+      rel32.assign(d->release, d->release + R);
+      sb32.resize(S);
+      se32.resize(S);
+      for (int64_t k = 0; k < S; ++k) {
+        sb32[k] = (uint32_t)d->slice_begin[k];
+        se32[k] = d->slice_end[k] == SS_TIME_INF ? UINT32_MAX : (uint32_t)d->slice_end[k];
+      }
+    }
+
     // ------------------------------------------------------------- staging
     Packer pk;
     const size_t o_pred_ptr = pk.add(pred_ptr);
@@ -157,6 +172,8 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     const size_t o_rel = pk.add(d->release, R * sizeof(int64_t));
     const size_t o_dl = pk.add(d->deadline, R * sizeof(int64_t));
     const size_t o_link = pk.add(d->link_class, D * D);
+    const size_t o_dur32 = pk.add(dur32), o_xfer32 = pk.add(xfer32), o_sb32 = pk.add(sb32), o_se32 = pk.add(se32),
+                 o_rel32 = pk.add(rel32);
     pk.add(nullptr, 256);  // tail padding
 
     ss_gmg *g = new ss_gmg();
@@ -196,6 +213,12 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     V.release = reinterpret_cast<const int64_t *>(base + o_rel);
     V.deadline = reinterpret_cast<const int64_t *>(base + o_dl);
     V.link_class = reinterpret_cast<const uint8_t *>(base + o_link);
+    V.time32 = time32 ? 1 : 0;
+    V.dur32 = reinterpret_cast<const uint32_t *>(base + o_dur32);
+    V.xfer32 = reinterpret_cast<const uint32_t *>(base + o_xfer32);
+    V.slice_begin32 = reinterpret_cast<const uint32_t *>(base + o_sb32);
+    V.slice_end32 = reinterpret_cast<const uint32_t *>(base + o_se32);
+    V.release32 = reinterpret_cast<const uint32_t *>(base + o_rel32);
     g->n_ops = N;
     g->n_edges = E;
     g->n_dev = D;
@@ -203,6 +226,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     g->n_link = K;
     g->n_req = R;
     g->max_slices = max_slices;
+    g->horizon = (int64_t)horizon;
     *out = g;
     return SS_OK;
   } catch (const std::bad_alloc &) {

@@ -18,6 +18,8 @@
 //   A device with more endpoints than fit in LDS uses the same code on a
 //   per-workgroup global buffer.
 #include <climits>
+#include <cstdlib>
+#include <cstring>
 
 #include "ss_internal.h"
 
@@ -325,8 +327,9 @@ int hip_fail(hipError_t err, const char *what) {
 
 }  // namespace
 
-int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
-                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream) {
+// General path: int64 times, any size the loader accepts.
+static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
+                                uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream) {
   const GmgView &G = g->view;
   const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req;
   const int64_t slot_cap = 2 * (N + E) + 2;
@@ -393,4 +396,21 @@ int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makes
   err = hipFreeAsync(scratch, stream);
   if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
   return rc;
+}
+
+// Path choice: the 32-bit fast path when the loader enabled it and its LDS
+// state fits; SS_PATH=generic or SS_PATH=fast in the environment forces one
+// (fast is still refused when the GMG does not qualify).
+int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
+                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream) {
+  int lds_max = 0;
+  hipError_t err = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, g->device);
+  if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
+  const bool fast_ok = g->view.time32 && ss_fast_schedule_lds(g) <= (size_t)lds_max;
+  const char *path = std::getenv("SS_PATH");
+  if (path && std::strcmp(path, "fast") == 0 && !fast_ok)
+    return ss_set_error(SS_ERR_UNSUPPORTED, "SS_PATH=fast but this GMG needs the general path");
+  const bool generic = !fast_ok || (path && std::strcmp(path, "generic") == 0);
+  if (generic) return run_simulate_generic(g, P, B, makespan, peak, violation, slack, sumfin, stream);
+  return ss_run_simulate_fast(g, P, B, makespan, peak, violation, slack, sumfin, stream);
 }

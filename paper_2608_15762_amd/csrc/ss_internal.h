@@ -21,12 +21,19 @@ struct GmgView {
   const int64_t *slice_begin, *slice_end;
   const int64_t *cap, *release, *deadline;
   const uint8_t *link_class;  // [D][D]
+  // 32-bit copies of every time quantity, present when the loader proved the
+  // whole time horizon (all starts, finishes, frees and finite slice bounds)
+  // stays below 2^32 - 1 and there are at most 65535 ops; the open slice end
+  // becomes 0xFFFFFFFF.
+  int32_t time32;
+  const uint32_t *dur32, *xfer32, *slice_begin32, *slice_end32, *release32;
 };
 
 struct ss_gmg {
   int device = 0;
   int64_t n_ops = 0, n_edges = 0, n_dev = 0, n_class = 0, n_link = 0, n_req = 0;
   int64_t max_slices = 0;  // largest slice count of any device
+  int64_t horizon = 0;     // loader's upper bound on every simulated time
   void *dev_mem = nullptr;
   GmgView view{};
 };
@@ -44,5 +51,9 @@ void ss_timing_stop(SsTimingRec *rec, hipStream_t stream);
 // Kernel drivers (simulate.hip / select.hip).  Arguments are already checked.
 int ss_run_simulate(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
                     uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream);
+// Fast path (sim_fast.hip): 32-bit times, N <= 65535.
+size_t ss_fast_schedule_lds(const ss_gmg *g);
+int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
+                         uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream);
 int ss_run_select(const ss_gmg *g, const uint8_t *violation, const int64_t *key, const int64_t *slack, int64_t B,
                   int require_sla, int64_t *out_best, hipStream_t stream);

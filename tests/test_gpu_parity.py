@@ -16,6 +16,17 @@ pytestmark = pytest.mark.gpu
 FIELDS = ("makespan", "peak", "violation", "slack", "sumfin")
 
 
+@pytest.fixture(params=["auto", "generic"])
+def path(request, monkeypatch):
+    """Run a case on the default path (the 32-bit fast path when the GMG
+    qualifies) and on the general int64 path."""
+    if request.param == "generic":
+        monkeypatch.setenv("SS_PATH", "generic")
+    else:
+        monkeypatch.delenv("SS_PATH", raising=False)
+    return request.param
+
+
 @pytest.fixture(scope="module")
 def dev():
     assert torch.cuda.is_available(), "GPU tests need a GPU"
@@ -42,7 +53,7 @@ def assert_same(gpu, ref, idx=None, label=""):
 
 
 @pytest.mark.parametrize("cid,nb", [(0, 256), (1, 1000), (2, 300), (3, 130), (4, 20)])
-def test_config_parity(dev, cid, nb):
+def test_config_parity(dev, path, cid, nb):
     print(f"config {cid}: {nb} candidates", flush=True)
     g = synth.build_gmg(cid)
     P = synth.placements(g, cid, 0, nb)
@@ -61,7 +72,7 @@ FUZZ = [dict(n_ops=n, n_dev=D, n_req=R, n_slices=S, n_class=C, n_link=K, rel_max
 
 
 @pytest.mark.parametrize("seed", range(len(FUZZ)))
-def test_fuzz_parity(dev, seed):
+def test_fuzz_parity(dev, path, seed):
     kw = FUZZ[seed]
     print(f"fuzz {seed}: {kw}", flush=True)
     g = synth.random_gmg(seed, **kw)
@@ -76,7 +87,7 @@ def test_fuzz_parity(dev, seed):
     assert (got["violation"] == 4).sum() >= 1
 
 
-def test_nullable_outputs_and_empty_batch(dev):
+def test_nullable_outputs_and_empty_batch(dev, path):
     g = synth.build_gmg(0)
     h = ss.Gmg(g)
     P = synth.placements(g, 0, 0, 70)
@@ -87,7 +98,7 @@ def test_nullable_outputs_and_empty_batch(dev):
     assert empty["makespan"].shape == (0,)
 
 
-def test_zero_ops_gmg(dev):
+def test_zero_ops_gmg(dev, path):
     g = make_gmg(3, [], [], [], np.zeros((0, 1), np.int64), [], [[(0, TIME_INF)]] * 3, [5, 5, 5], [4], [10])
     P = np.zeros((5, 0), np.uint8)
     ref = oracle.simulate_batch(g, P)
@@ -96,7 +107,7 @@ def test_zero_ops_gmg(dev):
     assert got["slack"].tolist() == [[6]] * 5
 
 
-def test_max_devices(dev):
+def test_max_devices(dev, path):
     g = synth.random_gmg(7, n_ops=300, n_dev=255, n_req=3, n_slices=3, n_link=2, cap_scale=3000)
     st = synth.Stream(99)
     P = np.array([[st.uniform_int(0, 255) for _ in range(g.n_ops)] for _ in range(130)], np.uint8)
@@ -105,7 +116,7 @@ def test_max_devices(dev):
     assert_same(got, ref, label="255 devices")
 
 
-def test_crowded_device_uses_global_sort_buffer(dev):
+def test_crowded_device_uses_global_sort_buffer(dev, path):
     """All 2,052 ops of the 4-tenant workload on one device: > 2,048 endpoints."""
     g = synth.build_gmg(2)
     P = np.zeros((6, g.n_ops), np.uint8)
@@ -114,6 +125,25 @@ def test_crowded_device_uses_global_sort_buffer(dev):
     ref = oracle.simulate_batch(g, P)
     got = gpu_run(ss.Gmg(g), P, dev)
     assert_same(got, ref, label="crowded")
+
+
+def test_horizon_beyond_32_bits_takes_general_path(dev, monkeypatch):
+    """Slices far beyond 2^32 us: the fast path must be refused and the general
+    path must still match the oracle."""
+    g = synth.random_gmg(11, n_ops=90, n_dev=4, n_req=2, n_slices=4, n_link=2, cap_scale=2000)
+    shift = 1 << 33
+    g.slice_begin = g.slice_begin + shift
+    g.slice_end = np.where(g.slice_end == TIME_INF, TIME_INF, g.slice_end + shift)
+    st = synth.Stream(5)
+    P = np.array([[st.uniform_int(0, 3) for _ in range(g.n_ops)] for _ in range(150)], np.uint8)
+    ref = oracle.simulate_batch(g, P)
+    assert ref["makespan"].min() > shift
+    h = ss.Gmg(g)
+    monkeypatch.delenv("SS_PATH", raising=False)
+    assert_same(gpu_run(h, P, dev), ref, label="horizon 2^33")
+    monkeypatch.setenv("SS_PATH", "fast")
+    with pytest.raises(ss.SSError):
+        gpu_run(h, P, dev)
 
 
 # ------------------------------------------------------------------ selection
@@ -155,7 +185,7 @@ def test_select_best_ties_and_sizes(dev, B):
 
 # ------------------------------------------------------------------ full-size batches
 @pytest.mark.parametrize("cid,n_sample", [(1, 256), (2, 64), (3, 32)])
-def test_full_batch_sampled_parity(dev, cid, n_sample):
+def test_full_batch_sampled_parity(dev, path, cid, n_sample):
     """The whole batch of a workload in one call (the configuration the
     benchmark times), checked against the oracle on sampled candidates."""
     g = synth.build_gmg(cid)
