@@ -173,6 +173,8 @@ int ss_select_best(const ss_gmg *g, const uint8_t *violation, const int64_t *key
 #define SS_KERNEL_SCHEDULE 0     /* per-candidate list schedule (one lane per candidate) */
 #define SS_KERNEL_MEMORY 1       /* per-device peak memory (one wave per candidate) */
 #define SS_KERNEL_SELECT 2       /* best-candidate reduction (both passes) */
+#define SS_KERNEL_INTERVALS 3    /* residency intervals into per-device buckets (fast path) */
+#define SS_KERNEL_TRANSPOSE 4    /* layout changes between the passes (fast path) */
 int ss_kernel_timing(int enable);
 int ss_kernel_time(int kernel, int64_t *launches, double *total_ms);
 

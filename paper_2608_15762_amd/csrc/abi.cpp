@@ -107,7 +107,7 @@ extern "C" int ss_kernel_timing(int enable) {
 
 extern "C" int ss_kernel_time(int kernel, int64_t *launches, double *total_ms) {
   ss_clear_error();
-  if (!launches || !total_ms || kernel < SS_KERNEL_SCHEDULE || kernel > SS_KERNEL_SELECT)
+  if (!launches || !total_ms || kernel < SS_KERNEL_SCHEDULE || kernel > SS_KERNEL_TRANSPOSE)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_kernel_time: bad kernel id or NULL output");
   std::lock_guard<std::mutex> lk(g_timing_mu);
   int64_t n = 0;

@@ -140,7 +140,9 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     if (S >= INT32_MAX) return ss_set_error(SS_ERR_UNSUPPORTED, "too many idle slices in total");
 
     // 32-bit time path: every time the simulation can produce is <= horizon
-    const bool time32 = horizon < (i128)UINT32_MAX && N <= 65535;
+    int64_t max_bytes = 0;
+    for (int64_t v = 0; v < N; ++v) max_bytes = std::max(max_bytes, d->out_bytes[v]);
+    const bool time32 = horizon < (i128)UINT32_MAX && N <= 65535 && max_bytes <= (int64_t)UINT32_MAX;
     std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32;
     if (time32) {
       dur32.assign(d->dur, d->dur + N * C);

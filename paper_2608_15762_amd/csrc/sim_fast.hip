@@ -1,29 +1,33 @@
 // Fast path of the batched what-if simulation (gfx950), used when the loader
 // proved that every simulated time fits in 32 bits and N <= 65535.
 //
-// fast_schedule: one lane per candidate, ops in index order (Sec. 3.3.2-3.3.3).
-//   Per (device, lane) LDS state, laid out [device][lane] so the 64 lanes of a
-//   wave fall in distinct banks whatever device each one touches:
-//     clk  u32  effective clock = max(device's last finish, current slice start)
-//     cur  u16  current idle slice (relative index)
-//     cnt  u16  ops placed on the device so far
-//   An op first tries the current slice (one load of its end); only when it
-//   does not fit does the lane walk forward through later slices.  Each op's
-//   finish time and its rank among the ops of its device are written to the
-//   candidate's scratch row; the per-device op counts at the end.
-//
-// fast_memory: one wave per candidate.
-//   1. A pass over the ops in index order (lanes = consecutive ops, so the
-//      candidate's rows are read with coalesced loads) writes every residency
-//      interval into a per-device bucket: an op's own output at the slot given
-//      by its rank (so a device's own intervals are in index order, hence in
-//      start-time order), and one copy per (output, remote device).
-//   2. Per device, only the copy allocations are sorted (LDS bitonic); they
-//      are merged with the already sorted own allocations by binary-search
-//      ranks, every free is scattered by binary search onto the first
-//      allocation at or after it (frees precede allocations at equal times),
-//      and peak = max over allocation instants of (bytes allocated so far -
-//      bytes freed so far).  No full sort of all endpoints is needed.
+// Per chunk of candidates:
+//   transpose     candidates' placement rows -> op-major [op][candidate]
+//   fast_schedule one lane per candidate, ops in index order (Sec. 3.3.2-3.3.3).
+//                 Per (device, lane) LDS state laid out [device][lane], so a
+//                 wave's 64 lanes fall in distinct banks whatever device each
+//                 touches: effective clock u32 (= max(last finish, current
+//                 slice start)), slice cursor u16, op count u16.  An op first
+//                 tries the current slice; only when it does not fit does the
+//                 lane walk forward through later slices.  While op v is
+//                 placed, the next op's device, predecessor values and slice
+//                 end are already being fetched.  Writes op-major finish times
+//                 and per-device ranks, and per-device op counts.
+//   transpose     finish times and ranks back to candidate rows
+// then per sub-chunk of candidates:
+//   fast_intervals one wave per candidate, lanes = consecutive ops (coalesced
+//                 row reads), almost no LDS so many waves hide the gathers.
+//                 Writes every residency interval (Sec. 3.3.2) into a
+//                 per-device bucket: own outputs at their rank (so a device's
+//                 own intervals are start-sorted), one copy per (output,
+//                 remote device) in a region bounded by the device's summed
+//                 in-degree.
+//   fast_peaks    one wave per candidate.  Per device: sort only the copy
+//                 allocations (LDS bitonic), merge them with the sorted own
+//                 allocations by binary-search ranks, scatter every free onto
+//                 the first allocation at or after it (frees precede
+//                 allocations at equal times), and take the maximum of
+//                 allocated-so-far minus freed-so-far over the allocations.
 #include <climits>
 
 #include "ss_internal.h"
@@ -33,32 +37,70 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kCap = 1024;            // allocations of one device evaluated in LDS
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
-constexpr int64_t kScratchBudget = int64_t(16) << 30;
-constexpr int kMemBlocksPerCU = 4;
+constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per chunk
+constexpr int64_t kRecordBudget = int64_t(12) << 30;   // interval records per sub-chunk
+constexpr int kPeakBlocksPerCU = 4;
+constexpr int kMaxPre = 4;            // predecessors fetched one op ahead
 
 __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
 __device__ __forceinline__ int64_t imax64(int64_t a, int64_t b) { return a > b ? a : b; }
 
+// ------------------------------------------------------------------ transpose
+// 64 x 64 tiles through LDS: both the read and the write are coalesced.
+template <class T>
+__global__ __launch_bounds__(256) void transpose_tiles(const T *__restrict__ in, int64_t rows, int64_t cols,
+                                                       T *__restrict__ out) {
+  __shared__ T tile[64][65];
+  const int64_t c0 = (int64_t)blockIdx.x * 64, r0 = (int64_t)blockIdx.y * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int64_t r = r0 + i, c = c0 + tx;
+    if (r < rows && c < cols) tile[i][tx] = in[r * cols + c];
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int64_t c = c0 + i, r = r0 + tx;
+    if (c < cols && r < rows) out[c * rows + r] = tile[tx][i];
+  }
+}
+
 // ------------------------------------------------------------------ schedule
-__global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const uint8_t *__restrict__ P, int64_t nb,
-                                                       uint32_t *__restrict__ fin, uint16_t *__restrict__ rank,
-                                                       uint16_t *__restrict__ dcnt, int64_t *__restrict__ makespan,
+__device__ __forceinline__ uint32_t xfer_of(const GmgView &G, int u, int du, int d) {
+  const int K = G.n_link;
+  if (K == 1) return G.xfer32[u];
+  const int k = G.link_class[du * G.n_dev + d];
+  if (K == 2) {  // both entries are wave-uniform loads
+    const uint32_t x0 = G.xfer32[2 * u], x1 = G.xfer32[2 * u + 1];
+    return k ? x1 : x0;
+  }
+  return G.xfer32[u * K + k];
+}
+
+// Operands are op-major ([op][candidate]): at every op the 64 lanes of a wave
+// read and write one contiguous 64-element segment.
+__global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const uint8_t *__restrict__ PT, int64_t nb,
+                                                       uint32_t *__restrict__ finT, uint16_t *__restrict__ rankT,
+                                                       uint16_t *__restrict__ dcntT, int64_t *__restrict__ makespan,
                                                        int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
                                                        uint8_t *__restrict__ violation) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
-  const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = G.n_class, K = G.n_link;
+  const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = G.n_class;
   const int lane = threadIdx.x;
-  uint32_t *clk = reinterpret_cast<uint32_t *>(lds_raw);                               // [D][64]
-  uint32_t *comp = clk + (size_t)D * kWave;                                            // [R][64]
-  uint16_t *cur = reinterpret_cast<uint16_t *>(comp + (size_t)R * kWave);              // [D][64]
-  uint16_t *cnt = cur + (size_t)D * kWave;                                             // [D][64]
+  uint32_t *clk = reinterpret_cast<uint32_t *>(lds_raw);                  // [D][64]
+  uint32_t *comp = clk + (size_t)D * kWave;                               // [R][64]
+  int32_t *sbase = reinterpret_cast<int32_t *>(comp + (size_t)R * kWave);  // [D+1] slice ranges of the devices
+  int32_t *dcls = sbase + D + 1;                                          // [D] device class
+  uint16_t *cur = reinterpret_cast<uint16_t *>(dcls + D);                 // [D][64]
+  uint16_t *cnt = cur + (size_t)D * kWave;                                // [D][64]
+  for (int d = lane; d <= D; d += kWave) {
+    sbase[d] = G.slice_ptr[d];
+    if (d < D) dcls[d] = G.dev_class[d];
+  }
+  __syncthreads();
   const int64_t c = (int64_t)blockIdx.x * kWave + lane;
   if (c >= nb) return;
-  const uint8_t *prow = P + c * N;
-  uint32_t *frow = fin + c * N;
-  uint16_t *rrow = rank + c * N;
   for (int d = 0; d < D; ++d) {
-    clk[d * kWave + lane] = G.slice_begin32[G.slice_ptr[d]];
+    clk[d * kWave + lane] = G.slice_begin32[sbase[d]];
     cur[d * kWave + lane] = 0;
     cnt[d * kWave + lane] = 0;
   }
@@ -67,36 +109,70 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   bool invalid = false;
   uint32_t ms = 0;
   uint64_t sum = 0;
-  for (int v = 0; v < N; ++v) {
-    int d = prow[v];
+  int d = 0;
+  uint32_t E = 0;  // end of the current slice of op v's device
+  if (N > 0) {
+    d = PT[c];
     if (d >= D) {
       invalid = true;
       d = 0;
     }
-    const uint32_t w = G.dur32[v * C + G.dev_class[d]];
+    E = G.slice_end32[sbase[d]];
+  }
+  uint32_t pf[kMaxPre];  // finish and device of op v's first predecessors (fetched during op v-1)
+  int pd[kMaxPre];
+#pragma unroll
+  for (int i = 0; i < kMaxPre; ++i) {
+    pf[i] = 0;
+    pd[i] = 0;
+  }
+  uint32_t f_prev = 0;
+  int d_prev = 0;
+  for (int v = 0; v < N; ++v) {
+    const int dn_raw = (v + 1 < N) ? PT[(int64_t)(v + 1) * nb + c] : 0;
+    const uint32_t w = (C == 1) ? G.dur32[v] : G.dur32[v * C + dcls[d]];
     const int r = G.op_req[v];
+    // ready: release, and every predecessor's finish plus its transfer
     uint32_t ready = G.release32[r];
-    const int e1 = G.pred_ptr[v + 1];
-    for (int e = G.pred_ptr[v]; e < e1; ++e) {
+    const int e0 = G.pred_ptr[v], e1 = G.pred_ptr[v + 1];
+#pragma unroll
+    for (int i = 0; i < kMaxPre; ++i) {
+      if (e0 + i < e1) {
+        const int u = G.pred_idx[e0 + i];
+        const bool last = (u == v - 1);
+        uint32_t t = last ? f_prev : pf[i];
+        const int du = last ? d_prev : pd[i];
+        if (du != d) t += xfer_of(G, u, du, d);
+        ready = umax32(ready, t);
+      }
+    }
+    for (int e = e0 + kMaxPre; e < e1; ++e) {  // more predecessors than were fetched ahead
       const int u = G.pred_idx[e];
-      uint32_t t = frow[u];
-      int du = prow[u];
-      if (du >= D) du = 0;
-      if (du != d) t += G.xfer32[u * K + G.link_class[du * D + d]];
+      uint32_t t;
+      int du;
+      if (u == v - 1) {
+        t = f_prev;
+        du = d_prev;
+      } else {
+        t = finT[(int64_t)u * nb + c];
+        du = PT[(int64_t)u * nb + c];
+        if (du >= D) du = 0;
+      }
+      if (du != d) t += xfer_of(G, u, du, d);
       ready = umax32(ready, t);
     }
+    // one op at a time, in the current idle slice if it fits there, else in the
+    // first later slice that holds it (later slices start after the device's
+    // last finish, so only the ready time and the slice start matter there)
     const int slot = d * kWave + lane;
-    const int sbase = G.slice_ptr[d];
-    int k = cur[slot];
-    uint32_t s = umax32(ready, clk[slot]);  // clk already includes the current slice's start
-    if (s + w > G.slice_end32[sbase + k]) {
-      // does not fit in the current slice: first later slice that holds it
-      // (every later slice starts after the device's last finish)
+    uint32_t s = umax32(ready, clk[slot]);
+    if (s + w > E) {
+      const int sb = sbase[d];
+      int k = cur[slot];
       for (;;) {
         ++k;
-        const uint32_t a = G.slice_begin32[sbase + k];
-        const uint32_t t = umax32(ready, a);
-        if (t + w <= G.slice_end32[sbase + k]) {
+        const uint32_t t = umax32(ready, G.slice_begin32[sb + k]);
+        if (t + w <= G.slice_end32[sb + k]) {
           s = t;
           break;
         }
@@ -107,62 +183,74 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     clk[slot] = f;
     const uint16_t rk = cnt[slot];
     cnt[slot] = rk + 1;
-    frow[v] = f;
-    rrow[v] = rk;
+    finT[(int64_t)v * nb + c] = f;
+    rankT[(int64_t)v * nb + c] = rk;
     ms = umax32(ms, f);
     sum += f;
     uint32_t *cr = comp + r * kWave + lane;
     *cr = umax32(*cr, f);
+    f_prev = f;
+    d_prev = d;
+    if (v + 1 < N) {  // fetch what op v+1 needs while this wave moves on
+      const int q0 = G.pred_ptr[v + 1], q1 = G.pred_ptr[v + 2];
+#pragma unroll
+      for (int i = 0; i < kMaxPre; ++i) {
+        if (q0 + i < q1) {
+          const int u = G.pred_idx[q0 + i];
+          if (u != v) {
+            pf[i] = finT[(int64_t)u * nb + c];
+            const int du = PT[(int64_t)u * nb + c];
+            pd[i] = du >= D ? 0 : du;
+          }
+        }
+      }
+      d = dn_raw;
+      if (d >= D) {
+        invalid = true;
+        d = 0;
+      }
+      E = G.slice_end32[sbase[d] + cur[d * kWave + lane]];
+    }
   }
-  uint16_t *crow = dcnt + c * D;
-  for (int d = 0; d < D; ++d) crow[d] = cnt[d * kWave + lane];
+  for (int dd = 0; dd < D; ++dd) dcntT[(int64_t)dd * nb + c] = cnt[dd * kWave + lane];
   if (invalid) {
     makespan[c] = INT64_MAX;
     if (sumfin) sumfin[c] = INT64_MAX;
     if (slack)
-      for (int r = 0; r < R; ++r) slack[c * R + r] = INT64_MIN;
+      for (int rr = 0; rr < R; ++rr) slack[c * R + rr] = INT64_MIN;
     violation[c] = SS_VIOLATION_INVALID;
   } else {
     makespan[c] = ms;
     if (sumfin) sumfin[c] = (int64_t)sum;
     if (slack)
-      for (int r = 0; r < R; ++r) slack[c * R + r] = G.deadline[r] - (int64_t)comp[r * kWave + lane];
+      for (int rr = 0; rr < R; ++rr) slack[c * R + rr] = G.deadline[rr] - (int64_t)comp[rr * kWave + lane];
     violation[c] = 0;
   }
 }
 
 // ------------------------------------------------------------------ memory
-struct Records {  // SoA interval records: [lo, hi) with bytes
-  uint32_t *lo, *hi;
-  int64_t *b;
-};
+// An interval record: {allocation time, free time (kInf32 = never), bytes}.
+using Rec = uint3;
 
-// Intervals of op v (own output, and one copy per remote destination device).
-// kWrite = false only counts the copies per destination (atomics on ccnt).
-template <bool kWrite>
+// Intervals of op v: its own output at its rank in its device's bucket, and
+// one copy per remote destination device (slot taken with an LDS atomic).
 __device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32_t *frow, const uint16_t *rrow, int v,
-                             const int *own_off, int *cfill, Records own, Records cp) {
-  const int D = G.n_dev, K = G.n_link, C = G.n_class;
+                             const int *own_off, int *cfill, Rec *own, Rec *cp) {
+  const int C = G.n_class;
   const int d = prow[v];
-  const int64_t b = G.out_bytes[v];
+  const uint32_t b = (uint32_t)G.out_bytes[v];
   const int x0 = G.succ_ptr[v], x1 = G.succ_ptr[v + 1];
-  if (kWrite) {
-    const uint32_t f = frow[v];
-    uint32_t F = kInf32;  // kept forever without consumers
-    if (x1 > x0) {
-      F = f;
-      for (int q = x0; q < x1; ++q) {
-        const int x = G.succ_idx[q];
-        const int dx = prow[x];
-        const uint32_t t = (dx == d) ? frow[x] : f + G.xfer32[v * K + G.link_class[d * D + dx]];
-        F = umax32(F, t);
-      }
+  const uint32_t f = frow[v];
+  uint32_t F = kInf32;  // kept forever without consumers
+  if (x1 > x0) {
+    F = f;
+    for (int q = x0; q < x1; ++q) {
+      const int x = G.succ_idx[q];
+      const int dx = prow[x];
+      F = umax32(F, (dx == d) ? frow[x] : f + xfer_of(G, v, d, dx));
     }
-    const int pos = own_off[d] + rrow[v];
-    own.lo[pos] = f - G.dur32[v * C + G.dev_class[d]];
-    own.hi[pos] = F;
-    own.b[pos] = b;
   }
+  own[own_off[d] + rrow[v]] = Rec{f - G.dur32[v * C + G.dev_class[d]], F, b};
   if (b == 0) return;
   for (int q = x0; q < x1; ++q) {
     const int e = prow[G.succ_idx[q]];
@@ -171,45 +259,91 @@ __device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32
     for (int q2 = x0; q2 < q; ++q2)
       if (prow[G.succ_idx[q2]] == e) first = false;
     if (!first) continue;
-    const int pos = atomicAdd(&cfill[e], 1);
-    if (kWrite) {
-      uint32_t g = 0;
-      for (int q2 = q; q2 < x1; ++q2) {
-        const int x = G.succ_idx[q2];
-        if (prow[x] == e) g = umax32(g, frow[x]);
-      }
-      cp.lo[pos] = frow[v];
-      cp.hi[pos] = g;
-      cp.b[pos] = b;
+    uint32_t g = 0;  // the copy lives until its last consumer on e finishes
+    for (int q2 = q; q2 < x1; ++q2) {
+      const int x = G.succ_idx[q2];
+      if (prow[x] == e) g = umax32(g, frow[x]);
     }
+    cp[atomicAdd(&cfill[e], 1)] = Rec{f, g, b};
   }
 }
 
-__device__ __forceinline__ int lower_bound_u32(const uint32_t *a, int n, uint32_t x) {  // first i with a[i] >= x
-  int lo = 0, hi = n;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (a[mid] < x)
-      lo = mid + 1;
-    else
-      hi = mid;
+// Per-candidate bucket geometry written by fast_intervals, read by fast_peaks.
+__device__ __forceinline__ int meta_stride(int D) { return 3 * (D + 1); }
+
+__global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const uint8_t *__restrict__ P,
+                                                        const uint32_t *__restrict__ fin,
+                                                        const uint16_t *__restrict__ rank,
+                                                        const uint16_t *__restrict__ dcntT, int64_t nb, int64_t j0,
+                                                        Rec *__restrict__ own_all, Rec *__restrict__ cp_all,
+                                                        int32_t *__restrict__ meta,
+                                                        const uint8_t *__restrict__ violation) {
+  __shared__ int own_off[257], cp_off[257], cfill[256];
+  const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops];
+  const int lane = threadIdx.x;
+  const int64_t j = blockIdx.x, c = j0 + j;
+  if (violation[c] & SS_VIOLATION_INVALID) return;
+  const uint8_t *prow = P + c * N;
+  const uint32_t *frow = fin + c * N;
+  const uint16_t *rrow = rank + c * N;
+  Rec *own = own_all + j * N;
+  Rec *cp = cp_all + j * E;
+  // copies landing on a device <= summed in-degree of its ops: bucket bound
+  for (int d = lane; d < D; d += kWave) cfill[d] = 0;
+  __syncthreads();
+  for (int v = lane; v < N; v += kWave) atomicAdd(&cfill[prow[v]], G.pred_ptr[v + 1] - G.pred_ptr[v]);
+  __syncthreads();
+  if (lane == 0) {
+    int so = 0, sc = 0;
+    for (int d = 0; d < D; ++d) {
+      own_off[d] = so;
+      so += dcntT[(int64_t)d * nb + c];
+      cp_off[d] = sc;
+      sc += cfill[d];
+      cfill[d] = cp_off[d];
+    }
+    own_off[D] = so;
+    cp_off[D] = sc;
   }
-  return lo;
+  __syncthreads();
+  for (int v = lane; v < N; v += kWave) op_intervals(G, prow, frow, rrow, v, own_off, cfill, own, cp);
+  __syncthreads();
+  int32_t *m = meta + j * meta_stride(D);
+  for (int d = lane; d <= D; d += kWave) {
+    m[d] = own_off[d];
+    m[D + 1 + d] = cp_off[d];
+    m[2 * (D + 1) + d] = d < D ? cfill[d] - cp_off[d] : 0;
+  }
 }
 
-__device__ __forceinline__ int upper_bound_u32(const uint32_t *a, int n, uint32_t x) {  // first i with a[i] > x
-  int lo = 0, hi = n;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (a[mid] <= x)
-      lo = mid + 1;
-    else
-      hi = mid;
+// Up to 4 searches per lane in lockstep (independent LDS loads in flight):
+// r[j] = first index i in a[0, n) with a[i] >= x[j] (kUpper: a[i] > x[j]).
+template <bool kUpper, class UP>
+__device__ __forceinline__ void search4(UP a, int n, const uint32_t (&x)[4], int (&r)[4]) {
+  int b[4] = {0, 0, 0, 0};
+  if (n == 0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r[j] = 0;
+    return;
   }
-  return lo;
+  int len = n;
+  while (len > 1) {
+    const int half = len >> 1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t v = a[b[j] + half];
+      if (kUpper ? (v <= x[j]) : (v < x[j])) b[j] += half;
+    }
+    len -= half;
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t v = a[b[j]];
+    r[j] = b[j] + ((kUpper ? (v <= x[j]) : (v < x[j])) ? 1 : 0);
+  }
 }
 
-// ascending bitonic sort of n (u32 key, i64 payload) pairs by one wave
+// ascending bitonic sort of n (u32 key, u64 payload) pairs by one wave
 template <class KP, class VP>
 __device__ void sort_u32_pairs(KP keys, VP vals, int n, int lane) {
   if (n < 2) return;
@@ -224,7 +358,7 @@ __device__ void sort_u32_pairs(KP keys, VP vals, int n, int lane) {
       if (l < n) {
         const uint32_t ki = keys[i], kl = keys[l];
         if (kl < ki) {
-          const int64_t vi = vals[i];
+          const uint64_t vi = vals[i];
           keys[i] = kl;
           keys[l] = ki;
           vals[i] = vals[l];
@@ -240,7 +374,7 @@ __device__ void sort_u32_pairs(KP keys, VP vals, int n, int lane) {
         if (l < n) {
           const uint32_t ki = keys[i], kl = keys[l];
           if (kl < ki) {
-            const int64_t vi = vals[i];
+            const uint64_t vi = vals[i];
             keys[i] = kl;
             keys[l] = ki;
             vals[i] = vals[l];
@@ -261,145 +395,231 @@ __device__ __forceinline__ int64_t wave_incl_scan64(int64_t x, int lane) {
   return x;
 }
 
-// Peak of one device from its own records (start-sorted) and copy records.
-// Work arrays (LDS or a global slot buffer): sk/sb (own then copy allocations),
-// mk/mb (merged allocations, then allocated-so-far), fd (bytes freed).
-template <class UP, class IP, class FP>
-__device__ int64_t device_peak(const Records own, int o0, int n1, const Records cp, int c0, int n4, UP sk, IP sb,
-                               UP mk, IP mb, FP fd, int lane) {
-  const int na = n1 + n4;
-  for (int i = lane; i < n1; i += kWave) {
-    sk[i] = own.lo[o0 + i];
-    sb[i] = own.b[o0 + i];
+__device__ __forceinline__ int wave_incl_scan32(int x, int lane) {
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(x, o, kWave);
+    if (lane >= o) x += y;
   }
-  for (int j = lane; j < n4; j += kWave) {
-    sk[n1 + j] = cp.lo[c0 + j];
-    sb[n1 + j] = cp.b[c0 + j];
+  return x;
+}
+
+constexpr int kSmallGap = 16;  // copies between two own allocations sorted by one lane
+
+// In-place inclusive prefix sum of a[0, n): each lane scans its own contiguous
+// run, one wave scan combines the runs.  Callers fence before and after.
+template <class CP>
+__device__ void prefix_inplace(CP a, int n, int lane) {
+  const int m = (n + kWave - 1) / kWave, lo = lane * m, hi = min(n, lo + m);
+  int s = 0;
+  for (int i = lo; i < hi; ++i) s += a[i];
+  int run = wave_incl_scan32(s, lane) - s;
+  for (int i = lo; i < hi; ++i) {
+    run += a[i];
+    a[i] = run;
+  }
+}
+
+// max(0, max_i sum_{k <= i} (alloc[k] - freed[k])): the peak live bytes, the
+// maximum being taken at allocation instants (each position is one).
+template <class IP, class FP>
+__device__ int64_t max_live(IP alloc, FP freed, int n, int lane) {
+  const int m = (n + kWave - 1) / kWave, lo = lane * m, hi = min(n, lo + m);
+  int64_t s = 0;
+  for (int i = lo; i < hi; ++i) s += alloc[i] - (int64_t)freed[i];
+  int64_t run = wave_incl_scan64(s, lane) - s, best = 0;
+  for (int i = lo; i < hi; ++i) {
+    run += alloc[i] - (int64_t)freed[i];
+    best = imax64(best, run);
+  }
+  for (int o = kWave / 2; o >= 1; o >>= 1) best = imax64(best, __shfl_xor(best, o, kWave));
+  return best;
+}
+
+// Peak of one device from its own records (start-sorted) and copy records.
+// Work arrays (LDS, or a global slot buffer when too large):
+//   sk/sp  allocation times and {free time, bytes} of own (first n1) then copy records
+//   sq     per copy: (gap << 16 | slot), kept in fd's storage until fd is needed;
+//          gap counts / prefix in gc (n1 + 2 ints)
+//   mk/mb  merged allocation times and bytes; fd bytes freed just before each
+template <class UP, class PP, class IP, class FP, class CP>
+__device__ int64_t device_peak(const Rec *own, int o0, int n1, const Rec *cp, int c0, int n4, UP sk, PP sp, CP gc,
+                               UP mk, IP mb, FP fd, int lane) {
+  constexpr int kB = 8;
+  uint32_t *sq = reinterpret_cast<uint32_t *>(fd);
+  const int na = n1 + n4;
+  for (int base = lane; base < na; base += kB * kWave) {  // all loads of a batch in flight together
+    Rec r[kB];
+#pragma unroll
+    for (int j = 0; j < kB; ++j) {
+      const int i = base + j * kWave;
+      if (i < na) r[j] = i < n1 ? own[o0 + i] : cp[c0 + i - n1];
+    }
+#pragma unroll
+    for (int j = 0; j < kB; ++j) {
+      const int i = base + j * kWave;
+      if (i < na) {
+        sk[i] = r[j].x;
+        sp[i] = ((uint64_t)r[j].y << 32) | r[j].z;
+      }
+    }
+  }
+  for (int i = lane; i <= n1 + 1; i += kWave) gc[i] = 0;
+  __syncthreads();
+  // each copy falls in the gap after the last own allocation at or before it
+  int big = 0;  // largest slot this lane saw
+  for (int base = lane; base < n4; base += 4 * kWave) {
+    uint32_t x[4];
+    int r[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j] = base + j * kWave < n4 ? sk[n1 + base + j * kWave] : 0;
+    search4<true>(sk, n1, x, r);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = base + j * kWave;
+      if (i < n4) {
+        const int slot = atomicAdd(&gc[r[j] + 1], 1);
+        sq[i] = ((uint32_t)r[j] << 16) | (uint32_t)slot;
+        big = max(big, slot + 1);
+      }
+    }
+  }
+  for (int o = kWave / 2; o >= 1; o >>= 1) big = max(big, __shfl_xor(big, o, kWave));
+  __syncthreads();
+  const bool small_gaps = big <= kSmallGap;
+  if (small_gaps) {
+    // gc[g + 1] = copies in gap g  ->  gc[g] = copies in gaps before g
+    prefix_inplace(gc, n1 + 2, lane);
+    __syncthreads();
+    // own allocation i follows gaps 0..i ; a copy in gap g follows own 0..g-1
+    for (int i = lane; i < n1; i += kWave) {
+      const int pos = i + gc[i + 1];
+      mk[pos] = sk[i];
+      mb[pos] = (int64_t)(sp[i] & 0xFFFFFFFFu);
+    }
+    for (int i = lane; i < n4; i += kWave) {
+      const int g = (int)(sq[i] >> 16), slot = (int)(sq[i] & 0xFFFFu);
+      const int pos = g + gc[g] + slot;
+      mk[pos] = sk[n1 + i];
+      mb[pos] = (int64_t)(sp[n1 + i] & 0xFFFFFFFFu);
+    }
+    __syncthreads();
+    // order the copies inside each gap (at most kSmallGap of them)
+    for (int g = lane; g <= n1; g += kWave) {
+      const int s0 = g + gc[g], cnt = gc[g + 1] - gc[g];
+      for (int a = 1; a < cnt; ++a) {
+        const uint32_t key = mk[s0 + a];
+        const int64_t val = mb[s0 + a];
+        int z = a - 1;
+        while (z >= 0 && mk[s0 + z] > key) {
+          mk[s0 + z + 1] = mk[s0 + z];
+          mb[s0 + z + 1] = mb[s0 + z];
+          --z;
+        }
+        mk[s0 + z + 1] = key;
+        mb[s0 + z + 1] = val;
+      }
+    }
+  } else {
+    // large gaps: sort the copies, then merge the two runs by ranks
+    sort_u32_pairs(sk + n1, sp + n1, n4, lane);
+    for (int base = lane; base < n1; base += 4 * kWave) {
+      uint32_t x[4];
+      int r[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) x[j] = base + j * kWave < n1 ? sk[base + j * kWave] : 0;
+      search4<false>(sk + n1, n4, x, r);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = base + j * kWave;
+        if (i < n1) {
+          mk[i + r[j]] = x[j];
+          mb[i + r[j]] = (int64_t)(sp[i] & 0xFFFFFFFFu);
+        }
+      }
+    }
+    for (int base = lane; base < n4; base += 4 * kWave) {
+      uint32_t x[4];
+      int r[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) x[j] = base + j * kWave < n4 ? sk[n1 + base + j * kWave] : 0;
+      search4<true>(sk, n1, x, r);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int i = base + j * kWave;
+        if (i < n4) {
+          mk[i + r[j]] = x[j];
+          mb[i + r[j]] = (int64_t)(sp[n1 + i] & 0xFFFFFFFFu);
+        }
+      }
+    }
   }
   __syncthreads();
-  sort_u32_pairs(sk + n1, sb + n1, n4, lane);
-  // merge the two sorted runs by ranks (own before copy at equal keys)
-  for (int i = lane; i < n1; i += kWave) {
-    const int pos = i + lower_bound_u32(sk + n1, n4, sk[i]);
-    mk[pos] = sk[i];
-    mb[pos] = sb[i];
-  }
-  for (int j = lane; j < n4; j += kWave) {
-    const int pos = j + upper_bound_u32(sk, n1, sk[n1 + j]);
-    mk[pos] = sk[n1 + j];
-    mb[pos] = sb[n1 + j];
-  }
   for (int i = lane; i < na; i += kWave) fd[i] = 0;
   __syncthreads();
-  // bytes allocated up to and including each allocation
-  int64_t carry = 0;
-  for (int base = 0; base < na; base += kWave) {
-    const int i = base + lane;
-    int64_t x = i < na ? mb[i] : 0;
-    x = wave_incl_scan64(x, lane) + carry;
-    if (i < na) mb[i] = x;
-    carry = __shfl(x, kWave - 1, kWave);
-  }
   // each free lands on the first allocation at or after its time
-  for (int i = lane; i < n1; i += kWave) {
-    const uint32_t h = own.hi[o0 + i];
-    if (h == kInf32) continue;
-    const int pos = lower_bound_u32(mk, na, h);
-    if (pos < na) atomicAdd(reinterpret_cast<unsigned long long *>(&fd[pos]), (unsigned long long)own.b[o0 + i]);
-  }
-  for (int j = lane; j < n4; j += kWave) {
-    const int pos = lower_bound_u32(mk, na, cp.hi[c0 + j]);
-    if (pos < na) atomicAdd(reinterpret_cast<unsigned long long *>(&fd[pos]), (unsigned long long)cp.b[c0 + j]);
+  for (int base = lane; base < na; base += 4 * kWave) {
+    uint32_t x[4];
+    int r[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j] = base + j * kWave < na ? (uint32_t)(sp[base + j * kWave] >> 32) : kInf32;
+    search4<false>(mk, na, x, r);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = base + j * kWave;
+      if (i < na && x[j] != kInf32 && r[j] < na)
+        atomicAdd(reinterpret_cast<unsigned long long *>(&fd[r[j]]),
+                  (unsigned long long)(sp[i] & 0xFFFFFFFFu));
+    }
   }
   __syncthreads();
-  int64_t freed = 0, best = 0;
-  for (int base = 0; base < na; base += kWave) {
-    const int i = base + lane;
-    int64_t x = i < na ? (int64_t)fd[i] : 0;
-    x = wave_incl_scan64(x, lane) + freed;
-    int64_t live = i < na ? mb[i] - x : 0;
-    for (int o = kWave / 2; o >= 1; o >>= 1) live = imax64(live, __shfl_xor(live, o, kWave));
-    best = imax64(best, live);
-    freed = __shfl(x, kWave - 1, kWave);
-  }
+  const int64_t best = max_live(mb, fd, na, lane);
   __syncthreads();
   return best;
 }
 
-__global__ __launch_bounds__(kWave) void fast_memory(const GmgView G, const uint8_t *__restrict__ P, int64_t nb,
-                                                     const uint32_t *__restrict__ fin,
-                                                     const uint16_t *__restrict__ rank,
-                                                     const uint16_t *__restrict__ dcnt, Records own_all,
-                                                     Records cp_all, uint32_t *__restrict__ wk_all,
-                                                     int64_t *__restrict__ wb_all, int64_t slot_cap,
-                                                     int64_t *__restrict__ peak, uint8_t *__restrict__ violation) {
+__global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0, int64_t nj,
+                                                    const Rec *__restrict__ own_all, const Rec *__restrict__ cp_all,
+                                                    const int32_t *__restrict__ meta, uint32_t *__restrict__ wk_all,
+                                                    uint64_t *__restrict__ wb_all, int32_t *__restrict__ wc_all,
+                                                    int64_t slot_cap, int64_t *__restrict__ peak,
+                                                    uint8_t *__restrict__ violation) {
   __shared__ uint32_t s_sk[kCap], s_mk[kCap];
-  __shared__ int64_t s_sb[kCap], s_mb[kCap];
-  __shared__ uint64_t s_fd[kCap];
-  __shared__ int own_off[257], cp_off[257], cfill[256];
-  const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[N];
+  __shared__ uint64_t s_sp[kCap], s_fd[kCap];
+  __shared__ int64_t s_mb[kCap];
+  __shared__ int s_gc[kCap + 2];
+  const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops];
   const int lane = threadIdx.x;
-  const Records own{own_all.lo + (int64_t)blockIdx.x * N, own_all.hi + (int64_t)blockIdx.x * N,
-                    own_all.b + (int64_t)blockIdx.x * N};
-  const Records cp{cp_all.lo + (int64_t)blockIdx.x * E, cp_all.hi + (int64_t)blockIdx.x * E,
-                   cp_all.b + (int64_t)blockIdx.x * E};
   uint32_t *g_sk = wk_all + (int64_t)blockIdx.x * 2 * slot_cap;
   uint32_t *g_mk = g_sk + slot_cap;
-  int64_t *g_sb = wb_all + (int64_t)blockIdx.x * 3 * slot_cap;
-  int64_t *g_mb = g_sb + slot_cap;
-  uint64_t *g_fd = reinterpret_cast<uint64_t *>(g_mb + slot_cap);
-
-  for (int64_t c = blockIdx.x; c < nb; c += gridDim.x) {
+  uint64_t *g_sp = wb_all + (int64_t)blockIdx.x * 3 * slot_cap;
+  int64_t *g_mb = reinterpret_cast<int64_t *>(g_sp + slot_cap);
+  uint64_t *g_fd = g_sp + 2 * slot_cap;
+  int32_t *g_gc = wc_all + (int64_t)blockIdx.x * (slot_cap + 2);
+  for (int64_t j = blockIdx.x; j < nj; j += gridDim.x) {
+    const int64_t c = j0 + j;
     if (violation[c] & SS_VIOLATION_INVALID) {
       if (peak)
         for (int d = lane; d < D; d += kWave) peak[c * D + d] = 0;
       continue;
     }
-    const uint8_t *prow = P + c * N;
-    const uint32_t *frow = fin + c * N;
-    const uint16_t *rrow = rank + c * N;
-    // own buckets from the per-device op counts; copy buckets counted here
-    if (lane == 0) {
-      int s = 0;
-      for (int d = 0; d < D; ++d) {
-        own_off[d] = s;
-        s += dcnt[c * D + d];
-      }
-      own_off[D] = s;
-    }
-    for (int d = lane; d < D; d += kWave) cfill[d] = 0;
-    __syncthreads();
-    for (int v = lane; v < N; v += kWave) op_intervals<false>(G, prow, frow, rrow, v, own_off, cfill, own, cp);
-    __syncthreads();
-    if (lane == 0) {
-      int s = 0;
-      for (int d = 0; d < D; ++d) {
-        cp_off[d] = s;
-        s += cfill[d];
-        cfill[d] = cp_off[d];
-      }
-      cp_off[D] = s;
-    }
-    __syncthreads();
-    for (int v = lane; v < N; v += kWave) op_intervals<true>(G, prow, frow, rrow, v, own_off, cfill, own, cp);
-    __syncthreads();
-
+    const Rec *own = own_all + j * N;
+    const Rec *cp = cp_all + j * E;
+    const int32_t *m = meta + j * meta_stride(D);
     uint8_t viol = 0;
     for (int e = 0; e < D; ++e) {
-      const int o0 = own_off[e], n1 = own_off[e + 1] - o0;
-      const int c0 = cp_off[e], n4 = cp_off[e + 1] - c0;
+      const int o0 = m[e], n1 = m[e + 1] - o0;
+      const int c0 = m[D + 1 + e], n4 = m[2 * (D + 1) + e];
       int64_t pk = 0;
       if (n1 + n4 > 0) {
-        if (n1 + n4 <= kCap)
-          pk = device_peak(own, o0, n1, cp, c0, n4, s_sk, s_sb, s_mk, s_mb, s_fd, lane);
+        if (n1 + n4 <= kCap && n1 + 2 <= kCap + 2)
+          pk = device_peak(own, o0, n1, cp, c0, n4, s_sk, s_sp, s_gc, s_mk, s_mb, s_fd, lane);
         else
-          pk = device_peak(own, o0, n1, cp, c0, n4, g_sk, g_sb, g_mk, g_mb, g_fd, lane);
+          pk = device_peak(own, o0, n1, cp, c0, n4, g_sk, g_sp, g_gc, g_mk, g_mb, g_fd, lane);
       }
       if (peak && lane == 0) peak[c * D + e] = pk;
       if (pk > G.cap[e]) viol = SS_VIOLATION_MEMORY;
     }
     if (lane == 0) violation[c] = viol;
-    __syncthreads();
   }
 }
 
@@ -411,7 +631,7 @@ int hip_fail(hipError_t err, const char *what) {
 }  // namespace
 
 size_t ss_fast_schedule_lds(const ss_gmg *g) {
-  return (size_t)g->n_dev * kWave * (4 + 2 + 2) + (size_t)g->n_req * kWave * 4;
+  return (size_t)g->n_dev * kWave * (4 + 2 + 2) + (size_t)g->n_req * kWave * 4 + (size_t)(g->n_dev + 1) * 8;
 }
 
 int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
@@ -426,24 +646,35 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
                             (int)sched_lds);
   if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
 
-  const int64_t per_cand = N * (4 + 2) + D * 2;
+  // chunk: op-major placements, finish times and ranks, their row-major
+  // copies, per-device op counts
+  const int64_t per_cand = N * (1 + 4 + 2 + 4 + 2) + D * 2;
   int64_t chunk = kScratchBudget / std::max<int64_t>(1, per_cand);
   chunk = std::max<int64_t>(kWave, chunk / kWave * kWave);
+  chunk = std::min<int64_t>(chunk, int64_t(65535) * 64);  // transpose grids index 64-candidate tiles in y
   chunk = std::min<int64_t>(chunk, B);
-  const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kMemBlocksPerCU, chunk));
+  // sub-chunk: interval records of each candidate (own N, copies <= E)
+  const int64_t rec_per_cand = (N + E) * (int64_t)sizeof(uint3) + 3 * (D + 1) * 4;
+  int64_t sub = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
+  sub = std::min<int64_t>(sub, chunk);
+  const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
   const int64_t slot_cap = N + E + 1;  // most allocations one device can hold
 
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
+  const size_t sz_pt = align((size_t)chunk * N + 1);
   const size_t sz_fin = align((size_t)chunk * N * 4 + 4);
   const size_t sz_rank = align((size_t)chunk * N * 2 + 2);
   const size_t sz_cnt = align((size_t)chunk * D * 2 + 2);
-  const size_t n_own = (size_t)nslots * N + 1, n_cp = (size_t)nslots * E + 1;
-  const size_t sz_own = align(n_own * 4) * 2 + align(n_own * 8);
-  const size_t sz_cp = align(n_cp * 4) * 2 + align(n_cp * 8);
+  const size_t sz_own = align(((size_t)sub * N + 1) * sizeof(uint3));
+  const size_t sz_cp = align(((size_t)sub * E + 1) * sizeof(uint3));
+  const size_t sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
   const size_t sz_wk = align((size_t)nslots * 2 * slot_cap * 4);
   const size_t sz_wb = align((size_t)nslots * 3 * slot_cap * 8);
+  const size_t sz_wc = align((size_t)nslots * (slot_cap + 2) * 4);
   void *scratch = nullptr;
-  err = hipMallocAsync(&scratch, sz_fin + sz_rank + sz_cnt + sz_own + sz_cp + sz_wk + sz_wb, stream);
+  err = hipMallocAsync(&scratch,
+                       sz_pt + 2 * sz_fin + 2 * sz_rank + sz_cnt + sz_own + sz_cp + sz_meta + sz_wk + sz_wb + sz_wc,
+                       stream);
   if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
   auto take = [&](size_t bytes) {
@@ -451,39 +682,67 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
     p += bytes;
     return q;
   };
+  auto *PT = reinterpret_cast<uint8_t *>(take(sz_pt));
+  auto *finT = reinterpret_cast<uint32_t *>(take(sz_fin));
+  auto *rankT = reinterpret_cast<uint16_t *>(take(sz_rank));
   auto *fin = reinterpret_cast<uint32_t *>(take(sz_fin));
   auto *rank = reinterpret_cast<uint16_t *>(take(sz_rank));
-  auto *dcnt = reinterpret_cast<uint16_t *>(take(sz_cnt));
-  Records own{reinterpret_cast<uint32_t *>(take(align(n_own * 4))), reinterpret_cast<uint32_t *>(take(align(n_own * 4))),
-              reinterpret_cast<int64_t *>(take(align(n_own * 8)))};
-  Records cp{reinterpret_cast<uint32_t *>(take(align(n_cp * 4))), reinterpret_cast<uint32_t *>(take(align(n_cp * 4))),
-             reinterpret_cast<int64_t *>(take(align(n_cp * 8)))};
+  auto *dcntT = reinterpret_cast<uint16_t *>(take(sz_cnt));
+  auto *own = reinterpret_cast<Rec *>(take(sz_own));
+  auto *cp = reinterpret_cast<Rec *>(take(sz_cp));
+  auto *meta = reinterpret_cast<int32_t *>(take(sz_meta));
   auto *wk = reinterpret_cast<uint32_t *>(take(sz_wk));
-  auto *wb = reinterpret_cast<int64_t *>(take(sz_wb));
+  auto *wb = reinterpret_cast<uint64_t *>(take(sz_wb));
+  auto *wc = reinterpret_cast<int32_t *>(take(sz_wc));
 
   int rc = SS_OK;
+  auto check = [&](const char *what) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess && rc == SS_OK) rc = hip_fail(e, what);
+    return rc == SS_OK;
+  };
   for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
     const int64_t nb = std::min(chunk, B - b0);
     const uint8_t *Pc = P + b0 * N;
-    SsTimingRec *t_sched = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
+    SsTimingRec *tt = ss_timing_start(SS_KERNEL_TRANSPOSE, stream);
+    if (N > 0)  // candidates' rows -> op-major
+      hipLaunchKernelGGL(transpose_tiles<uint8_t>, dim3((unsigned)((N + 63) / 64), (unsigned)((nb + 63) / 64)),
+                         dim3(256), 0, stream, Pc, nb, N, PT);
+    ss_timing_stop(tt, stream);
+    if (!check("transpose launch")) break;
+    SsTimingRec *ts = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
     hipLaunchKernelGGL(fast_schedule, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), sched_lds, stream, G,
-                       Pc, nb, fin, rank, dcnt, makespan + b0, sumfin ? sumfin + b0 : nullptr,
-                       slack ? slack + b0 * R : nullptr, violation + b0);
-    err = hipGetLastError();
-    ss_timing_stop(t_sched, stream);
-    if (err != hipSuccess) {
-      rc = hip_fail(err, "fast_schedule launch");
-      break;
+                       static_cast<const uint8_t *>(PT), nb, finT, rankT, dcntT, makespan + b0,
+                       sumfin ? sumfin + b0 : nullptr, slack ? slack + b0 * R : nullptr, violation + b0);
+    ss_timing_stop(ts, stream);
+    if (!check("fast_schedule launch")) break;
+    tt = ss_timing_start(SS_KERNEL_TRANSPOSE, stream);
+    if (N > 0) {  // op-major -> candidates' rows for the memory passes
+      const dim3 tg((unsigned)((nb + 63) / 64), (unsigned)((N + 63) / 64));
+      hipLaunchKernelGGL(transpose_tiles<uint32_t>, tg, dim3(256), 0, stream, static_cast<const uint32_t *>(finT),
+                         (int64_t)N, nb, fin);
+      hipLaunchKernelGGL(transpose_tiles<uint16_t>, tg, dim3(256), 0, stream, static_cast<const uint16_t *>(rankT),
+                         (int64_t)N, nb, rank);
     }
-    const int64_t grid = std::min<int64_t>(nb, nslots);
-    SsTimingRec *t_mem = ss_timing_start(SS_KERNEL_MEMORY, stream);
-    hipLaunchKernelGGL(fast_memory, dim3((unsigned)grid), dim3(kWave), 0, stream, G, Pc, nb,
-                       static_cast<const uint32_t *>(fin), static_cast<const uint16_t *>(rank),
-                       static_cast<const uint16_t *>(dcnt), own, cp, wk, wb, slot_cap,
-                       peak ? peak + b0 * D : nullptr, violation + b0);
-    err = hipGetLastError();
-    ss_timing_stop(t_mem, stream);
-    if (err != hipSuccess) rc = hip_fail(err, "fast_memory launch");
+    ss_timing_stop(tt, stream);
+    if (!check("transpose launch")) break;
+    for (int64_t j0 = 0; j0 < nb && rc == SS_OK; j0 += sub) {
+      const int64_t nj = std::min(sub, nb - j0);
+      SsTimingRec *ti = ss_timing_start(SS_KERNEL_INTERVALS, stream);
+      hipLaunchKernelGGL(fast_intervals, dim3((unsigned)nj), dim3(kWave), 0, stream, G, Pc,
+                         static_cast<const uint32_t *>(fin), static_cast<const uint16_t *>(rank),
+                         static_cast<const uint16_t *>(dcntT), nb, j0, own, cp, meta,
+                         static_cast<const uint8_t *>(violation + b0));
+      ss_timing_stop(ti, stream);
+      if (!check("fast_intervals launch")) break;
+      SsTimingRec *tm = ss_timing_start(SS_KERNEL_MEMORY, stream);
+      hipLaunchKernelGGL(fast_peaks, dim3((unsigned)std::min<int64_t>(nj, nslots)), dim3(kWave), 0, stream, G, j0, nj,
+                         static_cast<const Rec *>(own), static_cast<const Rec *>(cp),
+                         static_cast<const int32_t *>(meta), wk, wb, wc, slot_cap, peak ? peak + b0 * D : nullptr,
+                         violation + b0);
+      ss_timing_stop(tm, stream);
+      if (!check("fast_peaks launch")) break;
+    }
   }
   err = hipFreeAsync(scratch, stream);
   if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");

@@ -23,8 +23,8 @@ struct GmgView {
   const uint8_t *link_class;  // [D][D]
   // 32-bit copies of every time quantity, present when the loader proved the
   // whole time horizon (all starts, finishes, frees and finite slice bounds)
-  // stays below 2^32 - 1 and there are at most 65535 ops; the open slice end
-  // becomes 0xFFFFFFFF.
+  // stays below 2^32 - 1, there are at most 65535 ops and every output size
+  // fits in 32 bits; the open slice end becomes 0xFFFFFFFF.
   int32_t time32;
   const uint32_t *dur32, *xfer32, *slice_begin32, *slice_end32, *release32;
 };

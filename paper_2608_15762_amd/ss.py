@@ -24,8 +24,8 @@ SS_VIOLATION_INVALID = 0x4
 SS_SELECT_REQUIRE_SLA = 0x1
 EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "ss_select_best", "ss_kernel_timing",
             "ss_kernel_time", "ss_last_error")
-SS_KERNEL_SCHEDULE, SS_KERNEL_MEMORY, SS_KERNEL_SELECT = 0, 1, 2
-KERNEL_NAMES = {0: "schedule_kernel", 1: "memory_kernel", 2: "select"}
+SS_KERNEL_SCHEDULE, SS_KERNEL_MEMORY, SS_KERNEL_SELECT, SS_KERNEL_INTERVALS, SS_KERNEL_TRANSPOSE = 0, 1, 2, 3, 4
+KERNEL_NAMES = {0: "schedule_kernel", 1: "memory_kernel", 2: "select", 3: "intervals_kernel", 4: "transpose"}
 
 _lib = None
 _lock = threading.Lock()

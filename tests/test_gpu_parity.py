@@ -127,6 +127,21 @@ def test_crowded_device_uses_global_sort_buffer(dev, path):
     assert_same(got, ref, label="crowded")
 
 
+def test_fan_in_many_copies_in_one_gap(dev, path):
+    """One op consuming 40 remote outputs: all 40 copies land on its device
+    before its own allocation (exercises the sorted-gap fallback)."""
+    n = 41
+    st = synth.Stream(77)
+    edges = [(u, n - 1) for u in range(n - 1)]
+    g = make_gmg(4, ["op"] * n, edges, [0] * n, [[st.uniform_int(1, 30)] for _ in range(n)],
+                 [st.uniform_int(1, 500) for _ in range(n)], [[(0, TIME_INF)]] * 4, [10 ** 6] * 4, [0], [10 ** 5],
+                 bw=[3], lat=[2])
+    P = np.array([[1 + st.uniform_int(0, 2) for _ in range(n - 1)] + [0] for _ in range(64)], np.uint8)
+    P[1::2, : n - 1] = np.array([[st.uniform_int(0, 3) for _ in range(n - 1)] for _ in range(32)], np.uint8)
+    ref = oracle.simulate_batch(g, P)
+    assert_same(gpu_run(ss.Gmg(g), P, dev), ref, label="fan-in")
+
+
 def test_horizon_beyond_32_bits_takes_general_path(dev, monkeypatch):
     """Slices far beyond 2^32 us: the fast path must be refused and the general
     path must still match the oracle."""
