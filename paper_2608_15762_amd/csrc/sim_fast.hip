@@ -2,26 +2,28 @@
 // proved that every simulated time fits in 32 bits and N <= 65535.
 //
 // Per chunk of candidates:
-//   transpose     candidates' placement rows -> op-major [op][candidate]
 //   fast_schedule one lane per candidate, ops in index order (Sec. 3.3.2-3.3.3).
 //                 Per (device, lane) LDS state laid out [device][lane], so a
 //                 wave's 64 lanes fall in distinct banks whatever device each
 //                 touches: effective clock u32 (= max(last finish, current
-//                 slice start)), slice cursor u16, op count u16.  An op first
-//                 tries the current slice; only when it does not fit does the
-//                 lane walk forward through later slices.  While op v is
-//                 placed, the next op's device, predecessor values and slice
-//                 end are already being fetched.  Writes op-major finish times
-//                 and per-device ranks, and per-device op counts.
-//   transpose     finish times and ranks back to candidate rows
+//                 slice start)) and slice cursor u16.  An op first tries the
+//                 current slice; only when it does not fit does the lane walk
+//                 forward through later slices.  While op v is placed, the
+//                 next op's device, predecessor values and slice end are
+//                 already being fetched.  The lane reads its placement row in
+//                 16-op blocks; finish times are written op-major.
+//   transpose     finish times back to candidate rows
 // then per sub-chunk of candidates:
 //   fast_intervals one wave per candidate, lanes = consecutive ops (coalesced
 //                 row reads), almost no LDS so many waves hide the gathers.
-//                 Writes every residency interval (Sec. 3.3.2) into a
-//                 per-device bucket: own outputs at their rank (so a device's
-//                 own intervals are start-sorted), one copy per (output,
-//                 remote device) in a region bounded by the device's summed
-//                 in-degree.
+//                 A 64-key sort across the wave groups each chunk of ops by
+//                 device, giving every op its rank among the ops of its device
+//                 (and per-device counts and in-degree sums) without
+//                 same-address atomics.  Writes every residency interval
+//                 (Sec. 3.3.2) into a per-device bucket: own outputs at their
+//                 rank (so a device's own intervals are start-sorted), one copy
+//                 per (output, remote device) in a region bounded by the
+//                 device's summed in-degree.
 //   fast_peaks    one wave per candidate.  Per device: sort only the copy
 //                 allocations (LDS bitonic), merge them with the sorted own
 //                 allocations by binary-search ranks, scatter every free onto
@@ -76,11 +78,13 @@ __device__ __forceinline__ uint32_t xfer_of(const GmgView &G, int u, int du, int
   return G.xfer32[u * K + k];
 }
 
-// Operands are op-major ([op][candidate]): at every op the 64 lanes of a wave
-// read and write one contiguous 64-element segment.
-__global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const uint8_t *__restrict__ PT, int64_t nb,
-                                                       uint32_t *__restrict__ finT, uint16_t *__restrict__ rankT,
-                                                       uint16_t *__restrict__ dcntT, int64_t *__restrict__ makespan,
+// The lane streams its candidate's placement row (row-major, as the caller
+// passes it) in 16-op blocks, one block ahead; finish times are op-major
+// ([op][candidate]) so every per-op finish-time load or store of a wave is one
+// contiguous 64-element segment.
+template <bool kVec16>
+__global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const uint8_t *__restrict__ P, int64_t nb,
+                                                       uint32_t *__restrict__ finT, int64_t *__restrict__ makespan,
                                                        int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
                                                        uint8_t *__restrict__ violation) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
@@ -91,7 +95,6 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   int32_t *sbase = reinterpret_cast<int32_t *>(comp + (size_t)R * kWave);  // [D+1] slice ranges of the devices
   int32_t *dcls = sbase + D + 1;                                          // [D] device class
   uint16_t *cur = reinterpret_cast<uint16_t *>(dcls + D);                 // [D][64]
-  uint16_t *cnt = cur + (size_t)D * kWave;                                // [D][64]
   for (int d = lane; d <= D; d += kWave) {
     sbase[d] = G.slice_ptr[d];
     if (d < D) dcls[d] = G.dev_class[d];
@@ -99,12 +102,24 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   __syncthreads();
   const int64_t c = (int64_t)blockIdx.x * kWave + lane;
   if (c >= nb) return;
+  const uint8_t *prow = P + c * N;
   for (int d = 0; d < D; ++d) {
     clk[d * kWave + lane] = G.slice_begin32[sbase[d]];
     cur[d * kWave + lane] = 0;
-    cnt[d * kWave + lane] = 0;
   }
   for (int r = 0; r < R; ++r) comp[r * kWave + lane] = G.release32[r];
+
+  // placement stream
+  uint4 blk = make_uint4(0, 0, 0, 0), nxt = make_uint4(0, 0, 0, 0);
+  if (kVec16) {
+    if (N > 0) blk = *reinterpret_cast<const uint4 *>(prow);
+    if (N > 16) nxt = *reinterpret_cast<const uint4 *>(prow + 16);
+  }
+  auto dev_of = [&](int v) -> int {  // device of op v (v in the current block)
+    const int q = (v >> 2) & 3;
+    const uint32_t w = q == 0 ? blk.x : q == 1 ? blk.y : q == 2 ? blk.z : blk.w;
+    return (int)((w >> (8 * (v & 3))) & 0xFFu);
+  };
 
   bool invalid = false;
   uint32_t ms = 0;
@@ -112,7 +127,7 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   int d = 0;
   uint32_t E = 0;  // end of the current slice of op v's device
   if (N > 0) {
-    d = PT[c];
+    d = kVec16 ? dev_of(0) : prow[0];
     if (d >= D) {
       invalid = true;
       d = 0;
@@ -129,7 +144,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   uint32_t f_prev = 0;
   int d_prev = 0;
   for (int v = 0; v < N; ++v) {
-    const int dn_raw = (v + 1 < N) ? PT[(int64_t)(v + 1) * nb + c] : 0;
+    int dn_raw = 0;
+    if (!kVec16 && v + 1 < N) dn_raw = prow[v + 1];  // in flight while op v is placed
     const uint32_t w = (C == 1) ? G.dur32[v] : G.dur32[v * C + dcls[d]];
     const int r = G.op_req[v];
     // ready: release, and every predecessor's finish plus its transfer
@@ -155,7 +171,7 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
         du = d_prev;
       } else {
         t = finT[(int64_t)u * nb + c];
-        du = PT[(int64_t)u * nb + c];
+        du = prow[u];
         if (du >= D) du = 0;
       }
       if (du != d) t += xfer_of(G, u, du, d);
@@ -181,10 +197,7 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     }
     const uint32_t f = s + w;
     clk[slot] = f;
-    const uint16_t rk = cnt[slot];
-    cnt[slot] = rk + 1;
     finT[(int64_t)v * nb + c] = f;
-    rankT[(int64_t)v * nb + c] = rk;
     ms = umax32(ms, f);
     sum += f;
     uint32_t *cr = comp + r * kWave + lane;
@@ -199,10 +212,17 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
           const int u = G.pred_idx[q0 + i];
           if (u != v) {
             pf[i] = finT[(int64_t)u * nb + c];
-            const int du = PT[(int64_t)u * nb + c];
+            const int du = prow[u];
             pd[i] = du >= D ? 0 : du;
           }
         }
+      }
+      if (kVec16) {
+        if (((v + 1) & 15) == 0) {  // next block becomes current; fetch the one after
+          blk = nxt;
+          if (v + 17 < N) nxt = *reinterpret_cast<const uint4 *>(prow + v + 17);
+        }
+        dn_raw = dev_of(v + 1);
       }
       d = dn_raw;
       if (d >= D) {
@@ -212,7 +232,6 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
       E = G.slice_end32[sbase[d] + cur[d * kWave + lane]];
     }
   }
-  for (int dd = 0; dd < D; ++dd) dcntT[(int64_t)dd * nb + c] = cnt[dd * kWave + lane];
   if (invalid) {
     makespan[c] = INT64_MAX;
     if (sumfin) sumfin[c] = INT64_MAX;
@@ -232,10 +251,10 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
 // An interval record: {allocation time, free time (kInf32 = never), bytes}.
 using Rec = uint3;
 
-// Intervals of op v: its own output at its rank in its device's bucket, and
-// one copy per remote destination device (slot taken with an LDS atomic).
-__device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32_t *frow, const uint16_t *rrow, int v,
-                             const int *own_off, int *cfill, Rec *own, Rec *cp) {
+// Intervals of op v: its own output at slot own_pos of its device's bucket,
+// and one copy per remote destination device (slot taken with an LDS atomic).
+__device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32_t *frow, int v, int own_pos,
+                             int *cfill, Rec *own, Rec *cp) {
   const int C = G.n_class;
   const int d = prow[v];
   const uint32_t b = (uint32_t)G.out_bytes[v];
@@ -250,7 +269,7 @@ __device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32
       F = umax32(F, (dx == d) ? frow[x] : f + xfer_of(G, v, d, dx));
     }
   }
-  own[own_off[d] + rrow[v]] = Rec{f - G.dur32[v * C + G.dev_class[d]], F, b};
+  own[own_pos] = Rec{f - G.dur32[v * C + G.dev_class[d]], F, b};
   if (b == 0) return;
   for (int q = x0; q < x1; ++q) {
     const int e = prow[G.succ_idx[q]];
@@ -268,36 +287,90 @@ __device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32
   }
 }
 
+// Ascending sort of the 64 lanes' keys: bitonic network over lane shuffles.
+__device__ __forceinline__ uint32_t wave_sort64(uint32_t key, int lane) {
+#pragma unroll
+  for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const uint32_t other = __shfl_xor(key, j, kWave);
+      const bool asc = (lane & k) == 0, low = (lane & j) == 0;
+      key = (asc == low) ? min(key, other) : max(key, other);
+    }
+  }
+  return key;
+}
+
+// Groups a chunk of 64 ops by device.  For the op of this lane (device d,
+// active = it exists): rank = how many ops of the chunk with lower index are
+// on the same device.  Lanes that end a device's group in sorted order get
+// that device (grp_dev, else -1), the group size and the group's sum of val.
+__device__ __forceinline__ void chunk_groups(int d, bool active, int val, int lane, int &rank, int &grp_dev,
+                                             int &grp_cnt, int &grp_sum) {
+  const uint32_t key = ((active ? (uint32_t)d : 0x3FFu) << 6) | (uint32_t)lane;
+  const uint32_t sk = wave_sort64(key, lane);
+  const int sd = (int)(sk >> 6), src = (int)(sk & 63u);
+  const int sval = __shfl(val, src, kWave);
+  const int prev = __shfl_up(sd, 1, kWave), next = __shfl_down(sd, 1, kWave);
+  int start = (lane == 0 || prev != sd) ? lane : 0;
+  int sum = sval;
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(start, o, kWave);
+    if (lane >= o) start = max(start, y);
+  }
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int y = __shfl_up(sum, o, kWave);
+    if (lane - o >= start) sum += y;
+  }
+  const bool tail = lane == kWave - 1 || next != sd;
+  grp_dev = (tail && sd != 0x3FF) ? sd : -1;
+  grp_cnt = lane - start + 1;
+  grp_sum = sum;
+  rank = __builtin_amdgcn_ds_permute(src << 2, lane - start);
+}
+
 // Per-candidate bucket geometry written by fast_intervals, read by fast_peaks.
 __device__ __forceinline__ int meta_stride(int D) { return 3 * (D + 1); }
 
 __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const uint8_t *__restrict__ P,
-                                                        const uint32_t *__restrict__ fin,
-                                                        const uint16_t *__restrict__ rank,
-                                                        const uint16_t *__restrict__ dcntT, int64_t nb, int64_t j0,
+                                                        const uint32_t *__restrict__ fin, int64_t j0,
                                                         Rec *__restrict__ own_all, Rec *__restrict__ cp_all,
                                                         int32_t *__restrict__ meta,
                                                         const uint8_t *__restrict__ violation) {
-  __shared__ int own_off[257], cp_off[257], cfill[256];
+  __shared__ int own_off[257], cp_off[257], cfill[256], ocnt[256], base[256];
   const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops];
   const int lane = threadIdx.x;
   const int64_t j = blockIdx.x, c = j0 + j;
   if (violation[c] & SS_VIOLATION_INVALID) return;
   const uint8_t *prow = P + c * N;
   const uint32_t *frow = fin + c * N;
-  const uint16_t *rrow = rank + c * N;
   Rec *own = own_all + j * N;
   Rec *cp = cp_all + j * E;
-  // copies landing on a device <= summed in-degree of its ops: bucket bound
-  for (int d = lane; d < D; d += kWave) cfill[d] = 0;
+  for (int d = lane; d < D; d += kWave) {
+    cfill[d] = 0;
+    ocnt[d] = 0;
+    base[d] = 0;
+  }
   __syncthreads();
-  for (int v = lane; v < N; v += kWave) atomicAdd(&cfill[prow[v]], G.pred_ptr[v + 1] - G.pred_ptr[v]);
-  __syncthreads();
+  // ops per device, and summed in-degree (copies landing on a device <= it)
+  for (int v0 = 0; v0 < N; v0 += kWave) {
+    const int v = v0 + lane;
+    const bool act = v < N;
+    const int d = act ? prow[v] : 0;
+    const int indeg = act ? G.pred_ptr[v + 1] - G.pred_ptr[v] : 0;
+    int rank, gd, gcnt, gsum;
+    chunk_groups(d, act, indeg, lane, rank, gd, gcnt, gsum);
+    if (gd >= 0) {
+      ocnt[gd] += gcnt;
+      cfill[gd] += gsum;
+    }
+    __syncthreads();
+  }
   if (lane == 0) {
     int so = 0, sc = 0;
     for (int d = 0; d < D; ++d) {
       own_off[d] = so;
-      so += dcntT[(int64_t)d * nb + c];
+      so += ocnt[d];
       cp_off[d] = sc;
       sc += cfill[d];
       cfill[d] = cp_off[d];
@@ -306,8 +379,18 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
     cp_off[D] = sc;
   }
   __syncthreads();
-  for (int v = lane; v < N; v += kWave) op_intervals(G, prow, frow, rrow, v, own_off, cfill, own, cp);
-  __syncthreads();
+  for (int v0 = 0; v0 < N; v0 += kWave) {
+    const int v = v0 + lane;
+    const bool act = v < N;
+    const int d = act ? prow[v] : 0;
+    int rank, gd, gcnt, gsum;
+    chunk_groups(d, act, 0, lane, rank, gd, gcnt, gsum);
+    const int pos = act ? own_off[d] + base[d] + rank : 0;
+    __syncthreads();
+    if (gd >= 0) base[gd] += gcnt;
+    if (act) op_intervals(G, prow, frow, v, pos, cfill, own, cp);
+    __syncthreads();
+  }
   int32_t *m = meta + j * meta_stride(D);
   for (int d = lane; d <= D; d += kWave) {
     m[d] = own_off[d];
@@ -631,7 +714,7 @@ int hip_fail(hipError_t err, const char *what) {
 }  // namespace
 
 size_t ss_fast_schedule_lds(const ss_gmg *g) {
-  return (size_t)g->n_dev * kWave * (4 + 2 + 2) + (size_t)g->n_req * kWave * 4 + (size_t)(g->n_dev + 1) * 8;
+  return (size_t)g->n_dev * kWave * (4 + 2) + (size_t)g->n_req * kWave * 4 + (size_t)(g->n_dev + 1) * 8;
 }
 
 int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
@@ -642,13 +725,15 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   int cus = 0;
   hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
-  err = hipFuncSetAttribute(reinterpret_cast<const void *>(&fast_schedule), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)sched_lds);
+  // 16-byte placement blocks need every row (and so the batch) 16-byte aligned
+  const bool vec16 = N % 16 == 0 && (reinterpret_cast<uintptr_t>(P) & 15) == 0;
+  err = hipFuncSetAttribute(vec16 ? reinterpret_cast<const void *>(&fast_schedule<true>)
+                                  : reinterpret_cast<const void *>(&fast_schedule<false>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
   if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
 
-  // chunk: op-major placements, finish times and ranks, their row-major
-  // copies, per-device op counts
-  const int64_t per_cand = N * (1 + 4 + 2 + 4 + 2) + D * 2;
+  // chunk: op-major and row-major finish times
+  const int64_t per_cand = N * (4 + 4);
   int64_t chunk = kScratchBudget / std::max<int64_t>(1, per_cand);
   chunk = std::max<int64_t>(kWave, chunk / kWave * kWave);
   chunk = std::min<int64_t>(chunk, int64_t(65535) * 64);  // transpose grids index 64-candidate tiles in y
@@ -661,10 +746,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   const int64_t slot_cap = N + E + 1;  // most allocations one device can hold
 
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
-  const size_t sz_pt = align((size_t)chunk * N + 1);
   const size_t sz_fin = align((size_t)chunk * N * 4 + 4);
-  const size_t sz_rank = align((size_t)chunk * N * 2 + 2);
-  const size_t sz_cnt = align((size_t)chunk * D * 2 + 2);
   const size_t sz_own = align(((size_t)sub * N + 1) * sizeof(uint3));
   const size_t sz_cp = align(((size_t)sub * E + 1) * sizeof(uint3));
   const size_t sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
@@ -673,7 +755,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   const size_t sz_wc = align((size_t)nslots * (slot_cap + 2) * 4);
   void *scratch = nullptr;
   err = hipMallocAsync(&scratch,
-                       sz_pt + 2 * sz_fin + 2 * sz_rank + sz_cnt + sz_own + sz_cp + sz_meta + sz_wk + sz_wb + sz_wc,
+                       2 * sz_fin + sz_own + sz_cp + sz_meta + sz_wk + sz_wb + sz_wc,
                        stream);
   if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
@@ -682,12 +764,8 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
     p += bytes;
     return q;
   };
-  auto *PT = reinterpret_cast<uint8_t *>(take(sz_pt));
   auto *finT = reinterpret_cast<uint32_t *>(take(sz_fin));
-  auto *rankT = reinterpret_cast<uint16_t *>(take(sz_rank));
   auto *fin = reinterpret_cast<uint32_t *>(take(sz_fin));
-  auto *rank = reinterpret_cast<uint16_t *>(take(sz_rank));
-  auto *dcntT = reinterpret_cast<uint16_t *>(take(sz_cnt));
   auto *own = reinterpret_cast<Rec *>(take(sz_own));
   auto *cp = reinterpret_cast<Rec *>(take(sz_cp));
   auto *meta = reinterpret_cast<int32_t *>(take(sz_meta));
@@ -704,25 +782,22 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
     const int64_t nb = std::min(chunk, B - b0);
     const uint8_t *Pc = P + b0 * N;
-    SsTimingRec *tt = ss_timing_start(SS_KERNEL_TRANSPOSE, stream);
-    if (N > 0)  // candidates' rows -> op-major
-      hipLaunchKernelGGL(transpose_tiles<uint8_t>, dim3((unsigned)((N + 63) / 64), (unsigned)((nb + 63) / 64)),
-                         dim3(256), 0, stream, Pc, nb, N, PT);
-    ss_timing_stop(tt, stream);
-    if (!check("transpose launch")) break;
     SsTimingRec *ts = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
-    hipLaunchKernelGGL(fast_schedule, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), sched_lds, stream, G,
-                       static_cast<const uint8_t *>(PT), nb, finT, rankT, dcntT, makespan + b0,
-                       sumfin ? sumfin + b0 : nullptr, slack ? slack + b0 * R : nullptr, violation + b0);
+    const dim3 sgrid((unsigned)((nb + kWave - 1) / kWave));
+    if (vec16)
+      hipLaunchKernelGGL(fast_schedule<true>, sgrid, dim3(kWave), sched_lds, stream, G, Pc, nb, finT, makespan + b0,
+                         sumfin ? sumfin + b0 : nullptr, slack ? slack + b0 * R : nullptr, violation + b0);
+    else
+      hipLaunchKernelGGL(fast_schedule<false>, sgrid, dim3(kWave), sched_lds, stream, G, Pc, nb, finT, makespan + b0,
+                         sumfin ? sumfin + b0 : nullptr, slack ? slack + b0 * R : nullptr, violation + b0);
     ss_timing_stop(ts, stream);
     if (!check("fast_schedule launch")) break;
+    SsTimingRec *tt = nullptr;
     tt = ss_timing_start(SS_KERNEL_TRANSPOSE, stream);
     if (N > 0) {  // op-major -> candidates' rows for the memory passes
       const dim3 tg((unsigned)((nb + 63) / 64), (unsigned)((N + 63) / 64));
       hipLaunchKernelGGL(transpose_tiles<uint32_t>, tg, dim3(256), 0, stream, static_cast<const uint32_t *>(finT),
                          (int64_t)N, nb, fin);
-      hipLaunchKernelGGL(transpose_tiles<uint16_t>, tg, dim3(256), 0, stream, static_cast<const uint16_t *>(rankT),
-                         (int64_t)N, nb, rank);
     }
     ss_timing_stop(tt, stream);
     if (!check("transpose launch")) break;
@@ -730,8 +805,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
       const int64_t nj = std::min(sub, nb - j0);
       SsTimingRec *ti = ss_timing_start(SS_KERNEL_INTERVALS, stream);
       hipLaunchKernelGGL(fast_intervals, dim3((unsigned)nj), dim3(kWave), 0, stream, G, Pc,
-                         static_cast<const uint32_t *>(fin), static_cast<const uint16_t *>(rank),
-                         static_cast<const uint16_t *>(dcntT), nb, j0, own, cp, meta,
+                         static_cast<const uint32_t *>(fin), j0, own, cp, meta,
                          static_cast<const uint8_t *>(violation + b0));
       ss_timing_stop(ti, stream);
       if (!check("fast_intervals launch")) break;
