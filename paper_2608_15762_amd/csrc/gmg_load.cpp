@@ -143,13 +143,31 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     int64_t max_bytes = 0;
     for (int64_t v = 0; v < N; ++v) max_bytes = std::max(max_bytes, d->out_bytes[v]);
     const bool time32 = horizon < (i128)UINT32_MAX && N <= 65535 && max_bytes <= (int64_t)UINT32_MAX;
-    std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32;
+    std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32, meta;
+    const int64_t meta_stride = std::max<int64_t>(128, (N + 63) / 64 * 64 + 64);  // two blocks of 64 past any op
     if (time32) {
+      meta.assign((size_t)kOpMetaFields * meta_stride, 0);
+      auto M = [&](int f, int64_t v) -> uint32_t & { return meta[(size_t)f * meta_stride + v]; };
+      for (int64_t v = 0; v < N; ++v) {
+        const int64_t e0 = d->pred_ptr[v], np = d->pred_ptr[v + 1] - e0;
+        M(kMetaDur, v) = C == 1 ? (uint32_t)d->dur[v] : 0u;
+        M(kMetaReq, v) = (uint32_t)d->op_req[v] | (uint32_t)std::min<int64_t>(np, 0xFFFF) << 16;
+        M(kMetaRel, v) = (uint32_t)d->release[d->op_req[v]];
+        uint32_t p[4] = {0xFFFFu, 0xFFFFu, 0xFFFFu, 0xFFFFu};
+        for (int64_t i = 0; i < std::min<int64_t>(np, 4); ++i) {
+          const int64_t u = d->pred_idx[e0 + i];
+          p[i] = (uint32_t)u;
+          for (int64_t k = 0; k < 2; ++k) M(kMetaX + 2 * (int)i + (int)k, v) = (uint32_t)xfer[u * K + std::min<int64_t>(k, K - 1)];
+        }
+        M(kMetaP01, v) = p[0] | p[1] << 16;
+        M(kMetaP23, v) = p[2] | p[3] << 16;
+        M(kMetaE0, v) = (uint32_t)e0;
+      }
       dur32.assign(d->dur, d->dur + N * C);
       xfer32.assign(xfer.begin(), xfer.end());
       rel32.assign(d->release, d->release + R);
-      sb32.resize(S);
-      se32.resize(S);
+      sb32.assign(S + 1, UINT32_MAX);  // spare entry: read ahead, never used
+      se32.assign(S + 1, UINT32_MAX);
       for (int64_t k = 0; k < S; ++k) {
         sb32[k] = (uint32_t)d->slice_begin[k];
         se32[k] = d->slice_end[k] == SS_TIME_INF ? UINT32_MAX : (uint32_t)d->slice_end[k];
@@ -175,7 +193,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     const size_t o_dl = pk.add(d->deadline, R * sizeof(int64_t));
     const size_t o_link = pk.add(d->link_class, D * D);
     const size_t o_dur32 = pk.add(dur32), o_xfer32 = pk.add(xfer32), o_sb32 = pk.add(sb32), o_se32 = pk.add(se32),
-                 o_rel32 = pk.add(rel32);
+                 o_rel32 = pk.add(rel32), o_meta = pk.add(meta);
     pk.add(nullptr, 256);  // tail padding
 
     ss_gmg *g = new ss_gmg();
@@ -221,6 +239,8 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     V.slice_begin32 = reinterpret_cast<const uint32_t *>(base + o_sb32);
     V.slice_end32 = reinterpret_cast<const uint32_t *>(base + o_se32);
     V.release32 = reinterpret_cast<const uint32_t *>(base + o_rel32);
+    V.op_meta = reinterpret_cast<const uint32_t *>(base + o_meta);
+    V.meta_stride = (int32_t)meta_stride;
     g->n_ops = N;
     g->n_edges = E;
     g->n_dev = D;
@@ -229,6 +249,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     g->n_req = R;
     g->max_slices = max_slices;
     g->horizon = (int64_t)horizon;
+    for (int64_t v = 0; v < N; ++v) g->max_indeg = std::max<int64_t>(g->max_indeg, d->pred_ptr[v + 1] - d->pred_ptr[v]);
     *out = g;
     return SS_OK;
   } catch (const std::bad_alloc &) {

@@ -2,6 +2,7 @@
 // proved that every simulated time fits in 32 bits and N <= 65535.
 //
 // Per chunk of candidates:
+//   transpose     candidates' placement rows -> op-major [op][candidate]
 //   fast_schedule one lane per candidate, ops in index order (Sec. 3.3.2-3.3.3).
 //                 Per (device, lane) LDS state laid out [device][lane], so a
 //                 wave's 64 lanes fall in distinct banks whatever device each
@@ -9,9 +10,9 @@
 //                 slice start)) and slice cursor u16.  An op first tries the
 //                 current slice; only when it does not fit does the lane walk
 //                 forward through later slices.  While op v is placed, the
-//                 next op's device, predecessor values and slice end are
-//                 already being fetched.  The lane reads its placement row in
-//                 16-op blocks; finish times are written op-major.
+//                 next ops' devices, predecessor values, link classes and
+//                 slice ends are already in flight (a four-stage software
+//                 pipeline).  Finish times are written op-major.
 //   transpose     finish times back to candidate rows
 // then per sub-chunk of candidates:
 //   fast_intervals one wave per candidate, lanes = consecutive ops (coalesced
@@ -78,17 +79,38 @@ __device__ __forceinline__ uint32_t xfer_of(const GmgView &G, int u, int du, int
   return G.xfer32[u * K + k];
 }
 
-// The lane streams its candidate's placement row (row-major, as the caller
-// passes it) in 16-op blocks, one block ahead; finish times are op-major
-// ([op][candidate]) so every per-op finish-time load or store of a wave is one
-// contiguous 64-element segment.
-template <bool kVec16>
-__global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const uint8_t *__restrict__ P, int64_t nb,
+// Software pipeline of the schedule, for target op T (one lane per candidate):
+//   T-4  load the op's device from the op-major placements;
+//   T-3  load finish time and device of its first kPipePre predecessors when
+//        they are op T-4 or older (op-major finish times written earlier by
+//        this lane); ops T-3..T-1 come from a three-deep register history;
+//   T-2  gather the link class of each predecessor transfer,
+//        the op's duration on its device, and the device's current slice end
+//        plus the next slice's bounds;
+//   T    ready time, placement, stores.
+// Uniform per-op fields come from op_meta, fetched 64 ops at a time (lane j
+// holds op 64b+j) and broadcast with readlane.  Stage state is indexed by
+// T mod 4, static in the four-way unrolled loop.  Loads are unconditional
+// (indices clamped, unused values discarded by selects) so the loop body has
+// no branch around a memory operation and the compiler can keep the loads of
+// later stages in flight while op T waits only for its own.
+constexpr int kPipePre = 2;  // predecessors handled by the pipeline; more go through the CSR
+
+struct SchedPipe {
+  uint32_t dq[4];                // device of the target op (raw byte)
+  uint32_t pf[4][kPipePre];      // predecessor finish times (raw loads)
+  uint32_t pd[4][kPipePre];      // predecessor devices (raw loads)
+  uint32_t lc[4][kPipePre];      // link class between predecessor and target device
+  uint32_t wq[4];                // duration on the target device
+  uint32_t cq[4], e0[4], b1[4], e1[4];  // slice cursor, its end, next slice's bounds
+};
+template <bool kGeneralLink, bool kOverflow>
+__global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const uint8_t *__restrict__ PT, int64_t nb,
                                                        uint32_t *__restrict__ finT, int64_t *__restrict__ makespan,
                                                        int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
                                                        uint8_t *__restrict__ violation) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
-  const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = G.n_class;
+  const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = G.n_class, K = G.n_link;
   const int lane = threadIdx.x;
   uint32_t *clk = reinterpret_cast<uint32_t *>(lds_raw);                  // [D][64]
   uint32_t *comp = clk + (size_t)D * kWave;                               // [R][64]
@@ -100,138 +122,222 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     if (d < D) dcls[d] = G.dev_class[d];
   }
   __syncthreads();
-  const int64_t c = (int64_t)blockIdx.x * kWave + lane;
-  if (c >= nb) return;
-  const uint8_t *prow = P + c * N;
+  // Every lane runs (readlane needs the field blocks loaded in all lanes); a
+  // lane past the batch end shadows the last candidate, computing and storing
+  // exactly what that candidate's lane stores.
+  const int64_t c_raw = (int64_t)blockIdx.x * kWave + lane;
+  const bool live = c_raw < nb;
+  const int64_t c = live ? c_raw : nb - 1;
   for (int d = 0; d < D; ++d) {
     clk[d * kWave + lane] = G.slice_begin32[sbase[d]];
     cur[d * kWave + lane] = 0;
   }
   for (int r = 0; r < R; ++r) comp[r * kWave + lane] = G.release32[r];
-
-  // placement stream
-  uint4 blk = make_uint4(0, 0, 0, 0), nxt = make_uint4(0, 0, 0, 0);
-  if (kVec16) {
-    if (N > 0) blk = *reinterpret_cast<const uint4 *>(prow);
-    if (N > 16) nxt = *reinterpret_cast<const uint4 *>(prow + 16);
+  if (N == 0) {
+    if (live) {
+      makespan[c] = 0;
+      if (sumfin) sumfin[c] = 0;
+      if (slack)
+        for (int rr = 0; rr < R; ++rr) slack[c * R + rr] = G.deadline[rr] - (int64_t)G.release32[rr];
+      violation[c] = 0;
+    }
+    return;
   }
-  auto dev_of = [&](int v) -> int {  // device of op v (v in the current block)
-    const int q = (v >> 2) & 3;
-    const uint32_t w = q == 0 ? blk.x : q == 1 ? blk.y : q == 2 ? blk.z : blk.w;
-    return (int)((w >> (8 * (v & 3))) & 0xFFu);
+
+  const int ms_ = G.meta_stride;
+  uint32_t mA[kOpMetaFields], mB[kOpMetaFields];  // fields of ops [blk0, blk0+64) and the next 64
+#pragma unroll
+  for (int f = 0; f < kOpMetaFields; ++f) {
+    mA[f] = G.op_meta[(int64_t)f * ms_ + lane];
+    mB[f] = G.op_meta[(int64_t)f * ms_ + kWave + lane];
+  }
+  int blk0 = 0;
+  // uniform field f of op t, t in [blk0, blk0 + 128)
+  auto meta = [&](int f, int t) -> uint32_t {
+    const int j = t - blk0;
+    const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)mA[f], j & (kWave - 1));
+    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)mB[f], j & (kWave - 1));
+    return j < kWave ? a : b;
   };
+  auto pred_of = [](uint32_t p01, int i) -> uint32_t { return i ? (p01 >> 16) : (p01 & 0xFFFFu); };
 
   bool invalid = false;
+  // A loaded value is left untouched until the stage that consumes it, so the
+  // wait for it lands there and not right after the load.
+  auto clampD = [&](uint32_t x) -> uint32_t { return x >= (uint32_t)D ? 0u : x; };
+  auto load_dev = [&](int t) -> uint32_t { return PT[(int64_t)t * nb + c]; };
+  SchedPipe S;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    S.dq[q] = load_dev(q < N ? q : N - 1);
+    S.wq[q] = S.cq[q] = S.e0[q] = S.b1[q] = S.e1[q] = 0;
+#pragma unroll
+    for (int i = 0; i < kPipePre; ++i) S.pf[q][i] = S.pd[q][i] = S.lc[q][i] = 0;
+  }
+
+  // Results of the last three ops: h1 = op T (after its step), h2, h3 before it.
+  uint32_t h1f = 0, h1d = 0, h2f = 0, h2d = 0, h3f = 0, h3d = 0;
+
+  // Stage T-2 for target op t = T+2, after op T.
+  auto stage2 = [&](auto qq, int T) {
+    constexpr int q1 = (decltype(qq)::value + 1) & 3, q2 = (decltype(qq)::value + 2) & 3;
+    const int t = min(T + 2, N - 1);  // past the end: computed and never used
+    const uint32_t dt = clampD(S.dq[q2]);
+    const uint32_t p01 = meta(kMetaP01, t);
+#pragma unroll
+    for (int i = 0; i < kPipePre; ++i) {
+      const int u = (int)pred_of(p01, i);
+      const uint32_t du = u == T + 1 ? clampD(S.dq[q1]) : u == T ? h1d : u == T - 1 ? h2d : clampD(S.pd[q2][i]);
+      S.lc[q2][i] = G.link_class[du * D + dt];
+    }
+    const int sb = sbase[dt];
+    const uint32_t k = cur[dt * kWave + lane];
+    S.cq[q2] = k;
+    S.e0[q2] = G.slice_end32[sb + k];
+    S.b1[q2] = G.slice_begin32[sb + k + 1];  // the slice arrays carry one spare entry
+    S.e1[q2] = G.slice_end32[sb + k + 1];
+    S.wq[q2] = G.dur32[(int64_t)t * C + dcls[dt]];
+  };
+  // Stage T-3 for target op t = T+3: predecessors u <= T-1 (the others are
+  // forwarded from the register history when op t runs).
+  auto stage3 = [&](auto qq, int T) {
+    constexpr int q3 = (decltype(qq)::value + 3) & 3;
+    const int t = min(T + 3, N - 1);
+    const uint32_t p01 = meta(kMetaP01, t);
+#pragma unroll
+    for (int i = 0; i < kPipePre; ++i) {
+      const int u = (int)pred_of(p01, i);
+      const int us = u < T ? u : 0;  // rows not yet written (or absent) read row 0, never used
+      S.pf[q3][i] = finT[(int64_t)us * nb + c];
+      S.pd[q3][i] = PT[(int64_t)us * nb + c];
+    }
+  };
+
   uint32_t ms = 0;
+  bool adv_prev = false;  // op T-1 moved its device to a later slice
   uint64_t sum = 0;
-  int d = 0;
-  uint32_t E = 0;  // end of the current slice of op v's device
-  if (N > 0) {
-    d = kVec16 ? dev_of(0) : prow[0];
-    if (d >= D) {
-      invalid = true;
-      d = 0;
-    }
-    E = G.slice_end32[sbase[d]];
-  }
-  uint32_t pf[kMaxPre];  // finish and device of op v's first predecessors (fetched during op v-1)
-  int pd[kMaxPre];
+  stage2(std::integral_constant<int, 2>(), -2);
+  stage2(std::integral_constant<int, 3>(), -1);
+  stage3(std::integral_constant<int, 3>(), -1);  // op 2: every predecessor comes from the history
+
+  auto step = [&](auto qq, int T) {
+    constexpr int q0 = decltype(qq)::value;
+    const uint32_t draw = S.dq[q0];
+    invalid |= draw >= (uint32_t)D;
+    const uint32_t d = clampD(draw);
+    const int slot = (int)d * kWave + lane;
+    uint32_t s = clk[slot];
+    const uint32_t rq = meta(kMetaReq, T), np = rq >> 16;
+    const int r = (int)(rq & 0xFFFFu);
+    const uint32_t w = S.wq[q0];
+    uint32_t ready = meta(kMetaRel, T);
+    const uint32_t p01 = meta(kMetaP01, T);
 #pragma unroll
-  for (int i = 0; i < kMaxPre; ++i) {
-    pf[i] = 0;
-    pd[i] = 0;
-  }
-  uint32_t f_prev = 0;
-  int d_prev = 0;
-  for (int v = 0; v < N; ++v) {
-    int dn_raw = 0;
-    if (!kVec16 && v + 1 < N) dn_raw = prow[v + 1];  // in flight while op v is placed
-    const uint32_t w = (C == 1) ? G.dur32[v] : G.dur32[v * C + dcls[d]];
-    const int r = G.op_req[v];
-    // ready: release, and every predecessor's finish plus its transfer
-    uint32_t ready = G.release32[r];
-    const int e0 = G.pred_ptr[v], e1 = G.pred_ptr[v + 1];
-#pragma unroll
-    for (int i = 0; i < kMaxPre; ++i) {
-      if (e0 + i < e1) {
-        const int u = G.pred_idx[e0 + i];
-        const bool last = (u == v - 1);
-        uint32_t t = last ? f_prev : pf[i];
-        const int du = last ? d_prev : pd[i];
-        if (du != d) t += xfer_of(G, u, du, d);
-        ready = umax32(ready, t);
-      }
-    }
-    for (int e = e0 + kMaxPre; e < e1; ++e) {  // more predecessors than were fetched ahead
-      const int u = G.pred_idx[e];
-      uint32_t t;
-      int du;
-      if (u == v - 1) {
-        t = f_prev;
-        du = d_prev;
+    for (int i = 0; i < kPipePre; ++i) {
+      const int u = (int)pred_of(p01, i);
+      const uint32_t tt = u == T - 1 ? h1f : u == T - 2 ? h2f : u == T - 3 ? h3f : S.pf[q0][i];
+      const uint32_t du = u == T - 1 ? h1d : u == T - 2 ? h2d : u == T - 3 ? h3d : clampD(S.pd[q0][i]);
+      uint32_t x;
+      if (kGeneralLink) {
+        x = G.xfer32[(int64_t)(u < T ? u : 0) * K + S.lc[q0][i]];
       } else {
-        t = finT[(int64_t)u * nb + c];
-        du = prow[u];
-        if (du >= D) du = 0;
+        const uint32_t x0 = meta(kMetaX + 2 * i, T), x1 = meta(kMetaX + 2 * i + 1, T);
+        x = S.lc[q0][i] ? x1 : x0;
       }
-      if (du != d) t += xfer_of(G, u, du, d);
-      ready = umax32(ready, t);
+      const uint32_t a = tt + (du != d ? x : 0u);
+      ready = (uint32_t)i < np ? umax32(ready, a) : ready;
     }
-    // one op at a time, in the current idle slice if it fits there, else in the
-    // first later slice that holds it (later slices start after the device's
-    // last finish, so only the ready time and the slice start matter there)
-    const int slot = d * kWave + lane;
-    uint32_t s = umax32(ready, clk[slot]);
-    if (s + w > E) {
-      const int sb = sbase[d];
-      int k = cur[slot];
-      for (;;) {
-        ++k;
-        const uint32_t t = umax32(ready, G.slice_begin32[sb + k]);
-        if (t + w <= G.slice_end32[sb + k]) {
-          s = t;
-          break;
+    if (kOverflow && np > (uint32_t)kPipePre) {  // predecessors past the pipelined ones
+      const int e0 = (int)meta(kMetaE0, T);
+      for (int e = e0 + kPipePre; e < e0 + (int)np; ++e) {
+        const int u = G.pred_idx[e];
+        uint32_t tt, du;
+        if (u == T - 1) {
+          tt = h1f;
+          du = h1d;
+        } else {
+          tt = finT[(int64_t)u * nb + c];
+          du = PT[(int64_t)u * nb + c];
+          if (du >= (uint32_t)D) du = 0;
+        }
+        if (du != d) tt += xfer_of(G, u, (int)du, (int)d);
+        ready = umax32(ready, tt);
+      }
+    }
+    // one op at a time, inside one idle slice: the current slice if the op
+    // fits there, else the first later slice that holds it
+    s = umax32(s, ready);
+    const bool stale = adv_prev && h1d == d;  // op T-1 advanced this device after the prefetch
+    bool adv = false;
+    if (stale || s + w > S.e0[q0]) {
+      int k;
+      const uint32_t t1 = umax32(s, S.b1[q0]);
+      if (!stale && t1 + w <= S.e1[q0]) {
+        s = t1;
+        k = (int)S.cq[q0] + 1;
+      } else {
+        const int sb = sbase[d];
+        k = stale ? (int)cur[slot] : (int)S.cq[q0] + 2;
+        for (;;) {
+          const uint32_t t = umax32(s, G.slice_begin32[sb + k]);
+          if (t + w <= G.slice_end32[sb + k]) {
+            s = t;
+            break;
+          }
+          ++k;
         }
       }
+      adv = true;
       cur[slot] = (uint16_t)k;
     }
     const uint32_t f = s + w;
     clk[slot] = f;
-    finT[(int64_t)v * nb + c] = f;
+    finT[(int64_t)T * nb + c] = f;
+    atomicMax(&comp[r * kWave + lane], f);
     ms = umax32(ms, f);
     sum += f;
-    uint32_t *cr = comp + r * kWave + lane;
-    *cr = umax32(*cr, f);
-    f_prev = f;
-    d_prev = d;
-    if (v + 1 < N) {  // fetch what op v+1 needs while this wave moves on
-      const int q0 = G.pred_ptr[v + 1], q1 = G.pred_ptr[v + 2];
+    h3f = h2f;
+    h3d = h2d;
+    h2f = h1f;
+    h2d = h1d;
+    h1f = f;
+    h1d = d;
+    adv_prev = adv;
+    stage2(qq, T);
+    stage3(qq, T);
+    S.dq[q0] = load_dev(min(T + 4, N - 1));
+  };
+
+  const int n_main = N / kWave * kWave;
+  for (; blk0 < n_main; blk0 += kWave) {
+    if (blk0 > 0) {
 #pragma unroll
-      for (int i = 0; i < kMaxPre; ++i) {
-        if (q0 + i < q1) {
-          const int u = G.pred_idx[q0 + i];
-          if (u != v) {
-            pf[i] = finT[(int64_t)u * nb + c];
-            const int du = prow[u];
-            pd[i] = du >= D ? 0 : du;
-          }
-        }
+      for (int f = 0; f < kOpMetaFields; ++f) {
+        mA[f] = mB[f];
+        mB[f] = G.op_meta[(int64_t)f * ms_ + blk0 + kWave + lane];
       }
-      if (kVec16) {
-        if (((v + 1) & 15) == 0) {  // next block becomes current; fetch the one after
-          blk = nxt;
-          if (v + 17 < N) nxt = *reinterpret_cast<const uint4 *>(prow + v + 17);
-        }
-        dn_raw = dev_of(v + 1);
-      }
-      d = dn_raw;
-      if (d >= D) {
-        invalid = true;
-        d = 0;
-      }
-      E = G.slice_end32[sbase[d] + cur[d * kWave + lane]];
+    }
+    for (int T = blk0; T < blk0 + kWave; T += 4) {
+      step(std::integral_constant<int, 0>(), T);
+      step(std::integral_constant<int, 1>(), T + 1);
+      step(std::integral_constant<int, 2>(), T + 2);
+      step(std::integral_constant<int, 3>(), T + 3);
     }
   }
+  if (n_main < N) {  // last partial block
+    if (n_main > 0) {
+#pragma unroll
+      for (int f = 0; f < kOpMetaFields; ++f) mA[f] = mB[f];
+    }
+    blk0 = n_main;
+    for (int T = n_main; T < N; T += 4) {
+      step(std::integral_constant<int, 0>(), T);
+      if (T + 1 < N) step(std::integral_constant<int, 1>(), T + 1);
+      if (T + 2 < N) step(std::integral_constant<int, 2>(), T + 2);
+      if (T + 3 < N) step(std::integral_constant<int, 3>(), T + 3);
+    }
+  }
+  if (!live) return;
   if (invalid) {
     makespan[c] = INT64_MAX;
     if (sumfin) sumfin[c] = INT64_MAX;
@@ -725,15 +831,18 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   int cus = 0;
   hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
-  // 16-byte placement blocks need every row (and so the batch) 16-byte aligned
-  const bool vec16 = N % 16 == 0 && (reinterpret_cast<uintptr_t>(P) & 15) == 0;
-  err = hipFuncSetAttribute(vec16 ? reinterpret_cast<const void *>(&fast_schedule<true>)
-                                  : reinterpret_cast<const void *>(&fast_schedule<false>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
+  // kernel variant: link classes beyond two go through xfer32; in-degrees above
+  // the pipelined count go through the predecessor CSR
+  const bool general_link = g->n_link > 2, overflow = g->max_indeg > kPipePre;
+  const void *sched_fn = general_link ? (overflow ? reinterpret_cast<const void *>(&fast_schedule<true, true>)
+                                                  : reinterpret_cast<const void *>(&fast_schedule<true, false>))
+                                      : (overflow ? reinterpret_cast<const void *>(&fast_schedule<false, true>)
+                                                  : reinterpret_cast<const void *>(&fast_schedule<false, false>));
+  err = hipFuncSetAttribute(sched_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
   if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
 
-  // chunk: op-major and row-major finish times
-  const int64_t per_cand = N * (4 + 4);
+  // chunk: op-major placements, op-major and row-major finish times
+  const int64_t per_cand = N * (1 + 4 + 4);
   int64_t chunk = kScratchBudget / std::max<int64_t>(1, per_cand);
   chunk = std::max<int64_t>(kWave, chunk / kWave * kWave);
   chunk = std::min<int64_t>(chunk, int64_t(65535) * 64);  // transpose grids index 64-candidate tiles in y
@@ -746,6 +855,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   const int64_t slot_cap = N + E + 1;  // most allocations one device can hold
 
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
+  const size_t sz_pt = align((size_t)chunk * N + 1);
   const size_t sz_fin = align((size_t)chunk * N * 4 + 4);
   const size_t sz_own = align(((size_t)sub * N + 1) * sizeof(uint3));
   const size_t sz_cp = align(((size_t)sub * E + 1) * sizeof(uint3));
@@ -755,7 +865,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   const size_t sz_wc = align((size_t)nslots * (slot_cap + 2) * 4);
   void *scratch = nullptr;
   err = hipMallocAsync(&scratch,
-                       2 * sz_fin + sz_own + sz_cp + sz_meta + sz_wk + sz_wb + sz_wc,
+                       sz_pt + 2 * sz_fin + sz_own + sz_cp + sz_meta + sz_wk + sz_wb + sz_wc,
                        stream);
   if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
@@ -764,6 +874,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
     p += bytes;
     return q;
   };
+  auto *PT = reinterpret_cast<uint8_t *>(take(sz_pt));
   auto *finT = reinterpret_cast<uint32_t *>(take(sz_fin));
   auto *fin = reinterpret_cast<uint32_t *>(take(sz_fin));
   auto *own = reinterpret_cast<Rec *>(take(sz_own));
@@ -782,14 +893,25 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
     const int64_t nb = std::min(chunk, B - b0);
     const uint8_t *Pc = P + b0 * N;
+    SsTimingRec *tp = ss_timing_start(SS_KERNEL_TRANSPOSE, stream);
+    if (N > 0) {  // candidates' placement rows -> op-major [op][candidate]
+      const dim3 tg((unsigned)((N + 63) / 64), (unsigned)((nb + 63) / 64));
+      hipLaunchKernelGGL(transpose_tiles<uint8_t>, tg, dim3(256), 0, stream, Pc, nb, (int64_t)N, PT);
+    }
+    ss_timing_stop(tp, stream);
+    if (!check("transpose launch")) break;
     SsTimingRec *ts = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
-    const dim3 sgrid((unsigned)((nb + kWave - 1) / kWave));
-    if (vec16)
-      hipLaunchKernelGGL(fast_schedule<true>, sgrid, dim3(kWave), sched_lds, stream, G, Pc, nb, finT, makespan + b0,
-                         sumfin ? sumfin + b0 : nullptr, slack ? slack + b0 * R : nullptr, violation + b0);
-    else
-      hipLaunchKernelGGL(fast_schedule<false>, sgrid, dim3(kWave), sched_lds, stream, G, Pc, nb, finT, makespan + b0,
-                         sumfin ? sumfin + b0 : nullptr, slack ? slack + b0 * R : nullptr, violation + b0);
+    {
+      const uint8_t *PTc = PT;
+      int64_t *ms_out = makespan + b0, *sf_out = sumfin ? sumfin + b0 : nullptr,
+              *sl_out = slack ? slack + b0 * R : nullptr;
+      uint8_t *vi_out = violation + b0;
+      void *args[] = {const_cast<GmgView *>(&G), &PTc, const_cast<int64_t *>(&nb), &finT, &ms_out, &sf_out, &sl_out,
+                      &vi_out};
+      const hipError_t le = hipLaunchKernel(sched_fn, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), args,
+                                            sched_lds, stream);
+      if (le != hipSuccess && rc == SS_OK) rc = hip_fail(le, "fast_schedule launch");
+    }
     ss_timing_stop(ts, stream);
     if (!check("fast_schedule launch")) break;
     SsTimingRec *tt = nullptr;

@@ -24,9 +24,28 @@ struct GmgView {
   // 32-bit copies of every time quantity, present when the loader proved the
   // whole time horizon (all starts, finishes, frees and finite slice bounds)
   // stays below 2^32 - 1, there are at most 65535 ops and every output size
-  // fits in 32 bits; the open slice end becomes 0xFFFFFFFF.
+  // fits in 32 bits; the open slice end becomes 0xFFFFFFFF.  The 32-bit slice
+  // arrays hold one spare entry past the last slice.
   int32_t time32;
   const uint32_t *dur32, *xfer32, *slice_begin32, *slice_end32, *release32;
+  // Per-op fields of the 32-bit path, field-major [kOpMetaFields][meta_stride]
+  // so a wave reads the fields of 64 consecutive ops with one coalesced load
+  // per field (meta_stride = N rounded up to 64 plus one spare block, >= 128).
+  const uint32_t *op_meta;
+  int32_t meta_stride;
+};
+
+// Fields of op_meta for op v.  Predecessors beyond the first four and link
+// class counts above two are read from the CSR and xfer32 tables instead.
+enum OpMetaField {
+  kMetaDur = 0,   // dur32[v] when there is one device class, else 0
+  kMetaReq = 1,   // request id | predecessor count << 16 (count saturates at 0xFFFF)
+  kMetaRel = 2,   // release32 of the op's request
+  kMetaP01 = 3,   // predecessors 0 and 1 as u16 (0xFFFF: none)
+  kMetaP23 = 4,   // predecessors 2 and 3
+  kMetaX = 5,     // 8 fields: transfer time of predecessor i over link class k at kMetaX + 2 i + k
+  kMetaE0 = 13,   // pred_ptr[v]
+  kOpMetaFields = 14
 };
 
 struct ss_gmg {
@@ -34,6 +53,7 @@ struct ss_gmg {
   int64_t n_ops = 0, n_edges = 0, n_dev = 0, n_class = 0, n_link = 0, n_req = 0;
   int64_t max_slices = 0;  // largest slice count of any device
   int64_t horizon = 0;     // loader's upper bound on every simulated time
+  int64_t max_indeg = 0;   // largest predecessor count of any op
   void *dev_mem = nullptr;
   GmgView view{};
 };
