@@ -142,8 +142,12 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     // 32-bit time path: every time the simulation can produce is <= horizon
     int64_t max_bytes = 0;
     for (int64_t v = 0; v < N; ++v) max_bytes = std::max(max_bytes, d->out_bytes[v]);
-    const bool time32 = horizon < (i128)UINT32_MAX && N <= 65535 && max_bytes <= (int64_t)UINT32_MAX;
-    std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32, meta;
+    const bool time32 =
+        horizon < (i128)UINT32_MAX && N <= 65535 && E <= 65535 && max_bytes <= (int64_t)UINT32_MAX;
+    bool pos_dur = true;
+    for (int64_t i = 0; i < N * C; ++i) pos_dur = pos_dur && d->dur[i] >= 1;
+    std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32, meta, lbits, bytes32;
+    const int64_t lwords = (D + 31) / 32;
     const int64_t meta_stride = std::max<int64_t>(128, (N + 63) / 64 * 64 + 64);  // two blocks of 64 past any op
     if (time32) {
       meta.assign((size_t)kOpMetaFields * meta_stride, 0);
@@ -164,6 +168,13 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
         M(kMetaE0, v) = (uint32_t)e0;
       }
       dur32.assign(d->dur, d->dur + N * C);
+      bytes32.assign(d->out_bytes, d->out_bytes + N);
+      if (K <= 2) {
+        lbits.assign((size_t)D * lwords, 0u);
+        for (int64_t a = 0; a < D; ++a)
+          for (int64_t b = 0; b < D; ++b)
+            if (d->link_class[a * D + b]) lbits[a * lwords + b / 32] |= 1u << (b % 32);
+      }
       xfer32.assign(xfer.begin(), xfer.end());
       rel32.assign(d->release, d->release + R);
       sb32.assign(S + 1, UINT32_MAX);  // spare entry: read ahead, never used
@@ -193,7 +204,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     const size_t o_dl = pk.add(d->deadline, R * sizeof(int64_t));
     const size_t o_link = pk.add(d->link_class, D * D);
     const size_t o_dur32 = pk.add(dur32), o_xfer32 = pk.add(xfer32), o_sb32 = pk.add(sb32), o_se32 = pk.add(se32),
-                 o_rel32 = pk.add(rel32), o_meta = pk.add(meta);
+                 o_rel32 = pk.add(rel32), o_meta = pk.add(meta), o_lbits = pk.add(lbits), o_b32 = pk.add(bytes32);
     pk.add(nullptr, 256);  // tail padding
 
     ss_gmg *g = new ss_gmg();
@@ -241,6 +252,10 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     V.release32 = reinterpret_cast<const uint32_t *>(base + o_rel32);
     V.op_meta = reinterpret_cast<const uint32_t *>(base + o_meta);
     V.meta_stride = (int32_t)meta_stride;
+    V.pos_dur = pos_dur ? 1 : 0;
+    V.link_bits = lbits.empty() ? nullptr : reinterpret_cast<const uint32_t *>(base + o_lbits);
+    V.link_words = (int32_t)lwords;
+    V.bytes32 = reinterpret_cast<const uint32_t *>(base + o_b32);
     g->n_ops = N;
     g->n_edges = E;
     g->n_dev = D;

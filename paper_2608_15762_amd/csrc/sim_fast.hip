@@ -42,8 +42,7 @@ constexpr int kCap = 1024;            // allocations of one device evaluated in 
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per chunk
 constexpr int64_t kRecordBudget = int64_t(12) << 30;   // interval records per sub-chunk
-constexpr int kPeakBlocksPerCU = 4;
-constexpr int kMaxPre = 4;            // predecessors fetched one op ahead
+constexpr int kPeakBlocksPerCU = 7;  // fast_peaks holds about 22 KB of LDS
 
 __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
 __device__ __forceinline__ int64_t imax64(int64_t a, int64_t b) { return a > b ? a : b; }
@@ -68,15 +67,20 @@ __global__ __launch_bounds__(256) void transpose_tiles(const T *__restrict__ in,
 }
 
 // ------------------------------------------------------------------ schedule
+// link class of a transfer from device a to device b (at most two classes)
+__device__ __forceinline__ uint32_t link_bit(const GmgView &G, uint32_t a, uint32_t b) {
+  return (G.link_bits[a * G.link_words + (b >> 5)] >> (b & 31)) & 1u;
+}
+
 __device__ __forceinline__ uint32_t xfer_of(const GmgView &G, int u, int du, int d) {
   const int K = G.n_link;
   if (K == 1) return G.xfer32[u];
-  const int k = G.link_class[du * G.n_dev + d];
   if (K == 2) {  // both entries are wave-uniform loads
+    const uint32_t k = link_bit(G, (uint32_t)du, (uint32_t)d);
     const uint32_t x0 = G.xfer32[2 * u], x1 = G.xfer32[2 * u + 1];
     return k ? x1 : x0;
   }
-  return G.xfer32[u * K + k];
+  return G.xfer32[u * K + G.link_class[du * G.n_dev + d]];
 }
 
 // Software pipeline of the schedule, for target op T (one lane per candidate):
@@ -188,7 +192,7 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     for (int i = 0; i < kPipePre; ++i) {
       const int u = (int)pred_of(p01, i);
       const uint32_t du = u == T + 1 ? clampD(S.dq[q1]) : u == T ? h1d : u == T - 1 ? h2d : clampD(S.pd[q2][i]);
-      S.lc[q2][i] = G.link_class[du * D + dt];
+      S.lc[q2][i] = kGeneralLink ? (uint32_t)G.link_class[du * D + dt] : link_bit(G, du, dt);  // zero with one class
     }
     const int sb = sbase[dt];
     const uint32_t k = cur[dt * kWave + lane];
@@ -354,42 +358,77 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
 }
 
 // ------------------------------------------------------------------ memory
-// An interval record: {allocation time, free time (kInf32 = never), bytes}.
-using Rec = uint3;
+// Residency intervals (Sec. 3.3.2) are written by fast_intervals into
+// per-device buckets and evaluated by fast_peaks.
+//   own record  {start, free time (kInf32: never), bytes, free locator}
+//   copy record {allocation time, free time, bytes, alloc window << 16 | free locator}
+// A device's own starts S[0..m) (its ops in index order) are sorted, and
+// every event is placed by how many own starts precede it, its gap:
+//   allocation of a copy at time c:  #{k : S[k] <= c}
+//   free at time h:                  #{k : S[k] <  h}
+// (frees precede allocations at equal times: intervals are half-open).  The
+// writer knows each gap exactly or nearly: a free at the finish of a local
+// op of rank k (all durations positive) has gap k + 1; a copy is allocated
+// shortly before its first consumer of rank k starts, so its gap lies in
+// [k-3, k+1]; a transfer-bound free of an op of rank k lies in [k+1, k+5].
+// A locator holds the exact gap, or (kLocWindow) the start L of a window
+// [L, L+4] that is checked and, if the gap lies outside, replaced by a
+// binary search.
+using Rec = uint4;
+constexpr uint32_t kLocWindow = 0x80000000u;
 
-// Intervals of op v: its own output at slot own_pos of its device's bucket,
-// and one copy per remote destination device (slot taken with an LDS atomic).
-__device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32_t *frow, int v, int own_pos,
-                             int *cfill, Rec *own, Rec *cp) {
+__device__ __forceinline__ uint32_t loc_window(int L) { return kLocWindow | (uint32_t)max(L, 0); }
+
+// Intervals of op v (device d, rank rv among the ops of d): its own output at
+// slot own_pos of d's bucket, one copy per remote destination device (slot
+// taken with an LDS atomic).
+__device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32_t *frow, const uint16_t *rk, int v,
+                             int d, int rv, int own_pos, int *cfill, Rec *own, Rec *cp) {
   const int C = G.n_class;
-  const int d = prow[v];
-  const uint32_t b = (uint32_t)G.out_bytes[v];
+  const uint32_t b = G.bytes32[v];
   const int x0 = G.succ_ptr[v], x1 = G.succ_ptr[v + 1];
   const uint32_t f = frow[v];
-  uint32_t F = kInf32;  // kept forever without consumers
+  uint32_t F = kInf32, loc = 0;  // kept forever without consumers
   if (x1 > x0) {
-    F = f;
+    // local consumers finish in index order, so the last one finishes last
+    uint32_t L = f, A = 0;
+    int rl = rv;
     for (int q = x0; q < x1; ++q) {
       const int x = G.succ_idx[q];
       const int dx = prow[x];
-      F = umax32(F, (dx == d) ? frow[x] : f + xfer_of(G, v, d, dx));
+      if (dx == d) {
+        L = frow[x];
+        rl = rk[x];
+      } else {
+        A = umax32(A, f + xfer_of(G, v, d, dx));
+      }
+    }
+    if (A > L) {
+      F = A;
+      loc = loc_window(rv + 1);
+    } else {
+      F = L;
+      loc = G.pos_dur ? (uint32_t)(rl + 1) : loc_window(rl - 3);
     }
   }
-  own[own_pos] = Rec{f - G.dur32[v * C + G.dev_class[d]], F, b};
+  own[own_pos] = Rec{f - (C == 1 ? G.dur32[v] : G.dur32[v * C + G.dev_class[d]]), F, b, loc};
   if (b == 0) return;
   for (int q = x0; q < x1; ++q) {
-    const int e = prow[G.succ_idx[q]];
+    const int xf = G.succ_idx[q];
+    const int e = prow[xf];
     if (e == d) continue;
     bool first = true;
     for (int q2 = x0; q2 < q; ++q2)
       if (prow[G.succ_idx[q2]] == e) first = false;
     if (!first) continue;
-    uint32_t g = 0;  // the copy lives until its last consumer on e finishes
-    for (int q2 = q; q2 < x1; ++q2) {
+    int y = xf;  // last consumer on e: the copy lives until it finishes
+    for (int q2 = q + 1; q2 < x1; ++q2) {
       const int x = G.succ_idx[q2];
-      if (prow[x] == e) g = umax32(g, frow[x]);
+      if (prow[x] == e) y = x;
     }
-    cp[atomicAdd(&cfill[e], 1)] = Rec{f, g, b};
+    const int ra = rk[xf], ry = rk[y];
+    const uint32_t floc = G.pos_dur ? (uint32_t)(ry + 1) : (uint32_t)max(ry - 3, 0);
+    cp[atomicAdd(&cfill[e], 1)] = Rec{f, frow[y], b, (uint32_t)max(ra - 3, 0) << 16 | floc};
   }
 }
 
@@ -438,27 +477,29 @@ __device__ __forceinline__ void chunk_groups(int d, bool active, int val, int la
 // Per-candidate bucket geometry written by fast_intervals, read by fast_peaks.
 __device__ __forceinline__ int meta_stride(int D) { return 3 * (D + 1); }
 
+// One wave per candidate.  Pass A ranks every op among the ops of its device
+// (rank table rk) and counts ops and in-degrees per device; pass B writes the
+// records.
 __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const uint8_t *__restrict__ P,
                                                         const uint32_t *__restrict__ fin, int64_t j0,
                                                         Rec *__restrict__ own_all, Rec *__restrict__ cp_all,
-                                                        int32_t *__restrict__ meta,
+                                                        int32_t *__restrict__ meta, uint16_t *__restrict__ rank_all,
                                                         const uint8_t *__restrict__ violation) {
-  __shared__ int own_off[257], cp_off[257], cfill[256], ocnt[256], base[256];
+  __shared__ int own_off[257], cp_off[257], cfill[256], base[256];
   const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops];
   const int lane = threadIdx.x;
   const int64_t j = blockIdx.x, c = j0 + j;
   if (violation[c] & SS_VIOLATION_INVALID) return;
   const uint8_t *prow = P + c * N;
   const uint32_t *frow = fin + c * N;
+  uint16_t *rk = rank_all + j * N;
   Rec *own = own_all + j * N;
   Rec *cp = cp_all + j * E;
   for (int d = lane; d < D; d += kWave) {
     cfill[d] = 0;
-    ocnt[d] = 0;
     base[d] = 0;
   }
   __syncthreads();
-  // ops per device, and summed in-degree (copies landing on a device <= it)
   for (int v0 = 0; v0 < N; v0 += kWave) {
     const int v = v0 + lane;
     const bool act = v < N;
@@ -466,9 +507,11 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
     const int indeg = act ? G.pred_ptr[v + 1] - G.pred_ptr[v] : 0;
     int rank, gd, gcnt, gsum;
     chunk_groups(d, act, indeg, lane, rank, gd, gcnt, gsum);
+    if (act) rk[v] = (uint16_t)(base[d] + rank);
+    __syncthreads();
     if (gd >= 0) {
-      ocnt[gd] += gcnt;
-      cfill[gd] += gsum;
+      base[gd] += gcnt;
+      cfill[gd] += gsum;  // copies landing on a device <= its summed in-degree
     }
     __syncthreads();
   }
@@ -476,7 +519,7 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
     int so = 0, sc = 0;
     for (int d = 0; d < D; ++d) {
       own_off[d] = so;
-      so += ocnt[d];
+      so += base[d];
       cp_off[d] = sc;
       sc += cfill[d];
       cfill[d] = cp_off[d];
@@ -484,19 +527,15 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
     own_off[D] = so;
     cp_off[D] = sc;
   }
-  __syncthreads();
+  __syncthreads();  // also orders the rank-table stores before the loads below
   for (int v0 = 0; v0 < N; v0 += kWave) {
     const int v = v0 + lane;
-    const bool act = v < N;
-    const int d = act ? prow[v] : 0;
-    int rank, gd, gcnt, gsum;
-    chunk_groups(d, act, 0, lane, rank, gd, gcnt, gsum);
-    const int pos = act ? own_off[d] + base[d] + rank : 0;
-    __syncthreads();
-    if (gd >= 0) base[gd] += gcnt;
-    if (act) op_intervals(G, prow, frow, v, pos, cfill, own, cp);
-    __syncthreads();
+    if (v < N) {
+      const int d = prow[v], rv = rk[v];
+      op_intervals(G, prow, frow, rk, v, d, rv, own_off[d] + rv, cfill, own, cp);
+    }
   }
+  __syncthreads();
   int32_t *m = meta + j * meta_stride(D);
   for (int d = lane; d <= D; d += kWave) {
     m[d] = own_off[d];
@@ -505,75 +544,37 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
   }
 }
 
-// Up to 4 searches per lane in lockstep (independent LDS loads in flight):
-// r[j] = first index i in a[0, n) with a[i] >= x[j] (kUpper: a[i] > x[j]).
-template <bool kUpper, class UP>
-__device__ __forceinline__ void search4(UP a, int n, const uint32_t (&x)[4], int (&r)[4]) {
-  int b[4] = {0, 0, 0, 0};
-  if (n == 0) {
+// Gap of x among the sorted S[0, m): #{k : S[k] <= x} (kLe) or S[k] < x, with
+// the answer expected in [L, L+4]: six independent probes decide it, a
+// binary search covers the rest.
+template <bool kLe, class UP>
+__device__ __forceinline__ int gap_of(UP S, int m, uint32_t x, int L) {
+  if (m == 0) return 0;
+  L = min(L, m);
+  auto hit = [&](uint32_t sv) { return kLe ? sv <= x : sv < x; };
+  const uint32_t sm1 = S[max(L - 1, 0)];
+  uint32_t sv[5];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) r[j] = 0;
-    return;
-  }
-  int len = n;
-  while (len > 1) {
-    const int half = len >> 1;
+  for (int q = 0; q < 5; ++q) sv[q] = S[min(L + q, m - 1)];
+  const bool lo_ok = L == 0 || hit(sm1);
+  const bool hi_ok = L + 4 >= m || !hit(sv[4]);
+  if (lo_ok && hi_ok) {
+    int g = L;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t v = a[b[j] + half];
-      if (kUpper ? (v <= x[j]) : (v < x[j])) b[j] += half;
-    }
-    len -= half;
+    for (int q = 0; q < 4; ++q) g += (L + q < m && hit(sv[q])) ? 1 : 0;
+    return g;
   }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const uint32_t v = a[b[j]];
-    r[j] = b[j] + ((kUpper ? (v <= x[j]) : (v < x[j])) ? 1 : 0);
-  }
-}
-
-// ascending bitonic sort of n (u32 key, u64 payload) pairs by one wave
-template <class KP, class VP>
-__device__ void sort_u32_pairs(KP keys, VP vals, int n, int lane) {
-  if (n < 2) return;
-  int lg = 0;
-  while ((1 << lg) < n) ++lg;
-  const int half_total = 1 << (lg - 1);
-  for (int kb = 1; kb <= lg; ++kb) {
-    const int k = 1 << kb, hmask = (k >> 1) - 1;
-    for (int q = lane; q < half_total; q += kWave) {
-      const int base = (q >> (kb - 1)) << kb, off = q & hmask;
-      const int i = base + off, l = base + k - 1 - off;
-      if (l < n) {
-        const uint32_t ki = keys[i], kl = keys[l];
-        if (kl < ki) {
-          const uint64_t vi = vals[i];
-          keys[i] = kl;
-          keys[l] = ki;
-          vals[i] = vals[l];
-          vals[l] = vi;
-        }
-      }
-    }
-    __syncthreads();
-    for (int jb = kb - 2; jb >= 0; --jb) {
-      const int j = 1 << jb;
-      for (int q = lane; q < half_total; q += kWave) {
-        const int i = ((q >> jb) << (jb + 1)) + (q & (j - 1)), l = i + j;
-        if (l < n) {
-          const uint32_t ki = keys[i], kl = keys[l];
-          if (kl < ki) {
-            const uint64_t vi = vals[i];
-            keys[i] = kl;
-            keys[l] = ki;
-            vals[i] = vals[l];
-            vals[l] = vi;
-          }
-        }
-      }
-      __syncthreads();
+  int lo = 0, n = m;
+  while (n > 0) {
+    const int half = n >> 1;
+    if (hit(S[lo + half])) {
+      lo += half + 1;
+      n -= half + 1;
+    } else {
+      n = half;
     }
   }
+  return lo;
 }
 
 __device__ __forceinline__ int64_t wave_incl_scan64(int64_t x, int lane) {
@@ -591,8 +592,6 @@ __device__ __forceinline__ int wave_incl_scan32(int x, int lane) {
   }
   return x;
 }
-
-constexpr int kSmallGap = 16;  // copies between two own allocations sorted by one lane
 
 // In-place inclusive prefix sum of a[0, n): each lane scans its own contiguous
 // run, one wave scan combines the runs.  Callers fence before and after.
@@ -614,154 +613,107 @@ template <class IP, class FP>
 __device__ int64_t max_live(IP alloc, FP freed, int n, int lane) {
   const int m = (n + kWave - 1) / kWave, lo = lane * m, hi = min(n, lo + m);
   int64_t s = 0;
-  for (int i = lo; i < hi; ++i) s += alloc[i] - (int64_t)freed[i];
+  for (int i = lo; i < hi; ++i) s += (int64_t)alloc[i] - (int64_t)freed[i];
   int64_t run = wave_incl_scan64(s, lane) - s, best = 0;
   for (int i = lo; i < hi; ++i) {
-    run += alloc[i] - (int64_t)freed[i];
+    run += (int64_t)alloc[i] - (int64_t)freed[i];
     best = imax64(best, run);
   }
   for (int o = kWave / 2; o >= 1; o >>= 1) best = imax64(best, __shfl_xor(best, o, kWave));
   return best;
 }
 
-// Peak of one device from its own records (start-sorted) and copy records.
-// Work arrays (LDS, or a global slot buffer when too large):
-//   sk/sp  allocation times and {free time, bytes} of own (first n1) then copy records
-//   sq     per copy: (gap << 16 | slot), kept in fd's storage until fd is needed;
-//          gap counts / prefix in gc (n1 + 2 ints)
-//   mk/mb  merged allocation times and bytes; fd bytes freed just before each
-template <class UP, class PP, class IP, class FP, class CP>
-__device__ int64_t device_peak(const Rec *own, int o0, int n1, const Rec *cp, int c0, int n4, UP sk, PP sp, CP gc,
-                               UP mk, IP mb, FP fd, int lane) {
+// Peak of one device: m own records (start-sorted) and nc copy records.
+// Allocations are merged in time order as
+//   [copies of gap 0] own 0 [copies of gap 1] own 1 ... own m-1 [copies of gap m]
+// so own k sits at k + CG[k+1] and the copy of in-gap rank r of gap g at
+// g + CG[g] + r, where CG[g] counts the copies in gaps before g; a free of gap
+// g lands before the first allocation at or after it: g + CG[g] + the copies
+// of gap g allocated before it.  Work arrays (LDS, or global slot memory when
+// the device holds more than kCap allocations):
+//   ak  own starts S[0, m), then the copy times grouped by gap
+//   ag  gap counts / CG[0, m+2), then per copy (gap << 16 | slot in gap)
+//   ai  per grouped copy time, the copy's index (ties between equal times)
+//   mb  allocation bytes by merged position; fr bytes freed before each
+template <class UP, class IP, class HP, class FP>
+__device__ int64_t device_peak(const Rec *own, int m, const Rec *cp, int nc, bool pos_dur, UP ak, IP ag, HP ai, UP mb,
+                               FP fr, int lane) {
   constexpr int kB = 8;
-  uint32_t *sq = reinterpret_cast<uint32_t *>(fd);
-  const int na = n1 + n4;
-  for (int base = lane; base < na; base += kB * kWave) {  // all loads of a batch in flight together
+  const int na = m + nc;
+  UP bt = ak + m;                                       // grouped copy times
+  uint32_t *qg = reinterpret_cast<uint32_t *>(ag + m + 2);  // per copy: gap << 16 | slot
+  for (int base = lane; base < m; base += kB * kWave) {  // a batch of loads in flight together
     Rec r[kB];
 #pragma unroll
-    for (int j = 0; j < kB; ++j) {
-      const int i = base + j * kWave;
-      if (i < na) r[j] = i < n1 ? own[o0 + i] : cp[c0 + i - n1];
-    }
+    for (int q = 0; q < kB; ++q)
+      if (base + q * kWave < m) r[q] = own[base + q * kWave];
 #pragma unroll
-    for (int j = 0; j < kB; ++j) {
-      const int i = base + j * kWave;
-      if (i < na) {
-        sk[i] = r[j].x;
-        sp[i] = ((uint64_t)r[j].y << 32) | r[j].z;
+    for (int q = 0; q < kB; ++q) {
+      const int i = base + q * kWave;
+      if (i < m) {
+        ak[i] = r[q].x;
+        fr[i] = r[q].z;  // own bytes parked in fr until the merged order is known
       }
     }
   }
-  for (int i = lane; i <= n1 + 1; i += kWave) gc[i] = 0;
+  for (int i = m + lane; i < na; i += kWave) fr[i] = 0;
+  for (int i = lane; i < m + 2; i += kWave) ag[i] = 0;
   __syncthreads();
-  // each copy falls in the gap after the last own allocation at or before it
-  int big = 0;  // largest slot this lane saw
-  for (int base = lane; base < n4; base += 4 * kWave) {
-    uint32_t x[4];
-    int r[4];
+  // gap of every copy allocation, and its slot inside the gap
+  for (int base = lane; base < nc; base += 4 * kWave) {
+    Rec r[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) x[j] = base + j * kWave < n4 ? sk[n1 + base + j * kWave] : 0;
-    search4<true>(sk, n1, x, r);
+    for (int q = 0; q < 4; ++q)
+      if (base + q * kWave < nc) r[q] = cp[base + q * kWave];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = base + j * kWave;
-      if (i < n4) {
-        const int slot = atomicAdd(&gc[r[j] + 1], 1);
-        sq[i] = ((uint32_t)r[j] << 16) | (uint32_t)slot;
-        big = max(big, slot + 1);
-      }
-    }
-  }
-  for (int o = kWave / 2; o >= 1; o >>= 1) big = max(big, __shfl_xor(big, o, kWave));
-  __syncthreads();
-  const bool small_gaps = big <= kSmallGap;
-  if (small_gaps) {
-    // gc[g + 1] = copies in gap g  ->  gc[g] = copies in gaps before g
-    prefix_inplace(gc, n1 + 2, lane);
-    __syncthreads();
-    // own allocation i follows gaps 0..i ; a copy in gap g follows own 0..g-1
-    for (int i = lane; i < n1; i += kWave) {
-      const int pos = i + gc[i + 1];
-      mk[pos] = sk[i];
-      mb[pos] = (int64_t)(sp[i] & 0xFFFFFFFFu);
-    }
-    for (int i = lane; i < n4; i += kWave) {
-      const int g = (int)(sq[i] >> 16), slot = (int)(sq[i] & 0xFFFFu);
-      const int pos = g + gc[g] + slot;
-      mk[pos] = sk[n1 + i];
-      mb[pos] = (int64_t)(sp[n1 + i] & 0xFFFFFFFFu);
-    }
-    __syncthreads();
-    // order the copies inside each gap (at most kSmallGap of them)
-    for (int g = lane; g <= n1; g += kWave) {
-      const int s0 = g + gc[g], cnt = gc[g + 1] - gc[g];
-      for (int a = 1; a < cnt; ++a) {
-        const uint32_t key = mk[s0 + a];
-        const int64_t val = mb[s0 + a];
-        int z = a - 1;
-        while (z >= 0 && mk[s0 + z] > key) {
-          mk[s0 + z + 1] = mk[s0 + z];
-          mb[s0 + z + 1] = mb[s0 + z];
-          --z;
-        }
-        mk[s0 + z + 1] = key;
-        mb[s0 + z + 1] = val;
-      }
-    }
-  } else {
-    // large gaps: sort the copies, then merge the two runs by ranks
-    sort_u32_pairs(sk + n1, sp + n1, n4, lane);
-    for (int base = lane; base < n1; base += 4 * kWave) {
-      uint32_t x[4];
-      int r[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) x[j] = base + j * kWave < n1 ? sk[base + j * kWave] : 0;
-      search4<false>(sk + n1, n4, x, r);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int i = base + j * kWave;
-        if (i < n1) {
-          mk[i + r[j]] = x[j];
-          mb[i + r[j]] = (int64_t)(sp[i] & 0xFFFFFFFFu);
-        }
-      }
-    }
-    for (int base = lane; base < n4; base += 4 * kWave) {
-      uint32_t x[4];
-      int r[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) x[j] = base + j * kWave < n4 ? sk[n1 + base + j * kWave] : 0;
-      search4<true>(sk, n1, x, r);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int i = base + j * kWave;
-        if (i < n4) {
-          mk[i + r[j]] = x[j];
-          mb[i + r[j]] = (int64_t)(sp[n1 + i] & 0xFFFFFFFFu);
-        }
+    for (int q = 0; q < 4; ++q) {
+      const int i = base + q * kWave;
+      if (i < nc) {
+        const int g = gap_of<true>(ak, m, r[q].x, (int)(r[q].w >> 16));
+        const int slot = atomicAdd(&ag[g + 1], 1);
+        qg[i] = (uint32_t)g << 16 | (uint32_t)slot;
       }
     }
   }
   __syncthreads();
-  for (int i = lane; i < na; i += kWave) fd[i] = 0;
+  prefix_inplace(ag, m + 2, lane);  // ag[g] = CG[g]
   __syncthreads();
-  // each free lands on the first allocation at or after its time
-  for (int base = lane; base < na; base += 4 * kWave) {
-    uint32_t x[4];
-    int r[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) x[j] = base + j * kWave < na ? (uint32_t)(sp[base + j * kWave] >> 32) : kInf32;
-    search4<false>(mk, na, x, r);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = base + j * kWave;
-      if (i < na && x[j] != kInf32 && r[j] < na)
-        atomicAdd(reinterpret_cast<unsigned long long *>(&fd[r[j]]),
-                  (unsigned long long)(sp[i] & 0xFFFFFFFFu));
-    }
+  for (int i = lane; i < nc; i += kWave) {
+    const int g = (int)(qg[i] >> 16), slot = (int)(qg[i] & 0xFFFFu);
+    bt[ag[g] + slot] = cp[i].x;
+    ai[ag[g] + slot] = i;
+  }
+  for (int k = lane; k < m; k += kWave) {
+    mb[k + ag[k + 1]] = (uint32_t)fr[k];
+    fr[k] = 0;
   }
   __syncthreads();
-  const int64_t best = max_live(mb, fd, na, lane);
+  // frees: gap (exact or by window), then the copies of that gap allocated before
+  auto place_free = [&](int g, uint32_t h, uint32_t bytes) {
+    const int s0 = ag[g], s1 = ag[g + 1];
+    int pos = g + s0;
+    for (int z = s0; z < s1; ++z) pos += bt[z] < h ? 1 : 0;
+    if (pos < na) atomicAdd(reinterpret_cast<unsigned long long *>(&fr[pos]), (unsigned long long)bytes);
+  };
+  for (int i = lane; i < nc; i += kWave) {
+    const Rec r = cp[i];
+    const int g = (int)(qg[i] >> 16), s0 = ag[g], s1 = ag[g + 1];
+    int rank = 0;
+    for (int z = s0; z < s1; ++z) {
+      const uint32_t t = bt[z];
+      rank += (t < r.x || (t == r.x && (int)ai[z] < i)) ? 1 : 0;
+    }
+    mb[g + s0 + rank] = r.z;
+    const int fl = (int)(r.w & 0xFFFFu);
+    place_free(pos_dur ? fl : gap_of<false>(ak, m, r.y, fl), r.y, r.z);
+  }
+  for (int k = lane; k < m; k += kWave) {
+    const Rec r = own[k];
+    if (r.y != kInf32) place_free((r.w & kLocWindow) ? gap_of<false>(ak, m, r.y, (int)(r.w & 0xFFFFu)) : (int)r.w,
+                                  r.y, r.z);
+  }
+  __syncthreads();
+  const int64_t best = max_live(mb, fr, na, lane);
   __syncthreads();
   return best;
 }
@@ -769,21 +721,19 @@ __device__ int64_t device_peak(const Rec *own, int o0, int n1, const Rec *cp, in
 __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0, int64_t nj,
                                                     const Rec *__restrict__ own_all, const Rec *__restrict__ cp_all,
                                                     const int32_t *__restrict__ meta, uint32_t *__restrict__ wk_all,
-                                                    uint64_t *__restrict__ wb_all, int32_t *__restrict__ wc_all,
-                                                    int64_t slot_cap, int64_t *__restrict__ peak,
-                                                    uint8_t *__restrict__ violation) {
-  __shared__ uint32_t s_sk[kCap], s_mk[kCap];
-  __shared__ uint64_t s_sp[kCap], s_fd[kCap];
-  __shared__ int64_t s_mb[kCap];
-  __shared__ int s_gc[kCap + 2];
+                                                    uint64_t *__restrict__ wb_all, int64_t slot_cap,
+                                                    int64_t *__restrict__ peak, uint8_t *__restrict__ violation) {
+  __shared__ uint32_t s_ak[kCap], s_mb[kCap];
+  __shared__ int s_ag[kCap + 2];
+  __shared__ uint16_t s_ai[kCap];
+  __shared__ uint64_t s_fr[kCap];
   const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops];
   const int lane = threadIdx.x;
-  uint32_t *g_sk = wk_all + (int64_t)blockIdx.x * 2 * slot_cap;
-  uint32_t *g_mk = g_sk + slot_cap;
-  uint64_t *g_sp = wb_all + (int64_t)blockIdx.x * 3 * slot_cap;
-  int64_t *g_mb = reinterpret_cast<int64_t *>(g_sp + slot_cap);
-  uint64_t *g_fd = g_sp + 2 * slot_cap;
-  int32_t *g_gc = wc_all + (int64_t)blockIdx.x * (slot_cap + 2);
+  uint32_t *g_ak = wk_all + (int64_t)blockIdx.x * 4 * (slot_cap + 2);
+  int32_t *g_ag = reinterpret_cast<int32_t *>(g_ak + slot_cap + 2);
+  uint32_t *g_ai = g_ak + 2 * (slot_cap + 2);
+  uint32_t *g_mb = g_ak + 3 * (slot_cap + 2);
+  uint64_t *g_fr = wb_all + (int64_t)blockIdx.x * slot_cap;
   for (int64_t j = blockIdx.x; j < nj; j += gridDim.x) {
     const int64_t c = j0 + j;
     if (violation[c] & SS_VIOLATION_INVALID) {
@@ -793,17 +743,17 @@ __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0,
     }
     const Rec *own = own_all + j * N;
     const Rec *cp = cp_all + j * E;
-    const int32_t *m = meta + j * meta_stride(D);
+    const int32_t *mt = meta + j * meta_stride(D);
     uint8_t viol = 0;
     for (int e = 0; e < D; ++e) {
-      const int o0 = m[e], n1 = m[e + 1] - o0;
-      const int c0 = m[D + 1 + e], n4 = m[2 * (D + 1) + e];
+      const int o0 = mt[e], m = mt[e + 1] - o0;
+      const int c0 = mt[D + 1 + e], nc = mt[2 * (D + 1) + e];
       int64_t pk = 0;
-      if (n1 + n4 > 0) {
-        if (n1 + n4 <= kCap && n1 + 2 <= kCap + 2)
-          pk = device_peak(own, o0, n1, cp, c0, n4, s_sk, s_sp, s_gc, s_mk, s_mb, s_fd, lane);
+      if (m + nc > 0) {
+        if (m + nc <= kCap)
+          pk = device_peak(own + o0, m, cp + c0, nc, G.pos_dur != 0, s_ak, s_ag, s_ai, s_mb, s_fr, lane);
         else
-          pk = device_peak(own, o0, n1, cp, c0, n4, g_sk, g_sp, g_gc, g_mk, g_mb, g_fd, lane);
+          pk = device_peak(own + o0, m, cp + c0, nc, G.pos_dur != 0, g_ak, g_ag, g_ai, g_mb, g_fr, lane);
       }
       if (peak && lane == 0) peak[c * D + e] = pk;
       if (pk > G.cap[e]) viol = SS_VIOLATION_MEMORY;
@@ -848,7 +798,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   chunk = std::min<int64_t>(chunk, int64_t(65535) * 64);  // transpose grids index 64-candidate tiles in y
   chunk = std::min<int64_t>(chunk, B);
   // sub-chunk: interval records of each candidate (own N, copies <= E)
-  const int64_t rec_per_cand = (N + E) * (int64_t)sizeof(uint3) + 3 * (D + 1) * 4;
+  const int64_t rec_per_cand = (N + E) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4 + N * 2;
   int64_t sub = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
   sub = std::min<int64_t>(sub, chunk);
   const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
@@ -857,15 +807,15 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
   const size_t sz_pt = align((size_t)chunk * N + 1);
   const size_t sz_fin = align((size_t)chunk * N * 4 + 4);
-  const size_t sz_own = align(((size_t)sub * N + 1) * sizeof(uint3));
-  const size_t sz_cp = align(((size_t)sub * E + 1) * sizeof(uint3));
+  const size_t sz_own = align(((size_t)sub * N + 1) * sizeof(Rec));
+  const size_t sz_cp = align(((size_t)sub * E + 1) * sizeof(Rec));
   const size_t sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
-  const size_t sz_wk = align((size_t)nslots * 2 * slot_cap * 4);
-  const size_t sz_wb = align((size_t)nslots * 3 * slot_cap * 8);
-  const size_t sz_wc = align((size_t)nslots * (slot_cap + 2) * 4);
+  const size_t sz_rank = align(((size_t)sub * N + 1) * 2);
+  const size_t sz_wk = align((size_t)nslots * 4 * (slot_cap + 2) * 4);
+  const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
   void *scratch = nullptr;
   err = hipMallocAsync(&scratch,
-                       sz_pt + 2 * sz_fin + sz_own + sz_cp + sz_meta + sz_wk + sz_wb + sz_wc,
+                       sz_pt + 2 * sz_fin + sz_own + sz_cp + sz_meta + sz_rank + sz_wk + sz_wb,
                        stream);
   if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
@@ -880,9 +830,9 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   auto *own = reinterpret_cast<Rec *>(take(sz_own));
   auto *cp = reinterpret_cast<Rec *>(take(sz_cp));
   auto *meta = reinterpret_cast<int32_t *>(take(sz_meta));
+  auto *rank = reinterpret_cast<uint16_t *>(take(sz_rank));
   auto *wk = reinterpret_cast<uint32_t *>(take(sz_wk));
   auto *wb = reinterpret_cast<uint64_t *>(take(sz_wb));
-  auto *wc = reinterpret_cast<int32_t *>(take(sz_wc));
 
   int rc = SS_OK;
   auto check = [&](const char *what) {
@@ -927,14 +877,14 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
       const int64_t nj = std::min(sub, nb - j0);
       SsTimingRec *ti = ss_timing_start(SS_KERNEL_INTERVALS, stream);
       hipLaunchKernelGGL(fast_intervals, dim3((unsigned)nj), dim3(kWave), 0, stream, G, Pc,
-                         static_cast<const uint32_t *>(fin), j0, own, cp, meta,
+                         static_cast<const uint32_t *>(fin), j0, own, cp, meta, rank,
                          static_cast<const uint8_t *>(violation + b0));
       ss_timing_stop(ti, stream);
       if (!check("fast_intervals launch")) break;
       SsTimingRec *tm = ss_timing_start(SS_KERNEL_MEMORY, stream);
       hipLaunchKernelGGL(fast_peaks, dim3((unsigned)std::min<int64_t>(nj, nslots)), dim3(kWave), 0, stream, G, j0, nj,
                          static_cast<const Rec *>(own), static_cast<const Rec *>(cp),
-                         static_cast<const int32_t *>(meta), wk, wb, wc, slot_cap, peak ? peak + b0 * D : nullptr,
+                         static_cast<const int32_t *>(meta), wk, wb, slot_cap, peak ? peak + b0 * D : nullptr,
                          violation + b0);
       ss_timing_stop(tm, stream);
       if (!check("fast_peaks launch")) break;

@@ -23,8 +23,8 @@ struct GmgView {
   const uint8_t *link_class;  // [D][D]
   // 32-bit copies of every time quantity, present when the loader proved the
   // whole time horizon (all starts, finishes, frees and finite slice bounds)
-  // stays below 2^32 - 1, there are at most 65535 ops and every output size
-  // fits in 32 bits; the open slice end becomes 0xFFFFFFFF.  The 32-bit slice
+  // stays below 2^32 - 1, there are at most 65535 ops and 65535 edges and
+  // every output size fits in 32 bits; the open slice end becomes 0xFFFFFFFF.  The 32-bit slice
   // arrays hold one spare entry past the last slice.
   int32_t time32;
   const uint32_t *dur32, *xfer32, *slice_begin32, *slice_end32, *release32;
@@ -33,6 +33,12 @@ struct GmgView {
   // per field (meta_stride = N rounded up to 64 plus one spare block, >= 128).
   const uint32_t *op_meta;
   int32_t meta_stride;
+  int32_t pos_dur;  // every duration is at least 1 (an op's start precedes its finish)
+  // link classes as bits (two classes at most): bit b of word [a][b >> 5] is
+  // link_class[a][b]; link_words = ceil(n_dev / 32).  Null with more classes.
+  const uint32_t *link_bits;
+  int32_t link_words;
+  const uint32_t *bytes32;  // out_bytes as u32
 };
 
 // Fields of op_meta for op v.  Predecessors beyond the first four and link
