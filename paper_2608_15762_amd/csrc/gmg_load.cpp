@@ -144,9 +144,9 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     for (int64_t v = 0; v < N; ++v) max_bytes = std::max(max_bytes, d->out_bytes[v]);
     const bool time32 =
         horizon < (i128)UINT32_MAX && N <= 65535 && E <= 65535 && max_bytes <= (int64_t)UINT32_MAX;
-    bool pos_dur = true;
-    for (int64_t i = 0; i < N * C; ++i) pos_dur = pos_dur && d->dur[i] >= 1;
-    std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32, meta, lbits, bytes32;
+    std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32, meta, lbits, bytes32, succ2;
+    int64_t max_outdeg = 0;
+    for (int64_t v = 0; v < N; ++v) max_outdeg = std::max<int64_t>(max_outdeg, outdeg[v]);
     const int64_t lwords = (D + 31) / 32;
     const int64_t meta_stride = std::max<int64_t>(128, (N + 63) / 64 * 64 + 64);  // two blocks of 64 past any op
     if (time32) {
@@ -169,6 +169,14 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
       }
       dur32.assign(d->dur, d->dur + N * C);
       bytes32.assign(d->out_bytes, d->out_bytes + N);
+      if (max_outdeg <= 2) {
+        succ2.assign(N, 0xFFFFFFFFu);
+        for (int64_t v = 0; v < N; ++v)
+          for (int64_t q = 0; q < outdeg[v]; ++q) {
+            const uint32_t x = (uint32_t)succ_idx[succ_ptr[v] + q];
+            succ2[v] = q == 0 ? (0xFFFF0000u | x) : ((succ2[v] & 0xFFFFu) | x << 16);
+          }
+      }
       if (K <= 2) {
         lbits.assign((size_t)D * lwords, 0u);
         for (int64_t a = 0; a < D; ++a)
@@ -204,7 +212,8 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     const size_t o_dl = pk.add(d->deadline, R * sizeof(int64_t));
     const size_t o_link = pk.add(d->link_class, D * D);
     const size_t o_dur32 = pk.add(dur32), o_xfer32 = pk.add(xfer32), o_sb32 = pk.add(sb32), o_se32 = pk.add(se32),
-                 o_rel32 = pk.add(rel32), o_meta = pk.add(meta), o_lbits = pk.add(lbits), o_b32 = pk.add(bytes32);
+                 o_rel32 = pk.add(rel32), o_meta = pk.add(meta), o_lbits = pk.add(lbits), o_b32 = pk.add(bytes32),
+                 o_succ2 = pk.add(succ2);
     pk.add(nullptr, 256);  // tail padding
 
     ss_gmg *g = new ss_gmg();
@@ -252,10 +261,10 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     V.release32 = reinterpret_cast<const uint32_t *>(base + o_rel32);
     V.op_meta = reinterpret_cast<const uint32_t *>(base + o_meta);
     V.meta_stride = (int32_t)meta_stride;
-    V.pos_dur = pos_dur ? 1 : 0;
     V.link_bits = lbits.empty() ? nullptr : reinterpret_cast<const uint32_t *>(base + o_lbits);
     V.link_words = (int32_t)lwords;
     V.bytes32 = reinterpret_cast<const uint32_t *>(base + o_b32);
+    V.succ2 = succ2.empty() ? nullptr : reinterpret_cast<const uint32_t *>(base + o_succ2);
     g->n_ops = N;
     g->n_edges = E;
     g->n_dev = D;
@@ -265,6 +274,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     g->max_slices = max_slices;
     g->horizon = (int64_t)horizon;
     for (int64_t v = 0; v < N; ++v) g->max_indeg = std::max<int64_t>(g->max_indeg, d->pred_ptr[v + 1] - d->pred_ptr[v]);
+    g->max_outdeg = max_outdeg;
     *out = g;
     return SS_OK;
   } catch (const std::bad_alloc &) {

@@ -361,14 +361,14 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
 // Residency intervals (Sec. 3.3.2) are written by fast_intervals into
 // per-device buckets and evaluated by fast_peaks.
 //   own record  {start, free time (kInf32: never), bytes, free locator}
-//   copy record {allocation time, free time, bytes, alloc window << 16 | free locator}
+//   copy record {allocation time, free time, bytes, alloc window << 16 | free gap}
 // A device's own starts S[0..m) (its ops in index order) are sorted, and
 // every event is placed by how many own starts precede it, its gap:
 //   allocation of a copy at time c:  #{k : S[k] <= c}
 //   free at time h:                  #{k : S[k] <  h}
 // (frees precede allocations at equal times: intervals are half-open).  The
 // writer knows each gap exactly or nearly: a free at the finish of a local
-// op of rank k (all durations positive) has gap k + 1; a copy is allocated
+// op of rank k has gap k + 1 (durations are at least 1); a copy is allocated
 // shortly before its first consumer of rank k starts, so its gap lies in
 // [k-3, k+1]; a transfer-bound free of an op of rank k lies in [k+1, k+5].
 // A locator holds the exact gap, or (kLocWindow) the start L of a window
@@ -408,7 +408,7 @@ __device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32
       loc = loc_window(rv + 1);
     } else {
       F = L;
-      loc = G.pos_dur ? (uint32_t)(rl + 1) : loc_window(rl - 3);
+      loc = (uint32_t)(rl + 1);
     }
   }
   own[own_pos] = Rec{f - (C == 1 ? G.dur32[v] : G.dur32[v * C + G.dev_class[d]]), F, b, loc};
@@ -427,8 +427,7 @@ __device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32
       if (prow[x] == e) y = x;
     }
     const int ra = rk[xf], ry = rk[y];
-    const uint32_t floc = G.pos_dur ? (uint32_t)(ry + 1) : (uint32_t)max(ry - 3, 0);
-    cp[atomicAdd(&cfill[e], 1)] = Rec{f, frow[y], b, (uint32_t)max(ra - 3, 0) << 16 | floc};
+    cp[atomicAdd(&cfill[e], 1)] = Rec{f, frow[y], b, (uint32_t)max(ra - 3, 0) << 16 | (uint32_t)(ry + 1)};
   }
 }
 
@@ -478,42 +477,65 @@ __device__ __forceinline__ void chunk_groups(int d, bool active, int val, int la
 __device__ __forceinline__ int meta_stride(int D) { return 3 * (D + 1); }
 
 // One wave per candidate.  Pass A ranks every op among the ops of its device
-// (rank table rk) and counts ops and in-degrees per device; pass B writes the
-// records.
+// (rank table rk) and counts ops and in-degrees per device (copies landing on
+// a device are at most its summed in-degree); pass B writes the records.
+// Each candidate's own and copy regions hold one spare record past the end
+// (index N, resp. E) that absorbs the stores of lanes with nothing to write.
+//
+// kFast (one device class, at most two link classes, at most two successors
+// per op): pass B is branch free, reads each op's successors from succ2, and
+// software-pipelines the chunks of 64 ops: while chunk i is evaluated, the
+// op fields of chunk i+1 are in flight, and its successors' fields are
+// requested as soon as those arrive.
+struct IvOp {  // fields of the lane's op
+  uint32_t d, rv, f, b, w, s2, x0, x1;
+};
+struct IvSucc {  // device, finish and rank of the first two successors
+  uint32_t dx0, dx1, fx0, fx1, rx0, rx1;
+};
+
+template <bool kFast>
 __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const uint8_t *__restrict__ P,
                                                         const uint32_t *__restrict__ fin, int64_t j0,
                                                         Rec *__restrict__ own_all, Rec *__restrict__ cp_all,
                                                         int32_t *__restrict__ meta, uint16_t *__restrict__ rank_all,
                                                         const uint8_t *__restrict__ violation) {
-  __shared__ int own_off[257], cp_off[257], cfill[256], base[256];
-  const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops];
+  __shared__ int own_off[257], cp_off[257], cfill[256], base[256], nocopy[kWave];
+  const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops], K = G.n_link;
   const int lane = threadIdx.x;
   const int64_t j = blockIdx.x, c = j0 + j;
   if (violation[c] & SS_VIOLATION_INVALID) return;
   const uint8_t *prow = P + c * N;
   const uint32_t *frow = fin + c * N;
   uint16_t *rk = rank_all + j * N;
-  Rec *own = own_all + j * N;
-  Rec *cp = cp_all + j * E;
+  Rec *own = own_all + j * (int64_t)(N + 1);
+  Rec *cp = cp_all + j * (int64_t)(E + 1);
+  const uint32_t *indeg_f = G.op_meta + (int64_t)kMetaReq * G.meta_stride;  // predecessor count << 16
   for (int d = lane; d < D; d += kWave) {
     cfill[d] = 0;
     base[d] = 0;
   }
   __syncthreads();
-  for (int v0 = 0; v0 < N; v0 += kWave) {
-    const int v = v0 + lane;
-    const bool act = v < N;
-    const int d = act ? prow[v] : 0;
-    const int indeg = act ? G.pred_ptr[v + 1] - G.pred_ptr[v] : 0;
-    int rank, gd, gcnt, gsum;
-    chunk_groups(d, act, indeg, lane, rank, gd, gcnt, gsum);
-    if (act) rk[v] = (uint16_t)(base[d] + rank);
-    __syncthreads();
-    if (gd >= 0) {
-      base[gd] += gcnt;
-      cfill[gd] += gsum;  // copies landing on a device <= its summed in-degree
+  {
+    int vn = min(lane, N - 1);
+    uint32_t dn = N > 0 ? prow[vn] : 0, in = N > 0 ? indeg_f[vn] : 0;
+    for (int v0 = 0; v0 < N; v0 += kWave) {
+      const int v = v0 + lane;
+      const bool act = v < N;
+      const int d = (int)dn, indeg = act ? (int)(in >> 16) : 0;
+      vn = min(v0 + kWave + lane, N - 1);  // next chunk, in flight meanwhile
+      dn = prow[vn];
+      in = indeg_f[vn];
+      int rank, gd, gcnt, gsum;
+      chunk_groups(d, act, indeg, lane, rank, gd, gcnt, gsum);
+      if (act) rk[v] = (uint16_t)(base[d] + rank);
+      __syncthreads();
+      if (gd >= 0) {
+        base[gd] += gcnt;
+        cfill[gd] += gsum;
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
   if (lane == 0) {
     int so = 0, sc = 0;
@@ -528,11 +550,68 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
     cp_off[D] = sc;
   }
   __syncthreads();  // also orders the rank-table stores before the loads below
-  for (int v0 = 0; v0 < N; v0 += kWave) {
-    const int v = v0 + lane;
-    if (v < N) {
-      const int d = prow[v], rv = rk[v];
-      op_intervals(G, prow, frow, rk, v, d, rv, own_off[d] + rv, cfill, own, cp);
+  if (!kFast) {
+    for (int v0 = 0; v0 < N; v0 += kWave) {
+      const int v = v0 + lane;
+      if (v < N) {
+        const int d = prow[v], rv = rk[v];
+        op_intervals(G, prow, frow, rk, v, d, rv, own_off[d] + rv, cfill, own, cp);
+      }
+    }
+  } else if (N > 0) {
+    auto load_op = [&](int v) -> IvOp {
+      IvOp a;
+      a.d = prow[v];
+      a.rv = rk[v];
+      a.f = frow[v];
+      a.b = G.bytes32[v];
+      a.w = G.dur32[v];
+      a.s2 = G.succ2[v];
+      a.x0 = G.xfer32[v * K];
+      a.x1 = G.xfer32[v * K + K - 1];
+      return a;
+    };
+    auto load_succ = [&](const IvOp &a, int v) -> IvSucc {
+      const uint32_t x0 = a.s2 & 0xFFFFu, x1 = a.s2 >> 16;
+      const int y0 = x0 == 0xFFFFu ? v : (int)x0, y1 = x1 == 0xFFFFu ? v : (int)x1;
+      return IvSucc{prow[y0], prow[y1], frow[y0], frow[y1], rk[y0], rk[y1]};
+    };
+    nocopy[lane] = 0;
+    int vq = min(lane, N - 1);
+    IvOp a = load_op(vq);
+    IvSucc sc = load_succ(a, vq);
+    for (int v0 = 0; v0 < N; v0 += kWave) {
+      const bool act = v0 + lane < N;
+      const int vn = min(v0 + kWave + lane, N - 1);
+      const IvOp an = load_op(vn);  // next chunk
+      const uint32_t d = a.d, x0 = a.s2 & 0xFFFFu, x1 = a.s2 >> 16;
+      const bool has0 = x0 != 0xFFFFu, has1 = x1 != 0xFFFFu;
+      const bool loc0 = has0 && sc.dx0 == d, loc1 = has1 && sc.dx1 == d;
+      const uint32_t X0 = link_bit(G, d, sc.dx0) ? a.x1 : a.x0;  // transfer to each successor's device
+      const uint32_t X1 = link_bit(G, d, sc.dx1) ? a.x1 : a.x0;
+      // own output: local consumers finish in index order, so the last one finishes last
+      uint32_t L = a.f, rl = a.rv, A = 0;
+      L = loc0 ? sc.fx0 : L;
+      rl = loc0 ? sc.rx0 : rl;
+      L = loc1 ? sc.fx1 : L;
+      rl = loc1 ? sc.rx1 : rl;
+      A = (has0 && !loc0) ? umax32(A, a.f + X0) : A;
+      A = (has1 && !loc1) ? umax32(A, a.f + X1) : A;
+      const bool arrive = A > L;
+      const uint32_t F = !has0 ? kInf32 : arrive ? A : L;
+      const uint32_t loc = !has0 ? 0u : arrive ? loc_window((int)a.rv + 1) : rl + 1;
+      own[act ? own_off[d] + (int)a.rv : N] = Rec{a.f - a.w, F, a.b, loc};
+      // copies: one per remote successor device
+      const bool same = has1 && sc.dx1 == sc.dx0;
+      const bool c0 = act && has0 && !loc0 && a.b != 0;
+      const bool c1 = act && has1 && !loc1 && !same && a.b != 0;
+      const int s0 = atomicAdd(c0 ? &cfill[sc.dx0] : &nocopy[lane], c0 ? 1 : 0);
+      const int s1 = atomicAdd(c1 ? &cfill[sc.dx1] : &nocopy[lane], c1 ? 1 : 0);
+      const uint32_t ry0 = same ? sc.rx1 : sc.rx0, hi0 = same ? sc.fx1 : sc.fx0;
+      cp[c0 ? s0 : E] = Rec{a.f, hi0, a.b, (uint32_t)max((int)sc.rx0 - 3, 0) << 16 | (ry0 + 1)};
+      cp[c1 ? s1 : E] = Rec{a.f, sc.fx1, a.b, (uint32_t)max((int)sc.rx1 - 3, 0) << 16 | (sc.rx1 + 1)};
+      sc = load_succ(an, vn);
+      a = an;
     }
   }
   __syncthreads();
@@ -636,8 +715,8 @@ __device__ int64_t max_live(IP alloc, FP freed, int n, int lane) {
 //   ai  per grouped copy time, the copy's index (ties between equal times)
 //   mb  allocation bytes by merged position; fr bytes freed before each
 template <class UP, class IP, class HP, class FP>
-__device__ int64_t device_peak(const Rec *own, int m, const Rec *cp, int nc, bool pos_dur, UP ak, IP ag, HP ai, UP mb,
-                               FP fr, int lane) {
+__device__ int64_t device_peak(const Rec *own, int m, const Rec *cp, int nc, UP ak, IP ag, HP ai, UP mb, FP fr,
+                               int lane) {
   constexpr int kB = 8;
   const int na = m + nc;
   UP bt = ak + m;                                       // grouped copy times
@@ -704,8 +783,7 @@ __device__ int64_t device_peak(const Rec *own, int m, const Rec *cp, int nc, boo
       rank += (t < r.x || (t == r.x && (int)ai[z] < i)) ? 1 : 0;
     }
     mb[g + s0 + rank] = r.z;
-    const int fl = (int)(r.w & 0xFFFFu);
-    place_free(pos_dur ? fl : gap_of<false>(ak, m, r.y, fl), r.y, r.z);
+    place_free((int)(r.w & 0xFFFFu), r.y, r.z);
   }
   for (int k = lane; k < m; k += kWave) {
     const Rec r = own[k];
@@ -741,8 +819,8 @@ __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0,
         for (int d = lane; d < D; d += kWave) peak[c * D + d] = 0;
       continue;
     }
-    const Rec *own = own_all + j * N;
-    const Rec *cp = cp_all + j * E;
+    const Rec *own = own_all + j * (int64_t)(N + 1);
+    const Rec *cp = cp_all + j * (int64_t)(E + 1);
     const int32_t *mt = meta + j * meta_stride(D);
     uint8_t viol = 0;
     for (int e = 0; e < D; ++e) {
@@ -751,9 +829,9 @@ __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0,
       int64_t pk = 0;
       if (m + nc > 0) {
         if (m + nc <= kCap)
-          pk = device_peak(own + o0, m, cp + c0, nc, G.pos_dur != 0, s_ak, s_ag, s_ai, s_mb, s_fr, lane);
+          pk = device_peak(own + o0, m, cp + c0, nc, s_ak, s_ag, s_ai, s_mb, s_fr, lane);
         else
-          pk = device_peak(own + o0, m, cp + c0, nc, G.pos_dur != 0, g_ak, g_ag, g_ai, g_mb, g_fr, lane);
+          pk = device_peak(own + o0, m, cp + c0, nc, g_ak, g_ag, g_ai, g_mb, g_fr, lane);
       }
       if (peak && lane == 0) peak[c * D + e] = pk;
       if (pk > G.cap[e]) viol = SS_VIOLATION_MEMORY;
@@ -791,6 +869,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   err = hipFuncSetAttribute(sched_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
   if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
 
+  const bool iv_fast = g->n_class == 1 && g->n_link <= 2 && g->max_outdeg <= 2;
   // chunk: op-major placements, op-major and row-major finish times
   const int64_t per_cand = N * (1 + 4 + 4);
   int64_t chunk = kScratchBudget / std::max<int64_t>(1, per_cand);
@@ -798,7 +877,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   chunk = std::min<int64_t>(chunk, int64_t(65535) * 64);  // transpose grids index 64-candidate tiles in y
   chunk = std::min<int64_t>(chunk, B);
   // sub-chunk: interval records of each candidate (own N, copies <= E)
-  const int64_t rec_per_cand = (N + E) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4 + N * 2;
+  const int64_t rec_per_cand = (N + E + 2) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4 + N * 2;
   int64_t sub = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
   sub = std::min<int64_t>(sub, chunk);
   const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
@@ -807,8 +886,8 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
   const size_t sz_pt = align((size_t)chunk * N + 1);
   const size_t sz_fin = align((size_t)chunk * N * 4 + 4);
-  const size_t sz_own = align(((size_t)sub * N + 1) * sizeof(Rec));
-  const size_t sz_cp = align(((size_t)sub * E + 1) * sizeof(Rec));
+  const size_t sz_own = align((size_t)sub * (N + 1) * sizeof(Rec));
+  const size_t sz_cp = align((size_t)sub * (E + 1) * sizeof(Rec));
   const size_t sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
   const size_t sz_rank = align(((size_t)sub * N + 1) * 2);
   const size_t sz_wk = align((size_t)nslots * 4 * (slot_cap + 2) * 4);
@@ -876,9 +955,14 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
     for (int64_t j0 = 0; j0 < nb && rc == SS_OK; j0 += sub) {
       const int64_t nj = std::min(sub, nb - j0);
       SsTimingRec *ti = ss_timing_start(SS_KERNEL_INTERVALS, stream);
-      hipLaunchKernelGGL(fast_intervals, dim3((unsigned)nj), dim3(kWave), 0, stream, G, Pc,
-                         static_cast<const uint32_t *>(fin), j0, own, cp, meta, rank,
-                         static_cast<const uint8_t *>(violation + b0));
+      if (iv_fast)
+        hipLaunchKernelGGL(fast_intervals<true>, dim3((unsigned)nj), dim3(kWave), 0, stream, G, Pc,
+                           static_cast<const uint32_t *>(fin), j0, own, cp, meta, rank,
+                           static_cast<const uint8_t *>(violation + b0));
+      else
+        hipLaunchKernelGGL(fast_intervals<false>, dim3((unsigned)nj), dim3(kWave), 0, stream, G, Pc,
+                           static_cast<const uint32_t *>(fin), j0, own, cp, meta, rank,
+                           static_cast<const uint8_t *>(violation + b0));
       ss_timing_stop(ti, stream);
       if (!check("fast_intervals launch")) break;
       SsTimingRec *tm = ss_timing_start(SS_KERNEL_MEMORY, stream);

@@ -33,12 +33,13 @@ struct GmgView {
   // per field (meta_stride = N rounded up to 64 plus one spare block, >= 128).
   const uint32_t *op_meta;
   int32_t meta_stride;
-  int32_t pos_dur;  // every duration is at least 1 (an op's start precedes its finish)
   // link classes as bits (two classes at most): bit b of word [a][b >> 5] is
   // link_class[a][b]; link_words = ceil(n_dev / 32).  Null with more classes.
   const uint32_t *link_bits;
   int32_t link_words;
   const uint32_t *bytes32;  // out_bytes as u32
+  // first two successors of each op as u16 (0xFFFF: none), when no op has more
+  const uint32_t *succ2;
 };
 
 // Fields of op_meta for op v.  Predecessors beyond the first four and link
@@ -60,6 +61,7 @@ struct ss_gmg {
   int64_t max_slices = 0;  // largest slice count of any device
   int64_t horizon = 0;     // loader's upper bound on every simulated time
   int64_t max_indeg = 0;   // largest predecessor count of any op
+  int64_t max_outdeg = 0;  // largest successor count of any op
   void *dev_mem = nullptr;
   GmgView view{};
 };

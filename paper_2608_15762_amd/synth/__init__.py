@@ -540,17 +540,22 @@ def random_gmg(seed: int, n_ops: int, n_dev: int, n_req: int = 1, edge_p: float 
                n_slices: int = 3, n_class: int = 1, n_link: int = 1, max_dur: int = 40, max_bytes: int = 1000,
                zero_bytes_p: float = 0.1, slice_scale: int = 60, open_only: bool = False,
                cap_scale: int | None = None, lat_max: int = 3, bw_max: int = 50, rel_max: int = 0,
-               cross_req_p: float = 0.1) -> Gmg:
+               cross_req_p: float = 0.1, max_outdeg: int | None = None) -> Gmg:
     """A small random GMG: a random DAG over ``n_ops`` ops (edges u -> v with
-    v - max_span <= u < v), random slices, link classes, durations and sizes."""
+    v - max_span <= u < v), random slices, link classes, durations and sizes.
+    ``max_outdeg`` drops edges that would give an op more successors (it
+    changes no draw)."""
     st = Stream(draw(0xF022 + seed, 1))
     U = st.uniform_int
     op_req = [U(0, n_req - 1) for _ in range(n_ops)]
     edges = []
+    outdeg = [0] * n_ops
     for v in range(n_ops):
         for u in range(max(0, v - max_span), v):
             if st.unit() < edge_p and (op_req[u] == op_req[v] or st.unit() < cross_req_p):
-                edges.append((u, v))
+                if max_outdeg is None or outdeg[u] < max_outdeg:
+                    edges.append((u, v))
+                    outdeg[u] += 1
     dur = [[U(1, max_dur) for _ in range(n_class)] for _ in range(n_ops)]
     ob = [0 if st.unit() < zero_bytes_p else U(1, max_bytes) for _ in range(n_ops)]
     slices = []

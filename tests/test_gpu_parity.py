@@ -87,6 +87,34 @@ def test_fuzz_parity(dev, path, seed):
     assert (got["violation"] == 4).sum() >= 1
 
 
+# Graphs inside the limits of the branch-free interval writer (one device
+# class, at most two link classes and two successors per op), with zero-byte
+# outputs, zero transfer latencies, far-reaching edges and ragged op counts.
+FAST_WRITER = [dict(n_ops=n, n_dev=D, n_req=R, n_slices=S, n_link=K, zero_bytes_p=0.2, max_outdeg=2, cap_scale=cs,
+                    max_span=sp, edge_p=ep, max_dur=md)
+               for n, D, R, S, K, cs, sp, ep, md in [
+                   (64, 3, 1, 3, 1, 3000, 6, 0.4, 40), (130, 5, 2, 4, 2, 3000, 6, 0.5, 3),
+                   (257, 8, 3, 5, 2, 6000, 12, 0.3, 40), (700, 16, 4, 6, 2, 20000, 40, 0.1, 2),
+                   (1500, 40, 4, 3, 2, 50000, 200, 0.02, 40), (1025, 2, 2, 8, 2, 20000, 4, 0.6, 1)]]
+
+
+@pytest.mark.parametrize("seed", range(len(FAST_WRITER)))
+def test_fast_writer_parity(dev, path, seed):
+    kw = FAST_WRITER[seed]
+    print(f"fast writer {seed}: {kw}", flush=True)
+    g = synth.random_gmg(100 + seed, **kw)
+    assert np.bincount(np.asarray(g.pred_idx), minlength=g.n_ops).max() <= 2
+    st = synth.Stream(seed + 777)
+    B = 131
+    P = np.array([[st.uniform_int(0, g.n_dev - 1) for _ in range(g.n_ops)] for _ in range(B)], np.uint8)
+    P[1::3] = P[0]  # some candidates keep whole chains on one device
+    for b in range(0, B, 29):
+        P[b, st.uniform_int(0, g.n_ops - 1)] = g.n_dev + st.uniform_int(0, 255 - g.n_dev)
+    ref = oracle.simulate_batch(g, P)
+    got = gpu_run(ss.Gmg(g), P, dev)
+    assert_same(got, ref, label=f"fast writer {seed}")
+
+
 def test_nullable_outputs_and_empty_batch(dev, path):
     g = synth.build_gmg(0)
     h = ss.Gmg(g)

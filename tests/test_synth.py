@@ -117,3 +117,11 @@ def test_tight_capacity_constant_reproduces():
     mod = importlib.util.module_from_spec(spec)
     spec.loader.exec_module(mod)
     assert mod.compute() == synth.TIGHT_CAP_BYTES
+
+
+def test_random_gmg_outdeg_cap():
+    g = synth.random_gmg(5, n_ops=400, n_dev=4, edge_p=0.6, max_span=10, max_outdeg=2)
+    assert np.bincount(np.asarray(g.pred_idx), minlength=g.n_ops).max() <= 2
+    base = synth.random_gmg(5, n_ops=400, n_dev=4, edge_p=0.6, max_span=10)
+    assert base.n_edges > g.n_edges
+    assert np.array_equal(base.dur, g.dur)  # the cap changes no draw
