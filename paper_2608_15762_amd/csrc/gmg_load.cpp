@@ -142,9 +142,12 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     // 32-bit time path: every time the simulation can produce is <= horizon
     int64_t max_bytes = 0;
     for (int64_t v = 0; v < N; ++v) max_bytes = std::max(max_bytes, d->out_bytes[v]);
-    const bool time32 =
-        horizon < (i128)UINT32_MAX && N <= 65535 && E <= 65535 && max_bytes <= (int64_t)UINT32_MAX;
-    std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32, meta, lbits, bytes32, succ2;
+    const bool time32 = horizon < (i128)UINT32_MAX && N <= 65535 && E <= 65535 && max_slices <= 65535 &&
+                        max_bytes <= (int64_t)UINT32_MAX;
+    std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32, meta, lbits, bytes32, succ2, lutk, lutw;
+    std::vector<uint8_t> lgrp;
+    int32_t lsame = 0;
+    int64_t lut_nb = 0, lut_shift = 0;
     int64_t max_outdeg = 0;
     for (int64_t v = 0; v < N; ++v) max_outdeg = std::max<int64_t>(max_outdeg, outdeg[v]);
     const int64_t lwords = (D + 31) / 32;
@@ -178,6 +181,35 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
           }
       }
       if (K <= 2) {
+        // device groups: join devices linked by class `same`, then check that
+        // every distinct pair's class is `same` exactly within a group
+        for (int same = 0; same < 2 && lgrp.empty(); ++same) {
+          std::vector<int64_t> root(D);
+          for (int64_t a = 0; a < D; ++a) root[a] = a;
+          auto find = [&](int64_t a) {
+            while (root[a] != a) a = root[a] = root[root[a]];
+            return a;
+          };
+          for (int64_t a = 0; a < D; ++a)
+            for (int64_t b = 0; b < D; ++b)
+              if (a != b && d->link_class[a * D + b] == same) root[find(a)] = find(b);
+          std::vector<int64_t> id(D, -1);
+          std::vector<uint8_t> grp(D);
+          int64_t ng = 0;
+          for (int64_t a = 0; a < D; ++a) {
+            const int64_t r = find(a);
+            if (id[r] < 0) id[r] = ng++;
+            grp[a] = (uint8_t)id[r];
+          }
+          bool ok = ng <= 256;
+          for (int64_t a = 0; a < D && ok; ++a)
+            for (int64_t b = 0; b < D && ok; ++b)
+              if (a != b) ok = (d->link_class[a * D + b] == same) == (grp[a] == grp[b]);
+          if (ok) {
+            lgrp = grp;
+            lsame = same;
+          }
+        }
         lbits.assign((size_t)D * lwords, 0u);
         for (int64_t a = 0; a < D; ++a)
           for (int64_t b = 0; b < D; ++b)
@@ -187,9 +219,33 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
       rel32.assign(d->release, d->release + R);
       sb32.assign(S + 1, UINT32_MAX);  // spare entry: read ahead, never used
       se32.assign(S + 1, UINT32_MAX);
+
       for (int64_t k = 0; k < S; ++k) {
         sb32[k] = (uint32_t)d->slice_begin[k];
         se32[k] = d->slice_end[k] == SS_TIME_INF ? UINT32_MAX : (uint32_t)d->slice_end[k];
+      }
+      // time -> slice lookup: about 128K buckets in all (at least 64 per device)
+      uint32_t max_end = 0;
+      for (int64_t k = 0; k < S; ++k)
+        if (se32[k] != UINT32_MAX) max_end = std::max(max_end, se32[k]);
+      const int64_t nb_target = std::max<int64_t>(64, 131072 / D);
+      while (((int64_t)max_end >> lut_shift) + 2 > nb_target) ++lut_shift;
+      lut_nb = ((int64_t)max_end >> lut_shift) + 2;
+      lutk.assign((size_t)D * lut_nb, 0u);
+      lutw.assign((size_t)D * lut_nb * 4, UINT32_MAX);
+      for (int64_t x = 0; x < D; ++x) {
+        const int64_t a = d->slice_ptr[x], b = d->slice_ptr[x + 1];
+        int64_t k = 0;
+        for (int64_t bk = 0; bk < lut_nb; ++bk) {
+          const uint64_t t0 = (uint64_t)bk << lut_shift;
+          while (a + k < b - 1 && (uint64_t)se32[a + k] < t0) ++k;  // the last slice is open
+          const size_t e = (size_t)(x * lut_nb + bk);
+          lutk[e] = (uint32_t)k;
+          lutw[4 * e] = sb32[a + k];
+          lutw[4 * e + 1] = se32[a + k];
+          lutw[4 * e + 2] = sb32[a + k + 1];  // spare entry past the last slice
+          lutw[4 * e + 3] = se32[a + k + 1];
+        }
       }
     }
 
@@ -213,7 +269,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     const size_t o_link = pk.add(d->link_class, D * D);
     const size_t o_dur32 = pk.add(dur32), o_xfer32 = pk.add(xfer32), o_sb32 = pk.add(sb32), o_se32 = pk.add(se32),
                  o_rel32 = pk.add(rel32), o_meta = pk.add(meta), o_lbits = pk.add(lbits), o_b32 = pk.add(bytes32),
-                 o_succ2 = pk.add(succ2);
+                 o_succ2 = pk.add(succ2), o_lutk = pk.add(lutk), o_lutw = pk.add(lutw), o_lgrp = pk.add(lgrp);
     pk.add(nullptr, 256);  // tail padding
 
     ss_gmg *g = new ss_gmg();
@@ -265,6 +321,12 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     V.link_words = (int32_t)lwords;
     V.bytes32 = reinterpret_cast<const uint32_t *>(base + o_b32);
     V.succ2 = succ2.empty() ? nullptr : reinterpret_cast<const uint32_t *>(base + o_succ2);
+    V.link_grp = lgrp.empty() ? nullptr : reinterpret_cast<const uint8_t *>(base + o_lgrp);
+    V.link_same = lsame;
+    V.lut_k = reinterpret_cast<const uint32_t *>(base + o_lutk);
+    V.lut_w = reinterpret_cast<const uint4 *>(base + o_lutw);
+    V.lut_nb = (int32_t)lut_nb;
+    V.lut_shift = (int32_t)lut_shift;
     g->n_ops = N;
     g->n_edges = E;
     g->n_dev = D;

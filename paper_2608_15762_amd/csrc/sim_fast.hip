@@ -6,13 +6,12 @@
 //   fast_schedule one lane per candidate, ops in index order (Sec. 3.3.2-3.3.3).
 //                 Per (device, lane) LDS state laid out [device][lane], so a
 //                 wave's 64 lanes fall in distinct banks whatever device each
-//                 touches: effective clock u32 (= max(last finish, current
-//                 slice start)) and slice cursor u16.  An op first tries the
-//                 current slice; only when it does not fit does the lane walk
-//                 forward through later slices.  While op v is placed, the
-//                 next ops' devices, predecessor values, link classes and
-//                 slice ends are already in flight (a four-stage software
-//                 pipeline).  Finish times are written op-major.
+//                 touches: the device clock (last finish) only.  The idle
+//                 slice that holds an op comes from a per-device time ->
+//                 slice lookup taken two ops ahead at a lower bound of the
+//                 op's finish.  The next ops' devices, predecessor values,
+//                 link classes and lookups are already in flight (a four-
+//                 stage software pipeline).  Finish times are written op-major.
 //   transpose     finish times back to candidate rows
 // then per sub-chunk of candidates:
 //   fast_intervals one wave per candidate, lanes = consecutive ops (coalesced
@@ -106,9 +105,12 @@ struct SchedPipe {
   uint32_t pd[4][kPipePre];      // predecessor devices (raw loads)
   uint32_t lc[4][kPipePre];      // link class between predecessor and target device
   uint32_t wq[4];                // duration on the target device
-  uint32_t cq[4], e0[4], b1[4], e1[4];  // slice cursor, its end, next slice's bounds
+  uint32_t le[4];                // time -> slice lookup entry at a lower bound of the op's finish
+  uint4 lw[4];                   // its {begin, end} of slices lk and lk+1
 };
-template <bool kGeneralLink, bool kOverflow>
+// kLink: 0 = link classes from device groups (LDS), 1 = bit table (two
+// classes), 2 = byte table (more classes).
+template <int kLink, bool kOverflow>
 __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const uint8_t *__restrict__ PT, int64_t nb,
                                                        uint32_t *__restrict__ finT, int64_t *__restrict__ makespan,
                                                        int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
@@ -120,11 +122,13 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   uint32_t *comp = clk + (size_t)D * kWave;                               // [R][64]
   int32_t *sbase = reinterpret_cast<int32_t *>(comp + (size_t)R * kWave);  // [D+1] slice ranges of the devices
   int32_t *dcls = sbase + D + 1;                                          // [D] device class
-  uint16_t *cur = reinterpret_cast<uint16_t *>(dcls + D);                 // [D][64]
+  uint8_t *lgrp = reinterpret_cast<uint8_t *>(dcls + D);                  // [D] link group (kLink 0)
   for (int d = lane; d <= D; d += kWave) {
     sbase[d] = G.slice_ptr[d];
     if (d < D) dcls[d] = G.dev_class[d];
+    if (kLink == 0 && d < D) lgrp[d] = G.link_grp[d];
   }
+  const uint32_t lsame = (uint32_t)G.link_same;
   __syncthreads();
   // Every lane runs (readlane needs the field blocks loaded in all lanes); a
   // lane past the batch end shadows the last candidate, computing and storing
@@ -132,10 +136,7 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   const int64_t c_raw = (int64_t)blockIdx.x * kWave + lane;
   const bool live = c_raw < nb;
   const int64_t c = live ? c_raw : nb - 1;
-  for (int d = 0; d < D; ++d) {
-    clk[d * kWave + lane] = G.slice_begin32[sbase[d]];
-    cur[d * kWave + lane] = 0;
-  }
+  for (int d = 0; d < D; ++d) clk[d * kWave + lane] = G.slice_begin32[sbase[d]];
   for (int r = 0; r < R; ++r) comp[r * kWave + lane] = G.release32[r];
   if (N == 0) {
     if (live) {
@@ -174,7 +175,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     S.dq[q] = load_dev(q < N ? q : N - 1);
-    S.wq[q] = S.cq[q] = S.e0[q] = S.b1[q] = S.e1[q] = 0;
+    S.wq[q] = S.le[q] = 0;
+    S.lw[q] = make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int i = 0; i < kPipePre; ++i) S.pf[q][i] = S.pd[q][i] = S.lc[q][i] = 0;
   }
@@ -187,20 +189,32 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     constexpr int q1 = (decltype(qq)::value + 1) & 3, q2 = (decltype(qq)::value + 2) & 3;
     const int t = min(T + 2, N - 1);  // past the end: computed and never used
     const uint32_t dt = clampD(S.dq[q2]);
-    const uint32_t p01 = meta(kMetaP01, t);
+    const uint32_t p01 = meta(kMetaP01, t), np = meta(kMetaReq, t) >> 16;
+    // lower bound of op t's finish: its release, the predecessors finished by
+    // now (op t-1 is not) with the cheaper link class, the device clock now
+    uint32_t lb = meta(kMetaRel, t);
+    const uint32_t gdt = kLink == 0 ? (uint32_t)lgrp[dt] : 0u;
 #pragma unroll
     for (int i = 0; i < kPipePre; ++i) {
       const int u = (int)pred_of(p01, i);
       const uint32_t du = u == T + 1 ? clampD(S.dq[q1]) : u == T ? h1d : u == T - 1 ? h2d : clampD(S.pd[q2][i]);
-      S.lc[q2][i] = kGeneralLink ? (uint32_t)G.link_class[du * D + dt] : link_bit(G, du, dt);  // zero with one class
+      uint32_t lc;
+      if (kLink == 0) lc = (uint32_t)lgrp[du] == gdt ? lsame : 1u - lsame;
+      else if (kLink == 1) lc = link_bit(G, du, dt);  // zero with one class
+      else lc = G.link_class[du * D + dt];
+      S.lc[q2][i] = lc;
+      const uint32_t fu = u == T ? h1f : u == T - 1 ? h2f : S.pf[q2][i];
+      // transfer time in the bound: exact with device groups, else the
+      // cheapest class (the fields hold classes 0 and 1), else none
+      const uint32_t x0 = meta(kMetaX + 2 * i, t), x1 = meta(kMetaX + 2 * i + 1, t);
+      const uint32_t xm = kLink == 0 ? (lc ? x1 : x0) : kLink == 1 ? min(x0, x1) : 0u;
+      lb = ((uint32_t)i < np && u != T + 1) ? umax32(lb, fu + (du != dt ? xm : 0u)) : lb;
     }
-    const int sb = sbase[dt];
-    const uint32_t k = cur[dt * kWave + lane];
-    S.cq[q2] = k;
-    S.e0[q2] = G.slice_end32[sb + k];
-    S.b1[q2] = G.slice_begin32[sb + k + 1];  // the slice arrays carry one spare entry
-    S.e1[q2] = G.slice_end32[sb + k + 1];
     S.wq[q2] = G.dur32[(int64_t)t * C + dcls[dt]];
+    lb = umax32(lb, clk[(int)dt * kWave + lane]) + (C == 1 ? meta(kMetaDur, t) : 0u);
+    const uint32_t e = dt * (uint32_t)G.lut_nb + (uint32_t)min((int)(lb >> G.lut_shift), G.lut_nb - 1);
+    S.le[q2] = e;
+    S.lw[q2] = G.lut_w[e];
   };
   // Stage T-3 for target op t = T+3: predecessors u <= T-1 (the others are
   // forwarded from the register history when op t runs).
@@ -218,7 +232,6 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   };
 
   uint32_t ms = 0;
-  bool adv_prev = false;  // op T-1 moved its device to a later slice
   uint64_t sum = 0;
   stage2(std::integral_constant<int, 2>(), -2);
   stage2(std::integral_constant<int, 3>(), -1);
@@ -242,7 +255,7 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
       const uint32_t tt = u == T - 1 ? h1f : u == T - 2 ? h2f : u == T - 3 ? h3f : S.pf[q0][i];
       const uint32_t du = u == T - 1 ? h1d : u == T - 2 ? h2d : u == T - 3 ? h3d : clampD(S.pd[q0][i]);
       uint32_t x;
-      if (kGeneralLink) {
+      if (kLink == 2) {
         x = G.xfer32[(int64_t)(u < T ? u : 0) * K + S.lc[q0][i]];
       } else {
         const uint32_t x0 = meta(kMetaX + 2 * i, T), x1 = meta(kMetaX + 2 * i + 1, T);
@@ -268,31 +281,30 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
         ready = umax32(ready, tt);
       }
     }
-    // one op at a time, inside one idle slice: the current slice if the op
-    // fits there, else the first later slice that holds it
+    // One op at a time, in the first idle slice that holds it from its ready
+    // time and the device clock on.  Slices before lk end before the lookup
+    // bucket starts, hence before any finish the op can have; slices that
+    // end before the clock cannot hold it either (durations are >= 1), so
+    // the answer is the first of lk, lk+1, ... that fits, almost always one
+    // of the two whose bounds are already in registers.
     s = umax32(s, ready);
-    const bool stale = adv_prev && h1d == d;  // op T-1 advanced this device after the prefetch
-    bool adv = false;
-    if (stale || s + w > S.e0[q0]) {
-      int k;
-      const uint32_t t1 = umax32(s, S.b1[q0]);
-      if (!stale && t1 + w <= S.e1[q0]) {
+    {
+      const uint4 lw = S.lw[q0];
+      const uint32_t t0 = umax32(s, lw.x), t1 = umax32(s, lw.z);
+      if (t0 + w <= lw.y) {
+        s = t0;
+      } else if (t1 + w <= lw.w) {
         s = t1;
-        k = (int)S.cq[q0] + 1;
       } else {
         const int sb = sbase[d];
-        k = stale ? (int)cur[slot] : (int)S.cq[q0] + 2;
-        for (;;) {
+        for (int k = (int)G.lut_k[S.le[q0]] + 2;; ++k) {
           const uint32_t t = umax32(s, G.slice_begin32[sb + k]);
           if (t + w <= G.slice_end32[sb + k]) {
             s = t;
             break;
           }
-          ++k;
         }
       }
-      adv = true;
-      cur[slot] = (uint16_t)k;
     }
     const uint32_t f = s + w;
     clk[slot] = f;
@@ -306,7 +318,6 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     h2d = h1d;
     h1f = f;
     h1d = d;
-    adv_prev = adv;
     stage2(qq, T);
     stage3(qq, T);
     S.dq[q0] = load_dev(min(T + 4, N - 1));
@@ -848,7 +859,8 @@ int hip_fail(hipError_t err, const char *what) {
 }  // namespace
 
 size_t ss_fast_schedule_lds(const ss_gmg *g) {
-  return (size_t)g->n_dev * kWave * (4 + 2) + (size_t)g->n_req * kWave * 4 + (size_t)(g->n_dev + 1) * 8;
+  return (size_t)g->n_dev * kWave * 4 + (size_t)g->n_req * kWave * 4 + (size_t)(g->n_dev + 1) * 8 +
+         (size_t)(g->n_dev + 3) / 4 * 4;
 }
 
 int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
@@ -859,13 +871,16 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   int cus = 0;
   hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
-  // kernel variant: link classes beyond two go through xfer32; in-degrees above
-  // the pipelined count go through the predecessor CSR
-  const bool general_link = g->n_link > 2, overflow = g->max_indeg > kPipePre;
-  const void *sched_fn = general_link ? (overflow ? reinterpret_cast<const void *>(&fast_schedule<true, true>)
-                                                  : reinterpret_cast<const void *>(&fast_schedule<true, false>))
-                                      : (overflow ? reinterpret_cast<const void *>(&fast_schedule<false, true>)
-                                                  : reinterpret_cast<const void *>(&fast_schedule<false, false>));
+  // kernel variant: link classes from device groups, a bit table or (more
+  // than two classes) xfer32; in-degrees above the pipelined count go
+  // through the predecessor CSR
+  const int link_mode = G.link_grp ? 0 : g->n_link <= 2 ? 1 : 2;
+  const bool overflow = g->max_indeg > kPipePre;
+  const void *const sched_fns[3][2] = {
+      {reinterpret_cast<const void *>(&fast_schedule<0, false>), reinterpret_cast<const void *>(&fast_schedule<0, true>)},
+      {reinterpret_cast<const void *>(&fast_schedule<1, false>), reinterpret_cast<const void *>(&fast_schedule<1, true>)},
+      {reinterpret_cast<const void *>(&fast_schedule<2, false>), reinterpret_cast<const void *>(&fast_schedule<2, true>)}};
+  const void *sched_fn = sched_fns[link_mode][overflow ? 1 : 0];
   err = hipFuncSetAttribute(sched_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
   if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
 

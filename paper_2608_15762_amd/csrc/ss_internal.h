@@ -23,8 +23,8 @@ struct GmgView {
   const uint8_t *link_class;  // [D][D]
   // 32-bit copies of every time quantity, present when the loader proved the
   // whole time horizon (all starts, finishes, frees and finite slice bounds)
-  // stays below 2^32 - 1, there are at most 65535 ops and 65535 edges and
-  // every output size fits in 32 bits; the open slice end becomes 0xFFFFFFFF.  The 32-bit slice
+  // stays below 2^32 - 1, there are at most 65535 ops, 65535 edges and 65535
+  // slices per device, and every output size fits in 32 bits; the open slice end becomes 0xFFFFFFFF.  The 32-bit slice
   // arrays hold one spare entry past the last slice.
   int32_t time32;
   const uint32_t *dur32, *xfer32, *slice_begin32, *slice_end32, *release32;
@@ -37,9 +37,20 @@ struct GmgView {
   // link_class[a][b]; link_words = ceil(n_dev / 32).  Null with more classes.
   const uint32_t *link_bits;
   int32_t link_words;
+  // when the link classes follow device groups (two classes at most: one for
+  // every pair in the same group, the other across groups): group id per
+  // device and the class of a same-group pair; null otherwise
+  const uint8_t *link_grp;
+  int32_t link_same;
   const uint32_t *bytes32;  // out_bytes as u32
   // first two successors of each op as u16 (0xFFFF: none), when no op has more
   const uint32_t *succ2;
+  // time -> slice lookup per device, for buckets of 2^lut_shift us: entry
+  // [d][b] concerns the first slice k of d ending at or after b << lut_shift;
+  // lut_w holds {begin, end} of slices k and k+1, lut_k the device-local k
+  const uint32_t *lut_k;
+  const uint4 *lut_w;
+  int32_t lut_nb, lut_shift;
 };
 
 // Fields of op_meta for op v.  Predecessors beyond the first four and link
