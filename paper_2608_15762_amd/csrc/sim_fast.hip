@@ -15,20 +15,24 @@
 //   transpose     finish times back to candidate rows
 // then per sub-chunk of candidates:
 //   fast_intervals one wave per candidate, lanes = consecutive ops (coalesced
-//                 row reads), almost no LDS so many waves hide the gathers.
-//                 A 64-key sort across the wave groups each chunk of ops by
-//                 device, giving every op its rank among the ops of its device
-//                 (and per-device counts and in-degree sums) without
-//                 same-address atomics.  Writes every residency interval
-//                 (Sec. 3.3.2) into a per-device bucket: own outputs at their
-//                 rank (so a device's own intervals are start-sorted), one copy
-//                 per (output, remote device) in a region bounded by the
-//                 device's summed in-degree.
-//   fast_peaks    one wave per candidate.  Per device: sort only the copy
-//                 allocations (LDS bitonic), merge them with the sorted own
-//                 allocations by binary-search ranks, scatter every free onto
-//                 the first allocation at or after it (frees precede
-//                 allocations at equal times), and take the maximum of
+//                 row reads).  Pass A: a 64-key sort across the wave groups
+//                 each chunk of ops by device, giving every op its rank among
+//                 the ops of its device (a rank table) and per-device counts
+//                 and in-degree sums, without same-address atomics.  Pass B
+//                 writes every residency interval (Sec. 3.3.2) into a per-
+//                 device bucket: own outputs at their rank (so a device's own
+//                 intervals are start-sorted), one copy per (output, remote
+//                 device) in a region bounded by the device's summed in-degree,
+//                 each event tagged with where it falls among the device's own
+//                 starts (exact, or a small window around a known rank).  For
+//                 graphs of out-degree <= 2 pass B is branch free and software-
+//                 pipelined over chunks.
+//   fast_peaks    one wave per candidate, per device: each copy allocation is
+//                 placed between two own starts by six independent LDS probes
+//                 around its window (binary search only when outside), copies
+//                 are grouped by gap and ranked inside it, frees land on the
+//                 first allocation at or after them (frees precede allocations
+//                 at equal times), and one scan gives the maximum of
 //                 allocated-so-far minus freed-so-far over the allocations.
 #include <climits>
 
