@@ -41,14 +41,23 @@
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kCap = 1024;            // allocations of one device evaluated in LDS
+constexpr int kCap = 1024;            // LDS slots of fast_peaks per work array
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per chunk
 constexpr int64_t kRecordBudget = int64_t(12) << 30;   // interval records per sub-chunk
-constexpr int kPeakBlocksPerCU = 7;  // fast_peaks holds about 22 KB of LDS
+constexpr int kPeakBlocksPerCU = 10;  // fast_peaks holds about 16 KB of LDS
 
 __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
 __device__ __forceinline__ int64_t imax64(int64_t a, int64_t b) { return a > b ? a : b; }
+
+// Orders the LDS accesses of a one-wave workgroup at this point.  A wave's LDS
+// operations complete in issue order, so only the compiler must keep accesses
+// on their side; unlike __syncthreads there is no wait for outstanding global
+// memory operations.
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
 
 // ------------------------------------------------------------------ transpose
 // 64 x 64 tiles through LDS: both the read and the write are coalesced.
@@ -530,7 +539,7 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
     cfill[d] = 0;
     base[d] = 0;
   }
-  __syncthreads();
+  wave_lds_fence();
   {
     int vn = min(lane, N - 1);
     uint32_t dn = N > 0 ? prow[vn] : 0, in = N > 0 ? indeg_f[vn] : 0;
@@ -544,12 +553,12 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       int rank, gd, gcnt, gsum;
       chunk_groups(d, act, indeg, lane, rank, gd, gcnt, gsum);
       if (act) rk[v] = (uint16_t)(base[d] + rank);
-      __syncthreads();
+      wave_lds_fence();
       if (gd >= 0) {
         base[gd] += gcnt;
         cfill[gd] += gsum;
       }
-      __syncthreads();
+      wave_lds_fence();
     }
   }
   if (lane == 0) {
@@ -629,7 +638,7 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       a = an;
     }
   }
-  __syncthreads();
+  wave_lds_fence();
   int32_t *m = meta + j * meta_stride(D);
   for (int d = lane; d <= D; d += kWave) {
     m[d] = own_off[d];
@@ -638,30 +647,34 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
   }
 }
 
-// Gap of x among the sorted S[0, m): #{k : S[k] <= x} (kLe) or S[k] < x, with
-// the answer expected in [L, L+4]: six independent probes decide it, a
-// binary search covers the rest.
+// Gap of x among the sorted S[0, m): #{k : S[k] <= x} (kLe) or S[k] < x.
+// gap_win decides it from six independent probes when the answer lies in
+// [L, L+4] (ok), gap_search covers the rest.
 template <bool kLe, class UP>
-__device__ __forceinline__ int gap_of(UP S, int m, uint32_t x, int L) {
-  if (m == 0) return 0;
+__device__ __forceinline__ int gap_win(UP S, int m, uint32_t x, int L, bool &ok) {
+  if (m == 0) {
+    ok = true;
+    return 0;
+  }
   L = min(L, m);
   auto hit = [&](uint32_t sv) { return kLe ? sv <= x : sv < x; };
   const uint32_t sm1 = S[max(L - 1, 0)];
   uint32_t sv[5];
 #pragma unroll
   for (int q = 0; q < 5; ++q) sv[q] = S[min(L + q, m - 1)];
-  const bool lo_ok = L == 0 || hit(sm1);
-  const bool hi_ok = L + 4 >= m || !hit(sv[4]);
-  if (lo_ok && hi_ok) {
-    int g = L;
+  ok = (L == 0 || hit(sm1)) && (L + 4 >= m || !hit(sv[4]));
+  int g = L;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) g += (L + q < m && hit(sv[q])) ? 1 : 0;
-    return g;
-  }
+  for (int q = 0; q < 4; ++q) g += (L + q < m && hit(sv[q])) ? 1 : 0;
+  return g;
+}
+
+template <bool kLe, class UP>
+__device__ int gap_search(UP S, int m, uint32_t x) {
   int lo = 0, n = m;
   while (n > 0) {
     const int half = n >> 1;
-    if (hit(S[lo + half])) {
+    if (kLe ? S[lo + half] <= x : S[lo + half] < x) {
       lo += half + 1;
       n -= half + 1;
     } else {
@@ -701,16 +714,16 @@ __device__ void prefix_inplace(CP a, int n, int lane) {
   }
 }
 
-// max(0, max_i sum_{k <= i} (alloc[k] - freed[k])): the peak live bytes, the
-// maximum being taken at allocation instants (each position is one).
-template <class IP, class FP>
-__device__ int64_t max_live(IP alloc, FP freed, int n, int lane) {
+// max(0, max_i sum_{k <= i} delta[k]): the peak live bytes, the maximum being
+// taken at allocation instants (each position is one).
+template <class DP>
+__device__ int64_t max_live(DP delta, int n, int lane) {
   const int m = (n + kWave - 1) / kWave, lo = lane * m, hi = min(n, lo + m);
   int64_t s = 0;
-  for (int i = lo; i < hi; ++i) s += (int64_t)alloc[i] - (int64_t)freed[i];
+  for (int i = lo; i < hi; ++i) s += delta[i];
   int64_t run = wave_incl_scan64(s, lane) - s, best = 0;
   for (int i = lo; i < hi; ++i) {
-    run += (int64_t)alloc[i] - (int64_t)freed[i];
+    run += delta[i];
     best = imax64(best, run);
   }
   for (int o = kWave / 2; o >= 1; o >>= 1) best = imax64(best, __shfl_xor(best, o, kWave));
@@ -724,109 +737,112 @@ __device__ int64_t max_live(IP alloc, FP freed, int n, int lane) {
 // g + CG[g] + r, where CG[g] counts the copies in gaps before g; a free of gap
 // g lands before the first allocation at or after it: g + CG[g] + the copies
 // of gap g allocated before it.  Work arrays (LDS, or global slot memory when
-// the device holds more than kCap allocations):
+// the device holds more than kCap - 2 allocations):
 //   ak  own starts S[0, m), then the copy times grouped by gap
 //   ag  gap counts / CG[0, m+2), then per copy (gap << 16 | slot in gap)
-//   ai  per grouped copy time, the copy's index (ties between equal times)
-//   mb  allocation bytes by merged position; fr bytes freed before each
-template <class UP, class IP, class HP, class FP>
-__device__ int64_t device_peak(const Rec *own, int m, const Rec *cp, int nc, UP ak, IP ag, HP ai, UP mb, FP fr,
-                               int lane) {
+//   dl  by merged position: bytes allocated there minus bytes freed just before
+template <class UP, class IP, class DP>
+__device__ int64_t device_peak(const Rec *own, int m, const Rec *cp, int nc, UP ak, IP ag, DP dl, int lane) {
   constexpr int kB = 8;
   const int na = m + nc;
-  UP bt = ak + m;                                       // grouped copy times
+  UP bt = ak + m;                                           // grouped copy times
   uint32_t *qg = reinterpret_cast<uint32_t *>(ag + m + 2);  // per copy: gap << 16 | slot
-  for (int base = lane; base < m; base += kB * kWave) {  // a batch of loads in flight together
-    Rec r[kB];
+  for (int base = lane; base < m; base += kB * kWave) {      // a batch of loads in flight together
+    uint32_t r[kB];
 #pragma unroll
     for (int q = 0; q < kB; ++q)
-      if (base + q * kWave < m) r[q] = own[base + q * kWave];
+      if (base + q * kWave < m) r[q] = own[base + q * kWave].x;
 #pragma unroll
-    for (int q = 0; q < kB; ++q) {
-      const int i = base + q * kWave;
-      if (i < m) {
-        ak[i] = r[q].x;
-        fr[i] = r[q].z;  // own bytes parked in fr until the merged order is known
-      }
-    }
+    for (int q = 0; q < kB; ++q)
+      if (base + q * kWave < m) ak[base + q * kWave] = r[q];
   }
-  for (int i = m + lane; i < na; i += kWave) fr[i] = 0;
+  for (int i = lane; i < na; i += kWave) dl[i] = 0;
   for (int i = lane; i < m + 2; i += kWave) ag[i] = 0;
-  __syncthreads();
-  // gap of every copy allocation, and its slot inside the gap
+  wave_lds_fence();
+  // gap of every copy allocation, and its slot inside the gap: the window
+  // probes of four rows are in flight together, searches only where needed
   for (int base = lane; base < nc; base += 4 * kWave) {
-    Rec r[4];
+    uint32_t x[4], L[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (base + q * kWave < nc) r[q] = cp[base + q * kWave];
+    for (int q = 0; q < 4; ++q) {
+      const Rec r = cp[min(base + q * kWave, nc - 1)];
+      x[q] = r.x;
+      L[q] = r.w >> 16;
+    }
+    int g[4];
+    bool ok[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) g[q] = gap_win<true>(ak, m, x[q], (int)L[q], ok[q]);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int i = base + q * kWave;
       if (i < nc) {
-        const int g = gap_of<true>(ak, m, r[q].x, (int)(r[q].w >> 16));
-        const int slot = atomicAdd(&ag[g + 1], 1);
-        qg[i] = (uint32_t)g << 16 | (uint32_t)slot;
+        if (!ok[q]) g[q] = gap_search<true>(ak, m, x[q]);
+        const int slot = atomicAdd(&ag[g[q] + 1], 1);
+        qg[i] = (uint32_t)g[q] << 16 | (uint32_t)slot;
       }
     }
   }
-  __syncthreads();
+  wave_lds_fence();
   prefix_inplace(ag, m + 2, lane);  // ag[g] = CG[g]
-  __syncthreads();
+  wave_lds_fence();
+  for (int i = lane; i < nc; i += kWave) bt[ag[qg[i] >> 16] + (qg[i] & 0xFFFFu)] = cp[i].x;
+  for (int k = lane; k < m; k += kWave) dl[k + ag[k + 1]] = own[k].z;
+  wave_lds_fence();
+  // copy allocations: rank inside the gap by (time, slot)
   for (int i = lane; i < nc; i += kWave) {
-    const int g = (int)(qg[i] >> 16), slot = (int)(qg[i] & 0xFFFFu);
-    bt[ag[g] + slot] = cp[i].x;
-    ai[ag[g] + slot] = i;
+    const Rec r = cp[i];
+    const int g = (int)(qg[i] >> 16), s0 = ag[g], s1 = ag[g + 1], me = s0 + (int)(qg[i] & 0xFFFFu);
+    int rank = 0;
+    for (int z = s0; z < s1; ++z) {
+      const uint32_t t = bt[z];
+      rank += (t < r.x || (t == r.x && z < me)) ? 1 : 0;
+    }
+    dl[g + s0 + rank] = r.z;
   }
-  for (int k = lane; k < m; k += kWave) {
-    mb[k + ag[k + 1]] = (uint32_t)fr[k];
-    fr[k] = 0;
-  }
-  __syncthreads();
+  wave_lds_fence();
   // frees: gap (exact or by window), then the copies of that gap allocated before
   auto place_free = [&](int g, uint32_t h, uint32_t bytes) {
     const int s0 = ag[g], s1 = ag[g + 1];
     int pos = g + s0;
     for (int z = s0; z < s1; ++z) pos += bt[z] < h ? 1 : 0;
-    if (pos < na) atomicAdd(reinterpret_cast<unsigned long long *>(&fr[pos]), (unsigned long long)bytes);
+    if (pos < na) atomicAdd(reinterpret_cast<unsigned long long *>(&dl[pos]), (unsigned long long)(-(int64_t)bytes));
   };
   for (int i = lane; i < nc; i += kWave) {
     const Rec r = cp[i];
-    const int g = (int)(qg[i] >> 16), s0 = ag[g], s1 = ag[g + 1];
-    int rank = 0;
-    for (int z = s0; z < s1; ++z) {
-      const uint32_t t = bt[z];
-      rank += (t < r.x || (t == r.x && (int)ai[z] < i)) ? 1 : 0;
-    }
-    mb[g + s0 + rank] = r.z;
     place_free((int)(r.w & 0xFFFFu), r.y, r.z);
   }
   for (int k = lane; k < m; k += kWave) {
     const Rec r = own[k];
-    if (r.y != kInf32) place_free((r.w & kLocWindow) ? gap_of<false>(ak, m, r.y, (int)(r.w & 0xFFFFu)) : (int)r.w,
-                                  r.y, r.z);
+    if (r.y != kInf32) {
+      int g = (int)r.w;
+      if (r.w & kLocWindow) {
+        bool ok;
+        g = gap_win<false>(ak, m, r.y, (int)(r.w & 0xFFFFu), ok);
+        if (!ok) g = gap_search<false>(ak, m, r.y);
+      }
+      place_free(g, r.y, r.z);
+    }
   }
-  __syncthreads();
-  const int64_t best = max_live(mb, fr, na, lane);
-  __syncthreads();
+  wave_lds_fence();
+  const int64_t best = max_live(dl, na, lane);
+  wave_lds_fence();
   return best;
 }
 
 __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0, int64_t nj,
                                                     const Rec *__restrict__ own_all, const Rec *__restrict__ cp_all,
                                                     const int32_t *__restrict__ meta, uint32_t *__restrict__ wk_all,
-                                                    uint64_t *__restrict__ wb_all, int64_t slot_cap,
+                                                    int64_t *__restrict__ wb_all, int64_t slot_cap,
                                                     int64_t *__restrict__ peak, uint8_t *__restrict__ violation) {
-  __shared__ uint32_t s_ak[kCap], s_mb[kCap];
-  __shared__ int s_ag[kCap + 2];
-  __shared__ uint16_t s_ai[kCap];
-  __shared__ uint64_t s_fr[kCap];
+  __shared__ uint32_t s_ak[kCap];
+  __shared__ int s_ag[kCap];  // gap counts (m + 2) then per-copy slots (nc): holds up to kCap - 2 allocations
+  __shared__ int64_t s_dl[kCap];
   const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops];
   const int lane = threadIdx.x;
-  uint32_t *g_ak = wk_all + (int64_t)blockIdx.x * 4 * (slot_cap + 2);
+  uint32_t *g_ak = wk_all + (int64_t)blockIdx.x * 2 * (slot_cap + 2);
   int32_t *g_ag = reinterpret_cast<int32_t *>(g_ak + slot_cap + 2);
-  uint32_t *g_ai = g_ak + 2 * (slot_cap + 2);
-  uint32_t *g_mb = g_ak + 3 * (slot_cap + 2);
-  uint64_t *g_fr = wb_all + (int64_t)blockIdx.x * slot_cap;
+  int64_t *g_dl = wb_all + (int64_t)blockIdx.x * slot_cap;
   for (int64_t j = blockIdx.x; j < nj; j += gridDim.x) {
     const int64_t c = j0 + j;
     if (violation[c] & SS_VIOLATION_INVALID) {
@@ -843,10 +859,10 @@ __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0,
       const int c0 = mt[D + 1 + e], nc = mt[2 * (D + 1) + e];
       int64_t pk = 0;
       if (m + nc > 0) {
-        if (m + nc <= kCap)
-          pk = device_peak(own + o0, m, cp + c0, nc, s_ak, s_ag, s_ai, s_mb, s_fr, lane);
+        if (m + nc + 2 <= kCap)
+          pk = device_peak(own + o0, m, cp + c0, nc, s_ak, s_ag, s_dl, lane);
         else
-          pk = device_peak(own + o0, m, cp + c0, nc, g_ak, g_ag, g_ai, g_mb, g_fr, lane);
+          pk = device_peak(own + o0, m, cp + c0, nc, g_ak, g_ag, g_dl, lane);
       }
       if (peak && lane == 0) peak[c * D + e] = pk;
       if (pk > G.cap[e]) viol = SS_VIOLATION_MEMORY;
@@ -909,7 +925,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   const size_t sz_cp = align((size_t)sub * (E + 1) * sizeof(Rec));
   const size_t sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
   const size_t sz_rank = align(((size_t)sub * N + 1) * 2);
-  const size_t sz_wk = align((size_t)nslots * 4 * (slot_cap + 2) * 4);
+  const size_t sz_wk = align((size_t)nslots * 2 * (slot_cap + 2) * 4);
   const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
   void *scratch = nullptr;
   err = hipMallocAsync(&scratch,
@@ -930,7 +946,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   auto *meta = reinterpret_cast<int32_t *>(take(sz_meta));
   auto *rank = reinterpret_cast<uint16_t *>(take(sz_rank));
   auto *wk = reinterpret_cast<uint32_t *>(take(sz_wk));
-  auto *wb = reinterpret_cast<uint64_t *>(take(sz_wb));
+  auto *wb = reinterpret_cast<int64_t *>(take(sz_wb));
 
   int rc = SS_OK;
   auto check = [&](const char *what) {
