@@ -23,6 +23,11 @@ if ROOT not in sys.path:
 
 METRIC = "candidate placements simulated/sec (+ op-evals/sec, % HBM roofline), 1 GPU"
 HBM_PEAK_GBS = 8000.0
+COPY_BYTES = 1 << 31  # device-to-device copy: achievable bandwidth, and the counter calibration kernel
+# Measured HBM traffic of the kernels (rocprofv3 FETCH_SIZE / WRITE_SIZE, scaled by
+# the copy kernel's readings), valid while the kernel sources hash as recorded there.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_16tenant-50kop-128dev.md")
+KERNEL_SOURCES = ("paper_2608_15762_amd/csrc/sim_fast.hip", "paper_2608_15762_amd/csrc/gmg_load.cpp")
 
 
 def parse():
@@ -40,6 +45,49 @@ def parse():
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """{kernel: HBM bytes per candidate} from the committed counter summary, or
+    {} when it is missing or was taken on other kernel sources."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return {}
+    out, src = {}, None
+    for line in text.splitlines():
+        if line.startswith("source_hash:"):
+            src = line.split(":", 1)[1].strip()
+        elif line.startswith("bytes_per_candidate:"):
+            name, val = line.split(":", 1)[1].split()
+            out[name] = float(val)
+    return out if src == kernel_source_hash() else {}
+
+
+def copy_bandwidth(torch, dev):
+    """Achievable HBM bandwidth: a device-to-device copy of COPY_BYTES (read + write)."""
+    a = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 5
+    del a, b
+    return 2 * COPY_BYTES / (ms * 1e-3) / 1e9
 
 
 def stage_placements(torch, synth, g, cid, B, dev, chunk):
@@ -127,6 +175,8 @@ def main():
     if args.candidates > 0:
         B = min(B, args.candidates)
     log(f"workload {cfg.name}: N={N} E={g.n_edges} D={D} R={R} B={B}")
+    copy_gbs = copy_bandwidth(torch, dev)
+    log(f"device-to-device copy of {COPY_BYTES >> 20} MiB: {copy_gbs:.0f} GB/s")
     h = ss.Gmg(g)
     t0 = time.perf_counter()
     P = stage_placements(torch, synth, g, cid, B, dev, args.gen_chunk)
@@ -168,6 +218,9 @@ def main():
     launches_per_step = max(1, kernels[dom]["launches"] // args.steps)
     cand_per_launch = B / launches_per_step
     achieved = bytes_per_cand * cand_per_launch / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
+    traffic = measured_traffic().get(dom)
+    if traffic is not None:
+        traffic = round(traffic * cand_per_launch)
     result = {
         "metric": METRIC, "value": round(value, 1), "unit": "candidates/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 2), "higher_is_better": True,
@@ -177,8 +230,9 @@ def main():
         "op_evals_per_s": round(value * N, 1),
         "path_hbm_frac": round(value * bytes_per_cand / (HBM_PEAK_GBS * 1e9), 6),
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6), "traffic": None,
-                     "bytes_per_candidate": bytes_per_cand, "candidates_per_launch": cand_per_launch},
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6), "traffic": traffic,
+                     "bytes_per_candidate": bytes_per_cand, "candidates_per_launch": cand_per_launch,
+                     "copy_gbs": round(copy_gbs, 1)},
         "kernels": kernels,
     }
     torch.cuda.synchronize()
