@@ -907,8 +907,15 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   const bool iv_fast = g->n_class == 1 && g->n_link <= 2 && g->max_outdeg <= 2;
   // chunk: op-major placements, op-major and row-major finish times
   const int64_t per_cand = N * (1 + 4 + 4);
+  int lds_cu = 0;
+  err = hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, g->device);
+  if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
+  // A schedule launch is best a whole number of rounds of the waves the chip
+  // holds at once (every wave runs about as long as any other).
+  const int64_t round =
+      (int64_t)cus * std::max<int64_t>(1, lds_cu / (int64_t)std::max<size_t>(sched_lds, 1)) * kWave;
   int64_t chunk = kScratchBudget / std::max<int64_t>(1, per_cand);
-  chunk = std::max<int64_t>(kWave, chunk / kWave * kWave);
+  chunk = chunk >= round ? chunk / round * round : std::max<int64_t>(kWave, chunk / kWave * kWave);
   chunk = std::min<int64_t>(chunk, int64_t(65535) * 64);  // transpose grids index 64-candidate tiles in y
   chunk = std::min<int64_t>(chunk, B);
   // sub-chunk: interval records of each candidate (own N, copies <= E)
