@@ -45,7 +45,7 @@ constexpr int kCap = 1024;            // LDS slots of fast_peaks per work array
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per chunk
 constexpr int64_t kRecordBudget = int64_t(12) << 30;   // interval records per sub-chunk
-constexpr int kPeakBlocksPerCU = 10;  // fast_peaks holds about 16 KB of LDS
+constexpr int kPeakBlocksPerCU = 8;  // fast_peaks holds about 19.5 KB of LDS
 
 __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
 __device__ __forceinline__ int64_t imax64(int64_t a, int64_t b) { return a > b ? a : b; }
@@ -830,14 +830,195 @@ __device__ int64_t device_peak(const Rec *own, int m, const Rec *cp, int nc, UP 
   return best;
 }
 
+// Aggregate evaluation of one device (own starts S[0, m) sorted, nc copies).
+// With the merged order [gap 0] own 0 [gap 1] own 1 ... own m-1 [gap m] (a
+// gap's events: its copy allocations and the frees that land before the next
+// own allocation), let L[g] be the live bytes after all events of gap g:
+//   L[g] = sum_{g' <= g} (copies_g' - frees_g') + sum_{k < g} own_k,
+// so the live bytes at own allocation k are L[k] + own_k, exact from per-gap
+// sums alone.  Inside gap g the live bytes at a copy allocation are at most
+// U[g] = L[g] + frees_g (every copy counted, no free), and equal to it when
+// the gap holds no free.  Only a "hard" gap, holding copies and frees with
+// U[g] above the best exact value so far, needs its events in time order;
+// those few events are collected and swept exactly.
+constexpr int kAggCap = 512;   // own allocations per device for the aggregate method in LDS
+constexpr int kAggCopies = 1024;
+constexpr int kHardCap = 128;  // events of hard gaps per device
+
+struct AggLds {
+  uint32_t S[kAggCap];        // own starts
+  uint32_t ob[kAggCap];       // own bytes
+  int64_t dg[kAggCap + 1];    // per gap: copies - frees (+ own_{g-1}), then L[g]
+  int64_t fg[kAggCap + 1];    // per gap: freed bytes
+  uint32_t cg[kAggCopies];    // per copy: allocation gap << 16 | free gap
+  uint16_t og[kAggCap];       // per own allocation: free gap (0xFFFF: never freed)
+  uint8_t hard[kAggCap + 1];
+  uint32_t ht[kHardCap], hb[kHardCap], hx[kHardCap];  // collected events: time, bytes, gap << 1 | is_alloc
+  int hn;
+};
+
+// returns -1 if the hard events overflow (the caller then uses device_peak)
+__device__ int64_t device_peak_agg(const Rec *own, int m, const Rec *cp, int nc, AggLds &A, int lane) {
+  for (int base = lane; base < m; base += 8 * kWave) {  // a batch of loads in flight together
+    Rec r[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) r[q] = own[min(base + q * kWave, m - 1)];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int k = base + q * kWave;
+      if (k < m) {
+        A.S[k] = r[q].x;
+        A.ob[k] = r[q].z;
+      }
+    }
+  }
+  for (int g = lane; g <= m; g += kWave) {
+    A.fg[g] = 0;
+    A.hard[g] = 0;
+  }
+  if (lane == 0) A.hn = 0;
+  wave_lds_fence();
+  for (int g = lane; g <= m; g += kWave) A.dg[g] = g > 0 ? (int64_t)A.ob[g - 1] : 0;
+  wave_lds_fence();
+  auto add64 = [](int64_t *p, int64_t v) {
+    atomicAdd(reinterpret_cast<unsigned long long *>(p), (unsigned long long)v);
+  };
+  // copies: allocation gap (window probes, four rows in flight), free gap exact
+  for (int base = lane; base < nc; base += 4 * kWave) {
+    Rec r[4];
+    int g[4];
+    bool ok[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r[q] = cp[min(base + q * kWave, nc - 1)];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) g[q] = gap_win<true>(A.S, m, r[q].x, (int)(r[q].w >> 16), ok[q]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = base + q * kWave;
+      if (i < nc) {
+        if (!ok[q]) g[q] = gap_search<true>(A.S, m, r[q].x);
+        const int gf = (int)(r[q].w & 0xFFFFu);
+        A.cg[i] = (uint32_t)g[q] << 16 | (uint32_t)gf;
+        add64(&A.dg[g[q]], (int64_t)r[q].z);
+        add64(&A.dg[gf], -(int64_t)r[q].z);
+        add64(&A.fg[gf], (int64_t)r[q].z);
+      }
+    }
+  }
+  // own frees: exact gap or window probes
+  for (int base = lane; base < m; base += 4 * kWave) {
+    Rec r[4];
+    int g[4];
+    bool ok[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      r[q] = own[min(base + q * kWave, m - 1)];
+      ok[q] = true;
+      g[q] = (int)r[q].w;
+      if (r[q].w & kLocWindow) g[q] = gap_win<false>(A.S, m, r[q].y, (int)(r[q].w & 0xFFFFu), ok[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int k = base + q * kWave;
+      if (k < m) {
+        if (r[q].y == kInf32) {
+          A.og[k] = 0xFFFFu;
+        } else {
+          if (!ok[q]) g[q] = gap_search<false>(A.S, m, r[q].y);
+          A.og[k] = (uint16_t)g[q];
+          add64(&A.dg[g[q]], -(int64_t)r[q].z);
+          add64(&A.fg[g[q]], (int64_t)r[q].z);
+        }
+      }
+    }
+  }
+  wave_lds_fence();
+  // L[g] = prefix of dg; P0 at own allocations, exact values of copy-only gaps
+  {
+    const int n = m + 1, per = (n + kWave - 1) / kWave, lo = lane * per, hi = min(n, lo + per);
+    int64_t sacc = 0;
+    for (int g = lo; g < hi; ++g) sacc += A.dg[g];
+    int64_t run = wave_incl_scan64(sacc, lane) - sacc;
+    for (int g = lo; g < hi; ++g) {
+      run += A.dg[g];
+      A.dg[g] = run;
+    }
+  }
+  wave_lds_fence();
+  int64_t best = 0;
+  for (int g = lane; g <= m; g += kWave) {
+    const int64_t L = A.dg[g], prev = g > 0 ? A.dg[g - 1] + (int64_t)A.ob[g - 1] : 0;
+    if (g < m) best = imax64(best, L + (int64_t)A.ob[g]);
+    const int64_t copies = L - prev + A.fg[g];
+    if (copies > 0 && A.fg[g] == 0) best = imax64(best, L);  // copies only: all of them precede own g
+  }
+  for (int o = kWave / 2; o >= 1; o >>= 1) best = imax64(best, __shfl_xor(best, o, kWave));
+  bool any = false;
+  for (int g = lane; g <= m; g += kWave) {
+    const int64_t L = A.dg[g], prev = g > 0 ? A.dg[g - 1] + (int64_t)A.ob[g - 1] : 0;
+    const int64_t copies = L - prev + A.fg[g];
+    if (copies > 0 && A.fg[g] > 0 && L + A.fg[g] > best) {
+      A.hard[g] = 1;
+      any = true;
+    }
+  }
+  if (!__any(any)) return best;
+  wave_lds_fence();
+  // collect the events of the hard gaps
+  auto push = [&](uint32_t t, uint32_t b, uint32_t x) {
+    const int at = atomicAdd(&A.hn, 1);
+    if (at < kHardCap) {
+      A.ht[at] = t;
+      A.hb[at] = b;
+      A.hx[at] = x;
+    }
+  };
+  for (int i = lane; i < nc; i += kWave) {
+    const uint32_t gg = A.cg[i];
+    const int ga = (int)(gg >> 16), gf = (int)(gg & 0xFFFFu);
+    if (A.hard[ga] | A.hard[gf]) {
+      const Rec r = cp[i];
+      if (A.hard[ga]) push(r.x, r.z, (uint32_t)ga << 1 | 1u);
+      if (A.hard[gf]) push(r.y, r.z, (uint32_t)gf << 1);
+    }
+  }
+  for (int k = lane; k < m; k += kWave) {
+    const uint32_t gf = A.og[k];
+    if (gf != 0xFFFFu && A.hard[gf]) push(own[k].y, A.ob[k], gf << 1);
+  }
+  wave_lds_fence();
+  const int hn = A.hn;
+  if (hn > kHardCap) return -1;
+  // live bytes at each collected copy allocation: the gap's start value plus
+  // its copies up to it (ties by position) minus its frees at or before it
+  for (int e = lane; e < hn; e += kWave) {
+    const uint32_t x = A.hx[e];
+    if (!(x & 1u)) continue;
+    const int g = (int)(x >> 1);
+    const uint32_t t = A.ht[e];
+    int64_t live = g > 0 ? A.dg[g - 1] + (int64_t)A.ob[g - 1] : 0;
+    for (int z = 0; z < hn; ++z) {
+      const uint32_t xz = A.hx[z];
+      if ((int)(xz >> 1) != g) continue;
+      const uint32_t tz = A.ht[z];
+      if (xz & 1u) {
+        if (tz < t || (tz == t && z <= e)) live += A.hb[z];
+      } else if (tz <= t) {
+        live -= A.hb[z];
+      }
+    }
+    best = imax64(best, live);
+  }
+  for (int o = kWave / 2; o >= 1; o >>= 1) best = imax64(best, __shfl_xor(best, o, kWave));
+  return best;
+}
+
 __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0, int64_t nj,
                                                     const Rec *__restrict__ own_all, const Rec *__restrict__ cp_all,
                                                     const int32_t *__restrict__ meta, uint32_t *__restrict__ wk_all,
                                                     int64_t *__restrict__ wb_all, int64_t slot_cap,
                                                     int64_t *__restrict__ peak, uint8_t *__restrict__ violation) {
-  __shared__ uint32_t s_ak[kCap];
-  __shared__ int s_ag[kCap];  // gap counts (m + 2) then per-copy slots (nc): holds up to kCap - 2 allocations
-  __shared__ int64_t s_dl[kCap];
+  __shared__ AggLds s_agg;
   const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops];
   const int lane = threadIdx.x;
   uint32_t *g_ak = wk_all + (int64_t)blockIdx.x * 2 * (slot_cap + 2);
@@ -859,10 +1040,9 @@ __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0,
       const int c0 = mt[D + 1 + e], nc = mt[2 * (D + 1) + e];
       int64_t pk = 0;
       if (m + nc > 0) {
-        if (m + nc + 2 <= kCap)
-          pk = device_peak(own + o0, m, cp + c0, nc, s_ak, s_ag, s_dl, lane);
-        else
-          pk = device_peak(own + o0, m, cp + c0, nc, g_ak, g_ag, g_dl, lane);
+        pk = -1;
+        if (m < kAggCap && nc <= kAggCopies) pk = device_peak_agg(own + o0, m, cp + c0, nc, s_agg, lane);
+        if (pk < 0) pk = device_peak(own + o0, m, cp + c0, nc, g_ak, g_ag, g_dl, lane);
       }
       if (peak && lane == 0) peak[c * D + e] = pk;
       if (pk > G.cap[e]) viol = SS_VIOLATION_MEMORY;

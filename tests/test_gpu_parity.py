@@ -170,6 +170,30 @@ def test_fan_in_many_copies_in_one_gap(dev, path):
     assert_same(gpu_run(ss.Gmg(g), P, dev), ref, label="fan-in")
 
 
+@pytest.mark.parametrize("k", [30, 70])
+def test_copies_and_frees_crowding_one_gap(dev, path, k):
+    """Device 0 runs op A, then op B; device 1 runs k producers consumed by A,
+    then k producers consumed by B.  The copies for B arrive while A runs and
+    the copies for A are freed when A finishes: 2k events interleave between
+    the starts of A and B (with k = 70 more than the peak kernel collects
+    per device for its exact in-gap sweep, so it must fall back)."""
+    n = 2 * k + 2
+    a, b = 2 * k, 2 * k + 1
+    st = synth.Stream(k)
+    edges = [(i, a) for i in range(k)] + [(k + i, b) for i in range(k)]
+    dur = [[st.uniform_int(5, 15)] for _ in range(2 * k)] + [[10 * k], [7]]
+    out_b = [st.uniform_int(1000, 5000) for _ in range(n)]
+    g = make_gmg(2, ["op"] * n, edges, [0] * n, dur, out_b, [[(0, TIME_INF)]] * 2, [10 ** 9] * 2, [0], [10 ** 9],
+                 bw=[1000], lat=[1])
+    P = np.ones((4, n), np.uint8)
+    P[:, a] = P[:, b] = 0
+    P[1, : k // 2] = 0  # some producers local to A
+    P[2, k: k + k // 3] = 0  # some producers local to B
+    P[3] = np.array([st.uniform_int(0, 1) for _ in range(n)], np.uint8)
+    ref = oracle.simulate_batch(g, P)
+    assert_same(gpu_run(ss.Gmg(g), P, dev), ref, label=f"crowded gap k={k}")
+
+
 def test_horizon_beyond_32_bits_takes_general_path(dev, monkeypatch):
     """Slices far beyond 2^32 us: the fast path must be refused and the general
     path must still match the oracle."""
