@@ -31,6 +31,7 @@ extern "C" {
 #define SS_TIME_INF INT64_MAX    /* end of a device's last (open) idle slice */
 
 #define SS_LAYOUT_ROW_MAJOR 0    /* placements[b * n_ops + v] = device of op v in candidate b */
+#define SS_DISPATCH_READY 0x100  /* OR into layout: ready-time dispatch (see ss_simulate_batch) */
 
 #define SS_VIOLATION_MEMORY 0x1  /* some device's peak memory exceeds its capacity */
 #define SS_VIOLATION_INVALID 0x4 /* the placement names a device id >= n_dev; not simulated */
@@ -134,10 +135,21 @@ int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req)
  *                        when it has no ops); may be negative     (nullable)
  *   out_sumfin[B]        sum of finish times = N x the average completion
  *                        time that Sec. 3.4.2 minimises           (nullable)
+ * With layout | SS_DISPATCH_READY the dispatch rule is the ready-time rule
+ * of Sec. 3.3.2 instead of index order: of the ops whose predecessors have
+ * all been dispatched, the one with the earliest ready time (ties to the lower
+ * index) is dispatched next, at the earliest fit on its device at or after
+ * max(ready time, that device's previous finish).  Memory follows the same
+ * definitions with "last" meaning the consumer that finishes last.  This rule
+ * needs the 32-bit evaluation (the horizon H below 2^32 - 1, n_ops, n_edges
+ * and every device's slice count at most 65535, out_bytes below 2^32, and the
+ * per-candidate device state within one workgroup's LDS); otherwise the call
+ * returns SS_ERR_UNSUPPORTED.
  * A candidate naming a device >= n_dev is not simulated: violation =
  * SS_VIOLATION_INVALID, makespan = sumfin = INT64_MAX, peak = 0 and slack =
  * INT64_MIN.  This is a per-candidate result, not a call error.
- * placements: DEVICE pointer, uint8 [B][n_ops] for SS_LAYOUT_ROW_MAJOR.
+ * placements: DEVICE pointer, uint8 [B][n_ops] for SS_LAYOUT_ROW_MAJOR (with
+ * or without SS_DISPATCH_READY).
  * The call is asynchronous on hip_stream (NULL = the null stream); inputs must
  * stay valid and outputs are defined once that stream has been synchronised.
  * It allocates stream-ordered scratch on hip_stream for the duration of the

@@ -48,7 +48,8 @@ extern "C" int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int
   ss_clear_error();
   if (!g) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: g is NULL");
   if (B < 0) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: B < 0");
-  if (layout != SS_LAYOUT_ROW_MAJOR) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: unknown layout");
+  if ((layout & ~SS_DISPATCH_READY) != SS_LAYOUT_ROW_MAJOR)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: unknown layout");
   if (B == 0) return SS_OK;
   if (!out_makespan || !out_violation)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: out_makespan and out_violation are required");
@@ -56,7 +57,7 @@ extern "C" int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int
   const int rc = check_device(g);
   if (rc != SS_OK) return rc;
   return ss_run_simulate(g, placements, B, out_makespan, out_peak_mem, out_violation, out_sla_slack, out_sumfin,
-                         static_cast<hipStream_t>(hip_stream));
+                         static_cast<hipStream_t>(hip_stream), (layout & SS_DISPATCH_READY) != 0);
 }
 
 extern "C" int ss_select_best(const ss_gmg *g, const uint8_t *violation, const int64_t *key,

@@ -146,6 +146,10 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
                         max_bytes <= (int64_t)UINT32_MAX;
     std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32, meta, lbits, bytes32, succ2, lutk, lutw;
     std::vector<uint8_t> lgrp;
+    std::vector<uint64_t> src_keys;  // ready-time dispatch: sources by (release, index)
+    for (int64_t v = 0; v < N; ++v)
+      if (d->pred_ptr[v + 1] == d->pred_ptr[v]) src_keys.push_back((uint64_t)d->release[d->op_req[v]] << 16 | (uint64_t)v);
+    std::sort(src_keys.begin(), src_keys.end());
     int32_t lsame = 0;
     int64_t lut_nb = 0, lut_shift = 0;
     int64_t max_outdeg = 0;
@@ -269,7 +273,8 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     const size_t o_link = pk.add(d->link_class, D * D);
     const size_t o_dur32 = pk.add(dur32), o_xfer32 = pk.add(xfer32), o_sb32 = pk.add(sb32), o_se32 = pk.add(se32),
                  o_rel32 = pk.add(rel32), o_meta = pk.add(meta), o_lbits = pk.add(lbits), o_b32 = pk.add(bytes32),
-                 o_succ2 = pk.add(succ2), o_lutk = pk.add(lutk), o_lutw = pk.add(lutw), o_lgrp = pk.add(lgrp);
+                 o_succ2 = pk.add(succ2), o_lutk = pk.add(lutk), o_lutw = pk.add(lutw), o_lgrp = pk.add(lgrp),
+                 o_src = pk.add(src_keys);
     pk.add(nullptr, 256);  // tail padding
 
     ss_gmg *g = new ss_gmg();
@@ -322,6 +327,8 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     V.bytes32 = reinterpret_cast<const uint32_t *>(base + o_b32);
     V.succ2 = succ2.empty() ? nullptr : reinterpret_cast<const uint32_t *>(base + o_succ2);
     V.link_grp = lgrp.empty() ? nullptr : reinterpret_cast<const uint8_t *>(base + o_lgrp);
+    V.src_keys = reinterpret_cast<const uint64_t *>(base + o_src);
+    V.n_src = (int32_t)src_keys.size();
     V.link_same = lsame;
     V.lut_k = reinterpret_cast<const uint32_t *>(base + o_lutk);
     V.lut_w = reinterpret_cast<const uint4 *>(base + o_lutw);

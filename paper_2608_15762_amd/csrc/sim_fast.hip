@@ -41,7 +41,6 @@
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kCap = 1024;            // LDS slots of fast_peaks per work array
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per chunk
 constexpr int64_t kRecordBudget = int64_t(12) << 30;   // interval records per sub-chunk
@@ -381,6 +380,207 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   }
 }
 
+// ------------------------------------------------------------------ ready-time dispatch
+// The dispatch rule of Sec. 3.3.2: among the ops whose predecessors have all
+// been scheduled, the one with the earliest ready time runs next (ties to the
+// lower index), at the earliest fit on its device at or after max(ready time,
+// the device's previous finish).  One wave per candidate.  Ready ops are keys
+// ready << 16 | op (unique, so the order is total).  They live in the lanes'
+// registers (kReadySlots per lane); when those are full they go to the
+// candidate's spill list in global memory (at most N entries: ready ops form
+// an antichain), which is scanned while non-empty.  Sources (no predecessors)
+// come from a presorted list instead.  The next op is the smallest key of the
+// three.  The wave writes the finish times (candidate rows), each op's rank
+// among its device's ops in dispatch order (the order the memory pass needs),
+// and the per-candidate outputs.
+constexpr int kReadySlots = 4;
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t x) {
+  for (int o = kWave / 2; o >= 1; o >>= 1) {
+    const uint64_t y = __shfl_xor(x, o, kWave);
+    x = y < x ? y : x;
+  }
+  return x;
+}
+
+__global__ __launch_bounds__(kWave) void ready_schedule(const GmgView G, const uint8_t *__restrict__ P,
+                                                        uint32_t *__restrict__ fin, uint16_t *__restrict__ rank,
+                                                        uint16_t *__restrict__ missing, uint64_t *__restrict__ spill,
+                                                        int64_t *__restrict__ makespan, int64_t *__restrict__ sumfin,
+                                                        int64_t *__restrict__ slack, uint8_t *__restrict__ violation) {
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = G.n_class;
+  const int lane = threadIdx.x;
+  uint32_t *clk = reinterpret_cast<uint32_t *>(lds_raw);  // [D]
+  uint32_t *comp = clk + D;                               // [R]
+  uint32_t *cnt = comp + R;                               // [D] ops dispatched per device
+  int32_t *sbase = reinterpret_cast<int32_t *>(cnt + D);  // [D+1]
+  int32_t *dcls = sbase + D + 1;                          // [D]
+  const int64_t c = blockIdx.x;
+  const uint8_t *prow = P + c * N;
+  uint32_t *frow = fin + c * N;
+  uint16_t *rrow = rank + c * N;
+  uint16_t *mrow = missing + c * N;
+  uint64_t *srow = spill + c * N;
+  bool bad = false;
+  for (int v = lane; v < N; v += kWave) bad |= prow[v] >= (uint8_t)D;
+  if (__any(bad)) {
+    if (lane == 0) {
+      makespan[c] = INT64_MAX;
+      if (sumfin) sumfin[c] = INT64_MAX;
+      violation[c] = SS_VIOLATION_INVALID;
+    }
+    if (slack)
+      for (int r = lane; r < R; r += kWave) slack[c * R + r] = INT64_MIN;
+    return;
+  }
+  for (int d = lane; d <= D; d += kWave) {
+    sbase[d] = G.slice_ptr[d];
+    if (d < D) {
+      dcls[d] = G.dev_class[d];
+      cnt[d] = 0;
+    }
+  }
+  for (int r = lane; r < R; r += kWave) comp[r] = G.release32[r];
+  const uint32_t *indeg = G.op_meta + (int64_t)kMetaReq * G.meta_stride;  // predecessor count << 16
+  for (int v = lane; v < N; v += kWave) mrow[v] = (uint16_t)(indeg[v] >> 16);
+  wave_lds_fence();
+  for (int d = lane; d < D; d += kWave) clk[d] = G.slice_begin32[sbase[d]];
+  __syncthreads();  // LDS state and the missing-predecessor row before the loop reads them
+
+  constexpr uint64_t kNone = ~0ull;
+  uint64_t slot[kReadySlots];
+#pragma unroll
+  for (int k = 0; k < kReadySlots; ++k) slot[k] = kNone;
+  int sp = 0, ns = 0;  // next source, spill length (wave-uniform)
+  uint32_t ms = 0;
+  uint64_t sum = 0;
+  for (int step = 0; step < N; ++step) {
+    uint64_t my = slot[0];
+#pragma unroll
+    for (int k = 1; k < kReadySlots; ++k) my = slot[k] < my ? slot[k] : my;
+    const uint64_t wm = wave_min_u64(my);
+    uint64_t sm = kNone;
+    int si = 0;
+    if (ns > 0) {  // smallest spilled key and its position
+      uint64_t lm = kNone;
+      int li = 0;
+      for (int i = lane; i < ns; i += kWave) {
+        const uint64_t k = srow[i];
+        li = k < lm ? i : li;
+        lm = k < lm ? k : lm;
+      }
+      sm = wave_min_u64(lm);
+      if (sm != kNone) si = __shfl(li, __ffsll((unsigned long long)__ballot(lm == sm)) - 1, kWave);
+    }
+    const uint64_t sk = sp < G.n_src ? G.src_keys[sp] : kNone;
+    uint64_t key;
+    if (sk < wm && sk < sm) {
+      key = sk;
+      ++sp;
+    } else if (sm < wm) {
+      key = sm;
+      --ns;
+      if (lane == 0) srow[si] = srow[ns];  // the last entry fills the hole
+    } else {
+      key = wm;
+      const int owner = __ffsll((unsigned long long)__ballot(my == wm)) - 1;
+      if (lane == owner) {
+        bool done = false;
+#pragma unroll
+        for (int k = 0; k < kReadySlots; ++k)
+          if (!done && slot[k] == wm) {
+            slot[k] = kNone;
+            done = true;
+          }
+      }
+    }
+    const int v = (int)(key & 0xFFFFu);
+    const uint32_t ready = (uint32_t)(key >> 16);
+    const int d = prow[v];
+    const uint32_t w = G.dur32[(int64_t)v * C + dcls[d]];
+    uint32_t s = umax32(ready, clk[d]);
+    {  // the first idle slice that holds [s', s' + w) with s' >= s; slices
+       // before the table's entry end before s + w
+      const uint32_t e = (uint32_t)d * (uint32_t)G.lut_nb + (uint32_t)min((int)((s + w) >> G.lut_shift), G.lut_nb - 1);
+      const uint4 lw = G.lut_w[e];
+      const uint32_t t0 = umax32(s, lw.x), t1 = umax32(s, lw.z);
+      if (t0 + w <= lw.y) {
+        s = t0;
+      } else if (t1 + w <= lw.w) {
+        s = t1;
+      } else {
+        const int sb = sbase[d];
+        for (int k = (int)G.lut_k[e] + 2;; ++k) {
+          const uint32_t t = umax32(s, G.slice_begin32[sb + k]);
+          if (t + w <= G.slice_end32[sb + k]) {
+            s = t;
+            break;
+          }
+        }
+      }
+    }
+    const uint32_t f = s + w;
+    const int r = G.op_req[v];
+    const uint32_t rk = cnt[d];
+    wave_lds_fence();
+    if (lane == 0) {
+      clk[d] = f;
+      cnt[d] = rk + 1;
+      comp[r] = umax32(comp[r], f);
+      frow[v] = f;
+      rrow[v] = (uint16_t)rk;
+    }
+    __threadfence_block();  // the wave reads these back in later steps
+    ms = umax32(ms, f);
+    sum += f;
+    // successors whose last missing predecessor this was become ready
+    for (int q = G.succ_ptr[v]; q < G.succ_ptr[v + 1]; ++q) {
+      const int x = G.succ_idx[q];
+      const int left = (int)mrow[x] - 1;
+      if (lane == 0) mrow[x] = (uint16_t)left;
+      __threadfence_block();
+      if (left == 0) {
+        const int dx = prow[x];
+        uint32_t rx = G.release32[G.op_req[x]];
+        for (int e = G.pred_ptr[x]; e < G.pred_ptr[x + 1]; ++e) {
+          const int u = G.pred_idx[e];
+          const int du = prow[u];
+          uint32_t t = u == v ? f : frow[u];
+          if (du != dx) t += xfer_of(G, u, du, dx);
+          rx = umax32(rx, t);
+        }
+        const uint64_t nk = (uint64_t)rx << 16 | (uint64_t)x;
+        bool placed = false;
+#pragma unroll
+        for (int k = 0; k < kReadySlots; ++k) {
+          if (!placed) {
+            const unsigned long long free_lanes = __ballot(slot[k] == kNone);
+            if (free_lanes) {
+              if (lane == __ffsll(free_lanes) - 1) slot[k] = nk;
+              placed = true;
+            }
+          }
+        }
+        if (!placed) {
+          if (lane == 0) srow[ns] = nk;
+          ++ns;
+          __threadfence_block();
+        }
+      }
+    }
+  }
+  if (lane == 0) {
+    makespan[c] = ms;
+    if (sumfin) sumfin[c] = (int64_t)sum;
+    violation[c] = 0;
+  }
+  if (slack)
+    for (int rr = lane; rr < R; rr += kWave) slack[c * R + rr] = G.deadline[rr] - (int64_t)comp[rr];
+}
+
+size_t ready_schedule_lds(int D, int R) { return (size_t)(3 * D + R + 1 + D) * 4; }
+
 // ------------------------------------------------------------------ memory
 // Residency intervals (Sec. 3.3.2) are written by fast_intervals into
 // per-device buckets and evaluated by fast_peaks.
@@ -414,15 +614,17 @@ __device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32
   const uint32_t f = frow[v];
   uint32_t F = kInf32, loc = 0;  // kept forever without consumers
   if (x1 > x0) {
-    // local consumers finish in index order, so the last one finishes last
+    // the local consumer that finishes last (with index-order dispatch: the last one)
     uint32_t L = f, A = 0;
     int rl = rv;
     for (int q = x0; q < x1; ++q) {
       const int x = G.succ_idx[q];
       const int dx = prow[x];
       if (dx == d) {
-        L = frow[x];
-        rl = rk[x];
+        if (frow[x] > L) {
+          L = frow[x];
+          rl = rk[x];
+        }
       } else {
         A = umax32(A, f + xfer_of(G, v, d, dx));
       }
@@ -445,12 +647,17 @@ __device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32
     for (int q2 = x0; q2 < q; ++q2)
       if (prow[G.succ_idx[q2]] == e) first = false;
     if (!first) continue;
-    int y = xf;  // last consumer on e: the copy lives until it finishes
+    // the copy is allocated before the consumer on e that starts first (lowest
+    // rank) and lives until the consumer on e that finishes last
+    int y = xf, ra = rk[xf];
     for (int q2 = q + 1; q2 < x1; ++q2) {
       const int x = G.succ_idx[q2];
-      if (prow[x] == e) y = x;
+      if (prow[x] == e) {
+        if (frow[x] > frow[y]) y = x;
+        ra = min(ra, (int)rk[x]);
+      }
     }
-    const int ra = rk[xf], ry = rk[y];
+    const int ry = rk[y];
     cp[atomicAdd(&cfill[e], 1)] = Rec{f, frow[y], b, (uint32_t)max(ra - 3, 0) << 16 | (uint32_t)(ry + 1)};
   }
 }
@@ -518,7 +725,9 @@ struct IvSucc {  // device, finish and rank of the first two successors
   uint32_t dx0, dx1, fx0, fx1, rx0, rx1;
 };
 
-template <bool kFast>
+// kGivenRanks: the rank table already holds every op's rank on its device
+// (dispatch order), pass A only counts.
+template <bool kFast, bool kGivenRanks>
 __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const uint8_t *__restrict__ P,
                                                         const uint32_t *__restrict__ fin, int64_t j0,
                                                         Rec *__restrict__ own_all, Rec *__restrict__ cp_all,
@@ -550,15 +759,22 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       vn = min(v0 + kWave + lane, N - 1);  // next chunk, in flight meanwhile
       dn = prow[vn];
       in = indeg_f[vn];
-      int rank, gd, gcnt, gsum;
-      chunk_groups(d, act, indeg, lane, rank, gd, gcnt, gsum);
-      if (act) rk[v] = (uint16_t)(base[d] + rank);
-      wave_lds_fence();
-      if (gd >= 0) {
-        base[gd] += gcnt;
-        cfill[gd] += gsum;
+      if (kGivenRanks) {
+        if (act) {
+          atomicAdd(&base[d], 1);
+          atomicAdd(&cfill[d], indeg);
+        }
+      } else {
+        int rank, gd, gcnt, gsum;
+        chunk_groups(d, act, indeg, lane, rank, gd, gcnt, gsum);
+        if (act) rk[v] = (uint16_t)(base[d] + rank);
+        wave_lds_fence();
+        if (gd >= 0) {
+          base[gd] += gcnt;
+          cfill[gd] += gsum;
+        }
+        wave_lds_fence();
       }
-      wave_lds_fence();
     }
   }
   if (lane == 0) {
@@ -613,12 +829,12 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       const bool loc0 = has0 && sc.dx0 == d, loc1 = has1 && sc.dx1 == d;
       const uint32_t X0 = link_bit(G, d, sc.dx0) ? a.x1 : a.x0;  // transfer to each successor's device
       const uint32_t X1 = link_bit(G, d, sc.dx1) ? a.x1 : a.x0;
-      // own output: local consumers finish in index order, so the last one finishes last
+      // own output: until the local consumer that finishes last
       uint32_t L = a.f, rl = a.rv, A = 0;
-      L = loc0 ? sc.fx0 : L;
-      rl = loc0 ? sc.rx0 : rl;
-      L = loc1 ? sc.fx1 : L;
-      rl = loc1 ? sc.rx1 : rl;
+      rl = (loc0 && sc.fx0 > L) ? sc.rx0 : rl;
+      L = (loc0 && sc.fx0 > L) ? sc.fx0 : L;
+      rl = (loc1 && sc.fx1 > L) ? sc.rx1 : rl;
+      L = (loc1 && sc.fx1 > L) ? sc.fx1 : L;
       A = (has0 && !loc0) ? umax32(A, a.f + X0) : A;
       A = (has1 && !loc1) ? umax32(A, a.f + X1) : A;
       const bool arrive = A > L;
@@ -631,8 +847,12 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       const bool c1 = act && has1 && !loc1 && !same && a.b != 0;
       const int s0 = atomicAdd(c0 ? &cfill[sc.dx0] : &nocopy[lane], c0 ? 1 : 0);
       const int s1 = atomicAdd(c1 ? &cfill[sc.dx1] : &nocopy[lane], c1 ? 1 : 0);
-      const uint32_t ry0 = same ? sc.rx1 : sc.rx0, hi0 = same ? sc.fx1 : sc.fx0;
-      cp[c0 ? s0 : E] = Rec{a.f, hi0, a.b, (uint32_t)max((int)sc.rx0 - 3, 0) << 16 | (ry0 + 1)};
+      // both successors on one remote device: allocated before the one that
+      // starts first, freed after the one that finishes last
+      const bool late1 = same && sc.fx1 > sc.fx0;
+      const uint32_t ry0 = late1 ? sc.rx1 : sc.rx0, hi0 = late1 ? sc.fx1 : sc.fx0;
+      const uint32_t ra0 = same ? min(sc.rx0, sc.rx1) : sc.rx0;
+      cp[c0 ? s0 : E] = Rec{a.f, hi0, a.b, (uint32_t)max((int)ra0 - 3, 0) << 16 | (ry0 + 1)};
       cp[c1 ? s1 : E] = Rec{a.f, sc.fx1, a.b, (uint32_t)max((int)sc.rx1 - 3, 0) << 16 | (sc.rx1 + 1)};
       sc = load_succ(an, vn);
       a = an;
@@ -736,8 +956,8 @@ __device__ int64_t max_live(DP delta, int n, int lane) {
 // so own k sits at k + CG[k+1] and the copy of in-gap rank r of gap g at
 // g + CG[g] + r, where CG[g] counts the copies in gaps before g; a free of gap
 // g lands before the first allocation at or after it: g + CG[g] + the copies
-// of gap g allocated before it.  Work arrays (LDS, or global slot memory when
-// the device holds more than kCap - 2 allocations):
+// of gap g allocated before it.  Work arrays (the workgroup's global slot
+// memory):
 //   ak  own starts S[0, m), then the copy times grouped by gap
 //   ag  gap counts / CG[0, m+2), then per copy (gap << 16 | slot in gap)
 //   dl  by merged position: bytes allocated there minus bytes freed just before
@@ -1056,6 +1276,50 @@ int hip_fail(hipError_t err, const char *what) {
                       std::string(what) + ": " + hipGetErrorString(err));
 }
 
+// Sub-chunk scratch of the memory passes.
+struct MemPass {
+  Rec *own, *cp;
+  int32_t *meta;
+  uint16_t *rank;  // given ranks: candidate rows of the whole chunk; else sub rows
+  uint32_t *wk;
+  int64_t *wb;
+  int64_t sub, nslots, slot_cap;
+  bool iv_fast;
+};
+
+// Residency intervals, then peaks, for the nb candidates of one chunk (their
+// placements Pc and finish-time rows fin), sub candidates at a time.
+int memory_passes(const ss_gmg *g, const MemPass &M, const uint8_t *Pc, const uint32_t *fin, int64_t nb,
+                  bool given_ranks, int64_t *peak, uint8_t *violation, hipStream_t stream) {
+  const GmgView &G = g->view;
+  const int64_t N = g->n_ops;
+  for (int64_t j0 = 0; j0 < nb; j0 += M.sub) {
+    const int64_t nj = std::min(M.sub, nb - j0);
+    uint16_t *rank = given_ranks ? M.rank + j0 * N : M.rank;
+    const void *fn = M.iv_fast ? (given_ranks ? reinterpret_cast<const void *>(&fast_intervals<true, true>)
+                                              : reinterpret_cast<const void *>(&fast_intervals<true, false>))
+                               : (given_ranks ? reinterpret_cast<const void *>(&fast_intervals<false, true>)
+                                              : reinterpret_cast<const void *>(&fast_intervals<false, false>));
+    const uint8_t *vi = violation;
+    void *args[] = {const_cast<GmgView *>(&G), const_cast<uint8_t **>(&Pc), const_cast<uint32_t **>(&fin),
+                    &j0, const_cast<Rec **>(&M.own), const_cast<Rec **>(&M.cp), const_cast<int32_t **>(&M.meta),
+                    &rank, &vi};
+    SsTimingRec *ti = ss_timing_start(SS_KERNEL_INTERVALS, stream);
+    hipError_t err = hipLaunchKernel(fn, dim3((unsigned)nj), dim3(kWave), args, 0, stream);
+    ss_timing_stop(ti, stream);
+    if (err == hipSuccess) err = hipGetLastError();
+    if (err != hipSuccess) return hip_fail(err, "fast_intervals launch");
+    SsTimingRec *tm = ss_timing_start(SS_KERNEL_MEMORY, stream);
+    hipLaunchKernelGGL(fast_peaks, dim3((unsigned)std::min<int64_t>(nj, M.nslots)), dim3(kWave), 0, stream, G, j0, nj,
+                       static_cast<const Rec *>(M.own), static_cast<const Rec *>(M.cp),
+                       static_cast<const int32_t *>(M.meta), M.wk, M.wb, M.slot_cap, peak, violation);
+    ss_timing_stop(tm, stream);
+    err = hipGetLastError();
+    if (err != hipSuccess) return hip_fail(err, "fast_peaks launch");
+  }
+  return SS_OK;
+}
+
 }  // namespace
 
 size_t ss_fast_schedule_lds(const ss_gmg *g) {
@@ -1174,27 +1438,85 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
     }
     ss_timing_stop(tt, stream);
     if (!check("transpose launch")) break;
-    for (int64_t j0 = 0; j0 < nb && rc == SS_OK; j0 += sub) {
-      const int64_t nj = std::min(sub, nb - j0);
-      SsTimingRec *ti = ss_timing_start(SS_KERNEL_INTERVALS, stream);
-      if (iv_fast)
-        hipLaunchKernelGGL(fast_intervals<true>, dim3((unsigned)nj), dim3(kWave), 0, stream, G, Pc,
-                           static_cast<const uint32_t *>(fin), j0, own, cp, meta, rank,
-                           static_cast<const uint8_t *>(violation + b0));
-      else
-        hipLaunchKernelGGL(fast_intervals<false>, dim3((unsigned)nj), dim3(kWave), 0, stream, G, Pc,
-                           static_cast<const uint32_t *>(fin), j0, own, cp, meta, rank,
-                           static_cast<const uint8_t *>(violation + b0));
-      ss_timing_stop(ti, stream);
-      if (!check("fast_intervals launch")) break;
-      SsTimingRec *tm = ss_timing_start(SS_KERNEL_MEMORY, stream);
-      hipLaunchKernelGGL(fast_peaks, dim3((unsigned)std::min<int64_t>(nj, nslots)), dim3(kWave), 0, stream, G, j0, nj,
-                         static_cast<const Rec *>(own), static_cast<const Rec *>(cp),
-                         static_cast<const int32_t *>(meta), wk, wb, slot_cap, peak ? peak + b0 * D : nullptr,
-                         violation + b0);
-      ss_timing_stop(tm, stream);
-      if (!check("fast_peaks launch")) break;
+    const MemPass M{own, cp, meta, rank, wk, wb, sub, nslots, slot_cap, iv_fast};
+    rc = memory_passes(g, M, Pc, fin, nb, false, peak ? peak + b0 * D : nullptr, violation + b0, stream);
+  }
+  err = hipFreeAsync(scratch, stream);
+  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
+  return rc;
+}
+
+size_t ss_ready_schedule_lds(const ss_gmg *g) { return ready_schedule_lds((int)g->n_dev, (int)g->n_req); }
+
+int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
+                          uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream) {
+  const GmgView &G = g->view;
+  const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req;
+  const size_t lds = ss_ready_schedule_lds(g);
+  int cus = 0;
+  hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, g->device);
+  if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
+  err = hipFuncSetAttribute(reinterpret_cast<const void *>(&ready_schedule), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds);
+  if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
+  const bool iv_fast = g->n_class == 1 && g->n_link <= 2 && g->max_outdeg <= 2;
+  // chunk: finish times, ranks, missing-predecessor counts and the spill list
+  // of each candidate (candidate rows)
+  const int64_t per_cand = N * (4 + 2 + 2 + 8);
+  int64_t chunk = kScratchBudget / std::max<int64_t>(1, per_cand);
+  chunk = std::min<int64_t>(std::max<int64_t>(1, chunk), B);
+  const int64_t rec_per_cand = (N + E + 2) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4;
+  int64_t sub = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
+  sub = std::min<int64_t>(sub, chunk);
+  const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
+  const int64_t slot_cap = N + E + 1;
+
+  auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
+  const size_t sz_fin = align((size_t)chunk * N * 4 + 4);
+  const size_t sz_rank = align(((size_t)chunk * N + 1) * 2);
+  const size_t sz_miss = align(((size_t)chunk * N + 1) * 2);
+  const size_t sz_spill = align((size_t)chunk * N * 8 + 8);
+  const size_t sz_own = align((size_t)sub * (N + 1) * sizeof(Rec));
+  const size_t sz_cp = align((size_t)sub * (E + 1) * sizeof(Rec));
+  const size_t sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
+  const size_t sz_wk = align((size_t)nslots * 2 * (slot_cap + 2) * 4);
+  const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
+  void *scratch = nullptr;
+  err = hipMallocAsync(&scratch, sz_fin + sz_rank + sz_miss + sz_spill + sz_own + sz_cp + sz_meta + sz_wk + sz_wb,
+                       stream);
+  if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of simulation scratch");
+  unsigned char *p = static_cast<unsigned char *>(scratch);
+  auto take = [&](size_t bytes) {
+    unsigned char *q = p;
+    p += bytes;
+    return q;
+  };
+  auto *fin = reinterpret_cast<uint32_t *>(take(sz_fin));
+  auto *rank = reinterpret_cast<uint16_t *>(take(sz_rank));
+  auto *miss = reinterpret_cast<uint16_t *>(take(sz_miss));
+  auto *spill = reinterpret_cast<uint64_t *>(take(sz_spill));
+  auto *own = reinterpret_cast<Rec *>(take(sz_own));
+  auto *cp = reinterpret_cast<Rec *>(take(sz_cp));
+  auto *meta = reinterpret_cast<int32_t *>(take(sz_meta));
+  auto *wk = reinterpret_cast<uint32_t *>(take(sz_wk));
+  auto *wb = reinterpret_cast<int64_t *>(take(sz_wb));
+
+  int rc = SS_OK;
+  for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
+    const int64_t nb = std::min(chunk, B - b0);
+    const uint8_t *Pc = P + b0 * N;
+    SsTimingRec *ts = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
+    hipLaunchKernelGGL(ready_schedule, dim3((unsigned)nb), dim3(kWave), lds, stream, G, Pc, fin, rank, miss, spill,
+                       makespan + b0, sumfin ? sumfin + b0 : nullptr, slack ? slack + b0 * R : nullptr,
+                       violation + b0);
+    ss_timing_stop(ts, stream);
+    err = hipGetLastError();
+    if (err != hipSuccess) {
+      rc = hip_fail(err, "ready_schedule launch");
+      break;
     }
+    const MemPass M{own, cp, meta, rank, wk, wb, sub, nslots, slot_cap, iv_fast};
+    rc = memory_passes(g, M, Pc, fin, nb, true, peak ? peak + b0 * D : nullptr, violation + b0, stream);
   }
   err = hipFreeAsync(scratch, stream);
   if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");

@@ -402,10 +402,15 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
 // state fits; SS_PATH=generic or SS_PATH=fast in the environment forces one
 // (fast is still refused when the GMG does not qualify).
 int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
-                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream) {
+                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch) {
   int lds_max = 0;
   hipError_t err = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
+  if (ready_dispatch) {
+    if (!g->view.time32 || ss_ready_schedule_lds(g) > (size_t)lds_max)
+      return ss_set_error(SS_ERR_UNSUPPORTED, "ready-time dispatch needs the 32-bit path");
+    return ss_run_simulate_ready(g, P, B, makespan, peak, violation, slack, sumfin, stream);
+  }
   const bool fast_ok = g->view.time32 && ss_fast_schedule_lds(g) <= (size_t)lds_max;
   const char *path = std::getenv("SS_PATH");
   if (path && std::strcmp(path, "fast") == 0 && !fast_ok)

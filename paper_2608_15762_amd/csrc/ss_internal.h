@@ -51,6 +51,10 @@ struct GmgView {
   const uint32_t *lut_k;
   const uint4 *lut_w;
   int32_t lut_nb, lut_shift;
+  // ops without predecessors sorted by (release of their request, index), as
+  // release << 16 | op, for the ready-time dispatch
+  const uint64_t *src_keys;
+  int32_t n_src;
 };
 
 // Fields of op_meta for op v.  Predecessors beyond the first four and link
@@ -89,10 +93,14 @@ void ss_timing_stop(SsTimingRec *rec, hipStream_t stream);
 
 // Kernel drivers (simulate.hip / select.hip).  Arguments are already checked.
 int ss_run_simulate(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
-                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream);
+                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch);
 // Fast path (sim_fast.hip): 32-bit times, N <= 65535.
 size_t ss_fast_schedule_lds(const ss_gmg *g);
 int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
                          uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream);
+// Ready-time dispatch on the fast path (sim_fast.hip).
+size_t ss_ready_schedule_lds(const ss_gmg *g);
+int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
+                          uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream);
 int ss_run_select(const ss_gmg *g, const uint8_t *violation, const int64_t *key, const int64_t *slack, int64_t B,
                   int require_sla, int64_t *out_best, hipStream_t stream);

@@ -19,6 +19,8 @@ SS_OK = 0
 ERRORS = {-1: "SS_ERR_INVALID_ARG", -2: "SS_ERR_INVALID_GMG", -3: "SS_ERR_OOM", -4: "SS_ERR_DEVICE",
           -5: "SS_ERR_UNSUPPORTED"}
 SS_LAYOUT_ROW_MAJOR = 0
+SS_DISPATCH_READY = 0x100
+DISPATCH = {"index": 0, "ready": SS_DISPATCH_READY}
 SS_VIOLATION_MEMORY = 0x1
 SS_VIOLATION_INVALID = 0x4
 SS_SELECT_REQUIRE_SLA = 0x1
@@ -127,16 +129,21 @@ class Gmg:
 
 
 def simulate_batch_into(g: Gmg, placements, makespan, violation, peak=None, slack=None, sumfin=None,
-                        stream=None):
-    """ss_simulate_batch on caller-provided torch CUDA tensors (row-major)."""
+                        stream=None, dispatch="index"):
+    """ss_simulate_batch on caller-provided torch CUDA tensors (row-major).
+
+    dispatch: "index" (every device serves its ops in index order) or "ready"
+    (earliest ready time first, SS_DISPATCH_READY)."""
     B = placements.shape[0]
     assert placements.dtype.is_floating_point is False and placements.element_size() == 1
     assert placements.is_contiguous() and placements.shape == (B, g.n_ops)
-    _check(lib().ss_simulate_batch(g.handle, _ptr(placements), B, SS_LAYOUT_ROW_MAJOR, _ptr(makespan), _ptr(peak),
+    layout = SS_LAYOUT_ROW_MAJOR | DISPATCH[dispatch]
+    _check(lib().ss_simulate_batch(g.handle, _ptr(placements), B, layout, _ptr(makespan), _ptr(peak),
                                    _ptr(violation), _ptr(slack), _ptr(sumfin), _stream_ptr(stream)))
 
 
-def simulate_batch(g: Gmg, placements, want_peak=True, want_slack=True, want_sumfin=True, stream=None) -> dict:
+def simulate_batch(g: Gmg, placements, want_peak=True, want_slack=True, want_sumfin=True, stream=None,
+                   dispatch="index") -> dict:
     """Allocate outputs on placements' device and run ss_simulate_batch."""
     import torch
     B = placements.shape[0]
@@ -147,7 +154,7 @@ def simulate_batch(g: Gmg, placements, want_peak=True, want_slack=True, want_sum
                slack=torch.empty((B, g.n_req), dtype=torch.int64, device=dev) if want_slack else None,
                sumfin=torch.empty(B, dtype=torch.int64, device=dev) if want_sumfin else None)
     simulate_batch_into(g, placements, out["makespan"], out["violation"], out["peak"], out["slack"], out["sumfin"],
-                        stream)
+                        stream, dispatch)
     return out
 
 

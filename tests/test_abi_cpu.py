@@ -108,3 +108,27 @@ def test_loader_rejects_too_many_devices():
 def test_last_error_is_per_call():
     assert load_rc(_mut(BAD["zero_duration"])) == -2
     assert b"duration" in ss.lib().ss_last_error()
+
+
+def header_constants():
+    text = open(os.path.join(ROOT, "include", "ss.h")).read()
+    return {k: int(v, 0) for k, v in re.findall(r"#define\s+(SS_[A-Z_0-9]+)\s+\(?(-?(?:0x)?[0-9A-Fa-f]+)\)?", text)}
+
+
+def test_binding_constants_match_the_header():
+    c = header_constants()
+    assert c["SS_LAYOUT_ROW_MAJOR"] == ss.SS_LAYOUT_ROW_MAJOR
+    assert c["SS_DISPATCH_READY"] == ss.SS_DISPATCH_READY == ss.DISPATCH["ready"]
+    assert c["SS_DISPATCH_READY"] & c["SS_LAYOUT_ROW_MAJOR"] == 0
+    assert c["SS_VIOLATION_MEMORY"] == ss.SS_VIOLATION_MEMORY and c["SS_VIOLATION_INVALID"] == ss.SS_VIOLATION_INVALID
+    assert c["SS_SELECT_REQUIRE_SLA"] == ss.SS_SELECT_REQUIRE_SLA
+    for code, name in ss.ERRORS.items():
+        assert c[name] == code
+
+
+def test_unknown_layout_bits_are_rejected_before_the_device():
+    L = ss.lib()
+    # a non-null dummy handle is never dereferenced: the layout check comes first
+    for layout in (1, 0x200, 0x101):
+        assert L.ss_simulate_batch(ctypes.c_void_p(8), None, 1, layout, None, None, None, None, None, None) == -1
+        assert b"layout" in L.ss_last_error()
