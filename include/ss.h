@@ -140,11 +140,10 @@ int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req)
  * all been dispatched, the one with the earliest ready time (ties to the lower
  * index) is dispatched next, at the earliest fit on its device at or after
  * max(ready time, that device's previous finish).  Memory follows the same
- * definitions with "last" meaning the consumer that finishes last.  This rule
- * needs the 32-bit evaluation (the horizon H below 2^32 - 1, n_ops, n_edges
- * and every device's slice count at most 65535, out_bytes below 2^32, and the
- * per-candidate device state within one workgroup's LDS); otherwise the call
- * returns SS_ERR_UNSUPPORTED.
+ * definitions with "last" meaning the consumer that finishes last.  Both
+ * rules accept every GMG the loader accepts; the ready-time rule evaluates a
+ * candidate with one wavefront instead of one lane, so it costs more per
+ * candidate, and it needs scratch for N ready entries per candidate in flight.
  * A candidate naming a device >= n_dev is not simulated: violation =
  * SS_VIOLATION_INVALID, makespan = sumfin = INT64_MAX, peak = 0 and slack =
  * INT64_MIN.  This is a per-candidate result, not a call error.

@@ -146,10 +146,16 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
                         max_bytes <= (int64_t)UINT32_MAX;
     std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32, meta, lbits, bytes32, succ2, lutk, lutw;
     std::vector<uint8_t> lgrp;
-    std::vector<uint64_t> src_keys;  // ready-time dispatch: sources by (release, index)
+    // ready-time dispatch: the ops without predecessors by (release of their
+    // request, index); on the 32-bit path also as keys release << 16 | op
+    std::vector<int32_t> src_ops;
     for (int64_t v = 0; v < N; ++v)
-      if (d->pred_ptr[v + 1] == d->pred_ptr[v]) src_keys.push_back((uint64_t)d->release[d->op_req[v]] << 16 | (uint64_t)v);
-    std::sort(src_keys.begin(), src_keys.end());
+      if (d->pred_ptr[v + 1] == d->pred_ptr[v]) src_ops.push_back((int32_t)v);
+    std::stable_sort(src_ops.begin(), src_ops.end(),
+                     [&](int32_t a, int32_t b) { return d->release[d->op_req[a]] < d->release[d->op_req[b]]; });
+    std::vector<uint64_t> src_keys;
+    if (time32)
+      for (const int32_t v : src_ops) src_keys.push_back((uint64_t)d->release[d->op_req[v]] << 16 | (uint64_t)v);
     int32_t lsame = 0;
     int64_t lut_nb = 0, lut_shift = 0;
     int64_t max_outdeg = 0;
@@ -274,7 +280,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     const size_t o_dur32 = pk.add(dur32), o_xfer32 = pk.add(xfer32), o_sb32 = pk.add(sb32), o_se32 = pk.add(se32),
                  o_rel32 = pk.add(rel32), o_meta = pk.add(meta), o_lbits = pk.add(lbits), o_b32 = pk.add(bytes32),
                  o_succ2 = pk.add(succ2), o_lutk = pk.add(lutk), o_lutw = pk.add(lutw), o_lgrp = pk.add(lgrp),
-                 o_src = pk.add(src_keys);
+                 o_src = pk.add(src_keys), o_src_ops = pk.add(src_ops);
     pk.add(nullptr, 256);  // tail padding
 
     ss_gmg *g = new ss_gmg();
@@ -328,7 +334,8 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     V.succ2 = succ2.empty() ? nullptr : reinterpret_cast<const uint32_t *>(base + o_succ2);
     V.link_grp = lgrp.empty() ? nullptr : reinterpret_cast<const uint8_t *>(base + o_lgrp);
     V.src_keys = reinterpret_cast<const uint64_t *>(base + o_src);
-    V.n_src = (int32_t)src_keys.size();
+    V.src_ops = reinterpret_cast<const int32_t *>(base + o_src_ops);
+    V.n_src = (int32_t)src_ops.size();
     V.link_same = lsame;
     V.lut_k = reinterpret_cast<const uint32_t *>(base + o_lutk);
     V.lut_w = reinterpret_cast<const uint4 *>(base + o_lutw);

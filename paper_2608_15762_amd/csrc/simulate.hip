@@ -10,6 +10,9 @@
 //   (all lanes are at the same op), so it is read with wave-uniform loads.
 //   Finish times go to a per-chunk scratch row for the memory pass.
 //
+// ready_schedule_general: the ready-time dispatch rule, one wave per
+//   candidate (the ready set is searched by the whole wave at every step).
+//
 // memory_kernel: one wave per candidate.  It groups the candidate's ops by
 //   device, then for each device builds the endpoints of the residency
 //   intervals resident there (own outputs and remote copies, Sec. 3.3.2),
@@ -111,6 +114,227 @@ __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const 
   }
 }
 
+// ------------------------------------------------------------------ ready-time dispatch
+// The dispatch rule of Sec. 3.3.2 on the general path: among the ops whose
+// predecessors have all been scheduled, the one with the earliest ready time
+// (ties to the lower index) runs next, at the earliest fit on its device at or
+// after max(ready time, the device's previous finish).  One wave per
+// candidate.  Ready ops are (ready, op) pairs held kGenSlots per lane, and
+// beyond that in the candidate's spill list (at most N entries: ready ops form
+// an antichain), scanned while non-empty; sources come from the presorted
+// src_ops list.  A device's clock never decreases, so its slice cursor (LDS)
+// only moves forward.  The wave writes finish times (candidate rows, as
+// schedule_kernel does) and the per-candidate outputs; request completions
+// live in comp rows [candidate][R].
+constexpr int kGenSlots = 4;
+
+__device__ __forceinline__ bool pair_less(int64_t r1, int o1, int64_t r2, int o2) {
+  return r1 < r2 || (r1 == r2 && o1 < o2);
+}
+
+__device__ __forceinline__ void wave_min_pair(int64_t &r, int &o) {
+  for (int off = kWave / 2; off >= 1; off >>= 1) {
+    const int64_t r2 = __shfl_xor(r, off, kWave);
+    const int o2 = __shfl_xor(o, off, kWave);
+    if (pair_less(r2, o2, r, o)) {
+      r = r2;
+      o = o2;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kWave) void ready_schedule_general(
+    const GmgView G, const uint8_t *__restrict__ P, int64_t *__restrict__ fin, int32_t *__restrict__ missing,
+    int64_t *__restrict__ spill_r, int32_t *__restrict__ spill_o, int64_t *__restrict__ comp,
+    int64_t *__restrict__ makespan, int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
+    uint8_t *__restrict__ violation) {
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = G.n_class, K = G.n_link;
+  const int lane = threadIdx.x;
+  int64_t *clk = reinterpret_cast<int64_t *>(lds_raw);                     // [D]
+  int32_t *cur = reinterpret_cast<int32_t *>(lds_raw + (size_t)D * 8);   // [D] slice cursor
+  const int64_t c = blockIdx.x;
+  const uint8_t *prow = P + c * N;
+  int64_t *frow = fin + c * N;
+  int32_t *mrow = missing + c * N;
+  int64_t *srr = spill_r + c * N;
+  int32_t *sro = spill_o + c * N;
+  int64_t *crow = comp + c * R;
+  bool bad = false;
+  for (int v = lane; v < N; v += kWave) bad |= prow[v] >= (uint8_t)D;
+  if (__any(bad)) {
+    if (lane == 0) {
+      makespan[c] = INT64_MAX;
+      if (sumfin) sumfin[c] = INT64_MAX;
+      violation[c] = SS_VIOLATION_INVALID;
+    }
+    if (slack)
+      for (int r = lane; r < R; r += kWave) slack[c * R + r] = INT64_MIN;
+    return;
+  }
+  for (int d = lane; d < D; d += kWave) {
+    clk[d] = 0;
+    cur[d] = 0;
+  }
+  for (int r = lane; r < R; r += kWave) crow[r] = G.release[r];
+  for (int v = lane; v < N; v += kWave) mrow[v] = G.pred_ptr[v + 1] - G.pred_ptr[v];
+  __syncthreads();  // LDS state and this wave's rows before the loop reads them
+
+  constexpr int64_t kNoR = INT64_MAX;
+  constexpr int kNoO = INT32_MAX;
+  int64_t sr[kGenSlots];
+  int so[kGenSlots];
+#pragma unroll
+  for (int k = 0; k < kGenSlots; ++k) {
+    sr[k] = kNoR;
+    so[k] = kNoO;
+  }
+  int sp = 0, ns = 0;  // next source, spill length (wave-uniform)
+  int64_t ms = 0, sum = 0;
+  for (int step = 0; step < N; ++step) {
+    int64_t mr = sr[0];
+    int mo = so[0];
+#pragma unroll
+    for (int k = 1; k < kGenSlots; ++k)
+      if (pair_less(sr[k], so[k], mr, mo)) {
+        mr = sr[k];
+        mo = so[k];
+      }
+    int64_t wr = mr;
+    int wo = mo;
+    wave_min_pair(wr, wo);
+    int64_t xr = kNoR;
+    int xo = kNoO, xi = 0;
+    if (ns > 0) {  // smallest spilled pair and its position
+      int li = 0;
+      for (int i = lane; i < ns; i += kWave) {
+        const int64_t r = srr[i];
+        const int o = sro[i];
+        if (pair_less(r, o, xr, xo)) {
+          xr = r;
+          xo = o;
+          li = i;
+        }
+      }
+      const int64_t lr = xr;
+      const int lo = xo;
+      wave_min_pair(xr, xo);
+      xi = __shfl(li, __ffsll((unsigned long long)__ballot(lr == xr && lo == xo)) - 1, kWave);
+    }
+    int64_t qr = kNoR;
+    int qo = kNoO;
+    if (sp < G.n_src) {
+      qo = G.src_ops[sp];
+      qr = G.release[G.op_req[qo]];
+    }
+    int v;
+    int64_t ready;
+    if (pair_less(qr, qo, wr, wo) && pair_less(qr, qo, xr, xo)) {
+      v = qo;
+      ready = qr;
+      ++sp;
+    } else if (pair_less(xr, xo, wr, wo)) {
+      v = xo;
+      ready = xr;
+      --ns;
+      if (lane == 0) {  // the last entry fills the hole
+        srr[xi] = srr[ns];
+        sro[xi] = sro[ns];
+      }
+    } else {
+      v = wo;
+      ready = wr;
+      const int owner = __ffsll((unsigned long long)__ballot(mr == wr && mo == wo)) - 1;
+      if (lane == owner) {
+        bool done = false;
+#pragma unroll
+        for (int k = 0; k < kGenSlots; ++k)
+          if (!done && so[k] == wo) {
+            sr[k] = kNoR;
+            so[k] = kNoO;
+            done = true;
+          }
+      }
+    }
+    const int d = prow[v];
+    const int64_t w = G.dur[(int64_t)v * C + G.dev_class[d]];
+    const int64_t t = imax(ready, clk[d]);
+    const int sbase = G.slice_ptr[d];
+    int k = cur[d];
+    int64_t s;
+    for (;;) {
+      const int64_t a = G.slice_begin[sbase + k], e = G.slice_end[sbase + k];
+      s = imax(t, a);
+      if (s + w <= e) break;
+      ++k;
+    }
+    const int64_t f = s + w;
+    const int r = G.op_req[v];
+    const int64_t cr = crow[r];
+    __syncthreads();  // every lane has read the LDS state and the rows
+    if (lane == 0) {
+      cur[d] = k;
+      clk[d] = f;
+      frow[v] = f;
+      crow[r] = imax(cr, f);
+    }
+    __syncthreads();
+    ms = imax(ms, f);
+    sum += f;
+    // successors whose last missing predecessor this was become ready
+    const int q1 = G.succ_ptr[v + 1];
+    for (int q = G.succ_ptr[v]; q < q1; ++q) {
+      const int x = G.succ_idx[q];
+      const int left = mrow[x] - 1;
+      __syncthreads();
+      if (lane == 0) mrow[x] = left;
+      __syncthreads();
+      if (left == 0) {
+        const int dx = prow[x];
+        int64_t rx = G.release[G.op_req[x]];
+        const int e1 = G.pred_ptr[x + 1];
+        for (int e = G.pred_ptr[x]; e < e1; ++e) {
+          const int u = G.pred_idx[e];
+          const int du = prow[u];
+          int64_t tu = u == v ? f : frow[u];
+          if (du != dx) tu += G.xfer[(int64_t)u * K + G.link_class[du * D + dx]];
+          rx = imax(rx, tu);
+        }
+        bool placed = false;
+#pragma unroll
+        for (int kk = 0; kk < kGenSlots; ++kk) {
+          if (!placed) {
+            const unsigned long long free_lanes = __ballot(so[kk] == kNoO);
+            if (free_lanes) {
+              if (lane == __ffsll(free_lanes) - 1) {
+                sr[kk] = rx;
+                so[kk] = x;
+              }
+              placed = true;
+            }
+          }
+        }
+        if (!placed) {
+          if (lane == 0) {
+            srr[ns] = rx;
+            sro[ns] = x;
+          }
+          ++ns;
+          __syncthreads();
+        }
+      }
+    }
+  }
+  if (lane == 0) {
+    makespan[c] = ms;
+    if (sumfin) sumfin[c] = sum;
+    violation[c] = 0;
+  }
+  __syncthreads();
+  if (slack)
+    for (int r = lane; r < R; r += kWave) slack[c * R + r] = G.deadline[r] - crow[r];
+}
+
 // ------------------------------------------------------------------ memory
 // Interval endpoints contributed by op y placed on device e: its own output
 // (allocated at its start, freed when its last local consumer has finished and
@@ -119,7 +343,9 @@ __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const 
 // predecessor's copy on e (allocated at the predecessor's finish, freed at y's
 // finish).  Key = 2 * time + (1 for an allocation), so frees sort first at
 // equal times (half-open intervals).  Zero-byte tensors contribute nothing.
-template <bool kWrite, class KP, class VP>
+// kReady: the copy's last consumer on e is the one that finishes last (index
+// order and finish order agree under index-order dispatch).
+template <bool kWrite, bool kReady, class KP, class VP>
 __device__ int op_events(const GmgView &G, const uint8_t *prow, const int64_t *frow, int y, int e, KP keys,
                          VP vals, int w) {
   const int C = G.n_class, K = G.n_link, D = G.n_dev;
@@ -156,12 +382,22 @@ __device__ int op_events(const GmgView &G, const uint8_t *prow, const int64_t *f
     if (bu == 0) continue;
     bool last = true;  // no consumer of u on e after y?
     const int s0 = G.succ_ptr[u];
-    for (int s = G.succ_ptr[u + 1] - 1; s >= s0; --s) {
-      const int x = G.succ_idx[s];
-      if (x <= y) break;
-      if (prow[x] == e) {
-        last = false;
-        break;
+    if (kReady) {  // one op at a time on e: finishes there are distinct
+      for (int s = s0; s < G.succ_ptr[u + 1]; ++s) {
+        const int x = G.succ_idx[s];
+        if (prow[x] == e && frow[x] > fy) {
+          last = false;
+          break;
+        }
+      }
+    } else {
+      for (int s = G.succ_ptr[u + 1] - 1; s >= s0; --s) {
+        const int x = G.succ_idx[s];
+        if (x <= y) break;
+        if (prow[x] == e) {
+          last = false;
+          break;
+        }
       }
     }
     if (!last) continue;
@@ -247,6 +483,7 @@ __device__ __forceinline__ int wave_exclusive_scan(int x, int lane, int *total) 
   return s - x;
 }
 
+template <bool kReady>
 __global__ __launch_bounds__(kWave) void memory_kernel(const GmgView G, const uint8_t *__restrict__ P, int64_t nb,
                                                        const int64_t *__restrict__ fin, int32_t *__restrict__ bydev_all,
                                                        int64_t *__restrict__ gkeys_all,
@@ -296,16 +533,18 @@ __global__ __launch_bounds__(kWave) void memory_kernel(const GmgView G, const ui
       if (hi > lo) {
         int mine = 0;
         for (int q = lo + lane; q < hi; q += kWave)
-          mine += op_events<false>(G, prow, frow, bydev[q], e, (int64_t *)nullptr, (int64_t *)nullptr, 0);
+          mine += op_events<false, kReady>(G, prow, frow, bydev[q], e, (int64_t *)nullptr, (int64_t *)nullptr, 0);
         int total;
         int w = wave_exclusive_scan(mine, lane, &total);
         if (total <= kMemCap) {
-          for (int q = lo + lane; q < hi; q += kWave) w += op_events<true>(G, prow, frow, bydev[q], e, skeys, svals, w);
+          for (int q = lo + lane; q < hi; q += kWave)
+            w += op_events<true, kReady>(G, prow, frow, bydev[q], e, skeys, svals, w);
           __syncthreads();
           sort_pairs(skeys, svals, total, lane);
           pk = max_prefix_sum(svals, total, lane);
         } else {
-          for (int q = lo + lane; q < hi; q += kWave) w += op_events<true>(G, prow, frow, bydev[q], e, gkeys, gvals, w);
+          for (int q = lo + lane; q < hi; q += kWave)
+            w += op_events<true, kReady>(G, prow, frow, bydev[q], e, gkeys, gvals, w);
           __syncthreads();
           sort_pairs(gkeys, gvals, total, lane);
           pk = max_prefix_sum(gvals, total, lane);
@@ -327,14 +566,18 @@ int hip_fail(hipError_t err, const char *what) {
 
 }  // namespace
 
-// General path: int64 times, any size the loader accepts.
+// General path: int64 times, any size the loader accepts; either dispatch rule.
 static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
-                                uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream) {
+                                uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream,
+                                bool ready) {
   const GmgView &G = g->view;
   const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req;
   const int64_t slot_cap = 2 * (N + E) + 2;
   if (slot_cap >= INT32_MAX) return ss_set_error(SS_ERR_UNSUPPORTED, "n_ops + n_edges too large for the memory pass");
-  const size_t sched_lds = (size_t)D * kWave * (sizeof(int64_t) + sizeof(uint16_t));
+  const void *sched_fn = ready ? reinterpret_cast<const void *>(&ready_schedule_general)
+                               : reinterpret_cast<const void *>(&schedule_kernel);
+  const size_t sched_lds = ready ? (size_t)D * (sizeof(int64_t) + sizeof(int32_t))
+                                 : (size_t)D * kWave * (sizeof(int64_t) + sizeof(uint16_t));
   int cus = 0;
   hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
@@ -346,11 +589,13 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
     lds_max = (size_t)v;
   }
   if (sched_lds > lds_max) return ss_set_error(SS_ERR_UNSUPPORTED, "device state of the schedule pass exceeds LDS");
-  err = hipFuncSetAttribute(reinterpret_cast<const void *>(&schedule_kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
+  err = hipFuncSetAttribute(sched_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
   if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
 
-  int64_t chunk = kFinBudget / std::max<int64_t>(1, N * 8);
+  // per candidate: finish times and request completions; with ready-time
+  // dispatch also missing-predecessor counts and the spill list
+  const int64_t per_cand = N * 8 + R * 8 + (ready ? N * (4 + 8 + 4) : 0);
+  int64_t chunk = kFinBudget / std::max<int64_t>(1, per_cand);
   chunk = std::max<int64_t>(kWave, chunk / kWave * kWave);
   chunk = std::min<int64_t>(chunk, B);
   const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kMemBlocksPerCU, chunk));
@@ -358,36 +603,52 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
   const size_t sz_fin = align((size_t)chunk * N * 8 + 8);
   const size_t sz_comp = align((size_t)chunk * R * 8 + 8);
+  const size_t sz_miss = ready ? align((size_t)chunk * N * 4 + 4) : 0;
+  const size_t sz_spr = ready ? align((size_t)chunk * N * 8 + 8) : 0;
+  const size_t sz_spo = ready ? align((size_t)chunk * N * 4 + 4) : 0;
   const size_t sz_bydev = align((size_t)nslots * N * 4 + 4);
   const size_t sz_ev = align((size_t)nslots * slot_cap * 8);
   void *scratch = nullptr;
-  err = hipMallocAsync(&scratch, sz_fin + sz_comp + sz_bydev + 2 * sz_ev, stream);
+  err = hipMallocAsync(&scratch, sz_fin + sz_comp + sz_miss + sz_spr + sz_spo + sz_bydev + 2 * sz_ev, stream);
   if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of simulation scratch");
-  auto *base = static_cast<unsigned char *>(scratch);
-  auto *fin = reinterpret_cast<int64_t *>(base);
-  auto *comp = reinterpret_cast<int64_t *>(base + sz_fin);
-  auto *bydev = reinterpret_cast<int32_t *>(base + sz_fin + sz_comp);
-  auto *gkeys = reinterpret_cast<int64_t *>(base + sz_fin + sz_comp + sz_bydev);
-  auto *gvals = reinterpret_cast<int64_t *>(base + sz_fin + sz_comp + sz_bydev + sz_ev);
+  unsigned char *p = static_cast<unsigned char *>(scratch);
+  auto take = [&](size_t bytes) {
+    unsigned char *q = p;
+    p += bytes;
+    return q;
+  };
+  auto *fin = reinterpret_cast<int64_t *>(take(sz_fin));
+  auto *comp = reinterpret_cast<int64_t *>(take(sz_comp));
+  auto *miss = reinterpret_cast<int32_t *>(take(sz_miss));
+  auto *spr = reinterpret_cast<int64_t *>(take(sz_spr));
+  auto *spo = reinterpret_cast<int32_t *>(take(sz_spo));
+  auto *bydev = reinterpret_cast<int32_t *>(take(sz_bydev));
+  auto *gkeys = reinterpret_cast<int64_t *>(take(sz_ev));
+  auto *gvals = reinterpret_cast<int64_t *>(take(sz_ev));
 
   int rc = SS_OK;
   for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
     const int64_t nb = std::min(chunk, B - b0);
     const uint8_t *Pc = P + b0 * N;
     SsTimingRec *t_sched = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
-    hipLaunchKernelGGL(schedule_kernel, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), sched_lds, stream,
-                       G, Pc, nb, fin, comp, makespan + b0, sumfin ? sumfin + b0 : nullptr,
-                       slack ? slack + b0 * R : nullptr, violation + b0);
+    if (ready)
+      hipLaunchKernelGGL(ready_schedule_general, dim3((unsigned)nb), dim3(kWave), sched_lds, stream, G, Pc, fin, miss,
+                         spr, spo, comp, makespan + b0, sumfin ? sumfin + b0 : nullptr,
+                         slack ? slack + b0 * R : nullptr, violation + b0);
+    else
+      hipLaunchKernelGGL(schedule_kernel, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), sched_lds, stream,
+                         G, Pc, nb, fin, comp, makespan + b0, sumfin ? sumfin + b0 : nullptr,
+                         slack ? slack + b0 * R : nullptr, violation + b0);
     err = hipGetLastError();
     ss_timing_stop(t_sched, stream);
     if (err != hipSuccess) {
-      rc = hip_fail(err, "schedule_kernel launch");
+      rc = hip_fail(err, "schedule launch");
       break;
     }
     const int64_t grid = std::min<int64_t>(nb, nslots);
     SsTimingRec *t_mem = ss_timing_start(SS_KERNEL_MEMORY, stream);
-    hipLaunchKernelGGL(memory_kernel, dim3((unsigned)grid), dim3(kWave), 0, stream, G, Pc, nb,
-                       static_cast<const int64_t *>(fin), bydev, gkeys, gvals, slot_cap,
+    hipLaunchKernelGGL(ready ? memory_kernel<true> : memory_kernel<false>, dim3((unsigned)grid), dim3(kWave), 0,
+                       stream, G, Pc, nb, static_cast<const int64_t *>(fin), bydev, gkeys, gvals, slot_cap,
                        peak ? peak + b0 * D : nullptr, violation + b0);
     err = hipGetLastError();
     ss_timing_stop(t_mem, stream);
@@ -406,16 +667,13 @@ int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makes
   int lds_max = 0;
   hipError_t err = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
-  if (ready_dispatch) {
-    if (!g->view.time32 || ss_ready_schedule_lds(g) > (size_t)lds_max)
-      return ss_set_error(SS_ERR_UNSUPPORTED, "ready-time dispatch needs the 32-bit path");
-    return ss_run_simulate_ready(g, P, B, makespan, peak, violation, slack, sumfin, stream);
-  }
-  const bool fast_ok = g->view.time32 && ss_fast_schedule_lds(g) <= (size_t)lds_max;
+  const bool fast_ok = g->view.time32 && (ready_dispatch ? ss_ready_schedule_lds(g) : ss_fast_schedule_lds(g)) <=
+                                             (size_t)lds_max;
   const char *path = std::getenv("SS_PATH");
   if (path && std::strcmp(path, "fast") == 0 && !fast_ok)
     return ss_set_error(SS_ERR_UNSUPPORTED, "SS_PATH=fast but this GMG needs the general path");
   const bool generic = !fast_ok || (path && std::strcmp(path, "generic") == 0);
-  if (generic) return run_simulate_generic(g, P, B, makespan, peak, violation, slack, sumfin, stream);
+  if (generic) return run_simulate_generic(g, P, B, makespan, peak, violation, slack, sumfin, stream, ready_dispatch);
+  if (ready_dispatch) return ss_run_simulate_ready(g, P, B, makespan, peak, violation, slack, sumfin, stream);
   return ss_run_simulate_fast(g, P, B, makespan, peak, violation, slack, sumfin, stream);
 }

@@ -51,8 +51,10 @@ struct GmgView {
   const uint32_t *lut_k;
   const uint4 *lut_w;
   int32_t lut_nb, lut_shift;
-  // ops without predecessors sorted by (release of their request, index), as
-  // release << 16 | op, for the ready-time dispatch
+  // ready-time dispatch: the n_src ops without predecessors sorted by
+  // (release of their request, index); src_keys holds them as release << 16 |
+  // op on the 32-bit path
+  const int32_t *src_ops;
   const uint64_t *src_keys;
   int32_t n_src;
 };

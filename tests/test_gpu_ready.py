@@ -20,6 +20,17 @@ pytestmark = pytest.mark.gpu
 FIELDS = ("makespan", "peak", "violation", "slack", "sumfin")
 
 
+@pytest.fixture(params=["auto", "generic"])
+def path(request, monkeypatch):
+    """Run a case on the default path (the 32-bit path when the GMG qualifies)
+    and on the general int64 path."""
+    if request.param == "generic":
+        monkeypatch.setenv("SS_PATH", "generic")
+    else:
+        monkeypatch.delenv("SS_PATH", raising=False)
+    return request.param
+
+
 @pytest.fixture(scope="module")
 def dev():
     assert torch.cuda.is_available(), "GPU tests need a GPU"
@@ -55,7 +66,7 @@ def random_placements(g, seed, B, invalid_every=0):
 
 
 @pytest.mark.parametrize("cid,nb", [(0, 256), (1, 600), (2, 200), (3, 100), (4, 12)])
-def test_config_parity_ready(dev, cid, nb):
+def test_config_parity_ready(dev, path, cid, nb):
     print(f"ready dispatch, config {cid}: {nb} candidates", flush=True)
     g = synth.build_gmg(cid)
     P = synth.placements(g, cid, 0, nb)
@@ -74,7 +85,7 @@ FUZZ = [dict(n_ops=n, n_dev=D, n_req=R, n_slices=S, n_class=C, n_link=K, rel_max
 
 
 @pytest.mark.parametrize("seed", range(len(FUZZ)))
-def test_fuzz_parity_ready(dev, seed):
+def test_fuzz_parity_ready(dev, path, seed):
     kw = FUZZ[seed]
     print(f"ready dispatch, fuzz {seed}: {kw}", flush=True)
     g = synth.random_gmg(seed, **kw)
@@ -94,7 +105,7 @@ FAST_WRITER = [dict(n_ops=n, n_dev=D, n_req=R, n_slices=S, n_link=K, zero_bytes_
 
 
 @pytest.mark.parametrize("seed", range(len(FAST_WRITER)))
-def test_fast_writer_parity_ready(dev, seed):
+def test_fast_writer_parity_ready(dev, path, seed):
     """Graphs the branch-free interval writer takes, whose consumers on one
     device need not finish in index order under this rule."""
     kw = FAST_WRITER[seed]
@@ -107,7 +118,7 @@ def test_fast_writer_parity_ready(dev, seed):
     assert_same(got, ref, label=f"ready, fast writer {seed}")
 
 
-def test_ready_differs_from_index_order(dev):
+def test_ready_differs_from_index_order(dev, path):
     """The flag reaches the kernels: on random graphs the two rules give
     different schedules for some candidates, and each matches its oracle."""
     g = synth.random_gmg(5, **FUZZ[5])
@@ -132,7 +143,7 @@ def fan_out_gmg(width, n_dev):
 
 
 @pytest.mark.parametrize("width", [300, 1200])
-def test_wide_ready_set_spills(dev, width):
+def test_wide_ready_set_spills(dev, path, width):
     g = fan_out_gmg(width, 6)
     P = random_placements(g, width, 40)
     P[0] = 0  # everything on one device: the whole fan-out waits in the ready set
@@ -141,7 +152,7 @@ def test_wide_ready_set_spills(dev, width):
     assert_same(got, ref, label=f"ready, fan-out {width}")
 
 
-def test_zero_ops_and_empty_batch_ready(dev):
+def test_zero_ops_and_empty_batch_ready(dev, path):
     g = make_gmg(3, [], [], [], np.zeros((0, 1), np.int64), [], [[(0, TIME_INF)]] * 3, [5, 5, 5], [4], [10])
     P = np.zeros((5, 0), np.uint8)
     got = gpu_run(ss.Gmg(g), P, dev)
@@ -151,7 +162,7 @@ def test_zero_ops_and_empty_batch_ready(dev):
     assert empty["makespan"].shape == (0,)
 
 
-def test_nullable_outputs_ready(dev):
+def test_nullable_outputs_ready(dev, path):
     g = synth.build_gmg(1)
     P = synth.placements(g, 1, 3, 90)
     ref = oracle.simulate_batch(g, P, dispatch=oracle.READY_ORDER)
@@ -160,7 +171,7 @@ def test_nullable_outputs_ready(dev):
 
 
 @pytest.mark.parametrize("cid,n_sample", [(1, 128)])
-def test_full_batch_sampled_parity_ready(dev, cid, n_sample):
+def test_full_batch_sampled_parity_ready(dev, path, cid, n_sample):
     """A workload's whole batch in one call, sampled against the oracle."""
     g = synth.build_gmg(cid)
     B = synth.CONFIGS[cid].n_cand
@@ -171,3 +182,21 @@ def test_full_batch_sampled_parity_ready(dev, cid, n_sample):
     idx = np.unique(np.concatenate([[0, B - 1], rng.choice(B, n_sample, replace=False)]))
     ref = oracle.simulate_batch(g, P[idx], dispatch=oracle.READY_ORDER, n_threads=8)
     assert_same(got, ref, idx=idx, label=f"ready, config {cid} full")
+
+
+def test_horizon_beyond_32_bits_ready(dev, monkeypatch):
+    """Slices far beyond 2^32 us: the 32-bit path is refused and the general
+    path's ready-time dispatch still matches the oracle."""
+    g = synth.random_gmg(11, n_ops=90, n_dev=4, n_req=2, n_slices=4, n_link=2, cap_scale=2000)
+    shift = 1 << 33
+    g.slice_begin = g.slice_begin + shift
+    g.slice_end = np.where(g.slice_end == TIME_INF, TIME_INF, g.slice_end + shift)
+    P = random_placements(g, 5, 150)
+    ref = oracle.simulate_batch(g, P, dispatch=oracle.READY_ORDER)
+    assert ref["makespan"].min() > shift
+    h = ss.Gmg(g)
+    monkeypatch.delenv("SS_PATH", raising=False)
+    assert_same(gpu_run(h, P, dev), ref, label="ready, horizon 2^33")
+    monkeypatch.setenv("SS_PATH", "fast")
+    with pytest.raises(ss.SSError):
+        gpu_run(h, P, dev)
