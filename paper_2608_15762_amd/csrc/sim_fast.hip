@@ -601,6 +601,17 @@ size_t ready_schedule_lds(int D, int R) { return (size_t)(3 * D + R + 1 + D) * 4
 using Rec = uint4;
 constexpr uint32_t kLocWindow = 0x80000000u;
 
+// Records per candidate: own N plus a spare at index N, copies at most E plus
+// a spare at E, each region rounded to whole blocks of kBlockRecs records so
+// that every candidate's regions start on a block.
+constexpr int kBlockShift = 2, kBlockRecs = 1 << kBlockShift;  // 64-byte lines
+__host__ __device__ __forceinline__ int64_t own_stride(int64_t N) {
+  return (N + 1 + kBlockRecs - 1) & ~int64_t(kBlockRecs - 1);
+}
+__host__ __device__ __forceinline__ int64_t cp_stride(int64_t E) {
+  return (E + 1 + kBlockRecs - 1) & ~int64_t(kBlockRecs - 1);
+}
+
 __device__ __forceinline__ uint32_t loc_window(int L) { return kLocWindow | (uint32_t)max(L, 0); }
 
 // Intervals of op v (device d, rank rv among the ops of d): its own output at
@@ -725,6 +736,27 @@ struct IvSucc {  // device, finish and rank of the first two successors
   uint32_t dx0, dx1, fx0, fx1, rx0, rx1;
 };
 
+// Store staging.  A 64-byte line of a bucket holds the records of positions
+// 4L .. 4L+3.  A destination's records of one chunk have consecutive
+// positions [first, last], and with index ranks no later chunk writes below
+// them, so line L of a bucket [start, end) is complete once position
+// min(4L+3, end-1) has been produced.  A record's role:
+//   open   its line began in an earlier chunk: staged in LDS; the record that
+//          completes the line (close) queues it for a cooperative write
+//   direct its line lies inside this chunk's run and is complete: stored
+//   tail   its line begins in this chunk and is not complete: staged
+constexpr int kRoleNone = 0, kRoleDirect = 1, kRoleOpen = 2, kRoleClose = 6, kRoleTail = 8;
+
+__device__ __forceinline__ int line_role(int p, int first, int last, int end) {
+  const int L = p >> kBlockShift, Lo = first >> kBlockShift, Ll = last >> kBlockShift;
+  if (L == Lo) {
+    const int closer = min((Lo << kBlockShift) + kBlockRecs - 1, end - 1);
+    return (closer <= last && p == closer) ? kRoleClose : kRoleOpen;
+  }
+  const bool done = (L << kBlockShift) + kBlockRecs - 1 <= last || (last == end - 1 && L == Ll);
+  return done ? kRoleDirect : kRoleTail;
+}
+
 // kGivenRanks: the rank table already holds every op's rank on its device
 // (dispatch order), pass A only counts.
 template <bool kFast, bool kGivenRanks>
@@ -733,7 +765,20 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
                                                         Rec *__restrict__ own_all, Rec *__restrict__ cp_all,
                                                         int32_t *__restrict__ meta, uint16_t *__restrict__ rank_all,
                                                         const uint8_t *__restrict__ violation) {
-  __shared__ int own_off[257], cp_off[257], cfill[256], base[256], nocopy[kWave];
+  // LDS (dynamic, sized by the device count): bucket offsets and fill
+  // pointers; with staged stores (kFast with index ranks) also the open line of
+  // every device's own bucket and the queue of complete lines
+  constexpr bool kStage = kFast && !kGivenRanks;
+  extern __shared__ __align__(16) unsigned char iv_lds[];
+  const int Dv = G.n_dev;
+  Rec *obuf = reinterpret_cast<Rec *>(iv_lds);                             // [D][kBlockRecs]
+  int *own_off = reinterpret_cast<int *>(obuf + (kStage ? kBlockRecs * Dv : 0));  // [D+1]
+  int *cp_off = own_off + Dv + 1;                                          // [D+1]
+  int *cfill = cp_off + Dv + 1;                                            // [D] next copy slot
+  int *base = cfill + Dv;  // [D] ops counted so far; with staging then the next own position
+  int *nocopy = base + Dv;                                                 // [64]
+  uint32_t *fq = reinterpret_cast<uint32_t *>(nocopy + kWave);             // [64]
+  int &fqn = *reinterpret_cast<int *>(fq + kWave);
   const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops], K = G.n_link;
   const int lane = threadIdx.x;
   const int64_t j = blockIdx.x, c = j0 + j;
@@ -741,8 +786,8 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
   const uint8_t *prow = P + c * N;
   const uint32_t *frow = fin + c * N;
   uint16_t *rk = rank_all + j * N;
-  Rec *own = own_all + j * (int64_t)(N + 1);
-  Rec *cp = cp_all + j * (int64_t)(E + 1);
+  Rec *own = own_all + j * own_stride(N);
+  Rec *cp = cp_all + j * cp_stride(E);
   const uint32_t *indeg_f = G.op_meta + (int64_t)kMetaReq * G.meta_stride;  // predecessor count << 16
   for (int d = lane; d < D; d += kWave) {
     cfill[d] = 0;
@@ -788,6 +833,10 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
     }
     own_off[D] = so;
     cp_off[D] = sc;
+  }
+  if (kStage) {
+    for (int d = lane; d < D; d += kWave) base[d] = own_off[d];
+    if (lane == 0) fqn = 0;
   }
   __syncthreads();  // also orders the rank-table stores before the loads below
   if (!kFast) {
@@ -840,13 +889,20 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       const bool arrive = A > L;
       const uint32_t F = !has0 ? kInf32 : arrive ? A : L;
       const uint32_t loc = !has0 ? 0u : arrive ? loc_window((int)a.rv + 1) : rl + 1;
-      own[act ? own_off[d] + (int)a.rv : N] = Rec{a.f - a.w, F, a.b, loc};
+      const Rec ro = Rec{a.f - a.w, F, a.b, loc};
+      const int po = own_off[d] + (int)a.rv;
       // copies: one per remote successor device
       const bool same = has1 && sc.dx1 == sc.dx0;
       const bool c0 = act && has0 && !loc0 && a.b != 0;
       const bool c1 = act && has1 && !loc1 && !same && a.b != 0;
-      const int s0 = atomicAdd(c0 ? &cfill[sc.dx0] : &nocopy[lane], c0 ? 1 : 0);
-      const int s1 = atomicAdd(c1 ? &cfill[sc.dx1] : &nocopy[lane], c1 ? 1 : 0);
+      int *const f0 = c0 ? &cfill[sc.dx0] : &nocopy[lane], *const f1 = c1 ? &cfill[sc.dx1] : &nocopy[lane];
+      int qo = 0;
+      if (kStage) {  // first own position of each device's run in this chunk
+        qo = act ? base[d] : 0;
+        if (act) atomicAdd(&base[d], 1);
+      }
+      const int s0 = atomicAdd(f0, c0 ? 1 : 0);
+      const int s1 = atomicAdd(f1, c1 ? 1 : 0);
       // both successors on one remote device: allocated before the one that
       // starts first, freed after the one that finishes last
       const bool late1 = same && sc.fx1 > sc.fx0;
@@ -854,7 +910,34 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       const uint32_t ra0 = same ? min(sc.rx0, sc.rx1) : sc.rx0;
       cp[c0 ? s0 : E] = Rec{a.f, hi0, a.b, (uint32_t)max((int)ra0 - 3, 0) << 16 | (ry0 + 1)};
       cp[c1 ? s1 : E] = Rec{a.f, sc.fx1, a.b, (uint32_t)max((int)sc.rx1 - 3, 0) << 16 | (sc.rx1 + 1)};
-      sc = load_succ(an, vn);
+      sc = load_succ(an, vn);  // the next chunk's successors, in flight during the stores
+      if (!kStage) {
+        own[act ? po : N] = ro;
+      } else {
+        wave_lds_fence();
+        // each device's own positions in this chunk form one run [first, last]
+        const int eo = act ? base[d] - 1 : 0, bo = act ? own_off[d + 1] : 0;
+        const int ko = act ? line_role(po, qo, eo, bo) : kRoleNone;
+        if (ko == kRoleDirect) own[po] = ro;  // a line complete inside this chunk
+        // the line open since earlier chunks: staged, and queued once complete
+        if (ko & kRoleOpen) obuf[d * kBlockRecs + (po & (kBlockRecs - 1))] = ro;
+        if (ko == kRoleClose) fq[atomicAdd(&fqn, 1)] = d << 20 | (uint32_t)(po >> kBlockShift);
+        wave_lds_fence();
+        // write the queued lines: kBlockRecs lanes per line
+        const int nq = fqn;
+        for (int qb = 0; qb < nq; qb += kWave / kBlockRecs) {
+          const int qi = qb + (lane >> kBlockShift), part = lane & (kBlockRecs - 1);
+          if (qi < nq) {
+            const uint32_t ent = fq[qi];
+            const int dv = (int)(ent >> 20), pos = (int)(ent & 0xFFFFFu) * kBlockRecs + part;
+            if (pos >= own_off[dv] && pos < own_off[dv + 1]) own[pos] = obuf[dv * kBlockRecs + part];
+          }
+        }
+        wave_lds_fence();
+        // a line begun in this chunk but not complete: staged for later chunks
+        if (ko == kRoleTail) obuf[d * kBlockRecs + (po & (kBlockRecs - 1))] = ro;
+        if (lane == 0) fqn = 0;
+      }
       a = an;
     }
   }
@@ -1028,14 +1111,15 @@ __device__ int64_t device_peak(const Rec *own, int m, const Rec *cp, int nc, UP 
     for (int z = s0; z < s1; ++z) pos += bt[z] < h ? 1 : 0;
     if (pos < na) atomicAdd(reinterpret_cast<unsigned long long *>(&dl[pos]), (unsigned long long)(-(int64_t)bytes));
   };
+  // (gaps are clamped to [0, m] so that no record content can widen a loop)
   for (int i = lane; i < nc; i += kWave) {
     const Rec r = cp[i];
-    place_free((int)(r.w & 0xFFFFu), r.y, r.z);
+    place_free(min((int)(r.w & 0xFFFFu), m), r.y, r.z);
   }
   for (int k = lane; k < m; k += kWave) {
     const Rec r = own[k];
     if (r.y != kInf32) {
-      int g = (int)r.w;
+      int g = min((int)r.w, m);
       if (r.w & kLocWindow) {
         bool ok;
         g = gap_win<false>(ak, m, r.y, (int)(r.w & 0xFFFFu), ok);
@@ -1077,19 +1161,46 @@ struct AggLds {
   int hn;
 };
 
-// returns -1 if the hard events overflow (the caller then uses device_peak)
-__device__ int64_t device_peak_agg(const Rec *own, int m, const Rec *cp, int nc, AggLds &A, int lane) {
-  for (int base = lane; base < m; base += 8 * kWave) {  // a batch of loads in flight together
-    Rec r[8];
+// A device's share of one candidate's records.
+struct DevSpan {
+  const Rec *own, *cp;
+  int m, nc;
+};
+
+constexpr int kOwnPer = kAggCap / kWave;    // own records per lane held in registers
+constexpr int kCpPer = kAggCopies / kWave;  // copy records per lane
+constexpr int kCpPre = 8;                   // copy rows loaded ahead; the rest when needed
+
+__device__ __forceinline__ bool agg_fits(const DevSpan &s) { return s.m < kAggCap && s.nc <= kAggCopies; }
+
+// Record k of a device sits in register k / 64 of lane k % 64.  The loads are
+// unconditional (a load under a branch is waited for at the join): rows past
+// the end repeat the last record, or the region's spare record when the
+// device has none, and are never used.
+__device__ __forceinline__ void load_own(Rec (&ro)[kOwnPer], const DevSpan &s, int lane) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) r[q] = own[min(base + q * kWave, m - 1)];
+  for (int q = 0; q < kOwnPer; ++q) ro[q] = s.own[min(q * kWave + lane, max(s.m - 1, 0))];
+}
+
+__device__ __forceinline__ void load_cp(Rec (&rc)[kCpPre], const DevSpan &s, int lane) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int k = base + q * kWave;
-      if (k < m) {
-        A.S[k] = r[q].x;
-        A.ob[k] = r[q].z;
-      }
+  for (int q = 0; q < kCpPre; ++q) rc[q] = s.cp[min(q * kWave + lane, max(s.nc - 1, 0))];
+}
+
+// Peak of one device whose records the caller loaded into ro and rc (it fits
+// the LDS arrays: agg_fits).  Once a record array has been used for the last
+// time it is refilled with the records of the next device (nxt, when pf), so
+// those loads overlap the rest of this device's work.  Returns -1 if the hard
+// events overflow (the caller then uses device_peak).
+__device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (&rc)[kCpPre], const DevSpan &nxt,
+                                   bool pf, AggLds &A, int lane) {
+  const int m = cur.m, nc = cur.nc;
+#pragma unroll
+  for (int q = 0; q < kOwnPer; ++q) {
+    const int k = q * kWave + lane;
+    if (k < m) {
+      A.S[k] = ro[q].x;
+      A.ob[k] = ro[q].z;
     }
   }
   for (int g = lane; g <= m; g += kWave) {
@@ -1103,55 +1214,65 @@ __device__ int64_t device_peak_agg(const Rec *own, int m, const Rec *cp, int nc,
   auto add64 = [](int64_t *p, int64_t v) {
     atomicAdd(reinterpret_cast<unsigned long long *>(p), (unsigned long long)v);
   };
-  // copies: allocation gap (window probes, four rows in flight), free gap exact
-  for (int base = lane; base < nc; base += 4 * kWave) {
-    Rec r[4];
-    int g[4];
-    bool ok[4];
+  // copies: allocation gap (window probes, four rows at a time), free gap exact
 #pragma unroll
-    for (int q = 0; q < 4; ++q) r[q] = cp[min(base + q * kWave, nc - 1)];
+  for (int q0 = 0; q0 < kCpPer; q0 += 4) {
+    if (q0 * kWave < nc) {
+      Rec r4[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) g[q] = gap_win<true>(A.S, m, r[q].x, (int)(r[q].w >> 16), ok[q]);
+      for (int q = 0; q < 4; ++q)
+        r4[q] = q0 + q < kCpPre ? rc[(q0 + q) % kCpPre] : cur.cp[min((q0 + q) * kWave + lane, nc - 1)];
+      int g[4];
+      bool ok[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int i = base + q * kWave;
-      if (i < nc) {
-        if (!ok[q]) g[q] = gap_search<true>(A.S, m, r[q].x);
-        const int gf = (int)(r[q].w & 0xFFFFu);
-        A.cg[i] = (uint32_t)g[q] << 16 | (uint32_t)gf;
-        add64(&A.dg[g[q]], (int64_t)r[q].z);
-        add64(&A.dg[gf], -(int64_t)r[q].z);
-        add64(&A.fg[gf], (int64_t)r[q].z);
-      }
-    }
-  }
-  // own frees: exact gap or window probes
-  for (int base = lane; base < m; base += 4 * kWave) {
-    Rec r[4];
-    int g[4];
-    bool ok[4];
+      for (int q = 0; q < 4; ++q) g[q] = gap_win<true>(A.S, m, r4[q].x, (int)(r4[q].w >> 16), ok[q]);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      r[q] = own[min(base + q * kWave, m - 1)];
-      ok[q] = true;
-      g[q] = (int)r[q].w;
-      if (r[q].w & kLocWindow) g[q] = gap_win<false>(A.S, m, r[q].y, (int)(r[q].w & 0xFFFFu), ok[q]);
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int k = base + q * kWave;
-      if (k < m) {
-        if (r[q].y == kInf32) {
-          A.og[k] = 0xFFFFu;
-        } else {
-          if (!ok[q]) g[q] = gap_search<false>(A.S, m, r[q].y);
-          A.og[k] = (uint16_t)g[q];
-          add64(&A.dg[g[q]], -(int64_t)r[q].z);
-          add64(&A.fg[g[q]], (int64_t)r[q].z);
+      for (int q = 0; q < 4; ++q) {
+        const int i = (q0 + q) * kWave + lane;
+        if (i < nc) {
+          const Rec r = r4[q];
+          if (!ok[q]) g[q] = gap_search<true>(A.S, m, r.x);
+          const int gf = min((int)(r.w & 0xFFFFu), m);
+          A.cg[i] = (uint32_t)g[q] << 16 | (uint32_t)gf;
+          add64(&A.dg[g[q]], (int64_t)r.z);
+          add64(&A.dg[gf], -(int64_t)r.z);
+          add64(&A.fg[gf], (int64_t)r.z);
         }
       }
     }
   }
+  if (pf) load_cp(rc, nxt, lane);
+  // own frees: exact gap or window probes
+#pragma unroll
+  for (int q0 = 0; q0 < kOwnPer; q0 += 4) {
+    if (q0 * kWave < m) {
+      int g[4];
+      bool ok[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        ok[q] = true;
+        g[q] = min((int)ro[q0 + q].w, m);
+        if (ro[q0 + q].w & kLocWindow)
+          g[q] = gap_win<false>(A.S, m, ro[q0 + q].y, (int)(ro[q0 + q].w & 0xFFFFu), ok[q]);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int k = (q0 + q) * kWave + lane;
+        if (k < m) {
+          const Rec r = ro[q0 + q];
+          if (r.y == kInf32) {
+            A.og[k] = 0xFFFFu;
+          } else {
+            if (!ok[q]) g[q] = gap_search<false>(A.S, m, r.y);
+            A.og[k] = (uint16_t)g[q];
+            add64(&A.dg[g[q]], -(int64_t)r.z);
+            add64(&A.fg[g[q]], (int64_t)r.z);
+          }
+        }
+      }
+    }
+  }
+  if (pf) load_own(ro, nxt, lane);
   wave_lds_fence();
   // L[g] = prefix of dg; P0 at own allocations, exact values of copy-only gaps
   {
@@ -1197,14 +1318,14 @@ __device__ int64_t device_peak_agg(const Rec *own, int m, const Rec *cp, int nc,
     const uint32_t gg = A.cg[i];
     const int ga = (int)(gg >> 16), gf = (int)(gg & 0xFFFFu);
     if (A.hard[ga] | A.hard[gf]) {
-      const Rec r = cp[i];
+      const Rec r = cur.cp[i];
       if (A.hard[ga]) push(r.x, r.z, (uint32_t)ga << 1 | 1u);
       if (A.hard[gf]) push(r.y, r.z, (uint32_t)gf << 1);
     }
   }
   for (int k = lane; k < m; k += kWave) {
     const uint32_t gf = A.og[k];
-    if (gf != 0xFFFFu && A.hard[gf]) push(own[k].y, A.ob[k], gf << 1);
+    if (gf != 0xFFFFu && A.hard[gf]) push(cur.own[k].y, A.ob[k], gf << 1);
   }
   wave_lds_fence();
   const int hn = A.hn;
@@ -1251,21 +1372,36 @@ __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0,
         for (int d = lane; d < D; d += kWave) peak[c * D + d] = 0;
       continue;
     }
-    const Rec *own = own_all + j * (int64_t)(N + 1);
-    const Rec *cp = cp_all + j * (int64_t)(E + 1);
+    const Rec *own = own_all + j * own_stride(N);
+    const Rec *cp = cp_all + j * cp_stride(E);
     const int32_t *mt = meta + j * meta_stride(D);
+    auto span = [&](int e) {
+      const int o0 = mt[e];
+      return DevSpan{own + o0, cp + mt[D + 1 + e], mt[e + 1] - o0, mt[2 * (D + 1) + e]};
+    };
     uint8_t viol = 0;
+    // each device's records are loaded while the previous device is evaluated
+    Rec ro[kOwnPer], rc[kCpPre];
+    DevSpan cur = span(0);
+    if (agg_fits(cur)) {
+      load_own(ro, cur, lane);
+      load_cp(rc, cur, lane);
+    }
     for (int e = 0; e < D; ++e) {
-      const int o0 = mt[e], m = mt[e + 1] - o0;
-      const int c0 = mt[D + 1 + e], nc = mt[2 * (D + 1) + e];
+      const DevSpan nxt = e + 1 < D ? span(e + 1) : cur;
+      const bool pf = e + 1 < D && agg_fits(nxt);
       int64_t pk = 0;
-      if (m + nc > 0) {
-        pk = -1;
-        if (m < kAggCap && nc <= kAggCopies) pk = device_peak_agg(own + o0, m, cp + c0, nc, s_agg, lane);
-        if (pk < 0) pk = device_peak(own + o0, m, cp + c0, nc, g_ak, g_ag, g_dl, lane);
+      if (cur.m + cur.nc > 0 && agg_fits(cur)) {
+        pk = device_peak_agg(cur, ro, rc, nxt, pf, s_agg, lane);
+      } else if (pf) {
+        load_own(ro, nxt, lane);
+        load_cp(rc, nxt, lane);
       }
+      if (pk < 0 || (cur.m + cur.nc > 0 && !agg_fits(cur)))
+        pk = device_peak(cur.own, cur.m, cur.cp, cur.nc, g_ak, g_ag, g_dl, lane);
       if (peak && lane == 0) peak[c * D + e] = pk;
       if (pk > G.cap[e]) viol = SS_VIOLATION_MEMORY;
+      cur = nxt;
     }
     if (lane == 0) violation[c] = viol;
   }
@@ -1274,6 +1410,12 @@ __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0,
 int hip_fail(hipError_t err, const char *what) {
   return ss_set_error(err == hipErrorOutOfMemory ? SS_ERR_OOM : SS_ERR_DEVICE,
                       std::string(what) + ": " + hipGetErrorString(err));
+}
+
+// Dynamic LDS of fast_intervals: per-device offsets and fill pointers, and
+// with staged stores the open line of every device's own bucket.
+size_t intervals_lds(int D, bool stage) {
+  return (stage ? (size_t)D * kBlockRecs * sizeof(Rec) : 0) + (size_t)(4 * D + 2 + 2 * kWave + 1) * sizeof(int);
 }
 
 // Sub-chunk scratch of the memory passes.
@@ -1304,8 +1446,12 @@ int memory_passes(const ss_gmg *g, const MemPass &M, const uint8_t *Pc, const ui
     void *args[] = {const_cast<GmgView *>(&G), const_cast<uint8_t **>(&Pc), const_cast<uint32_t **>(&fin),
                     &j0, const_cast<Rec **>(&M.own), const_cast<Rec **>(&M.cp), const_cast<int32_t **>(&M.meta),
                     &rank, &vi};
+    // the branch-free writer with index ranks stages its own-record stores
+    const size_t lds = intervals_lds((int)g->n_dev, M.iv_fast && !given_ranks);
+    hipError_t err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
     SsTimingRec *ti = ss_timing_start(SS_KERNEL_INTERVALS, stream);
-    hipError_t err = hipLaunchKernel(fn, dim3((unsigned)nj), dim3(kWave), args, 0, stream);
+    err = hipLaunchKernel(fn, dim3((unsigned)nj), dim3(kWave), args, lds, stream);
     ss_timing_stop(ti, stream);
     if (err == hipSuccess) err = hipGetLastError();
     if (err != hipSuccess) return hip_fail(err, "fast_intervals launch");
@@ -1363,7 +1509,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   chunk = std::min<int64_t>(chunk, int64_t(65535) * 64);  // transpose grids index 64-candidate tiles in y
   chunk = std::min<int64_t>(chunk, B);
   // sub-chunk: interval records of each candidate (own N, copies <= E)
-  const int64_t rec_per_cand = (N + E + 2) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4 + N * 2;
+  const int64_t rec_per_cand = (own_stride(N) + cp_stride(E)) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4 + N * 2;
   int64_t sub = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
   sub = std::min<int64_t>(sub, chunk);
   const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
@@ -1372,8 +1518,8 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
   const size_t sz_pt = align((size_t)chunk * N + 1);
   const size_t sz_fin = align((size_t)chunk * N * 4 + 4);
-  const size_t sz_own = align((size_t)sub * (N + 1) * sizeof(Rec));
-  const size_t sz_cp = align((size_t)sub * (E + 1) * sizeof(Rec));
+  const size_t sz_own = align((size_t)sub * own_stride(N) * sizeof(Rec));
+  const size_t sz_cp = align((size_t)sub * cp_stride(E) * sizeof(Rec));
   const size_t sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
   const size_t sz_rank = align(((size_t)sub * N + 1) * 2);
   const size_t sz_wk = align((size_t)nslots * 2 * (slot_cap + 2) * 4);
@@ -1465,7 +1611,7 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   const int64_t per_cand = N * (4 + 2 + 2 + 8);
   int64_t chunk = kScratchBudget / std::max<int64_t>(1, per_cand);
   chunk = std::min<int64_t>(std::max<int64_t>(1, chunk), B);
-  const int64_t rec_per_cand = (N + E + 2) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4;
+  const int64_t rec_per_cand = (own_stride(N) + cp_stride(E)) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4;
   int64_t sub = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
   sub = std::min<int64_t>(sub, chunk);
   const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
@@ -1476,8 +1622,8 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   const size_t sz_rank = align(((size_t)chunk * N + 1) * 2);
   const size_t sz_miss = align(((size_t)chunk * N + 1) * 2);
   const size_t sz_spill = align((size_t)chunk * N * 8 + 8);
-  const size_t sz_own = align((size_t)sub * (N + 1) * sizeof(Rec));
-  const size_t sz_cp = align((size_t)sub * (E + 1) * sizeof(Rec));
+  const size_t sz_own = align((size_t)sub * own_stride(N) * sizeof(Rec));
+  const size_t sz_cp = align((size_t)sub * cp_stride(E) * sizeof(Rec));
   const size_t sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
   const size_t sz_wk = align((size_t)nslots * 2 * (slot_cap + 2) * 4);
   const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
