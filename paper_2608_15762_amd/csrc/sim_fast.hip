@@ -673,46 +673,15 @@ __device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32
   }
 }
 
-// Ascending sort of the 64 lanes' keys: bitonic network over lane shuffles.
-__device__ __forceinline__ uint32_t wave_sort64(uint32_t key, int lane) {
-#pragma unroll
-  for (int k = 2; k <= kWave; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const uint32_t other = __shfl_xor(key, j, kWave);
-      const bool asc = (lane & k) == 0, low = (lane & j) == 0;
-      key = (asc == low) ? min(key, other) : max(key, other);
-    }
+// Lanes whose key equals this lane's key, among the active lanes: one ballot
+// per key bit (keys below 2^nbits, nbits wave-uniform).
+__device__ __forceinline__ uint64_t same_key_lanes(int key, bool active, int nbits) {
+  uint64_t peers = (uint64_t)__ballot(active);
+  for (int b = 0; b < nbits; ++b) {
+    const uint64_t m = (uint64_t)__ballot((key >> b) & 1);
+    peers &= ((key >> b) & 1) ? m : ~m;
   }
-  return key;
-}
-
-// Groups a chunk of 64 ops by device.  For the op of this lane (device d,
-// active = it exists): rank = how many ops of the chunk with lower index are
-// on the same device.  Lanes that end a device's group in sorted order get
-// that device (grp_dev, else -1), the group size and the group's sum of val.
-__device__ __forceinline__ void chunk_groups(int d, bool active, int val, int lane, int &rank, int &grp_dev,
-                                             int &grp_cnt, int &grp_sum) {
-  const uint32_t key = ((active ? (uint32_t)d : 0x3FFu) << 6) | (uint32_t)lane;
-  const uint32_t sk = wave_sort64(key, lane);
-  const int sd = (int)(sk >> 6), src = (int)(sk & 63u);
-  const int sval = __shfl(val, src, kWave);
-  const int prev = __shfl_up(sd, 1, kWave), next = __shfl_down(sd, 1, kWave);
-  int start = (lane == 0 || prev != sd) ? lane : 0;
-  int sum = sval;
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int y = __shfl_up(start, o, kWave);
-    if (lane >= o) start = max(start, y);
-  }
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int y = __shfl_up(sum, o, kWave);
-    if (lane - o >= start) sum += y;
-  }
-  const bool tail = lane == kWave - 1 || next != sd;
-  grp_dev = (tail && sd != 0x3FF) ? sd : -1;
-  grp_cnt = lane - start + 1;
-  grp_sum = sum;
-  rank = __builtin_amdgcn_ds_permute(src << 2, lane - start);
+  return peers;
 }
 
 // Per-candidate bucket geometry written by fast_intervals, read by fast_peaks.
@@ -795,6 +764,7 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
   }
   wave_lds_fence();
   {
+    const int dbits = 32 - __builtin_clz((unsigned)max(D - 1, 1));  // bits of a device id
     int vn = min(lane, N - 1);
     uint32_t dn = N > 0 ? prow[vn] : 0, in = N > 0 ? indeg_f[vn] : 0;
     for (int v0 = 0; v0 < N; v0 += kWave) {
@@ -804,21 +774,14 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       vn = min(v0 + kWave + lane, N - 1);  // next chunk, in flight meanwhile
       dn = prow[vn];
       in = indeg_f[vn];
-      if (kGivenRanks) {
-        if (act) {
-          atomicAdd(&base[d], 1);
-          atomicAdd(&cfill[d], indeg);
-        }
-      } else {
-        int rank, gd, gcnt, gsum;
-        chunk_groups(d, act, indeg, lane, rank, gd, gcnt, gsum);
-        if (act) rk[v] = (uint16_t)(base[d] + rank);
-        wave_lds_fence();
-        if (gd >= 0) {
-          base[gd] += gcnt;
-          cfill[gd] += gsum;
-        }
-        wave_lds_fence();
+      if (!kGivenRanks) {  // rank = ops of d so far + lower lanes of this chunk on d
+        const uint64_t peers = same_key_lanes(d, act, dbits);
+        if (act) rk[v] = (uint16_t)(base[d] + __builtin_amdgcn_mbcnt_hi((uint32_t)(peers >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u)));
+      }
+      if (act) {  // counts: the order of these adds does not matter
+        atomicAdd(&base[d], 1);
+        atomicAdd(&cfill[d], indeg);
       }
     }
   }
