@@ -1237,32 +1237,49 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
   }
   if (pf) load_own(ro, nxt, lane);
   wave_lds_fence();
-  // L[g] = prefix of dg; P0 at own allocations, exact values of copy-only gaps
+  // L[g] = prefix of dg; P0 at own allocations, exact values of copy-only gaps.
+  // Every loop below runs a fixed number of rows (m < kAggCap, nc <= kAggCopies)
+  // with clamped, unconditional LDS loads, so that each row's loads overlap.
   {
-    const int n = m + 1, per = (n + kWave - 1) / kWave, lo = lane * per, hi = min(n, lo + per);
+    const int n = m + 1, per = (n + kWave - 1) / kWave, lo = lane * per;
+    int64_t v[kOwnPer];
     int64_t sacc = 0;
-    for (int g = lo; g < hi; ++g) sacc += A.dg[g];
+#pragma unroll
+    for (int t = 0; t < kOwnPer; ++t) {
+      v[t] = A.dg[min(lo + t, n - 1)];
+      if (t >= per || lo + t >= n) v[t] = 0;
+      sacc += v[t];
+    }
     int64_t run = wave_incl_scan64(sacc, lane) - sacc;
-    for (int g = lo; g < hi; ++g) {
-      run += A.dg[g];
-      A.dg[g] = run;
+#pragma unroll
+    for (int t = 0; t < kOwnPer; ++t) {
+      run += v[t];
+      if (t < per && lo + t < n) A.dg[lo + t] = run;
     }
   }
   wave_lds_fence();
   int64_t best = 0;
-  for (int g = lane; g <= m; g += kWave) {
-    const int64_t L = A.dg[g], prev = g > 0 ? A.dg[g - 1] + (int64_t)A.ob[g - 1] : 0;
-    if (g < m) best = imax64(best, L + (int64_t)A.ob[g]);
-    const int64_t copies = L - prev + A.fg[g];
-    if (copies > 0 && A.fg[g] == 0) best = imax64(best, L);  // copies only: all of them precede own g
+  int64_t bound[kOwnPer];  // per gap of this lane: L + frees when the gap holds copies and frees, else -1
+#pragma unroll
+  for (int q = 0; q < kOwnPer; ++q) {
+    const int g = q * kWave + lane, gc = min(g, m), gp = max(gc - 1, 0);
+    const int64_t L = A.dg[gc], F = A.fg[gc];
+    const int64_t prev = gc > 0 ? A.dg[gp] + (int64_t)A.ob[gp] : 0;
+    const int64_t obg = (int64_t)A.ob[min(gc, max(m - 1, 0))];
+    const int64_t copies = L - prev + F;
+    bound[q] = -1;
+    if (g <= m) {
+      if (g < m) best = imax64(best, L + obg);
+      if (copies > 0 && F == 0) best = imax64(best, L);  // copies only: all of them precede own g
+      if (copies > 0 && F > 0) bound[q] = L + F;
+    }
   }
   for (int o = kWave / 2; o >= 1; o >>= 1) best = imax64(best, __shfl_xor(best, o, kWave));
   bool any = false;
-  for (int g = lane; g <= m; g += kWave) {
-    const int64_t L = A.dg[g], prev = g > 0 ? A.dg[g - 1] + (int64_t)A.ob[g - 1] : 0;
-    const int64_t copies = L - prev + A.fg[g];
-    if (copies > 0 && A.fg[g] > 0 && L + A.fg[g] > best) {
-      A.hard[g] = 1;
+#pragma unroll
+  for (int q = 0; q < kOwnPer; ++q) {
+    if (bound[q] > best) {
+      A.hard[q * kWave + lane] = 1;
       any = true;
     }
   }
@@ -1277,18 +1294,34 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
       A.hx[at] = x;
     }
   };
-  for (int i = lane; i < nc; i += kWave) {
-    const uint32_t gg = A.cg[i];
-    const int ga = (int)(gg >> 16), gf = (int)(gg & 0xFFFFu);
-    if (A.hard[ga] | A.hard[gf]) {
-      const Rec r = cur.cp[i];
-      if (A.hard[ga]) push(r.x, r.z, (uint32_t)ga << 1 | 1u);
-      if (A.hard[gf]) push(r.y, r.z, (uint32_t)gf << 1);
+#pragma unroll
+  for (int q0 = 0; q0 < kCpPer; q0 += 4) {
+    if (q0 * kWave < nc) {
+      uint32_t gg[4];
+      bool ha[4], hf[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) gg[q] = A.cg[min((q0 + q) * kWave + lane, nc - 1)];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        ha[q] = A.hard[gg[q] >> 16];
+        hf[q] = A.hard[gg[q] & 0xFFFFu];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = (q0 + q) * kWave + lane;
+        if (i < nc && (ha[q] || hf[q])) {
+          const Rec r = cur.cp[i];
+          if (ha[q]) push(r.x, r.z, (gg[q] >> 16) << 1 | 1u);
+          if (hf[q]) push(r.y, r.z, (gg[q] & 0xFFFFu) << 1);
+        }
+      }
     }
   }
-  for (int k = lane; k < m; k += kWave) {
-    const uint32_t gf = A.og[k];
-    if (gf != 0xFFFFu && A.hard[gf]) push(cur.own[k].y, A.ob[k], gf << 1);
+#pragma unroll
+  for (int q = 0; q < kOwnPer; ++q) {
+    const int k = q * kWave + lane, kc = min(k, max(m - 1, 0));
+    const uint32_t gf = A.og[kc];
+    if (k < m && gf != 0xFFFFu && A.hard[gf]) push(cur.own[k].y, A.ob[k], gf << 1);
   }
   wave_lds_fence();
   const int hn = A.hn;
