@@ -1158,21 +1158,24 @@ __device__ __forceinline__ void load_cp(Rec (&rc)[kCpPre], const DevSpan &s, int
 __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (&rc)[kCpPre], const DevSpan &nxt,
                                    bool pf, AggLds &A, int lane) {
   const int m = cur.m, nc = cur.nc;
+  // own k: start, bytes, and its allocation as the opening value of gap k + 1
 #pragma unroll
   for (int q = 0; q < kOwnPer; ++q) {
     const int k = q * kWave + lane;
     if (k < m) {
       A.S[k] = ro[q].x;
       A.ob[k] = ro[q].z;
+      A.dg[k + 1] = (int64_t)ro[q].z;
+    }
+    if (k <= m) {
+      A.fg[k] = 0;
+      A.hard[k] = 0;
     }
   }
-  for (int g = lane; g <= m; g += kWave) {
-    A.fg[g] = 0;
-    A.hard[g] = 0;
+  if (lane == 0) {
+    A.dg[0] = 0;
+    A.hn = 0;
   }
-  if (lane == 0) A.hn = 0;
-  wave_lds_fence();
-  for (int g = lane; g <= m; g += kWave) A.dg[g] = g > 0 ? (int64_t)A.ob[g - 1] : 0;
   wave_lds_fence();
   auto add64 = [](int64_t *p, int64_t v) {
     atomicAdd(reinterpret_cast<unsigned long long *>(p), (unsigned long long)v);
