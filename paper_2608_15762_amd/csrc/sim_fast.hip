@@ -1115,7 +1115,7 @@ constexpr int kHardCap = 128;  // events of hard gaps per device
 struct AggLds {
   uint32_t S[kAggCap];        // own starts
   uint32_t ob[kAggCap];       // own bytes
-  int64_t dg[kAggCap + 1];    // per gap: copies - frees (+ own_{g-1}), then L[g]
+  int64_t dg[kAggCap + 1];    // per gap: copies allocated (+ own_{g-1}), then L[g]
   int64_t fg[kAggCap + 1];    // per gap: freed bytes
   uint32_t cg[kAggCopies];    // per copy: allocation gap << 16 | free gap
   uint16_t og[kAggCap];       // per own allocation: free gap (0xFFFF: never freed)
@@ -1201,7 +1201,6 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
           const int gf = min((int)(r.w & 0xFFFFu), m);
           A.cg[i] = (uint32_t)g[q] << 16 | (uint32_t)gf;
           add64(&A.dg[g[q]], (int64_t)r.z);
-          add64(&A.dg[gf], -(int64_t)r.z);
           add64(&A.fg[gf], (int64_t)r.z);
         }
       }
@@ -1231,7 +1230,6 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
           } else {
             if (!ok[q]) g[q] = gap_search<false>(A.S, m, r.y);
             A.og[k] = (uint16_t)g[q];
-            add64(&A.dg[g[q]], -(int64_t)r.z);
             add64(&A.fg[g[q]], (int64_t)r.z);
           }
         }
@@ -1249,7 +1247,8 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
     int64_t sacc = 0;
 #pragma unroll
     for (int t = 0; t < kOwnPer; ++t) {
-      v[t] = A.dg[min(lo + t, n - 1)];
+      const int g = min(lo + t, n - 1);
+      v[t] = A.dg[g] - A.fg[g];
       if (t >= per || lo + t >= n) v[t] = 0;
       sacc += v[t];
     }
