@@ -1,7 +1,7 @@
 // Fast path of the batched what-if simulation (gfx950), used when the loader
 // proved that every simulated time fits in 32 bits and N <= 65535.
 //
-// Per chunk of candidates:
+// Index-order dispatch, per chunk of candidates:
 //   transpose     candidates' placement rows -> op-major [op][candidate]
 //   fast_schedule one lane per candidate, ops in index order (Sec. 3.3.2-3.3.3).
 //                 Per (device, lane) LDS state laid out [device][lane], so a
@@ -15,25 +15,29 @@
 //   transpose     finish times back to candidate rows
 // then per sub-chunk of candidates:
 //   fast_intervals one wave per candidate, lanes = consecutive ops (coalesced
-//                 row reads).  Pass A: a 64-key sort across the wave groups
-//                 each chunk of ops by device, giving every op its rank among
-//                 the ops of its device (a rank table) and per-device counts
-//                 and in-degree sums, without same-address atomics.  Pass B
-//                 writes every residency interval (Sec. 3.3.2) into a per-
-//                 device bucket: own outputs at their rank (so a device's own
-//                 intervals are start-sorted), one copy per (output, remote
-//                 device) in a region bounded by the device's summed in-degree,
-//                 each event tagged with where it falls among the device's own
+//                 row reads).  Pass A ranks every op among the ops of its
+//                 device (lanes sharing a device from one ballot per bit of
+//                 the device id) into a rank table and counts per device.
+//                 Pass B writes every residency interval (Sec. 3.3.2) into a
+//                 per-device bucket: own outputs at their rank (so a device's
+//                 own intervals are start-sorted; staged in LDS and written in
+//                 whole 64-byte lines), one copy per (output, remote device)
+//                 in a region bounded by the device's summed in-degree, each
+//                 event tagged with where it falls among the device's own
 //                 starts (exact, or a small window around a known rank).  For
-//                 graphs of out-degree <= 2 pass B is branch free and software-
-//                 pipelined over chunks.
-//   fast_peaks    one wave per candidate, per device: each copy allocation is
-//                 placed between two own starts by six independent LDS probes
-//                 around its window (binary search only when outside), copies
-//                 are grouped by gap and ranked inside it, frees land on the
-//                 first allocation at or after them (frees precede allocations
-//                 at equal times), and one scan gives the maximum of
-//                 allocated-so-far minus freed-so-far over the allocations.
+//                 graphs of out-degree <= 2 pass B is branch free and
+//                 software-pipelined over chunks.
+//   fast_peaks    one wave per candidate, devices in turn, each device's
+//                 records in registers (the next device's loaded meanwhile):
+//                 per-gap sums of allocations and frees between consecutive
+//                 own starts give the exact live bytes at every own start;
+//                 only gaps holding copies and frees whose bound exceeds the
+//                 best so far are swept event by event.
+// Ready-time dispatch (the rule of Sec. 3.3.2), per chunk:
+//   ready_schedule one wave per candidate, the ready set in registers (a
+//                 spill list beyond), finish times in candidate rows and each
+//                 op's rank in dispatch order; then fast_intervals with those
+//                 ranks and fast_peaks as above.
 #include <climits>
 
 #include "ss_internal.h"
