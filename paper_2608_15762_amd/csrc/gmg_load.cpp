@@ -297,6 +297,11 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
       delete g;
       return ss_set_error(SS_ERR_DEVICE, "hipMemcpy of the staged GMG failed");
     }
+    if (hipStreamCreateWithFlags(&g->aux, hipStreamNonBlocking) != hipSuccess) {
+      (void)hipFree(g->dev_mem);
+      delete g;
+      return ss_set_error(SS_ERR_DEVICE, "hipStreamCreateWithFlags failed");
+    }
     auto *base = static_cast<unsigned char *>(g->dev_mem);
     GmgView &V = g->view;
     V.n_ops = (int32_t)N;
@@ -364,6 +369,7 @@ extern "C" void ss_gmg_free(ss_gmg *g) {
   (void)hipGetDevice(&prev);
   (void)hipSetDevice(g->device);
   (void)hipDeviceSynchronize();
+  if (g->aux) (void)hipStreamDestroy(g->aux);
   (void)hipFree(g->dev_mem);
   (void)hipSetDevice(prev);
   delete g;

@@ -720,15 +720,22 @@ struct IvSucc {  // device, finish and rank of the first two successors
 //   tail   its line begins in this chunk and is not complete: staged
 constexpr int kRoleNone = 0, kRoleDirect = 1, kRoleOpen = 2, kRoleClose = 6, kRoleTail = 8;
 
+template <int kShift>
 __device__ __forceinline__ int line_role(int p, int first, int last, int end) {
-  const int L = p >> kBlockShift, Lo = first >> kBlockShift, Ll = last >> kBlockShift;
+  constexpr int kRecs = 1 << kShift;
+  const int L = p >> kShift, Lo = first >> kShift, Ll = last >> kShift;
   if (L == Lo) {
-    const int closer = min((Lo << kBlockShift) + kBlockRecs - 1, end - 1);
+    const int closer = min((Lo << kShift) + kRecs - 1, end - 1);
     return (closer <= last && p == closer) ? kRoleClose : kRoleOpen;
   }
-  const bool done = (L << kBlockShift) + kBlockRecs - 1 <= last || (last == end - 1 && L == Ll);
+  const bool done = (L << kShift) + kRecs - 1 <= last || (last == end - 1 && L == Ll);
   return done ? kRoleDirect : kRoleTail;
 }
+
+// Staged blocks: own records and copies in 32-byte pairs (a smaller stage
+// leaves more waves per CU, which this kernel needs).
+constexpr int kOwnShift = 1, kOwnRecs = 1 << kOwnShift;
+constexpr int kCpShift = 1, kCpRecs = 1 << kCpShift;
 
 // kGivenRanks: the rank table already holds every op's rank on its device
 // (dispatch order), pass A only counts.
@@ -744,14 +751,17 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
   constexpr bool kStage = kFast && !kGivenRanks;
   extern __shared__ __align__(16) unsigned char iv_lds[];
   const int Dv = G.n_dev;
-  Rec *obuf = reinterpret_cast<Rec *>(iv_lds);                             // [D][kBlockRecs]
-  int *own_off = reinterpret_cast<int *>(obuf + (kStage ? kBlockRecs * Dv : 0));  // [D+1]
+  Rec *obuf = reinterpret_cast<Rec *>(iv_lds);                           // [D][kOwnRecs]
+  Rec *cbuf = obuf + (kStage ? kOwnRecs * Dv : 0);                       // [D][kCpRecs]
+  int *own_off = reinterpret_cast<int *>(cbuf + (kStage ? kCpRecs * Dv : 0));  // [D+1]
   int *cp_off = own_off + Dv + 1;                                          // [D+1]
   int *cfill = cp_off + Dv + 1;                                            // [D] next copy slot
   int *base = cfill + Dv;  // [D] ops counted so far; with staging then the next own position
   int *nocopy = base + Dv;                                                 // [64]
-  uint32_t *fq = reinterpret_cast<uint32_t *>(nocopy + kWave);             // [64]
-  int &fqn = *reinterpret_cast<int *>(fq + kWave);
+  uint32_t *fq = reinterpret_cast<uint32_t *>(nocopy + kWave);  // [64] own lines to write
+  uint32_t *fc = fq + kWave;                                    // [128] copy blocks to write
+  int &fqn = *reinterpret_cast<int *>(fc + 2 * kWave);
+  int &fcn = *(&fqn + 1);
   const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops], K = G.n_link;
   const int lane = threadIdx.x;
   const int64_t j = blockIdx.x, c = j0 + j;
@@ -803,7 +813,7 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
   }
   if (kStage) {
     for (int d = lane; d < D; d += kWave) base[d] = own_off[d];
-    if (lane == 0) fqn = 0;
+    if (lane == 0) fqn = fcn = 0;
   }
   __syncthreads();  // also orders the rank-table stores before the loads below
   if (!kFast) {
@@ -863,8 +873,10 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       const bool c0 = act && has0 && !loc0 && a.b != 0;
       const bool c1 = act && has1 && !loc1 && !same && a.b != 0;
       int *const f0 = c0 ? &cfill[sc.dx0] : &nocopy[lane], *const f1 = c1 ? &cfill[sc.dx1] : &nocopy[lane];
-      int qo = 0;
-      if (kStage) {  // first own position of each device's run in this chunk
+      int qo = 0, q0 = 0, q1 = 0;
+      if (kStage) {  // first position of each destination's run in this chunk
+        q0 = *f0;
+        q1 = *f1;
         qo = act ? base[d] : 0;
         if (act) atomicAdd(&base[d], 1);
       }
@@ -875,37 +887,67 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       const bool late1 = same && sc.fx1 > sc.fx0;
       const uint32_t ry0 = late1 ? sc.rx1 : sc.rx0, hi0 = late1 ? sc.fx1 : sc.fx0;
       const uint32_t ra0 = same ? min(sc.rx0, sc.rx1) : sc.rx0;
-      cp[c0 ? s0 : E] = Rec{a.f, hi0, a.b, (uint32_t)max((int)ra0 - 3, 0) << 16 | (ry0 + 1)};
-      cp[c1 ? s1 : E] = Rec{a.f, sc.fx1, a.b, (uint32_t)max((int)sc.rx1 - 3, 0) << 16 | (sc.rx1 + 1)};
+      const Rec r0 = Rec{a.f, hi0, a.b, (uint32_t)max((int)ra0 - 3, 0) << 16 | (ry0 + 1)};
+      const Rec r1 = Rec{a.f, sc.fx1, a.b, (uint32_t)max((int)sc.rx1 - 3, 0) << 16 | (sc.rx1 + 1)};
+      const uint32_t dx0 = sc.dx0, dx1 = sc.dx1;
       sc = load_succ(an, vn);  // the next chunk's successors, in flight during the stores
       if (!kStage) {
         own[act ? po : N] = ro;
+        cp[c0 ? s0 : E] = r0;
+        cp[c1 ? s1 : E] = r1;
       } else {
         wave_lds_fence();
-        // each device's own positions in this chunk form one run [first, last]
+        // each destination's positions in this chunk form one run [first, last]
         const int eo = act ? base[d] - 1 : 0, bo = act ? own_off[d + 1] : 0;
-        const int ko = act ? line_role(po, qo, eo, bo) : kRoleNone;
-        if (ko == kRoleDirect) own[po] = ro;  // a line complete inside this chunk
-        // the line open since earlier chunks: staged, and queued once complete
-        if (ko & kRoleOpen) obuf[d * kBlockRecs + (po & (kBlockRecs - 1))] = ro;
-        if (ko == kRoleClose) fq[atomicAdd(&fqn, 1)] = d << 20 | (uint32_t)(po >> kBlockShift);
+        const int e0 = *f0 - 1, e1 = *f1 - 1;
+        const int ko = act ? line_role<kOwnShift>(po, qo, eo, bo) : kRoleNone;
+        const int k0 = c0 ? line_role<kCpShift>(s0, q0, e0, INT_MAX) : kRoleNone;
+        const int k1 = c1 ? line_role<kCpShift>(s1, q1, e1, INT_MAX) : kRoleNone;
+        // blocks complete inside this chunk: stored directly
+        if (ko == kRoleDirect) own[po] = ro;
+        if (k0 == kRoleDirect) cp[s0] = r0;
+        if (k1 == kRoleDirect) cp[s1] = r1;
+        // the block open since earlier chunks: staged, and queued once complete
+        if (ko & kRoleOpen) obuf[d * kOwnRecs + (po & (kOwnRecs - 1))] = ro;
+        if (k0 & kRoleOpen) cbuf[dx0 * kCpRecs + (s0 & (kCpRecs - 1))] = r0;
+        if (k1 & kRoleOpen) cbuf[dx1 * kCpRecs + (s1 & (kCpRecs - 1))] = r1;
+        if (ko == kRoleClose) fq[atomicAdd(&fqn, 1)] = d << 20 | (uint32_t)(po >> kOwnShift);
+        if (k0 == kRoleClose) fc[atomicAdd(&fcn, 1)] = dx0 << 20 | (uint32_t)(s0 >> kCpShift);
+        if (k1 == kRoleClose) fc[atomicAdd(&fcn, 1)] = dx1 << 20 | (uint32_t)(s1 >> kCpShift);
         wave_lds_fence();
-        // write the queued lines: kBlockRecs lanes per line
-        const int nq = fqn;
-        for (int qb = 0; qb < nq; qb += kWave / kBlockRecs) {
-          const int qi = qb + (lane >> kBlockShift), part = lane & (kBlockRecs - 1);
+        // write the queued blocks, adjacent lanes to adjacent records
+        const int nq = fqn, nc = fcn;
+        for (int qb = 0; qb < nq; qb += kWave / kOwnRecs) {
+          const int qi = qb + (lane >> kOwnShift), part = lane & (kOwnRecs - 1);
           if (qi < nq) {
             const uint32_t ent = fq[qi];
-            const int dv = (int)(ent >> 20), pos = (int)(ent & 0xFFFFFu) * kBlockRecs + part;
-            if (pos >= own_off[dv] && pos < own_off[dv + 1]) own[pos] = obuf[dv * kBlockRecs + part];
+            const int dv = (int)(ent >> 20), pos = (int)(ent & 0xFFFFFu) * kOwnRecs + part;
+            if (pos >= own_off[dv] && pos < own_off[dv + 1]) own[pos] = obuf[dv * kOwnRecs + part];
+          }
+        }
+        for (int qb = 0; qb < nc; qb += kWave / kCpRecs) {
+          const int qi = qb + (lane >> kCpShift), part = lane & (kCpRecs - 1);
+          if (qi < nc) {
+            const uint32_t ent = fc[qi];
+            const int dv = (int)(ent >> 20), pos = (int)(ent & 0xFFFFFu) * kCpRecs + part;
+            if (pos >= cp_off[dv]) cp[pos] = cbuf[dv * kCpRecs + part];
           }
         }
         wave_lds_fence();
-        // a line begun in this chunk but not complete: staged for later chunks
-        if (ko == kRoleTail) obuf[d * kBlockRecs + (po & (kBlockRecs - 1))] = ro;
-        if (lane == 0) fqn = 0;
+        // a block begun in this chunk but not complete: staged for later chunks
+        if (ko == kRoleTail) obuf[d * kOwnRecs + (po & (kOwnRecs - 1))] = ro;
+        if (k0 == kRoleTail) cbuf[dx0 * kCpRecs + (s0 & (kCpRecs - 1))] = r0;
+        if (k1 == kRoleTail) cbuf[dx1 * kCpRecs + (s1 & (kCpRecs - 1))] = r1;
+        if (lane == 0) fqn = fcn = 0;
       }
       a = an;
+    }
+    if (kStage) {  // copy blocks still open (a bucket ends short of its reserve)
+      wave_lds_fence();
+      for (int e = lane; e < D; e += kWave) {
+        const int end = cfill[e], lo = max(end & ~(kCpRecs - 1), cp_off[e]);
+        for (int pos = lo; pos < end; ++pos) cp[pos] = cbuf[e * kCpRecs + (pos & (kCpRecs - 1))];
+      }
     }
   }
   wave_lds_fence();
@@ -1414,56 +1456,107 @@ int hip_fail(hipError_t err, const char *what) {
                       std::string(what) + ": " + hipGetErrorString(err));
 }
 
-// Dynamic LDS of fast_intervals: per-device offsets and fill pointers, and
-// with staged stores the open line of every device's own bucket.
-size_t intervals_lds(int D, bool stage) {
-  return (stage ? (size_t)D * kBlockRecs * sizeof(Rec) : 0) + (size_t)(4 * D + 2 + 2 * kWave + 1) * sizeof(int);
-}
-
-// Sub-chunk scratch of the memory passes.
+// Sub-chunk scratch of the memory passes.  The records (own, cp, meta) are
+// double-buffered: the interval pass of sub-chunk i runs on the caller's
+// stream while the peak pass of sub-chunk i-1 runs on the GMG's second
+// stream; events order each peak pass after its interval pass, and the reuse
+// of a buffer after the peak pass that read it.
 struct MemPass {
-  Rec *own, *cp;
-  int32_t *meta;
+  Rec *own[2], *cp[2];
+  int32_t *meta[2];
   uint16_t *rank;  // given ranks: candidate rows of the whole chunk; else sub rows
   uint32_t *wk;
   int64_t *wb;
   int64_t sub, nslots, slot_cap;
   bool iv_fast;
+  hipStream_t aux;
+  hipEvent_t iv_done[2], pk_done[2];
+  int64_t it;  // sub-chunks issued so far in this call
 };
+
+int mem_pass_events(MemPass &M) {
+  for (int k = 0; k < 2; ++k) {
+    M.iv_done[k] = M.pk_done[k] = nullptr;
+  }
+  for (int k = 0; k < 2; ++k) {
+    hipError_t err = hipEventCreateWithFlags(&M.iv_done[k], hipEventDisableTiming);
+    if (err == hipSuccess) err = hipEventCreateWithFlags(&M.pk_done[k], hipEventDisableTiming);
+    if (err != hipSuccess) return hip_fail(err, "hipEventCreateWithFlags");
+  }
+  M.it = 0;
+  return SS_OK;
+}
+
+// Joins the second stream back into the caller's and releases the events
+// (always, also after an error, before the scratch is freed).
+int mem_pass_join(MemPass &M, hipStream_t stream) {
+  hipError_t err = hipSuccess;
+  hipEvent_t done = nullptr;
+  err = hipEventCreateWithFlags(&done, hipEventDisableTiming);
+  if (err == hipSuccess) err = hipEventRecord(done, M.aux);
+  if (err == hipSuccess) err = hipStreamWaitEvent(stream, done, 0);
+  if (done) (void)hipEventDestroy(done);
+  for (int k = 0; k < 2; ++k) {
+    if (M.iv_done[k]) (void)hipEventDestroy(M.iv_done[k]);
+    if (M.pk_done[k]) (void)hipEventDestroy(M.pk_done[k]);
+  }
+  if (err != hipSuccess) {
+    (void)hipStreamSynchronize(M.aux);  // the scratch must outlive the second stream's work
+    return hip_fail(err, "joining the memory-pass stream");
+  }
+  return SS_OK;
+}
+
+// Dynamic LDS of fast_intervals: per-device offsets and fill pointers, and
+// with staged stores the open blocks of every device's buckets.
+size_t intervals_lds(int D, bool stage) {
+  return (stage ? (size_t)D * (kOwnRecs + kCpRecs) * sizeof(Rec) : 0) +
+         (size_t)(4 * D + 2 + 4 * kWave + 2) * sizeof(int);
+}
 
 // Residency intervals, then peaks, for the nb candidates of one chunk (their
 // placements Pc and finish-time rows fin), sub candidates at a time.
-int memory_passes(const ss_gmg *g, const MemPass &M, const uint8_t *Pc, const uint32_t *fin, int64_t nb,
+int memory_passes(const ss_gmg *g, MemPass &M, const uint8_t *Pc, const uint32_t *fin, int64_t nb,
                   bool given_ranks, int64_t *peak, uint8_t *violation, hipStream_t stream) {
   const GmgView &G = g->view;
   const int64_t N = g->n_ops;
-  for (int64_t j0 = 0; j0 < nb; j0 += M.sub) {
+  for (int64_t j0 = 0; j0 < nb; j0 += M.sub, ++M.it) {
     const int64_t nj = std::min(M.sub, nb - j0);
+    const int set = (int)(M.it & 1);
+    hipError_t err = hipSuccess;
+    if (M.it >= 2) err = hipStreamWaitEvent(stream, M.pk_done[set], 0);  // its buffers are free again
+    if (err != hipSuccess) return hip_fail(err, "hipStreamWaitEvent");
     uint16_t *rank = given_ranks ? M.rank + j0 * N : M.rank;
     const void *fn = M.iv_fast ? (given_ranks ? reinterpret_cast<const void *>(&fast_intervals<true, true>)
                                               : reinterpret_cast<const void *>(&fast_intervals<true, false>))
                                : (given_ranks ? reinterpret_cast<const void *>(&fast_intervals<false, true>)
                                               : reinterpret_cast<const void *>(&fast_intervals<false, false>));
     const uint8_t *vi = violation;
+    Rec *own = M.own[set], *cp = M.cp[set];
+    int32_t *meta = M.meta[set];
     void *args[] = {const_cast<GmgView *>(&G), const_cast<uint8_t **>(&Pc), const_cast<uint32_t **>(&fin),
-                    &j0, const_cast<Rec **>(&M.own), const_cast<Rec **>(&M.cp), const_cast<int32_t **>(&M.meta),
-                    &rank, &vi};
-    // the branch-free writer with index ranks stages its own-record stores
+                    &j0, &own, &cp, &meta, &rank, &vi};
+    // the branch-free writer with index ranks stages its stores
     const size_t lds = intervals_lds((int)g->n_dev, M.iv_fast && !given_ranks);
-    hipError_t err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
     SsTimingRec *ti = ss_timing_start(SS_KERNEL_INTERVALS, stream);
     err = hipLaunchKernel(fn, dim3((unsigned)nj), dim3(kWave), args, lds, stream);
     ss_timing_stop(ti, stream);
     if (err == hipSuccess) err = hipGetLastError();
     if (err != hipSuccess) return hip_fail(err, "fast_intervals launch");
-    SsTimingRec *tm = ss_timing_start(SS_KERNEL_MEMORY, stream);
-    hipLaunchKernelGGL(fast_peaks, dim3((unsigned)std::min<int64_t>(nj, M.nslots)), dim3(kWave), 0, stream, G, j0, nj,
-                       static_cast<const Rec *>(M.own), static_cast<const Rec *>(M.cp),
-                       static_cast<const int32_t *>(M.meta), M.wk, M.wb, M.slot_cap, peak, violation);
-    ss_timing_stop(tm, stream);
+    err = hipEventRecord(M.iv_done[set], stream);
+    if (err == hipSuccess) err = hipStreamWaitEvent(M.aux, M.iv_done[set], 0);
+    if (err != hipSuccess) return hip_fail(err, "ordering the peak pass");
+    SsTimingRec *tm = ss_timing_start(SS_KERNEL_MEMORY, M.aux);
+    hipLaunchKernelGGL(fast_peaks, dim3((unsigned)std::min<int64_t>(nj, M.nslots)), dim3(kWave), 0, M.aux, G, j0, nj,
+                       static_cast<const Rec *>(own), static_cast<const Rec *>(cp),
+                       static_cast<const int32_t *>(meta), M.wk, M.wb, M.slot_cap, peak, violation);
+    ss_timing_stop(tm, M.aux);
     err = hipGetLastError();
     if (err != hipSuccess) return hip_fail(err, "fast_peaks launch");
+    err = hipEventRecord(M.pk_done[set], M.aux);
+    if (err != hipSuccess) return hip_fail(err, "hipEventRecord");
   }
   return SS_OK;
 }
@@ -1528,7 +1621,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
   void *scratch = nullptr;
   err = hipMallocAsync(&scratch,
-                       sz_pt + 2 * sz_fin + sz_own + sz_cp + sz_meta + sz_rank + sz_wk + sz_wb,
+                       sz_pt + 2 * sz_fin + 2 * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb,
                        stream);
   if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
@@ -1540,14 +1633,22 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   auto *PT = reinterpret_cast<uint8_t *>(take(sz_pt));
   auto *finT = reinterpret_cast<uint32_t *>(take(sz_fin));
   auto *fin = reinterpret_cast<uint32_t *>(take(sz_fin));
-  auto *own = reinterpret_cast<Rec *>(take(sz_own));
-  auto *cp = reinterpret_cast<Rec *>(take(sz_cp));
-  auto *meta = reinterpret_cast<int32_t *>(take(sz_meta));
-  auto *rank = reinterpret_cast<uint16_t *>(take(sz_rank));
-  auto *wk = reinterpret_cast<uint32_t *>(take(sz_wk));
-  auto *wb = reinterpret_cast<int64_t *>(take(sz_wb));
+  MemPass M{};
+  for (int k = 0; k < 2; ++k) {
+    M.own[k] = reinterpret_cast<Rec *>(take(sz_own));
+    M.cp[k] = reinterpret_cast<Rec *>(take(sz_cp));
+    M.meta[k] = reinterpret_cast<int32_t *>(take(sz_meta));
+  }
+  M.rank = reinterpret_cast<uint16_t *>(take(sz_rank));
+  M.wk = reinterpret_cast<uint32_t *>(take(sz_wk));
+  M.wb = reinterpret_cast<int64_t *>(take(sz_wb));
+  M.sub = sub;
+  M.nslots = nslots;
+  M.slot_cap = slot_cap;
+  M.iv_fast = iv_fast;
+  M.aux = g->aux;
 
-  int rc = SS_OK;
+  int rc = mem_pass_events(M);
   auto check = [&](const char *what) {
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess && rc == SS_OK) rc = hip_fail(e, what);
@@ -1586,9 +1687,10 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
     }
     ss_timing_stop(tt, stream);
     if (!check("transpose launch")) break;
-    const MemPass M{own, cp, meta, rank, wk, wb, sub, nslots, slot_cap, iv_fast};
     rc = memory_passes(g, M, Pc, fin, nb, false, peak ? peak + b0 * D : nullptr, violation + b0, stream);
   }
+  const int jrc = mem_pass_join(M, stream);
+  if (rc == SS_OK) rc = jrc;
   err = hipFreeAsync(scratch, stream);
   if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
   return rc;
@@ -1630,8 +1732,8 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   const size_t sz_wk = align((size_t)nslots * 2 * (slot_cap + 2) * 4);
   const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
   void *scratch = nullptr;
-  err = hipMallocAsync(&scratch, sz_fin + sz_rank + sz_miss + sz_spill + sz_own + sz_cp + sz_meta + sz_wk + sz_wb,
-                       stream);
+  err = hipMallocAsync(&scratch,
+                       sz_fin + sz_rank + sz_miss + sz_spill + 2 * (sz_own + sz_cp + sz_meta) + sz_wk + sz_wb, stream);
   if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
   auto take = [&](size_t bytes) {
@@ -1643,13 +1745,22 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   auto *rank = reinterpret_cast<uint16_t *>(take(sz_rank));
   auto *miss = reinterpret_cast<uint16_t *>(take(sz_miss));
   auto *spill = reinterpret_cast<uint64_t *>(take(sz_spill));
-  auto *own = reinterpret_cast<Rec *>(take(sz_own));
-  auto *cp = reinterpret_cast<Rec *>(take(sz_cp));
-  auto *meta = reinterpret_cast<int32_t *>(take(sz_meta));
-  auto *wk = reinterpret_cast<uint32_t *>(take(sz_wk));
-  auto *wb = reinterpret_cast<int64_t *>(take(sz_wb));
+  MemPass M{};
+  for (int k = 0; k < 2; ++k) {
+    M.own[k] = reinterpret_cast<Rec *>(take(sz_own));
+    M.cp[k] = reinterpret_cast<Rec *>(take(sz_cp));
+    M.meta[k] = reinterpret_cast<int32_t *>(take(sz_meta));
+  }
+  M.rank = rank;
+  M.wk = reinterpret_cast<uint32_t *>(take(sz_wk));
+  M.wb = reinterpret_cast<int64_t *>(take(sz_wb));
+  M.sub = sub;
+  M.nslots = nslots;
+  M.slot_cap = slot_cap;
+  M.iv_fast = iv_fast;
+  M.aux = g->aux;
 
-  int rc = SS_OK;
+  int rc = mem_pass_events(M);
   for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
     const int64_t nb = std::min(chunk, B - b0);
     const uint8_t *Pc = P + b0 * N;
@@ -1663,9 +1774,10 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
       rc = hip_fail(err, "ready_schedule launch");
       break;
     }
-    const MemPass M{own, cp, meta, rank, wk, wb, sub, nslots, slot_cap, iv_fast};
     rc = memory_passes(g, M, Pc, fin, nb, true, peak ? peak + b0 * D : nullptr, violation + b0, stream);
   }
+  const int jrc = mem_pass_join(M, stream);
+  if (rc == SS_OK) rc = jrc;
   err = hipFreeAsync(scratch, stream);
   if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
   return rc;

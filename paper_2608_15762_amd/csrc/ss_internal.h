@@ -80,6 +80,9 @@ struct ss_gmg {
   int64_t max_indeg = 0;   // largest predecessor count of any op
   int64_t max_outdeg = 0;  // largest successor count of any op
   void *dev_mem = nullptr;
+  // second stream of the memory passes (the peak evaluation of one sub-chunk
+  // overlaps the interval pass of the next); default priority, non-blocking
+  hipStream_t aux = nullptr;
   GmgView view{};
 };
 
