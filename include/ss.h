@@ -186,8 +186,60 @@ int ss_select_best(const ss_gmg *g, const uint8_t *violation, const int64_t *key
 #define SS_KERNEL_SELECT 2       /* best-candidate reduction (both passes) */
 #define SS_KERNEL_INTERVALS 3    /* residency intervals into per-device buckets (fast path) */
 #define SS_KERNEL_TRANSPOSE 4    /* layout changes between the passes (fast path) */
+#define SS_KERNEL_ESTIMATOR 6    /* estimator accumulation, solves and predictions */
 int ss_kernel_timing(int enable);
 int ss_kernel_time(int kernel, int64_t *launches, double *total_ms);
+
+/*
+ * Online linear estimators (Sec. 3.3.1): the transfer estimator of an
+ * accelerator pair, t = alpha * size + c, and the operator estimator of an
+ * (accelerator type, template operator) pair, t = sum_j beta_j * phi_j(shape)
+ * over shape-derived features (e.g. bmnk, bmk, bkn, bmn, 1 for a batched
+ * matrix multiply), refined as the executor feeds back measured times.  An
+ * estimator set holds n_est ordinary least-squares fits with n_feat (1..8)
+ * features each.  Its state, on the HIP device current at creation, is every
+ * fit's sufficient statistics in float64: sum x x^T, sum x y and the sample
+ * count, accumulated over all samples added so far.  Calls on one set must be
+ * ordered (one stream, or synchronised): concurrent calls race.
+ */
+#define SS_EST_MAX_FEAT 8
+#define SS_EST_FITTED 0           /* coefficients solved */
+#define SS_EST_UNDERDETERMINED 1  /* fewer samples than features; coefficients 0 */
+#define SS_EST_SINGULAR 2         /* Gram matrix not positive definite (a Cholesky
+                                     pivot <= 1e-12 x its diagonal entry); coefficients 0 */
+typedef struct ss_est ss_est;
+
+/* Create a set with zeroed statistics on the current device.  n_est >= 0,
+ * 1 <= n_feat <= SS_EST_MAX_FEAT.  Errors: SS_ERR_INVALID_ARG, SS_ERR_OOM,
+ * SS_ERR_DEVICE. */
+int ss_est_create(int64_t n_est, int64_t n_feat, ss_est **out);
+
+/* Release a set (synchronises its device first).  NULL is a no-op. */
+void ss_est_free(ss_est *e);
+
+/* Add n_samples feedback samples, grouped by estimator: the samples of
+ * estimator i are rows [sample_ptr[i], sample_ptr[i+1]) of x[n_samples][n_feat]
+ * (features) and y[n_samples] (measured times).  DEVICE pointers; sample_ptr
+ * has n_est + 1 entries, non-decreasing from 0 to n_samples (ranges outside
+ * [0, n_samples) are clamped to it, never read beyond it).  Asynchronous on
+ * hip_stream; the sums of a set do not depend on how the device schedules the
+ * work (a fixed reduction order).  Errors: SS_ERR_INVALID_ARG, SS_ERR_DEVICE. */
+int ss_est_add(ss_est *e, const int64_t *sample_ptr, int64_t n_samples, const double *x, const double *y,
+               void *hip_stream);
+
+/* Solve every fit: coef[n_est][n_feat] (DEVICE, float64) and status[n_est]
+ * (DEVICE, SS_EST_*), from the normal equations by Cholesky factorisation.
+ * Asynchronous on hip_stream.  Errors: SS_ERR_INVALID_ARG, SS_ERR_DEVICE. */
+int ss_est_solve(const ss_est *e, double *coef, int32_t *status, void *hip_stream);
+
+/* Integer times for the simulator (durations of ss_gmg_desc.dur, or transfer
+ * times): out_us[i] = max(1, ceil(x[i] . coef[est_of[i]])) for M queries.
+ * DEVICE pointers: coef[n_est][n_feat], est_of[M], x[M][n_feat], out_us[M].
+ * out_us[i] = 0 marks a query naming an estimator outside [0, n_est) or whose
+ * prediction is not finite or reaches 2^62.  Asynchronous on hip_stream.
+ * Errors: SS_ERR_INVALID_ARG, SS_ERR_DEVICE. */
+int ss_est_predict(const double *coef, int64_t n_est, int64_t n_feat, const int32_t *est_of, const double *x,
+                   int64_t M, int64_t *out_us, void *hip_stream);
 
 /* Message for the calling thread's most recent failed call ("" if none). */
 const char *ss_last_error(void);

@@ -17,7 +17,9 @@ Readings where the paper is silent (each is listed in the design notes):
     fitted (status 2); the relative pivot threshold is 1e-12;
   - unfitted estimators report zero coefficients;
   - an integer time for the simulator is max(1, ceil(x . beta)) microseconds
-    (the simulator takes integer durations >= 1).
+    (the simulator takes integer durations >= 1); a query naming an unknown
+    estimator, or whose prediction is not finite or reaches 2^62, gets 0 (a
+    value no valid prediction takes).
 
 Everything is float64, plain numpy; nothing here is shared with the library.
 Pinned by tests/test_estimator_pins.py (exact recovery, the closed form of
@@ -102,5 +104,18 @@ def predict(coef, est, x):
 
 
 def predict_us(coef, est, x):
-    """Integer times for the simulator: max(1, ceil(x . coef[est]))."""
-    return np.array([max(1, math.ceil(t)) for t in predict(coef, est, x)], np.int64)
+    """Integer times for the simulator: max(1, ceil(x . coef[est])), or 0 for a
+    query naming an unknown estimator or predicting a non-finite time or one
+    of 2^62 or more."""
+    coef = np.asarray(coef, np.float64)
+    x = np.asarray(x, np.float64)
+    out = []
+    for i, e in enumerate(np.asarray(est, np.int64)):
+        if not 0 <= e < len(coef):
+            out.append(0)
+            continue
+        t = 0.0
+        for j in range(coef.shape[1]):  # the sum in feature order
+            t += x[i][j] * coef[e][j]
+        out.append(0 if not (math.isfinite(t) and math.ceil(t) < 2 ** 62) else max(1, math.ceil(t)))
+    return np.array(out, np.int64)

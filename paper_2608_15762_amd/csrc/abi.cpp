@@ -5,6 +5,8 @@
 #include <string>
 #include <vector>
 
+#include <climits>
+
 #include "ss_internal.h"
 
 struct SsTimingRec {
@@ -60,6 +62,62 @@ extern "C" int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int
                          static_cast<hipStream_t>(hip_stream), (layout & SS_DISPATCH_READY) != 0);
 }
 
+extern "C" int ss_est_create(int64_t n_est, int64_t n_feat, ss_est **out) {
+  ss_clear_error();
+  if (!out) return ss_set_error(SS_ERR_INVALID_ARG, "ss_est_create: out is NULL");
+  *out = nullptr;
+  if (n_est < 0 || n_feat < 1 || n_feat > SS_EST_MAX_FEAT)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_est_create: n_est < 0 or n_feat outside 1..8");
+  if (n_est > INT32_MAX || n_est > (int64_t(1) << 40) / (n_feat * n_feat + n_feat + 1))
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_est_create: n_est too large");
+  return ss_run_est_create(n_est, n_feat, out);
+}
+
+extern "C" void ss_est_free(ss_est *e) {
+  if (e) ss_run_est_free(e);
+}
+
+namespace {
+int check_est_device(const ss_est *e) {
+  int dev = 0, cur = 0;
+  ss_run_est_info(e, nullptr, nullptr, &dev);
+  if (hipGetDevice(&cur) != hipSuccess) return ss_set_error(SS_ERR_DEVICE, "hipGetDevice failed");
+  if (cur != dev) return ss_set_error(SS_ERR_INVALID_ARG, "the current HIP device is not the estimator set's");
+  return SS_OK;
+}
+}  // namespace
+
+extern "C" int ss_est_add(ss_est *e, const int64_t *sample_ptr, int64_t n_samples, const double *x, const double *y,
+                          void *hip_stream) {
+  ss_clear_error();
+  if (!e) return ss_set_error(SS_ERR_INVALID_ARG, "ss_est_add: e is NULL");
+  int64_t n_est = 0;
+  ss_run_est_info(e, &n_est, nullptr, nullptr);
+  if (n_samples < 0 || !sample_ptr || (n_samples > 0 && (!x || !y)))
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_est_add: n_samples < 0 or a NULL array");
+  const int rc = check_est_device(e);
+  if (rc != SS_OK) return rc;
+  return ss_run_est_add(e, sample_ptr, n_samples, x, y, static_cast<hipStream_t>(hip_stream));
+}
+
+extern "C" int ss_est_solve(const ss_est *e, double *coef, int32_t *status, void *hip_stream) {
+  ss_clear_error();
+  if (!e || !coef || !status) return ss_set_error(SS_ERR_INVALID_ARG, "ss_est_solve: a NULL argument");
+  const int rc = check_est_device(e);
+  if (rc != SS_OK) return rc;
+  return ss_run_est_solve(e, coef, status, static_cast<hipStream_t>(hip_stream));
+}
+
+extern "C" int ss_est_predict(const double *coef, int64_t n_est, int64_t n_feat, const int32_t *est_of,
+                              const double *x, int64_t M, int64_t *out_us, void *hip_stream) {
+  ss_clear_error();
+  if (n_est < 0 || n_feat < 1 || n_feat > SS_EST_MAX_FEAT || M < 0)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_est_predict: bad n_est, n_feat or M");
+  if (M > 0 && (!coef || !est_of || !x || !out_us))
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_est_predict: a NULL array");
+  return ss_run_est_predict(coef, n_est, n_feat, est_of, x, M, out_us, static_cast<hipStream_t>(hip_stream));
+}
+
 extern "C" int ss_select_best(const ss_gmg *g, const uint8_t *violation, const int64_t *key,
                               const int64_t *sla_slack, int64_t B, int flags, int64_t *out_best, void *hip_stream) {
   ss_clear_error();
@@ -108,7 +166,7 @@ extern "C" int ss_kernel_timing(int enable) {
 
 extern "C" int ss_kernel_time(int kernel, int64_t *launches, double *total_ms) {
   ss_clear_error();
-  if (!launches || !total_ms || kernel < SS_KERNEL_SCHEDULE || kernel > SS_KERNEL_TRANSPOSE)
+  if (!launches || !total_ms || kernel < SS_KERNEL_SCHEDULE || kernel > SS_KERNEL_ESTIMATOR)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_kernel_time: bad kernel id or NULL output");
   std::lock_guard<std::mutex> lk(g_timing_mu);
   int64_t n = 0;

@@ -107,5 +107,14 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *placements, int64_t B, 
 size_t ss_ready_schedule_lds(const ss_gmg *g);
 int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
                           uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream);
+// Estimators (estimator.hip).  Arguments are already checked.
+int ss_run_est_create(int64_t n_est, int64_t n_feat, ss_est **out);
+void ss_run_est_free(ss_est *e);
+int ss_run_est_info(const ss_est *e, int64_t *n_est, int64_t *n_feat, int *device);
+int ss_run_est_add(const ss_est *e, const int64_t *ptr, int64_t n_samples, const double *x, const double *y,
+                   hipStream_t stream);
+int ss_run_est_solve(const ss_est *e, double *coef, int32_t *status, hipStream_t stream);
+int ss_run_est_predict(const double *coef, int64_t n_est, int64_t n_feat, const int32_t *est_of, const double *x,
+                       int64_t M, int64_t *out, hipStream_t stream);
 int ss_run_select(const ss_gmg *g, const uint8_t *violation, const int64_t *key, const int64_t *slack, int64_t B,
                   int require_sla, int64_t *out_best, hipStream_t stream);

@@ -25,9 +25,14 @@ SS_VIOLATION_MEMORY = 0x1
 SS_VIOLATION_INVALID = 0x4
 SS_SELECT_REQUIRE_SLA = 0x1
 EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "ss_select_best", "ss_kernel_timing",
-            "ss_kernel_time", "ss_last_error")
+            "ss_kernel_time", "ss_last_error", "ss_est_create", "ss_est_free", "ss_est_add", "ss_est_solve",
+            "ss_est_predict")
 SS_KERNEL_SCHEDULE, SS_KERNEL_MEMORY, SS_KERNEL_SELECT, SS_KERNEL_INTERVALS, SS_KERNEL_TRANSPOSE = 0, 1, 2, 3, 4
-KERNEL_NAMES = {0: "schedule_kernel", 1: "memory_kernel", 2: "select", 3: "intervals_kernel", 4: "transpose"}
+SS_KERNEL_ESTIMATOR = 6
+KERNEL_NAMES = {0: "schedule_kernel", 1: "memory_kernel", 2: "select", 3: "intervals_kernel", 4: "transpose",
+                6: "estimator"}
+SS_EST_MAX_FEAT = 8
+SS_EST_FITTED, SS_EST_UNDERDETERMINED, SS_EST_SINGULAR = 0, 1, 2
 
 _lib = None
 _lock = threading.Lock()
@@ -70,6 +75,16 @@ def lib():
             L.ss_kernel_time.restype = ctypes.c_int
             L.ss_last_error.argtypes = []
             L.ss_last_error.restype = ctypes.c_char_p
+            L.ss_est_create.argtypes = [I64, I64, ctypes.POINTER(ctypes.c_void_p)]
+            L.ss_est_create.restype = ctypes.c_int
+            L.ss_est_free.argtypes = [P]
+            L.ss_est_free.restype = None
+            L.ss_est_add.argtypes = [P, P, I64, P, P, P]
+            L.ss_est_add.restype = ctypes.c_int
+            L.ss_est_solve.argtypes = [P, P, P, P]
+            L.ss_est_solve.restype = ctypes.c_int
+            L.ss_est_predict.argtypes = [P, I64, I64, P, P, I64, P, P]
+            L.ss_est_predict.restype = ctypes.c_int
             _lib = L
     return _lib
 
@@ -179,3 +194,50 @@ def kernel_time(kernel: int) -> tuple[int, float]:
     n, ms = ctypes.c_int64(), ctypes.c_double()
     _check(lib().ss_kernel_time(kernel, ctypes.byref(n), ctypes.byref(ms)))
     return n.value, ms.value
+
+
+class Estimators:
+    """An ss_est set: n_est online least-squares fits of n_feat features (Sec. 3.3.1)."""
+
+    def __init__(self, n_est: int, n_feat: int):
+        h = ctypes.c_void_p()
+        _check(lib().ss_est_create(n_est, n_feat, ctypes.byref(h)))
+        self.handle, self.n_est, self.n_feat = h, n_est, n_feat
+
+    def add(self, sample_ptr, x, y, stream=None):
+        """Samples grouped by estimator: int64 sample_ptr[n_est+1], float64 x[S][n_feat], y[S] (device)."""
+        S = y.shape[0]
+        assert sample_ptr.shape == (self.n_est + 1,) and x.shape == (S, self.n_feat)
+        assert sample_ptr.is_contiguous() and x.is_contiguous() and y.is_contiguous()
+        _check(lib().ss_est_add(self.handle, _ptr(sample_ptr), S, _ptr(x), _ptr(y), _stream_ptr(stream)))
+
+    def solve(self, stream=None):
+        """(coef float64[n_est][n_feat], status int32[n_est]) on the device."""
+        import torch
+        dev = torch.device("cuda", torch.cuda.current_device())
+        coef = torch.empty((self.n_est, self.n_feat), dtype=torch.float64, device=dev)
+        status = torch.empty(self.n_est, dtype=torch.int32, device=dev)
+        _check(lib().ss_est_solve(self.handle, _ptr(coef), _ptr(status), _stream_ptr(stream)))
+        return coef, status
+
+    def free(self):
+        if self.handle:
+            lib().ss_est_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def est_predict(coef, est_of, x, stream=None):
+    """Integer microseconds max(1, ceil(x . coef[est_of])) per query (0: invalid query)."""
+    import torch
+    M = est_of.shape[0]
+    n_est, n_feat = coef.shape
+    out = torch.empty(M, dtype=torch.int64, device=x.device)
+    _check(lib().ss_est_predict(_ptr(coef), n_est, n_feat, _ptr(est_of), _ptr(x), M, _ptr(out),
+                                _stream_ptr(stream)))
+    return out

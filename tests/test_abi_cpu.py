@@ -132,3 +132,20 @@ def test_unknown_layout_bits_are_rejected_before_the_device():
     for layout in (1, 0x200, 0x101):
         assert L.ss_simulate_batch(ctypes.c_void_p(8), None, 1, layout, None, None, None, None, None, None) == -1
         assert b"layout" in L.ss_last_error()
+
+
+def test_estimator_arguments_are_checked_before_the_device():
+    L = ss.lib()
+    h = ctypes.c_void_p()
+    assert L.ss_est_create(4, 0, ctypes.byref(h)) == -1
+    assert L.ss_est_create(4, 9, ctypes.byref(h)) == -1
+    assert L.ss_est_create(-1, 3, ctypes.byref(h)) == -1
+    assert L.ss_est_create(4, 3, None) == -1
+    assert L.ss_est_create(1 << 40, 1, ctypes.byref(h)) == -1
+    assert L.ss_est_add(None, None, 0, None, None, None) == -1
+    assert L.ss_est_solve(None, None, None, None) == -1
+    assert L.ss_est_predict(None, 1, 0, None, None, 1, None, None) == -1
+    assert L.ss_est_predict(None, 1, 2, None, None, -1, None, None) == -1
+    assert L.ss_est_predict(None, 1, 2, None, None, 3, None, None) == -1
+    assert L.ss_est_predict(None, 1, 2, None, None, 0, None, None) == 0  # nothing to do
+    L.ss_est_free(None)

@@ -137,3 +137,9 @@ def test_rank_handling():
 def test_integer_times_round_up_with_a_floor_of_one(t, expect):
     coef = np.array([[t]])
     assert est.predict_us(coef, [0], [[1.0]])[0] == expect
+
+
+def test_invalid_queries_give_zero():
+    coef = np.array([[2.0], [1e300]])
+    assert list(est.predict_us(coef, [0, 1, 2, -1], [[1.5], [10.0], [1.0], [1.0]])) == [3, 0, 0, 0]
+    assert est.predict_us(np.array([[float("nan")]]), [0], [[1.0]])[0] == 0
