@@ -3,9 +3,10 @@
 // sufficient statistics of every fit, in device memory, float64:
 //   gram[e][F][F] = sum x x^T,  mom[e][F] = sum x y,  count[e].
 //
-// est_accumulate  one wave per estimator: its lanes stride over the estimator's
+// est_accumulate  a group of lanes per estimator (sized to the batch's average
+//                 samples per estimator): its lanes stride over the estimator's
 //                 samples (grouped by estimator), sum in registers, and reduce
-//                 across the wave in a fixed order (results do not depend on
+//                 across the group in a fixed order (results do not depend on
 //                 scheduling), then add to the state.
 // est_solve       one lane per estimator: Cholesky factorisation of the Gram
 //                 matrix and two triangular solves for the coefficients.
@@ -27,55 +28,62 @@ namespace {
 constexpr int kWave = 64;
 constexpr double kPivotRtol = 1e-12;  // relative pivot below which a Gram matrix is singular
 
-__device__ __forceinline__ double wave_sum(double v) {
-  for (int o = kWave / 2; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
-}
-
-template <int F>
-__global__ __launch_bounds__(kWave) void est_accumulate(const int64_t *__restrict__ ptr, int64_t n_samples,
-                                                        const double *__restrict__ x, const double *__restrict__ y,
-                                                        double *__restrict__ gram, double *__restrict__ mom,
-                                                        int64_t *__restrict__ count) {
-  const int64_t e = blockIdx.x;
-  const int lane = threadIdx.x;
+// kL lanes per estimator (a power of two dividing 64): each wave serves
+// 64 / kL estimators, lane t of a group takes samples t, t + kL, ...; the
+// group then reduces by a fixed butterfly, so the sums do not depend on how
+// the device schedules the work.
+template <int F, int kL>
+__global__ __launch_bounds__(kWave) void est_accumulate(int64_t n_est, const int64_t *__restrict__ ptr,
+                                                        int64_t n_samples, const double *__restrict__ x,
+                                                        const double *__restrict__ y, double *__restrict__ gram,
+                                                        double *__restrict__ mom, int64_t *__restrict__ count) {
+  const int lane = threadIdx.x, t = lane & (kL - 1);
+  const int64_t e = (int64_t)blockIdx.x * (kWave / kL) + lane / kL;
+  const bool live = e < n_est;
+  const int64_t ec = live ? e : n_est - 1;
   // the estimator's samples, clamped to [0, n_samples)
-  const int64_t s0 = min(max(ptr[e], (int64_t)0), n_samples);
-  const int64_t s1 = min(max(ptr[e + 1], s0), n_samples);
+  const int64_t s0 = min(max(ptr[ec], (int64_t)0), n_samples);
+  const int64_t s1 = live ? min(max(ptr[ec + 1], s0), n_samples) : s0;
   double g[F * (F + 1) / 2], m[F];
 #pragma unroll
   for (int i = 0; i < F * (F + 1) / 2; ++i) g[i] = 0.0;
 #pragma unroll
   for (int i = 0; i < F; ++i) m[i] = 0.0;
-  for (int64_t s = s0 + lane; s < s1; s += kWave) {
+  for (int64_t s = s0 + t; s < s1; s += kL) {
     double v[F];
 #pragma unroll
     for (int i = 0; i < F; ++i) v[i] = x[s * F + i];
-    const double t = y[s];
+    const double yt = y[s];
     int k = 0;
 #pragma unroll
     for (int i = 0; i < F; ++i) {
-      m[i] = fma(v[i], t, m[i]);
+      m[i] = fma(v[i], yt, m[i]);
 #pragma unroll
       for (int j = i; j < F; ++j, ++k) g[k] = fma(v[i], v[j], g[k]);
     }
   }
-  double *ge = gram + e * F * F, *me = mom + e * F;
+  auto group_sum = [&](double v) {
+#pragma unroll
+    for (int o = kL / 2; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+  };
+  double *ge = gram + ec * F * F, *me = mom + ec * F;
+  const bool writer = live && t == 0;
   int k = 0;
 #pragma unroll
   for (int i = 0; i < F; ++i) {
-    const double mi = wave_sum(m[i]);
-    if (lane == 0) me[i] += mi;
+    const double mi = group_sum(m[i]);
+    if (writer) me[i] += mi;
 #pragma unroll
-    for (int j = i; j < F; ++j) {
-      const double gij = wave_sum(g[k++]);
-      if (lane == 0) {
+    for (int j = i; j < F; ++j, ++k) {
+      const double gij = group_sum(g[k]);
+      if (writer) {
         ge[i * F + j] += gij;
         if (j != i) ge[j * F + i] += gij;
       }
     }
   }
-  if (lane == 0) count[e] += s1 - s0;
+  if (writer) count[ec] += s1 - s0;
 }
 
 template <int F>
@@ -141,11 +149,30 @@ int hip_fail(hipError_t err, const char *what) {
                       std::string(what) + ": " + hipGetErrorString(err));
 }
 
+template <int F, int kL>
+void launch_group(const ss_est *E, const int64_t *ptr, int64_t S, const double *x, const double *y,
+                  hipStream_t stream) {
+  constexpr int64_t per = kWave / kL;  // estimators per wave
+  hipLaunchKernelGGL((est_accumulate<F, kL>), dim3((unsigned)((E->n_est + per - 1) / per)), dim3(kWave), 0, stream,
+                     E->n_est, ptr, S, x, y, E->gram, E->mom, E->count);
+}
+
+// Lanes per estimator from the average samples per estimator of the batch
+// (4 .. 64), so that most lanes have a sample.
 template <int F>
 void launch_accumulate(const ss_est *E, const int64_t *ptr, int64_t S, const double *x, const double *y,
                        hipStream_t stream) {
-  hipLaunchKernelGGL(est_accumulate<F>, dim3((unsigned)E->n_est), dim3(kWave), 0, stream, ptr, S, x, y, E->gram,
-                     E->mom, E->count);
+  const int64_t avg = S / E->n_est;
+  if (avg >= 48)
+    launch_group<F, 64>(E, ptr, S, x, y, stream);
+  else if (avg >= 24)
+    launch_group<F, 32>(E, ptr, S, x, y, stream);
+  else if (avg >= 12)
+    launch_group<F, 16>(E, ptr, S, x, y, stream);
+  else if (avg >= 6)
+    launch_group<F, 8>(E, ptr, S, x, y, stream);
+  else
+    launch_group<F, 4>(E, ptr, S, x, y, stream);
 }
 
 template <int F>

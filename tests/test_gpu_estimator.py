@@ -158,3 +158,17 @@ def test_large_set_sampled(dev):
         ref.add(np.full(s1 - s0, i), x[s0:s1], y[s0:s1])
     rc, rs = ref.solve()
     assert np.array_equal(gs[pick], rs) and np.allclose(gc[pick], rc, rtol=RTOL, atol=ATOL)
+
+
+@pytest.mark.parametrize("n_est,hi", [(1000, 6), (300, 20), (40, 400), (3, 1)])
+def test_lane_groups_for_every_batch_density(dev, n_est, hi):
+    """Batches with about 3, 10, 200 and under 1 samples per estimator take
+    different lane-group sizes (and estimator counts not divisible by them)."""
+    rng = np.random.default_rng(n_est + hi)
+    F = 3
+    ptr, x, y, ids, _ = grouped(rng, n_est, F, rng.integers(0, hi + 1, n_est))
+    ref = est.EstimatorSet(n_est, F)
+    ref.add(ids, x, y)
+    rc, rs = ref.solve()
+    gc, gs = gpu_fit(dev, n_est, F, [(ptr, x, y)])
+    assert np.array_equal(gs, rs) and np.allclose(gc, rc, rtol=RTOL, atol=ATOL)
