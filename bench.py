@@ -161,7 +161,7 @@ def cpu_baseline(g, cid, B, seconds, got, dispatch):
                 op_evals_per_s=len(idx) * g.n_ops / wall), dict(checked=int(len(idx)), mismatching_candidates=mism)
 
 
-EST_N, EST_F, EST_SAMPLES = 65536, 5, 1 << 20  # estimators, features, samples fed back per step
+EST_N, EST_F, EST_SAMPLES = 65536, 5, 1 << 23  # estimators, features, samples fed back per step
 
 
 def estimator_workload(seed=0):
