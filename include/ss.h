@@ -106,7 +106,8 @@ typedef struct ss_gmg_desc {
  */
 int ss_gmg_load(const ss_gmg_desc *desc, ss_gmg **out);
 
-/* Release a GMG (synchronises the device first).  NULL is a no-op. */
+/* Release a GMG and its scratch pool (synchronises the device first).  NULL
+ * is a no-op. */
 void ss_gmg_free(ss_gmg *g);
 
 /* Sizes of a loaded GMG; any output pointer may be NULL. */
@@ -151,8 +152,11 @@ int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req)
  * or without SS_DISPATCH_READY).
  * The call is asynchronous on hip_stream (NULL = the null stream); inputs must
  * stay valid and outputs are defined once that stream has been synchronised.
- * It allocates stream-ordered scratch on hip_stream for the duration of the
- * work.  B = 0 is a no-op.  Results are bit-identical to a sequential CPU
+ * It takes stream-ordered scratch on hip_stream, for the duration of the
+ * work, from a memory pool that g owns; the pool keeps that memory for later
+ * calls instead of handing it back to the device, so g holds the scratch of
+ * its largest call (for a fixed workload, calls after the first allocate no
+ * device memory) until ss_gmg_free.  B = 0 is a no-op.  Results are bit-identical to a sequential CPU
  * evaluation of the same rules.
  * Errors: SS_ERR_INVALID_ARG, SS_ERR_OOM, SS_ERR_DEVICE, SS_ERR_UNSUPPORTED.
  */

@@ -302,6 +302,23 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
       delete g;
       return ss_set_error(SS_ERR_DEVICE, "hipStreamCreateWithFlags failed");
     }
+    {
+      hipMemPoolProps props{};
+      props.allocType = hipMemAllocationTypePinned;
+      props.handleTypes = hipMemHandleTypeNone;
+      props.location.type = hipMemLocationTypeDevice;
+      props.location.id = g->device;
+      uint64_t keep = UINT64_MAX;  // never return freed scratch to the device early
+      hipError_t e = hipMemPoolCreate(&g->pool, &props);
+      if (e == hipSuccess) e = hipMemPoolSetAttribute(g->pool, hipMemPoolAttrReleaseThreshold, &keep);
+      if (e != hipSuccess) {
+        if (g->pool) (void)hipMemPoolDestroy(g->pool);
+        (void)hipStreamDestroy(g->aux);
+        (void)hipFree(g->dev_mem);
+        delete g;
+        return ss_set_error(SS_ERR_DEVICE, std::string("creating the scratch pool: ") + hipGetErrorString(e));
+      }
+    }
     auto *base = static_cast<unsigned char *>(g->dev_mem);
     GmgView &V = g->view;
     V.n_ops = (int32_t)N;
@@ -370,6 +387,7 @@ extern "C" void ss_gmg_free(ss_gmg *g) {
   (void)hipSetDevice(g->device);
   (void)hipDeviceSynchronize();
   if (g->aux) (void)hipStreamDestroy(g->aux);
+  if (g->pool) (void)hipMemPoolDestroy(g->pool);
   (void)hipFree(g->dev_mem);
   (void)hipSetDevice(prev);
   delete g;

@@ -20,19 +20,25 @@
 //                 the device id) into a rank table and counts per device.
 //                 Pass B writes every residency interval (Sec. 3.3.2) into a
 //                 per-device bucket: own outputs at their rank (so a device's
-//                 own intervals are start-sorted; staged in LDS and written in
-//                 whole 64-byte lines), one copy per (output, remote device)
-//                 in a region bounded by the device's summed in-degree, each
-//                 event tagged with where it falls among the device's own
-//                 starts (exact, or a small window around a known rank).  For
-//                 graphs of out-degree <= 2 pass B is branch free and
-//                 software-pipelined over chunks.
-//   fast_peaks    one wave per candidate, devices in turn, each device's
+//                 own intervals are start-sorted), one copy per (output,
+//                 remote device) in a region bounded by the device's summed
+//                 in-degree, each event tagged with where it falls among the
+//                 device's own starts (exact, or a small window around a
+//                 known rank).  For graphs of out-degree <= 2 pass B is
+//                 branch free and software-pipelined over chunks, and stages
+//                 both kinds of record in LDS to write them in 32-byte pairs.
+//   fast_peaks    persistent waves that take candidates from a ticket
+//                 counter; per candidate, devices in turn, each device's
 //                 records in registers (the next device's loaded meanwhile):
 //                 per-gap sums of allocations and frees between consecutive
 //                 own starts give the exact live bytes at every own start;
 //                 only gaps holding copies and frees whose bound exceeds the
 //                 best so far are swept event by event.
+// The peak pass of a sub-chunk runs on a second stream beside the interval
+// pass of the next one (the records are double-buffered).  The schedule of
+// the next chunk waits for the last peak pass: its launch is exactly one round
+// of resident waves, and waves placed late behind another kernel's would add
+// a second round.
 // Ready-time dispatch (the rule of Sec. 3.3.2), per chunk:
 //   ready_schedule one wave per candidate, the ready set in registers (a
 //                 spill list beyond), finish times in candidate rows and each
@@ -60,6 +66,11 @@ __device__ __forceinline__ int64_t imax64(int64_t a, int64_t b) { return a > b ?
 __device__ __forceinline__ void wave_lds_fence() {
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   __builtin_amdgcn_wave_barrier();
+}
+
+// Zero fill (used for counters that kernels take work tickets from).
+__global__ __launch_bounds__(256) void fill_zero_u32(uint32_t *__restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = 0;
 }
 
 // ------------------------------------------------------------------ transpose
@@ -1398,18 +1409,25 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
   return best;
 }
 
+// Blocks take candidates from a ticket counter (zero at launch) rather than
+// in a fixed stride: a block that starts late, or shares its CU with another
+// kernel's waves, takes fewer candidates instead of holding up the launch.
 __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0, int64_t nj,
                                                     const Rec *__restrict__ own_all, const Rec *__restrict__ cp_all,
                                                     const int32_t *__restrict__ meta, uint32_t *__restrict__ wk_all,
                                                     int64_t *__restrict__ wb_all, int64_t slot_cap,
-                                                    int64_t *__restrict__ peak, uint8_t *__restrict__ violation) {
+                                                    uint32_t *__restrict__ ticket, int64_t *__restrict__ peak,
+                                                    uint8_t *__restrict__ violation) {
   __shared__ AggLds s_agg;
   const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops];
   const int lane = threadIdx.x;
   uint32_t *g_ak = wk_all + (int64_t)blockIdx.x * 2 * (slot_cap + 2);
   int32_t *g_ag = reinterpret_cast<int32_t *>(g_ak + slot_cap + 2);
   int64_t *g_dl = wb_all + (int64_t)blockIdx.x * slot_cap;
-  for (int64_t j = blockIdx.x; j < nj; j += gridDim.x) {
+  // the next candidate's ticket is fetched while the current one runs
+  uint32_t tk = lane == 0 ? atomicAdd(ticket, 1u) : 0u;
+  for (int64_t j = (uint32_t)__shfl((int)tk, 0, kWave); j < nj; j = (uint32_t)__shfl((int)tk, 0, kWave)) {
+    tk = lane == 0 ? atomicAdd(ticket, 1u) : 0u;
     const int64_t c = j0 + j;
     if (violation[c] & SS_VIOLATION_INVALID) {
       if (peak)
@@ -1467,6 +1485,8 @@ struct MemPass {
   uint16_t *rank;  // given ranks: candidate rows of the whole chunk; else sub rows
   uint32_t *wk;
   int64_t *wb;
+  uint32_t *ticket;  // one zeroed counter per peak launch of the call
+  int64_t n_ticket;
   int64_t sub, nslots, slot_cap;
   bool iv_fast;
   hipStream_t aux;
@@ -1548,10 +1568,11 @@ int memory_passes(const ss_gmg *g, MemPass &M, const uint8_t *Pc, const uint32_t
     err = hipEventRecord(M.iv_done[set], stream);
     if (err == hipSuccess) err = hipStreamWaitEvent(M.aux, M.iv_done[set], 0);
     if (err != hipSuccess) return hip_fail(err, "ordering the peak pass");
+    if (M.it >= M.n_ticket) return ss_set_error(SS_ERR_DEVICE, "memory passes: more peak launches than counters");
     SsTimingRec *tm = ss_timing_start(SS_KERNEL_MEMORY, M.aux);
     hipLaunchKernelGGL(fast_peaks, dim3((unsigned)std::min<int64_t>(nj, M.nslots)), dim3(kWave), 0, M.aux, G, j0, nj,
                        static_cast<const Rec *>(own), static_cast<const Rec *>(cp),
-                       static_cast<const int32_t *>(meta), M.wk, M.wb, M.slot_cap, peak, violation);
+                       static_cast<const int32_t *>(meta), M.wk, M.wb, M.slot_cap, M.ticket + M.it, peak, violation);
     ss_timing_stop(tm, M.aux);
     err = hipGetLastError();
     if (err != hipSuccess) return hip_fail(err, "fast_peaks launch");
@@ -1619,11 +1640,13 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   const size_t sz_rank = align(((size_t)sub * N + 1) * 2);
   const size_t sz_wk = align((size_t)nslots * 2 * (slot_cap + 2) * 4);
   const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
+  const int64_t n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
+  const size_t sz_tk = align((size_t)n_ticket * 4);
   void *scratch = nullptr;
-  err = hipMallocAsync(&scratch,
-                       sz_pt + 2 * sz_fin + 2 * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb,
-                       stream);
-  if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of simulation scratch");
+  err = hipMallocFromPoolAsync(&scratch,
+                               sz_pt + 2 * sz_fin + 2 * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
+                               g->pool, stream);
+  if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
   auto take = [&](size_t bytes) {
     unsigned char *q = p;
@@ -1642,6 +1665,8 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   M.rank = reinterpret_cast<uint16_t *>(take(sz_rank));
   M.wk = reinterpret_cast<uint32_t *>(take(sz_wk));
   M.wb = reinterpret_cast<int64_t *>(take(sz_wb));
+  M.ticket = reinterpret_cast<uint32_t *>(take(sz_tk));
+  M.n_ticket = n_ticket;
   M.sub = sub;
   M.nslots = nslots;
   M.slot_cap = slot_cap;
@@ -1649,6 +1674,12 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   M.aux = g->aux;
 
   int rc = mem_pass_events(M);
+  if (rc == SS_OK) {
+    hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)std::min<int64_t>((n_ticket + 255) / 256, 1024)), dim3(256), 0,
+                       stream, M.ticket, n_ticket);
+    const hipError_t fe = hipGetLastError();
+    if (fe != hipSuccess) rc = hip_fail(fe, "fill_zero_u32 launch");
+  }
   auto check = [&](const char *what) {
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess && rc == SS_OK) rc = hip_fail(e, what);
@@ -1664,6 +1695,10 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
     }
     ss_timing_stop(tp, stream);
     if (!check("transpose launch")) break;
+    if (M.it > 0) {  // the schedule runs with no peak pass beside it
+      const hipError_t we = hipStreamWaitEvent(stream, M.pk_done[(M.it - 1) & 1], 0);
+      if (we != hipSuccess && rc == SS_OK) rc = hip_fail(we, "hipStreamWaitEvent");
+    }
     SsTimingRec *ts = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
     {
       const uint8_t *PTc = PT;
@@ -1731,10 +1766,13 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   const size_t sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
   const size_t sz_wk = align((size_t)nslots * 2 * (slot_cap + 2) * 4);
   const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
+  const int64_t n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
+  const size_t sz_tk = align((size_t)n_ticket * 4);
   void *scratch = nullptr;
-  err = hipMallocAsync(&scratch,
-                       sz_fin + sz_rank + sz_miss + sz_spill + 2 * (sz_own + sz_cp + sz_meta) + sz_wk + sz_wb, stream);
-  if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of simulation scratch");
+  err = hipMallocFromPoolAsync(
+      &scratch, sz_fin + sz_rank + sz_miss + sz_spill + 2 * (sz_own + sz_cp + sz_meta) + sz_wk + sz_wb + sz_tk, g->pool,
+      stream);
+  if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
   auto take = [&](size_t bytes) {
     unsigned char *q = p;
@@ -1754,6 +1792,8 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   M.rank = rank;
   M.wk = reinterpret_cast<uint32_t *>(take(sz_wk));
   M.wb = reinterpret_cast<int64_t *>(take(sz_wb));
+  M.ticket = reinterpret_cast<uint32_t *>(take(sz_tk));
+  M.n_ticket = n_ticket;
   M.sub = sub;
   M.nslots = nslots;
   M.slot_cap = slot_cap;
@@ -1761,6 +1801,12 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   M.aux = g->aux;
 
   int rc = mem_pass_events(M);
+  if (rc == SS_OK) {
+    hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)std::min<int64_t>((n_ticket + 255) / 256, 1024)), dim3(256), 0,
+                       stream, M.ticket, n_ticket);
+    const hipError_t fe = hipGetLastError();
+    if (fe != hipSuccess) rc = hip_fail(fe, "fill_zero_u32 launch");
+  }
   for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
     const int64_t nb = std::min(chunk, B - b0);
     const uint8_t *Pc = P + b0 * N;

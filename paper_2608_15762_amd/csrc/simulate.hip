@@ -609,8 +609,9 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
   const size_t sz_bydev = align((size_t)nslots * N * 4 + 4);
   const size_t sz_ev = align((size_t)nslots * slot_cap * 8);
   void *scratch = nullptr;
-  err = hipMallocAsync(&scratch, sz_fin + sz_comp + sz_miss + sz_spr + sz_spo + sz_bydev + 2 * sz_ev, stream);
-  if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of simulation scratch");
+  err = hipMallocFromPoolAsync(&scratch, sz_fin + sz_comp + sz_miss + sz_spr + sz_spo + sz_bydev + 2 * sz_ev,
+                               g->pool, stream);
+  if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
   auto take = [&](size_t bytes) {
     unsigned char *q = p;

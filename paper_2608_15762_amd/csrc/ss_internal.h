@@ -83,6 +83,10 @@ struct ss_gmg {
   // second stream of the memory passes (the peak evaluation of one sub-chunk
   // overlaps the interval pass of the next); default priority, non-blocking
   hipStream_t aux = nullptr;
+  // stream-ordered pool of the simulation scratch: freed scratch stays in
+  // the pool for the next call (no device allocation once the largest call
+  // has run) and goes back to the device with the handle
+  hipMemPool_t pool = nullptr;
   GmgView view{};
 };
 
