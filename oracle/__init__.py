@@ -21,7 +21,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liboracle.so")
-INDEX_ORDER, READY_ORDER = 0, 1
+INDEX_ORDER, READY_ORDER, LINK_PORTS = 0, 1, 2
 _lib = None
 _lock = threading.Lock()
 
@@ -58,6 +58,7 @@ def _get():
             lib.sso_peak_sweep.argtypes = [ctypes.POINTER(_Gmg), _P, _P, _P, _P]
             lib.sso_peak_pairwise.argtypes = [ctypes.POINTER(_Gmg), _P, _P, _P, _P]
             lib.sso_select_best.argtypes = [_I64, _I64, _P, _P, _P, ctypes.c_int, _P, _P]
+            lib.sso_port_transfers.argtypes = [ctypes.POINTER(_Gmg), _P, _P, _P, _P, _P, _P, _P]
             lib.sso_select_best.restype = None
             _lib = lib
     return _lib
@@ -171,6 +172,21 @@ def peak_pairwise(g, placement, st, fin) -> np.ndarray:
                                 peak.ctypes.data):
         raise MemoryError
     return peak
+
+
+def port_transfers(g, placement) -> dict:
+    """Transfers of one candidate under LINK_PORTS in admission order: producer
+    op, source and destination device, start and arrival (Sec. 3.5.2)."""
+    og = _og(g)
+    p = np.ascontiguousarray(placement, dtype=np.uint8)
+    E = max(int(og.g.pred_ptr[-1]), 1)
+    out = {k: np.zeros(E, np.int64) for k in ("op", "src", "dst", "start", "arrive")}
+    n = np.zeros(1, np.int64)
+    rc = _get().sso_port_transfers(ctypes.byref(og.c), p.ctypes.data, *(out[k].ctypes.data for k in
+                                   ("op", "src", "dst", "start", "arrive")), n.ctypes.data)
+    if rc != 0:
+        raise ValueError(f"sso_port_transfers returned {rc}")
+    return {k: v[:int(n[0])] for k, v in out.items()}
 
 
 def select_best(violation, key, slack=None, require_sla: bool = False) -> tuple[int, int]:

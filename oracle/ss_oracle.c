@@ -21,7 +21,9 @@
  *     priority order of the GMG); the ready-time dispatch of Sec. 3.3.2 is
  *     the SSO_READY_ORDER variant;
  *   - a transfer is pure latency starting at the producer's finish, one per
- *     (tensor, destination device), shared by all consumers there;
+ *     (tensor, destination device), shared by all consumers there; the
+ *     SSO_LINK_PORTS variant arbitrates transfers over per-device ports
+ *     instead (Sec. 3.5.2, see schedule_index_order_ports);
  *   - memory: an op's output occupies its device from the op's start until the
  *     later of its last local consumer's finish and its last outgoing
  *     transfer's arrival; a remote copy occupies the destination from the
@@ -128,6 +130,72 @@ static void schedule_index_order(const sso_gmg *g, const uint8_t *place, int64_t
   }
 }
 
+/* Position of consumer v in the successor list of u. */
+static int64_t succ_entry(const succ_csr *sc, int64_t u, int64_t v) {
+  for (int64_t q = sc->ptr[u]; q < sc->ptr[u + 1]; ++q)
+    if (sc->idx[q] == v) return q;
+  return -1; /* not reached: v is a successor of each of its predecessors */
+}
+
+/* SSO_LINK_PORTS.  The executor admits pending transfers as sets that share
+ * no source and no destination accelerator (Sec. 3.5.2): a device sends at
+ * most one tensor at a time and receives at most one at a time.  Reading for
+ * the simulator: the transfer of u's output to a remote device e is requested
+ * when u finishes; requests are admitted in the order their producers are
+ * dispatched (index order), and the requests of one producer in the order of
+ * their destinations' first consumers; an admitted transfer starts at the
+ * latest of its request, the moment its source's send port frees and the
+ * moment its destination's receive port frees, and holds both ports for its
+ * transfer estimate (ports are served in admission order, like a device's
+ * compute queue in index order).  A transfer whose estimate is zero moves
+ * nothing and neither waits for nor holds a port.  A consumer's input from
+ * another device is there when that transfer arrives.  xs/xa: start and arrival per successor entry of the
+ * successor CSR (equal for the consumers of u on one device; unused for local
+ * consumers). */
+static void schedule_index_order_ports(const sso_gmg *g, const uint8_t *place, const succ_csr *sc, int64_t *clock,
+                                       int64_t *send_free, int64_t *recv_free, int64_t *st, int64_t *fin,
+                                       int64_t *xs, int64_t *xa) {
+  for (int64_t d = 0; d < g->n_dev; ++d) clock[d] = send_free[d] = recv_free[d] = 0;
+  for (int64_t v = 0; v < g->n_ops; ++v) {
+    const int64_t d = place[v];
+    const int64_t w = op_duration(g, v, d);
+    int64_t ready = g->release[g->op_req[v]];
+    if (ready < 0) ready = 0;
+    for (int64_t e = g->pred_ptr[v]; e < g->pred_ptr[v + 1]; ++e) {
+      const int64_t u = g->pred_idx[e];
+      const int64_t arrive = place[u] == d ? fin[u] : xa[succ_entry(sc, u, v)];
+      if (arrive > ready) ready = arrive;
+    }
+    const int64_t t = ready > clock[d] ? ready : clock[d];
+    st[v] = earliest_fit(g, d, t, w);
+    fin[v] = st[v] + w;
+    clock[d] = fin[v];
+    for (int64_t q = sc->ptr[v]; q < sc->ptr[v + 1]; ++q) {
+      const int64_t dst = place[sc->idx[q]];
+      if (dst == d) continue;
+      int64_t first = q;
+      for (int64_t q2 = sc->ptr[v]; q2 < q; ++q2)
+        if (place[sc->idx[q2]] == dst) { first = q2; break; }
+      if (first != q) {  /* the tensor is already on its way to dst */
+        xs[q] = xs[first];
+        xa[q] = xa[first];
+        continue;
+      }
+      const int64_t x = transfer_time(g, v, d, dst);
+      if (x == 0) {
+        xs[q] = xa[q] = fin[v];
+        continue;
+      }
+      int64_t s0 = fin[v];
+      if (send_free[d] > s0) s0 = send_free[d];
+      if (recv_free[dst] > s0) s0 = recv_free[dst];
+      xs[q] = s0;
+      xa[q] = s0 + x;
+      send_free[d] = recv_free[dst] = xa[q];
+    }
+  }
+}
+
 /* binary min-heap of (ready, op) pairs */
 typedef struct { int64_t ready, op; } ready_item;
 
@@ -202,7 +270,7 @@ typedef struct { int64_t dev, lo, hi, bytes; } interval;
 /* Residency intervals of one scheduled candidate (see the memory reading in
  * the file header).  Returns the count, or -1 on allocation failure. */
 static int64_t residency_intervals(const sso_gmg *g, const uint8_t *place, const succ_csr *sc, const int64_t *st,
-                                   const int64_t *fin, interval **out) {
+                                   const int64_t *fin, const int64_t *xs, const int64_t *xa, interval **out) {
   const int64_t N = g->n_ops;
   int64_t cap = N + sc->ptr[N] + 1, n = 0;
   interval *iv = (interval *)malloc((size_t)cap * sizeof(interval));
@@ -218,12 +286,13 @@ static int64_t residency_intervals(const sso_gmg *g, const uint8_t *place, const
       free_at = fin[v];
       for (int64_t e = s0; e < s1; ++e) {
         const int64_t x = sc->idx[e], dx = place[x];
-        const int64_t t = (dx == d) ? fin[x] : fin[v] + transfer_time(g, v, d, dx);
+        const int64_t t = (dx == d) ? fin[x] : xa ? xa[e] : fin[v] + transfer_time(g, v, d, dx);
         if (t > free_at) free_at = t;
       }
     }
     iv[n++] = (interval){d, st[v], free_at, b};
-    /* one remote copy per destination device, from v's finish until the last
+    /* one remote copy per destination device, from the transfer's start (v's
+     * finish, or the admitted start with arbitrated ports) until the last
      * consumer on that device finishes */
     for (int64_t e = s0; e < s1; ++e) {
       const int64_t dx = place[sc->idx[e]];
@@ -235,7 +304,7 @@ static int64_t residency_intervals(const sso_gmg *g, const uint8_t *place, const
       int64_t last = 0;
       for (int64_t e2 = s0; e2 < s1; ++e2)
         if (place[sc->idx[e2]] == dx && fin[sc->idx[e2]] > last) last = fin[sc->idx[e2]];
-      iv[n++] = (interval){dx, fin[v], last, b};
+      iv[n++] = (interval){dx, xs ? xs[e] : fin[v], last, b};
     }
   }
   *out = iv;
@@ -295,9 +364,15 @@ static int valid_placement(const sso_gmg *g, const uint8_t *place) {
   return 1;
 }
 
-static int simulate_with(const sso_gmg *g, const succ_csr *sc, const uint8_t *place, int dispatch, int64_t *st,
-                         int64_t *fin, int64_t *clock, int64_t *peak_buf, int64_t *makespan, int64_t *peak,
-                         uint8_t *violation, int64_t *slack, int64_t *sumfin) {
+typedef struct {
+  int64_t *st, *fin, *clock, *peak, *send_free, *recv_free, *xs, *xa;
+} work_bufs;
+
+static int simulate_with(const sso_gmg *g, const succ_csr *sc, const uint8_t *place, int dispatch,
+                         const work_bufs *wb, int64_t *makespan, int64_t *peak, uint8_t *violation, int64_t *slack,
+                         int64_t *sumfin) {
+  int64_t *st = wb->st, *fin = wb->fin, *clock = wb->clock, *peak_buf = wb->peak;
+  const int ports = dispatch == SSO_LINK_PORTS;
   const int64_t N = g->n_ops, D = g->n_dev, R = g->n_req;
   if (!valid_placement(g, place)) {
     /* a placement naming a device outside the set is not simulated */
@@ -310,6 +385,8 @@ static int simulate_with(const sso_gmg *g, const succ_csr *sc, const uint8_t *pl
   }
   if (dispatch == SSO_READY_ORDER) {
     if (schedule_ready_order(g, place, sc, clock, st, fin) != 0) return -1;
+  } else if (ports) {
+    schedule_index_order_ports(g, place, sc, clock, wb->send_free, wb->recv_free, st, fin, wb->xs, wb->xa);
   } else {
     schedule_index_order(g, place, clock, st, fin);
   }
@@ -330,7 +407,7 @@ static int simulate_with(const sso_gmg *g, const succ_csr *sc, const uint8_t *pl
     for (int64_t r = 0; r < R; ++r) slack[r] = g->deadline[r] - slack[r];
   }
   interval *iv = 0;
-  const int64_t n = residency_intervals(g, place, sc, st, fin, &iv);
+  const int64_t n = residency_intervals(g, place, sc, st, fin, ports ? wb->xs : 0, ports ? wb->xa : 0, &iv);
   if (n < 0) return -1;
   const int rc = peak_by_sweep(g, iv, n, peak_buf);
   free(iv);
@@ -343,19 +420,23 @@ static int simulate_with(const sso_gmg *g, const succ_csr *sc, const uint8_t *pl
   return 0;
 }
 
-typedef struct {
-  int64_t *st, *fin, *clock, *peak;
-} work_bufs;
-
 static int alloc_work(const sso_gmg *g, work_bufs *w) {
-  w->st = (int64_t *)malloc(((size_t)g->n_ops + 1) * sizeof(int64_t));
-  w->fin = (int64_t *)malloc(((size_t)g->n_ops + 1) * sizeof(int64_t));
-  w->clock = (int64_t *)malloc(((size_t)g->n_dev + 1) * sizeof(int64_t));
-  w->peak = (int64_t *)malloc(((size_t)g->n_dev + 1) * sizeof(int64_t));
-  return (w->st && w->fin && w->clock && w->peak) ? 0 : -1;
+  const size_t N = (size_t)g->n_ops + 1, D = (size_t)g->n_dev + 1, E = (size_t)g->pred_ptr[g->n_ops] + 1;
+  w->st = (int64_t *)malloc(N * sizeof(int64_t));
+  w->fin = (int64_t *)malloc(N * sizeof(int64_t));
+  w->clock = (int64_t *)malloc(D * sizeof(int64_t));
+  w->peak = (int64_t *)malloc(D * sizeof(int64_t));
+  w->send_free = (int64_t *)malloc(D * sizeof(int64_t));
+  w->recv_free = (int64_t *)malloc(D * sizeof(int64_t));
+  w->xs = (int64_t *)malloc(E * sizeof(int64_t));
+  w->xa = (int64_t *)malloc(E * sizeof(int64_t));
+  return (w->st && w->fin && w->clock && w->peak && w->send_free && w->recv_free && w->xs && w->xa) ? 0 : -1;
 }
 
-static void free_work(work_bufs *w) { free(w->st); free(w->fin); free(w->clock); free(w->peak); }
+static void free_work(work_bufs *w) {
+  free(w->st); free(w->fin); free(w->clock); free(w->peak);
+  free(w->send_free); free(w->recv_free); free(w->xs); free(w->xa);
+}
 
 int sso_simulate_one(const sso_gmg *g, const uint8_t *place, int dispatch, int64_t *st, int64_t *fin,
                      int64_t *makespan, int64_t *peak, uint8_t *violation, int64_t *slack, int64_t *sumfin) {
@@ -363,8 +444,7 @@ int sso_simulate_one(const sso_gmg *g, const uint8_t *place, int dispatch, int64
   work_bufs w;
   if (build_succ(g, &sc) != 0) return -1;
   if (alloc_work(g, &w) != 0) { free_succ(&sc); free_work(&w); return -1; }
-  const int rc = simulate_with(g, &sc, place, dispatch, w.st, w.fin, w.clock, w.peak, makespan, peak, violation,
-                               slack, sumfin);
+  const int rc = simulate_with(g, &sc, place, dispatch, &w, makespan, peak, violation, slack, sumfin);
   if (rc == 0 && valid_placement(g, place)) {
     if (st) memcpy(st, w.st, (size_t)g->n_ops * sizeof(int64_t));
     if (fin) memcpy(fin, w.fin, (size_t)g->n_ops * sizeof(int64_t));
@@ -382,9 +462,8 @@ int sso_simulate_batch(const sso_gmg *g, const uint8_t *places, int64_t B, int d
   if (alloc_work(g, &w) != 0) { free_succ(&sc); free_work(&w); return -1; }
   int rc = 0;
   for (int64_t b = 0; b < B && rc == 0; ++b)
-    rc = simulate_with(g, &sc, places + b * g->n_ops, dispatch, w.st, w.fin, w.clock, w.peak, &makespan[b],
-                       peak ? peak + b * g->n_dev : 0, &violation[b], slack ? slack + b * g->n_req : 0,
-                       &sumfin[b]);
+    rc = simulate_with(g, &sc, places + b * g->n_ops, dispatch, &w, &makespan[b], peak ? peak + b * g->n_dev : 0,
+                       &violation[b], slack ? slack + b * g->n_req : 0, &sumfin[b]);
   free_work(&w);
   free_succ(&sc);
   return rc;
@@ -395,7 +474,7 @@ static int peak_common(const sso_gmg *g, const uint8_t *place, const int64_t *st
   succ_csr sc;
   if (build_succ(g, &sc) != 0) return -1;
   interval *iv = 0;
-  const int64_t n = residency_intervals(g, place, &sc, st, fin, &iv);
+  const int64_t n = residency_intervals(g, place, &sc, st, fin, 0, 0, &iv);
   free_succ(&sc);
   if (n < 0) return -1;
   int rc = 0;
@@ -438,4 +517,33 @@ void sso_select_best(int64_t B, int64_t n_req, const uint8_t *violation, const i
   }
   *best_idx = bi;
   *best_key = bk;
+}
+
+int sso_port_transfers(const sso_gmg *g, const uint8_t *place, int64_t *op, int64_t *src, int64_t *dst,
+                       int64_t *start, int64_t *arrive, int64_t *n) {
+  *n = 0;
+  if (!valid_placement(g, place)) return -2;
+  succ_csr sc;
+  work_bufs w;
+  if (build_succ(g, &sc) != 0) return -1;
+  if (alloc_work(g, &w) != 0) { free_succ(&sc); free_work(&w); return -1; }
+  schedule_index_order_ports(g, place, &sc, w.clock, w.send_free, w.recv_free, w.st, w.fin, w.xs, w.xa);
+  for (int64_t v = 0; v < g->n_ops; ++v)
+    for (int64_t q = sc.ptr[v]; q < sc.ptr[v + 1]; ++q) {
+      const int64_t dx = place[sc.idx[q]];
+      if (dx == place[v]) continue;
+      int first = 1;
+      for (int64_t q2 = sc.ptr[v]; q2 < q; ++q2)
+        if (place[sc.idx[q2]] == dx) first = 0;
+      if (!first) continue;
+      op[*n] = v;
+      src[*n] = place[v];
+      dst[*n] = dx;
+      start[*n] = w.xs[q];
+      arrive[*n] = w.xa[q];
+      ++*n;
+    }
+  free_work(&w);
+  free_succ(&sc);
+  return 0;
 }

@@ -44,6 +44,7 @@ typedef struct {
 /* dispatch rules */
 #define SSO_INDEX_ORDER 0  /* each device serves its ops in index (priority) order */
 #define SSO_READY_ORDER 1  /* global earliest-ready-time-first dispatch */
+#define SSO_LINK_PORTS 2   /* index order, transfers arbitrated over per-device send and receive ports */
 
 /* One candidate.  st/fin (length n_ops) and peak (n_dev), slack (n_req) may be
  * NULL.  Returns 0, or -1 on allocation failure. */
@@ -60,6 +61,13 @@ int sso_simulate_batch(const sso_gmg *g, const uint8_t *places, int64_t B, int d
 int sso_peak_sweep(const sso_gmg *g, const uint8_t *place, const int64_t *st, const int64_t *fin, int64_t *peak);
 int sso_peak_pairwise(const sso_gmg *g, const uint8_t *place, const int64_t *st, const int64_t *fin,
                       int64_t *peak);
+
+/* The transfers of one candidate under SSO_LINK_PORTS, in admission order:
+ * producer op, source and destination device, start and arrival.  The arrays
+ * hold at least n_edges entries; *n receives the count.  Returns 0, -1 on
+ * allocation failure, -2 for a placement naming a device outside the set. */
+int sso_port_transfers(const sso_gmg *g, const uint8_t *place, int64_t *op, int64_t *src, int64_t *dst,
+                       int64_t *start, int64_t *arrive, int64_t *n);
 
 /* Best feasible candidate: argmin over feasible b of (key[b], b); -1 if none. */
 void sso_select_best(int64_t B, int64_t n_req, const uint8_t *violation, const int64_t *key,
