@@ -32,6 +32,7 @@ extern "C" {
 
 #define SS_LAYOUT_ROW_MAJOR 0    /* placements[b * n_ops + v] = device of op v in candidate b */
 #define SS_DISPATCH_READY 0x100  /* OR into layout: ready-time dispatch (see ss_simulate_batch) */
+#define SS_LINK_PORTS 0x200      /* OR into layout: transfers arbitrated over device ports (see ss_simulate_batch) */
 
 #define SS_VIOLATION_MEMORY 0x1  /* some device's peak memory exceeds its capacity */
 #define SS_VIOLATION_INVALID 0x4 /* the placement names a device id >= n_dev; not simulated */
@@ -145,11 +146,27 @@ int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req)
  * rules accept every GMG the loader accepts; the ready-time rule evaluates a
  * candidate with one wavefront instead of one lane, so it costs more per
  * candidate, and it needs scratch for N ready entries per candidate in flight.
+ * With layout | SS_LINK_PORTS transfers contend for the devices' ports, after
+ * the arbitration of Sec. 3.5.2 (pending transfers that share a source or a
+ * destination are not admitted together): each device sends one tensor at a
+ * time and receives one at a time.  The transfer of an output to a remote
+ * device is requested at the producer's finish; requests are admitted in the
+ * order their producers are dispatched (for one producer, in the order of
+ * each destination's first consumer) and start at the latest of the request
+ * and the moments the source's send port and the destination's receive port
+ * free; a transfer holds both for its estimate (a zero estimate holds
+ * nothing).  Consumers on that device wait for its arrival; the copy there is
+ * allocated at the transfer's start and the producer's output is kept until
+ * its last transfer has arrived.  Index-order dispatch only: with
+ * SS_DISPATCH_READY as well the call fails with SS_ERR_UNSUPPORTED.  This
+ * variant runs on the general int64 kernels and needs scratch for two port
+ * clocks per device and one arrival time per edge for each candidate in
+ * flight.
  * A candidate naming a device >= n_dev is not simulated: violation =
  * SS_VIOLATION_INVALID, makespan = sumfin = INT64_MAX, peak = 0 and slack =
  * INT64_MIN.  This is a per-candidate result, not a call error.
  * placements: DEVICE pointer, uint8 [B][n_ops] for SS_LAYOUT_ROW_MAJOR (with
- * or without SS_DISPATCH_READY).
+ * or without the flags above).
  * The call is asynchronous on hip_stream (NULL = the null stream); inputs must
  * stay valid and outputs are defined once that stream has been synchronised.
  * It takes stream-ordered scratch on hip_stream, for the duration of the

@@ -50,8 +50,10 @@ extern "C" int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int
   ss_clear_error();
   if (!g) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: g is NULL");
   if (B < 0) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: B < 0");
-  if ((layout & ~SS_DISPATCH_READY) != SS_LAYOUT_ROW_MAJOR)
+  if ((layout & ~(SS_DISPATCH_READY | SS_LINK_PORTS)) != SS_LAYOUT_ROW_MAJOR)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: unknown layout");
+  if ((layout & SS_DISPATCH_READY) && (layout & SS_LINK_PORTS))
+    return ss_set_error(SS_ERR_UNSUPPORTED, "ss_simulate_batch: SS_LINK_PORTS takes index-order dispatch only");
   if (B == 0) return SS_OK;
   if (!out_makespan || !out_violation)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: out_makespan and out_violation are required");
@@ -59,7 +61,8 @@ extern "C" int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int
   const int rc = check_device(g);
   if (rc != SS_OK) return rc;
   return ss_run_simulate(g, placements, B, out_makespan, out_peak_mem, out_violation, out_sla_slack, out_sumfin,
-                         static_cast<hipStream_t>(hip_stream), (layout & SS_DISPATCH_READY) != 0);
+                         static_cast<hipStream_t>(hip_stream), (layout & SS_DISPATCH_READY) != 0,
+                         (layout & SS_LINK_PORTS) != 0);
 }
 
 extern "C" int ss_est_create(int64_t n_est, int64_t n_feat, ss_est **out) {

@@ -127,11 +127,12 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     if (horizon * (i128)std::max<int64_t>(N, 1) >= kSumLimit) return bad("n_ops times the horizon reaches 2^63");
 
     // successor CSR, ascending within each op
-    std::vector<int32_t> succ_ptr(N + 1, 0), succ_idx(E), fill(N, 0);
+    std::vector<int32_t> succ_ptr(N + 1, 0), succ_idx(E), succ_pe(E), fill(N, 0);
     for (int64_t v = 0; v < N; ++v) succ_ptr[v + 1] = succ_ptr[v] + outdeg[v];
     for (int64_t v = 0; v < N; ++v)
       for (int64_t e = d->pred_ptr[v]; e < d->pred_ptr[v + 1]; ++e) {
         const int32_t u = d->pred_idx[e];
+        succ_pe[succ_ptr[u] + fill[u]] = (int32_t)e;
         succ_idx[succ_ptr[u] + fill[u]++] = (int32_t)v;
       }
     std::vector<int32_t> pred_ptr(d->pred_ptr, d->pred_ptr + N + 1), slice_ptr(D + 1);
@@ -265,6 +266,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     const size_t o_pred_idx = pk.add(d->pred_idx, E * sizeof(int32_t));
     const size_t o_succ_ptr = pk.add(succ_ptr);
     const size_t o_succ_idx = pk.add(succ_idx);
+    const size_t o_succ_pe = pk.add(succ_pe);
     const size_t o_op_req = pk.add(d->op_req, N * sizeof(int32_t));
     const size_t o_dev_class = pk.add(d->dev_class, D * sizeof(int32_t));
     const size_t o_slice_ptr = pk.add(slice_ptr);
@@ -330,6 +332,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     V.pred_idx = reinterpret_cast<const int32_t *>(base + o_pred_idx);
     V.succ_ptr = reinterpret_cast<const int32_t *>(base + o_succ_ptr);
     V.succ_idx = reinterpret_cast<const int32_t *>(base + o_succ_idx);
+    V.succ_pe = reinterpret_cast<const int32_t *>(base + o_succ_pe);
     V.op_req = reinterpret_cast<const int32_t *>(base + o_op_req);
     V.dev_class = reinterpret_cast<const int32_t *>(base + o_dev_class);
     V.slice_ptr = reinterpret_cast<const int32_t *>(base + o_slice_ptr);

@@ -10,6 +10,11 @@
 //   (all lanes are at the same op), so it is read with wave-uniform loads.
 //   Finish times go to a per-chunk scratch row for the memory pass.
 //
+//   With kPorts (SS_LINK_PORTS) the lane also reserves each output's
+//   transfers on the devices' send and receive ports (clocks per device in
+//   global scratch, [2][device][candidate]) right after the producer is
+//   placed, and records each edge's arrival time ([edge][candidate]).
+//
 // ready_schedule_general: the ready-time dispatch rule, one wave per
 //   candidate (the ready set is searched by the whole wave at every step).
 //
@@ -36,9 +41,53 @@ constexpr int kMemBlocksPerCU = 4;
 __device__ __forceinline__ int64_t imax(int64_t a, int64_t b) { return a > b ? a : b; }
 
 // ------------------------------------------------------------------ schedule
+// Transfer arbitration over device ports (Sec. 3.5.2): a device sends one
+// tensor at a time and receives one at a time.  The transfers of op v's
+// output are requested at its finish f and admitted now, right after v is
+// placed (producers in index order; for one producer, destinations in the
+// order of their first consumers): start = max(f, send port of v's device,
+// receive port of the destination), both ports busy until the arrival.  A
+// zero estimate moves nothing and takes no port.  The arrival is written for
+// every edge from v into the destination device ([edge][candidate]).
+__device__ __forceinline__ void reserve_transfers(const GmgView &G, const uint8_t *prow, int v, int d, int64_t f,
+                                                  int64_t *port, int64_t *arr, int64_t nb, int64_t c) {
+  const int D = G.n_dev, K = G.n_link;
+  const int q0 = G.succ_ptr[v], q1 = G.succ_ptr[v + 1];
+  for (int q = q0; q < q1; ++q) {
+    int e = prow[G.succ_idx[q]];
+    if (e >= D) e = 0;  // an invalid candidate: walked on device 0, never reported
+    if (e == d) continue;
+    int first = q;
+    for (int q2 = q0; q2 < q; ++q2) {
+      int e2 = prow[G.succ_idx[q2]];
+      if (e2 >= D) e2 = 0;
+      if (e2 == e) {
+        first = q2;
+        break;
+      }
+    }
+    int64_t a;
+    if (first != q) {
+      a = arr[(int64_t)G.succ_pe[first] * nb + c];  // the tensor is already on its way to e
+    } else {
+      const int64_t x = G.xfer[(int64_t)v * K + G.link_class[d * D + e]];
+      a = f;
+      if (x > 0) {
+        int64_t *send = port + (int64_t)d * nb + c, *recv = port + (int64_t)(D + e) * nb + c;
+        a = imax(f, imax(*send, *recv)) + x;
+        *send = a;
+        *recv = a;
+      }
+    }
+    arr[(int64_t)G.succ_pe[q] * nb + c] = a;
+  }
+}
+
+template <bool kPorts>
 __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const uint8_t *__restrict__ P,
                                                          int64_t nb, int64_t *__restrict__ fin,
-                                                         int64_t *__restrict__ comp, int64_t *__restrict__ makespan,
+                                                         int64_t *__restrict__ comp, int64_t *__restrict__ port,
+                                                         int64_t *__restrict__ arr, int64_t *__restrict__ makespan,
                                                          int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
                                                          uint8_t *__restrict__ violation) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
@@ -55,6 +104,8 @@ __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const 
     cur[d * kWave + lane] = 0;
   }
   for (int r = 0; r < R; ++r) comp[(int64_t)r * nb + c] = G.release[r];
+  if (kPorts)
+    for (int d = 0; d < 2 * D; ++d) port[(int64_t)d * nb + c] = 0;
 
   bool invalid = false;
   int64_t ms = 0, sum = 0;
@@ -74,7 +125,7 @@ __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const 
       int64_t t = frow[u];
       int du = prow[u];
       if (du >= D) du = 0;
-      if (du != d) t += G.xfer[(int64_t)u * K + G.link_class[du * D + d]];
+      if (du != d) t = kPorts ? arr[(int64_t)e * nb + c] : t + G.xfer[(int64_t)u * K + G.link_class[du * D + d]];
       ready = imax(ready, t);
     }
     // one op at a time: not before the device's previous finish; then the
@@ -94,6 +145,7 @@ __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const 
     const int64_t f = s + w;
     frow[v] = f;
     clk[slot] = f;
+    if (kPorts) reserve_transfers(G, prow, v, d, f, port, arr, nb, c);
     ms = imax(ms, f);
     sum += f;
     int64_t *cr = comp + (int64_t)r * nb + c;
@@ -344,10 +396,12 @@ __global__ __launch_bounds__(kWave) void ready_schedule_general(
 // finish).  Key = 2 * time + (1 for an allocation), so frees sort first at
 // equal times (half-open intervals).  Zero-byte tensors contribute nothing.
 // kReady: the copy's last consumer on e is the one that finishes last (index
-// order and finish order agree under index-order dispatch).
-template <bool kWrite, bool kReady, class KP, class VP>
+// order and finish order agree under index-order dispatch).  kPorts: arrivals
+// come from the port reservations (arr, [edge][candidate]); a copy is
+// allocated at its transfer's start = arrival - estimate.
+template <bool kWrite, bool kReady, bool kPorts, class KP, class VP>
 __device__ int op_events(const GmgView &G, const uint8_t *prow, const int64_t *frow, int y, int e, KP keys,
-                         VP vals, int w) {
+                         VP vals, int w, const int64_t *arr, int64_t nb, int64_t c) {
   const int C = G.n_class, K = G.n_link, D = G.n_dev;
   int n = 0;
   const int64_t fy = frow[y];
@@ -365,7 +419,9 @@ __device__ int op_events(const GmgView &G, const uint8_t *prow, const int64_t *f
         for (int q = x0; q < x1; ++q) {
           const int x = G.succ_idx[q];
           const int dx = prow[x];
-          const int64_t t = (dx == e) ? frow[x] : fy + G.xfer[(int64_t)y * K + G.link_class[e * D + dx]];
+          const int64_t t = (dx == e)  ? frow[x]
+                            : kPorts ? arr[(int64_t)G.succ_pe[q] * nb + c]
+                                     : fy + G.xfer[(int64_t)y * K + G.link_class[e * D + dx]];
           F = imax(F, t);
         }
         keys[w + n] = 2 * F;
@@ -402,7 +458,9 @@ __device__ int op_events(const GmgView &G, const uint8_t *prow, const int64_t *f
     }
     if (!last) continue;
     if (kWrite) {
-      keys[w + n] = 2 * frow[u] + 1;
+      const int64_t t0 = kPorts ? arr[(int64_t)q * nb + c] - G.xfer[(int64_t)u * K + G.link_class[prow[u] * D + e]]
+                                : frow[u];
+      keys[w + n] = 2 * t0 + 1;
       vals[w + n] = bu;
       keys[w + n + 1] = 2 * fy;
       vals[w + n + 1] = -bu;
@@ -483,9 +541,10 @@ __device__ __forceinline__ int wave_exclusive_scan(int x, int lane, int *total) 
   return s - x;
 }
 
-template <bool kReady>
+template <bool kReady, bool kPorts>
 __global__ __launch_bounds__(kWave) void memory_kernel(const GmgView G, const uint8_t *__restrict__ P, int64_t nb,
-                                                       const int64_t *__restrict__ fin, int32_t *__restrict__ bydev_all,
+                                                       const int64_t *__restrict__ fin,
+                                                       const int64_t *__restrict__ arr, int32_t *__restrict__ bydev_all,
                                                        int64_t *__restrict__ gkeys_all,
                                                        int64_t *__restrict__ gvals_all, int64_t slot_cap,
                                                        int64_t *__restrict__ peak, uint8_t *__restrict__ violation) {
@@ -533,18 +592,19 @@ __global__ __launch_bounds__(kWave) void memory_kernel(const GmgView G, const ui
       if (hi > lo) {
         int mine = 0;
         for (int q = lo + lane; q < hi; q += kWave)
-          mine += op_events<false, kReady>(G, prow, frow, bydev[q], e, (int64_t *)nullptr, (int64_t *)nullptr, 0);
+          mine += op_events<false, kReady, kPorts>(G, prow, frow, bydev[q], e, (int64_t *)nullptr, (int64_t *)nullptr,
+                                                   0, arr, nb, c);
         int total;
         int w = wave_exclusive_scan(mine, lane, &total);
         if (total <= kMemCap) {
           for (int q = lo + lane; q < hi; q += kWave)
-            w += op_events<true, kReady>(G, prow, frow, bydev[q], e, skeys, svals, w);
+            w += op_events<true, kReady, kPorts>(G, prow, frow, bydev[q], e, skeys, svals, w, arr, nb, c);
           __syncthreads();
           sort_pairs(skeys, svals, total, lane);
           pk = max_prefix_sum(svals, total, lane);
         } else {
           for (int q = lo + lane; q < hi; q += kWave)
-            w += op_events<true, kReady>(G, prow, frow, bydev[q], e, gkeys, gvals, w);
+            w += op_events<true, kReady, kPorts>(G, prow, frow, bydev[q], e, gkeys, gvals, w, arr, nb, c);
           __syncthreads();
           sort_pairs(gkeys, gvals, total, lane);
           pk = max_prefix_sum(gvals, total, lane);
@@ -569,13 +629,15 @@ int hip_fail(hipError_t err, const char *what) {
 // General path: int64 times, any size the loader accepts; either dispatch rule.
 static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
                                 uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream,
-                                bool ready) {
+                                bool ready, bool ports) {
   const GmgView &G = g->view;
   const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req;
   const int64_t slot_cap = 2 * (N + E) + 2;
   if (slot_cap >= INT32_MAX) return ss_set_error(SS_ERR_UNSUPPORTED, "n_ops + n_edges too large for the memory pass");
-  const void *sched_fn = ready ? reinterpret_cast<const void *>(&ready_schedule_general)
-                               : reinterpret_cast<const void *>(&schedule_kernel);
+  if (ready && ports) return ss_set_error(SS_ERR_UNSUPPORTED, "transfer ports take index-order dispatch only");
+  const void *sched_fn = ready   ? reinterpret_cast<const void *>(&ready_schedule_general)
+                         : ports ? reinterpret_cast<const void *>(&schedule_kernel<true>)
+                                 : reinterpret_cast<const void *>(&schedule_kernel<false>);
   const size_t sched_lds = ready ? (size_t)D * (sizeof(int64_t) + sizeof(int32_t))
                                  : (size_t)D * kWave * (sizeof(int64_t) + sizeof(uint16_t));
   int cus = 0;
@@ -594,7 +656,8 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
 
   // per candidate: finish times and request completions; with ready-time
   // dispatch also missing-predecessor counts and the spill list
-  const int64_t per_cand = N * 8 + R * 8 + (ready ? N * (4 + 8 + 4) : 0);
+  // with transfer ports also two port clocks per device and an arrival per edge
+  const int64_t per_cand = N * 8 + R * 8 + (ready ? N * (4 + 8 + 4) : 0) + (ports ? (2 * D + E) * 8 : 0);
   int64_t chunk = kFinBudget / std::max<int64_t>(1, per_cand);
   chunk = std::max<int64_t>(kWave, chunk / kWave * kWave);
   chunk = std::min<int64_t>(chunk, B);
@@ -608,8 +671,11 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
   const size_t sz_spo = ready ? align((size_t)chunk * N * 4 + 4) : 0;
   const size_t sz_bydev = align((size_t)nslots * N * 4 + 4);
   const size_t sz_ev = align((size_t)nslots * slot_cap * 8);
+  const size_t sz_port = ports ? align((size_t)2 * D * chunk * 8) : 0;
+  const size_t sz_arr = ports ? align((size_t)E * chunk * 8 + 8) : 0;
   void *scratch = nullptr;
-  err = hipMallocFromPoolAsync(&scratch, sz_fin + sz_comp + sz_miss + sz_spr + sz_spo + sz_bydev + 2 * sz_ev,
+  err = hipMallocFromPoolAsync(&scratch,
+                               sz_fin + sz_comp + sz_miss + sz_spr + sz_spo + sz_bydev + 2 * sz_ev + sz_port + sz_arr,
                                g->pool, stream);
   if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
@@ -626,6 +692,8 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
   auto *bydev = reinterpret_cast<int32_t *>(take(sz_bydev));
   auto *gkeys = reinterpret_cast<int64_t *>(take(sz_ev));
   auto *gvals = reinterpret_cast<int64_t *>(take(sz_ev));
+  auto *port = ports ? reinterpret_cast<int64_t *>(take(sz_port)) : nullptr;
+  auto *arr = ports ? reinterpret_cast<int64_t *>(take(sz_arr)) : nullptr;
 
   int rc = SS_OK;
   for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
@@ -637,8 +705,9 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
                          spr, spo, comp, makespan + b0, sumfin ? sumfin + b0 : nullptr,
                          slack ? slack + b0 * R : nullptr, violation + b0);
     else
-      hipLaunchKernelGGL(schedule_kernel, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), sched_lds, stream,
-                         G, Pc, nb, fin, comp, makespan + b0, sumfin ? sumfin + b0 : nullptr,
+      hipLaunchKernelGGL(ports ? schedule_kernel<true> : schedule_kernel<false>,
+                         dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), sched_lds, stream, G, Pc, nb, fin,
+                         comp, port, arr, makespan + b0, sumfin ? sumfin + b0 : nullptr,
                          slack ? slack + b0 * R : nullptr, violation + b0);
     err = hipGetLastError();
     ss_timing_stop(t_sched, stream);
@@ -648,9 +717,10 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
     }
     const int64_t grid = std::min<int64_t>(nb, nslots);
     SsTimingRec *t_mem = ss_timing_start(SS_KERNEL_MEMORY, stream);
-    hipLaunchKernelGGL(ready ? memory_kernel<true> : memory_kernel<false>, dim3((unsigned)grid), dim3(kWave), 0,
-                       stream, G, Pc, nb, static_cast<const int64_t *>(fin), bydev, gkeys, gvals, slot_cap,
-                       peak ? peak + b0 * D : nullptr, violation + b0);
+    auto *mem_fn = ready ? &memory_kernel<true, false> : ports ? &memory_kernel<false, true> : &memory_kernel<false, false>;
+    hipLaunchKernelGGL(mem_fn, dim3((unsigned)grid), dim3(kWave), 0, stream, G, Pc, nb,
+                       static_cast<const int64_t *>(fin), static_cast<const int64_t *>(arr), bydev, gkeys, gvals,
+                       slot_cap, peak ? peak + b0 * D : nullptr, violation + b0);
     err = hipGetLastError();
     ss_timing_stop(t_mem, stream);
     if (err != hipSuccess) rc = hip_fail(err, "memory_kernel launch");
@@ -664,17 +734,20 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
 // state fits; SS_PATH=generic or SS_PATH=fast in the environment forces one
 // (fast is still refused when the GMG does not qualify).
 int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
-                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch) {
+                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch,
+                    bool link_ports) {
   int lds_max = 0;
   hipError_t err = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
   const bool fast_ok = g->view.time32 && (ready_dispatch ? ss_ready_schedule_lds(g) : ss_fast_schedule_lds(g)) <=
                                              (size_t)lds_max;
   const char *path = std::getenv("SS_PATH");
-  if (path && std::strcmp(path, "fast") == 0 && !fast_ok)
-    return ss_set_error(SS_ERR_UNSUPPORTED, "SS_PATH=fast but this GMG needs the general path");
-  const bool generic = !fast_ok || (path && std::strcmp(path, "generic") == 0);
-  if (generic) return run_simulate_generic(g, P, B, makespan, peak, violation, slack, sumfin, stream, ready_dispatch);
+  if (path && std::strcmp(path, "fast") == 0 && (!fast_ok || link_ports))
+    return ss_set_error(SS_ERR_UNSUPPORTED, "SS_PATH=fast but this GMG or dispatch needs the general path");
+  // transfer ports run on the general kernels only
+  const bool generic = !fast_ok || link_ports || (path && std::strcmp(path, "generic") == 0);
+  if (generic)
+    return run_simulate_generic(g, P, B, makespan, peak, violation, slack, sumfin, stream, ready_dispatch, link_ports);
   if (ready_dispatch) return ss_run_simulate_ready(g, P, B, makespan, peak, violation, slack, sumfin, stream);
   return ss_run_simulate_fast(g, P, B, makespan, peak, violation, slack, sumfin, stream);
 }

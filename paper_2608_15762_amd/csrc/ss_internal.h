@@ -14,6 +14,7 @@ struct GmgView {
   int32_t n_ops, n_dev, n_class, n_link, n_req;
   const int32_t *pred_ptr, *pred_idx;  // predecessor CSR
   const int32_t *succ_ptr, *succ_idx;  // successor CSR, ascending within an op
+  const int32_t *succ_pe;              // [E] position of each successor entry's edge in the predecessor CSR
   const int32_t *op_req, *dev_class, *slice_ptr;
   const int64_t *dur;        // [N][n_class]
   const int64_t *out_bytes;  // [N]
@@ -102,7 +103,8 @@ void ss_timing_stop(SsTimingRec *rec, hipStream_t stream);
 
 // Kernel drivers (simulate.hip / select.hip).  Arguments are already checked.
 int ss_run_simulate(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
-                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch);
+                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch,
+                    bool link_ports);
 // Fast path (sim_fast.hip): 32-bit times, N <= 65535.
 size_t ss_fast_schedule_lds(const ss_gmg *g);
 int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,

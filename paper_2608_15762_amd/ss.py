@@ -20,7 +20,9 @@ ERRORS = {-1: "SS_ERR_INVALID_ARG", -2: "SS_ERR_INVALID_GMG", -3: "SS_ERR_OOM", 
           -5: "SS_ERR_UNSUPPORTED"}
 SS_LAYOUT_ROW_MAJOR = 0
 SS_DISPATCH_READY = 0x100
+SS_LINK_PORTS = 0x200
 DISPATCH = {"index": 0, "ready": SS_DISPATCH_READY}
+LINKS = {"latency": 0, "ports": SS_LINK_PORTS}
 SS_VIOLATION_MEMORY = 0x1
 SS_VIOLATION_INVALID = 0x4
 SS_SELECT_REQUIRE_SLA = 0x1
@@ -144,21 +146,24 @@ class Gmg:
 
 
 def simulate_batch_into(g: Gmg, placements, makespan, violation, peak=None, slack=None, sumfin=None,
-                        stream=None, dispatch="index"):
+                        stream=None, dispatch="index", links="latency"):
     """ss_simulate_batch on caller-provided torch CUDA tensors (row-major).
 
     dispatch: "index" (every device serves its ops in index order) or "ready"
-    (earliest ready time first, SS_DISPATCH_READY)."""
+    (earliest ready time first, SS_DISPATCH_READY).
+    links: "latency" (a transfer takes its estimate from the producer's
+    finish) or "ports" (transfers arbitrated over the devices' send and
+    receive ports, SS_LINK_PORTS)."""
     B = placements.shape[0]
     assert placements.dtype.is_floating_point is False and placements.element_size() == 1
     assert placements.is_contiguous() and placements.shape == (B, g.n_ops)
-    layout = SS_LAYOUT_ROW_MAJOR | DISPATCH[dispatch]
+    layout = SS_LAYOUT_ROW_MAJOR | DISPATCH[dispatch] | LINKS[links]
     _check(lib().ss_simulate_batch(g.handle, _ptr(placements), B, layout, _ptr(makespan), _ptr(peak),
                                    _ptr(violation), _ptr(slack), _ptr(sumfin), _stream_ptr(stream)))
 
 
 def simulate_batch(g: Gmg, placements, want_peak=True, want_slack=True, want_sumfin=True, stream=None,
-                   dispatch="index") -> dict:
+                   dispatch="index", links="latency") -> dict:
     """Allocate outputs on placements' device and run ss_simulate_batch."""
     import torch
     B = placements.shape[0]
@@ -169,7 +174,7 @@ def simulate_batch(g: Gmg, placements, want_peak=True, want_slack=True, want_sum
                slack=torch.empty((B, g.n_req), dtype=torch.int64, device=dev) if want_slack else None,
                sumfin=torch.empty(B, dtype=torch.int64, device=dev) if want_sumfin else None)
     simulate_batch_into(g, placements, out["makespan"], out["violation"], out["peak"], out["slack"], out["sumfin"],
-                        stream, dispatch)
+                        stream, dispatch, links)
     return out
 
 

@@ -120,6 +120,8 @@ def test_binding_constants_match_the_header():
     assert c["SS_LAYOUT_ROW_MAJOR"] == ss.SS_LAYOUT_ROW_MAJOR
     assert c["SS_DISPATCH_READY"] == ss.SS_DISPATCH_READY == ss.DISPATCH["ready"]
     assert c["SS_DISPATCH_READY"] & c["SS_LAYOUT_ROW_MAJOR"] == 0
+    assert c["SS_LINK_PORTS"] == ss.SS_LINK_PORTS == ss.LINKS["ports"]
+    assert c["SS_LINK_PORTS"] & (c["SS_DISPATCH_READY"] | c["SS_LAYOUT_ROW_MAJOR"]) == 0
     assert c["SS_VIOLATION_MEMORY"] == ss.SS_VIOLATION_MEMORY and c["SS_VIOLATION_INVALID"] == ss.SS_VIOLATION_INVALID
     assert c["SS_SELECT_REQUIRE_SLA"] == ss.SS_SELECT_REQUIRE_SLA
     for code, name in ss.ERRORS.items():
@@ -129,9 +131,12 @@ def test_binding_constants_match_the_header():
 def test_unknown_layout_bits_are_rejected_before_the_device():
     L = ss.lib()
     # a non-null dummy handle is never dereferenced: the layout check comes first
-    for layout in (1, 0x200, 0x101):
+    for layout in (1, 0x400, 0x101, 0x201):
         assert L.ss_simulate_batch(ctypes.c_void_p(8), None, 1, layout, None, None, None, None, None, None) == -1
         assert b"layout" in L.ss_last_error()
+    # transfer ports with ready-time dispatch: refused as unsupported
+    assert L.ss_simulate_batch(ctypes.c_void_p(8), None, 1, 0x300, None, None, None, None, None, None) == -5
+    assert b"SS_LINK_PORTS" in L.ss_last_error()
 
 
 def test_estimator_arguments_are_checked_before_the_device():
