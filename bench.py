@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--candidates", type=int, default=0, help="first N candidates only (default: the whole batch)")
     ap.add_argument("--dispatch", choices=("index", "ready"), default="index",
                     help="device queues in index order (default) or earliest ready time first")
+    ap.add_argument("--links", choices=("latency", "ports"), default="latency",
+                    help="transfers take their estimate (default) or contend for device send/receive ports")
     ap.add_argument("--part", choices=("simulate", "estimator"), default="simulate",
                     help="the what-if simulator (default) or the online estimators")
     return ap.parse_args()
@@ -129,14 +131,14 @@ def sample_rows(synth, g, cid, idx):
     return out
 
 
-def cpu_baseline(g, cid, B, seconds, got, dispatch):
+def cpu_baseline(g, cid, B, seconds, got, dispatch, links="latency"):
     """The oracle, as it stands, on a bounded evenly spaced sample of the same
     batch, on the host's cores; its results are also compared with the GPU's."""
     import oracle
     from paper_2608_15762_amd import synth
 
     threads = max(1, min(16, len(os.sched_getaffinity(0))))
-    mode = oracle.READY_ORDER if dispatch == "ready" else oracle.INDEX_ORDER
+    mode = oracle.READY_ORDER if dispatch == "ready" else oracle.LINK_PORTS if links == "ports" else oracle.INDEX_ORDER
     og = oracle.OracleGmg(g)
     pilot = sample_rows(synth, g, cid, np.linspace(0, B - 1, 9).astype(np.int64))
     oracle.simulate_batch(og, pilot[:1], dispatch=mode, n_threads=1)  # first call pays one-time costs
@@ -292,7 +294,7 @@ def main():
 
     def step():
         ss.simulate_batch_into(h, P, out["makespan"], out["violation"], out["peak"], out["slack"], out["sumfin"],
-                               stream=stream, dispatch=args.dispatch)
+                               stream=stream, dispatch=args.dispatch, links=args.links)
         ss.select_best(h, out["violation"], out["sumfin"], out=best, stream=stream)
 
     for i in range(args.warmup):
@@ -319,7 +321,7 @@ def main():
     launches_per_step = max(1, kernels[dom]["launches"] // args.steps)
     cand_per_launch = B / launches_per_step
     achieved = bytes_per_cand * cand_per_launch / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
-    traffic = measured_traffic().get(dom) if args.dispatch == "index" else None
+    traffic = measured_traffic().get(dom) if args.dispatch == "index" and args.links == "latency" else None
     if traffic is not None:
         traffic = round(traffic * cand_per_launch)
     result = {
@@ -327,7 +329,8 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 2), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
         "config": {"workload": cfg.name, "n_ops": N, "n_edges": g.n_edges, "n_dev": D, "n_req": R,
-                   "candidates": B, "idle_slices_per_device": cfg.n_slices, "dispatch": args.dispatch},
+                   "candidates": B, "idle_slices_per_device": cfg.n_slices, "dispatch": args.dispatch,
+                   "links": args.links},
         "op_evals_per_s": round(value * N, 1),
         "path_hbm_frac": round(value * bytes_per_cand / (HBM_PEAK_GBS * 1e9), 6),
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS,
@@ -342,7 +345,7 @@ def main():
     if not args.no_cpu_baseline:
         got = {k: v.cpu().numpy() for k, v in out.items()}
         log("running the oracle CPU baseline")
-        cb, par = cpu_baseline(g, cid, B, args.cpu_seconds, got, args.dispatch)
+        cb, par = cpu_baseline(g, cid, B, args.cpu_seconds, got, args.dispatch, args.links)
         result["cpu_baseline"] = cb
         result["parity_sample"] = par
     print(json.dumps(result), flush=True)
