@@ -465,6 +465,55 @@ def base_placement(g: Gmg, cid: int) -> np.ndarray:
     return p
 
 
+def partition_table(g: Gmg, cid: int) -> np.ndarray:
+    """Pre-defined partitions for the incremental loop (Sec. 3.4.2): for every node
+    and every group size k in (devices per node, half of it, ..., 1), the node's
+    devices (by id) split into groups of k; each group is one partition.  The
+    mapping of a request's ops onto a partition is fixed: its ops, in index order,
+    cut into k contiguous stages balanced by cumulative duration, stage s on the
+    group's s-th device.  Returns part_dev [n_part][n_ops] (uint8)."""
+    cfg = CONFIGS[cid]
+    D = g.n_dev
+    dpn = D // cfg.n_nodes
+    sizes = []
+    k = dpn
+    while k >= 1:
+        sizes.append(k)
+        k //= 2
+    groups = [list(range(n * dpn + j * k, n * dpn + (j + 1) * k))
+              for n in range(cfg.n_nodes) for k in sizes for j in range(dpn // k)]
+    out = np.zeros((len(groups), g.n_ops), np.uint8)
+    for r in range(g.n_req):
+        ops = np.nonzero(g.op_req == r)[0]
+        w = g.dur[ops, 0]
+        total = max(int(w.sum()), 1)
+        before = np.concatenate([[0], np.cumsum(w)[:-1]]) if len(ops) else np.zeros(0, np.int64)
+        for p, grp in enumerate(groups):
+            stage = np.minimum(len(grp) - 1, (before * len(grp)) // total)
+            out[p, ops] = np.asarray(grp, np.uint8)[stage]
+    return out
+
+
+def completion_feedback(g: Gmg, issued, place, key: int, step: int) -> list:
+    """Executor feedback for a driver of the incremental loop: the lower-index half
+    (at least one) of the issued ops complete, each with a measured duration equal
+    to its estimate on its device scaled by a seeded factor in [0.9, 1.1] (>= 1).
+    Returns [(op, measured duration)]."""
+    issued = sorted(int(v) for v in issued)
+    done = issued[:max(1, len(issued) // 2)]
+    st = Stream(draw(key, 0x5C4ED + step))
+    out = []
+    for v in done:
+        est = int(g.dur[v, g.dev_class[place[v]]])
+        out.append((v, max(1, est * st.uniform_int(900, 1100) // 1000)))
+    return out
+
+
+def request_priority(g: Gmg) -> np.ndarray:
+    """Per-request priority of the incremental loop: the deadline (earlier first)."""
+    return np.asarray(g.deadline, np.int64).copy()
+
+
 # --------------------------------------------------------------------------------------
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libsynth.so")
