@@ -262,6 +262,82 @@ int ss_est_solve(const ss_est *e, double *coef, int32_t *status, void *hip_strea
 int ss_est_predict(const double *coef, int64_t n_est, int64_t n_feat, const int32_t *est_of, const double *x,
                    int64_t M, int64_t *out_us, void *hip_stream);
 
+/*
+ * Incremental simulation-based scheduling (Alg. 1, Sec. 3.4).  A scheduler
+ * holds the GMG of a whole run (every op that will be scheduled) with a state
+ * per op, and keeps the two frontiers of Sec. 3.4.1: the scheduled frontier
+ * (issued or done ops with an unscheduled successor, whose outputs stay on
+ * their devices as checkpoints) and the unscheduled frontier (unscheduled ops
+ * whose predecessors are all issued or done).
+ *
+ * ss_sched_desc (HOST pointers, copied by ss_sched_create):
+ *   gmg            the run's GMG; the loader's rules apply (ss_gmg_load).
+ *   n_part, part_dev[n_part][n_ops]  the pre-defined partitions (Sec. 3.4.2):
+ *                  partition p places op v on device part_dev[p][v] (< n_dev).
+ *   priority[n_req] request priority, smaller first (for instance the
+ *                  deadline); ties go to the lower op index.
+ *   issue_budget   Alg. 1's budget on issued (not yet done) ops, >= 1.
+ *   batch_cap      the batch cap of CollectConnectedGraph, >= 1.
+ *   flags          0 or SS_SELECT_REQUIRE_SLA (feasibility also requires every
+ *                  request's slack >= 0).
+ */
+#define SS_OP_UNSCHEDULED 0
+#define SS_OP_ISSUED 1
+#define SS_OP_DONE 2
+#define SS_ROUND_ISSUED 0     /* a batch was placed and marked issued */
+#define SS_ROUND_BUDGET 1     /* issued ops >= issue_budget: nothing done */
+#define SS_ROUND_IDLE 2       /* the unscheduled frontier is empty (all ops scheduled) */
+#define SS_ROUND_INFEASIBLE 3 /* no partition is feasible for the batch: nothing issued */
+
+typedef struct ss_sched ss_sched;
+typedef struct ss_sched_desc {
+  const ss_gmg_desc *gmg;
+  int64_t n_part;
+  const uint8_t *part_dev;
+  const int64_t *priority;
+  int64_t issue_budget;
+  int64_t batch_cap;
+  int flags;
+} ss_sched_desc;
+
+/* Create a scheduler on the CURRENT HIP device; every op starts unscheduled.
+ * Errors: SS_ERR_INVALID_ARG, SS_ERR_INVALID_GMG, SS_ERR_OOM, SS_ERR_DEVICE,
+ * SS_ERR_UNSUPPORTED. */
+int ss_sched_create(const ss_sched_desc *desc, ss_sched **out);
+
+/* Release a scheduler (synchronises its device first).  NULL is a no-op. */
+void ss_sched_free(ss_sched *s);
+
+/*
+ * One round of Alg. 1.  Returns at once (SS_ROUND_BUDGET, SS_ROUND_IDLE) when
+ * the issued ops reach the budget or the unscheduled frontier is empty.
+ * Otherwise: the highest-priority op of the unscheduled frontier; its batch,
+ * collected by repeatedly adding the lowest-index unscheduled successor of a
+ * batch op whose predecessors are all issued, done or in the batch, up to
+ * batch_cap ops; one candidate per partition, simulated together on the GPU
+ * (ss_simulate_batch, index-order dispatch) over the graph of the done ops,
+ * the issued ops and the batch (in that order; a done op takes its measured
+ * duration); the feasible candidate with the smallest sum of finish times
+ * (ties to the lower partition) is written back and the batch marked issued.
+ * out_ops (HOST, >= batch_cap entries) receives the batch in index order and
+ * *out_n its size (also for SS_ROUND_INFEASIBLE, 0 otherwise); *out_part the
+ * partition (-1 unless issued); *out_status an SS_ROUND_* value.  The call
+ * runs its GPU work on hip_stream and synchronises it before returning.
+ * Errors: SS_ERR_INVALID_ARG, SS_ERR_INVALID_GMG (a measured duration breaks
+ * the loader's bounds), SS_ERR_OOM, SS_ERR_DEVICE.
+ */
+int ss_sched_round(ss_sched *s, int *out_status, int64_t *out_ops, int64_t *out_n, int64_t *out_part,
+                   void *hip_stream);
+
+/* Executor feedback: issued op `op` is done; measured_dur >= 1 replaces its
+ * estimate in later rounds' simulations, 0 keeps the estimate.  Errors:
+ * SS_ERR_INVALID_ARG (op not issued, measured_dur < 0). */
+int ss_sched_complete(ss_sched *s, int64_t op, int64_t measured_dur);
+
+/* Current state (SS_OP_*) and device of every op, HOST arrays of n_ops
+ * entries; either may be NULL.  The device of an unscheduled op is 0. */
+int ss_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place);
+
 /* Message for the calling thread's most recent failed call ("" if none). */
 const char *ss_last_error(void);
 

@@ -1,5 +1,6 @@
 // C ABI entry points: argument checks, error reporting, dispatch to the
 // kernel drivers.  The GMG loader lives in gmg_load.cpp.
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 #include <string>
@@ -192,4 +193,50 @@ extern "C" int ss_kernel_time(int kernel, int64_t *launches, double *total_ms) {
   *launches = n;
   *total_ms = ms;
   return rc;
+}
+
+extern "C" int ss_sched_create(const ss_sched_desc *d, ss_sched **out) {
+  ss_clear_error();
+  if (!out) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: out is NULL");
+  *out = nullptr;
+  if (!d || !d->gmg) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: desc or desc->gmg is NULL");
+  if (d->n_part < 1 || d->n_part > INT32_MAX || !d->part_dev)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: n_part < 1 or part_dev is NULL");
+  if (d->gmg->n_req > 0 && !d->priority) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: priority is NULL");
+  if (d->issue_budget < 1 || d->batch_cap < 1)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: issue_budget and batch_cap must be >= 1");
+  if (d->flags & ~SS_SELECT_REQUIRE_SLA) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: unknown flags");
+  const int64_t N = d->gmg->n_ops, D = d->gmg->n_dev;
+  if (N < 0 || D < 1) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: bad GMG sizes");
+  if (d->n_part > (int64_t(1) << 40) / std::max<int64_t>(N, 1))
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: n_part * n_ops too large");
+  for (int64_t i = 0; i < d->n_part * N; ++i)
+    if (d->part_dev[i] >= D) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: part_dev names a device >= n_dev");
+  return ss_run_sched_create(d, out);
+}
+
+extern "C" void ss_sched_free(ss_sched *s) {
+  if (s) ss_run_sched_free(s);
+}
+
+extern "C" int ss_sched_round(ss_sched *s, int *out_status, int64_t *out_ops, int64_t *out_n, int64_t *out_part,
+                              void *hip_stream) {
+  ss_clear_error();
+  if (!s || !out_status || !out_ops || !out_n || !out_part)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_round: NULL argument");
+  return ss_run_sched_round(s, out_status, out_ops, out_n, out_part, static_cast<hipStream_t>(hip_stream));
+}
+
+extern "C" int ss_sched_complete(ss_sched *s, int64_t op, int64_t measured_dur) {
+  ss_clear_error();
+  if (!s) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_complete: s is NULL");
+  if (measured_dur < 0) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_complete: measured_dur < 0");
+  return ss_run_sched_complete(s, op, measured_dur);
+}
+
+extern "C" int ss_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place) {
+  ss_clear_error();
+  if (!s) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_state: s is NULL");
+  ss_run_sched_state(s, state, place);
+  return SS_OK;
 }

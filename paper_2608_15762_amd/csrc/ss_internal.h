@@ -101,6 +101,13 @@ struct SsTimingRec;
 SsTimingRec *ss_timing_start(int kernel, hipStream_t stream);
 void ss_timing_stop(SsTimingRec *rec, hipStream_t stream);
 
+// Incremental scheduling loop (sched.cpp).  Arguments are already checked.
+int ss_run_sched_create(const ss_sched_desc *d, ss_sched **out);
+void ss_run_sched_free(ss_sched *s);
+int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, int64_t *part, hipStream_t stream);
+int ss_run_sched_complete(ss_sched *s, int64_t op, int64_t measured);
+void ss_run_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place);
+
 // Kernel drivers (simulate.hip / select.hip).  Arguments are already checked.
 int ss_run_simulate(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
                     uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch,

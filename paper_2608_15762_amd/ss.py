@@ -28,7 +28,10 @@ SS_VIOLATION_INVALID = 0x4
 SS_SELECT_REQUIRE_SLA = 0x1
 EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "ss_select_best", "ss_kernel_timing",
             "ss_kernel_time", "ss_last_error", "ss_est_create", "ss_est_free", "ss_est_add", "ss_est_solve",
-            "ss_est_predict")
+            "ss_est_predict", "ss_sched_create", "ss_sched_free", "ss_sched_round", "ss_sched_complete",
+            "ss_sched_state")
+SS_OP_UNSCHEDULED, SS_OP_ISSUED, SS_OP_DONE = 0, 1, 2
+SS_ROUND_ISSUED, SS_ROUND_BUDGET, SS_ROUND_IDLE, SS_ROUND_INFEASIBLE = 0, 1, 2, 3
 SS_KERNEL_SCHEDULE, SS_KERNEL_MEMORY, SS_KERNEL_SELECT, SS_KERNEL_INTERVALS, SS_KERNEL_TRANSPOSE = 0, 1, 2, 3, 4
 SS_KERNEL_ESTIMATOR = 6
 KERNEL_NAMES = {0: "schedule_kernel", 1: "memory_kernel", 2: "select", 3: "intervals_kernel", 4: "transpose",
@@ -87,6 +90,16 @@ def lib():
             L.ss_est_solve.restype = ctypes.c_int
             L.ss_est_predict.argtypes = [P, I64, I64, P, P, I64, P, P]
             L.ss_est_predict.restype = ctypes.c_int
+            L.ss_sched_create.argtypes = [ctypes.POINTER(_SchedDesc), ctypes.POINTER(ctypes.c_void_p)]
+            L.ss_sched_create.restype = ctypes.c_int
+            L.ss_sched_free.argtypes = [P]
+            L.ss_sched_free.restype = None
+            L.ss_sched_round.argtypes = [P, P, P, P, P, P]
+            L.ss_sched_round.restype = ctypes.c_int
+            L.ss_sched_complete.argtypes = [P, I64, I64]
+            L.ss_sched_complete.restype = ctypes.c_int
+            L.ss_sched_state.argtypes = [P, P, P]
+            L.ss_sched_state.restype = ctypes.c_int
             _lib = L
     return _lib
 
@@ -106,23 +119,28 @@ def _stream_ptr(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _gmg_desc(g, keep):
+    """An ss_gmg_desc over contiguous copies of g's arrays (kept alive in `keep`)."""
+
+    def arr(name, dtype):
+        a = np.ascontiguousarray(getattr(g, name), dtype)
+        keep[name] = a
+        return a.ctypes.data
+
+    return _Desc(int(g.n_ops), int(g.pred_ptr[-1]), int(g.n_dev), int(g.n_class), int(g.n_link), int(g.n_req),
+                 arr("pred_ptr", np.int32), arr("pred_idx", np.int32), arr("op_req", np.int32),
+                 arr("dur", np.int64), arr("out_bytes", np.int64), arr("dev_class", np.int32),
+                 arr("link_class", np.uint8), arr("bw", np.int64), arr("lat", np.int64),
+                 arr("slice_ptr", np.int64), arr("slice_begin", np.int64), arr("slice_end", np.int64),
+                 arr("cap", np.int64), arr("release", np.int64), arr("deadline", np.int64))
+
+
 class Gmg:
     """A GMG snapshot staged on the current HIP device (ss_gmg_load)."""
 
     def __init__(self, g):
         keep = {}
-
-        def arr(name, dtype):
-            a = np.ascontiguousarray(getattr(g, name), dtype)
-            keep[name] = a
-            return a.ctypes.data
-
-        d = _Desc(int(g.n_ops), int(g.pred_ptr[-1]), int(g.n_dev), int(g.n_class), int(g.n_link), int(g.n_req),
-                  arr("pred_ptr", np.int32), arr("pred_idx", np.int32), arr("op_req", np.int32),
-                  arr("dur", np.int64), arr("out_bytes", np.int64), arr("dev_class", np.int32),
-                  arr("link_class", np.uint8), arr("bw", np.int64), arr("lat", np.int64),
-                  arr("slice_ptr", np.int64), arr("slice_begin", np.int64), arr("slice_end", np.int64),
-                  arr("cap", np.int64), arr("release", np.int64), arr("deadline", np.int64))
+        d = _gmg_desc(g, keep)
         h = ctypes.c_void_p()
         _check(lib().ss_gmg_load(ctypes.byref(d), ctypes.byref(h)))
         self.handle = h
@@ -136,6 +154,59 @@ class Gmg:
     def free(self):
         if self.handle:
             lib().ss_gmg_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+class _SchedDesc(ctypes.Structure):
+    _fields_ = [("gmg", ctypes.POINTER(_Desc)), ("n_part", ctypes.c_int64), ("part_dev", ctypes.c_void_p),
+                ("priority", ctypes.c_void_p), ("issue_budget", ctypes.c_int64), ("batch_cap", ctypes.c_int64),
+                ("flags", ctypes.c_int)]
+
+
+class Scheduler:
+    """The incremental scheduling loop of Alg. 1 (ss_sched_*) over a run's GMG,
+    its pre-defined partitions part_dev[n_part][n_ops] and request priorities."""
+
+    def __init__(self, g, part_dev, priority, budget, cap, require_sla=False):
+        keep = {}
+        desc = _gmg_desc(g, keep)
+        part = np.ascontiguousarray(part_dev, np.uint8)
+        prio = np.ascontiguousarray(priority, np.int64)
+        assert part.ndim == 2 and part.shape[1] == g.n_ops and prio.shape == (g.n_req,)
+        d = _SchedDesc(ctypes.pointer(desc), part.shape[0], part.ctypes.data, prio.ctypes.data, int(budget),
+                       int(cap), SS_SELECT_REQUIRE_SLA if require_sla else 0)
+        h = ctypes.c_void_p()
+        _check(lib().ss_sched_create(ctypes.byref(d), ctypes.byref(h)))
+        self.handle = h
+        self.n_ops, self.cap = int(g.n_ops), int(cap)
+        self._ops = np.zeros(max(1, int(cap)), np.int64)
+
+    def round(self, stream=None):
+        """(status, batch ops, partition or -1)."""
+        st, n, p = ctypes.c_int(), ctypes.c_int64(), ctypes.c_int64()
+        _check(lib().ss_sched_round(self.handle, ctypes.byref(st), self._ops.ctypes.data, ctypes.byref(n),
+                                    ctypes.byref(p), _stream_ptr(stream)))
+        return st.value, self._ops[:n.value].tolist(), p.value
+
+    def complete(self, op, measured_dur=0):
+        _check(lib().ss_sched_complete(self.handle, int(op), int(measured_dur)))
+
+    def state(self):
+        """(state[n_ops] of SS_OP_*, place[n_ops])."""
+        st = np.zeros(self.n_ops, np.uint8)
+        pl = np.zeros(self.n_ops, np.uint8)
+        _check(lib().ss_sched_state(self.handle, st.ctypes.data, pl.ctypes.data))
+        return st, pl
+
+    def free(self):
+        if self.handle:
+            lib().ss_sched_free(self.handle)
             self.handle = None
 
     def __del__(self):

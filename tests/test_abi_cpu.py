@@ -154,3 +154,25 @@ def test_estimator_arguments_are_checked_before_the_device():
     assert L.ss_est_predict(None, 1, 2, None, None, 3, None, None) == -1
     assert L.ss_est_predict(None, 1, 2, None, None, 0, None, None) == 0  # nothing to do
     L.ss_est_free(None)
+
+
+def test_scheduler_arguments_are_checked_before_the_device():
+    L = ss.lib()
+    h = ctypes.c_void_p()
+    assert L.ss_sched_create(None, ctypes.byref(h)) == -1
+    g = synth.build_gmg(0)
+    keep = {}
+    desc = ss._gmg_desc(g, keep)
+    part = synth.partition_table(g, 0)
+    prio = synth.request_priority(g)
+    for n_part, budget, cap, flags, bad_dev in [(0, 4, 4, 0, False), (3, 0, 4, 0, False), (3, 4, 0, 0, False),
+                                                (3, 4, 4, 2, False), (3, 4, 4, 0, True)]:
+        pd = part.copy()
+        if bad_dev:
+            pd[1, 5] = g.n_dev
+        d = ss._SchedDesc(ctypes.pointer(desc), n_part, pd.ctypes.data, prio.ctypes.data, budget, cap, flags)
+        assert L.ss_sched_create(ctypes.byref(d), ctypes.byref(h)) == -1
+    assert L.ss_sched_round(None, None, None, None, None, None) == -1
+    assert L.ss_sched_complete(None, 0, 0) == -1
+    assert L.ss_sched_state(None, None, None) == -1
+    L.ss_sched_free(None)
