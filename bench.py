@@ -44,8 +44,10 @@ def parse():
                     help="device queues in index order (default) or earliest ready time first")
     ap.add_argument("--links", choices=("latency", "ports"), default="latency",
                     help="transfers take their estimate (default) or contend for device send/receive ports")
-    ap.add_argument("--part", choices=("simulate", "estimator"), default="simulate",
-                    help="the what-if simulator (default) or the online estimators")
+    ap.add_argument("--part", choices=("simulate", "estimator", "sched"), default="simulate",
+                    help="the what-if simulator (default), the online estimators, or the incremental loop")
+    ap.add_argument("--batch-cap", type=int, default=400, help="incremental loop: ops per batch")
+    ap.add_argument("--budget", type=int, default=1600, help="incremental loop: issued-op budget")
     return ap.parse_args()
 
 
@@ -257,10 +259,136 @@ def estimator_main(args):
     print(json.dumps(result), flush=True)
 
 
+def sched_run(S, g, synth, key, record=None, max_rounds=None):
+    """One scheduling run: rounds until every op is issued or done, the executor
+    feeding back completions whenever a round issues nothing.  Returns
+    (rounds, issued rounds)."""
+    rounds = issued_rounds = step = 0
+    while max_rounds is None or rounds < max_rounds:
+        st, batch, p = S.round()
+        rounds += 1
+        if record is not None:
+            record.append((st, tuple(batch), p))
+        if st == 0:
+            issued_rounds += 1
+            continue
+        state, place = S.state()
+        issued = np.nonzero(state == 1)[0]
+        if len(issued) == 0:
+            break
+        for v in synth.completion_feedback(issued, key, step):
+            S.complete(v)
+        step += 1
+    return rounds, issued_rounds
+
+
+def sched_main(args):
+    """The incremental loop of Alg. 1: one step is a whole scheduling run of the
+    workload (every op issued), each round simulating all pre-defined
+    partitions of its batch on the GPU; throughput in rounds per second."""
+    import torch
+
+    from paper_2608_15762_amd import ss, synth
+
+    dev = torch.device("cuda:0")
+    cid = args.workload
+    cfg = synth.CONFIGS[cid]
+    g = synth.build_gmg(cid)
+    part = synth.partition_table(g, cid)
+    prio = synth.request_priority(g)
+    log(f"incremental loop on {cfg.name}: N={g.n_ops} partitions={len(part)} cap={args.batch_cap} "
+        f"budget={args.budget}")
+    copy_gbs = copy_bandwidth(torch, dev)
+    for i in range(args.warmup):
+        S = ss.Scheduler(g, part, prio, args.budget, args.batch_cap)
+        sched_run(S, g, synth, cid)
+        S.free()
+        log(f"warmup run {i + 1}/{args.warmup} done")
+    ss.kernel_timing(True)
+    rounds = issued = 0
+    gpu_rec = []
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        S = ss.Scheduler(g, part, prio, args.budget, args.batch_cap)
+        r, ir = sched_run(S, g, synth, cid, record=gpu_rec if i == 0 else None)
+        S.free()
+        rounds += r
+        issued += ir
+        log(f"timed run {i + 1}/{args.steps} done: {r} rounds ({ir} issuing) in "
+            f"{(time.perf_counter() - t0) / (i + 1) * 1e3:.0f} ms per run")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kernels = {}
+    for k, name in ss.KERNEL_NAMES.items():
+        n, ms = ss.kernel_time(k)
+        kernels[name] = dict(launches=n, total_ms=round(ms, 3), avg_ms=round(ms / max(n, 1), 4))
+    ss.kernel_timing(False)
+    # algorithmic bytes of the simulations: per candidate its placement row of
+    # the round's graph and its outputs (makespan, violation, slack, sumfin)
+    per_run, n_ops_sim = 0, 0
+    dom = max((k for k in kernels if k != "select"), key=lambda k: kernels[k]["total_ms"])
+    D, R = g.n_dev, g.n_req
+    # the round graphs of the first run: done + issued + batch ops at each issuing round
+    n_sched = 0
+    for st, batch, p in gpu_rec:
+        if st == 0:
+            n_sched += len(batch)
+            per_run += len(part) * (n_sched + 8 + 1 + 8 * R + 8)
+            n_ops_sim += len(part) * n_sched
+    alg_bytes = per_run * args.steps
+    achieved = alg_bytes / max(kernels[dom]["launches"], 1) / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
+    result = {
+        "metric": "incremental scheduling rounds/sec (Alg. 1 loop, all partitions simulated per round, 1 GPU)",
+        "value": round(issued / elapsed, 2), "unit": "rounds/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 2), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}-incremental", "n_ops": g.n_ops, "partitions": len(part),
+                   "batch_cap": args.batch_cap, "issue_budget": args.budget, "rounds_per_run": rounds // args.steps,
+                   "issuing_rounds_per_run": issued // args.steps},
+        "simulated_op_evals_per_s": round(n_ops_sim * args.steps / elapsed, 1),
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 4), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 7), "traffic": None,
+                     "bytes_per_launch": round(alg_bytes / max(kernels[dom]["launches"], 1)),
+                     "copy_gbs": round(copy_gbs, 1)},
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        # the oracle loop on the same run, for as many rounds as fit in the CPU
+        # time budget; its rounds must be the GPU's
+        from oracle import sched as osch
+        O = osch.Scheduler(g, part, prio, args.budget, args.batch_cap)
+        rec = []
+        t0 = time.perf_counter()
+        n_issuing = 0
+        step = 0
+        while time.perf_counter() - t0 < args.cpu_seconds:
+            st, batch, p = O.round()
+            rec.append((st, tuple(batch), p))
+            if st == 0:
+                n_issuing += 1
+                continue
+            issued_ops = np.nonzero(O.state == osch.ISSUED)[0]
+            if len(issued_ops) == 0:
+                break
+            for v in synth.completion_feedback(issued_ops, cid, step):
+                O.complete(v)
+            step += 1
+        wall = time.perf_counter() - t0
+        mism = sum(1 for a, b in zip(rec, gpu_rec) if a != b)
+        result["cpu_baseline"] = {"value": round(n_issuing / wall, 3), "unit": "rounds/s", "cores": 1,
+                                  "kind": "oracle",
+                                  "sample": f"the first {len(rec)} rounds ({n_issuing} issuing) of the same run, "
+                                            f"one thread, {wall:.1f} s wall"}
+        result["parity_sample"] = {"checked_rounds": len(rec), "mismatching_rounds": mism}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     if args.part == "estimator" and args.gpus == 1:
         return estimator_main(args)
+    if args.part == "sched" and args.gpus == 1:
+        return sched_main(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the candidate batch shards "
               "across GPUs by contiguous ranges but no multi-GPU run is part of this build.", file=sys.stderr)

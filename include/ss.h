@@ -315,24 +315,25 @@ void ss_sched_free(ss_sched *s);
  * collected by repeatedly adding the lowest-index unscheduled successor of a
  * batch op whose predecessors are all issued, done or in the batch, up to
  * batch_cap ops; one candidate per partition, simulated together on the GPU
- * (ss_simulate_batch, index-order dispatch) over the graph of the done ops,
- * the issued ops and the batch (in that order; a done op takes its measured
- * duration); the feasible candidate with the smallest sum of finish times
- * (ties to the lower partition) is written back and the batch marked issued.
+ * (ss_simulate_batch, index-order dispatch) over the graph of the scheduled
+ * ops in the order they were issued (the device queues' order) followed by
+ * the batch in index order, with the estimated durations; the feasible
+ * candidate with the smallest sum of finish times (ties to the lower
+ * partition) is written back and the batch marked issued.
  * out_ops (HOST, >= batch_cap entries) receives the batch in index order and
  * *out_n its size (also for SS_ROUND_INFEASIBLE, 0 otherwise); *out_part the
  * partition (-1 unless issued); *out_status an SS_ROUND_* value.  The call
  * runs its GPU work on hip_stream and synchronises it before returning.
- * Errors: SS_ERR_INVALID_ARG, SS_ERR_INVALID_GMG (a measured duration breaks
- * the loader's bounds), SS_ERR_OOM, SS_ERR_DEVICE.
+ * Errors: SS_ERR_INVALID_ARG, SS_ERR_OOM, SS_ERR_DEVICE.
  */
 int ss_sched_round(ss_sched *s, int *out_status, int64_t *out_ops, int64_t *out_n, int64_t *out_part,
                    void *hip_stream);
 
-/* Executor feedback: issued op `op` is done; measured_dur >= 1 replaces its
- * estimate in later rounds' simulations, 0 keeps the estimate.  Errors:
- * SS_ERR_INVALID_ARG (op not issued, measured_dur < 0). */
-int ss_sched_complete(ss_sched *s, int64_t op, int64_t measured_dur);
+/* Executor feedback: issued op `op` is done and no longer counts against the
+ * issue budget (its place in the simulated history is unchanged; measured
+ * times refine the estimators, ss_est_*).  Errors: SS_ERR_INVALID_ARG (op not
+ * issued). */
+int ss_sched_complete(ss_sched *s, int64_t op);
 
 /* Current state (SS_OP_*) and device of every op, HOST arrays of n_ops
  * entries; either may be NULL.  The device of an unscheduled op is 0. */

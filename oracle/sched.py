@@ -21,10 +21,14 @@ Readings where the paper is silent (each is listed in the design notes):
   - batch collection: starting from the chosen op, repeatedly add the
     lowest-index unscheduled successor of a batch op whose predecessors are
     all issued, done or already in the batch, until the cap or no such op;
-  - the simulated graph of a round holds the done ops, then the issued ops,
-    then the batch, each group in index order (a topological order in which
-    every candidate shares the placement of all ops before the batch); a done
-    op takes its measured duration when one was fed back;
+  - the simulated graph of a round holds the scheduled (issued or done) ops
+    in the order they were issued (the order of the device queues; a batch in
+    index order), then the batch in index order: a topological order in which
+    every candidate places the ops before the batch alike, and which later
+    rounds only extend;
+  - durations are the estimates: executor feedback marks an op done (it no
+    longer counts against the budget); measured times refine the estimators
+    (Sec. 3.3.1), not the simulated history;
   - candidate b is partition b; the score is the sum of finish times over the
     simulated graph (the ops before the batch are the same for every
     candidate, so the argmin is that of the batch's average completion);
@@ -57,7 +61,7 @@ class Scheduler:
         N = g.n_ops
         self.state = np.full(N, UNSCHEDULED, np.uint8)
         self.place = np.zeros(N, np.uint8)
-        self.measured = np.zeros(N, np.int64)  # 0: no measurement fed back
+        self.issue_order = []  # scheduled ops in the order they were issued
         self.preds = [[int(g.pred_idx[e]) for e in range(g.pred_ptr[v], g.pred_ptr[v + 1])] for v in range(N)]
         self.succs = [[] for _ in range(N)]
         for v in range(N):
@@ -89,11 +93,9 @@ class Scheduler:
 
     # ---------------------------------------------------------------- the round's simulated graph
     def round_graph(self, batch):
-        """(sub-GMG, op order): done ops, issued ops, then the batch."""
+        """(sub-GMG, op order): the scheduled ops in issue order, then the batch."""
         g = self.g
-        done = [v for v in range(g.n_ops) if self.state[v] == DONE]
-        issued = [v for v in range(g.n_ops) if self.state[v] == ISSUED]
-        order = done + issued + list(batch)
+        order = self.issue_order + list(batch)
         new = {v: i for i, v in enumerate(order)}
         pred_ptr = [0]
         pred_idx = []
@@ -101,8 +103,7 @@ class Scheduler:
             ps = sorted(new[u] for u in self.preds[v])
             pred_idx += ps
             pred_ptr.append(len(pred_idx))
-        dur = np.array([g.dur[v] if self.measured[v] == 0 else np.full(g.n_class, self.measured[v]) for v in order],
-                       np.int64).reshape(len(order), g.n_class)
+        dur = np.array([g.dur[v] for v in order], np.int64).reshape(len(order), g.n_class)
         sub = type(g)(len(order), g.n_dev, g.n_class, g.n_link, g.n_req,
                       np.asarray(pred_ptr, np.int32), np.asarray(pred_idx, np.int32),
                       np.asarray([g.op_req[v] for v in order], np.int32), dur,
@@ -131,10 +132,10 @@ class Scheduler:
             return ROUND_INFEASIBLE, batch, -1
         self.state[batch] = ISSUED
         self.place[batch] = self.part[best, batch]
+        self.issue_order += list(batch)
         return ROUND_ISSUED, batch, int(best)
 
-    def complete(self, v, measured_dur: int = 0):
-        """Feedback: issued op v is done (measured duration, 0 = none)."""
+    def complete(self, v):
+        """Feedback: issued op v is done."""
         assert self.state[v] == ISSUED
         self.state[v] = DONE
-        self.measured[v] = int(measured_dur)

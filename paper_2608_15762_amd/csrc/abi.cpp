@@ -227,11 +227,10 @@ extern "C" int ss_sched_round(ss_sched *s, int *out_status, int64_t *out_ops, in
   return ss_run_sched_round(s, out_status, out_ops, out_n, out_part, static_cast<hipStream_t>(hip_stream));
 }
 
-extern "C" int ss_sched_complete(ss_sched *s, int64_t op, int64_t measured_dur) {
+extern "C" int ss_sched_complete(ss_sched *s, int64_t op) {
   ss_clear_error();
   if (!s) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_complete: s is NULL");
-  if (measured_dur < 0) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_complete: measured_dur < 0");
-  return ss_run_sched_complete(s, op, measured_dur);
+  return ss_run_sched_complete(s, op);
 }
 
 extern "C" int ss_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place) {

@@ -4,16 +4,18 @@
 // call on the GPU, selection by ss_select_best, write-back.
 //
 // Host-side state, per op: unscheduled / issued / done, the device chosen for
-// it, a measured duration fed back by the executor, and the number of its
-// predecessors still unscheduled (it is on the unscheduled frontier when that
-// count is zero).  The frontier is kept ordered by (request priority, op), so
-// the highest-priority op is its first element.
+// it, and the number of its predecessors still unscheduled (it is on the
+// unscheduled frontier when that count is zero).  The frontier is kept
+// ordered by (request priority, op), so the highest-priority op is its first
+// element.
 //
-// A round's simulated graph holds the done ops, then the issued ops, then the
-// batch, each group in index order: a topological order in which all
-// candidates place the ops before the batch alike, so under index-order
-// dispatch those ops have the same schedule in every candidate and the
-// candidates' finish-time sums differ by the batch's alone.
+// A round's simulated graph holds the scheduled ops in the order they were
+// issued (the order of the device queues), then the batch in index order: a
+// topological order in which all candidates place the ops before the batch
+// alike, so under index-order dispatch those ops have the same schedule in
+// every candidate and the candidates' finish-time sums differ by the batch's
+// alone.  Later rounds only extend the order.  Durations are the estimates;
+// completion feedback changes an op's state, not the simulated history.
 #include <algorithm>
 #include <new>
 #include <queue>
@@ -33,7 +35,7 @@ struct ss_sched {
   int flags = 0;
   int device = 0;
   std::vector<uint8_t> state, place;
-  std::vector<int64_t> measured;
+  std::vector<int32_t> issue_order;  // scheduled ops in the order they were issued
   std::vector<int32_t> missing;  // unscheduled predecessors
   std::set<std::pair<int64_t, int32_t>> frontier;
   int64_t n_issued = 0;
@@ -134,7 +136,6 @@ int ss_run_sched_create(const ss_sched_desc *d, ss_sched **out) {
     s->flags = d->flags;
     s->state.assign((size_t)s->N, SS_OP_UNSCHEDULED);
     s->place.assign((size_t)s->N, 0);
-    s->measured.assign((size_t)s->N, 0);
     s->missing.assign((size_t)s->N, 0);
     s->succ_ptr.assign((size_t)s->N + 1, 0);
     s->succ_idx.assign((size_t)s->E, 0);
@@ -186,12 +187,9 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
   std::vector<int32_t> order;
   try {
     batch = collect(s, op);
-    order.reserve((size_t)s->N);
-    for (int64_t v = 0; v < s->N; ++v)
-      if (s->state[v] == SS_OP_DONE) order.push_back((int32_t)v);
-    for (int64_t v = 0; v < s->N; ++v)
-      if (s->state[v] == SS_OP_ISSUED) order.push_back((int32_t)v);
+    order = s->issue_order;
     order.insert(order.end(), batch.begin(), batch.end());
+    s->issue_order.reserve(order.size());  // the write-back cannot fail half-way
   } catch (const std::bad_alloc &) {
     return ss_set_error(SS_ERR_OOM, "ss_sched_round: host allocation failed");
   }
@@ -208,7 +206,7 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
     std::sort(sp_idx.begin() + (std::ptrdiff_t)first, sp_idx.end());
     sp_ptr.push_back((int32_t)sp_idx.size());
     sreq[i] = s->op_req[v];
-    for (int64_t c = 0; c < s->C; ++c) sdur[i * s->C + c] = s->measured[v] > 0 ? s->measured[v] : s->dur[v * s->C + c];
+    for (int64_t c = 0; c < s->C; ++c) sdur[i * s->C + c] = s->dur[v * s->C + c];
     sbytes[i] = s->out_bytes[v];
   }
   ss_gmg_desc gd{};
@@ -291,16 +289,16 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
     return SS_OK;
   }
   for (int64_t i = 0; i < nb; ++i) mark_issued(s, batch[i], s->part[best[0] * s->N + batch[i]]);
+  s->issue_order.insert(s->issue_order.end(), batch.begin(), batch.end());
   *part = best[0];
   *status = SS_ROUND_ISSUED;
   return SS_OK;
 }
 
-int ss_run_sched_complete(ss_sched *s, int64_t op, int64_t measured) {
+int ss_run_sched_complete(ss_sched *s, int64_t op) {
   if (op < 0 || op >= s->N || s->state[op] != SS_OP_ISSUED)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_complete: op is not issued");
   s->state[op] = SS_OP_DONE;
-  s->measured[op] = measured;
   --s->n_issued;
   return SS_OK;
 }

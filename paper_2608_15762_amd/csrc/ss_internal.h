@@ -105,7 +105,7 @@ void ss_timing_stop(SsTimingRec *rec, hipStream_t stream);
 int ss_run_sched_create(const ss_sched_desc *d, ss_sched **out);
 void ss_run_sched_free(ss_sched *s);
 int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, int64_t *part, hipStream_t stream);
-int ss_run_sched_complete(ss_sched *s, int64_t op, int64_t measured);
+int ss_run_sched_complete(ss_sched *s, int64_t op);
 void ss_run_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place);
 
 // Kernel drivers (simulate.hip / select.hip).  Arguments are already checked.

@@ -96,7 +96,7 @@ def lib():
             L.ss_sched_free.restype = None
             L.ss_sched_round.argtypes = [P, P, P, P, P, P]
             L.ss_sched_round.restype = ctypes.c_int
-            L.ss_sched_complete.argtypes = [P, I64, I64]
+            L.ss_sched_complete.argtypes = [P, I64]
             L.ss_sched_complete.restype = ctypes.c_int
             L.ss_sched_state.argtypes = [P, P, P]
             L.ss_sched_state.restype = ctypes.c_int
@@ -194,8 +194,8 @@ class Scheduler:
                                     ctypes.byref(p), _stream_ptr(stream)))
         return st.value, self._ops[:n.value].tolist(), p.value
 
-    def complete(self, op, measured_dur=0):
-        _check(lib().ss_sched_complete(self.handle, int(op), int(measured_dur)))
+    def complete(self, op):
+        _check(lib().ss_sched_complete(self.handle, int(op)))
 
     def state(self):
         """(state[n_ops] of SS_OP_*, place[n_ops])."""

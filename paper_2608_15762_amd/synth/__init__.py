@@ -494,19 +494,14 @@ def partition_table(g: Gmg, cid: int) -> np.ndarray:
     return out
 
 
-def completion_feedback(g: Gmg, issued, place, key: int, step: int) -> list:
-    """Executor feedback for a driver of the incremental loop: the lower-index half
-    (at least one) of the issued ops complete, each with a measured duration equal
-    to its estimate on its device scaled by a seeded factor in [0.9, 1.1] (>= 1).
-    Returns [(op, measured duration)]."""
+def completion_feedback(issued, key: int, step: int) -> list:
+    """Executor feedback for a driver of the incremental loop: a seeded random
+    half (at least one) of the issued ops complete.  Returns those ops,
+    ascending."""
     issued = sorted(int(v) for v in issued)
-    done = issued[:max(1, len(issued) // 2)]
     st = Stream(draw(key, 0x5C4ED + step))
-    out = []
-    for v in done:
-        est = int(g.dur[v, g.dev_class[place[v]]])
-        out.append((v, max(1, est * st.uniform_int(900, 1100) // 1000)))
-    return out
+    order = sorted(issued, key=lambda v: (st.next(), v))
+    return sorted(order[:max(1, len(issued) // 2)])
 
 
 def request_priority(g: Gmg) -> np.ndarray:

@@ -173,6 +173,6 @@ def test_scheduler_arguments_are_checked_before_the_device():
         d = ss._SchedDesc(ctypes.pointer(desc), n_part, pd.ctypes.data, prio.ctypes.data, budget, cap, flags)
         assert L.ss_sched_create(ctypes.byref(d), ctypes.byref(h)) == -1
     assert L.ss_sched_round(None, None, None, None, None, None) == -1
-    assert L.ss_sched_complete(None, 0, 0) == -1
+    assert L.ss_sched_complete(None, 0) == -1
     assert L.ss_sched_state(None, None, None) == -1
     L.ss_sched_free(None)

@@ -38,9 +38,9 @@ def drive_both(g, part, prio, budget, cap, key, require_sla=False, max_rounds=10
             issued = np.nonzero(O.state == osch.ISSUED)[0]
             if len(issued) == 0:
                 break
-            for v, m in synth.completion_feedback(g, issued, O.place, key, step):
-                O.complete(v, m)
-                L.complete(v, m)
+            for v in synth.completion_feedback(issued, key, step):
+                O.complete(v)
+                L.complete(v)
             step += 1
         st, pl = L.state()
         assert np.array_equal(st, O.state) and np.array_equal(pl, O.place)
@@ -91,6 +91,7 @@ def test_argument_errors(dev):
         L.complete(0)  # not issued
     st, batch, p = L.round()
     assert st == ss.SS_ROUND_ISSUED
+    L.complete(batch[0])
     with pytest.raises(ss.SSError):
-        L.complete(batch[0], -1)
+        L.complete(batch[0])  # already done
     L.free()

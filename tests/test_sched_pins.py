@@ -57,7 +57,7 @@ def test_budget_and_completion():
     st, batch, _ = S.round()
     assert st == osch.ROUND_ISSUED and batch == [0, 1]
     assert S.round() == (osch.ROUND_BUDGET, [], -1)       # 2 issued >= budget 2
-    S.complete(0, 12)
+    S.complete(0)
     st, batch, _ = S.round()                              # 1 issued < 2: a full batch again
     assert st == osch.ROUND_ISSUED and batch == [2, 3]
     assert int((S.state == osch.ISSUED).sum()) == 3       # budget - 1 + cap at most
@@ -65,22 +65,23 @@ def test_budget_and_completion():
     S.complete(2)
     S.complete(3)
     assert S.round() == (osch.ROUND_IDLE, [], -1)
-    assert S.measured.tolist() == [12, 0, 0, 0]
 
 
-def test_measured_duration_enters_the_simulation():
-    """Op 0 done with a measured 50 us instead of 10: in the next round the
-    simulated graph has op 0 at [0, 50), op 1 at [50, 60) on device 1, and op 2
-    on device 1 at [60, 70) (partition 1) against device 0 at [60, 70) too:
-    a tie in the sum, so the lower partition (0)."""
-    g, part = two_device_chain([(0, INF)], [(0, INF)], 0, 0)
-    S = osch.Scheduler(g, part, [0], budget=10, cap=1)
-    assert S.round() == (osch.ROUND_ISSUED, [0], 0)       # tie -> partition 0
-    S.complete(0, 50)
-    sub, order = S.round_graph([1])
-    assert order == [0, 1] and sub.dur[:, 0].tolist() == [50, 10]
-    fin = oracle.simulate_one(sub, np.array([0, 1], np.uint8))["fin"]
-    assert fin.tolist() == [50, 60]
+def test_round_graph_follows_issue_order():
+    """Two independent requests issued high-priority first: the round graph
+    lists the scheduled ops in issue order (op 1, then op 0), which completion
+    does not change, then the batch."""
+    g = make_gmg(2, ["op"] * 3, [(0, 2)], [0, 1, 0], [[5], [7], [3]], [1, 1, 1], [[(0, INF)]] * 2, [10 ** 6] * 2,
+                 [0, 0], [100, 50], bw=(10,), lat=(0,))
+    part = np.array([[0, 0, 0], [1, 1, 1]], np.uint8)
+    S = osch.Scheduler(g, part, [100, 50], budget=10, cap=1)
+    assert S.round() == (osch.ROUND_ISSUED, [1], 0)
+    assert S.round() == (osch.ROUND_ISSUED, [0], 1)  # device 0 busy with op 1 until 7: device 1 finishes op 0 at 5
+    S.complete(1)
+    sub, order = S.round_graph([2])
+    assert order == [1, 0, 2] and sub.dur[:, 0].tolist() == [7, 5, 3]
+    # op 1 on d0 [0,7), op 0 on d1 [0,5); op 2 after op 0: on d1 [5,8) (sum 20) or d0 [7,10) (sum 22)
+    assert S.round() == (osch.ROUND_ISSUED, [2], 1)
 
 
 def test_infeasible_round_changes_nothing():
@@ -165,8 +166,8 @@ def run_checked(g, part, prio, budget, cap, key, require_sla=False, check_choice
         issued = np.nonzero(S.state == osch.ISSUED)[0]
         if len(issued) == 0:
             break
-        for v, m in synth.completion_feedback(g, issued, S.place, key, step):
-            S.complete(v, m)
+        for v in synth.completion_feedback(issued, key, step):
+            S.complete(v)
         step += 1
     assert (S.state == osch.DONE).sum() + (S.state == osch.ISSUED).sum() == g.n_ops or st == osch.ROUND_INFEASIBLE
     return S, issued_by
@@ -174,12 +175,14 @@ def run_checked(g, part, prio, budget, cap, key, require_sla=False, check_choice
 
 def _graph_before(S, before, batch):
     """The round graph as it was before the write-back of an issued round."""
-    saved = S.state.copy()
+    saved, saved_order = S.state.copy(), list(S.issue_order)
     S.state[:] = before
+    S.issue_order = saved_order[:len(saved_order) - len(batch)]
     try:
         return S.round_graph(batch)
     finally:
         S.state[:] = saved
+        S.issue_order = saved_order
 
 
 @pytest.mark.parametrize("cid,budget,cap", [(0, 8, 5), (1, 64, 40), (2, 600, 150)])
