@@ -182,6 +182,54 @@ int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int64_t B, int
                       void *hip_stream);
 
 /*
+ * Prefix reuse for candidates that share their first ops (the ops before a
+ * batch in Alg. 1's rounds, Sec. 3.4.2).  A state holds one simulated
+ * candidate after the first k ops of a GMG: their finish times, every
+ * device's clock and slice position, every request's completion so far, and
+ * the running makespan and finish-time sum (device memory of the current
+ * device, grown at capture).
+ */
+typedef struct ss_state ss_state;
+
+/* An empty state (k = 0) on the current HIP device.  Errors: SS_ERR_INVALID_ARG,
+ * SS_ERR_OOM, SS_ERR_DEVICE. */
+int ss_state_create(ss_state **out);
+
+/* Release a state (synchronises its device first).  NULL is a no-op. */
+void ss_state_free(ss_state *st);
+
+/* The number of ops the state holds (0 for an empty state or a failed capture). */
+int ss_state_info(const ss_state *st, int64_t *n_ops);
+
+/*
+ * ss_simulate_batch (index-order dispatch, latency-only transfers, row-major
+ * placements) resumed from `from`: the results are those of ss_simulate_batch
+ * on the same arguments when `from` was captured from a simulation of a GMG
+ * whose first k ops (and their predecessors, requests, durations, sizes) are
+ * g's first k ops and whose placement of them is every candidate's (the
+ * caller's contract; the library checks k <= n_ops and the device and request
+ * counts).  Each candidate's schedule is walked from op k only; the memory
+ * pass covers all ops.  from may be NULL or empty (a full simulation).
+ * Placements of the first k ops are still checked against n_dev
+ * (SS_VIOLATION_INVALID).  Asynchronous on hip_stream.  Errors:
+ * SS_ERR_INVALID_ARG, SS_ERR_OOM, SS_ERR_DEVICE, SS_ERR_UNSUPPORTED.
+ */
+int ss_simulate_batch_resume(const ss_gmg *g, const ss_state *from, const uint8_t *placements, int64_t B,
+                             int64_t *out_makespan, int64_t *out_peak_mem, uint8_t *out_violation,
+                             int64_t *out_sla_slack, int64_t *out_sumfin, void *hip_stream);
+
+/*
+ * The schedule of one candidate (placement: DEVICE uint8 [n_ops]), resumed
+ * from `from` as above, its state after all n_ops ops stored in capture
+ * (capture != from; no memory pass, no outputs): the prefix for the next
+ * call on a GMG that extends g with this placement of g's ops.  Asynchronous
+ * on hip_stream (growing the state's buffer synchronises it first).  Errors:
+ * SS_ERR_INVALID_ARG, SS_ERR_OOM, SS_ERR_DEVICE.
+ */
+int ss_state_capture(const ss_gmg *g, const ss_state *from, const uint8_t *placement, ss_state *capture,
+                     void *hip_stream);
+
+/*
  * Best-candidate selection of Alg. 1 / Sec. 3.4.2: discard infeasible
  * candidates (violation != 0, and with SS_SELECT_REQUIRE_SLA also any
  * negative slack), then take the smallest key, ties to the lowest index.

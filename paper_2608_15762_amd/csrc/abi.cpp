@@ -3,6 +3,7 @@
 #include <algorithm>
 #include <atomic>
 #include <mutex>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -238,4 +239,77 @@ extern "C" int ss_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place)
   if (!s) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_state: s is NULL");
   ss_run_sched_state(s, state, place);
   return SS_OK;
+}
+
+extern "C" int ss_state_create(ss_state **out) {
+  ss_clear_error();
+  if (!out) return ss_set_error(SS_ERR_INVALID_ARG, "ss_state_create: out is NULL");
+  *out = nullptr;
+  ss_state *st = new (std::nothrow) ss_state();
+  if (!st) return ss_set_error(SS_ERR_OOM, "ss_state_create: host allocation failed");
+  if (hipGetDevice(&st->device) != hipSuccess) {
+    delete st;
+    return ss_set_error(SS_ERR_DEVICE, "hipGetDevice failed");
+  }
+  *out = st;
+  return SS_OK;
+}
+
+extern "C" void ss_state_free(ss_state *st) {
+  if (!st) return;
+  if (st->mem) {
+    int prev = 0;
+    (void)hipGetDevice(&prev);
+    (void)hipSetDevice(st->device);
+    (void)hipDeviceSynchronize();
+    (void)hipFree(st->mem);
+    (void)hipSetDevice(prev);
+  }
+  delete st;
+}
+
+extern "C" int ss_state_info(const ss_state *st, int64_t *n_ops) {
+  ss_clear_error();
+  if (!st) return ss_set_error(SS_ERR_INVALID_ARG, "ss_state_info: st is NULL");
+  if (n_ops) *n_ops = st->k;
+  return SS_OK;
+}
+
+namespace {
+bool state_fits(const ss_state *from, const ss_gmg *g) {
+  return !from || from->k == 0 ||
+         (from->k <= g->n_ops && from->d == g->n_dev && from->r == g->n_req && from->device == g->device);
+}
+}  // namespace
+
+extern "C" int ss_simulate_batch_resume(const ss_gmg *g, const ss_state *from, const uint8_t *placements, int64_t B,
+                                        int64_t *out_makespan, int64_t *out_peak_mem, uint8_t *out_violation,
+                                        int64_t *out_sla_slack, int64_t *out_sumfin, void *hip_stream) {
+  ss_clear_error();
+  if (!g) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch_resume: g is NULL");
+  if (B < 0) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch_resume: B < 0");
+  if (!state_fits(from, g))
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch_resume: the state does not fit this GMG");
+  if (B == 0) return SS_OK;
+  if (!out_makespan || !out_violation)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch_resume: out_makespan and out_violation are required");
+  if (!placements && g->n_ops > 0)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch_resume: placements is NULL");
+  const int rc = check_device(g);
+  if (rc != SS_OK) return rc;
+  return ss_run_simulate_resume(g, from, placements, B, out_makespan, out_peak_mem, out_violation, out_sla_slack,
+                                out_sumfin, static_cast<hipStream_t>(hip_stream));
+}
+
+extern "C" int ss_state_capture(const ss_gmg *g, const ss_state *from, const uint8_t *placement, ss_state *capture,
+                                void *hip_stream) {
+  ss_clear_error();
+  if (!g || !capture) return ss_set_error(SS_ERR_INVALID_ARG, "ss_state_capture: g or capture is NULL");
+  if (!state_fits(from, g)) return ss_set_error(SS_ERR_INVALID_ARG, "ss_state_capture: the state does not fit this GMG");
+  if (capture == from || capture->device != g->device)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_state_capture: capture must be its own state on g's device");
+  if (!placement && g->n_ops > 0) return ss_set_error(SS_ERR_INVALID_ARG, "ss_state_capture: placement is NULL");
+  const int rc = check_device(g);
+  if (rc != SS_OK) return rc;
+  return ss_run_state_capture(g, from, placement, capture, static_cast<hipStream_t>(hip_stream));
 }

@@ -42,6 +42,9 @@ struct ss_sched {
   // reused device buffers: candidate rows and per-candidate outputs
   void *dev_buf = nullptr;
   size_t dev_bytes = 0;
+  // the chosen candidate's simulation state after the scheduled ops (the
+  // prefix of the next round), and a second state to capture the next one in
+  ss_state *prefix = nullptr, *next = nullptr;
 };
 
 namespace {
@@ -157,6 +160,13 @@ int ss_run_sched_create(const ss_sched_desc *d, ss_sched **out) {
     delete s;
     return ss_set_error(SS_ERR_DEVICE, "hipGetDevice failed");
   }
+  rc = ss_state_create(&s->prefix);
+  if (rc == SS_OK) rc = ss_state_create(&s->next);
+  if (rc != SS_OK) {
+    ss_state_free(s->prefix);
+    delete s;
+    return rc;
+  }
   *out = s;
   return SS_OK;
 }
@@ -168,6 +178,8 @@ void ss_run_sched_free(ss_sched *s) {
   (void)hipDeviceSynchronize();
   if (s->dev_buf) (void)hipFree(s->dev_buf);
   (void)hipSetDevice(prev);
+  ss_state_free(s->prefix);
+  ss_state_free(s->next);
   delete s;
 }
 
@@ -272,11 +284,22 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
   int64_t best[2] = {-1, 0};
   err = hipMemcpyAsync(d_rows, rows.data(), (size_t)(P * Ns), hipMemcpyHostToDevice, stream);
   if (err == hipSuccess) {
-    rc = ss_simulate_batch(g, d_rows, P, SS_LAYOUT_ROW_MAJOR, d_ms, nullptr, d_vi, d_sl, d_sum, stream);
+    // every candidate resumes after the scheduled ops (the prefix state holds
+    // them when the previous issuing round captured; else all ops are walked)
+    int64_t k = 0;
+    (void)ss_state_info(s->prefix, &k);
+    const ss_state *from = k == npre ? s->prefix : nullptr;
+    rc = ss_simulate_batch_resume(g, from, d_rows, P, d_ms, nullptr, d_vi, d_sl, d_sum, stream);
     if (rc == SS_OK)
       rc = ss_select_best(g, d_vi, d_sum, d_sl, P, s->flags & SS_SELECT_REQUIRE_SLA, d_best, stream);
     if (rc == SS_OK) err = hipMemcpyAsync(best, d_best, sizeof(best), hipMemcpyDeviceToHost, stream);
     if (rc == SS_OK && err == hipSuccess) err = hipStreamSynchronize(stream);
+    if (rc == SS_OK && err == hipSuccess && best[0] >= 0) {
+      // the chosen candidate's schedule once more, captured for the next round
+      rc = ss_state_capture(g, from, d_rows + best[0] * Ns, s->next, stream);
+      if (rc == SS_OK) err = hipStreamSynchronize(stream);
+      if (rc == SS_OK && err == hipSuccess) std::swap(s->prefix, s->next);
+    }
   }
   ss_gmg_free(g);
   if (rc != SS_OK) return rc;

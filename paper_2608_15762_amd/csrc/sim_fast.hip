@@ -1828,3 +1828,91 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
   return rc;
 }
+
+// The memory passes of the 32-bit path (fast_intervals, fast_peaks) for
+// schedules computed elsewhere: candidate rows of placements P[B][N] and int64
+// finish times fin[B][N] (every time below 2^32, which the loader proved when
+// it enabled the 32-bit path).  Candidates already marked invalid are skipped.
+namespace {
+__global__ __launch_bounds__(256) void narrow_times(const int64_t *__restrict__ in, int64_t n, uint32_t *__restrict__ out) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    out[i] = (uint32_t)in[i];
+}
+}  // namespace
+
+int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, int64_t B, int64_t *peak,
+                       uint8_t *violation, hipStream_t stream) {
+  const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev;
+  if (!g->view.time32 || N == 0) return ss_set_error(SS_ERR_UNSUPPORTED, "the 32-bit memory passes need ops and a 32-bit horizon");
+  if (B == 0) return SS_OK;
+  int cus = 0;
+  hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, g->device);
+  if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
+  const bool iv_fast = g->n_class == 1 && g->n_link <= 2 && g->max_outdeg <= 2;
+  const int64_t rec_per_cand = (own_stride(N) + cp_stride(E)) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4 + N * 2;
+  const int64_t sub = std::min<int64_t>(B, std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand)));
+  const int64_t chunk = std::min<int64_t>(B, std::max<int64_t>(1, kScratchBudget / (N * 4)));
+  const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
+  const int64_t slot_cap = N + E + 1;
+  auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
+  const size_t sz_fin = align((size_t)chunk * N * 4 + 4);
+  const size_t sz_own = align((size_t)sub * own_stride(N) * sizeof(Rec));
+  const size_t sz_cp = align((size_t)sub * cp_stride(E) * sizeof(Rec));
+  const size_t sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
+  const size_t sz_rank = align(((size_t)sub * N + 1) * 2);
+  const size_t sz_wk = align((size_t)nslots * 2 * (slot_cap + 2) * 4);
+  const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
+  const int64_t n_chunk = (B + chunk - 1) / chunk;
+  const int64_t n_ticket = n_chunk * ((chunk + sub - 1) / sub);
+  const size_t sz_tk = align((size_t)n_ticket * 4);
+  void *scratch = nullptr;
+  err = hipMallocFromPoolAsync(&scratch, sz_fin + 2 * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
+                               g->pool, stream);
+  if (err != hipSuccess) return hip_fail(err, "allocating the memory-pass scratch");
+  unsigned char *p = static_cast<unsigned char *>(scratch);
+  auto take = [&](size_t bytes) {
+    unsigned char *q = p;
+    p += bytes;
+    return q;
+  };
+  auto *fin = reinterpret_cast<uint32_t *>(take(sz_fin));
+  MemPass M{};
+  for (int k = 0; k < 2; ++k) {
+    M.own[k] = reinterpret_cast<Rec *>(take(sz_own));
+    M.cp[k] = reinterpret_cast<Rec *>(take(sz_cp));
+    M.meta[k] = reinterpret_cast<int32_t *>(take(sz_meta));
+  }
+  M.rank = reinterpret_cast<uint16_t *>(take(sz_rank));
+  M.wk = reinterpret_cast<uint32_t *>(take(sz_wk));
+  M.wb = reinterpret_cast<int64_t *>(take(sz_wb));
+  M.ticket = reinterpret_cast<uint32_t *>(take(sz_tk));
+  M.n_ticket = n_ticket;
+  M.sub = sub;
+  M.nslots = nslots;
+  M.slot_cap = slot_cap;
+  M.iv_fast = iv_fast;
+  M.aux = g->aux;
+  int rc = mem_pass_events(M);
+  if (rc == SS_OK) {
+    hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)std::min<int64_t>((n_ticket + 255) / 256, 1024)), dim3(256), 0,
+                       stream, M.ticket, n_ticket);
+    const hipError_t fe = hipGetLastError();
+    if (fe != hipSuccess) rc = hip_fail(fe, "fill_zero_u32 launch");
+  }
+  for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
+    const int64_t nb = std::min(chunk, B - b0);
+    hipLaunchKernelGGL(narrow_times, dim3((unsigned)std::min<int64_t>((nb * N + 255) / 256, 8192)), dim3(256), 0,
+                       stream, fin64 + b0 * N, nb * N, fin);
+    err = hipGetLastError();
+    if (err != hipSuccess) {
+      rc = hip_fail(err, "narrow_times launch");
+      break;
+    }
+    rc = memory_passes(g, M, P + b0 * N, fin, nb, false, peak ? peak + b0 * D : nullptr, violation + b0, stream);
+  }
+  const int jrc = mem_pass_join(M, stream);
+  if (rc == SS_OK) rc = jrc;
+  err = hipFreeAsync(scratch, stream);
+  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
+  return rc;
+}

@@ -25,6 +25,7 @@
 //   and takes the maximum prefix sum of the byte deltas: the device's peak.
 //   A device with more endpoints than fit in LDS uses the same code on a
 //   per-workgroup global buffer.
+#include <algorithm>
 #include <climits>
 #include <cstdlib>
 #include <cstring>
@@ -83,11 +84,52 @@ __device__ __forceinline__ void reserve_transfers(const GmgView &G, const uint8_
   }
 }
 
+// Resumption from a captured state (ss_simulate_batch_resume): every
+// candidate places its first k0 ops as the captured run did, so a lane starts
+// at op k0 with the captured device clocks, slice cursors, request
+// completions, makespan and finish-time sum; the finish times of ops < k0 are
+// already in its row (fill_prefix).  With cap_* set (one candidate) the lane
+// stores its state after its last op.
+struct Resume {
+  int32_t k0 = 0;
+  const int64_t *clk = nullptr, *comp = nullptr, *scal = nullptr;  // [D], [R], {makespan, sum}
+  const int32_t *cur = nullptr;                                    // [D]
+  const uint32_t *bad = nullptr;  // [nb]: nonzero when the candidate's first k0 ops name a device >= D
+  int64_t *cap_clk = nullptr, *cap_scal = nullptr;
+  int32_t *cap_cur = nullptr;
+};
+
+__global__ __launch_bounds__(256) void zero_u32(uint32_t *__restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = 0;
+}
+
+// Flags the candidates whose first k0 placements name a device >= D (rows
+// read with consecutive threads on consecutive bytes).
+__global__ __launch_bounds__(256) void prefix_check(const uint8_t *__restrict__ P, int64_t nb, int64_t N, int64_t k0,
+                                                    int D, uint32_t *__restrict__ bad) {
+  const int64_t total = nb * k0;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t c = i / k0, v = i - c * k0;
+    if (P[c * N + v] >= D) atomicOr(&bad[c], 1u);
+  }
+}
+
+// Copies the captured finish times of ops [0, k0) into every candidate's row.
+__global__ __launch_bounds__(256) void fill_prefix(int64_t *__restrict__ fin, int64_t nb, int64_t N, int64_t k0,
+                                                   const int64_t *__restrict__ pre) {
+  const int64_t total = nb * k0;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t c = i / k0, v = i - c * k0;
+    fin[c * N + v] = pre[v];
+  }
+}
+
 template <bool kPorts>
 __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const uint8_t *__restrict__ P,
                                                          int64_t nb, int64_t *__restrict__ fin,
                                                          int64_t *__restrict__ comp, int64_t *__restrict__ port,
-                                                         int64_t *__restrict__ arr, int64_t *__restrict__ makespan,
+                                                         int64_t *__restrict__ arr, const Resume RS,
+                                                         int64_t *__restrict__ makespan,
                                                          int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
                                                          uint8_t *__restrict__ violation) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
@@ -99,17 +141,19 @@ __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const 
   if (c >= nb) return;
   const uint8_t *prow = P + c * N;
   int64_t *frow = fin + c * N;
+  const bool from = RS.clk != nullptr;
   for (int d = 0; d < D; ++d) {
-    clk[d * kWave + lane] = 0;
-    cur[d * kWave + lane] = 0;
+    clk[d * kWave + lane] = from ? RS.clk[d] : 0;
+    cur[d * kWave + lane] = from ? (uint16_t)RS.cur[d] : 0;
   }
-  for (int r = 0; r < R; ++r) comp[(int64_t)r * nb + c] = G.release[r];
+  for (int r = 0; r < R; ++r) comp[(int64_t)r * nb + c] = from ? RS.comp[r] : G.release[r];
   if (kPorts)
     for (int d = 0; d < 2 * D; ++d) port[(int64_t)d * nb + c] = 0;
 
   bool invalid = false;
-  int64_t ms = 0, sum = 0;
-  for (int v = 0; v < N; ++v) {
+  int64_t ms = from ? RS.scal[0] : 0, sum = from ? RS.scal[1] : 0;
+  if (RS.bad) invalid = RS.bad[c] != 0;  // the prefix is not walked, but must name devices
+  for (int v = RS.k0; v < N; ++v) {
     int d = prow[v];
     if (d >= D) {  // not a device of the set: finish the walk on device 0, report sentinels
       invalid = true;
@@ -150,6 +194,14 @@ __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const 
     sum += f;
     int64_t *cr = comp + (int64_t)r * nb + c;
     *cr = imax(*cr, f);
+  }
+  if (RS.cap_clk) {  // one candidate: its state after its last op
+    for (int d = 0; d < D; ++d) {
+      RS.cap_clk[d] = clk[d * kWave + lane];
+      RS.cap_cur[d] = cur[d * kWave + lane];
+    }
+    RS.cap_scal[0] = ms;
+    RS.cap_scal[1] = sum;
   }
   if (invalid) {
     makespan[c] = INT64_MAX;
@@ -627,9 +679,13 @@ int hip_fail(hipError_t err, const char *what) {
 }  // namespace
 
 // General path: int64 times, any size the loader accepts; either dispatch rule.
+// from: resume every candidate after the state's ops; capture (B == 1): store
+// the candidate's state after its last op and skip the memory pass; mem_fast:
+// the 32-bit memory passes instead of memory_kernel.
 static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
                                 uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream,
-                                bool ready, bool ports) {
+                                bool ready, bool ports, const ss_state *from = nullptr,
+                                ss_state *capture = nullptr, bool mem_fast = false) {
   const GmgView &G = g->view;
   const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req;
   const int64_t slot_cap = 2 * (N + E) + 2;
@@ -673,9 +729,12 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
   const size_t sz_ev = align((size_t)nslots * slot_cap * 8);
   const size_t sz_port = ports ? align((size_t)2 * D * chunk * 8) : 0;
   const size_t sz_arr = ports ? align((size_t)E * chunk * 8 + 8) : 0;
+  const bool resumed = from && from->k > 0;
+  const size_t sz_bad = resumed ? align((size_t)chunk * 4) : 0;
   void *scratch = nullptr;
   err = hipMallocFromPoolAsync(&scratch,
-                               sz_fin + sz_comp + sz_miss + sz_spr + sz_spo + sz_bydev + 2 * sz_ev + sz_port + sz_arr,
+                               sz_fin + sz_comp + sz_miss + sz_spr + sz_spo + sz_bydev + 2 * sz_ev + sz_port + sz_arr +
+                                   sz_bad,
                                g->pool, stream);
   if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
@@ -694,6 +753,20 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
   auto *gvals = reinterpret_cast<int64_t *>(take(sz_ev));
   auto *port = ports ? reinterpret_cast<int64_t *>(take(sz_port)) : nullptr;
   auto *arr = ports ? reinterpret_cast<int64_t *>(take(sz_arr)) : nullptr;
+  auto *bad = resumed ? reinterpret_cast<uint32_t *>(take(sz_bad)) : nullptr;
+  Resume RS;
+  if (resumed) {
+    RS.k0 = (int32_t)from->k;
+    RS.clk = from->clk;
+    RS.cur = from->cur;
+    RS.comp = from->comp;
+    RS.scal = from->scal;
+  }
+  if (capture) {
+    RS.cap_clk = capture->clk;
+    RS.cap_cur = capture->cur;
+    RS.cap_scal = capture->scal;
+  }
 
   int rc = SS_OK;
   for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
@@ -704,16 +777,40 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
       hipLaunchKernelGGL(ready_schedule_general, dim3((unsigned)nb), dim3(kWave), sched_lds, stream, G, Pc, fin, miss,
                          spr, spo, comp, makespan + b0, sumfin ? sumfin + b0 : nullptr,
                          slack ? slack + b0 * R : nullptr, violation + b0);
-    else
+    else {
+      if (RS.k0 > 0) {
+        const unsigned grid = (unsigned)std::min<int64_t>((nb * RS.k0 + 255) / 256, 4096);
+        hipLaunchKernelGGL(fill_prefix, dim3(grid), dim3(256), 0, stream, fin, nb, N, (int64_t)RS.k0,
+                           static_cast<const int64_t *>(from->fin));
+        hipLaunchKernelGGL(zero_u32, dim3((unsigned)std::min<int64_t>((nb + 255) / 256, 1024)), dim3(256), 0, stream,
+                           bad, nb);
+        hipLaunchKernelGGL(prefix_check, dim3(grid), dim3(256), 0, stream, Pc, nb, N, (int64_t)RS.k0, (int)D, bad);
+        RS.bad = bad;
+      }
       hipLaunchKernelGGL(ports ? schedule_kernel<true> : schedule_kernel<false>,
                          dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), sched_lds, stream, G, Pc, nb, fin,
-                         comp, port, arr, makespan + b0, sumfin ? sumfin + b0 : nullptr,
+                         comp, port, arr, RS, makespan + b0, sumfin ? sumfin + b0 : nullptr,
                          slack ? slack + b0 * R : nullptr, violation + b0);
+      if (capture) {  // one candidate: its finish times and request completions
+        err = hipMemcpyAsync(capture->fin, fin, (size_t)N * 8, hipMemcpyDeviceToDevice, stream);
+        if (err == hipSuccess)
+          err = hipMemcpyAsync(capture->comp, comp, (size_t)R * 8, hipMemcpyDeviceToDevice, stream);
+        if (err != hipSuccess) {
+          rc = hip_fail(err, "capturing the simulation state");
+          break;
+        }
+      }
+    }
     err = hipGetLastError();
     ss_timing_stop(t_sched, stream);
     if (err != hipSuccess) {
       rc = hip_fail(err, "schedule launch");
       break;
+    }
+    if (capture) continue;  // the state is all a capture needs
+    if (mem_fast) {
+      rc = ss_run_memory_fast(g, Pc, fin, nb, peak ? peak + b0 * D : nullptr, violation + b0, stream);
+      continue;
     }
     const int64_t grid = std::min<int64_t>(nb, nslots);
     SsTimingRec *t_mem = ss_timing_start(SS_KERNEL_MEMORY, stream);
@@ -750,4 +847,64 @@ int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makes
     return run_simulate_generic(g, P, B, makespan, peak, violation, slack, sumfin, stream, ready_dispatch, link_ports);
   if (ready_dispatch) return ss_run_simulate_ready(g, P, B, makespan, peak, violation, slack, sumfin, stream);
   return ss_run_simulate_fast(g, P, B, makespan, peak, violation, slack, sumfin, stream);
+}
+
+// The state's buffer grows to hold a capture of g (synchronising the stream
+// before the old buffer is released).
+static int state_reserve(ss_state *st, const ss_gmg *g, hipStream_t stream) {
+  const int64_t n = g->n_ops, d = g->n_dev, r = g->n_req;
+  if (st->mem && n <= st->cap_n && d <= st->cap_d && r <= st->cap_r) return SS_OK;
+  const int64_t cn = std::max<int64_t>(n, 2 * st->cap_n), cd = std::max<int64_t>(d, st->cap_d),
+                cr = std::max<int64_t>(r, st->cap_r);
+  const size_t bytes = (size_t)(cn + cd + cr + 2) * 8 + (size_t)cd * 4 + 16;
+  hipError_t err = hipSuccess;
+  if (st->mem) {
+    err = hipStreamSynchronize(stream);
+    if (err == hipSuccess) err = hipFree(st->mem);
+    st->mem = nullptr;
+    if (err != hipSuccess) return hip_fail(err, "releasing a state buffer");
+  }
+  err = hipMalloc(&st->mem, bytes);
+  if (err != hipSuccess) {
+    st->mem = nullptr;
+    st->cap_n = st->cap_d = st->cap_r = 0;
+    st->k = 0;
+    return hip_fail(err, "allocating a state buffer");
+  }
+  auto *p = static_cast<int64_t *>(st->mem);
+  st->fin = p;
+  st->clk = p + cn;
+  st->comp = st->clk + cd;
+  st->scal = st->comp + cr;
+  st->cur = reinterpret_cast<int32_t *>(st->scal + 2);
+  st->cap_n = cn;
+  st->cap_d = cd;
+  st->cap_r = cr;
+  st->k = 0;
+  return SS_OK;
+}
+
+int ss_run_simulate_resume(const ss_gmg *g, const ss_state *from, const uint8_t *P, int64_t B, int64_t *makespan,
+                           int64_t *peak, uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream) {
+  return run_simulate_generic(g, P, B, makespan, peak, violation, slack, sumfin, stream, false, false, from, nullptr,
+                              g->view.time32 && g->n_ops > 0);
+}
+
+int ss_run_state_capture(const ss_gmg *g, const ss_state *from, const uint8_t *placement, ss_state *capture,
+                         hipStream_t stream) {
+  int rc = state_reserve(capture, g, stream);
+  if (rc != SS_OK) return rc;
+  // the schedule kernel's per-candidate outputs, unused here
+  void *outs = nullptr;
+  hipError_t err = hipMallocFromPoolAsync(&outs, 256 + (size_t)g->n_req * 8 + 8, g->pool, stream);
+  if (err != hipSuccess) return hip_fail(err, "allocating capture outputs");
+  auto *o = static_cast<int64_t *>(outs);
+  rc = run_simulate_generic(g, placement, 1, o, nullptr, reinterpret_cast<uint8_t *>(o + 2), o + 4, o + 1, stream,
+                            false, false, from, capture);
+  err = hipFreeAsync(outs, stream);
+  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
+  capture->k = rc == SS_OK ? g->n_ops : 0;
+  capture->d = g->n_dev;
+  capture->r = g->n_req;
+  return rc;
 }

@@ -91,6 +91,18 @@ struct ss_gmg {
   GmgView view{};
 };
 
+// A captured simulation state (ss_simulate_batch_resume): one candidate after
+// its first k ops of a GMG with d devices and r requests.  One device
+// allocation: fin[cap_n] | clk[cap_d] | comp[cap_r] | scal[2] | cur[cap_d].
+struct ss_state {
+  int device = 0;
+  int64_t k = 0, d = 0, r = 0;
+  int64_t cap_n = 0, cap_d = 0, cap_r = 0;
+  void *mem = nullptr;
+  int64_t *fin = nullptr, *clk = nullptr, *comp = nullptr, *scal = nullptr;
+  int32_t *cur = nullptr;
+};
+
 // Record an error message for ss_last_error() and return the code.
 int ss_set_error(int code, const std::string &msg);
 void ss_clear_error();
@@ -112,6 +124,17 @@ void ss_run_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place);
 int ss_run_simulate(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
                     uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch,
                     bool link_ports);
+// Resumption from a captured state (general schedule kernel; the 32-bit
+// memory passes when the GMG has a 32-bit horizon); from may be null or empty.
+int ss_run_simulate_resume(const ss_gmg *g, const ss_state *from, const uint8_t *placements, int64_t B,
+                           int64_t *makespan, int64_t *peak, uint8_t *violation, int64_t *slack, int64_t *sumfin,
+                           hipStream_t stream);
+// The schedule of one candidate (resumed from `from`), its state stored in capture.
+int ss_run_state_capture(const ss_gmg *g, const ss_state *from, const uint8_t *placement, ss_state *capture,
+                         hipStream_t stream);
+// Memory passes of the 32-bit path over int64 finish rows (sim_fast.hip).
+int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, int64_t B, int64_t *peak,
+                       uint8_t *violation, hipStream_t stream);
 // Fast path (sim_fast.hip): 32-bit times, N <= 65535.
 size_t ss_fast_schedule_lds(const ss_gmg *g);
 int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,

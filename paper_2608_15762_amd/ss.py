@@ -29,7 +29,8 @@ SS_SELECT_REQUIRE_SLA = 0x1
 EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "ss_select_best", "ss_kernel_timing",
             "ss_kernel_time", "ss_last_error", "ss_est_create", "ss_est_free", "ss_est_add", "ss_est_solve",
             "ss_est_predict", "ss_sched_create", "ss_sched_free", "ss_sched_round", "ss_sched_complete",
-            "ss_sched_state")
+            "ss_sched_state", "ss_state_create", "ss_state_free", "ss_state_info", "ss_simulate_batch_resume",
+            "ss_state_capture")
 SS_OP_UNSCHEDULED, SS_OP_ISSUED, SS_OP_DONE = 0, 1, 2
 SS_ROUND_ISSUED, SS_ROUND_BUDGET, SS_ROUND_IDLE, SS_ROUND_INFEASIBLE = 0, 1, 2, 3
 SS_KERNEL_SCHEDULE, SS_KERNEL_MEMORY, SS_KERNEL_SELECT, SS_KERNEL_INTERVALS, SS_KERNEL_TRANSPOSE = 0, 1, 2, 3, 4
@@ -100,6 +101,16 @@ def lib():
             L.ss_sched_complete.restype = ctypes.c_int
             L.ss_sched_state.argtypes = [P, P, P]
             L.ss_sched_state.restype = ctypes.c_int
+            L.ss_state_create.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+            L.ss_state_create.restype = ctypes.c_int
+            L.ss_state_free.argtypes = [P]
+            L.ss_state_free.restype = None
+            L.ss_state_info.argtypes = [P, P]
+            L.ss_state_info.restype = ctypes.c_int
+            L.ss_simulate_batch_resume.argtypes = [P, P, P, I64, P, P, P, P, P, P]
+            L.ss_simulate_batch_resume.restype = ctypes.c_int
+            L.ss_state_capture.argtypes = [P, P, P, P, P]
+            L.ss_state_capture.restype = ctypes.c_int
             _lib = L
     return _lib
 
@@ -246,6 +257,59 @@ def simulate_batch(g: Gmg, placements, want_peak=True, want_slack=True, want_sum
                sumfin=torch.empty(B, dtype=torch.int64, device=dev) if want_sumfin else None)
     simulate_batch_into(g, placements, out["makespan"], out["violation"], out["peak"], out["slack"], out["sumfin"],
                         stream, dispatch, links)
+    return out
+
+
+class State:
+    """A captured simulation state (ss_state_*): one candidate after the first
+    ops of a GMG, for resuming candidates that share those ops."""
+
+    def __init__(self):
+        h = ctypes.c_void_p()
+        _check(lib().ss_state_create(ctypes.byref(h)))
+        self.handle = h
+
+    def n_ops(self):
+        k = ctypes.c_int64()
+        _check(lib().ss_state_info(self.handle, ctypes.byref(k)))
+        return k.value
+
+    def free(self):
+        if self.handle:
+            lib().ss_state_free(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def state_capture(g: Gmg, placement, capture, start=None, stream=None):
+    """ss_state_capture: the schedule of one placement (device uint8 [n_ops]),
+    resumed from State `start`, its state stored in State `capture`."""
+    assert placement.is_contiguous() and placement.numel() == g.n_ops
+    _check(lib().ss_state_capture(g.handle, None if start is None else start.handle, _ptr(placement),
+                                  capture.handle, _stream_ptr(stream)))
+
+
+def simulate_batch_resume(g: Gmg, placements, start=None, want_peak=True, want_slack=True, want_sumfin=True,
+                          stream=None) -> dict:
+    """ss_simulate_batch_resume: candidates resumed from State `start` (None:
+    from op 0)."""
+    import torch
+    B = placements.shape[0]
+    assert placements.dtype == torch.uint8 and placements.is_contiguous() and placements.shape == (B, g.n_ops)
+    dev = placements.device
+    out = dict(makespan=torch.empty(B, dtype=torch.int64, device=dev),
+               violation=torch.empty(B, dtype=torch.uint8, device=dev),
+               peak=torch.empty((B, g.n_dev), dtype=torch.int64, device=dev) if want_peak else None,
+               slack=torch.empty((B, g.n_req), dtype=torch.int64, device=dev) if want_slack else None,
+               sumfin=torch.empty(B, dtype=torch.int64, device=dev) if want_sumfin else None)
+    _check(lib().ss_simulate_batch_resume(g.handle, None if start is None else start.handle, _ptr(placements), B,
+                                          _ptr(out["makespan"]), _ptr(out["peak"]), _ptr(out["violation"]),
+                                          _ptr(out["slack"]), _ptr(out["sumfin"]), _stream_ptr(stream)))
     return out
 
 
