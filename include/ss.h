@@ -107,8 +107,8 @@ typedef struct ss_gmg_desc {
  */
 int ss_gmg_load(const ss_gmg_desc *desc, ss_gmg **out);
 
-/* Release a GMG and its scratch pool (synchronises the device first).  NULL
- * is a no-op. */
+/* Release a GMG (synchronises the device first; its memory goes back to the
+ * library's pool, see ss_release_cached_memory).  NULL is a no-op. */
 void ss_gmg_free(ss_gmg *g);
 
 /* Sizes of a loaded GMG; any output pointer may be NULL. */
@@ -170,10 +170,10 @@ int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req)
  * The call is asynchronous on hip_stream (NULL = the null stream); inputs must
  * stay valid and outputs are defined once that stream has been synchronised.
  * It takes stream-ordered scratch on hip_stream, for the duration of the
- * work, from a memory pool that g owns; the pool keeps that memory for later
- * calls instead of handing it back to the device, so g holds the scratch of
- * its largest call (for a fixed workload, calls after the first allocate no
- * device memory) until ss_gmg_free.  B = 0 is a no-op.  Results are bit-identical to a sequential CPU
+ * work, from the library's memory pool for g's device, which keeps that
+ * memory for later calls (for a fixed workload, calls after the first
+ * allocate no device memory; see ss_release_cached_memory).  B = 0 is a
+ * no-op.  Results are bit-identical to a sequential CPU
  * evaluation of the same rules.
  * Errors: SS_ERR_INVALID_ARG, SS_ERR_OOM, SS_ERR_DEVICE, SS_ERR_UNSUPPORTED.
  */
@@ -386,6 +386,16 @@ int ss_sched_complete(ss_sched *s, int64_t op);
 /* Current state (SS_OP_*) and device of every op, HOST arrays of n_ops
  * entries; either may be NULL.  The device of an unscheduled op is 0. */
 int ss_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place);
+
+/*
+ * The library takes every device buffer (staged GMGs, scratch, scheduler and
+ * state buffers) from one stream-ordered memory pool per device that keeps
+ * freed memory for later calls: handing large buffers back to the driver and
+ * allocating again soon after stalls for up to seconds.  This call returns
+ * the pools' unused memory to the driver (synchronising each device that has
+ * a pool first); buffers in use stay.  Errors: SS_ERR_DEVICE.
+ */
+int ss_release_cached_memory(void);
 
 /* Message for the calling thread's most recent failed call ("" if none). */
 const char *ss_last_error(void);

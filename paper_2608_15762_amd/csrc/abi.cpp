@@ -262,7 +262,8 @@ extern "C" void ss_state_free(ss_state *st) {
     (void)hipGetDevice(&prev);
     (void)hipSetDevice(st->device);
     (void)hipDeviceSynchronize();
-    (void)hipFree(st->mem);
+    ss_pool_free(st->mem, nullptr);
+    (void)hipDeviceSynchronize();
     (void)hipSetDevice(prev);
   }
   delete st;

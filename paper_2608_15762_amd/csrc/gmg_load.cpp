@@ -3,6 +3,7 @@
 // Sec. 3.3.2; the per-candidate work happens in simulate.hip).
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <sstream>
 #include <vector>
@@ -32,6 +33,97 @@ struct Packer {
 int bad(const std::string &msg) { return ss_set_error(SS_ERR_INVALID_GMG, "invalid GMG: " + msg); }
 
 }  // namespace
+
+namespace {
+constexpr int kMaxDevices = 256;
+std::mutex g_pool_mu;
+hipMemPool_t g_pools[kMaxDevices] = {};
+hipStream_t g_aux[kMaxDevices] = {};
+}  // namespace
+
+hipStream_t ss_device_aux(int device) {
+  if (device < 0 || device >= kMaxDevices) {
+    ss_set_error(SS_ERR_UNSUPPORTED, "device id beyond the library's stream table");
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_pool_mu);
+  if (!g_aux[device]) {
+    int prev = 0;
+    (void)hipGetDevice(&prev);
+    hipStream_t s = nullptr;
+    hipError_t e = hipSetDevice(device);
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+    (void)hipSetDevice(prev);
+    if (e != hipSuccess) {
+      ss_set_error(SS_ERR_DEVICE, std::string("creating the second stream: ") + hipGetErrorString(e));
+      return nullptr;
+    }
+    g_aux[device] = s;
+  }
+  return g_aux[device];
+}
+
+hipMemPool_t ss_device_pool(int device) {
+  if (device < 0 || device >= kMaxDevices) {
+    ss_set_error(SS_ERR_UNSUPPORTED, "device id beyond the library's pool table");
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_pool_mu);
+  if (g_pools[device]) return g_pools[device];
+  hipMemPoolProps props{};
+  props.allocType = hipMemAllocationTypePinned;
+  props.handleTypes = hipMemHandleTypeNone;
+  props.location.type = hipMemLocationTypeDevice;
+  props.location.id = device;
+  uint64_t keep = UINT64_MAX;  // never hand freed memory back on synchronisation
+  hipMemPool_t pool = nullptr;
+  hipError_t e = hipMemPoolCreate(&pool, &props);
+  if (e == hipSuccess) e = hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+  if (e != hipSuccess) {
+    if (pool) (void)hipMemPoolDestroy(pool);
+    ss_set_error(SS_ERR_DEVICE, std::string("creating the scratch pool: ") + hipGetErrorString(e));
+    return nullptr;
+  }
+  g_pools[device] = pool;
+  return pool;
+}
+
+int ss_pool_alloc(int device, size_t bytes, hipStream_t stream, void **out) {
+  *out = nullptr;
+  hipMemPool_t pool = ss_device_pool(device);
+  if (!pool) return SS_ERR_DEVICE;
+  hipError_t e = ss_pool_malloc(out, bytes, pool, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) {
+    if (*out) (void)hipFreeAsync(*out, stream);
+    *out = nullptr;
+    return ss_set_error(e == hipErrorOutOfMemory ? SS_ERR_OOM : SS_ERR_DEVICE,
+                        std::string("allocating from the scratch pool: ") + hipGetErrorString(e));
+  }
+  return SS_OK;
+}
+
+void ss_pool_free(void *p, hipStream_t stream) {
+  if (p) (void)hipFreeAsync(p, stream);
+}
+
+extern "C" int ss_release_cached_memory(void) {
+  ss_clear_error();
+  std::lock_guard<std::mutex> lock(g_pool_mu);
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  int rc = SS_OK;
+  for (int d = 0; d < kMaxDevices; ++d) {
+    if (!g_pools[d]) continue;
+    hipError_t e = hipSetDevice(d);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = hipMemPoolTrimTo(g_pools[d], 0);
+    if (e != hipSuccess && rc == SS_OK)
+      rc = ss_set_error(SS_ERR_DEVICE, std::string("trimming a scratch pool: ") + hipGetErrorString(e));
+  }
+  (void)hipSetDevice(prev);
+  return rc;
+}
 
 extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
   ss_clear_error();
@@ -290,36 +382,22 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
       delete g;
       return ss_set_error(SS_ERR_DEVICE, "hipGetDevice failed");
     }
-    if (hipMalloc(&g->dev_mem, pk.host.size()) != hipSuccess) {
-      delete g;
-      return ss_set_error(SS_ERR_OOM, "hipMalloc of the staged GMG failed");
+    g->aux = ss_device_aux(g->device);
+    g->pool = g->aux ? ss_device_pool(g->device) : nullptr;
+    int arc = g->pool ? ss_pool_alloc(g->device, pk.host.size(), g->aux, &g->dev_mem) : SS_ERR_DEVICE;
+    hipError_t e = hipSuccess;
+    if (arc == SS_OK) {
+      e = hipMemcpyAsync(g->dev_mem, pk.host.data(), pk.host.size(), hipMemcpyHostToDevice, g->aux);
+      if (e == hipSuccess) e = hipStreamSynchronize(g->aux);
+      if (e != hipSuccess) arc = ss_set_error(SS_ERR_DEVICE, "copying the staged GMG failed");
     }
-    if (hipMemcpy(g->dev_mem, pk.host.data(), pk.host.size(), hipMemcpyHostToDevice) != hipSuccess) {
-      (void)hipFree(g->dev_mem);
-      delete g;
-      return ss_set_error(SS_ERR_DEVICE, "hipMemcpy of the staged GMG failed");
-    }
-    if (hipStreamCreateWithFlags(&g->aux, hipStreamNonBlocking) != hipSuccess) {
-      (void)hipFree(g->dev_mem);
-      delete g;
-      return ss_set_error(SS_ERR_DEVICE, "hipStreamCreateWithFlags failed");
-    }
-    {
-      hipMemPoolProps props{};
-      props.allocType = hipMemAllocationTypePinned;
-      props.handleTypes = hipMemHandleTypeNone;
-      props.location.type = hipMemLocationTypeDevice;
-      props.location.id = g->device;
-      uint64_t keep = UINT64_MAX;  // never return freed scratch to the device early
-      hipError_t e = hipMemPoolCreate(&g->pool, &props);
-      if (e == hipSuccess) e = hipMemPoolSetAttribute(g->pool, hipMemPoolAttrReleaseThreshold, &keep);
-      if (e != hipSuccess) {
-        if (g->pool) (void)hipMemPoolDestroy(g->pool);
-        (void)hipStreamDestroy(g->aux);
-        (void)hipFree(g->dev_mem);
-        delete g;
-        return ss_set_error(SS_ERR_DEVICE, std::string("creating the scratch pool: ") + hipGetErrorString(e));
+    if (arc != SS_OK) {
+      if (g->aux) {
+        ss_pool_free(g->dev_mem, g->aux);
+        (void)hipStreamSynchronize(g->aux);
       }
+      delete g;
+      return arc;
     }
     auto *base = static_cast<unsigned char *>(g->dev_mem);
     GmgView &V = g->view;
@@ -389,9 +467,8 @@ extern "C" void ss_gmg_free(ss_gmg *g) {
   (void)hipGetDevice(&prev);
   (void)hipSetDevice(g->device);
   (void)hipDeviceSynchronize();
-  if (g->aux) (void)hipStreamDestroy(g->aux);
-  if (g->pool) (void)hipMemPoolDestroy(g->pool);
-  (void)hipFree(g->dev_mem);
+  ss_pool_free(g->dev_mem, g->aux);
+  (void)hipStreamSynchronize(g->aux);
   (void)hipSetDevice(prev);
   delete g;
 }

@@ -45,6 +45,7 @@ struct ss_sched {
   // the chosen candidate's simulation state after the scheduled ops (the
   // prefix of the next round), and a second state to capture the next one in
   ss_state *prefix = nullptr, *next = nullptr;
+
 };
 
 namespace {
@@ -164,6 +165,7 @@ int ss_run_sched_create(const ss_sched_desc *d, ss_sched **out) {
   if (rc == SS_OK) rc = ss_state_create(&s->next);
   if (rc != SS_OK) {
     ss_state_free(s->prefix);
+    ss_state_free(s->next);
     delete s;
     return rc;
   }
@@ -176,7 +178,10 @@ void ss_run_sched_free(ss_sched *s) {
   (void)hipGetDevice(&prev);
   (void)hipSetDevice(s->device);
   (void)hipDeviceSynchronize();
-  if (s->dev_buf) (void)hipFree(s->dev_buf);
+  if (s->dev_buf) {
+    ss_pool_free(s->dev_buf, nullptr);
+    (void)hipDeviceSynchronize();
+  }
   (void)hipSetDevice(prev);
   ss_state_free(s->prefix);
   ss_state_free(s->next);
@@ -261,18 +266,19 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
   const size_t need = sz_rows + 2 * sz_ms + sz_vi + sz_sl + sz_best;
   hipError_t err = hipSuccess;
   if (need > s->dev_bytes) {
+    const size_t grow = std::max(need, 2 * s->dev_bytes);  // rounds' graphs grow: few reallocations
     if (s->dev_buf) {
-      (void)hipDeviceSynchronize();
-      (void)hipFree(s->dev_buf);
+      (void)hipStreamSynchronize(stream);
+      ss_pool_free(s->dev_buf, stream);
       s->dev_buf = nullptr;
       s->dev_bytes = 0;
     }
-    err = hipMalloc(&s->dev_buf, need);
-    if (err != hipSuccess) {
+    rc = ss_pool_alloc(s->device, grow, stream, &s->dev_buf);
+    if (rc != SS_OK) {
       ss_gmg_free(g);
-      return sched_fail(err, "ss_sched_round: device buffer");
+      return rc;
     }
-    s->dev_bytes = need;
+    s->dev_bytes = grow;
   }
   unsigned char *p = static_cast<unsigned char *>(s->dev_buf);
   auto *d_rows = reinterpret_cast<uint8_t *>(p);

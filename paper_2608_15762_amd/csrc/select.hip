@@ -83,8 +83,8 @@ int ss_run_select(const ss_gmg *g, const uint8_t *violation, const int64_t *key,
                   int require_sla, int64_t *out_best, hipStream_t stream) {
   const int nblk = (int)std::max<int64_t>(1, std::min<int64_t>(kMaxBlocks, (B + kThreads - 1) / kThreads));
   void *part = nullptr;
-  hipError_t err = hipMallocAsync(&part, (size_t)nblk * 2 * sizeof(int64_t), stream);
-  if (err != hipSuccess) return hip_fail(err, "hipMallocAsync of selection scratch");
+  hipError_t err = ss_pool_malloc(&part, (size_t)nblk * 2 * sizeof(int64_t), g->pool, stream);
+  if (err != hipSuccess) return hip_fail(err, "allocating the selection scratch");
   int rc = SS_OK;
   SsTimingRec *t_sel = ss_timing_start(SS_KERNEL_SELECT, stream);
   hipLaunchKernelGGL(select_partial, dim3(nblk), dim3(kThreads), 0, stream, violation, key, slack, g->n_req, B,

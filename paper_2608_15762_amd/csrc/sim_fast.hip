@@ -1643,7 +1643,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   const int64_t n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
   const size_t sz_tk = align((size_t)n_ticket * 4);
   void *scratch = nullptr;
-  err = hipMallocFromPoolAsync(&scratch,
+  err = ss_pool_malloc(&scratch,
                                sz_pt + 2 * sz_fin + 2 * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
                                g->pool, stream);
   if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
@@ -1769,7 +1769,7 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   const int64_t n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
   const size_t sz_tk = align((size_t)n_ticket * 4);
   void *scratch = nullptr;
-  err = hipMallocFromPoolAsync(
+  err = ss_pool_malloc(
       &scratch, sz_fin + sz_rank + sz_miss + sz_spill + 2 * (sz_own + sz_cp + sz_meta) + sz_wk + sz_wb + sz_tk, g->pool,
       stream);
   if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
@@ -1866,7 +1866,7 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
   const int64_t n_ticket = n_chunk * ((chunk + sub - 1) / sub);
   const size_t sz_tk = align((size_t)n_ticket * 4);
   void *scratch = nullptr;
-  err = hipMallocFromPoolAsync(&scratch, sz_fin + 2 * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
+  err = ss_pool_malloc(&scratch, sz_fin + 2 * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
                                g->pool, stream);
   if (err != hipSuccess) return hip_fail(err, "allocating the memory-pass scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);

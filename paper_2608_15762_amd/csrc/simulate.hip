@@ -732,7 +732,7 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
   const bool resumed = from && from->k > 0;
   const size_t sz_bad = resumed ? align((size_t)chunk * 4) : 0;
   void *scratch = nullptr;
-  err = hipMallocFromPoolAsync(&scratch,
+  err = ss_pool_malloc(&scratch,
                                sz_fin + sz_comp + sz_miss + sz_spr + sz_spo + sz_bydev + 2 * sz_ev + sz_port + sz_arr +
                                    sz_bad,
                                g->pool, stream);
@@ -857,19 +857,18 @@ static int state_reserve(ss_state *st, const ss_gmg *g, hipStream_t stream) {
   const int64_t cn = std::max<int64_t>(n, 2 * st->cap_n), cd = std::max<int64_t>(d, st->cap_d),
                 cr = std::max<int64_t>(r, st->cap_r);
   const size_t bytes = (size_t)(cn + cd + cr + 2) * 8 + (size_t)cd * 4 + 16;
-  hipError_t err = hipSuccess;
   if (st->mem) {
-    err = hipStreamSynchronize(stream);
-    if (err == hipSuccess) err = hipFree(st->mem);
-    st->mem = nullptr;
+    const hipError_t err = hipStreamSynchronize(stream);
     if (err != hipSuccess) return hip_fail(err, "releasing a state buffer");
+    ss_pool_free(st->mem, stream);
+    st->mem = nullptr;
   }
-  err = hipMalloc(&st->mem, bytes);
-  if (err != hipSuccess) {
+  const int rc = ss_pool_alloc(g->device, bytes, stream, &st->mem);
+  if (rc != SS_OK) {
     st->mem = nullptr;
     st->cap_n = st->cap_d = st->cap_r = 0;
     st->k = 0;
-    return hip_fail(err, "allocating a state buffer");
+    return rc;
   }
   auto *p = static_cast<int64_t *>(st->mem);
   st->fin = p;
@@ -896,7 +895,7 @@ int ss_run_state_capture(const ss_gmg *g, const ss_state *from, const uint8_t *p
   if (rc != SS_OK) return rc;
   // the schedule kernel's per-candidate outputs, unused here
   void *outs = nullptr;
-  hipError_t err = hipMallocFromPoolAsync(&outs, 256 + (size_t)g->n_req * 8 + 8, g->pool, stream);
+  hipError_t err = ss_pool_malloc(&outs, 256 + (size_t)g->n_req * 8 + 8, g->pool, stream);
   if (err != hipSuccess) return hip_fail(err, "allocating capture outputs");
   auto *o = static_cast<int64_t *>(outs);
   rc = run_simulate_generic(g, placement, 1, o, nullptr, reinterpret_cast<uint8_t *>(o + 2), o + 4, o + 1, stream,

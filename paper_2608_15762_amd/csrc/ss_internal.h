@@ -82,14 +82,41 @@ struct ss_gmg {
   int64_t max_outdeg = 0;  // largest successor count of any op
   void *dev_mem = nullptr;
   // second stream of the memory passes (the peak evaluation of one sub-chunk
-  // overlaps the interval pass of the next); default priority, non-blocking
+  // overlaps the interval pass of the next): the device's (ss_device_aux)
   hipStream_t aux = nullptr;
-  // stream-ordered pool of the simulation scratch: freed scratch stays in
-  // the pool for the next call (no device allocation once the largest call
-  // has run) and goes back to the device with the handle
+  // the device's scratch pool (ss_device_pool), also holding dev_mem
   hipMemPool_t pool = nullptr;
   GmgView view{};
 };
+
+// The process-wide stream-ordered pool of a device: every device buffer of
+// the library comes from it, and freed memory stays in it (release threshold:
+// never) until ss_release_cached_memory.  Handing large buffers back to the
+// driver and allocating again soon after stalls for up to seconds.  Returns
+// nullptr (with the error recorded) when the pool cannot be made.
+hipMemPool_t ss_device_pool(int device);
+// Requests to the pool are rounded up to the next size of the form
+// 2^k x {1, 1.25, 1.5, 1.75}: calls whose scratch grows a little each time (the
+// incremental loop's rounds, whose graph gains a batch per round) reuse the
+// pool's blocks instead of taking new memory from the driver every call.
+inline size_t ss_pool_round(size_t x) {
+  if (x <= 4096) return 4096;
+  int k = 63 - __builtin_clzll((unsigned long long)x);  // 2^k <= x < 2^(k+1)
+  const size_t base = size_t(1) << k, q = base >> 2;
+  return base + ((x - base + q - 1) / q) * q;
+}
+inline hipError_t ss_pool_malloc(void **p, size_t bytes, hipMemPool_t pool, hipStream_t stream) {
+  return hipMallocFromPoolAsync(p, ss_pool_round(bytes), pool, stream);
+}
+// A buffer from the device's pool, ready for use on any stream when it returns
+// (allocated on `stream`, which is synchronised), and its release.
+int ss_pool_alloc(int device, size_t bytes, hipStream_t stream, void **out);
+void ss_pool_free(void *p, hipStream_t stream);
+// The process-wide second stream of a device (default priority, non-blocking),
+// made once: creating and destroying streams as objects come and go remaps the
+// few hardware queues and stalled host calls for up to a second.  nullptr
+// (with the error recorded) when it cannot be made.
+hipStream_t ss_device_aux(int device);
 
 // A captured simulation state (ss_simulate_batch_resume): one candidate after
 // its first k ops of a GMG with d devices and r requests.  One device

@@ -30,7 +30,7 @@ EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "s
             "ss_kernel_time", "ss_last_error", "ss_est_create", "ss_est_free", "ss_est_add", "ss_est_solve",
             "ss_est_predict", "ss_sched_create", "ss_sched_free", "ss_sched_round", "ss_sched_complete",
             "ss_sched_state", "ss_state_create", "ss_state_free", "ss_state_info", "ss_simulate_batch_resume",
-            "ss_state_capture")
+            "ss_state_capture", "ss_release_cached_memory")
 SS_OP_UNSCHEDULED, SS_OP_ISSUED, SS_OP_DONE = 0, 1, 2
 SS_ROUND_ISSUED, SS_ROUND_BUDGET, SS_ROUND_IDLE, SS_ROUND_INFEASIBLE = 0, 1, 2, 3
 SS_KERNEL_SCHEDULE, SS_KERNEL_MEMORY, SS_KERNEL_SELECT, SS_KERNEL_INTERVALS, SS_KERNEL_TRANSPOSE = 0, 1, 2, 3, 4
@@ -111,6 +111,8 @@ def lib():
             L.ss_simulate_batch_resume.restype = ctypes.c_int
             L.ss_state_capture.argtypes = [P, P, P, P, P]
             L.ss_state_capture.restype = ctypes.c_int
+            L.ss_release_cached_memory.argtypes = []
+            L.ss_release_cached_memory.restype = ctypes.c_int
             _lib = L
     return _lib
 
@@ -311,6 +313,11 @@ def simulate_batch_resume(g: Gmg, placements, start=None, want_peak=True, want_s
                                           _ptr(out["makespan"]), _ptr(out["peak"]), _ptr(out["violation"]),
                                           _ptr(out["slack"]), _ptr(out["sumfin"]), _stream_ptr(stream)))
     return out
+
+
+def release_cached_memory():
+    """ss_release_cached_memory: hand the library pools' unused memory back."""
+    _check(lib().ss_release_cached_memory())
 
 
 def select_best(g: Gmg, violation, key, slack=None, require_sla=False, out=None, stream=None):
