@@ -53,7 +53,7 @@ namespace {
 constexpr int kWave = 64;
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per chunk
-constexpr int64_t kRecordBudget = int64_t(12) << 30;   // interval records per sub-chunk
+constexpr int64_t kRecordBudget = int64_t(32) << 30;   // interval records per sub-chunk (two sets)
 constexpr int kPeakBlocksPerCU = 8;  // fast_peaks holds about 19.5 KB of LDS
 
 __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
@@ -1628,6 +1628,11 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   const int64_t rec_per_cand = (own_stride(N) + cp_stride(E)) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4 + N * 2;
   int64_t sub = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
   sub = std::min<int64_t>(sub, chunk);
+  {  // equal sub-chunks, at least two for a large chunk (the peak pass of one
+     // overlaps the interval pass of the next)
+    const int64_t n = std::max<int64_t>((chunk + sub - 1) / sub, chunk >= 8192 ? 2 : 1);
+    sub = (chunk + n - 1) / n;
+  }
   const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
   const int64_t slot_cap = N + E + 1;  // most allocations one device can hold
 
@@ -1753,6 +1758,11 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   const int64_t rec_per_cand = (own_stride(N) + cp_stride(E)) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4;
   int64_t sub = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
   sub = std::min<int64_t>(sub, chunk);
+  {  // equal sub-chunks, at least two for a large chunk (the peak pass of one
+     // overlaps the interval pass of the next)
+    const int64_t n = std::max<int64_t>((chunk + sub - 1) / sub, chunk >= 8192 ? 2 : 1);
+    sub = (chunk + n - 1) / n;
+  }
   const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
   const int64_t slot_cap = N + E + 1;
 
