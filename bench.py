@@ -46,6 +46,9 @@ def parse():
                     help="transfers take their estimate (default) or contend for device send/receive ports")
     ap.add_argument("--part", choices=("simulate", "estimator", "sched"), default="simulate",
                     help="the what-if simulator (default), the online estimators, or the incremental loop")
+    ap.add_argument("--pipeline", type=int, default=0, metavar="CHUNK",
+                    help="also time the batch streamed through the GPU in CHUNK-candidate pieces (host generation, "
+                         "host-to-device copy and simulation overlapped; reported beside value, not as it)")
     ap.add_argument("--batch-cap", type=int, default=400, help="incremental loop: ops per batch")
     ap.add_argument("--budget", type=int, default=1600, help="incremental loop: issued-op budget")
     return ap.parse_args()
@@ -121,6 +124,54 @@ def stage_placements(torch, synth, g, cid, B, dev, chunk):
         events[k].record()
     torch.cuda.synchronize()
     return P
+
+
+def pipeline_rate(torch, ss, synth, g, cid, h, B, chunk, out, best):
+    """The batch streamed through the GPU: the host generator fills a ring of
+    three pinned chunk buffers, each chunk is copied to one of two device slots
+    on a copy stream while the previous chunk is simulated.  Returns (candidates
+    per second over the whole stream, host-to-device GB/s of the copies)."""
+    N = g.n_ops
+    rec = synth.CONFIGS[cid].placement
+    base = synth.base_placement(g, cid) if (rec["mode_even"] == 1 or rec["mode_odd"] == 1) else None
+    ring = [torch.empty((chunk, N), dtype=torch.uint8, pin_memory=True) for _ in range(3)]
+    dev = out["makespan"].device
+    slots = [torch.empty((chunk, N), dtype=torch.uint8, device=dev) for _ in range(2)]
+    copy_stream = torch.cuda.Stream()
+    comp = torch.cuda.current_stream()
+    copied = [torch.cuda.Event() for _ in range(2)]
+    freed = [torch.cuda.Event() for _ in range(2)]
+    host_free = [None, None, None]
+    n_chunks = (B + chunk - 1) // chunk
+    c_start = [torch.cuda.Event(enable_timing=True) for _ in range(n_chunks)]
+    c_stop = [torch.cuda.Event(enable_timing=True) for _ in range(n_chunks)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i, b0 in enumerate(range(0, B, chunk)):
+        nb = min(chunk, B - b0)
+        r, k = i % 3, i % 2
+        if host_free[r] is not None:
+            host_free[r].synchronize()  # the copy that read this host buffer has finished
+        synth.placements(g, cid, b0, nb, out=ring[r].numpy()[:nb], base=base)
+        with torch.cuda.stream(copy_stream):
+            if i >= 2:
+                copy_stream.wait_event(freed[k])
+            c_start[i].record(copy_stream)
+            slots[k][:nb].copy_(ring[r][:nb], non_blocking=True)
+            c_stop[i].record(copy_stream)
+            copied[k].record(copy_stream)
+            host_free[r] = torch.cuda.Event()
+            host_free[r].record(copy_stream)
+        comp.wait_event(copied[k])
+        ss.simulate_batch_into(h, slots[k][:nb], out["makespan"][b0:b0 + nb], out["violation"][b0:b0 + nb],
+                               out["peak"][b0:b0 + nb], out["slack"][b0:b0 + nb], out["sumfin"][b0:b0 + nb],
+                               stream=comp)
+        freed[k].record(comp)
+    ss.select_best(h, out["violation"], out["sumfin"], out=best, stream=comp)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    copy_ms = sum(c_start[i].elapsed_time(c_stop[i]) for i in range(n_chunks))
+    return B / elapsed, B * N / (copy_ms * 1e-3) / 1e9
 
 
 def sample_rows(synth, g, cid, idx):
@@ -470,6 +521,12 @@ def main():
     torch.cuda.synchronize()
     bi, bk = best.cpu().tolist()
     result["best"] = {"index": bi, "sumfin": bk}
+    if args.pipeline > 0:
+        log(f"streaming the batch through the GPU in chunks of {args.pipeline}")
+        rate, h2d = pipeline_rate(torch, ss, synth, g, cid, h, B, args.pipeline, out, best)
+        bi2, bk2 = best.cpu().tolist()
+        result["pipeline"] = {"chunk": args.pipeline, "value": round(rate, 1), "unit": "candidates/s",
+                              "h2d_gbs": round(h2d, 1), "same_best": (bi2, bk2) == (bi, bk)}
     if not args.no_cpu_baseline:
         got = {k: v.cpu().numpy() for k, v in out.items()}
         log("running the oracle CPU baseline")
