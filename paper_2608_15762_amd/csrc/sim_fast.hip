@@ -35,7 +35,8 @@
 //                 only gaps holding copies and frees whose bound exceeds the
 //                 best so far are swept event by event.
 // The peak pass of a sub-chunk runs on a second stream beside the interval
-// pass of the next one (the records are double-buffered).  The schedule of
+// pass of the next ones (three record sets, so an interval pass rarely waits
+// for the peak pass that still reads its set).  The schedule of
 // the next chunk waits for the last peak pass: its launch is exactly one round
 // of resident waves, and waves placed late behind another kernel's would add
 // a second round.
@@ -53,7 +54,7 @@ namespace {
 constexpr int kWave = 64;
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per chunk
-constexpr int64_t kRecordBudget = int64_t(32) << 30;   // interval records per sub-chunk (two sets)
+constexpr int64_t kRecordBudget = int64_t(32) << 30;   // sizes the sub-chunks (record bytes of about two sets)
 constexpr int kPeakBlocksPerCU = 8;  // fast_peaks holds about 19.5 KB of LDS
 
 __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
@@ -113,18 +114,24 @@ __device__ __forceinline__ uint32_t xfer_of(const GmgView &G, int u, int du, int
 //   T-4  load the op's device from the op-major placements;
 //   T-3  load finish time and device of its first kPipePre predecessors when
 //        they are op T-4 or older (op-major finish times written earlier by
-//        this lane); ops T-3..T-1 come from a three-deep register history;
-//   T-2  gather the link class of each predecessor transfer,
-//        the op's duration on its device, and the device's current slice end
-//        plus the next slice's bounds;
-//   T    ready time, placement, stores.
-// Uniform per-op fields come from op_meta, fetched 64 ops at a time (lane j
-// holds op 64b+j) and broadcast with readlane.  Stage state is indexed by
+//        this lane);
+//   T-2  resolve each predecessor: ops T-3 and T-2 from a two-deep register
+//        history (op T-1's device is already loaded), the rest from the T-3
+//        loads, kept for step T; gather the link class of each predecessor
+//        transfer, the op's duration on its device, and the device's current
+//        slice end plus the next slice's bounds;
+//   T    ready time (only a predecessor T-1 still comes from the history),
+//        placement, stores.
+// Uniform per-op fields come from op_meta through a 64-op window that
+// advances by 32 ops (lane j holds op w0+j), broadcast with one readlane
+// each.  Row offsets are 32 x 32-bit products (a chunk holds fewer than 2^32
+// candidates).  Stage state is indexed by
 // T mod 4, static in the four-way unrolled loop.  Loads are unconditional
 // (indices clamped, unused values discarded by selects) so the loop body has
 // no branch around a memory operation and the compiler can keep the loads of
 // later stages in flight while op T waits only for its own.
 constexpr int kPipePre = 2;  // predecessors handled by the pipeline; more go through the CSR
+constexpr int kWindowStep = 32;  // ops per advance of the op-field window
 
 struct SchedPipe {
   uint32_t dq[4];                // device of the target op (raw byte)
@@ -177,27 +184,28 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   }
 
   const int ms_ = G.meta_stride;
-  uint32_t mA[kOpMetaFields], mB[kOpMetaFields];  // fields of ops [blk0, blk0+64) and the next 64
+  // Fields of ops [w0, w0 + 64) in mA (lane j: op w0 + j), of [w0 + 32,
+  // w0 + 96) in mB.  The window advances by 32 ops, so every op a step reads
+  // (T .. T+3) lies in mA and a field costs one readlane.
+  uint32_t mA[kOpMetaFields], mB[kOpMetaFields];
 #pragma unroll
   for (int f = 0; f < kOpMetaFields; ++f) {
     mA[f] = G.op_meta[(int64_t)f * ms_ + lane];
-    mB[f] = G.op_meta[(int64_t)f * ms_ + kWave + lane];
+    mB[f] = G.op_meta[(int64_t)f * ms_ + kWindowStep + lane];
   }
-  int blk0 = 0;
-  // uniform field f of op t, t in [blk0, blk0 + 128)
-  auto meta = [&](int f, int t) -> uint32_t {
-    const int j = t - blk0;
-    const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)mA[f], j & (kWave - 1));
-    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)mB[f], j & (kWave - 1));
-    return j < kWave ? a : b;
-  };
+  int w0 = 0;
+  auto meta = [&](int f, int t) -> uint32_t { return (uint32_t)__builtin_amdgcn_readlane((int)mA[f], t - w0); };
   auto pred_of = [](uint32_t p01, int i) -> uint32_t { return i ? (p01 >> 16) : (p01 & 0xFFFFu); };
 
   bool invalid = false;
   // A loaded value is left untouched until the stage that consumes it, so the
   // wait for it lands there and not right after the load.
   auto clampD = [&](uint32_t x) -> uint32_t { return x >= (uint32_t)D ? 0u : x; };
-  auto load_dev = [&](int t) -> uint32_t { return PT[(int64_t)t * nb + c]; };
+  const uint64_t nbu = (uint64_t)(uint32_t)nb;  // a chunk holds fewer than 2^32 candidates
+  const uint8_t *const PTc = PT + c;
+  uint32_t *const finTc = finT + c;
+  auto row = [&](int t) -> uint64_t { return (uint64_t)(uint32_t)t * nbu; };
+  auto load_dev = [&](int t) -> uint32_t { return PTc[row(t)]; };
   SchedPipe S;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -208,8 +216,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     for (int i = 0; i < kPipePre; ++i) S.pf[q][i] = S.pd[q][i] = S.lc[q][i] = 0;
   }
 
-  // Results of the last three ops: h1 = op T (after its step), h2, h3 before it.
-  uint32_t h1f = 0, h1d = 0, h2f = 0, h2d = 0, h3f = 0, h3d = 0;
+  // Results of the last two ops: h1 = op T (after its step), h2 before it.
+  uint32_t h1f = 0, h1d = 0, h2f = 0, h2d = 0;
 
   // Stage T-2 for target op t = T+2, after op T.
   auto stage2 = [&](auto qq, int T) {
@@ -231,6 +239,10 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
       else lc = G.link_class[du * D + dt];
       S.lc[q2][i] = lc;
       const uint32_t fu = u == T ? h1f : u == T - 1 ? h2f : S.pf[q2][i];
+      // resolved for the step (a predecessor T+1 takes its finish from the
+      // step's history; its device is already final)
+      S.pd[q2][i] = du;
+      S.pf[q2][i] = fu;
       // transfer time in the bound: exact with device groups, else the
       // cheapest class (the fields hold classes 0 and 1), else none
       const uint32_t x0 = meta(kMetaX + 2 * i, t), x1 = meta(kMetaX + 2 * i + 1, t);
@@ -253,8 +265,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     for (int i = 0; i < kPipePre; ++i) {
       const int u = (int)pred_of(p01, i);
       const int us = u < T ? u : 0;  // rows not yet written (or absent) read row 0, never used
-      S.pf[q3][i] = finT[(int64_t)us * nb + c];
-      S.pd[q3][i] = PT[(int64_t)us * nb + c];
+      S.pf[q3][i] = finTc[row(us)];
+      S.pd[q3][i] = PTc[row(us)];
     }
   };
 
@@ -279,8 +291,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
 #pragma unroll
     for (int i = 0; i < kPipePre; ++i) {
       const int u = (int)pred_of(p01, i);
-      const uint32_t tt = u == T - 1 ? h1f : u == T - 2 ? h2f : u == T - 3 ? h3f : S.pf[q0][i];
-      const uint32_t du = u == T - 1 ? h1d : u == T - 2 ? h2d : u == T - 3 ? h3d : clampD(S.pd[q0][i]);
+      const uint32_t tt = u == T - 1 ? h1f : S.pf[q0][i];
+      const uint32_t du = S.pd[q0][i];
       uint32_t x;
       if (kLink == 2) {
         x = G.xfer32[(int64_t)(u < T ? u : 0) * K + S.lc[q0][i]];
@@ -300,8 +312,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
           tt = h1f;
           du = h1d;
         } else {
-          tt = finT[(int64_t)u * nb + c];
-          du = PT[(int64_t)u * nb + c];
+          tt = finTc[row(u)];
+          du = PTc[row(u)];
           if (du >= (uint32_t)D) du = 0;
         }
         if (du != d) tt += xfer_of(G, u, (int)du, (int)d);
@@ -335,12 +347,10 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     }
     const uint32_t f = s + w;
     clk[slot] = f;
-    finT[(int64_t)T * nb + c] = f;
+    finTc[row(T)] = f;
     atomicMax(&comp[r * kWave + lane], f);
     ms = umax32(ms, f);
     sum += f;
-    h3f = h2f;
-    h3d = h2d;
     h2f = h1f;
     h2d = h1d;
     h1f = f;
@@ -350,16 +360,16 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     S.dq[q0] = load_dev(min(T + 4, N - 1));
   };
 
-  const int n_main = N / kWave * kWave;
-  for (; blk0 < n_main; blk0 += kWave) {
-    if (blk0 > 0) {
+  const int n_main = N / kWindowStep * kWindowStep;
+  for (; w0 < n_main; w0 += kWindowStep) {
+    if (w0 > 0) {
 #pragma unroll
       for (int f = 0; f < kOpMetaFields; ++f) {
         mA[f] = mB[f];
-        mB[f] = G.op_meta[(int64_t)f * ms_ + blk0 + kWave + lane];
+        mB[f] = G.op_meta[(int64_t)f * ms_ + min(w0 + kWindowStep + lane, ms_ - 1)];
       }
     }
-    for (int T = blk0; T < blk0 + kWave; T += 4) {
+    for (int T = w0; T < w0 + kWindowStep; T += 4) {
       step(std::integral_constant<int, 0>(), T);
       step(std::integral_constant<int, 1>(), T + 1);
       step(std::integral_constant<int, 2>(), T + 2);
@@ -371,7 +381,7 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
 #pragma unroll
       for (int f = 0; f < kOpMetaFields; ++f) mA[f] = mB[f];
     }
-    blk0 = n_main;
+    w0 = n_main;
     for (int T = n_main; T < N; T += 4) {
       step(std::integral_constant<int, 0>(), T);
       if (T + 1 < N) step(std::integral_constant<int, 1>(), T + 1);
@@ -1474,14 +1484,15 @@ int hip_fail(hipError_t err, const char *what) {
                       std::string(what) + ": " + hipGetErrorString(err));
 }
 
-// Sub-chunk scratch of the memory passes.  The records (own, cp, meta) are
-// double-buffered: the interval pass of sub-chunk i runs on the caller's
-// stream while the peak pass of sub-chunk i-1 runs on the GMG's second
-// stream; events order each peak pass after its interval pass, and the reuse
-// of a buffer after the peak pass that read it.
+// Sub-chunk scratch of the memory passes.  The records (own, cp, meta) come in
+// kRecSets sets used in turn: the interval pass of sub-chunk i runs on the
+// caller's stream while peak passes of earlier sub-chunks run on the GMG's
+// second stream; events order each peak pass after its interval pass, and the
+// reuse of a set after the peak pass that read it.
+constexpr int kRecSets = 3;
 struct MemPass {
-  Rec *own[2], *cp[2];
-  int32_t *meta[2];
+  Rec *own[kRecSets], *cp[kRecSets];
+  int32_t *meta[kRecSets];
   uint16_t *rank;  // given ranks: candidate rows of the whole chunk; else sub rows
   uint32_t *wk;
   int64_t *wb;
@@ -1490,15 +1501,15 @@ struct MemPass {
   int64_t sub, nslots, slot_cap;
   bool iv_fast;
   hipStream_t aux;
-  hipEvent_t iv_done[2], pk_done[2];
+  hipEvent_t iv_done[kRecSets], pk_done[kRecSets];
   int64_t it;  // sub-chunks issued so far in this call
 };
 
 int mem_pass_events(MemPass &M) {
-  for (int k = 0; k < 2; ++k) {
+  for (int k = 0; k < kRecSets; ++k) {
     M.iv_done[k] = M.pk_done[k] = nullptr;
   }
-  for (int k = 0; k < 2; ++k) {
+  for (int k = 0; k < kRecSets; ++k) {
     hipError_t err = hipEventCreateWithFlags(&M.iv_done[k], hipEventDisableTiming);
     if (err == hipSuccess) err = hipEventCreateWithFlags(&M.pk_done[k], hipEventDisableTiming);
     if (err != hipSuccess) return hip_fail(err, "hipEventCreateWithFlags");
@@ -1516,7 +1527,7 @@ int mem_pass_join(MemPass &M, hipStream_t stream) {
   if (err == hipSuccess) err = hipEventRecord(done, M.aux);
   if (err == hipSuccess) err = hipStreamWaitEvent(stream, done, 0);
   if (done) (void)hipEventDestroy(done);
-  for (int k = 0; k < 2; ++k) {
+  for (int k = 0; k < kRecSets; ++k) {
     if (M.iv_done[k]) (void)hipEventDestroy(M.iv_done[k]);
     if (M.pk_done[k]) (void)hipEventDestroy(M.pk_done[k]);
   }
@@ -1542,9 +1553,9 @@ int memory_passes(const ss_gmg *g, MemPass &M, const uint8_t *Pc, const uint32_t
   const int64_t N = g->n_ops;
   for (int64_t j0 = 0; j0 < nb; j0 += M.sub, ++M.it) {
     const int64_t nj = std::min(M.sub, nb - j0);
-    const int set = (int)(M.it & 1);
+    const int set = (int)(M.it % kRecSets);
     hipError_t err = hipSuccess;
-    if (M.it >= 2) err = hipStreamWaitEvent(stream, M.pk_done[set], 0);  // its buffers are free again
+    if (M.it >= kRecSets) err = hipStreamWaitEvent(stream, M.pk_done[set], 0);  // its buffers are free again
     if (err != hipSuccess) return hip_fail(err, "hipStreamWaitEvent");
     uint16_t *rank = given_ranks ? M.rank + j0 * N : M.rank;
     const void *fn = M.iv_fast ? (given_ranks ? reinterpret_cast<const void *>(&fast_intervals<true, true>)
@@ -1649,7 +1660,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   const size_t sz_tk = align((size_t)n_ticket * 4);
   void *scratch = nullptr;
   err = ss_pool_malloc(&scratch,
-                               sz_pt + 2 * sz_fin + 2 * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
+                               sz_pt + 2 * sz_fin + kRecSets * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
                                g->pool, stream);
   if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
@@ -1662,7 +1673,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   auto *finT = reinterpret_cast<uint32_t *>(take(sz_fin));
   auto *fin = reinterpret_cast<uint32_t *>(take(sz_fin));
   MemPass M{};
-  for (int k = 0; k < 2; ++k) {
+  for (int k = 0; k < kRecSets; ++k) {
     M.own[k] = reinterpret_cast<Rec *>(take(sz_own));
     M.cp[k] = reinterpret_cast<Rec *>(take(sz_cp));
     M.meta[k] = reinterpret_cast<int32_t *>(take(sz_meta));
@@ -1701,7 +1712,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
     ss_timing_stop(tp, stream);
     if (!check("transpose launch")) break;
     if (M.it > 0) {  // the schedule runs with no peak pass beside it
-      const hipError_t we = hipStreamWaitEvent(stream, M.pk_done[(M.it - 1) & 1], 0);
+      const hipError_t we = hipStreamWaitEvent(stream, M.pk_done[(M.it - 1) % kRecSets], 0);
       if (we != hipSuccess && rc == SS_OK) rc = hip_fail(we, "hipStreamWaitEvent");
     }
     SsTimingRec *ts = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
@@ -1780,7 +1791,7 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   const size_t sz_tk = align((size_t)n_ticket * 4);
   void *scratch = nullptr;
   err = ss_pool_malloc(
-      &scratch, sz_fin + sz_rank + sz_miss + sz_spill + 2 * (sz_own + sz_cp + sz_meta) + sz_wk + sz_wb + sz_tk, g->pool,
+      &scratch, sz_fin + sz_rank + sz_miss + sz_spill + kRecSets * (sz_own + sz_cp + sz_meta) + sz_wk + sz_wb + sz_tk, g->pool,
       stream);
   if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
@@ -1794,7 +1805,7 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   auto *miss = reinterpret_cast<uint16_t *>(take(sz_miss));
   auto *spill = reinterpret_cast<uint64_t *>(take(sz_spill));
   MemPass M{};
-  for (int k = 0; k < 2; ++k) {
+  for (int k = 0; k < kRecSets; ++k) {
     M.own[k] = reinterpret_cast<Rec *>(take(sz_own));
     M.cp[k] = reinterpret_cast<Rec *>(take(sz_cp));
     M.meta[k] = reinterpret_cast<int32_t *>(take(sz_meta));
@@ -1876,7 +1887,7 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
   const int64_t n_ticket = n_chunk * ((chunk + sub - 1) / sub);
   const size_t sz_tk = align((size_t)n_ticket * 4);
   void *scratch = nullptr;
-  err = ss_pool_malloc(&scratch, sz_fin + 2 * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
+  err = ss_pool_malloc(&scratch, sz_fin + kRecSets * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
                                g->pool, stream);
   if (err != hipSuccess) return hip_fail(err, "allocating the memory-pass scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
@@ -1887,7 +1898,7 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
   };
   auto *fin = reinterpret_cast<uint32_t *>(take(sz_fin));
   MemPass M{};
-  for (int k = 0; k < 2; ++k) {
+  for (int k = 0; k < kRecSets; ++k) {
     M.own[k] = reinterpret_cast<Rec *>(take(sz_own));
     M.cp[k] = reinterpret_cast<Rec *>(take(sz_cp));
     M.meta[k] = reinterpret_cast<int32_t *>(take(sz_meta));
