@@ -249,7 +249,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     std::vector<uint64_t> src_keys;
     if (time32)
       for (const int32_t v : src_ops) src_keys.push_back((uint64_t)d->release[d->op_req[v]] << 16 | (uint64_t)v);
-    int32_t lsame = 0;
+    int32_t lsame = 0, lshift = -1;
     int64_t lut_nb = 0, lut_shift = 0;
     int64_t max_outdeg = 0;
     for (int64_t v = 0; v < N; ++v) max_outdeg = std::max<int64_t>(max_outdeg, outdeg[v]);
@@ -311,6 +311,11 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
           if (ok) {
             lgrp = grp;
             lsame = same;
+            for (int s = 0; s < 8 && lshift < 0; ++s) {
+              bool pow2 = true;
+              for (int64_t a = 0; a < D && pow2; ++a) pow2 = grp[a] == (a >> s);
+              if (pow2) lshift = s;
+            }
           }
         }
         lbits.assign((size_t)D * lwords, 0u);
@@ -440,6 +445,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     V.src_ops = reinterpret_cast<const int32_t *>(base + o_src_ops);
     V.n_src = (int32_t)src_ops.size();
     V.link_same = lsame;
+    V.link_shift = lshift;
     V.lut_k = reinterpret_cast<const uint32_t *>(base + o_lutk);
     V.lut_w = reinterpret_cast<const uint4 *>(base + o_lutw);
     V.lut_nb = (int32_t)lut_nb;

@@ -138,19 +138,22 @@ struct SchedPipe {
   uint32_t pf[4][kPipePre];      // predecessor finish times (raw loads)
   uint32_t pd[4][kPipePre];      // predecessor devices (raw loads)
   uint32_t lc[4][kPipePre];      // link class between predecessor and target device
+  uint32_t xf[4][kPipePre];      // with device groups: transfer time to the target device
   uint32_t wq[4];                // duration on the target device
   uint32_t le[4];                // time -> slice lookup entry at a lower bound of the op's finish
   uint4 lw[4];                   // its {begin, end} of slices lk and lk+1
 };
 // kLink: 0 = link classes from device groups (LDS), 1 = bit table (two
-// classes), 2 = byte table (more classes).
-template <int kLink, bool kOverflow>
+// classes), 2 = byte table (more classes), 3 = device groups of 2^s
+// consecutive devices (group = device >> s).  With groups (0, 3) stage T-2
+// computes each predecessor's transfer time itself.
+template <int kLink, bool kOverflow, bool kOneClass>
 __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const uint8_t *__restrict__ PT, int64_t nb,
                                                        uint32_t *__restrict__ finT, int64_t *__restrict__ makespan,
                                                        int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
                                                        uint8_t *__restrict__ violation) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
-  const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = G.n_class, K = G.n_link;
+  const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = kOneClass ? 1 : G.n_class, K = G.n_link;
   const int lane = threadIdx.x;
   uint32_t *clk = reinterpret_cast<uint32_t *>(lds_raw);                  // [D][64]
   uint32_t *comp = clk + (size_t)D * kWave;                               // [R][64]
@@ -162,7 +165,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     if (d < D) dcls[d] = G.dev_class[d];
     if (kLink == 0 && d < D) lgrp[d] = G.link_grp[d];
   }
-  const uint32_t lsame = (uint32_t)G.link_same;
+  const uint32_t lsame = (uint32_t)G.link_same, lshift = (uint32_t)max(G.link_shift, 0);
+  constexpr bool kGroups = kLink == 0 || kLink == 3;
   __syncthreads();
   // Every lane runs (readlane needs the field blocks loaded in all lanes); a
   // lane past the batch end shadows the last candidate, computing and storing
@@ -228,13 +232,14 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     // lower bound of op t's finish: its release, the predecessors finished by
     // now (op t-1 is not) with the cheaper link class, the device clock now
     uint32_t lb = meta(kMetaRel, t);
-    const uint32_t gdt = kLink == 0 ? (uint32_t)lgrp[dt] : 0u;
+    const uint32_t gdt = kLink == 0 ? (uint32_t)lgrp[dt] : kLink == 3 ? dt >> lshift : 0u;
 #pragma unroll
     for (int i = 0; i < kPipePre; ++i) {
       const int u = (int)pred_of(p01, i);
       const uint32_t du = u == T + 1 ? clampD(S.dq[q1]) : u == T ? h1d : u == T - 1 ? h2d : clampD(S.pd[q2][i]);
       uint32_t lc;
       if (kLink == 0) lc = (uint32_t)lgrp[du] == gdt ? lsame : 1u - lsame;
+      else if (kLink == 3) lc = du >> lshift == gdt ? lsame : 1u - lsame;
       else if (kLink == 1) lc = link_bit(G, du, dt);  // zero with one class
       else lc = G.link_class[du * D + dt];
       S.lc[q2][i] = lc;
@@ -246,11 +251,13 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
       // transfer time in the bound: exact with device groups, else the
       // cheapest class (the fields hold classes 0 and 1), else none
       const uint32_t x0 = meta(kMetaX + 2 * i, t), x1 = meta(kMetaX + 2 * i + 1, t);
-      const uint32_t xm = kLink == 0 ? (lc ? x1 : x0) : kLink == 1 ? min(x0, x1) : 0u;
-      lb = ((uint32_t)i < np && u != T + 1) ? umax32(lb, fu + (du != dt ? xm : 0u)) : lb;
+      const uint32_t xm = kGroups ? (lc ? x1 : x0) : kLink == 1 ? min(x0, x1) : 0u;
+      const uint32_t xe = du != dt ? xm : 0u;
+      if (kGroups) S.xf[q2][i] = xe;  // exact
+      lb = ((uint32_t)i < np && u != T + 1) ? umax32(lb, fu + xe) : lb;
     }
-    S.wq[q2] = G.dur32[(int64_t)t * C + dcls[dt]];
-    lb = umax32(lb, clk[(int)dt * kWave + lane]) + (C == 1 ? meta(kMetaDur, t) : 0u);
+    S.wq[q2] = kOneClass ? meta(kMetaDur, t) : G.dur32[(int64_t)t * C + dcls[dt]];
+    lb = umax32(lb, clk[(int)dt * kWave + lane]) + (kOneClass ? meta(kMetaDur, t) : 0u);
     const uint32_t e = dt * (uint32_t)G.lut_nb + (uint32_t)min((int)(lb >> G.lut_shift), G.lut_nb - 1);
     S.le[q2] = e;
     S.lw[q2] = G.lut_w[e];
@@ -294,13 +301,15 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
       const uint32_t tt = u == T - 1 ? h1f : S.pf[q0][i];
       const uint32_t du = S.pd[q0][i];
       uint32_t x;
-      if (kLink == 2) {
+      if (kGroups) {
+        x = S.xf[q0][i];  // zero on the same device
+      } else if (kLink == 2) {
         x = G.xfer32[(int64_t)(u < T ? u : 0) * K + S.lc[q0][i]];
       } else {
         const uint32_t x0 = meta(kMetaX + 2 * i, T), x1 = meta(kMetaX + 2 * i + 1, T);
         x = S.lc[q0][i] ? x1 : x0;
       }
-      const uint32_t a = tt + (du != d ? x : 0u);
+      const uint32_t a = tt + (kGroups || du != d ? x : 0u);
       ready = (uint32_t)i < np ? umax32(ready, a) : ready;
     }
     if (kOverflow && np > (uint32_t)kPipePre) {  // predecessors past the pipelined ones
@@ -1479,6 +1488,15 @@ __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0,
   }
 }
 
+template <int kLink>
+const void *schedule_fn(bool overflow, bool one_class) {
+  if (overflow)
+    return one_class ? reinterpret_cast<const void *>(&fast_schedule<kLink, true, true>)
+                     : reinterpret_cast<const void *>(&fast_schedule<kLink, true, false>);
+  return one_class ? reinterpret_cast<const void *>(&fast_schedule<kLink, false, true>)
+                   : reinterpret_cast<const void *>(&fast_schedule<kLink, false, false>);
+}
+
 int hip_fail(hipError_t err, const char *what) {
   return ss_set_error(err == hipErrorOutOfMemory ? SS_ERR_OOM : SS_ERR_DEVICE,
                       std::string(what) + ": " + hipGetErrorString(err));
@@ -1611,13 +1629,13 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   // kernel variant: link classes from device groups, a bit table or (more
   // than two classes) xfer32; in-degrees above the pipelined count go
   // through the predecessor CSR
-  const int link_mode = G.link_grp ? 0 : g->n_link <= 2 ? 1 : 2;
+  const int link_mode = G.link_shift >= 0 ? 3 : G.link_grp ? 0 : g->n_link <= 2 ? 1 : 2;
   const bool overflow = g->max_indeg > kPipePre;
-  const void *const sched_fns[3][2] = {
-      {reinterpret_cast<const void *>(&fast_schedule<0, false>), reinterpret_cast<const void *>(&fast_schedule<0, true>)},
-      {reinterpret_cast<const void *>(&fast_schedule<1, false>), reinterpret_cast<const void *>(&fast_schedule<1, true>)},
-      {reinterpret_cast<const void *>(&fast_schedule<2, false>), reinterpret_cast<const void *>(&fast_schedule<2, true>)}};
-  const void *sched_fn = sched_fns[link_mode][overflow ? 1 : 0];
+  const bool one_class = g->n_class == 1;
+  const void *const sched_fn = link_mode == 0   ? schedule_fn<0>(overflow, one_class)
+                               : link_mode == 1 ? schedule_fn<1>(overflow, one_class)
+                               : link_mode == 2 ? schedule_fn<2>(overflow, one_class)
+                                                : schedule_fn<3>(overflow, one_class);
   err = hipFuncSetAttribute(sched_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
   if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
 

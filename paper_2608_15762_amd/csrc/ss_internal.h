@@ -43,6 +43,9 @@ struct GmgView {
   // device and the class of a same-group pair; null otherwise
   const uint8_t *link_grp;
   int32_t link_same;
+  // with such groups: s when device a's group is a >> s (contiguous groups of
+  // 2^s devices), else -1
+  int32_t link_shift;
   const uint32_t *bytes32;  // out_bytes as u32
   // first two successors of each op as u16 (0xFFFF: none), when no op has more
   const uint32_t *succ2;

@@ -115,6 +115,31 @@ def test_fast_writer_parity(dev, path, seed):
     assert_same(got, ref, label=f"fast writer {seed}")
 
 
+# Link classes that follow device groups, as the schedule kernel reads them:
+# contiguous groups of 2^s devices (group = device >> s), contiguous groups of
+# another size, interleaved groups (both from a per-device group table), groups
+# whose same-group class is 1, and a single group.
+GROUPS = [([0, 0, 0, 0, 1, 1, 1, 1], 0), ([0, 0, 0, 1, 1, 1], 0), ([0, 1, 0, 1, 0, 1, 0, 1], 0),
+          ([0, 0, 1, 1, 2, 2, 3, 3], 1), ([0] * 8, 0)]
+
+
+@pytest.mark.parametrize("case", range(len(GROUPS)))
+def test_device_group_links(dev, path, case):
+    grp, same = GROUPS[case]
+    D = len(grp)
+    print(f"device groups {grp}, same-group class {same}", flush=True)
+    g = synth.random_gmg(300 + case, n_ops=150, n_dev=D, n_req=2, n_slices=3, n_link=2, cap_scale=3000, lat_max=9)
+    g.link_class = np.array([[0 if a == b else (same if grp[a] == grp[b] else 1 - same) for b in range(D)]
+                             for a in range(D)], np.uint8)
+    st = synth.Stream(case + 4242)
+    B = 200
+    P = np.array([[st.uniform_int(0, D - 1) for _ in range(g.n_ops)] for _ in range(B)], np.uint8)
+    P[1::5] = np.repeat(np.arange(D, dtype=np.uint8), (g.n_ops + D - 1) // D)[:g.n_ops]  # runs per device
+    ref = oracle.simulate_batch(g, P)
+    got = gpu_run(ss.Gmg(g), P, dev)
+    assert_same(got, ref, label=f"device groups {case}")
+
+
 def test_nullable_outputs_and_empty_batch(dev, path):
     g = synth.build_gmg(0)
     h = ss.Gmg(g)
