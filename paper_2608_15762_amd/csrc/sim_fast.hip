@@ -768,8 +768,10 @@ constexpr int kOwnShift = 1, kOwnRecs = 1 << kOwnShift;
 constexpr int kCpShift = 1, kCpRecs = 1 << kCpShift;
 
 // kGivenRanks: the rank table already holds every op's rank on its device
-// (dispatch order), pass A only counts.
-template <bool kFast, bool kGivenRanks>
+// (dispatch order), pass A only counts.  kShiftLinks (with kFast): link
+// classes follow contiguous device groups of 2^s devices, so a transfer's
+// class comes from the two device ids instead of the bit table.
+template <bool kFast, bool kGivenRanks, bool kShiftLinks>
 __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const uint8_t *__restrict__ P,
                                                         const uint32_t *__restrict__ fin, int64_t j0,
                                                         Rec *__restrict__ own_all, Rec *__restrict__ cp_all,
@@ -883,8 +885,13 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       const uint32_t d = a.d, x0 = a.s2 & 0xFFFFu, x1 = a.s2 >> 16;
       const bool has0 = x0 != 0xFFFFu, has1 = x1 != 0xFFFFu;
       const bool loc0 = has0 && sc.dx0 == d, loc1 = has1 && sc.dx1 == d;
-      const uint32_t X0 = link_bit(G, d, sc.dx0) ? a.x1 : a.x0;  // transfer to each successor's device
-      const uint32_t X1 = link_bit(G, d, sc.dx1) ? a.x1 : a.x0;
+      auto link_of = [&](uint32_t u, uint32_t w) -> uint32_t {
+        if (!kShiftLinks) return link_bit(G, u, w);
+        const uint32_t s = (uint32_t)G.link_shift, same = (uint32_t)G.link_same;
+        return (u >> s) == (w >> s) ? same : 1u - same;
+      };
+      const uint32_t X0 = link_of(d, sc.dx0) ? a.x1 : a.x0;  // transfer to each successor's device
+      const uint32_t X1 = link_of(d, sc.dx1) ? a.x1 : a.x0;
       // own output: until the local consumer that finishes last
       uint32_t L = a.f, rl = a.rv, A = 0;
       rl = (loc0 && sc.fx0 > L) ? sc.rx0 : rl;
@@ -1576,10 +1583,14 @@ int memory_passes(const ss_gmg *g, MemPass &M, const uint8_t *Pc, const uint32_t
     if (M.it >= kRecSets) err = hipStreamWaitEvent(stream, M.pk_done[set], 0);  // its buffers are free again
     if (err != hipSuccess) return hip_fail(err, "hipStreamWaitEvent");
     uint16_t *rank = given_ranks ? M.rank + j0 * N : M.rank;
-    const void *fn = M.iv_fast ? (given_ranks ? reinterpret_cast<const void *>(&fast_intervals<true, true>)
-                                              : reinterpret_cast<const void *>(&fast_intervals<true, false>))
-                               : (given_ranks ? reinterpret_cast<const void *>(&fast_intervals<false, true>)
-                                              : reinterpret_cast<const void *>(&fast_intervals<false, false>));
+    const bool shift = G.link_shift >= 0;
+    const void *fn =
+        M.iv_fast ? (given_ranks ? (shift ? reinterpret_cast<const void *>(&fast_intervals<true, true, true>)
+                                          : reinterpret_cast<const void *>(&fast_intervals<true, true, false>))
+                                 : (shift ? reinterpret_cast<const void *>(&fast_intervals<true, false, true>)
+                                          : reinterpret_cast<const void *>(&fast_intervals<true, false, false>)))
+                  : (given_ranks ? reinterpret_cast<const void *>(&fast_intervals<false, true, false>)
+                                 : reinterpret_cast<const void *>(&fast_intervals<false, false, false>));
     const uint8_t *vi = violation;
     Rec *own = M.own[set], *cp = M.cp[set];
     int32_t *meta = M.meta[set];
