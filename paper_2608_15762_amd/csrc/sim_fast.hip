@@ -914,8 +914,8 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       if (kStage) {  // first position of each destination's run in this chunk
         q0 = *f0;
         q1 = *f1;
-        qo = act ? base[d] : 0;
-        if (act) atomicAdd(&base[d], 1);
+        qo = base[d];  // d is valid in every lane (inactive lanes repeat the last op)
+        atomicAdd(&base[d], act ? 1 : 0);
       }
       const int s0 = atomicAdd(f0, c0 ? 1 : 0);
       const int s1 = atomicAdd(f1, c1 ? 1 : 0);
@@ -935,7 +935,7 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       } else {
         wave_lds_fence();
         // each destination's positions in this chunk form one run [first, last]
-        const int eo = act ? base[d] - 1 : 0, bo = act ? own_off[d + 1] : 0;
+        const int eo = base[d] - 1, bo = own_off[d + 1];
         const int e0 = *f0 - 1, e1 = *f1 - 1;
         const int ko = act ? line_role<kOwnShift>(po, qo, eo, bo) : kRoleNone;
         const int k0 = c0 ? line_role<kCpShift>(s0, q0, e0, INT_MAX) : kRoleNone;
@@ -956,10 +956,12 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
         const int nq = fqn, nc = fcn;
         for (int qb = 0; qb < nq; qb += kWave / kOwnRecs) {
           const int qi = qb + (lane >> kOwnShift), part = lane & (kOwnRecs - 1);
-          if (qi < nq) {
+          if (qi < nq) {  // bounds and record read together; a slot outside the bucket goes to the spare
             const uint32_t ent = fq[qi];
             const int dv = (int)(ent >> 20), pos = (int)(ent & 0xFFFFFu) * kOwnRecs + part;
-            if (pos >= own_off[dv] && pos < own_off[dv + 1]) own[pos] = obuf[dv * kOwnRecs + part];
+            const int lo = own_off[dv], hi = own_off[dv + 1];
+            const Rec r = obuf[dv * kOwnRecs + part];
+            own[(pos >= lo) & (pos < hi) ? pos : N] = r;
           }
         }
         for (int qb = 0; qb < nc; qb += kWave / kCpRecs) {
@@ -967,7 +969,9 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
           if (qi < nc) {
             const uint32_t ent = fc[qi];
             const int dv = (int)(ent >> 20), pos = (int)(ent & 0xFFFFFu) * kCpRecs + part;
-            if (pos >= cp_off[dv]) cp[pos] = cbuf[dv * kCpRecs + part];
+            const int lo = cp_off[dv];
+            const Rec r = cbuf[dv * kCpRecs + part];
+            cp[pos >= lo ? pos : E] = r;
           }
         }
         wave_lds_fence();
