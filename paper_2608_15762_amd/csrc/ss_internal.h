@@ -108,8 +108,19 @@ inline size_t ss_pool_round(size_t x) {
   const size_t base = size_t(1) << k, q = base >> 2;
   return base + ((x - base + q - 1) / q) * q;
 }
+// On running out of memory the pool first gives back the blocks it keeps from
+// earlier calls (a block cached for one size is not reused for another), once
+// the stream's earlier frees have completed, and the allocation is retried once.
 inline hipError_t ss_pool_malloc(void **p, size_t bytes, hipMemPool_t pool, hipStream_t stream) {
-  return hipMallocFromPoolAsync(p, ss_pool_round(bytes), pool, stream);
+  const size_t n = ss_pool_round(bytes);
+  hipError_t e = hipMallocFromPoolAsync(p, n, pool, stream);
+  if (e == hipErrorOutOfMemory) {
+    (void)hipGetLastError();
+    if (hipStreamSynchronize(stream) == hipSuccess && hipMemPoolTrimTo(pool, 0) == hipSuccess)
+      e = hipMallocFromPoolAsync(p, n, pool, stream);
+    if (e != hipSuccess) (void)hipGetLastError();
+  }
+  return e;
 }
 // A buffer from the device's pool, ready for use on any stream when it returns
 // (allocated on `stream`, which is synchronised), and its release.
