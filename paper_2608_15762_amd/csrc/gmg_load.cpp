@@ -39,6 +39,34 @@ constexpr int kMaxDevices = 256;
 std::mutex g_pool_mu;
 hipMemPool_t g_pools[kMaxDevices] = {};
 hipStream_t g_aux[kMaxDevices] = {};
+
+// Idle scratch blocks per device, each with the event that marks its last use.
+struct IdleScratch {
+  void *p;
+  size_t bytes;
+  hipEvent_t last_use;
+};
+constexpr size_t kIdleBlocks = 4;
+std::mutex g_scratch_mu;
+std::vector<IdleScratch> g_idle[kMaxDevices];
+
+// Frees a block after its last use, in `stream`'s order.
+void free_after(const IdleScratch &b, hipStream_t stream) {
+  (void)hipStreamWaitEvent(stream, b.last_use, 0);
+  (void)hipFreeAsync(b.p, stream);
+  (void)hipEventDestroy(b.last_use);
+}
+
+// Gives every idle scratch block of the device back to the pool (in
+// `stream`'s order).
+void drop_idle(int device, hipStream_t stream) {
+  std::vector<IdleScratch> v;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    v.swap(g_idle[device]);
+  }
+  for (const IdleScratch &b : v) free_after(b, stream);
+}
 }  // namespace
 
 hipStream_t ss_device_aux(int device) {
@@ -88,6 +116,96 @@ hipMemPool_t ss_device_pool(int device) {
   return pool;
 }
 
+hipError_t ss_pool_malloc(void **p, size_t bytes, hipMemPool_t pool, hipStream_t stream) {
+  const size_t n = ss_pool_round(bytes);
+  hipError_t e = hipMallocFromPoolAsync(p, n, pool, stream);
+  if (e != hipErrorOutOfMemory) return e;
+  (void)hipGetLastError();
+  int device = -1;
+  {
+    std::lock_guard<std::mutex> lock(g_pool_mu);
+    for (int d = 0; d < kMaxDevices && device < 0; ++d)
+      if (g_pools[d] == pool) device = d;
+  }
+  if (device >= 0) drop_idle(device, stream);
+  if (hipStreamSynchronize(stream) == hipSuccess && hipMemPoolTrimTo(pool, 0) == hipSuccess)
+    e = hipMallocFromPoolAsync(p, n, pool, stream);
+  if (e != hipSuccess) (void)hipGetLastError();
+  return e;
+}
+
+hipError_t ss_scratch_get(int device, hipMemPool_t pool, size_t bytes, hipStream_t stream, SsScratch *s) {
+  s->p = nullptr;
+  s->bytes = 0;
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  IdleScratch b{};
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    std::vector<IdleScratch> &v = g_idle[device];
+    int best = -1;
+    for (int i = 0; i < (int)v.size(); ++i)
+      if (v[i].bytes >= bytes && (best < 0 || v[i].bytes < v[best].bytes)) best = i;
+    if (best >= 0) {
+      b = v[best];
+      v.erase(v.begin() + best);
+    }
+  }
+  if (b.p) {
+    const hipError_t e = hipStreamWaitEvent(stream, b.last_use, 0);
+    if (e != hipSuccess) {
+      free_after(b, stream);
+      return e;
+    }
+    (void)hipEventDestroy(b.last_use);
+    s->p = b.p;
+    s->bytes = b.bytes;
+    return hipSuccess;
+  }
+  // a quarter of headroom, so a slowly growing size finds its block again;
+  // the exact size when that does not fit
+  const size_t roomy = ss_pool_round(bytes + bytes / 4);
+  hipError_t e = hipMallocFromPoolAsync(&s->p, roomy, pool, stream);
+  if (e == hipSuccess) {
+    s->bytes = roomy;
+    return e;
+  }
+  (void)hipGetLastError();
+  s->p = nullptr;
+  e = ss_pool_malloc(&s->p, bytes, pool, stream);
+  if (e == hipSuccess) s->bytes = ss_pool_round(bytes);
+  else s->p = nullptr;
+  return e;
+}
+
+hipError_t ss_scratch_put(int device, SsScratch *s, hipStream_t stream) {
+  if (!s->p) return hipSuccess;
+  IdleScratch b{s->p, s->bytes, nullptr};
+  s->p = nullptr;
+  s->bytes = 0;
+  hipError_t e = hipEventCreateWithFlags(&b.last_use, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventRecord(b.last_use, stream);
+  if (e != hipSuccess || device < 0 || device >= kMaxDevices) {
+    if (b.last_use) (void)hipEventDestroy(b.last_use);
+    const hipError_t f = hipFreeAsync(b.p, stream);
+    return e != hipSuccess ? e : f;
+  }
+  IdleScratch out{};
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    std::vector<IdleScratch> &v = g_idle[device];
+    v.push_back(b);
+    if (v.size() > kIdleBlocks) {
+      size_t k = 0;
+      for (size_t i = 1; i < v.size(); ++i)
+        if (v[i].bytes < v[k].bytes) k = i;
+      out = v[k];
+      v.erase(v.begin() + (ptrdiff_t)k);
+    }
+  }
+  if (out.p) free_after(out, stream);
+  return hipSuccess;
+}
+
 int ss_pool_alloc(int device, size_t bytes, hipStream_t stream, void **out) {
   *out = nullptr;
   hipMemPool_t pool = ss_device_pool(device);
@@ -117,6 +235,10 @@ extern "C" int ss_release_cached_memory(void) {
     if (!g_pools[d]) continue;
     hipError_t e = hipSetDevice(d);
     if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e == hipSuccess && g_aux[d]) {
+      drop_idle(d, g_aux[d]);
+      e = hipStreamSynchronize(g_aux[d]);
+    }
     if (e == hipSuccess) e = hipMemPoolTrimTo(g_pools[d], 0);
     if (e != hipSuccess && rc == SS_OK)
       rc = ss_set_error(SS_ERR_DEVICE, std::string("trimming a scratch pool: ") + hipGetErrorString(e));

@@ -1691,10 +1691,11 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
   const int64_t n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
   const size_t sz_tk = align((size_t)n_ticket * 4);
-  void *scratch = nullptr;
-  err = ss_pool_malloc(&scratch,
-                               sz_pt + 2 * sz_fin + kRecSets * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
-                               g->pool, stream);
+  SsScratch scr;
+  err = ss_scratch_get(g->device, g->pool,
+                       sz_pt + 2 * sz_fin + kRecSets * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
+                       stream, &scr);
+  void *scratch = scr.p;
   if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
   auto take = [&](size_t bytes) {
@@ -1775,8 +1776,8 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   }
   const int jrc = mem_pass_join(M, stream);
   if (rc == SS_OK) rc = jrc;
-  err = hipFreeAsync(scratch, stream);
-  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
+  err = ss_scratch_put(g->device, &scr, stream);
+  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "releasing the scratch");
   return rc;
 }
 
@@ -1822,10 +1823,11 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
   const int64_t n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
   const size_t sz_tk = align((size_t)n_ticket * 4);
-  void *scratch = nullptr;
-  err = ss_pool_malloc(
-      &scratch, sz_fin + sz_rank + sz_miss + sz_spill + kRecSets * (sz_own + sz_cp + sz_meta) + sz_wk + sz_wb + sz_tk, g->pool,
-      stream);
+  SsScratch scr;
+  err = ss_scratch_get(g->device, g->pool,
+                       sz_fin + sz_rank + sz_miss + sz_spill + kRecSets * (sz_own + sz_cp + sz_meta) + sz_wk + sz_wb + sz_tk,
+                       stream, &scr);
+  void *scratch = scr.p;
   if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
   auto take = [&](size_t bytes) {
@@ -1878,8 +1880,8 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   }
   const int jrc = mem_pass_join(M, stream);
   if (rc == SS_OK) rc = jrc;
-  err = hipFreeAsync(scratch, stream);
-  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
+  err = ss_scratch_put(g->device, &scr, stream);
+  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "releasing the scratch");
   return rc;
 }
 
@@ -1919,9 +1921,11 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
   const int64_t n_chunk = (B + chunk - 1) / chunk;
   const int64_t n_ticket = n_chunk * ((chunk + sub - 1) / sub);
   const size_t sz_tk = align((size_t)n_ticket * 4);
-  void *scratch = nullptr;
-  err = ss_pool_malloc(&scratch, sz_fin + kRecSets * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
-                               g->pool, stream);
+  SsScratch scr;
+  err = ss_scratch_get(g->device, g->pool,
+                       sz_fin + kRecSets * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
+                       stream, &scr);
+  void *scratch = scr.p;
   if (err != hipSuccess) return hip_fail(err, "allocating the memory-pass scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
   auto take = [&](size_t bytes) {
@@ -1966,7 +1970,7 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
   }
   const int jrc = mem_pass_join(M, stream);
   if (rc == SS_OK) rc = jrc;
-  err = hipFreeAsync(scratch, stream);
-  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
+  err = ss_scratch_put(g->device, &scr, stream);
+  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "releasing the scratch");
   return rc;
 }

@@ -731,11 +731,11 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
   const size_t sz_arr = ports ? align((size_t)E * chunk * 8 + 8) : 0;
   const bool resumed = from && from->k > 0;
   const size_t sz_bad = resumed ? align((size_t)chunk * 4) : 0;
-  void *scratch = nullptr;
-  err = ss_pool_malloc(&scratch,
-                               sz_fin + sz_comp + sz_miss + sz_spr + sz_spo + sz_bydev + 2 * sz_ev + sz_port + sz_arr +
-                                   sz_bad,
-                               g->pool, stream);
+  SsScratch scr;
+  err = ss_scratch_get(g->device, g->pool,
+                       sz_fin + sz_comp + sz_miss + sz_spr + sz_spo + sz_bydev + 2 * sz_ev + sz_port + sz_arr + sz_bad,
+                       stream, &scr);
+  void *scratch = scr.p;
   if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
   auto take = [&](size_t bytes) {
@@ -822,8 +822,8 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
     ss_timing_stop(t_mem, stream);
     if (err != hipSuccess) rc = hip_fail(err, "memory_kernel launch");
   }
-  err = hipFreeAsync(scratch, stream);
-  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
+  err = ss_scratch_put(g->device, &scr, stream);
+  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "releasing the scratch");
   return rc;
 }
 

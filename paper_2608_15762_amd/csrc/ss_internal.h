@@ -108,20 +108,28 @@ inline size_t ss_pool_round(size_t x) {
   const size_t base = size_t(1) << k, q = base >> 2;
   return base + ((x - base + q - 1) / q) * q;
 }
-// On running out of memory the pool first gives back the blocks it keeps from
-// earlier calls (a block cached for one size is not reused for another), once
-// the stream's earlier frees have completed, and the allocation is retried once.
-inline hipError_t ss_pool_malloc(void **p, size_t bytes, hipMemPool_t pool, hipStream_t stream) {
-  const size_t n = ss_pool_round(bytes);
-  hipError_t e = hipMallocFromPoolAsync(p, n, pool, stream);
-  if (e == hipErrorOutOfMemory) {
-    (void)hipGetLastError();
-    if (hipStreamSynchronize(stream) == hipSuccess && hipMemPoolTrimTo(pool, 0) == hipSuccess)
-      e = hipMallocFromPoolAsync(p, n, pool, stream);
-    if (e != hipSuccess) (void)hipGetLastError();
-  }
-  return e;
-}
+// A block from `pool` on `stream`, its size rounded by ss_pool_round.  On
+// running out of memory the device's idle scratch blocks and the pool's unused
+// memory are given back (once the stream's earlier work has completed) and the
+// allocation is retried once.
+hipError_t ss_pool_malloc(void **p, size_t bytes, hipMemPool_t pool, hipStream_t stream);
+
+// Per-call scratch.  Repeated calls whose sizes vary (the rounds of the
+// incremental loop grow their graph op by op) would otherwise allocate from
+// the pool at almost every call, and the runtime's pool stalls for up to
+// seconds on such churn.  ss_scratch_get takes the smallest idle block of the
+// device that holds `bytes` (the calling stream first waits for the block's
+// last use), else a new block from the pool with a quarter of headroom;
+// ss_scratch_put returns it as idle, marked by an event on `stream`, and
+// frees the device's smallest idle block to the pool when more than four are
+// idle.  Idle blocks stay until ss_release_cached_memory or an allocation
+// that runs out of memory.
+struct SsScratch {
+  void *p = nullptr;
+  size_t bytes = 0;
+};
+hipError_t ss_scratch_get(int device, hipMemPool_t pool, size_t bytes, hipStream_t stream, SsScratch *s);
+hipError_t ss_scratch_put(int device, SsScratch *s, hipStream_t stream);
 // A buffer from the device's pool, ready for use on any stream when it returns
 // (allocated on `stream`, which is synchronised), and its release.
 int ss_pool_alloc(int device, size_t bytes, hipStream_t stream, void **out);
