@@ -391,12 +391,15 @@ int ss_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place);
  * The library takes every device buffer (staged GMGs, scratch, scheduler and
  * state buffers) from one stream-ordered memory pool per device that keeps
  * freed memory for later calls: handing large buffers back to the driver and
- * allocating again soon after stalls for up to seconds.  An allocation that
- * fails for lack of memory first returns that pool's unused memory (after
- * synchronising the calling stream) and is tried once more; only then does
- * the call fail with SS_ERR_OOM.  This call returns the pools' unused memory
- * to the driver (synchronising each device that has a pool first); buffers in
- * use stay.  Errors: SS_ERR_DEVICE.
+ * allocating again soon after stalls for up to seconds.  A simulation call's
+ * scratch is, in addition, kept as an idle block (at most four per device)
+ * that a later call on any stream reuses after the block's last use, so that
+ * calls whose sizes vary do not allocate each time.  An allocation that fails
+ * for lack of memory first returns the idle blocks and the pool's unused
+ * memory (after synchronising the calling stream) and is tried once more;
+ * only then does the call fail with SS_ERR_OOM.  This call returns the idle
+ * blocks and the pools' unused memory to the driver (synchronising each
+ * device that has a pool first); buffers in use stay.  Errors: SS_ERR_DEVICE.
  */
 int ss_release_cached_memory(void);
 

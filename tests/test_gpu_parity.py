@@ -140,6 +140,24 @@ def test_device_group_links(dev, path, case):
     assert_same(got, ref, label=f"device groups {case}")
 
 
+def test_scratch_reuse_across_streams(dev):
+    """Calls on two streams with no host synchronisation between them: the
+    smaller call on the second stream takes the first call's idle scratch
+    block, and may use it only after that call's work (its stream waits for
+    the block's last use); the third call reuses a block again."""
+    g = synth.build_gmg(2)
+    h = ss.Gmg(g)
+    rows = [synth.placements(g, 2, 0, 300), synth.placements(g, 2, 300, 120), synth.placements(g, 2, 420, 300)]
+    refs = [oracle.simulate_batch(g, P, n_threads=8) for P in rows]
+    ins = [torch.from_numpy(np.ascontiguousarray(P)).to(dev) for P in rows]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    outs = [ss.simulate_batch(h, P, stream=s) for P, s in zip(ins, (s1, s2, s1))]
+    torch.cuda.synchronize()
+    for i, (o, r) in enumerate(zip(outs, refs)):
+        assert_same({k: (None if v is None else v.cpu().numpy()) for k, v in o.items()}, r, label=f"call {i}")
+
+
 def test_nullable_outputs_and_empty_batch(dev, path):
     g = synth.build_gmg(0)
     h = ss.Gmg(g)
