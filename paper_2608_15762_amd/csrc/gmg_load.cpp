@@ -359,7 +359,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     for (int64_t v = 0; v < N; ++v) max_bytes = std::max(max_bytes, d->out_bytes[v]);
     const bool time32 = horizon < (i128)UINT32_MAX && N <= 65535 && E <= 65535 && max_slices <= 65535 &&
                         max_bytes <= (int64_t)UINT32_MAX;
-    std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32, meta, lbits, bytes32, succ2, lutk, lutw;
+    std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32, meta, lbits, bytes32, succ2, succ2_pe, lutk, lutw;
     std::vector<uint8_t> lgrp;
     // ready-time dispatch: the ops without predecessors by (release of their
     // request, index); on the 32-bit path also as keys release << 16 | op
@@ -404,6 +404,14 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
             const uint32_t x = (uint32_t)succ_idx[succ_ptr[v] + q];
             succ2[v] = q == 0 ? (0xFFFF0000u | x) : ((succ2[v] & 0xFFFFu) | x << 16);
           }
+        if (E < 0xFFFF) {
+          succ2_pe.assign(N, 0xFFFFFFFFu);
+          for (int64_t v = 0; v < N; ++v)
+            for (int64_t q = 0; q < outdeg[v]; ++q) {
+              const uint32_t pe = (uint32_t)succ_pe[succ_ptr[v] + q];
+              succ2_pe[v] = q == 0 ? (0xFFFF0000u | pe) : ((succ2_pe[v] & 0xFFFFu) | pe << 16);
+            }
+        }
       }
       if (K <= 2) {
         // device groups: join devices linked by class `same`, then check that
@@ -500,7 +508,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     const size_t o_link = pk.add(d->link_class, D * D);
     const size_t o_dur32 = pk.add(dur32), o_xfer32 = pk.add(xfer32), o_sb32 = pk.add(sb32), o_se32 = pk.add(se32),
                  o_rel32 = pk.add(rel32), o_meta = pk.add(meta), o_lbits = pk.add(lbits), o_b32 = pk.add(bytes32),
-                 o_succ2 = pk.add(succ2), o_lutk = pk.add(lutk), o_lutw = pk.add(lutw), o_lgrp = pk.add(lgrp),
+                 o_succ2 = pk.add(succ2), o_succ2_pe = pk.add(succ2_pe), o_lutk = pk.add(lutk), o_lutw = pk.add(lutw), o_lgrp = pk.add(lgrp),
                  o_src = pk.add(src_keys), o_src_ops = pk.add(src_ops);
     pk.add(nullptr, 256);  // tail padding
 
@@ -562,6 +570,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     V.link_words = (int32_t)lwords;
     V.bytes32 = reinterpret_cast<const uint32_t *>(base + o_b32);
     V.succ2 = succ2.empty() ? nullptr : reinterpret_cast<const uint32_t *>(base + o_succ2);
+    V.succ2_pe = succ2_pe.empty() ? nullptr : reinterpret_cast<const uint32_t *>(base + o_succ2_pe);
     V.link_grp = lgrp.empty() ? nullptr : reinterpret_cast<const uint8_t *>(base + o_lgrp);
     V.src_keys = reinterpret_cast<const uint64_t *>(base + o_src);
     V.src_ops = reinterpret_cast<const int32_t *>(base + o_src_ops);

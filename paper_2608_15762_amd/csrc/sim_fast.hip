@@ -733,10 +733,10 @@ __device__ __forceinline__ int meta_stride(int D) { return 3 * (D + 1); }
 // op fields of chunk i+1 are in flight, and its successors' fields are
 // requested as soon as those arrive.
 struct IvOp {  // fields of the lane's op
-  uint32_t d, rv, f, b, w, s2, x0, x1;
+  uint32_t d, rv, f, b, w, s2, x0, x1, pe;
 };
-struct IvSucc {  // device, finish and rank of the first two successors
-  uint32_t dx0, dx1, fx0, fx1, rx0, rx1;
+struct IvSucc {  // device, finish and rank of the first two successors (with ports: their inputs' arrivals)
+  uint32_t dx0, dx1, fx0, fx1, rx0, rx1, ax0, ax1;
 };
 
 // Store staging.  A 64-byte line of a bucket holds the records of positions
@@ -770,13 +770,18 @@ constexpr int kCpShift = 1, kCpRecs = 1 << kCpShift;
 // kGivenRanks: the rank table already holds every op's rank on its device
 // (dispatch order), pass A only counts.  kShiftLinks (with kFast): link
 // classes follow contiguous device groups of 2^s devices, so a transfer's
-// class comes from the two device ids instead of the bit table.
-template <bool kFast, bool kGivenRanks, bool kShiftLinks>
+// class comes from the two device ids instead of the bit table.  kPorts (with
+// kFast, index ranks): transfers were arbitrated over device ports, and arr
+// holds every candidate's arrival per predecessor edge (rows of E, like fin):
+// an own output is kept until its last remote arrival, a copy is allocated at
+// its transfer's start (arrival minus estimate).
+template <bool kFast, bool kGivenRanks, bool kShiftLinks, bool kPorts>
 __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const uint8_t *__restrict__ P,
                                                         const uint32_t *__restrict__ fin, int64_t j0,
                                                         Rec *__restrict__ own_all, Rec *__restrict__ cp_all,
                                                         int32_t *__restrict__ meta, uint16_t *__restrict__ rank_all,
-                                                        const uint8_t *__restrict__ violation) {
+                                                        const uint8_t *__restrict__ violation,
+                                                        const uint32_t *__restrict__ arr) {
   // LDS (dynamic, sized by the device count): bucket offsets and fill
   // pointers; with staged stores (kFast with index ranks) also the open line of
   // every device's own bucket and the queue of complete lines
@@ -800,6 +805,7 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
   if (violation[c] & SS_VIOLATION_INVALID) return;
   const uint8_t *prow = P + c * N;
   const uint32_t *frow = fin + c * N;
+  const uint32_t *arow = kPorts ? arr + c * E : nullptr;
   uint16_t *rk = rank_all + j * N;
   Rec *own = own_all + j * own_stride(N);
   Rec *cp = cp_all + j * cp_stride(E);
@@ -867,12 +873,19 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       a.s2 = G.succ2[v];
       a.x0 = G.xfer32[v * K];
       a.x1 = G.xfer32[v * K + K - 1];
+      a.pe = kPorts ? G.succ2_pe[v] : 0u;
       return a;
     };
     auto load_succ = [&](const IvOp &a, int v) -> IvSucc {
       const uint32_t x0 = a.s2 & 0xFFFFu, x1 = a.s2 >> 16;
       const int y0 = x0 == 0xFFFFu ? v : (int)x0, y1 = x1 == 0xFFFFu ? v : (int)x1;
-      return IvSucc{prow[y0], prow[y1], frow[y0], frow[y1], rk[y0], rk[y1]};
+      uint32_t ax0 = 0, ax1 = 0;
+      if (kPorts) {  // an absent successor reads edge 0 (E >= 1 when there is one), never used
+        const uint32_t e0 = a.pe & 0xFFFFu, e1 = a.pe >> 16;
+        ax0 = arow[e0 == 0xFFFFu ? 0u : e0];
+        ax1 = arow[e1 == 0xFFFFu ? 0u : e1];
+      }
+      return IvSucc{prow[y0], prow[y1], frow[y0], frow[y1], rk[y0], rk[y1], ax0, ax1};
     };
     nocopy[lane] = 0;
     int vq = min(lane, N - 1);
@@ -898,8 +911,11 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       L = (loc0 && sc.fx0 > L) ? sc.fx0 : L;
       rl = (loc1 && sc.fx1 > L) ? sc.rx1 : rl;
       L = (loc1 && sc.fx1 > L) ? sc.fx1 : L;
-      A = (has0 && !loc0) ? umax32(A, a.f + X0) : A;
-      A = (has1 && !loc1) ? umax32(A, a.f + X1) : A;
+      // arrival of each remote transfer (two successors on one remote device
+      // share the first one's transfer)
+      const uint32_t T0 = kPorts ? sc.ax0 : a.f + X0, T1 = kPorts ? sc.ax1 : a.f + X1;
+      A = (has0 && !loc0) ? umax32(A, T0) : A;
+      A = (has1 && !loc1) ? umax32(A, T1) : A;
       const bool arrive = A > L;
       const uint32_t F = !has0 ? kInf32 : arrive ? A : L;
       const uint32_t loc = !has0 ? 0u : arrive ? loc_window((int)a.rv + 1) : rl + 1;
@@ -924,8 +940,9 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       const bool late1 = same && sc.fx1 > sc.fx0;
       const uint32_t ry0 = late1 ? sc.rx1 : sc.rx0, hi0 = late1 ? sc.fx1 : sc.fx0;
       const uint32_t ra0 = same ? min(sc.rx0, sc.rx1) : sc.rx0;
-      const Rec r0 = Rec{a.f, hi0, a.b, (uint32_t)max((int)ra0 - 3, 0) << 16 | (ry0 + 1)};
-      const Rec r1 = Rec{a.f, sc.fx1, a.b, (uint32_t)max((int)sc.rx1 - 3, 0) << 16 | (sc.rx1 + 1)};
+      const uint32_t st0 = kPorts ? T0 - X0 : a.f, st1 = kPorts ? T1 - X1 : a.f;  // transfer starts
+      const Rec r0 = Rec{st0, hi0, a.b, (uint32_t)max((int)ra0 - 3, 0) << 16 | (ry0 + 1)};
+      const Rec r1 = Rec{st1, sc.fx1, a.b, (uint32_t)max((int)sc.rx1 - 3, 0) << 16 | (sc.rx1 + 1)};
       const uint32_t dx0 = sc.dx0, dx1 = sc.dx1;
       sc = load_succ(an, vn);  // the next chunk's successors, in flight during the stores
       if (!kStage) {
@@ -1576,8 +1593,12 @@ size_t intervals_lds(int D, bool stage) {
 
 // Residency intervals, then peaks, for the nb candidates of one chunk (their
 // placements Pc and finish-time rows fin), sub candidates at a time.
+// arr (rows of arrivals per predecessor edge, transfers arbitrated over
+// ports) is null in the latency model; with it, the branch-free writer with
+// index ranks is required.
 int memory_passes(const ss_gmg *g, MemPass &M, const uint8_t *Pc, const uint32_t *fin, int64_t nb,
-                  bool given_ranks, int64_t *peak, uint8_t *violation, hipStream_t stream) {
+                  bool given_ranks, int64_t *peak, uint8_t *violation, hipStream_t stream,
+                  const uint32_t *arr = nullptr) {
   const GmgView &G = g->view;
   const int64_t N = g->n_ops;
   for (int64_t j0 = 0; j0 < nb; j0 += M.sub, ++M.it) {
@@ -1587,19 +1608,24 @@ int memory_passes(const ss_gmg *g, MemPass &M, const uint8_t *Pc, const uint32_t
     if (M.it >= kRecSets) err = hipStreamWaitEvent(stream, M.pk_done[set], 0);  // its buffers are free again
     if (err != hipSuccess) return hip_fail(err, "hipStreamWaitEvent");
     uint16_t *rank = given_ranks ? M.rank + j0 * N : M.rank;
+    if (arr && (!M.iv_fast || given_ranks))
+      return ss_set_error(SS_ERR_UNSUPPORTED, "port arrivals need the branch-free interval writer");
     const bool shift = G.link_shift >= 0;
     const void *fn =
-        M.iv_fast ? (given_ranks ? (shift ? reinterpret_cast<const void *>(&fast_intervals<true, true, true>)
-                                          : reinterpret_cast<const void *>(&fast_intervals<true, true, false>))
-                                 : (shift ? reinterpret_cast<const void *>(&fast_intervals<true, false, true>)
-                                          : reinterpret_cast<const void *>(&fast_intervals<true, false, false>)))
-                  : (given_ranks ? reinterpret_cast<const void *>(&fast_intervals<false, true, false>)
-                                 : reinterpret_cast<const void *>(&fast_intervals<false, false, false>));
+        arr ? (shift ? reinterpret_cast<const void *>(&fast_intervals<true, false, true, true>)
+                     : reinterpret_cast<const void *>(&fast_intervals<true, false, false, true>))
+        : M.iv_fast
+            ? (given_ranks ? (shift ? reinterpret_cast<const void *>(&fast_intervals<true, true, true, false>)
+                                    : reinterpret_cast<const void *>(&fast_intervals<true, true, false, false>))
+                           : (shift ? reinterpret_cast<const void *>(&fast_intervals<true, false, true, false>)
+                                    : reinterpret_cast<const void *>(&fast_intervals<true, false, false, false>)))
+            : (given_ranks ? reinterpret_cast<const void *>(&fast_intervals<false, true, false, false>)
+                           : reinterpret_cast<const void *>(&fast_intervals<false, false, false, false>));
     const uint8_t *vi = violation;
     Rec *own = M.own[set], *cp = M.cp[set];
     int32_t *meta = M.meta[set];
     void *args[] = {const_cast<GmgView *>(&G), const_cast<uint8_t **>(&Pc), const_cast<uint32_t **>(&fin),
-                    &j0, &own, &cp, &meta, &rank, &vi};
+                    &j0, &own, &cp, &meta, &rank, &vi, const_cast<uint32_t **>(&arr)};
     // the branch-free writer with index ranks stages its stores
     const size_t lds = intervals_lds((int)g->n_dev, M.iv_fast && !given_ranks);
     err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -1890,6 +1916,25 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
 // finish times fin[B][N] (every time below 2^32, which the loader proved when
 // it enabled the 32-bit path).  Candidates already marked invalid are skipped.
 namespace {
+// Arrivals of one chunk, [edge][stride] int64 (candidate-minor, as the port
+// schedule writes them), to candidate rows [nb][E] of u32 through 64 x 64
+// LDS tiles (times fit 32 bits on this path).
+__global__ __launch_bounds__(256) void arrival_rows(const int64_t *__restrict__ arr, int64_t stride, int64_t E,
+                                                    int64_t nb, uint32_t *__restrict__ out) {
+  __shared__ uint32_t tile[64][65];
+  const int64_t c0 = (int64_t)blockIdx.x * 64, e0 = (int64_t)blockIdx.y * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int64_t e = e0 + i, c = c0 + tx;
+    if (e < E && c < nb) tile[i][tx] = (uint32_t)arr[e * stride + c];
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int64_t c = c0 + i, e = e0 + tx;
+    if (c < nb && e < E) out[c * E + e] = tile[tx][i];
+  }
+}
+
 __global__ __launch_bounds__(256) void narrow_times(const int64_t *__restrict__ in, int64_t n, uint32_t *__restrict__ out) {
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
     out[i] = (uint32_t)in[i];
@@ -1897,7 +1942,7 @@ __global__ __launch_bounds__(256) void narrow_times(const int64_t *__restrict__ 
 }  // namespace
 
 int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, int64_t B, int64_t *peak,
-                       uint8_t *violation, hipStream_t stream) {
+                       uint8_t *violation, hipStream_t stream, const int64_t *arr64, int64_t arr_stride) {
   const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev;
   if (!g->view.time32 || N == 0) return ss_set_error(SS_ERR_UNSUPPORTED, "the 32-bit memory passes need ops and a 32-bit horizon");
   if (B == 0) return SS_OK;
@@ -1905,9 +1950,12 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
   hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
   const bool iv_fast = g->n_class == 1 && g->n_link <= 2 && g->max_outdeg <= 2;
+  const bool ports = arr64 != nullptr && E > 0;
+  if (ports && (!iv_fast || !g->view.succ2_pe))
+    return ss_set_error(SS_ERR_UNSUPPORTED, "port arrivals need the branch-free interval writer");
   const int64_t rec_per_cand = (own_stride(N) + cp_stride(E)) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4 + N * 2;
   const int64_t sub = std::min<int64_t>(B, std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand)));
-  const int64_t chunk = std::min<int64_t>(B, std::max<int64_t>(1, kScratchBudget / (N * 4)));
+  const int64_t chunk = std::min<int64_t>(B, std::max<int64_t>(1, kScratchBudget / ((N + (ports ? E : 0)) * 4)));
   const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
   const int64_t slot_cap = N + E + 1;
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
@@ -1921,9 +1969,10 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
   const int64_t n_chunk = (B + chunk - 1) / chunk;
   const int64_t n_ticket = n_chunk * ((chunk + sub - 1) / sub);
   const size_t sz_tk = align((size_t)n_ticket * 4);
+  const size_t sz_arr = ports ? align((size_t)chunk * E * 4) : 0;
   SsScratch scr;
   err = ss_scratch_get(g->device, g->pool,
-                       sz_fin + kRecSets * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
+                       sz_fin + sz_arr + kRecSets * (sz_own + sz_cp + sz_meta) + sz_rank + sz_wk + sz_wb + sz_tk,
                        stream, &scr);
   void *scratch = scr.p;
   if (err != hipSuccess) return hip_fail(err, "allocating the memory-pass scratch");
@@ -1934,6 +1983,7 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
     return q;
   };
   auto *fin = reinterpret_cast<uint32_t *>(take(sz_fin));
+  auto *arr = ports ? reinterpret_cast<uint32_t *>(take(sz_arr)) : nullptr;
   MemPass M{};
   for (int k = 0; k < kRecSets; ++k) {
     M.own[k] = reinterpret_cast<Rec *>(take(sz_own));
@@ -1966,7 +2016,16 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
       rc = hip_fail(err, "narrow_times launch");
       break;
     }
-    rc = memory_passes(g, M, P + b0 * N, fin, nb, false, peak ? peak + b0 * D : nullptr, violation + b0, stream);
+    if (ports) {
+      const dim3 tg((unsigned)((nb + 63) / 64), (unsigned)((E + 63) / 64));
+      hipLaunchKernelGGL(arrival_rows, tg, dim3(256), 0, stream, arr64 + b0, arr_stride, E, nb, arr);
+      err = hipGetLastError();
+      if (err != hipSuccess) {
+        rc = hip_fail(err, "arrival_rows launch");
+        break;
+      }
+    }
+    rc = memory_passes(g, M, P + b0 * N, fin, nb, false, peak ? peak + b0 * D : nullptr, violation + b0, stream, arr);
   }
   const int jrc = mem_pass_join(M, stream);
   if (rc == SS_OK) rc = jrc;

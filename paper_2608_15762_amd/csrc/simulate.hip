@@ -808,8 +808,9 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
       break;
     }
     if (capture) continue;  // the state is all a capture needs
-    if (mem_fast) {
-      rc = ss_run_memory_fast(g, Pc, fin, nb, peak ? peak + b0 * D : nullptr, violation + b0, stream);
+    if (mem_fast) {  // with ports the arrivals, [edge][nb] for this chunk, go along
+      rc = ss_run_memory_fast(g, Pc, fin, nb, peak ? peak + b0 * D : nullptr, violation + b0, stream,
+                              ports ? static_cast<const int64_t *>(arr) : nullptr, nb);
       continue;
     }
     const int64_t grid = std::min<int64_t>(nb, nslots);
@@ -841,10 +842,16 @@ int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makes
   const char *path = std::getenv("SS_PATH");
   if (path && std::strcmp(path, "fast") == 0 && (!fast_ok || link_ports))
     return ss_set_error(SS_ERR_UNSUPPORTED, "SS_PATH=fast but this GMG or dispatch needs the general path");
-  // transfer ports run on the general kernels only
-  const bool generic = !fast_ok || link_ports || (path && std::strcmp(path, "generic") == 0);
+  // transfer ports run on the general schedule kernel; their memory pass is
+  // the 32-bit one when the GMG fits the branch-free interval writer (not
+  // with SS_PATH=generic)
+  const bool force_generic = path && std::strcmp(path, "generic") == 0;
+  const bool generic = !fast_ok || link_ports || force_generic;
+  const bool ports_mem_fast = link_ports && !force_generic && g->view.time32 && g->n_ops > 0 && g->n_class == 1 &&
+                              g->n_link <= 2 && g->max_outdeg <= 2 && g->view.succ2_pe;
   if (generic)
-    return run_simulate_generic(g, P, B, makespan, peak, violation, slack, sumfin, stream, ready_dispatch, link_ports);
+    return run_simulate_generic(g, P, B, makespan, peak, violation, slack, sumfin, stream, ready_dispatch, link_ports,
+                                nullptr, nullptr, ports_mem_fast);
   if (ready_dispatch) return ss_run_simulate_ready(g, P, B, makespan, peak, violation, slack, sumfin, stream);
   return ss_run_simulate_fast(g, P, B, makespan, peak, violation, slack, sumfin, stream);
 }

@@ -49,6 +49,9 @@ struct GmgView {
   const uint32_t *bytes32;  // out_bytes as u32
   // first two successors of each op as u16 (0xFFFF: none), when no op has more
   const uint32_t *succ2;
+  // with succ2 and fewer than 65,535 edges: the predecessor-edge index of each
+  // of those two successor entries, same packing
+  const uint32_t *succ2_pe;
   // time -> slice lookup per device, for buckets of 2^lut_shift us: entry
   // [d][b] concerns the first slice k of d ending at or after b << lut_shift;
   // lut_w holds {begin, end} of slices k and k+1, lut_k the device-local k
@@ -181,9 +184,13 @@ int ss_run_simulate_resume(const ss_gmg *g, const ss_state *from, const uint8_t 
 // The schedule of one candidate (resumed from `from`), its state stored in capture.
 int ss_run_state_capture(const ss_gmg *g, const ss_state *from, const uint8_t *placement, ss_state *capture,
                          hipStream_t stream);
-// Memory passes of the 32-bit path over int64 finish rows (sim_fast.hip).
+// Memory passes of the 32-bit path over int64 finish rows (sim_fast.hip).  With
+// arr64 (transfers over device ports) the arrivals per predecessor edge,
+// [edge][arr_stride] int64 from the first candidate of P: copies start at
+// their transfer's start and own outputs are kept until their last arrival.
 int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, int64_t B, int64_t *peak,
-                       uint8_t *violation, hipStream_t stream);
+                       uint8_t *violation, hipStream_t stream, const int64_t *arr64 = nullptr,
+                       int64_t arr_stride = 0);
 // Fast path (sim_fast.hip): 32-bit times, N <= 65535.
 size_t ss_fast_schedule_lds(const ss_gmg *g);
 int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,

@@ -26,6 +26,18 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 FIELDS = ("makespan", "peak", "violation", "slack", "sumfin")
 
 
+@pytest.fixture(params=["auto", "generic"])
+def path(request, monkeypatch):
+    """The memory pass of a port run: the 32-bit passes reading the arrivals
+    (default, when the GMG fits the branch-free interval writer) or the
+    general int64 memory kernel (SS_PATH=generic)."""
+    if request.param == "generic":
+        monkeypatch.setenv("SS_PATH", "generic")
+    else:
+        monkeypatch.delenv("SS_PATH", raising=False)
+    return request.param
+
+
 @pytest.fixture(scope="module")
 def dev():
     assert torch.cuda.is_available(), "GPU tests need a GPU"
@@ -78,8 +90,8 @@ def test_hand_cases_on_gpu(dev, case):
 
 
 @pytest.mark.parametrize("cid,nb", [(0, 256), (1, 300), (2, 150), (3, 64), (4, 8)])
-def test_config_parity_ports(dev, cid, nb):
-    print(f"transfer ports, config {cid}: {nb} candidates", flush=True)
+def test_config_parity_ports(dev, path, cid, nb):
+    print(f"transfer ports, config {cid}: {nb} candidates, {path} memory pass", flush=True)
     g = synth.build_gmg(cid)
     P = synth.placements(g, cid, 0, nb)
     ref = oracle.simulate_batch(g, P, dispatch=oracle.LINK_PORTS, n_threads=8)
@@ -106,6 +118,30 @@ def test_fuzz_parity_ports(dev, seed):
     got = gpu_run(ss.Gmg(g), P, dev)
     assert_same(got, ref, label=f"ports, fuzz {seed}")
     assert (got["violation"] == 4).sum() >= 1
+
+
+# Graphs inside the branch-free interval writer's limits (one device class, at
+# most two link classes and two successors per op) with slow links, so that
+# transfers queue on the ports: the 32-bit memory pass reads the arrivals.
+PORT_WRITER = [dict(n_ops=n, n_dev=D, n_req=R, n_slices=S, n_link=K, zero_bytes_p=0.2, max_outdeg=2, cap_scale=cs,
+                    max_span=sp, edge_p=ep, lat_max=lm, bw_max=bm)
+               for n, D, R, S, K, cs, sp, ep, lm, bm in [
+                   (64, 3, 1, 3, 1, 3000, 6, 0.5, 3, 2), (130, 5, 2, 4, 2, 3000, 6, 0.5, 9, 3),
+                   (257, 8, 3, 5, 2, 6000, 12, 0.3, 0, 1), (700, 16, 4, 6, 2, 20000, 40, 0.1, 5, 4),
+                   (1025, 2, 2, 8, 2, 20000, 4, 0.6, 2, 1)]]
+
+
+@pytest.mark.parametrize("seed", range(len(PORT_WRITER)))
+def test_port_writer_parity(dev, path, seed):
+    kw = PORT_WRITER[seed]
+    print(f"transfer ports, branch-free writer {seed}: {kw}, {path} memory pass", flush=True)
+    g = synth.random_gmg(600 + seed, **kw)
+    assert np.bincount(np.asarray(g.pred_idx), minlength=g.n_ops).max() <= 2
+    P = random_placements(g, seed + 5151, 131, invalid_every=29)
+    P[1::4] = P[0]  # some candidates keep whole chains on one device
+    ref = oracle.simulate_batch(g, P, dispatch=oracle.LINK_PORTS)
+    got = gpu_run(ss.Gmg(g), P, dev)
+    assert_same(got, ref, label=f"ports, branch-free writer {seed}")
 
 
 def test_ports_differ_from_latency_only(dev):
