@@ -159,9 +159,11 @@ int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req)
  * allocated at the transfer's start and the producer's output is kept until
  * its last transfer has arrived.  Index-order dispatch only: with
  * SS_DISPATCH_READY as well the call fails with SS_ERR_UNSUPPORTED.  This
- * variant runs on the general int64 kernels and needs scratch for two port
- * clocks per device and one arrival time per edge for each candidate in
- * flight.
+ * variant runs on the 32-bit kernels when the GMG fits them (a 32-bit time
+ * horizon, one device class, at most two link classes and at most two
+ * predecessors and two successors per op), else on the general int64
+ * kernels; it needs scratch for two port clocks per device and one or two
+ * arrival times per edge for each candidate in flight.
  * A candidate naming a device >= n_dev is not simulated: violation =
  * SS_VIOLATION_INVALID, makespan = sumfin = INT64_MAX, peak = 0 and slack =
  * INT64_MIN.  This is a per-candidate result, not a call error.

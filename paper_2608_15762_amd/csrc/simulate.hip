@@ -839,21 +839,23 @@ int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makes
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
   const bool fast_ok = g->view.time32 && (ready_dispatch ? ss_ready_schedule_lds(g) : ss_fast_schedule_lds(g)) <=
                                              (size_t)lds_max;
+  const bool ports_fast = link_ports && fast_ok && ss_fast_ports_ok(g);
   const char *path = std::getenv("SS_PATH");
-  if (path && std::strcmp(path, "fast") == 0 && (!fast_ok || link_ports))
+  if (path && std::strcmp(path, "fast") == 0 && (!fast_ok || (link_ports && !ports_fast)))
     return ss_set_error(SS_ERR_UNSUPPORTED, "SS_PATH=fast but this GMG or dispatch needs the general path");
-  // transfer ports run on the general schedule kernel; their memory pass is
-  // the 32-bit one when the GMG fits the branch-free interval writer (not
-  // with SS_PATH=generic)
+  // transfer ports run on the 32-bit kernels when the GMG fits them, else on
+  // the general schedule kernel, whose memory pass is still the 32-bit one
+  // when the GMG fits the branch-free interval writer (SS_PATH=generic: the
+  // general kernels throughout)
   const bool force_generic = path && std::strcmp(path, "generic") == 0;
-  const bool generic = !fast_ok || link_ports || force_generic;
+  const bool generic = !fast_ok || (link_ports && !ports_fast) || force_generic;
   const bool ports_mem_fast = link_ports && !force_generic && g->view.time32 && g->n_ops > 0 && g->n_class == 1 &&
                               g->n_link <= 2 && g->max_outdeg <= 2 && g->view.succ2_pe;
   if (generic)
     return run_simulate_generic(g, P, B, makespan, peak, violation, slack, sumfin, stream, ready_dispatch, link_ports,
                                 nullptr, nullptr, ports_mem_fast);
   if (ready_dispatch) return ss_run_simulate_ready(g, P, B, makespan, peak, violation, slack, sumfin, stream);
-  return ss_run_simulate_fast(g, P, B, makespan, peak, violation, slack, sumfin, stream);
+  return ss_run_simulate_fast(g, P, B, makespan, peak, violation, slack, sumfin, stream, link_ports);
 }
 
 // The state's buffer grows to hold a capture of g (synchronising the stream

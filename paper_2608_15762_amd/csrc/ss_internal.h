@@ -194,7 +194,11 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
 // Fast path (sim_fast.hip): 32-bit times, N <= 65535.
 size_t ss_fast_schedule_lds(const ss_gmg *g);
 int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
-                         uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream);
+                         uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream,
+                         bool link_ports = false);
+// Whether transfer ports can run on the 32-bit kernels: one device class, at
+// most two link classes, two predecessors and two successors per op.
+bool ss_fast_ports_ok(const ss_gmg *g);
 // Ready-time dispatch on the fast path (sim_fast.hip).
 size_t ss_ready_schedule_lds(const ss_gmg *g);
 int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,

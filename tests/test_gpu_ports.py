@@ -213,6 +213,10 @@ def test_refusals(dev, monkeypatch):
     Pt = torch.from_numpy(synth.placements(g, 0, 0, 8)).to(dev)
     with pytest.raises(ss.SSError):
         ss.simulate_batch(h, Pt, dispatch="ready", links="ports")
+    # a graph with an op of three predecessors needs the general kernels for ports
+    g3 = make_gmg(2, ["op"] * 4, [(0, 3), (1, 3), (2, 3)], [0] * 4, [[5]] * 4, [10] * 4, [[(0, TIME_INF)]] * 2,
+                  [10 ** 6] * 2, [0], [10 ** 6], bw=(10,), lat=(1,))
+    P3 = torch.zeros((2, 4), dtype=torch.uint8, device=dev)
     monkeypatch.setenv("SS_PATH", "fast")
     with pytest.raises(ss.SSError):
-        ss.simulate_batch(h, Pt, links="ports")
+        ss.simulate_batch(ss.Gmg(g3), P3, links="ports")
