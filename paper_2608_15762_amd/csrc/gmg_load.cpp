@@ -16,17 +16,41 @@ using i128 = __int128;
 constexpr i128 kTimeLimit = (i128)1 << 62;
 constexpr i128 kSumLimit = (i128)1 << 63;
 
+// The arrays of one device allocation at 256-byte aligned offsets: add()
+// records where each goes, pack() copies them once into a buffer of the
+// calling thread that its later loads reuse (a load has uploaded it before it
+// returns); gaps and arrays without a source are zero.  The sources must stay
+// alive until pack().
 struct Packer {
-  std::vector<unsigned char> host;
+  struct Part {
+    const void *src;
+    size_t bytes, off;
+  };
+  std::vector<Part> parts;
+  size_t size = 0;
   size_t add(const void *src, size_t bytes) {
-    size_t off = (host.size() + 255) & ~size_t(255);
-    host.resize(off + bytes);
-    if (bytes && src) std::memcpy(host.data() + off, src, bytes);
+    const size_t off = (size + 255) & ~size_t(255);
+    parts.push_back({src, bytes, off});
+    size = off + bytes;
     return off;
   }
   template <class T>
   size_t add(const std::vector<T> &v) {
     return add(v.data(), v.size() * sizeof(T));
+  }
+  const unsigned char *pack() const {
+    static thread_local std::vector<unsigned char> buf;
+    if (buf.size() < size) buf.resize(size);
+    size_t end = 0;
+    for (const Part &p : parts) {
+      if (p.off > end) std::memset(buf.data() + end, 0, p.off - end);
+      if (p.bytes) {
+        if (p.src) std::memcpy(buf.data() + p.off, p.src, p.bytes);
+        else std::memset(buf.data() + p.off, 0, p.bytes);
+      }
+      end = p.off + p.bytes;
+    }
+    return buf.data();
   }
 };
 
@@ -519,10 +543,11 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     }
     g->aux = ss_device_aux(g->device);
     g->pool = g->aux ? ss_device_pool(g->device) : nullptr;
-    int arc = g->pool ? ss_pool_alloc(g->device, pk.host.size(), g->aux, &g->dev_mem) : SS_ERR_DEVICE;
+    const unsigned char *packed = pk.pack();
+    int arc = g->pool ? ss_pool_alloc(g->device, pk.size, g->aux, &g->dev_mem) : SS_ERR_DEVICE;
     hipError_t e = hipSuccess;
     if (arc == SS_OK) {
-      e = hipMemcpyAsync(g->dev_mem, pk.host.data(), pk.host.size(), hipMemcpyHostToDevice, g->aux);
+      e = hipMemcpyAsync(g->dev_mem, packed, pk.size, hipMemcpyHostToDevice, g->aux);
       if (e == hipSuccess) e = hipStreamSynchronize(g->aux);
       if (e != hipSuccess) arc = ss_set_error(SS_ERR_DEVICE, "copying the staged GMG failed");
     }

@@ -37,6 +37,7 @@ struct ss_sched {
   std::vector<uint8_t> state, place;
   std::vector<int32_t> issue_order;  // scheduled ops in the order they were issued
   std::vector<int32_t> missing;  // unscheduled predecessors
+  std::vector<uint8_t> rows;     // host candidate rows of the current round (kept: no new pages each round)
   std::set<std::pair<int64_t, int32_t>> frontier;
   int64_t n_issued = 0;
   // reused device buffers: candidate rows and per-candidate outputs
@@ -214,6 +215,8 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
 
   // the round's graph: the scheduled ops and the batch, renumbered
   std::vector<int32_t> newid((size_t)s->N, -1), sp_ptr(1, 0), sp_idx, sreq((size_t)Ns);
+  sp_idx.reserve(s->pred_idx.size());
+  sp_ptr.reserve((size_t)Ns + 1);
   std::vector<int64_t> sdur((size_t)(Ns * s->C)), sbytes((size_t)Ns);
   for (int64_t i = 0; i < Ns; ++i) newid[order[i]] = (int32_t)i;
   for (int64_t i = 0; i < Ns; ++i) {
@@ -250,7 +253,12 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
   gd.deadline = s->deadline.data();
 
   // candidate b = partition b: the scheduled ops where they are, the batch by the partition
-  std::vector<uint8_t> rows((size_t)(P * Ns));
+  try {
+    if (s->rows.size() < (size_t)(P * Ns)) s->rows.resize((size_t)(P * Ns));
+  } catch (const std::bad_alloc &) {
+    return ss_set_error(SS_ERR_OOM, "ss_sched_round: host allocation failed");
+  }
+  std::vector<uint8_t> &rows = s->rows;
   for (int64_t b = 0; b < P; ++b) {
     uint8_t *row = rows.data() + b * Ns;
     for (int64_t i = 0; i < npre; ++i) row[i] = s->place[order[i]];
