@@ -54,6 +54,9 @@ namespace {
 constexpr int kWave = 64;
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per chunk
+// index-order 32-bit path: larger chunks (fewer pipeline fills and drains of
+// the memory passes), halved while the scratch does not fit
+constexpr int64_t kFastScratchBudget = int64_t(96) << 30;
 constexpr int64_t kRecordBudget = int64_t(32) << 30;   // sizes the sub-chunks (record bytes of about two sets)
 constexpr int kPeakBlocksPerCU = 8;  // fast_peaks holds about 19.5 KB of LDS
 
@@ -1782,40 +1785,47 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   // holds at once (every wave runs about as long as any other).
   const int64_t round =
       (int64_t)cus * std::max<int64_t>(1, lds_cu / (int64_t)std::max<size_t>(sched_lds, 1)) * kWave;
-  int64_t chunk = kScratchBudget / std::max<int64_t>(1, per_cand);
-  chunk = chunk >= round ? chunk / round * round : std::max<int64_t>(kWave, chunk / kWave * kWave);
-  chunk = std::min<int64_t>(chunk, int64_t(65535) * 64);  // transpose grids index 64-candidate tiles in y
-  chunk = std::min<int64_t>(chunk, B);
   // sub-chunk: interval records of each candidate (own N, copies <= E)
   const int64_t rec_per_cand = (own_stride(N) + cp_stride(E)) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4 + N * 2;
-  int64_t sub = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
-  sub = std::min<int64_t>(sub, chunk);
-  {  // equal sub-chunks, at least two for a large chunk (the peak pass of one
-     // overlaps the interval pass of the next)
-    const int64_t n = std::max<int64_t>((chunk + sub - 1) / sub, chunk >= 8192 ? 2 : 1);
-    sub = (chunk + n - 1) / n;
-  }
-  const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
   const int64_t slot_cap = N + E + 1;  // most allocations one device can hold
-
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
-  const size_t sz_pt = align((size_t)chunk * N + 1);
-  const size_t sz_fin = align((size_t)chunk * N * 4 + 4);
-  const size_t sz_own = align((size_t)sub * own_stride(N) * sizeof(Rec));
-  const size_t sz_cp = align((size_t)sub * cp_stride(E) * sizeof(Rec));
-  const size_t sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
-  const size_t sz_rank = align(((size_t)sub * N + 1) * 2);
-  const size_t sz_wk = align((size_t)nslots * 2 * (slot_cap + 2) * 4);
-  const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
-  const int64_t n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
-  const size_t sz_tk = align((size_t)n_ticket * 4);
-  const size_t sz_port = ports ? align((size_t)2 * D * chunk * 4) : 0;
-  const size_t sz_arr = ports ? align((size_t)E * chunk * 4) : 0;
+  int64_t chunk = 0, sub = 0, nslots = 0, n_ticket = 0;
+  size_t sz_pt = 0, sz_fin = 0, sz_own = 0, sz_cp = 0, sz_meta = 0, sz_rank = 0, sz_wk = 0, sz_wb = 0, sz_tk = 0,
+         sz_port = 0, sz_arr = 0;
   SsScratch scr;
-  err = ss_scratch_get(g->device, g->pool,
-                       sz_pt + 2 * sz_fin + sz_port + 2 * sz_arr + kRecSets * (sz_own + sz_cp + sz_meta) + sz_rank +
-                           sz_wk + sz_wb + sz_tk,
-                       stream, &scr);
+  // the largest chunk within the scratch budget; when its scratch does not
+  // fit in the device's free memory, half the budget (down to one round)
+  for (int64_t budget = kFastScratchBudget;; budget /= 2) {
+    chunk = budget / std::max<int64_t>(1, per_cand);
+    chunk = chunk >= round ? chunk / round * round : std::max<int64_t>(kWave, chunk / kWave * kWave);
+    chunk = std::min<int64_t>(chunk, int64_t(65535) * 64);  // transpose grids index 64-candidate tiles in y
+    chunk = std::min<int64_t>(chunk, B);
+    sub = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
+    sub = std::min<int64_t>(sub, chunk);
+    {  // equal sub-chunks, at least two for a large chunk (the peak pass of one
+       // overlaps the interval pass of the next)
+      const int64_t n = std::max<int64_t>((chunk + sub - 1) / sub, chunk >= 8192 ? 2 : 1);
+      sub = (chunk + n - 1) / n;
+    }
+    nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
+    sz_pt = align((size_t)chunk * N + 1);
+    sz_fin = align((size_t)chunk * N * 4 + 4);
+    sz_own = align((size_t)sub * own_stride(N) * sizeof(Rec));
+    sz_cp = align((size_t)sub * cp_stride(E) * sizeof(Rec));
+    sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
+    sz_rank = align(((size_t)sub * N + 1) * 2);
+    sz_wk = align((size_t)nslots * 2 * (slot_cap + 2) * 4);
+    sz_wb = align((size_t)nslots * slot_cap * 8);
+    n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
+    sz_tk = align((size_t)n_ticket * 4);
+    sz_port = ports ? align((size_t)2 * D * chunk * 4) : 0;
+    sz_arr = ports ? align((size_t)E * chunk * 4) : 0;
+    err = ss_scratch_get(g->device, g->pool,
+                         sz_pt + 2 * sz_fin + sz_port + 2 * sz_arr + kRecSets * (sz_own + sz_cp + sz_meta) + sz_rank +
+                             sz_wk + sz_wb + sz_tk,
+                         stream, &scr);
+    if (err != hipErrorOutOfMemory || chunk <= std::min<int64_t>(round, B)) break;
+  }
   void *scratch = scr.p;
   if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
