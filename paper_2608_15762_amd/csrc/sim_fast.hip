@@ -45,6 +45,7 @@
 //                 spill list beyond), finish times in candidate rows and each
 //                 op's rank in dispatch order; then fast_intervals with those
 //                 ranks and fast_peaks as above.
+#include <atomic>
 #include <climits>
 
 #include "ss_internal.h"
@@ -55,8 +56,10 @@ constexpr int kWave = 64;
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per chunk
 // index-order 32-bit path: larger chunks (fewer pipeline fills and drains of
-// the memory passes), halved while the scratch does not fit
+// the memory passes), halved while the scratch does not fit; later calls on
+// the device start from the last budget that fitted
 constexpr int64_t kFastScratchBudget = int64_t(96) << 30;
+std::atomic<int64_t> g_fast_budget[256];  // 0: not tried yet
 constexpr int64_t kRecordBudget = int64_t(32) << 30;   // sizes the sub-chunks (record bytes of about two sets)
 constexpr int kPeakBlocksPerCU = 8;  // fast_peaks holds about 19.5 KB of LDS
 
@@ -1795,7 +1798,9 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   SsScratch scr;
   // the largest chunk within the scratch budget; when its scratch does not
   // fit in the device's free memory, half the budget (down to one round)
-  for (int64_t budget = kFastScratchBudget;; budget /= 2) {
+  std::atomic<int64_t> &fitted = g_fast_budget[g->device & 255];
+  int64_t budget = fitted.load();
+  for (budget = budget > 0 ? budget : kFastScratchBudget;; budget /= 2) {
     chunk = budget / std::max<int64_t>(1, per_cand);
     chunk = chunk >= round ? chunk / round * round : std::max<int64_t>(kWave, chunk / kWave * kWave);
     chunk = std::min<int64_t>(chunk, int64_t(65535) * 64);  // transpose grids index 64-candidate tiles in y
@@ -1826,6 +1831,7 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
                          stream, &scr);
     if (err != hipErrorOutOfMemory || chunk <= std::min<int64_t>(round, B)) break;
   }
+  if (err == hipSuccess && chunk < B) fitted.store(budget);  // a budget that bounded the chunk and fitted
   void *scratch = scr.p;
   if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
   unsigned char *p = static_cast<unsigned char *>(scratch);
