@@ -99,6 +99,37 @@ __global__ __launch_bounds__(256) void transpose_tiles(const T *__restrict__ in,
   }
 }
 
+// Byte matrices whose sizes are multiples of 4 (and 4-byte aligned input):
+// 128 x 128 tiles moved as 4-byte words on both sides. A word read holds 4
+// columns of one row; a word written packs 4 rows of one column, gathered
+// byte by byte from LDS (row pitch 33 words).
+__global__ __launch_bounds__(256) void transpose_u8_words(const uint8_t *__restrict__ in, int64_t rows, int64_t cols,
+                                                          uint8_t *__restrict__ out) {
+  __shared__ uint32_t tile[128 * 33];
+  const int64_t c0 = (int64_t)blockIdx.x * 128, r0 = (int64_t)blockIdx.y * 128;
+  const int w = threadIdx.x & 31, i0 = threadIdx.x >> 5;
+  const bool col_in = c0 + 4 * w < cols;
+#pragma unroll
+  for (int p = 0; p < 16; ++p) {
+    const int i = i0 + 8 * p;
+    if (col_in && r0 + i < rows)
+      tile[i * 33 + w] = *reinterpret_cast<const uint32_t *>(in + (r0 + i) * cols + c0 + 4 * w);
+  }
+  __syncthreads();
+  const uint8_t *t8 = reinterpret_cast<const uint8_t *>(tile);
+  const int q = w;  // rows 4q..4q+3 of the tile
+  const bool row_in = r0 + 4 * q < rows;
+#pragma unroll
+  for (int p = 0; p < 16; ++p) {
+    const int c = i0 + 8 * p;
+    if (row_in && c0 + c < cols) {
+      const uint32_t v = (uint32_t)t8[(4 * q) * 132 + c] | (uint32_t)t8[(4 * q + 1) * 132 + c] << 8 |
+                         (uint32_t)t8[(4 * q + 2) * 132 + c] << 16 | (uint32_t)t8[(4 * q + 3) * 132 + c] << 24;
+      *reinterpret_cast<uint32_t *>(out + (c0 + c) * rows + r0 + 4 * q) = v;
+    }
+  }
+}
+
 // ------------------------------------------------------------------ schedule
 // link class of a transfer from device a to device b (at most two classes)
 __device__ __forceinline__ uint32_t link_bit(const GmgView &G, uint32_t a, uint32_t b) {
@@ -1880,8 +1911,13 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
     const uint8_t *Pc = P + b0 * N;
     SsTimingRec *tp = ss_timing_start(SS_KERNEL_TRANSPOSE, stream);
     if (N > 0) {  // candidates' placement rows -> op-major [op][candidate]
-      const dim3 tg((unsigned)((N + 63) / 64), (unsigned)((nb + 63) / 64));
-      hipLaunchKernelGGL(transpose_tiles<uint8_t>, tg, dim3(256), 0, stream, Pc, nb, (int64_t)N, PT);
+      if (N % 4 == 0 && nb % 4 == 0 && (reinterpret_cast<uintptr_t>(Pc) & 3) == 0) {
+        const dim3 tg((unsigned)((N + 127) / 128), (unsigned)((nb + 127) / 128));
+        hipLaunchKernelGGL(transpose_u8_words, tg, dim3(256), 0, stream, Pc, nb, (int64_t)N, PT);
+      } else {
+        const dim3 tg((unsigned)((N + 63) / 64), (unsigned)((nb + 63) / 64));
+        hipLaunchKernelGGL(transpose_tiles<uint8_t>, tg, dim3(256), 0, stream, Pc, nb, (int64_t)N, PT);
+      }
     }
     ss_timing_stop(tp, stream);
     if (!check("transpose launch")) break;

@@ -87,6 +87,20 @@ def test_fuzz_parity(dev, path, seed):
     assert (got["violation"] == 4).sum() >= 1
 
 
+
+@pytest.mark.parametrize("n_ops,B", [(260, 388), (132, 4), (516, 1020)])
+def test_word_transpose_ragged_tiles(dev, path, n_ops, B):
+    # op and candidate counts divisible by 4 but not by the 128-wide tiles of
+    # the word transpose of the placements: several tiles and ragged edges
+    print(f"word transpose: {n_ops} ops, {B} candidates", flush=True)
+    g = synth.random_gmg(n_ops, n_ops=n_ops, n_dev=6, n_req=2, n_slices=4, n_link=2, zero_bytes_p=0.1,
+                         max_outdeg=2, cap_scale=4000)
+    st = synth.Stream(n_ops * 7 + B)
+    P = np.array([[st.uniform_int(0, g.n_dev - 1) for _ in range(g.n_ops)] for _ in range(B)], np.uint8)
+    ref = oracle.simulate_batch(g, P, n_threads=8)
+    got = gpu_run(ss.Gmg(g), P, dev)
+    assert_same(got, ref, label=f"word transpose {n_ops}x{B}")
+
 # Graphs inside the limits of the branch-free interval writer (one device
 # class, at most two link classes and two successors per op), with zero-byte
 # outputs, zero transfer latencies, far-reaching edges and ragged op counts.
