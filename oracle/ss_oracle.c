@@ -23,7 +23,7 @@
  *   - a transfer is pure latency starting at the producer's finish, one per
  *     (tensor, destination device), shared by all consumers there; the
  *     SSO_LINK_PORTS variant arbitrates transfers over per-device ports
- *     instead (Sec. 3.5.2, see schedule_index_order_ports);
+ *     instead, event by event (Sec. 3.5.2, see schedule_index_order_ports);
  *   - memory: an op's output occupies its device from the op's start until the
  *     later of its last local consumer's finish and its last outgoing
  *     transfer's arrival; a remote copy occupies the destination from the
@@ -130,70 +130,203 @@ static void schedule_index_order(const sso_gmg *g, const uint8_t *place, int64_t
   }
 }
 
-/* Position of consumer v in the successor list of u. */
-static int64_t succ_entry(const succ_csr *sc, int64_t u, int64_t v) {
-  for (int64_t q = sc->ptr[u]; q < sc->ptr[u + 1]; ++q)
-    if (sc->idx[q] == v) return q;
-  return -1; /* not reached: v is a successor of each of its predecessors */
+/* SSO_LINK_PORTS: transfers arbitrated over the devices' ports, as the
+ * executor's arbitration does (Sec. 3.5.2), inside an event-driven simulation.
+ *   - Compute queues are those of contract A: each device runs its ops in
+ *     index order, one at a time, each at the earliest fit at or after
+ *     max(ready, the device's previous finish).
+ *   - The output of u is moved once to every other device that holds a
+ *     consumer of u (one transfer per (tensor, destination device)).  Its
+ *     Intent arrives when u finishes; the transfer is then pending.
+ *   - The arbitration is triggered by every Intent arrival and every transfer
+ *     completion.  At such an instant t the pending transfers are examined in
+ *     order of request time, then producer index, then destination device,
+ *     and each one whose source's send port and destination's receive port
+ *     are both idle at t starts at t (so the started set shares no source and
+ *     no destination); it holds both ports until it arrives, t + X.  Nothing
+ *     is booked ahead of time.
+ *   - A transfer whose estimate X is zero moves nothing: it completes at its
+ *     request, takes no port and waits for none.
+ *   - A consumer's remote input is there when its transfer arrives.
+ * An op is placed as soon as every input's availability time is known and
+ * the op ahead of it on its device is placed; its start depends on nothing
+ * else, and it never precedes the instant at which it is placed, so placing
+ * it then gives the same schedule as placing it at its ready time.
+ * xs/xa receive the start and arrival of the transfer that serves each
+ * successor entry (equal for every consumer of u on one device; unused for
+ * local consumers).  order/n_order (nullable) receive the first successor
+ * entry of each transfer in the order the transfers start.
+ * Returns 0, or -1 on allocation failure. */
+typedef struct { int64_t time, kind, id; } sim_event; /* kind 0: op finishes, 1: transfer arrives */
+
+static int event_before(sim_event a, sim_event b) {
+  if (a.time != b.time) return a.time < b.time;
+  if (a.kind != b.kind) return a.kind < b.kind;
+  return a.id < b.id;
 }
 
-/* SSO_LINK_PORTS.  The executor admits pending transfers as sets that share
- * no source and no destination accelerator (Sec. 3.5.2): a device sends at
- * most one tensor at a time and receives at most one at a time.  Reading for
- * the simulator: the transfer of u's output to a remote device e is requested
- * when u finishes; requests are admitted in the order their producers are
- * dispatched (index order), and the requests of one producer in the order of
- * their destinations' first consumers; an admitted transfer starts at the
- * latest of its request, the moment its source's send port frees and the
- * moment its destination's receive port frees, and holds both ports for its
- * transfer estimate (ports are served in admission order, like a device's
- * compute queue in index order).  A transfer whose estimate is zero moves
- * nothing and neither waits for nor holds a port.  A consumer's input from
- * another device is there when that transfer arrives.  xs/xa: start and arrival per successor entry of the
- * successor CSR (equal for the consumers of u on one device; unused for local
- * consumers). */
-static void schedule_index_order_ports(const sso_gmg *g, const uint8_t *place, const succ_csr *sc, int64_t *clock,
-                                       int64_t *send_free, int64_t *recv_free, int64_t *st, int64_t *fin,
-                                       int64_t *xs, int64_t *xa) {
-  for (int64_t d = 0; d < g->n_dev; ++d) clock[d] = send_free[d] = recv_free[d] = 0;
-  for (int64_t v = 0; v < g->n_ops; ++v) {
-    const int64_t d = place[v];
-    const int64_t w = op_duration(g, v, d);
-    int64_t ready = g->release[g->op_req[v]];
-    if (ready < 0) ready = 0;
-    for (int64_t e = g->pred_ptr[v]; e < g->pred_ptr[v + 1]; ++e) {
-      const int64_t u = g->pred_idx[e];
-      const int64_t arrive = place[u] == d ? fin[u] : xa[succ_entry(sc, u, v)];
-      if (arrive > ready) ready = arrive;
-    }
-    const int64_t t = ready > clock[d] ? ready : clock[d];
-    st[v] = earliest_fit(g, d, t, w);
-    fin[v] = st[v] + w;
-    clock[d] = fin[v];
-    for (int64_t q = sc->ptr[v]; q < sc->ptr[v + 1]; ++q) {
-      const int64_t dst = place[sc->idx[q]];
-      if (dst == d) continue;
-      int64_t first = q;
-      for (int64_t q2 = sc->ptr[v]; q2 < q; ++q2)
-        if (place[sc->idx[q2]] == dst) { first = q2; break; }
-      if (first != q) {  /* the tensor is already on its way to dst */
-        xs[q] = xs[first];
-        xa[q] = xa[first];
-        continue;
-      }
-      const int64_t x = transfer_time(g, v, d, dst);
-      if (x == 0) {
-        xs[q] = xa[q] = fin[v];
-        continue;
-      }
-      int64_t s0 = fin[v];
-      if (send_free[d] > s0) s0 = send_free[d];
-      if (recv_free[dst] > s0) s0 = recv_free[dst];
-      xs[q] = s0;
-      xa[q] = s0 + x;
-      send_free[d] = recv_free[dst] = xa[q];
-    }
+static void event_push(sim_event *h, int64_t *n, sim_event x) {
+  int64_t i = (*n)++;
+  h[i] = x;
+  while (i > 0) {
+    const int64_t p = (i - 1) / 2;
+    if (!event_before(h[i], h[p])) break;
+    sim_event t = h[i]; h[i] = h[p]; h[p] = t;
+    i = p;
   }
+}
+
+static sim_event event_pop(sim_event *h, int64_t *n) {
+  sim_event top = h[0];
+  h[0] = h[--(*n)];
+  int64_t i = 0;
+  for (;;) {
+    const int64_t l = 2 * i + 1, r = l + 1;
+    int64_t m = i;
+    if (l < *n && event_before(h[l], h[m])) m = l;
+    if (r < *n && event_before(h[r], h[m])) m = r;
+    if (m == i) break;
+    sim_event t = h[i]; h[i] = h[m]; h[m] = t;
+    i = m;
+  }
+  return top;
+}
+
+/* First successor entry of u whose consumer runs on device e, or -1. */
+static int64_t first_entry_to(const succ_csr *sc, const uint8_t *place, int64_t u, int64_t e) {
+  for (int64_t q = sc->ptr[u]; q < sc->ptr[u + 1]; ++q)
+    if (place[sc->idx[q]] == e) return q;
+  return -1;
+}
+
+/* Start (or, with a zero estimate, complete) the transfer of u to e at t. */
+static void set_transfer(const succ_csr *sc, const uint8_t *place, int64_t u, int64_t e, int64_t start,
+                         int64_t arrive, int64_t *xs, int64_t *xa) {
+  for (int64_t q = sc->ptr[u]; q < sc->ptr[u + 1]; ++q)
+    if (place[sc->idx[q]] == e) {
+      xs[q] = start;
+      xa[q] = arrive;
+    }
+}
+
+static int schedule_index_order_ports(const sso_gmg *g, const uint8_t *place, const succ_csr *sc, int64_t *clock,
+                                      int64_t *st, int64_t *fin, int64_t *xs, int64_t *xa, int64_t *order,
+                                      int64_t *n_order) {
+  const int64_t N = g->n_ops, D = g->n_dev, E = sc->ptr[N];
+  int64_t *dev_ptr = (int64_t *)calloc((size_t)D + 1, sizeof(int64_t));
+  int64_t *dev_ops = (int64_t *)malloc(((size_t)N + 1) * sizeof(int64_t));
+  int64_t *head = (int64_t *)malloc(((size_t)D + 1) * sizeof(int64_t));
+  int64_t *send_until = (int64_t *)malloc(((size_t)D + 1) * sizeof(int64_t));
+  int64_t *recv_until = (int64_t *)malloc(((size_t)D + 1) * sizeof(int64_t));
+  char *dirty = (char *)calloc((size_t)D + 1, 1);
+  /* pending transfers: producer, destination, request time (in arbitration order) */
+  int64_t *pend_u = (int64_t *)malloc(((size_t)E + 1) * sizeof(int64_t));
+  int64_t *pend_e = (int64_t *)malloc(((size_t)E + 1) * sizeof(int64_t));
+  int64_t *fresh = (int64_t *)malloc(((size_t)D + 1) * sizeof(int64_t));
+  sim_event *heap = (sim_event *)malloc(((size_t)N + E + 1) * sizeof(sim_event));
+  int rc = -1;
+  if (!dev_ptr || !dev_ops || !head || !send_until || !recv_until || !dirty || !pend_u || !pend_e || !fresh ||
+      !heap)
+    goto out;
+  int64_t n_pend = 0, n_heap = 0, n_ord = 0;
+  /* the compute queue of each device: its ops in index order */
+  for (int64_t v = 0; v < N; ++v) dev_ptr[place[v] + 1]++;
+  for (int64_t d = 0; d < D; ++d) dev_ptr[d + 1] += dev_ptr[d];
+  for (int64_t d = 0; d < D; ++d) head[d] = dev_ptr[d];
+  for (int64_t v = 0; v < N; ++v) dev_ops[head[place[v]]++] = v;
+  for (int64_t d = 0; d < D; ++d) {
+    head[d] = dev_ptr[d];
+    clock[d] = send_until[d] = recv_until[d] = 0;
+    dirty[d] = 1;
+  }
+  for (int64_t q = 0; q < E; ++q) xs[q] = xa[q] = -1;
+  for (;;) {
+    /* place every queue head whose inputs' availability is known */
+    for (int64_t d = 0; d < D; ++d) {
+      if (!dirty[d]) continue;
+      dirty[d] = 0;
+      for (; head[d] < dev_ptr[d + 1]; ++head[d]) {
+        const int64_t v = dev_ops[head[d]];
+        int64_t ready = g->release[g->op_req[v]];
+        if (ready < 0) ready = 0;
+        int known = 1;
+        for (int64_t e = g->pred_ptr[v]; e < g->pred_ptr[v + 1] && known; ++e) {
+          const int64_t u = g->pred_idx[e];
+          int64_t avail;
+          if (place[u] == d) {
+            avail = fin[u]; /* earlier in this queue, hence placed */
+          } else {
+            avail = xa[first_entry_to(sc, place, u, d)];
+            if (avail < 0) known = 0; /* its transfer has not started */
+          }
+          if (avail > ready) ready = avail;
+        }
+        if (!known) break;
+        const int64_t w = op_duration(g, v, d);
+        const int64_t t = ready > clock[d] ? ready : clock[d];
+        st[v] = earliest_fit(g, d, t, w);
+        fin[v] = st[v] + w;
+        clock[d] = fin[v];
+        event_push(heap, &n_heap, (sim_event){fin[v], 0, v});
+      }
+    }
+    if (n_heap == 0) break;
+    /* every event of the next instant t */
+    const int64_t t = heap[0].time;
+    while (n_heap > 0 && heap[0].time == t) {
+      const sim_event ev = event_pop(heap, &n_heap);
+      if (ev.kind != 0) continue; /* an arrival: its ports are idle from t on */
+      const int64_t u = ev.id, du = place[u];
+      /* Intents of u, one per remote destination device, by device id */
+      int64_t nf = 0;
+      for (int64_t q = sc->ptr[u]; q < sc->ptr[u + 1]; ++q) {
+        const int64_t e = place[sc->idx[q]];
+        if (e == du || first_entry_to(sc, place, u, e) != q) continue;
+        int64_t i = nf++;
+        while (i > 0 && fresh[i - 1] > e) { fresh[i] = fresh[i - 1]; --i; }
+        fresh[i] = e;
+      }
+      for (int64_t i = 0; i < nf; ++i) {
+        const int64_t e = fresh[i];
+        if (transfer_time(g, u, du, e) == 0) { /* nothing moves */
+          set_transfer(sc, place, u, e, t, t, xs, xa);
+          if (order) order[n_ord] = first_entry_to(sc, place, u, e);
+          ++n_ord;
+          dirty[e] = 1;
+        } else {
+          pend_u[n_pend] = u;
+          pend_e[n_pend] = e;
+          ++n_pend;
+        }
+      }
+    }
+    /* arbitration at t: pending transfers in order, each started when both of
+     * its ports are idle */
+    int64_t kept = 0;
+    for (int64_t i = 0; i < n_pend; ++i) {
+      const int64_t u = pend_u[i], e = pend_e[i], s = place[u];
+      if (send_until[s] <= t && recv_until[e] <= t) {
+        const int64_t a = t + transfer_time(g, u, s, e);
+        set_transfer(sc, place, u, e, t, a, xs, xa);
+        send_until[s] = recv_until[e] = a;
+        event_push(heap, &n_heap, (sim_event){a, 1, first_entry_to(sc, place, u, e)});
+        if (order) order[n_ord] = first_entry_to(sc, place, u, e);
+        ++n_ord;
+        dirty[e] = 1;
+      } else {
+        pend_u[kept] = u;
+        pend_e[kept] = e;
+        ++kept;
+      }
+    }
+    n_pend = kept;
+  }
+  if (n_order) *n_order = n_ord;
+  rc = 0;
+out:
+  free(dev_ptr); free(dev_ops); free(head); free(send_until); free(recv_until); free(dirty);
+  free(pend_u); free(pend_e); free(fresh); free(heap);
+  return rc;
 }
 
 /* binary min-heap of (ready, op) pairs */
@@ -365,7 +498,7 @@ static int valid_placement(const sso_gmg *g, const uint8_t *place) {
 }
 
 typedef struct {
-  int64_t *st, *fin, *clock, *peak, *send_free, *recv_free, *xs, *xa;
+  int64_t *st, *fin, *clock, *peak, *xs, *xa, *order;
 } work_bufs;
 
 static int simulate_with(const sso_gmg *g, const succ_csr *sc, const uint8_t *place, int dispatch,
@@ -386,7 +519,7 @@ static int simulate_with(const sso_gmg *g, const succ_csr *sc, const uint8_t *pl
   if (dispatch == SSO_READY_ORDER) {
     if (schedule_ready_order(g, place, sc, clock, st, fin) != 0) return -1;
   } else if (ports) {
-    schedule_index_order_ports(g, place, sc, clock, wb->send_free, wb->recv_free, st, fin, wb->xs, wb->xa);
+    if (schedule_index_order_ports(g, place, sc, clock, st, fin, wb->xs, wb->xa, 0, 0) != 0) return -1;
   } else {
     schedule_index_order(g, place, clock, st, fin);
   }
@@ -426,16 +559,15 @@ static int alloc_work(const sso_gmg *g, work_bufs *w) {
   w->fin = (int64_t *)malloc(N * sizeof(int64_t));
   w->clock = (int64_t *)malloc(D * sizeof(int64_t));
   w->peak = (int64_t *)malloc(D * sizeof(int64_t));
-  w->send_free = (int64_t *)malloc(D * sizeof(int64_t));
-  w->recv_free = (int64_t *)malloc(D * sizeof(int64_t));
+  w->order = (int64_t *)malloc(E * sizeof(int64_t));
   w->xs = (int64_t *)malloc(E * sizeof(int64_t));
   w->xa = (int64_t *)malloc(E * sizeof(int64_t));
-  return (w->st && w->fin && w->clock && w->peak && w->send_free && w->recv_free && w->xs && w->xa) ? 0 : -1;
+  return (w->st && w->fin && w->clock && w->peak && w->order && w->xs && w->xa) ? 0 : -1;
 }
 
 static void free_work(work_bufs *w) {
   free(w->st); free(w->fin); free(w->clock); free(w->peak);
-  free(w->send_free); free(w->recv_free); free(w->xs); free(w->xa);
+  free(w->order); free(w->xs); free(w->xa);
 }
 
 int sso_simulate_one(const sso_gmg *g, const uint8_t *place, int dispatch, int64_t *st, int64_t *fin,
@@ -526,24 +658,27 @@ int sso_port_transfers(const sso_gmg *g, const uint8_t *place, int64_t *op, int6
   succ_csr sc;
   work_bufs w;
   if (build_succ(g, &sc) != 0) return -1;
-  if (alloc_work(g, &w) != 0) { free_succ(&sc); free_work(&w); return -1; }
-  schedule_index_order_ports(g, place, &sc, w.clock, w.send_free, w.recv_free, w.st, w.fin, w.xs, w.xa);
+  int64_t *owner = (int64_t *)malloc(((size_t)sc.ptr[g->n_ops] + 1) * sizeof(int64_t));
+  if (!owner || alloc_work(g, &w) != 0) {
+    free(owner); free_succ(&sc); free_work(&w);
+    return -1;
+  }
+  /* producer of every successor entry */
   for (int64_t v = 0; v < g->n_ops; ++v)
-    for (int64_t q = sc.ptr[v]; q < sc.ptr[v + 1]; ++q) {
-      const int64_t dx = place[sc.idx[q]];
-      if (dx == place[v]) continue;
-      int first = 1;
-      for (int64_t q2 = sc.ptr[v]; q2 < q; ++q2)
-        if (place[sc.idx[q2]] == dx) first = 0;
-      if (!first) continue;
-      op[*n] = v;
-      src[*n] = place[v];
-      dst[*n] = dx;
-      start[*n] = w.xs[q];
-      arrive[*n] = w.xa[q];
-      ++*n;
-    }
+    for (int64_t q = sc.ptr[v]; q < sc.ptr[v + 1]; ++q) owner[q] = v;
+  int64_t m = 0;
+  int rc = schedule_index_order_ports(g, place, &sc, w.clock, w.st, w.fin, w.xs, w.xa, w.order, &m);
+  for (int64_t i = 0; rc == 0 && i < m; ++i) { /* in the order the transfers started */
+    const int64_t q = w.order[i], v = owner[q];
+    op[i] = v;
+    src[i] = place[v];
+    dst[i] = place[sc.idx[q]];
+    start[i] = w.xs[q];
+    arrive[i] = w.xa[q];
+  }
+  if (rc == 0) *n = m;
+  free(owner);
   free_work(&w);
   free_succ(&sc);
-  return 0;
+  return rc;
 }

@@ -44,7 +44,7 @@ typedef struct {
 /* dispatch rules */
 #define SSO_INDEX_ORDER 0  /* each device serves its ops in index (priority) order */
 #define SSO_READY_ORDER 1  /* global earliest-ready-time-first dispatch */
-#define SSO_LINK_PORTS 2   /* index order, transfers arbitrated over per-device send and receive ports */
+#define SSO_LINK_PORTS 2   /* index order; transfers arbitrated event by event over per-device send and receive ports */
 
 /* One candidate.  st/fin (length n_ops) and peak (n_dev), slack (n_req) may be
  * NULL.  Returns 0, or -1 on allocation failure. */
@@ -62,7 +62,7 @@ int sso_peak_sweep(const sso_gmg *g, const uint8_t *place, const int64_t *st, co
 int sso_peak_pairwise(const sso_gmg *g, const uint8_t *place, const int64_t *st, const int64_t *fin,
                       int64_t *peak);
 
-/* The transfers of one candidate under SSO_LINK_PORTS, in admission order:
+/* The transfers of one candidate under SSO_LINK_PORTS, in the order they start:
  * producer op, source and destination device, start and arrival.  The arrays
  * hold at least n_edges entries; *n receives the count.  Returns 0, -1 on
  * allocation failure, -2 for a placement naming a device outside the set. */

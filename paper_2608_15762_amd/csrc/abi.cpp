@@ -54,8 +54,9 @@ extern "C" int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int
   if (B < 0) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: B < 0");
   if ((layout & ~(SS_DISPATCH_READY | SS_LINK_PORTS)) != SS_LAYOUT_ROW_MAJOR)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: unknown layout");
-  if ((layout & SS_DISPATCH_READY) && (layout & SS_LINK_PORTS))
-    return ss_set_error(SS_ERR_UNSUPPORTED, "ss_simulate_batch: SS_LINK_PORTS takes index-order dispatch only");
+  if (layout & SS_LINK_PORTS)
+    return ss_set_error(SS_ERR_UNSUPPORTED,
+                        "ss_simulate_batch: SS_LINK_PORTS (event-driven transfer arbitration) is not built yet");
   if (B == 0) return SS_OK;
   if (!out_makespan || !out_violation)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: out_makespan and out_violation are required");

@@ -16,6 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libss.so")
 
 SS_OK = 0
+SS_ERR_INVALID_ARG, SS_ERR_INVALID_GMG, SS_ERR_OOM, SS_ERR_DEVICE, SS_ERR_UNSUPPORTED = -1, -2, -3, -4, -5
 ERRORS = {-1: "SS_ERR_INVALID_ARG", -2: "SS_ERR_INVALID_GMG", -3: "SS_ERR_OOM", -4: "SS_ERR_DEVICE",
           -5: "SS_ERR_UNSUPPORTED"}
 SS_LAYOUT_ROW_MAJOR = 0

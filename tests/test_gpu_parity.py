@@ -321,3 +321,13 @@ def test_full_batch_sampled_parity(dev, path, cid, n_sample):
     idx = np.unique(np.concatenate([[0, B - 1], rng.choice(B, n_sample, replace=False)]))
     ref = oracle.simulate_batch(g, P[idx], n_threads=8)
     assert_same(got, ref, idx=idx, label=f"config {cid} full")
+
+
+def test_link_ports_refused(dev):
+    """Transfer arbitration (SS_LINK_PORTS) is refused with SS_ERR_UNSUPPORTED
+    until GPU kernels of the event-driven rule match the oracle."""
+    g = synth.build_gmg(0)
+    Pt = torch.from_numpy(synth.placements(g, 0, 0, 8)).to(dev)
+    with pytest.raises(ss.SSError) as e:
+        ss.simulate_batch(ss.Gmg(g), Pt, links="ports")
+    assert e.value.code == ss.SS_ERR_UNSUPPORTED

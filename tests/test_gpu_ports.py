@@ -20,7 +20,15 @@ from paper_2608_15762_amd import ss, synth
 from paper_2608_15762_amd.synth import TIME_INF, make_gmg
 
 torch = pytest.importorskip("torch")
-pytestmark = pytest.mark.gpu
+# The oracle now takes the arbitration of Sec. 3.5.2 event by event (a
+# transfer starts when its Intent arrives or a transfer on its ports
+# completes); the library's port kernels booked ports in producer index order
+# and no longer match it, so the library refuses SS_LINK_PORTS
+# (SS_ERR_UNSUPPORTED, checked in test_gpu_parity.py) until kernels of the
+# event-driven rule replace them.
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skip(reason="SS_LINK_PORTS is refused until GPU kernels of the event-driven arbitration "
+                                      "(Sec. 3.5.2) match the oracle")]
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 FIELDS = ("makespan", "peak", "violation", "slack", "sumfin")

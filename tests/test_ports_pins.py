@@ -1,13 +1,17 @@
-"""Pins of the oracle's transfer-port variant (LINK_PORTS): the arbitration of
-Sec. 3.5.2 read into the what-if simulation.  A device sends at most one
-tensor at a time and receives at most one at a time; the transfer of an
-output to a remote device is requested at the producer's finish and admitted
-in producer dispatch order (for one producer, by first consumer).
+"""Pins of the oracle's transfer-port variant (LINK_PORTS): the event-driven
+arbitration of Sec. 3.5.2 read into the what-if simulation.  A device sends at
+most one tensor at a time and receives at most one at a time; the transfer of
+an output to a remote device is requested (its Intent arrives) when the
+producer finishes; at every Intent arrival and every transfer completion the
+pending transfers are examined in order of request time, producer index and
+destination device, and each one whose two ports are idle starts.
 
 Expected values are hand derivations (tests/golden/port_cases.json), special
 cases that reduce to the latency-only rule, a monotonicity bound against it,
 and properties of the transfer list checked from scratch here (port
-exclusivity, durations, non-idling, arrival before use).
+exclusivity, durations, arrival before use, no pending transfer with both
+ports idle at any instant, starts only at a request or a completion, and the
+examination order of pending transfers).
 """
 import json
 import os
@@ -144,14 +148,9 @@ def test_transfer_list_properties(gi):
             for x in succ[u]:  # every consumer on d starts after the arrival
                 if p[x] == d:
                     assert sim["st"][x] >= tr["arrive"][i]
-            # non-idling: a transfer starts at its request or when an earlier
-            # admitted transfer on one of its ports ends (zero-estimate
-            # transfers hold no port)
-            ends = [int(tr["arrive"][j]) for j in range(i)
-                    if (tr["src"][j] == s or tr["dst"][j] == d) and tr["arrive"][j] > tr["start"][j]]
-            assert tr["start"][i] == sim["fin"][u] or int(tr["start"][i]) in ends
             if tr["arrive"][i] == tr["start"][i]:
                 assert tr["start"][i] == sim["fin"][u]
+        check_arbitration(tr, sim["fin"])
         # a port carries one transfer at a time (non-empty intervals disjoint)
         for key in ("src", "dst"):
             for dev in range(g.n_dev):
@@ -159,6 +158,41 @@ def test_transfer_list_properties(gi):
                             if tr[key][i] == dev and tr["arrive"][i] > tr["start"][i])
                 for (a0, a1), (b0, b1) in zip(iv, iv[1:]):
                     assert a1 <= b0, (key, dev)
+
+
+def check_arbitration(tr, fin):
+    """The arbitration rule, checked from the transfer list alone."""
+    n = len(tr["op"])
+    req = [int(fin[int(tr["op"][i])]) for i in range(n)]
+    st = [int(x) for x in tr["start"]]
+    ar = [int(x) for x in tr["arrive"]]
+    src = [int(x) for x in tr["src"]]
+    dst = [int(x) for x in tr["dst"]]
+    busy = [i for i in range(n) if ar[i] > st[i]]  # zero-estimate transfers hold no port
+    key = {i: (req[i], int(tr["op"][i]), dst[i]) for i in range(n)}
+
+    def shares_port(i, j):
+        return src[i] == src[j] or dst[i] == dst[j]
+
+    for i in busy:
+        # it starts at its request or when a transfer on one of its ports completes
+        assert st[i] == req[i] or any(ar[j] == st[i] for j in busy if j != i and shares_port(i, j))
+        # while it waits, one of its ports is always held (no idle pair of ports is left unused)
+        cover = sorted((st[j], ar[j]) for j in busy if j != i and shares_port(i, j))
+        t = req[i]
+        for lo, hi in cover:
+            if lo <= t < hi:
+                t = hi
+        assert t >= st[i], (i, req[i], st[i], cover)
+        # pending transfers are examined in order: a later one (j) that starts
+        # while i still waits found i blocked by a third transfer, started
+        # earlier or examined before i
+        for j in busy:
+            if j == i or key[j] <= key[i] or not (req[i] <= st[j] < st[i]):
+                continue
+            t = st[j]
+            assert any(k not in (i, j) and shares_port(i, k) and st[k] <= t < ar[k] and (st[k] < t or key[k] < key[i])
+                       for k in busy), (i, j)
 
 
 def test_invalid_placement_sentinels():
