@@ -31,8 +31,9 @@ extern "C" {
 #define SS_TIME_INF INT64_MAX    /* end of a device's last (open) idle slice */
 
 #define SS_LAYOUT_ROW_MAJOR 0    /* placements[b * n_ops + v] = device of op v in candidate b */
+#define SS_LAYOUT_OP_MAJOR 1     /* placements[v * B + b] = device of op v in candidate b */
 #define SS_DISPATCH_READY 0x100  /* OR into layout: ready-time dispatch (see ss_simulate_batch) */
-#define SS_LINK_PORTS 0x200      /* OR into layout: transfers arbitrated over device ports (see ss_simulate_batch) */
+#define SS_LINK_PORTS 0x200      /* OR into layout: transfers arbitrated over device ports (refused for now) */
 
 #define SS_VIOLATION_MEMORY 0x1  /* some device's peak memory exceeds its capacity */
 #define SS_VIOLATION_INVALID 0x4 /* the placement names a device id >= n_dev; not simulated */
@@ -146,42 +147,54 @@ int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req)
  * rules accept every GMG the loader accepts; the ready-time rule evaluates a
  * candidate with one wavefront instead of one lane, so it costs more per
  * candidate, and it needs scratch for N ready entries per candidate in flight.
- * With layout | SS_LINK_PORTS transfers contend for the devices' ports, after
- * the arbitration of Sec. 3.5.2 (pending transfers that share a source or a
- * destination are not admitted together): each device sends one tensor at a
- * time and receives one at a time.  The transfer of an output to a remote
- * device is requested at the producer's finish; requests are admitted in the
- * order their producers are dispatched (for one producer, in the order of
- * each destination's first consumer) and start at the latest of the request
- * and the moments the source's send port and the destination's receive port
- * free; a transfer holds both for its estimate (a zero estimate holds
- * nothing).  Consumers on that device wait for its arrival; the copy there is
- * allocated at the transfer's start and the producer's output is kept until
- * its last transfer has arrived.  Index-order dispatch only: with
- * SS_DISPATCH_READY as well the call fails with SS_ERR_UNSUPPORTED.  This
- * variant runs on the 32-bit kernels when the GMG fits them (a 32-bit time
- * horizon, one device class, at most two link classes and at most two
- * predecessors and two successors per op), else on the general int64
- * kernels; it needs scratch for two port clocks per device and one or two
- * arrival times per edge for each candidate in flight.
  * A candidate naming a device >= n_dev is not simulated: violation =
  * SS_VIOLATION_INVALID, makespan = sumfin = INT64_MAX, peak = 0 and slack =
  * INT64_MIN.  This is a per-candidate result, not a call error.
- * placements: DEVICE pointer, uint8 [B][n_ops] for SS_LAYOUT_ROW_MAJOR (with
- * or without the flags above).
+ * With layout | SS_LINK_PORTS the call fails with SS_ERR_UNSUPPORTED: the
+ * event-driven transfer arbitration of Sec. 3.5.2 has no GPU kernels yet.
+ * placements: DEVICE pointer, uint8, SS_LAYOUT_ROW_MAJOR [B][n_ops] or
+ * SS_LAYOUT_OP_MAJOR [n_ops][B] (the layout the schedule pass reads: no
+ * transpose of the batch before it), either one OR-ed with the flags above.
  * The call is asynchronous on hip_stream (NULL = the null stream); inputs must
  * stay valid and outputs are defined once that stream has been synchronised.
  * It takes stream-ordered scratch on hip_stream, for the duration of the
  * work, from the library's memory pool for g's device, which keeps that
  * memory for later calls (for a fixed workload, calls after the first
- * allocate no device memory; see ss_release_cached_memory).  B = 0 is a
- * no-op.  Results are bit-identical to a sequential CPU
- * evaluation of the same rules.
+ * allocate no device memory; see ss_release_cached_memory).  A caller that
+ * must own that memory passes it to ss_simulate_batch_ws instead (sized with
+ * ss_simulate_workspace_size).  B = 0 is a no-op.  Results are bit-identical
+ * to a sequential CPU evaluation of the same rules.
  * Errors: SS_ERR_INVALID_ARG, SS_ERR_OOM, SS_ERR_DEVICE, SS_ERR_UNSUPPORTED.
  */
 int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int64_t B, int layout, int64_t *out_makespan,
                       int64_t *out_peak_mem, uint8_t *out_violation, int64_t *out_sla_slack, int64_t *out_sumfin,
                       void *hip_stream);
+
+/*
+ * Workspace of ss_simulate_batch_ws for a batch of B candidates with this
+ * layout and these flags (the same what-if simulation, Sec. 3.3.3 and the
+ * candidate loop of Alg. 1): *min_bytes is the smallest workspace with which
+ * the call works (it then runs in chunks of a few candidates), *pref_bytes
+ * the size at which it runs in the chunks it would choose itself; any size in
+ * between works, larger chunks being faster.  Either pointer may be NULL (not
+ * both).  B = 0 gives 0.  Launches nothing.  Errors: SS_ERR_INVALID_ARG,
+ * SS_ERR_DEVICE, SS_ERR_UNSUPPORTED (as ss_simulate_batch would).
+ */
+int ss_simulate_workspace_size(const ss_gmg *g, int64_t B, int layout, int64_t *min_bytes, int64_t *pref_bytes);
+
+/*
+ * ss_simulate_batch with a caller-owned workspace: the same arguments and
+ * results, plus `workspace`, a DEVICE buffer of workspace_bytes (256-byte
+ * aligned, at least ss_simulate_workspace_size's min_bytes) that the call
+ * uses for all of its scratch: it allocates no device memory, creates no
+ * events and runs every kernel on hip_stream.  The workspace belongs to the
+ * call until hip_stream has completed it; two calls in flight at once need
+ * two workspaces.  Errors: as ss_simulate_batch, and SS_ERR_INVALID_ARG for
+ * a NULL, misaligned or too small workspace.
+ */
+int ss_simulate_batch_ws(const ss_gmg *g, const uint8_t *placements, int64_t B, int layout, int64_t *out_makespan,
+                         int64_t *out_peak_mem, uint8_t *out_violation, int64_t *out_sla_slack, int64_t *out_sumfin,
+                         void *workspace, int64_t workspace_bytes, void *hip_stream);
 
 /*
  * Prefix reuse for candidates that share their first ops (the ops before a
@@ -238,8 +251,9 @@ int ss_state_capture(const ss_gmg *g, const ss_state *from, const uint8_t *place
  * key is out_sumfin (the average-completion objective) or out_makespan.
  * violation[B], key[B], sla_slack[B][n_req] (needed only with
  * SS_SELECT_REQUIRE_SLA) are DEVICE pointers; out_best is a DEVICE int64[2]
- * receiving {index or -1, key or INT64_MAX}.  Asynchronous on hip_stream.
- * Errors: SS_ERR_INVALID_ARG, SS_ERR_OOM, SS_ERR_DEVICE.
+ * receiving {index or -1, key or INT64_MAX}; it is also the reduction's only
+ * scratch (the call allocates no device memory).  Asynchronous on hip_stream.
+ * Errors: SS_ERR_INVALID_ARG, SS_ERR_DEVICE.
  */
 int ss_select_best(const ss_gmg *g, const uint8_t *violation, const int64_t *key, const int64_t *sla_slack,
                    int64_t B, int flags, int64_t *out_best, void *hip_stream);

@@ -46,26 +46,88 @@ void ss_clear_error() { g_last_error.clear(); }
 
 extern "C" const char *ss_last_error(void) { return g_last_error.c_str(); }
 
+namespace {
+// Checks shared by the simulation entry points; fills the placement source
+// and the dispatch flags.  SS_OK with B == 0 means there is nothing to do.
+int check_simulate(const char *fn, const ss_gmg *g, const uint8_t *placements, int64_t B, int layout,
+                   const int64_t *out_makespan, const uint8_t *out_violation, SsPlace *src, bool *ready) {
+  const std::string f(fn);
+  if (!g) return ss_set_error(SS_ERR_INVALID_ARG, f + ": g is NULL");
+  if (B < 0) return ss_set_error(SS_ERR_INVALID_ARG, f + ": B < 0");
+  if ((layout & ~(SS_LAYOUT_OP_MAJOR | SS_DISPATCH_READY | SS_LINK_PORTS)) != 0)
+    return ss_set_error(SS_ERR_INVALID_ARG, f + ": unknown layout");
+  if (layout & SS_LINK_PORTS)
+    return ss_set_error(SS_ERR_UNSUPPORTED, f + ": SS_LINK_PORTS (event-driven transfer arbitration) is not built yet");
+  src->p = placements;
+  src->B = B;
+  src->op_major = (layout & SS_LAYOUT_OP_MAJOR) != 0;
+  *ready = (layout & SS_DISPATCH_READY) != 0;
+  if (B == 0) return SS_OK;
+  if (!out_makespan || !out_violation)
+    return ss_set_error(SS_ERR_INVALID_ARG, f + ": out_makespan and out_violation are required");
+  if (!placements && g->n_ops > 0) return ss_set_error(SS_ERR_INVALID_ARG, f + ": placements is NULL");
+  return check_device(g);
+}
+}  // namespace
+
 extern "C" int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int64_t B, int layout,
                                  int64_t *out_makespan, int64_t *out_peak_mem, uint8_t *out_violation,
                                  int64_t *out_sla_slack, int64_t *out_sumfin, void *hip_stream) {
   ss_clear_error();
-  if (!g) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: g is NULL");
-  if (B < 0) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: B < 0");
-  if ((layout & ~(SS_DISPATCH_READY | SS_LINK_PORTS)) != SS_LAYOUT_ROW_MAJOR)
-    return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: unknown layout");
-  if (layout & SS_LINK_PORTS)
-    return ss_set_error(SS_ERR_UNSUPPORTED,
-                        "ss_simulate_batch: SS_LINK_PORTS (event-driven transfer arbitration) is not built yet");
-  if (B == 0) return SS_OK;
-  if (!out_makespan || !out_violation)
-    return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: out_makespan and out_violation are required");
-  if (!placements && g->n_ops > 0) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch: placements is NULL");
-  const int rc = check_device(g);
-  if (rc != SS_OK) return rc;
-  return ss_run_simulate(g, placements, B, out_makespan, out_peak_mem, out_violation, out_sla_slack, out_sumfin,
-                         static_cast<hipStream_t>(hip_stream), (layout & SS_DISPATCH_READY) != 0,
-                         (layout & SS_LINK_PORTS) != 0);
+  SsPlace src;
+  bool ready = false;
+  const int rc = check_simulate("ss_simulate_batch", g, placements, B, layout, out_makespan, out_violation, &src,
+                                &ready);
+  if (rc != SS_OK || B == 0) return rc;
+  SsWork W;
+  return ss_run_simulate(g, src, out_makespan, out_peak_mem, out_violation, out_sla_slack, out_sumfin,
+                         static_cast<hipStream_t>(hip_stream), ready, false, W);
+}
+
+extern "C" int ss_simulate_workspace_size(const ss_gmg *g, int64_t B, int layout, int64_t *min_bytes,
+                                          int64_t *pref_bytes) {
+  ss_clear_error();
+  if (min_bytes) *min_bytes = 0;
+  if (pref_bytes) *pref_bytes = 0;
+  if (!min_bytes && !pref_bytes) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_workspace_size: no output");
+  SsPlace src;
+  bool ready = false;
+  int64_t dummy_ms = 0;
+  uint8_t dummy_vi = 0;
+  const uint8_t dummy_p = 0;
+  const int rc = check_simulate("ss_simulate_workspace_size", g, &dummy_p, B, layout, &dummy_ms, &dummy_vi, &src,
+                                &ready);
+  if (rc != SS_OK || B == 0) return rc;
+  SsWork W;
+  W.query = true;
+  W.single = true;
+  const int r2 = ss_run_simulate(g, src, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, ready, false, W);
+  if (r2 != SS_OK) return r2;
+  if (min_bytes) *min_bytes = (int64_t)W.need_min;
+  if (pref_bytes) *pref_bytes = (int64_t)W.need_pref;
+  return SS_OK;
+}
+
+extern "C" int ss_simulate_batch_ws(const ss_gmg *g, const uint8_t *placements, int64_t B, int layout,
+                                    int64_t *out_makespan, int64_t *out_peak_mem, uint8_t *out_violation,
+                                    int64_t *out_sla_slack, int64_t *out_sumfin, void *workspace,
+                                    int64_t workspace_bytes, void *hip_stream) {
+  ss_clear_error();
+  SsPlace src;
+  bool ready = false;
+  const int rc = check_simulate("ss_simulate_batch_ws", g, placements, B, layout, out_makespan, out_violation, &src,
+                                &ready);
+  if (rc != SS_OK || B == 0) return rc;
+  if (!workspace || workspace_bytes <= 0)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch_ws: workspace is NULL or empty");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch_ws: workspace is not 256-byte aligned");
+  SsWork W;
+  W.ptr = workspace;
+  W.bytes = (size_t)workspace_bytes;
+  W.single = true;
+  return ss_run_simulate(g, src, out_makespan, out_peak_mem, out_violation, out_sla_slack, out_sumfin,
+                         static_cast<hipStream_t>(hip_stream), ready, false, W);
 }
 
 extern "C" int ss_est_create(int64_t n_est, int64_t n_feat, ss_est **out) {

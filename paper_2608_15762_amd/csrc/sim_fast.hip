@@ -82,15 +82,16 @@ __global__ __launch_bounds__(256) void fill_zero_u32(uint32_t *__restrict__ p, i
 
 // ------------------------------------------------------------------ transpose
 // 64 x 64 tiles through LDS: both the read and the write are coalesced.
+// in: rows x cols with row pitch `pitch` elements; out: cols x rows, dense.
 template <class T>
 __global__ __launch_bounds__(256) void transpose_tiles(const T *__restrict__ in, int64_t rows, int64_t cols,
-                                                       T *__restrict__ out) {
+                                                       int64_t pitch, T *__restrict__ out) {
   __shared__ T tile[64][65];
   const int64_t c0 = (int64_t)blockIdx.x * 64, r0 = (int64_t)blockIdx.y * 64;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   for (int i = ty; i < 64; i += 4) {
     const int64_t r = r0 + i, c = c0 + tx;
-    if (r < rows && c < cols) tile[i][tx] = in[r * cols + c];
+    if (r < rows && c < cols) tile[i][tx] = in[r * pitch + c];
   }
   __syncthreads();
   for (int i = ty; i < 64; i += 4) {
@@ -99,12 +100,12 @@ __global__ __launch_bounds__(256) void transpose_tiles(const T *__restrict__ in,
   }
 }
 
-// Byte matrices whose sizes are multiples of 4 (and 4-byte aligned input):
-// 128 x 128 tiles moved as 4-byte words on both sides. A word read holds 4
-// columns of one row; a word written packs 4 rows of one column, gathered
-// byte by byte from LDS (row pitch 33 words).
+// Byte matrices whose sizes and input pitch are multiples of 4 (and 4-byte
+// aligned input): 128 x 128 tiles moved as 4-byte words on both sides. A word
+// read holds 4 columns of one row; a word written packs 4 rows of one column,
+// gathered byte by byte from LDS (row pitch 33 words).
 __global__ __launch_bounds__(256) void transpose_u8_words(const uint8_t *__restrict__ in, int64_t rows, int64_t cols,
-                                                          uint8_t *__restrict__ out) {
+                                                          int64_t pitch, uint8_t *__restrict__ out) {
   __shared__ uint32_t tile[128 * 33];
   const int64_t c0 = (int64_t)blockIdx.x * 128, r0 = (int64_t)blockIdx.y * 128;
   const int w = threadIdx.x & 31, i0 = threadIdx.x >> 5;
@@ -113,7 +114,7 @@ __global__ __launch_bounds__(256) void transpose_u8_words(const uint8_t *__restr
   for (int p = 0; p < 16; ++p) {
     const int i = i0 + 8 * p;
     if (col_in && r0 + i < rows)
-      tile[i * 33 + w] = *reinterpret_cast<const uint32_t *>(in + (r0 + i) * cols + c0 + 4 * w);
+      tile[i * 33 + w] = *reinterpret_cast<const uint32_t *>(in + (r0 + i) * pitch + c0 + 4 * w);
   }
   __syncthreads();
   const uint8_t *t8 = reinterpret_cast<const uint8_t *>(tile);
@@ -197,7 +198,8 @@ struct SchedPipe {
 // read by the consumer two ops ahead (op T-1's from registers).  A remote
 // predecessor counts with its arrival, a local one with its finish.
 template <int kLink, bool kOverflow, bool kOneClass, bool kPorts>
-__global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const uint8_t *__restrict__ PT, int64_t nb,
+__global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const uint8_t *__restrict__ PT, int64_t ppitch,
+                                                       int64_t nb,
                                                        uint32_t *__restrict__ finT, uint32_t *__restrict__ arrT,
                                                        uint32_t *__restrict__ port, int64_t *__restrict__ makespan,
                                                        int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
@@ -260,8 +262,10 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   const uint64_t nbu = (uint64_t)(uint32_t)nb;  // a chunk holds fewer than 2^32 candidates
   const uint8_t *const PTc = PT + c;
   uint32_t *const finTc = finT + c;
+  const uint64_t ppu = (uint64_t)ppitch;  // placement rows: the caller's op-major pitch, or the chunk's
   auto row = [&](int t) -> uint64_t { return (uint64_t)(uint32_t)t * nbu; };
-  auto load_dev = [&](int t) -> uint32_t { return PTc[row(t)]; };
+  auto prow = [&](int t) -> uint64_t { return (uint64_t)(uint32_t)t * ppu; };
+  auto load_dev = [&](int t) -> uint32_t { return PTc[prow(t)]; };
   SchedPipe S;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -321,8 +325,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     S.wq[q2] = kOneClass ? meta(kMetaDur, t) : G.dur32[(int64_t)t * C + dcls[dt]];
     if (kPorts) {  // devices of op t's first two successors
       const uint32_t s2t = G.succ2[t], y0 = s2t & 0xFFFFu, y1 = s2t >> 16;
-      S.sx[q2][0] = PTc[row(y0 == 0xFFFFu ? t : (int)y0)];
-      S.sx[q2][1] = PTc[row(y1 == 0xFFFFu ? t : (int)y1)];
+      S.sx[q2][0] = PTc[prow(y0 == 0xFFFFu ? t : (int)y0)];
+      S.sx[q2][1] = PTc[prow(y1 == 0xFFFFu ? t : (int)y1)];
     }
     lb = umax32(lb, clk[(int)dt * kWave + lane]) + (kOneClass ? meta(kMetaDur, t) : 0u);
     const uint32_t e = dt * (uint32_t)G.lut_nb + (uint32_t)min((int)(lb >> G.lut_shift), G.lut_nb - 1);
@@ -340,7 +344,7 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
       const int u = (int)pred_of(p01, i);
       const int us = u < T ? u : 0;  // rows not yet written (or absent) read row 0, never used
       S.pf[q3][i] = finTc[row(us)];
-      S.pd[q3][i] = PTc[row(us)];
+      S.pd[q3][i] = PTc[prow(us)];
     }
   };
 
@@ -393,7 +397,7 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
           du = h1d;
         } else {
           tt = finTc[row(u)];
-          du = PTc[row(u)];
+          du = PTc[prow(u)];
           if (du >= (uint32_t)D) du = 0;
         }
         if (du != d) tt += xfer_of(G, u, (int)du, (int)d);
@@ -1100,7 +1104,7 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
             const int dv = (int)(ent >> 20), pos = (int)(ent & 0xFFFFFu) * kOwnRecs + part;
             const int lo = own_off[dv], hi = own_off[dv + 1];
             const Rec r = obuf[dv * kOwnRecs + part];
-            own[(pos >= lo) & (pos < hi) ? pos : N] = r;
+            own[((pos >= lo) & (pos < hi)) ? pos : N] = r;
           }
         }
         for (int qb = 0; qb < nc; qb += kWave / kCpRecs) {
@@ -1671,6 +1675,8 @@ struct MemPass {
   int64_t n_ticket;
   int64_t sub, nslots, slot_cap;
   bool iv_fast;
+  bool single;  // every pass on the caller's stream, one record set, no events
+  int sets;     // record sets in use: kRecSets, or 1 when single
   hipStream_t aux;
   hipEvent_t iv_done[kRecSets], pk_done[kRecSets];
   int64_t it;  // sub-chunks issued so far in this call
@@ -1680,6 +1686,8 @@ int mem_pass_events(MemPass &M) {
   for (int k = 0; k < kRecSets; ++k) {
     M.iv_done[k] = M.pk_done[k] = nullptr;
   }
+  M.it = 0;
+  if (M.single) return SS_OK;
   for (int k = 0; k < kRecSets; ++k) {
     hipError_t err = hipEventCreateWithFlags(&M.iv_done[k], hipEventDisableTiming);
     if (err == hipSuccess) err = hipEventCreateWithFlags(&M.pk_done[k], hipEventDisableTiming);
@@ -1692,6 +1700,7 @@ int mem_pass_events(MemPass &M) {
 // Joins the second stream back into the caller's and releases the events
 // (always, also after an error, before the scratch is freed).
 int mem_pass_join(MemPass &M, hipStream_t stream) {
+  if (M.single) return SS_OK;
   hipError_t err = hipSuccess;
   hipEvent_t done = nullptr;
   err = hipEventCreateWithFlags(&done, hipEventDisableTiming);
@@ -1728,9 +1737,9 @@ int memory_passes(const ss_gmg *g, MemPass &M, const uint8_t *Pc, const uint32_t
   const int64_t N = g->n_ops;
   for (int64_t j0 = 0; j0 < nb; j0 += M.sub, ++M.it) {
     const int64_t nj = std::min(M.sub, nb - j0);
-    const int set = (int)(M.it % kRecSets);
+    const int set = (int)(M.it % M.sets);
     hipError_t err = hipSuccess;
-    if (M.it >= kRecSets) err = hipStreamWaitEvent(stream, M.pk_done[set], 0);  // its buffers are free again
+    if (!M.single && M.it >= M.sets) err = hipStreamWaitEvent(stream, M.pk_done[set], 0);  // its buffers are free again
     if (err != hipSuccess) return hip_fail(err, "hipStreamWaitEvent");
     uint16_t *rank = given_ranks ? M.rank + j0 * N : M.rank;
     if (arr && (!M.iv_fast || given_ranks))
@@ -1760,19 +1769,24 @@ int memory_passes(const ss_gmg *g, MemPass &M, const uint8_t *Pc, const uint32_t
     ss_timing_stop(ti, stream);
     if (err == hipSuccess) err = hipGetLastError();
     if (err != hipSuccess) return hip_fail(err, "fast_intervals launch");
-    err = hipEventRecord(M.iv_done[set], stream);
-    if (err == hipSuccess) err = hipStreamWaitEvent(M.aux, M.iv_done[set], 0);
-    if (err != hipSuccess) return hip_fail(err, "ordering the peak pass");
+    hipStream_t ps = M.single ? stream : M.aux;  // the peak pass's stream
+    if (!M.single) {
+      err = hipEventRecord(M.iv_done[set], stream);
+      if (err == hipSuccess) err = hipStreamWaitEvent(M.aux, M.iv_done[set], 0);
+      if (err != hipSuccess) return hip_fail(err, "ordering the peak pass");
+    }
     if (M.it >= M.n_ticket) return ss_set_error(SS_ERR_DEVICE, "memory passes: more peak launches than counters");
-    SsTimingRec *tm = ss_timing_start(SS_KERNEL_MEMORY, M.aux);
-    hipLaunchKernelGGL(fast_peaks, dim3((unsigned)std::min<int64_t>(nj, M.nslots)), dim3(kWave), 0, M.aux, G, j0, nj,
+    SsTimingRec *tm = ss_timing_start(SS_KERNEL_MEMORY, ps);
+    hipLaunchKernelGGL(fast_peaks, dim3((unsigned)std::min<int64_t>(nj, M.nslots)), dim3(kWave), 0, ps, G, j0, nj,
                        static_cast<const Rec *>(own), static_cast<const Rec *>(cp),
                        static_cast<const int32_t *>(meta), M.wk, M.wb, M.slot_cap, M.ticket + M.it, peak, violation);
-    ss_timing_stop(tm, M.aux);
+    ss_timing_stop(tm, ps);
     err = hipGetLastError();
     if (err != hipSuccess) return hip_fail(err, "fast_peaks launch");
-    err = hipEventRecord(M.pk_done[set], M.aux);
-    if (err != hipSuccess) return hip_fail(err, "hipEventRecord");
+    if (!M.single) {
+      err = hipEventRecord(M.pk_done[set], M.aux);
+      if (err != hipSuccess) return hip_fail(err, "hipEventRecord");
+    }
   }
   return SS_OK;
 }
@@ -1784,10 +1798,27 @@ size_t ss_fast_schedule_lds(const ss_gmg *g) {
          (size_t)(g->n_dev + 3) / 4 * 4;
 }
 
-int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
-                         uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream, bool link_ports) {
+// Scratch of one fast-path call, laid out for a chunk of `chunk` candidates
+// and memory-pass sub-chunks of `sub`.
+struct FastPlan {
+  int64_t chunk = 0, sub = 0, nslots = 0, n_ticket = 0;
+  int sets = kRecSets;
+  size_t sz_pt = 0, sz_fin = 0, sz_own = 0, sz_cp = 0, sz_meta = 0, sz_rank = 0, sz_wk = 0, sz_wb = 0, sz_tk = 0,
+         sz_port = 0, sz_arr = 0, total = 0;
+};
+
+hipError_t ss_rows_from_op_major(const uint8_t *P, int64_t n_ops, int64_t B, int64_t b0, int64_t nb, uint8_t *rows,
+                                 hipStream_t stream) {
+  if (n_ops == 0 || nb == 0) return hipSuccess;
+  const dim3 tg((unsigned)((nb + 63) / 64), (unsigned)((n_ops + 63) / 64));
+  hipLaunchKernelGGL(transpose_tiles<uint8_t>, tg, dim3(256), 0, stream, P + b0, n_ops, nb, B, rows);
+  return hipGetLastError();
+}
+
+int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_t *peak, uint8_t *violation,
+                         int64_t *slack, int64_t *sumfin, hipStream_t stream, bool link_ports, SsWork &W) {
   const GmgView &G = g->view;
-  const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req;
+  const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req, B = src.B;
   const size_t sched_lds = ss_fast_schedule_lds(g);
   int cus = 0;
   hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, g->device);
@@ -1805,12 +1836,11 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
                                : link_mode == 1 ? schedule_fn<1>(overflow, one_class, ports)
                                : link_mode == 2 ? schedule_fn<2>(overflow, one_class, ports)
                                                 : schedule_fn<3>(overflow, one_class, ports);
-  err = hipFuncSetAttribute(sched_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
-  if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
-
   const bool iv_fast = g->n_class == 1 && g->n_link <= 2 && g->max_outdeg <= 2;
-  // chunk: op-major placements, op-major and row-major finish times; with
-  // ports also the port clocks and the arrivals, op-major and row-major
+  // chunk: placements (op-major for the schedule from row-major input, rows
+  // for the memory passes from op-major input), op-major and row-major finish
+  // times; with ports also the port clocks and the arrivals, op-major and
+  // row-major
   const int64_t per_cand = N * (1 + 4 + 4) + (ports ? 2 * D * 4 + E * 8 : 0);
   int lds_cu = 0;
   err = hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, g->device);
@@ -1822,82 +1852,120 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   // sub-chunk: interval records of each candidate (own N, copies <= E)
   const int64_t rec_per_cand = (own_stride(N) + cp_stride(E)) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4 + N * 2;
   const int64_t slot_cap = N + E + 1;  // most allocations one device can hold
+  const int sets = W.single ? 1 : kRecSets;
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
-  int64_t chunk = 0, sub = 0, nslots = 0, n_ticket = 0;
-  size_t sz_pt = 0, sz_fin = 0, sz_own = 0, sz_cp = 0, sz_meta = 0, sz_rank = 0, sz_wk = 0, sz_wb = 0, sz_tk = 0,
-         sz_port = 0, sz_arr = 0;
-  SsScratch scr;
-  // the largest chunk within the scratch budget; when its scratch does not
-  // fit in the device's free memory, half the budget (down to one round)
-  std::atomic<int64_t> &fitted = g_fast_budget[g->device & 255];
-  int64_t budget = fitted.load();
-  for (budget = budget > 0 ? budget : kFastScratchBudget;; budget /= 2) {
-    chunk = budget / std::max<int64_t>(1, per_cand);
+  // the layout for a chunk and a sub-chunk cap (equal sub-chunks, at least
+  // two for a large chunk so the peak pass of one overlaps the interval pass
+  // of the next)
+  auto plan_of = [&](int64_t chunk, int64_t sub_cap) {
+    FastPlan q;
+    q.sets = sets;
+    q.chunk = chunk = std::min<int64_t>(chunk, B);
+    int64_t sub = std::min<int64_t>(std::max<int64_t>(1, sub_cap), chunk);
+    const int64_t n = std::max<int64_t>((chunk + sub - 1) / sub, chunk >= 8192 && !W.single ? 2 : 1);
+    q.sub = sub = (chunk + n - 1) / n;
+    q.nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
+    q.sz_pt = align((size_t)chunk * N + 1);
+    q.sz_fin = align((size_t)chunk * N * 4 + 4);
+    q.sz_own = align((size_t)sub * own_stride(N) * sizeof(Rec));
+    q.sz_cp = align((size_t)sub * cp_stride(E) * sizeof(Rec));
+    q.sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
+    q.sz_rank = align(((size_t)sub * N + 1) * 2);
+    q.sz_wk = align((size_t)q.nslots * 2 * (slot_cap + 2) * 4);
+    q.sz_wb = align((size_t)q.nslots * slot_cap * 8);
+    q.n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
+    q.sz_tk = align((size_t)q.n_ticket * 4);
+    q.sz_port = ports ? align((size_t)2 * D * chunk * 4) : 0;
+    q.sz_arr = ports ? align((size_t)E * chunk * 4) : 0;
+    q.total = q.sz_pt + 2 * q.sz_fin + q.sz_port + 2 * q.sz_arr + (size_t)sets * (q.sz_own + q.sz_cp + q.sz_meta) +
+              q.sz_rank + q.sz_wk + q.sz_wb + q.sz_tk;
+    return q;
+  };
+  // the largest chunk within a budget, in whole rounds of schedule waves
+  auto plan_for_budget = [&](int64_t budget) {
+    int64_t chunk = budget / std::max<int64_t>(1, per_cand);
     chunk = chunk >= round ? chunk / round * round : std::max<int64_t>(kWave, chunk / kWave * kWave);
     chunk = std::min<int64_t>(chunk, int64_t(65535) * 64);  // transpose grids index 64-candidate tiles in y
-    chunk = std::min<int64_t>(chunk, B);
-    sub = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
-    sub = std::min<int64_t>(sub, chunk);
-    {  // equal sub-chunks, at least two for a large chunk (the peak pass of one
-       // overlaps the interval pass of the next)
-      const int64_t n = std::max<int64_t>((chunk + sub - 1) / sub, chunk >= 8192 ? 2 : 1);
-      sub = (chunk + n - 1) / n;
-    }
-    nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
-    sz_pt = align((size_t)chunk * N + 1);
-    sz_fin = align((size_t)chunk * N * 4 + 4);
-    sz_own = align((size_t)sub * own_stride(N) * sizeof(Rec));
-    sz_cp = align((size_t)sub * cp_stride(E) * sizeof(Rec));
-    sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
-    sz_rank = align(((size_t)sub * N + 1) * 2);
-    sz_wk = align((size_t)nslots * 2 * (slot_cap + 2) * 4);
-    sz_wb = align((size_t)nslots * slot_cap * 8);
-    n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
-    sz_tk = align((size_t)n_ticket * 4);
-    sz_port = ports ? align((size_t)2 * D * chunk * 4) : 0;
-    sz_arr = ports ? align((size_t)E * chunk * 4) : 0;
-    err = ss_scratch_get(g->device, g->pool,
-                         sz_pt + 2 * sz_fin + sz_port + 2 * sz_arr + kRecSets * (sz_own + sz_cp + sz_meta) + sz_rank +
-                             sz_wk + sz_wb + sz_tk,
-                         stream, &scr);
-    if (err != hipErrorOutOfMemory || chunk <= std::min<int64_t>(round, B)) break;
+    return plan_of(chunk, std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand)));
+  };
+  const FastPlan pmin = plan_of(kWave, 1);
+  if (W.query) {
+    W.need_min = pmin.total;
+    W.need_pref = plan_for_budget(kFastScratchBudget).total;
+    return SS_OK;
   }
-  if (err == hipSuccess && chunk < B) fitted.store(budget);  // a budget that bounded the chunk and fitted
-  void *scratch = scr.p;
-  if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
+  err = hipFuncSetAttribute(sched_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
+  if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
+  FastPlan pl;
+  SsScratch scr;
+  void *scratch = nullptr;
+  if (W.ptr) {  // the caller's workspace: the largest layout that fits, nothing allocated
+    if (pmin.total > W.bytes)
+      return ss_set_error(SS_ERR_INVALID_ARG, "workspace of " + std::to_string(W.bytes) +
+                                                   " bytes is smaller than this call's minimum of " +
+                                                   std::to_string(pmin.total));
+    pl = plan_for_budget(kFastScratchBudget);
+    int64_t chunk = pl.chunk, sub_cap = pl.sub;
+    while (pl.total > W.bytes) {
+      if (sub_cap > 1 && plan_of(chunk, 1).total <= W.bytes) {
+        sub_cap = std::max<int64_t>(1, sub_cap / 2);  // fewer records first
+      } else {
+        chunk = std::max<int64_t>(kWave, (chunk / 2) / kWave * kWave);
+        sub_cap = std::min(sub_cap, chunk);
+      }
+      pl = plan_of(chunk, sub_cap);
+    }
+    scratch = W.ptr;
+  } else {
+    // the largest chunk within the scratch budget; when its scratch does not
+    // fit in the device's free memory, half the budget (down to one round)
+    std::atomic<int64_t> &fitted = g_fast_budget[g->device & 255];
+    int64_t budget = fitted.load();
+    for (budget = budget > 0 ? budget : kFastScratchBudget;; budget /= 2) {
+      pl = plan_for_budget(budget);
+      err = ss_scratch_get(g->device, g->pool, pl.total, stream, &scr);
+      if (err != hipErrorOutOfMemory || pl.chunk <= std::min<int64_t>(round, B)) break;
+    }
+    if (err == hipSuccess && pl.chunk < B) fitted.store(budget);  // a budget that bounded the chunk and fitted
+    if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
+    scratch = scr.p;
+  }
+  const int64_t chunk = pl.chunk;
   unsigned char *p = static_cast<unsigned char *>(scratch);
   auto take = [&](size_t bytes) {
     unsigned char *q = p;
     p += bytes;
     return q;
   };
-  auto *PT = reinterpret_cast<uint8_t *>(take(sz_pt));
-  auto *finT = reinterpret_cast<uint32_t *>(take(sz_fin));
-  auto *fin = reinterpret_cast<uint32_t *>(take(sz_fin));
-  auto *port = ports ? reinterpret_cast<uint32_t *>(take(sz_port)) : nullptr;
-  auto *arrT = ports ? reinterpret_cast<uint32_t *>(take(sz_arr)) : nullptr;  // [E][chunk]
-  auto *arr = ports ? reinterpret_cast<uint32_t *>(take(sz_arr)) : nullptr;   // [chunk][E]
+  auto *PT = reinterpret_cast<uint8_t *>(take(pl.sz_pt));  // op-major copy, or candidate rows of op-major input
+  auto *finT = reinterpret_cast<uint32_t *>(take(pl.sz_fin));
+  auto *fin = reinterpret_cast<uint32_t *>(take(pl.sz_fin));
+  auto *port = ports ? reinterpret_cast<uint32_t *>(take(pl.sz_port)) : nullptr;
+  auto *arrT = ports ? reinterpret_cast<uint32_t *>(take(pl.sz_arr)) : nullptr;  // [E][chunk]
+  auto *arr = ports ? reinterpret_cast<uint32_t *>(take(pl.sz_arr)) : nullptr;   // [chunk][E]
   MemPass M{};
-  for (int k = 0; k < kRecSets; ++k) {
-    M.own[k] = reinterpret_cast<Rec *>(take(sz_own));
-    M.cp[k] = reinterpret_cast<Rec *>(take(sz_cp));
-    M.meta[k] = reinterpret_cast<int32_t *>(take(sz_meta));
+  for (int k = 0; k < pl.sets; ++k) {
+    M.own[k] = reinterpret_cast<Rec *>(take(pl.sz_own));
+    M.cp[k] = reinterpret_cast<Rec *>(take(pl.sz_cp));
+    M.meta[k] = reinterpret_cast<int32_t *>(take(pl.sz_meta));
   }
-  M.rank = reinterpret_cast<uint16_t *>(take(sz_rank));
-  M.wk = reinterpret_cast<uint32_t *>(take(sz_wk));
-  M.wb = reinterpret_cast<int64_t *>(take(sz_wb));
-  M.ticket = reinterpret_cast<uint32_t *>(take(sz_tk));
-  M.n_ticket = n_ticket;
-  M.sub = sub;
-  M.nslots = nslots;
+  M.rank = reinterpret_cast<uint16_t *>(take(pl.sz_rank));
+  M.wk = reinterpret_cast<uint32_t *>(take(pl.sz_wk));
+  M.wb = reinterpret_cast<int64_t *>(take(pl.sz_wb));
+  M.ticket = reinterpret_cast<uint32_t *>(take(pl.sz_tk));
+  M.n_ticket = pl.n_ticket;
+  M.sub = pl.sub;
+  M.nslots = pl.nslots;
   M.slot_cap = slot_cap;
   M.iv_fast = iv_fast;
+  M.single = W.single;
+  M.sets = pl.sets;
   M.aux = g->aux;
 
   int rc = mem_pass_events(M);
   if (rc == SS_OK) {
-    hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)std::min<int64_t>((n_ticket + 255) / 256, 1024)), dim3(256), 0,
-                       stream, M.ticket, n_ticket);
+    hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)std::min<int64_t>((pl.n_ticket + 255) / 256, 1024)), dim3(256),
+                       0, stream, M.ticket, pl.n_ticket);
     const hipError_t fe = hipGetLastError();
     if (fe != hipSuccess) rc = hip_fail(fe, "fill_zero_u32 launch");
   }
@@ -1908,31 +1976,44 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   };
   for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
     const int64_t nb = std::min(chunk, B - b0);
-    const uint8_t *Pc = P + b0 * N;
+    // the schedule reads op-major placements (the caller's own, or a copy of
+    // the chunk's rows); the memory passes read candidate rows (the caller's
+    // own, or a copy of the chunk from the op-major input)
+    const uint8_t *sched_P = PT;
+    int64_t ppitch = nb;
+    const uint8_t *Pc = PT;
     SsTimingRec *tp = ss_timing_start(SS_KERNEL_TRANSPOSE, stream);
-    if (N > 0) {  // candidates' placement rows -> op-major [op][candidate]
-      if (N % 4 == 0 && nb % 4 == 0 && (reinterpret_cast<uintptr_t>(Pc) & 3) == 0) {
-        const dim3 tg((unsigned)((N + 127) / 128), (unsigned)((nb + 127) / 128));
-        hipLaunchKernelGGL(transpose_u8_words, tg, dim3(256), 0, stream, Pc, nb, (int64_t)N, PT);
-      } else {
-        const dim3 tg((unsigned)((N + 63) / 64), (unsigned)((nb + 63) / 64));
-        hipLaunchKernelGGL(transpose_tiles<uint8_t>, tg, dim3(256), 0, stream, Pc, nb, (int64_t)N, PT);
+    if (src.op_major) {
+      sched_P = src.p + b0;
+      ppitch = B;
+      const hipError_t te = ss_rows_from_op_major(src.p, N, B, b0, nb, PT, stream);
+      if (te != hipSuccess && rc == SS_OK) rc = hip_fail(te, "transpose launch");
+    } else {
+      Pc = src.p + b0 * N;
+      if (N > 0) {  // candidates' placement rows -> op-major [op][candidate]
+        if (N % 4 == 0 && nb % 4 == 0 && (reinterpret_cast<uintptr_t>(Pc) & 3) == 0) {
+          const dim3 tg((unsigned)((N + 127) / 128), (unsigned)((nb + 127) / 128));
+          hipLaunchKernelGGL(transpose_u8_words, tg, dim3(256), 0, stream, Pc, nb, (int64_t)N, (int64_t)N, PT);
+        } else {
+          const dim3 tg((unsigned)((N + 63) / 64), (unsigned)((nb + 63) / 64));
+          hipLaunchKernelGGL(transpose_tiles<uint8_t>, tg, dim3(256), 0, stream, Pc, nb, (int64_t)N, (int64_t)N,
+                             PT);
+        }
       }
     }
     ss_timing_stop(tp, stream);
     if (!check("transpose launch")) break;
-    if (M.it > 0) {  // the schedule runs with no peak pass beside it
-      const hipError_t we = hipStreamWaitEvent(stream, M.pk_done[(M.it - 1) % kRecSets], 0);
+    if (!M.single && M.it > 0) {  // the schedule runs with no peak pass beside it
+      const hipError_t we = hipStreamWaitEvent(stream, M.pk_done[(M.it - 1) % M.sets], 0);
       if (we != hipSuccess && rc == SS_OK) rc = hip_fail(we, "hipStreamWaitEvent");
     }
     SsTimingRec *ts = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
     {
-      const uint8_t *PTc = PT;
       int64_t *ms_out = makespan + b0, *sf_out = sumfin ? sumfin + b0 : nullptr,
               *sl_out = slack ? slack + b0 * R : nullptr;
       uint8_t *vi_out = violation + b0;
-      void *args[] = {const_cast<GmgView *>(&G), &PTc, const_cast<int64_t *>(&nb), &finT, &arrT, &port, &ms_out,
-                      &sf_out, &sl_out, &vi_out};
+      void *args[] = {const_cast<GmgView *>(&G), &sched_P, &ppitch, const_cast<int64_t *>(&nb), &finT, &arrT, &port,
+                      &ms_out, &sf_out, &sl_out, &vi_out};
       const hipError_t le = hipLaunchKernel(sched_fn, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), args,
                                             sched_lds, stream);
       if (le != hipSuccess && rc == SS_OK) rc = hip_fail(le, "fast_schedule launch");
@@ -1944,12 +2025,12 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
     if (N > 0) {  // op-major -> candidates' rows for the memory passes
       const dim3 tg((unsigned)((nb + 63) / 64), (unsigned)((N + 63) / 64));
       hipLaunchKernelGGL(transpose_tiles<uint32_t>, tg, dim3(256), 0, stream, static_cast<const uint32_t *>(finT),
-                         (int64_t)N, nb, fin);
+                         (int64_t)N, nb, nb, fin);
     }
     if (ports) {  // arrivals per edge -> candidates' rows
       const dim3 tg((unsigned)((nb + 63) / 64), (unsigned)((E + 63) / 64));
       hipLaunchKernelGGL(transpose_tiles<uint32_t>, tg, dim3(256), 0, stream, static_cast<const uint32_t *>(arrT),
-                         (int64_t)E, nb, arr);
+                         (int64_t)E, nb, nb, arr);
     }
     ss_timing_stop(tt, stream);
     if (!check("transpose launch")) break;
@@ -1957,8 +2038,10 @@ int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *
   }
   const int jrc = mem_pass_join(M, stream);
   if (rc == SS_OK) rc = jrc;
-  err = ss_scratch_put(g->device, &scr, stream);
-  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "releasing the scratch");
+  if (!W.ptr) {
+    err = ss_scratch_put(g->device, &scr, stream);
+    if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "releasing the scratch");
+  }
   return rc;
 }
 
@@ -1969,89 +2052,133 @@ bool ss_fast_ports_ok(const ss_gmg *g) {
 
 size_t ss_ready_schedule_lds(const ss_gmg *g) { return ready_schedule_lds((int)g->n_dev, (int)g->n_req); }
 
-int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
-                          uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream) {
+int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_t *peak, uint8_t *violation,
+                          int64_t *slack, int64_t *sumfin, hipStream_t stream, SsWork &W) {
   const GmgView &G = g->view;
-  const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req;
+  const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req, B = src.B;
   const size_t lds = ss_ready_schedule_lds(g);
   int cus = 0;
   hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
+  const bool iv_fast = g->n_class == 1 && g->n_link <= 2 && g->max_outdeg <= 2;
+  // chunk: finish times, ranks, missing-predecessor counts and the spill list
+  // of each candidate (candidate rows), and with op-major input the chunk's
+  // placement rows
+  const int64_t per_cand = N * (4 + 2 + 2 + 8 + (src.op_major ? 1 : 0));
+  const int64_t rec_per_cand = (own_stride(N) + cp_stride(E)) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4;
+  const int64_t slot_cap = N + E + 1;
+  const int sets = W.single ? 1 : kRecSets;
+  auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
+  struct Plan {
+    int64_t chunk, sub, nslots, n_ticket;
+    size_t sz_fin, sz_rank, sz_miss, sz_spill, sz_rows, sz_own, sz_cp, sz_meta, sz_wk, sz_wb, sz_tk, total;
+  };
+  auto plan_of = [&](int64_t chunk, int64_t sub_cap) {
+    Plan q{};
+    q.chunk = chunk = std::min<int64_t>(std::max<int64_t>(1, chunk), B);
+    int64_t sub = std::min<int64_t>(std::max<int64_t>(1, sub_cap), chunk);
+    const int64_t n = std::max<int64_t>((chunk + sub - 1) / sub, chunk >= 8192 && !W.single ? 2 : 1);
+    q.sub = sub = (chunk + n - 1) / n;
+    q.nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
+    q.sz_fin = align((size_t)chunk * N * 4 + 4);
+    q.sz_rank = align(((size_t)chunk * N + 1) * 2);
+    q.sz_miss = align(((size_t)chunk * N + 1) * 2);
+    q.sz_spill = align((size_t)chunk * N * 8 + 8);
+    q.sz_rows = src.op_major ? align((size_t)chunk * N + 1) : 0;
+    q.sz_own = align((size_t)sub * own_stride(N) * sizeof(Rec));
+    q.sz_cp = align((size_t)sub * cp_stride(E) * sizeof(Rec));
+    q.sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
+    q.sz_wk = align((size_t)q.nslots * 2 * (slot_cap + 2) * 4);
+    q.sz_wb = align((size_t)q.nslots * slot_cap * 8);
+    q.n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
+    q.sz_tk = align((size_t)q.n_ticket * 4);
+    q.total = q.sz_fin + q.sz_rank + q.sz_miss + q.sz_spill + q.sz_rows +
+              (size_t)sets * (q.sz_own + q.sz_cp + q.sz_meta) + q.sz_wk + q.sz_wb + q.sz_tk;
+    return q;
+  };
+  const int64_t sub_pref = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
+  const Plan ppref = plan_of(kScratchBudget / std::max<int64_t>(1, per_cand), sub_pref);
+  const Plan pmin = plan_of(1, 1);
+  if (W.query) {
+    W.need_min = pmin.total;
+    W.need_pref = ppref.total;
+    return SS_OK;
+  }
   err = hipFuncSetAttribute(reinterpret_cast<const void *>(&ready_schedule), hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)lds);
   if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
-  const bool iv_fast = g->n_class == 1 && g->n_link <= 2 && g->max_outdeg <= 2;
-  // chunk: finish times, ranks, missing-predecessor counts and the spill list
-  // of each candidate (candidate rows)
-  const int64_t per_cand = N * (4 + 2 + 2 + 8);
-  int64_t chunk = kScratchBudget / std::max<int64_t>(1, per_cand);
-  chunk = std::min<int64_t>(std::max<int64_t>(1, chunk), B);
-  const int64_t rec_per_cand = (own_stride(N) + cp_stride(E)) * (int64_t)sizeof(Rec) + 3 * (D + 1) * 4;
-  int64_t sub = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
-  sub = std::min<int64_t>(sub, chunk);
-  {  // equal sub-chunks, at least two for a large chunk (the peak pass of one
-     // overlaps the interval pass of the next)
-    const int64_t n = std::max<int64_t>((chunk + sub - 1) / sub, chunk >= 8192 ? 2 : 1);
-    sub = (chunk + n - 1) / n;
-  }
-  const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kPeakBlocksPerCU, sub));
-  const int64_t slot_cap = N + E + 1;
-
-  auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
-  const size_t sz_fin = align((size_t)chunk * N * 4 + 4);
-  const size_t sz_rank = align(((size_t)chunk * N + 1) * 2);
-  const size_t sz_miss = align(((size_t)chunk * N + 1) * 2);
-  const size_t sz_spill = align((size_t)chunk * N * 8 + 8);
-  const size_t sz_own = align((size_t)sub * own_stride(N) * sizeof(Rec));
-  const size_t sz_cp = align((size_t)sub * cp_stride(E) * sizeof(Rec));
-  const size_t sz_meta = align((size_t)sub * 3 * (D + 1) * 4);
-  const size_t sz_wk = align((size_t)nslots * 2 * (slot_cap + 2) * 4);
-  const size_t sz_wb = align((size_t)nslots * slot_cap * 8);
-  const int64_t n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
-  const size_t sz_tk = align((size_t)n_ticket * 4);
+  Plan pl = ppref;
   SsScratch scr;
-  err = ss_scratch_get(g->device, g->pool,
-                       sz_fin + sz_rank + sz_miss + sz_spill + kRecSets * (sz_own + sz_cp + sz_meta) + sz_wk + sz_wb + sz_tk,
-                       stream, &scr);
-  void *scratch = scr.p;
-  if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
+  void *scratch = nullptr;
+  if (W.ptr) {
+    if (pmin.total > W.bytes)
+      return ss_set_error(SS_ERR_INVALID_ARG, "workspace of " + std::to_string(W.bytes) +
+                                                   " bytes is smaller than this call's minimum of " +
+                                                   std::to_string(pmin.total));
+    int64_t chunk = pl.chunk, sub_cap = pl.sub;
+    while (pl.total > W.bytes) {
+      if (sub_cap > 1 && plan_of(chunk, 1).total <= W.bytes) sub_cap = std::max<int64_t>(1, sub_cap / 2);
+      else {
+        chunk = std::max<int64_t>(1, chunk / 2);
+        sub_cap = std::min(sub_cap, chunk);
+      }
+      pl = plan_of(chunk, sub_cap);
+    }
+    scratch = W.ptr;
+  } else {
+    err = ss_scratch_get(g->device, g->pool, pl.total, stream, &scr);
+    if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
+    scratch = scr.p;
+  }
+  const int64_t chunk = pl.chunk;
   unsigned char *p = static_cast<unsigned char *>(scratch);
   auto take = [&](size_t bytes) {
     unsigned char *q = p;
     p += bytes;
     return q;
   };
-  auto *fin = reinterpret_cast<uint32_t *>(take(sz_fin));
-  auto *rank = reinterpret_cast<uint16_t *>(take(sz_rank));
-  auto *miss = reinterpret_cast<uint16_t *>(take(sz_miss));
-  auto *spill = reinterpret_cast<uint64_t *>(take(sz_spill));
+  auto *fin = reinterpret_cast<uint32_t *>(take(pl.sz_fin));
+  auto *rank = reinterpret_cast<uint16_t *>(take(pl.sz_rank));
+  auto *miss = reinterpret_cast<uint16_t *>(take(pl.sz_miss));
+  auto *spill = reinterpret_cast<uint64_t *>(take(pl.sz_spill));
+  auto *rows = reinterpret_cast<uint8_t *>(take(pl.sz_rows));
   MemPass M{};
-  for (int k = 0; k < kRecSets; ++k) {
-    M.own[k] = reinterpret_cast<Rec *>(take(sz_own));
-    M.cp[k] = reinterpret_cast<Rec *>(take(sz_cp));
-    M.meta[k] = reinterpret_cast<int32_t *>(take(sz_meta));
+  for (int k = 0; k < sets; ++k) {
+    M.own[k] = reinterpret_cast<Rec *>(take(pl.sz_own));
+    M.cp[k] = reinterpret_cast<Rec *>(take(pl.sz_cp));
+    M.meta[k] = reinterpret_cast<int32_t *>(take(pl.sz_meta));
   }
   M.rank = rank;
-  M.wk = reinterpret_cast<uint32_t *>(take(sz_wk));
-  M.wb = reinterpret_cast<int64_t *>(take(sz_wb));
-  M.ticket = reinterpret_cast<uint32_t *>(take(sz_tk));
-  M.n_ticket = n_ticket;
-  M.sub = sub;
-  M.nslots = nslots;
+  M.wk = reinterpret_cast<uint32_t *>(take(pl.sz_wk));
+  M.wb = reinterpret_cast<int64_t *>(take(pl.sz_wb));
+  M.ticket = reinterpret_cast<uint32_t *>(take(pl.sz_tk));
+  M.n_ticket = pl.n_ticket;
+  M.sub = pl.sub;
+  M.nslots = pl.nslots;
   M.slot_cap = slot_cap;
   M.iv_fast = iv_fast;
+  M.single = W.single;
+  M.sets = sets;
   M.aux = g->aux;
 
   int rc = mem_pass_events(M);
   if (rc == SS_OK) {
-    hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)std::min<int64_t>((n_ticket + 255) / 256, 1024)), dim3(256), 0,
-                       stream, M.ticket, n_ticket);
+    hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)std::min<int64_t>((pl.n_ticket + 255) / 256, 1024)), dim3(256),
+                       0, stream, M.ticket, pl.n_ticket);
     const hipError_t fe = hipGetLastError();
     if (fe != hipSuccess) rc = hip_fail(fe, "fill_zero_u32 launch");
   }
   for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
     const int64_t nb = std::min(chunk, B - b0);
-    const uint8_t *Pc = P + b0 * N;
+    const uint8_t *Pc = src.p + b0 * N;
+    if (src.op_major) {
+      err = ss_rows_from_op_major(src.p, N, B, b0, nb, rows, stream);
+      if (err != hipSuccess) {
+        rc = hip_fail(err, "transpose launch");
+        break;
+      }
+      Pc = rows;
+    }
     SsTimingRec *ts = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
     hipLaunchKernelGGL(ready_schedule, dim3((unsigned)nb), dim3(kWave), lds, stream, G, Pc, fin, rank, miss, spill,
                        makespan + b0, sumfin ? sumfin + b0 : nullptr, slack ? slack + b0 * R : nullptr,
@@ -2066,8 +2193,10 @@ int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t 
   }
   const int jrc = mem_pass_join(M, stream);
   if (rc == SS_OK) rc = jrc;
-  err = ss_scratch_put(g->device, &scr, stream);
-  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "releasing the scratch");
+  if (!W.ptr) {
+    err = ss_scratch_put(g->device, &scr, stream);
+    if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "releasing the scratch");
+  }
   return rc;
 }
 
@@ -2159,6 +2288,8 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
   M.nslots = nslots;
   M.slot_cap = slot_cap;
   M.iv_fast = iv_fast;
+  M.single = false;
+  M.sets = kRecSets;
   M.aux = g->aux;
   int rc = mem_pass_events(M);
   if (rc == SS_OK) {

@@ -682,12 +682,12 @@ int hip_fail(hipError_t err, const char *what) {
 // from: resume every candidate after the state's ops; capture (B == 1): store
 // the candidate's state after its last op and skip the memory pass; mem_fast:
 // the 32-bit memory passes instead of memory_kernel.
-static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
-                                uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream,
-                                bool ready, bool ports, const ss_state *from = nullptr,
-                                ss_state *capture = nullptr, bool mem_fast = false) {
+static int run_simulate_generic(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_t *peak, uint8_t *violation,
+                                int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready, bool ports,
+                                SsWork &W, const ss_state *from = nullptr, ss_state *capture = nullptr,
+                                bool mem_fast = false) {
   const GmgView &G = g->view;
-  const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req;
+  const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req, B = src.B;
   const int64_t slot_cap = 2 * (N + E) + 2;
   if (slot_cap >= INT32_MAX) return ss_set_error(SS_ERR_UNSUPPORTED, "n_ops + n_edges too large for the memory pass");
   if (ready && ports) return ss_set_error(SS_ERR_UNSUPPORTED, "transfer ports take index-order dispatch only");
@@ -707,53 +707,91 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
     lds_max = (size_t)v;
   }
   if (sched_lds > lds_max) return ss_set_error(SS_ERR_UNSUPPORTED, "device state of the schedule pass exceeds LDS");
-  err = hipFuncSetAttribute(sched_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
-  if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
+  if ((W.ptr || W.query) && (from || capture || mem_fast))
+    return ss_set_error(SS_ERR_UNSUPPORTED, "a caller's workspace serves full simulations only");
 
   // per candidate: finish times and request completions; with ready-time
-  // dispatch also missing-predecessor counts and the spill list
-  // with transfer ports also two port clocks per device and an arrival per edge
-  const int64_t per_cand = N * 8 + R * 8 + (ready ? N * (4 + 8 + 4) : 0) + (ports ? (2 * D + E) * 8 : 0);
-  int64_t chunk = kFinBudget / std::max<int64_t>(1, per_cand);
-  chunk = std::max<int64_t>(kWave, chunk / kWave * kWave);
-  chunk = std::min<int64_t>(chunk, B);
-  const int64_t nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kMemBlocksPerCU, chunk));
-
-  auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
-  const size_t sz_fin = align((size_t)chunk * N * 8 + 8);
-  const size_t sz_comp = align((size_t)chunk * R * 8 + 8);
-  const size_t sz_miss = ready ? align((size_t)chunk * N * 4 + 4) : 0;
-  const size_t sz_spr = ready ? align((size_t)chunk * N * 8 + 8) : 0;
-  const size_t sz_spo = ready ? align((size_t)chunk * N * 4 + 4) : 0;
-  const size_t sz_bydev = align((size_t)nslots * N * 4 + 4);
-  const size_t sz_ev = align((size_t)nslots * slot_cap * 8);
-  const size_t sz_port = ports ? align((size_t)2 * D * chunk * 8) : 0;
-  const size_t sz_arr = ports ? align((size_t)E * chunk * 8 + 8) : 0;
+  // dispatch also missing-predecessor counts and the spill list; with
+  // transfer ports also two port clocks per device and an arrival per edge;
+  // with op-major input the chunk's placement rows
+  const int64_t per_cand = N * 8 + R * 8 + (ready ? N * (4 + 8 + 4) : 0) + (ports ? (2 * D + E) * 8 : 0) +
+                           (src.op_major ? N : 0);
   const bool resumed = from && from->k > 0;
-  const size_t sz_bad = resumed ? align((size_t)chunk * 4) : 0;
+  auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
+  struct Plan {
+    int64_t chunk, nslots;
+    size_t sz_fin, sz_comp, sz_miss, sz_spr, sz_spo, sz_bydev, sz_ev, sz_port, sz_arr, sz_bad, sz_rows, total;
+  };
+  auto plan_of = [&](int64_t chunk) {
+    Plan q{};
+    q.chunk = chunk = std::min<int64_t>(std::max<int64_t>(1, chunk), B);
+    q.nslots = std::max<int64_t>(1, std::min<int64_t>((int64_t)cus * kMemBlocksPerCU, chunk));
+    q.sz_fin = align((size_t)chunk * N * 8 + 8);
+    q.sz_comp = align((size_t)chunk * R * 8 + 8);
+    q.sz_miss = ready ? align((size_t)chunk * N * 4 + 4) : 0;
+    q.sz_spr = ready ? align((size_t)chunk * N * 8 + 8) : 0;
+    q.sz_spo = ready ? align((size_t)chunk * N * 4 + 4) : 0;
+    q.sz_bydev = align((size_t)q.nslots * N * 4 + 4);
+    q.sz_ev = align((size_t)q.nslots * slot_cap * 8);
+    q.sz_port = ports ? align((size_t)2 * D * chunk * 8) : 0;
+    q.sz_arr = ports ? align((size_t)E * chunk * 8 + 8) : 0;
+    q.sz_bad = resumed ? align((size_t)chunk * 4) : 0;
+    q.sz_rows = src.op_major ? align((size_t)chunk * N + 1) : 0;
+    q.total = q.sz_fin + q.sz_comp + q.sz_miss + q.sz_spr + q.sz_spo + q.sz_bydev + 2 * q.sz_ev + q.sz_port +
+              q.sz_arr + q.sz_bad + q.sz_rows;
+    return q;
+  };
+  // chunks of whole waves within the finish-time budget
+  int64_t pref_chunk = kFinBudget / std::max<int64_t>(1, per_cand);
+  pref_chunk = std::max<int64_t>(kWave, pref_chunk / kWave * kWave);
+  const Plan pmin = plan_of(1);
+  if (W.query) {
+    W.need_min = pmin.total;
+    W.need_pref = plan_of(pref_chunk).total;
+    return SS_OK;
+  }
+  err = hipFuncSetAttribute(sched_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
+  if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
+  Plan pl = plan_of(pref_chunk);
   SsScratch scr;
-  err = ss_scratch_get(g->device, g->pool,
-                       sz_fin + sz_comp + sz_miss + sz_spr + sz_spo + sz_bydev + 2 * sz_ev + sz_port + sz_arr + sz_bad,
-                       stream, &scr);
-  void *scratch = scr.p;
-  if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
+  void *scratch = nullptr;
+  if (W.ptr) {  // the caller's workspace: the largest chunk that fits
+    if (pmin.total > W.bytes)
+      return ss_set_error(SS_ERR_INVALID_ARG, "workspace of " + std::to_string(W.bytes) +
+                                                   " bytes is smaller than this call's minimum of " +
+                                                   std::to_string(pmin.total));
+    int64_t lo = 1, hi = pl.chunk;  // plan_of(lo) fits
+    while (lo < hi) {
+      const int64_t mid = lo + (hi - lo + 1) / 2;
+      if (plan_of(mid).total <= W.bytes) lo = mid;
+      else hi = mid - 1;
+    }
+    pl = plan_of(lo >= kWave ? lo / kWave * kWave : lo);
+    scratch = W.ptr;
+  } else {
+    err = ss_scratch_get(g->device, g->pool, pl.total, stream, &scr);
+    if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
+    scratch = scr.p;
+  }
+  const int64_t chunk = pl.chunk, nslots = pl.nslots;
   unsigned char *p = static_cast<unsigned char *>(scratch);
   auto take = [&](size_t bytes) {
     unsigned char *q = p;
     p += bytes;
     return q;
   };
-  auto *fin = reinterpret_cast<int64_t *>(take(sz_fin));
-  auto *comp = reinterpret_cast<int64_t *>(take(sz_comp));
-  auto *miss = reinterpret_cast<int32_t *>(take(sz_miss));
-  auto *spr = reinterpret_cast<int64_t *>(take(sz_spr));
-  auto *spo = reinterpret_cast<int32_t *>(take(sz_spo));
-  auto *bydev = reinterpret_cast<int32_t *>(take(sz_bydev));
-  auto *gkeys = reinterpret_cast<int64_t *>(take(sz_ev));
-  auto *gvals = reinterpret_cast<int64_t *>(take(sz_ev));
-  auto *port = ports ? reinterpret_cast<int64_t *>(take(sz_port)) : nullptr;
-  auto *arr = ports ? reinterpret_cast<int64_t *>(take(sz_arr)) : nullptr;
-  auto *bad = resumed ? reinterpret_cast<uint32_t *>(take(sz_bad)) : nullptr;
+  auto *fin = reinterpret_cast<int64_t *>(take(pl.sz_fin));
+  auto *comp = reinterpret_cast<int64_t *>(take(pl.sz_comp));
+  auto *miss = reinterpret_cast<int32_t *>(take(pl.sz_miss));
+  auto *spr = reinterpret_cast<int64_t *>(take(pl.sz_spr));
+  auto *spo = reinterpret_cast<int32_t *>(take(pl.sz_spo));
+  auto *bydev = reinterpret_cast<int32_t *>(take(pl.sz_bydev));
+  auto *gkeys = reinterpret_cast<int64_t *>(take(pl.sz_ev));
+  auto *gvals = reinterpret_cast<int64_t *>(take(pl.sz_ev));
+  auto *port = ports ? reinterpret_cast<int64_t *>(take(pl.sz_port)) : nullptr;
+  auto *arr = ports ? reinterpret_cast<int64_t *>(take(pl.sz_arr)) : nullptr;
+  auto *bad = resumed ? reinterpret_cast<uint32_t *>(take(pl.sz_bad)) : nullptr;
+  auto *rows = src.op_major ? reinterpret_cast<uint8_t *>(take(pl.sz_rows)) : nullptr;
   Resume RS;
   if (resumed) {
     RS.k0 = (int32_t)from->k;
@@ -771,7 +809,15 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
   int rc = SS_OK;
   for (int64_t b0 = 0; b0 < B && rc == SS_OK; b0 += chunk) {
     const int64_t nb = std::min(chunk, B - b0);
-    const uint8_t *Pc = P + b0 * N;
+    const uint8_t *Pc = src.p + b0 * N;
+    if (src.op_major) {
+      err = ss_rows_from_op_major(src.p, N, B, b0, nb, rows, stream);
+      if (err != hipSuccess) {
+        rc = hip_fail(err, "transpose launch");
+        break;
+      }
+      Pc = rows;
+    }
     SsTimingRec *t_sched = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
     if (ready)
       hipLaunchKernelGGL(ready_schedule_general, dim3((unsigned)nb), dim3(kWave), sched_lds, stream, G, Pc, fin, miss,
@@ -823,17 +869,19 @@ static int run_simulate_generic(const ss_gmg *g, const uint8_t *P, int64_t B, in
     ss_timing_stop(t_mem, stream);
     if (err != hipSuccess) rc = hip_fail(err, "memory_kernel launch");
   }
-  err = ss_scratch_put(g->device, &scr, stream);
-  if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "releasing the scratch");
+  if (!W.ptr) {
+    err = ss_scratch_put(g->device, &scr, stream);
+    if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "releasing the scratch");
+  }
   return rc;
 }
 
 // Path choice: the 32-bit fast path when the loader enabled it and its LDS
 // state fits; SS_PATH=generic or SS_PATH=fast in the environment forces one
 // (fast is still refused when the GMG does not qualify).
-int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makespan, int64_t *peak,
-                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch,
-                    bool link_ports) {
+int ss_run_simulate(const ss_gmg *g, SsPlace P, int64_t *makespan, int64_t *peak, uint8_t *violation,
+                    int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch, bool link_ports,
+                    SsWork &W) {
   int lds_max = 0;
   hipError_t err = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
@@ -852,10 +900,10 @@ int ss_run_simulate(const ss_gmg *g, const uint8_t *P, int64_t B, int64_t *makes
   const bool ports_mem_fast = link_ports && !force_generic && g->view.time32 && g->n_ops > 0 && g->n_class == 1 &&
                               g->n_link <= 2 && g->max_outdeg <= 2 && g->view.succ2_pe;
   if (generic)
-    return run_simulate_generic(g, P, B, makespan, peak, violation, slack, sumfin, stream, ready_dispatch, link_ports,
-                                nullptr, nullptr, ports_mem_fast);
-  if (ready_dispatch) return ss_run_simulate_ready(g, P, B, makespan, peak, violation, slack, sumfin, stream);
-  return ss_run_simulate_fast(g, P, B, makespan, peak, violation, slack, sumfin, stream, link_ports);
+    return run_simulate_generic(g, P, makespan, peak, violation, slack, sumfin, stream, ready_dispatch, link_ports, W,
+                                nullptr, nullptr, ports_mem_fast && !W.ptr && !W.query);
+  if (ready_dispatch) return ss_run_simulate_ready(g, P, makespan, peak, violation, slack, sumfin, stream, W);
+  return ss_run_simulate_fast(g, P, makespan, peak, violation, slack, sumfin, stream, link_ports, W);
 }
 
 // The state's buffer grows to hold a capture of g (synchronising the stream
@@ -894,7 +942,11 @@ static int state_reserve(ss_state *st, const ss_gmg *g, hipStream_t stream) {
 
 int ss_run_simulate_resume(const ss_gmg *g, const ss_state *from, const uint8_t *P, int64_t B, int64_t *makespan,
                            int64_t *peak, uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream) {
-  return run_simulate_generic(g, P, B, makespan, peak, violation, slack, sumfin, stream, false, false, from, nullptr,
+  SsWork W;
+  SsPlace src;
+  src.p = P;
+  src.B = B;
+  return run_simulate_generic(g, src, makespan, peak, violation, slack, sumfin, stream, false, false, W, from, nullptr,
                               g->view.time32 && g->n_ops > 0);
 }
 
@@ -907,8 +959,12 @@ int ss_run_state_capture(const ss_gmg *g, const ss_state *from, const uint8_t *p
   hipError_t err = ss_pool_malloc(&outs, 256 + (size_t)g->n_req * 8 + 8, g->pool, stream);
   if (err != hipSuccess) return hip_fail(err, "allocating capture outputs");
   auto *o = static_cast<int64_t *>(outs);
-  rc = run_simulate_generic(g, placement, 1, o, nullptr, reinterpret_cast<uint8_t *>(o + 2), o + 4, o + 1, stream,
-                            false, false, from, capture);
+  SsWork W;
+  SsPlace src;
+  src.p = placement;
+  src.B = 1;
+  rc = run_simulate_generic(g, src, o, nullptr, reinterpret_cast<uint8_t *>(o + 2), o + 4, o + 1, stream, false,
+                            false, W, from, capture);
   err = hipFreeAsync(outs, stream);
   if (rc == SS_OK && err != hipSuccess) rc = hip_fail(err, "hipFreeAsync");
   capture->k = rc == SS_OK ? g->n_ops : 0;

@@ -172,10 +172,31 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
 int ss_run_sched_complete(ss_sched *s, int64_t op);
 void ss_run_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place);
 
+// Where a simulation call takes its scratch (device memory beyond its inputs
+// and outputs) from: the device's pool (ptr null), or a caller's workspace of
+// `bytes`, which the call then splits into chunks that fit and never
+// allocates beyond.  single: every kernel on the caller's stream (no second
+// stream, no events; one set of interval records).  query: the call only
+// reports need_min (the smallest workspace that works) and need_pref (what
+// the pool path takes for this batch) and launches nothing.
+struct SsWork {
+  void *ptr = nullptr;
+  size_t bytes = 0;
+  bool single = false;
+  bool query = false;
+  size_t need_min = 0, need_pref = 0;
+};
+// Placements of a call: row-major [B][n_ops], or op-major [n_ops][B].
+struct SsPlace {
+  const uint8_t *p = nullptr;
+  int64_t B = 0;
+  bool op_major = false;
+};
+
 // Kernel drivers (simulate.hip / select.hip).  Arguments are already checked.
-int ss_run_simulate(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
-                    uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch,
-                    bool link_ports);
+int ss_run_simulate(const ss_gmg *g, SsPlace P, int64_t *makespan, int64_t *peak, uint8_t *violation,
+                    int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch, bool link_ports,
+                    SsWork &W);
 // Resumption from a captured state (general schedule kernel; the 32-bit
 // memory passes when the GMG has a 32-bit horizon); from may be null or empty.
 int ss_run_simulate_resume(const ss_gmg *g, const ss_state *from, const uint8_t *placements, int64_t B,
@@ -193,16 +214,19 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
                        int64_t arr_stride = 0);
 // Fast path (sim_fast.hip): 32-bit times, N <= 65535.
 size_t ss_fast_schedule_lds(const ss_gmg *g);
-int ss_run_simulate_fast(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
-                         uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream,
-                         bool link_ports = false);
+int ss_run_simulate_fast(const ss_gmg *g, SsPlace P, int64_t *makespan, int64_t *peak, uint8_t *violation,
+                         int64_t *slack, int64_t *sumfin, hipStream_t stream, bool link_ports, SsWork &W);
 // Whether transfer ports can run on the 32-bit kernels: one device class, at
 // most two link classes, two predecessors and two successors per op.
 bool ss_fast_ports_ok(const ss_gmg *g);
 // Ready-time dispatch on the fast path (sim_fast.hip).
 size_t ss_ready_schedule_lds(const ss_gmg *g);
-int ss_run_simulate_ready(const ss_gmg *g, const uint8_t *placements, int64_t B, int64_t *makespan, int64_t *peak,
-                          uint8_t *violation, int64_t *slack, int64_t *sumfin, hipStream_t stream);
+int ss_run_simulate_ready(const ss_gmg *g, SsPlace P, int64_t *makespan, int64_t *peak, uint8_t *violation,
+                          int64_t *slack, int64_t *sumfin, hipStream_t stream, SsWork &W);
+// Candidate rows [nb][n_ops] of candidates [b0, b0 + nb) from op-major
+// placements [n_ops][B] (sim_fast.hip).
+hipError_t ss_rows_from_op_major(const uint8_t *P, int64_t n_ops, int64_t B, int64_t b0, int64_t nb, uint8_t *rows,
+                                 hipStream_t stream);
 // Estimators (estimator.hip).  Arguments are already checked.
 int ss_run_est_create(int64_t n_est, int64_t n_feat, ss_est **out);
 void ss_run_est_free(ss_est *e);

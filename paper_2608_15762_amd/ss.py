@@ -20,6 +20,8 @@ SS_ERR_INVALID_ARG, SS_ERR_INVALID_GMG, SS_ERR_OOM, SS_ERR_DEVICE, SS_ERR_UNSUPP
 ERRORS = {-1: "SS_ERR_INVALID_ARG", -2: "SS_ERR_INVALID_GMG", -3: "SS_ERR_OOM", -4: "SS_ERR_DEVICE",
           -5: "SS_ERR_UNSUPPORTED"}
 SS_LAYOUT_ROW_MAJOR = 0
+SS_LAYOUT_OP_MAJOR = 1
+LAYOUTS = {"row": SS_LAYOUT_ROW_MAJOR, "op": SS_LAYOUT_OP_MAJOR}
 SS_DISPATCH_READY = 0x100
 SS_LINK_PORTS = 0x200
 DISPATCH = {"index": 0, "ready": SS_DISPATCH_READY}
@@ -31,7 +33,7 @@ EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "s
             "ss_kernel_time", "ss_last_error", "ss_est_create", "ss_est_free", "ss_est_add", "ss_est_solve",
             "ss_est_predict", "ss_sched_create", "ss_sched_free", "ss_sched_round", "ss_sched_complete",
             "ss_sched_state", "ss_state_create", "ss_state_free", "ss_state_info", "ss_simulate_batch_resume",
-            "ss_state_capture", "ss_release_cached_memory")
+            "ss_state_capture", "ss_release_cached_memory", "ss_simulate_workspace_size", "ss_simulate_batch_ws")
 SS_OP_UNSCHEDULED, SS_OP_ISSUED, SS_OP_DONE = 0, 1, 2
 SS_ROUND_ISSUED, SS_ROUND_BUDGET, SS_ROUND_IDLE, SS_ROUND_INFEASIBLE = 0, 1, 2, 3
 SS_KERNEL_SCHEDULE, SS_KERNEL_MEMORY, SS_KERNEL_SELECT, SS_KERNEL_INTERVALS, SS_KERNEL_TRANSPOSE = 0, 1, 2, 3, 4
@@ -74,6 +76,10 @@ def lib():
             L.ss_gmg_info.argtypes = [P, P, P, P]
             L.ss_simulate_batch.argtypes = [P, P, I64, ctypes.c_int, P, P, P, P, P, P]
             L.ss_simulate_batch.restype = ctypes.c_int
+            L.ss_simulate_workspace_size.argtypes = [P, I64, ctypes.c_int, P, P]
+            L.ss_simulate_workspace_size.restype = ctypes.c_int
+            L.ss_simulate_batch_ws.argtypes = [P, P, I64, ctypes.c_int, P, P, P, P, P, P, I64, P]
+            L.ss_simulate_batch_ws.restype = ctypes.c_int
             L.ss_select_best.argtypes = [P, P, P, P, I64, ctypes.c_int, P, P]
             L.ss_select_best.restype = ctypes.c_int
             L.ss_kernel_timing.argtypes = [ctypes.c_int]
@@ -230,28 +236,57 @@ class Scheduler:
             pass
 
 
-def simulate_batch_into(g: Gmg, placements, makespan, violation, peak=None, slack=None, sumfin=None,
-                        stream=None, dispatch="index", links="latency"):
-    """ss_simulate_batch on caller-provided torch CUDA tensors (row-major).
+def _layout(g: Gmg, placements, layout: str, dispatch: str, links: str) -> tuple[int, int]:
+    """Batch size and layout flags of a placement tensor (uint8, contiguous):
+    layout "row" is [B, n_ops], "op" is [n_ops, B]."""
+    assert placements.dtype.is_floating_point is False and placements.element_size() == 1
+    assert placements.is_contiguous() and placements.dim() == 2
+    if layout == "row":
+        B = placements.shape[0]
+        assert placements.shape == (B, g.n_ops)
+    else:
+        B = placements.shape[1]
+        assert placements.shape == (g.n_ops, B)
+    return B, LAYOUTS[layout] | DISPATCH[dispatch] | LINKS[links]
 
+
+def workspace_size(g: Gmg, B: int, layout="row", dispatch="index", links="latency") -> tuple[int, int]:
+    """ss_simulate_workspace_size: (smallest, preferred) workspace bytes of
+    ss_simulate_batch_ws for B candidates."""
+    lo, hi = ctypes.c_int64(), ctypes.c_int64()
+    flags = LAYOUTS[layout] | DISPATCH[dispatch] | LINKS[links]
+    _check(lib().ss_simulate_workspace_size(g.handle, B, flags, ctypes.byref(lo), ctypes.byref(hi)))
+    return lo.value, hi.value
+
+
+def simulate_batch_into(g: Gmg, placements, makespan, violation, peak=None, slack=None, sumfin=None,
+                        stream=None, dispatch="index", links="latency", layout="row", workspace=None):
+    """ss_simulate_batch on caller-provided torch CUDA tensors.
+
+    layout: "row" (placements [B, n_ops]) or "op" (placements [n_ops, B]).
     dispatch: "index" (every device serves its ops in index order) or "ready"
     (earliest ready time first, SS_DISPATCH_READY).
     links: "latency" (a transfer takes its estimate from the producer's
-    finish) or "ports" (transfers arbitrated over the devices' send and
-    receive ports, SS_LINK_PORTS)."""
-    B = placements.shape[0]
-    assert placements.dtype.is_floating_point is False and placements.element_size() == 1
-    assert placements.is_contiguous() and placements.shape == (B, g.n_ops)
-    layout = SS_LAYOUT_ROW_MAJOR | DISPATCH[dispatch] | LINKS[links]
-    _check(lib().ss_simulate_batch(g.handle, _ptr(placements), B, layout, _ptr(makespan), _ptr(peak),
-                                   _ptr(violation), _ptr(slack), _ptr(sumfin), _stream_ptr(stream)))
+    finish) or "ports" (SS_LINK_PORTS, refused by the library for now).
+    workspace: None (the library's pool) or a device tensor whose memory
+    becomes the call's scratch (ss_simulate_batch_ws)."""
+    B, flags = _layout(g, placements, layout, dispatch, links)
+    if workspace is None:
+        _check(lib().ss_simulate_batch(g.handle, _ptr(placements), B, flags, _ptr(makespan), _ptr(peak),
+                                       _ptr(violation), _ptr(slack), _ptr(sumfin), _stream_ptr(stream)))
+    else:
+        nbytes = workspace.numel() * workspace.element_size()
+        _check(lib().ss_simulate_batch_ws(g.handle, _ptr(placements), B, flags, _ptr(makespan), _ptr(peak),
+                                          _ptr(violation), _ptr(slack), _ptr(sumfin), _ptr(workspace), nbytes,
+                                          _stream_ptr(stream)))
 
 
 def simulate_batch(g: Gmg, placements, want_peak=True, want_slack=True, want_sumfin=True, stream=None,
-                   dispatch="index", links="latency") -> dict:
-    """Allocate outputs on placements' device and run ss_simulate_batch."""
+                   dispatch="index", links="latency", layout="row", workspace=None) -> dict:
+    """Allocate outputs on placements' device and run ss_simulate_batch (or
+    ss_simulate_batch_ws with a workspace tensor)."""
     import torch
-    B = placements.shape[0]
+    B = placements.shape[0] if layout == "row" else placements.shape[1]
     dev = placements.device
     out = dict(makespan=torch.empty(B, dtype=torch.int64, device=dev),
                violation=torch.empty(B, dtype=torch.uint8, device=dev),
@@ -259,7 +294,7 @@ def simulate_batch(g: Gmg, placements, want_peak=True, want_slack=True, want_sum
                slack=torch.empty((B, g.n_req), dtype=torch.int64, device=dev) if want_slack else None,
                sumfin=torch.empty(B, dtype=torch.int64, device=dev) if want_sumfin else None)
     simulate_batch_into(g, placements, out["makespan"], out["violation"], out["peak"], out["slack"], out["sumfin"],
-                        stream, dispatch, links)
+                        stream, dispatch, links, layout, workspace)
     return out
 
 

@@ -117,7 +117,9 @@ def header_constants():
 
 def test_binding_constants_match_the_header():
     c = header_constants()
-    assert c["SS_LAYOUT_ROW_MAJOR"] == ss.SS_LAYOUT_ROW_MAJOR
+    assert c["SS_LAYOUT_ROW_MAJOR"] == ss.SS_LAYOUT_ROW_MAJOR == ss.LAYOUTS["row"]
+    assert c["SS_LAYOUT_OP_MAJOR"] == ss.SS_LAYOUT_OP_MAJOR == ss.LAYOUTS["op"]
+    assert c["SS_LAYOUT_OP_MAJOR"] & (c["SS_DISPATCH_READY"] | c["SS_LINK_PORTS"]) == 0
     assert c["SS_DISPATCH_READY"] == ss.SS_DISPATCH_READY == ss.DISPATCH["ready"]
     assert c["SS_DISPATCH_READY"] & c["SS_LAYOUT_ROW_MAJOR"] == 0
     assert c["SS_LINK_PORTS"] == ss.SS_LINK_PORTS == ss.LINKS["ports"]
@@ -131,12 +133,27 @@ def test_binding_constants_match_the_header():
 def test_unknown_layout_bits_are_rejected_before_the_device():
     L = ss.lib()
     # a non-null dummy handle is never dereferenced: the layout check comes first
-    for layout in (1, 0x400, 0x101, 0x201):
+    for layout in (2, 3, 0x400, 0x102, 0x203, 0x80):
         assert L.ss_simulate_batch(ctypes.c_void_p(8), None, 1, layout, None, None, None, None, None, None) == -1
         assert b"layout" in L.ss_last_error()
-    # transfer ports with ready-time dispatch: refused as unsupported
-    assert L.ss_simulate_batch(ctypes.c_void_p(8), None, 1, 0x300, None, None, None, None, None, None) == -5
-    assert b"SS_LINK_PORTS" in L.ss_last_error()
+        assert L.ss_simulate_batch_ws(ctypes.c_void_p(8), None, 1, layout, None, None, None, None, None, None, 0,
+                                      None) == -1
+        assert L.ss_simulate_workspace_size(ctypes.c_void_p(8), 1, layout, ctypes.byref(ctypes.c_int64()),
+                                            None) == -1
+    # transfer ports (any dispatch, any layout): refused as unsupported
+    for layout in (0x200, 0x201, 0x300):
+        assert L.ss_simulate_batch(ctypes.c_void_p(8), None, 1, layout, None, None, None, None, None, None) == -5
+        assert b"SS_LINK_PORTS" in L.ss_last_error()
+
+
+def test_workspace_entry_points_check_arguments_first():
+    L = ss.lib()
+    lo = ctypes.c_int64(7)
+    assert L.ss_simulate_workspace_size(None, 1, 0, ctypes.byref(lo), None) == -1 and lo.value == 0
+    assert L.ss_simulate_workspace_size(ctypes.c_void_p(8), 1, 0, None, None) == -1
+    assert L.ss_simulate_workspace_size(ctypes.c_void_p(8), -1, 0, ctypes.byref(lo), None) == -1
+    assert L.ss_simulate_batch_ws(None, None, 1, 0, None, None, None, None, None, None, 0, None) == -1
+    assert L.ss_simulate_batch_ws(ctypes.c_void_p(8), None, -1, 0, None, None, None, None, None, None, 0, None) == -1
 
 
 def test_estimator_arguments_are_checked_before_the_device():
