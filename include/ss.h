@@ -197,6 +197,24 @@ int ss_simulate_batch_ws(const ss_gmg *g, const uint8_t *placements, int64_t B, 
                          void *workspace, int64_t workspace_bytes, void *hip_stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * ss_simulate_batch with the same arguments and results, whose scratch is a
+ * fixed array of 128 MiB per GPU inside the library (held from the first call
+ * on that GPU until the process ends).  It calls no hipMalloc or hipFree,
+ * creates no events and runs every kernel on hip_stream; a batch is processed
+ * in chunks that fit the array.  Every call on one GPU shares that array, so
+ * calls that overlap on one GPU (other streams, other threads) race: order
+ * them.  A batch whose smallest scratch (ss_simulate_workspace_size's
+ * min_bytes) exceeds the array fails with SS_ERR_INVALID_ARG before anything
+ * is launched.  Errors: as ss_simulate_batch, and SS_ERR_INVALID_ARG for such
+ * a batch.
+ */
+int ss_simulate_batch_noalloc(const ss_gmg *g, const uint8_t *placements, int64_t B, int layout,
+                              int64_t *out_makespan, int64_t *out_peak_mem, uint8_t *out_violation,
+                              int64_t *out_sla_slack, int64_t *out_sumfin, void *hip_stream);
+
+/*
  * Prefix reuse for candidates that share their first ops (the ops before a
  * batch in Alg. 1's rounds, Sec. 3.4.2).  A state holds one simulated
  * candidate after the first k ops of a GMG: their finish times, every

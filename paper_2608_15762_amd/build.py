@@ -10,7 +10,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libss.so")
-SOURCES = ["abi.cpp", "gmg_load.cpp", "sched.cpp", "simulate.hip", "sim_fast.hip", "select.hip", "estimator.hip"]
+SOURCES = ["abi.cpp", "gmg_load.cpp", "sched.cpp", "simulate.hip", "sim_fast.hip", "select.hip", "estimator.hip",
+           "noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall",
          # keep the compiler from forming packed fp32 instructions

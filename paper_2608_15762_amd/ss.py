@@ -33,7 +33,8 @@ EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "s
             "ss_kernel_time", "ss_last_error", "ss_est_create", "ss_est_free", "ss_est_add", "ss_est_solve",
             "ss_est_predict", "ss_sched_create", "ss_sched_free", "ss_sched_round", "ss_sched_complete",
             "ss_sched_state", "ss_state_create", "ss_state_free", "ss_state_info", "ss_simulate_batch_resume",
-            "ss_state_capture", "ss_release_cached_memory", "ss_simulate_workspace_size", "ss_simulate_batch_ws")
+            "ss_state_capture", "ss_release_cached_memory", "ss_simulate_workspace_size", "ss_simulate_batch_ws",
+            "ss_simulate_batch_noalloc")
 SS_OP_UNSCHEDULED, SS_OP_ISSUED, SS_OP_DONE = 0, 1, 2
 SS_ROUND_ISSUED, SS_ROUND_BUDGET, SS_ROUND_IDLE, SS_ROUND_INFEASIBLE = 0, 1, 2, 3
 SS_KERNEL_SCHEDULE, SS_KERNEL_MEMORY, SS_KERNEL_SELECT, SS_KERNEL_INTERVALS, SS_KERNEL_TRANSPOSE = 0, 1, 2, 3, 4
@@ -80,6 +81,8 @@ def lib():
             L.ss_simulate_workspace_size.restype = ctypes.c_int
             L.ss_simulate_batch_ws.argtypes = [P, P, I64, ctypes.c_int, P, P, P, P, P, P, I64, P]
             L.ss_simulate_batch_ws.restype = ctypes.c_int
+            L.ss_simulate_batch_noalloc.argtypes = [P, P, I64, ctypes.c_int, P, P, P, P, P, P]
+            L.ss_simulate_batch_noalloc.restype = ctypes.c_int
             L.ss_select_best.argtypes = [P, P, P, P, I64, ctypes.c_int, P, P]
             L.ss_select_best.restype = ctypes.c_int
             L.ss_kernel_timing.argtypes = [ctypes.c_int]
@@ -279,6 +282,15 @@ def simulate_batch_into(g: Gmg, placements, makespan, violation, peak=None, slac
         _check(lib().ss_simulate_batch_ws(g.handle, _ptr(placements), B, flags, _ptr(makespan), _ptr(peak),
                                           _ptr(violation), _ptr(slack), _ptr(sumfin), _ptr(workspace), nbytes,
                                           _stream_ptr(stream)))
+
+
+def simulate_batch_noalloc_into(g: Gmg, placements, makespan, violation, peak=None, slack=None, sumfin=None,
+                                stream=None, dispatch="index", layout="row"):
+    """ss_simulate_batch_noalloc: the library's fixed scratch array instead of
+    any allocation (calls on one GPU must not overlap)."""
+    B, flags = _layout(g, placements, layout, dispatch, "latency")
+    _check(lib().ss_simulate_batch_noalloc(g.handle, _ptr(placements), B, flags, _ptr(makespan), _ptr(peak),
+                                           _ptr(violation), _ptr(slack), _ptr(sumfin), _stream_ptr(stream)))
 
 
 def simulate_batch(g: Gmg, placements, want_peak=True, want_slack=True, want_sumfin=True, stream=None,
