@@ -192,36 +192,84 @@ def sample_rows(synth, g, cid, idx):
     return out
 
 
-def cpu_baseline(g, cid, B, seconds, got, dispatch, links="latency"):
-    """The oracle, as it stands, on a bounded evenly spaced sample of the same
-    batch, on the host's cores; its results are also compared with the GPU's."""
+def host_cpu():
+    """The host's CPU model (from /proc/cpuinfo, as lscpu reports it), the
+    logical CPUs this process may run on, and the thread count the baseline
+    uses: all of them, or the host share the environment states for this
+    GPU (OMP_NUM_THREADS), whichever is smaller."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    avail = len(os.sched_getaffinity(0))
+    share = os.environ.get("OMP_NUM_THREADS", "")
+    threads = min(avail, int(share)) if share.isdigit() and int(share) > 0 else avail
+    return model, avail, threads
+
+
+def parity_indices(B, chunk, sub, n_even):
+    """Evenly spaced candidates plus the first and last candidate of every
+    chunk and of every memory-pass sub-chunk of the call's split."""
+    idx = set(np.linspace(0, B - 1, n_even).astype(np.int64).tolist())
+    for b0 in range(0, B, chunk):
+        b1 = min(b0 + chunk, B)
+        idx.update((b0, b1 - 1))
+        for s0 in range(b0, b1, max(1, sub)):
+            idx.update((s0, min(s0 + sub, b1) - 1))
+    return np.array(sorted(idx), np.int64)
+
+
+def cpu_baseline(g, cid, B, seconds, got, dispatch, links="latency", split=None):
+    """The oracle, as it stands, on the host's cores: a one-thread rate on the
+    first 4,096 candidates of the batch, then a bounded sample of the batch
+    (evenly spaced, plus every chunk's and sub-chunk's first and last
+    candidate) on all the threads the host share allows; every candidate it
+    evaluates is compared with the GPU's results."""
     import oracle
     from paper_2608_15762_amd import synth
 
-    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    model, avail, threads = host_cpu()
     mode = oracle.READY_ORDER if dispatch == "ready" else oracle.LINK_PORTS if links == "ports" else oracle.INDEX_ORDER
     og = oracle.OracleGmg(g)
-    pilot = sample_rows(synth, g, cid, np.linspace(0, B - 1, 9).astype(np.int64))
-    oracle.simulate_batch(og, pilot[:1], dispatch=mode, n_threads=1)  # first call pays one-time costs
+    fields = ("makespan", "peak", "violation", "slack", "sumfin")
+
+    def mismatches(idx, ref):
+        return int(sum((got[f][idx] != ref[f]).reshape(len(idx), -1).any(axis=1) for f in fields).astype(bool).sum())
+
+    # one thread, the first 4,096 candidates
+    first = np.arange(min(B, 4096), dtype=np.int64)
+    P1 = sample_rows(synth, g, cid, first)
+    oracle.simulate_batch(og, P1[:1], dispatch=mode, n_threads=1)  # first call pays one-time costs
     t0 = time.perf_counter()
-    oracle.simulate_batch(og, pilot[1:], dispatch=mode, n_threads=1)
-    per = (time.perf_counter() - t0) / (len(pilot) - 1)
-    n = int(max(threads, min(B, 65536, seconds * threads / max(per, 1e-9))))
-    idx = np.unique(np.linspace(0, B - 1, n).astype(np.int64))
-    log(f"oracle: {per * 1e3:.2f} ms per candidate on one core; timing {len(idx)} candidates on {threads} threads")
+    ref1 = oracle.simulate_batch(og, P1, dispatch=mode, n_threads=1)
+    wall1 = time.perf_counter() - t0
+    per = wall1 / len(first)
+    mism = mismatches(first, ref1)
+    log(f"oracle: {per * 1e3:.2f} ms per candidate on one thread over the first {len(first)}; {mism} differ")
+    # all threads, a sample sized to about `seconds` of CPU work per thread
+    n_even = int(max(threads, min(B, 65536, seconds * threads / max(per, 1e-9))))
+    chunk, sub = split if split else (B, B)
+    idx = parity_indices(B, chunk, sub, n_even)
+    log(f"oracle: timing {len(idx)} candidates on {threads} threads ({avail} CPUs available, {model})")
     P = sample_rows(synth, g, cid, idx)
     t0 = time.perf_counter()
     ref = oracle.simulate_batch(og, P, dispatch=mode, n_threads=threads)
     wall = time.perf_counter() - t0
-    mism = 0
-    for f in ("makespan", "peak", "violation", "slack", "sumfin"):
-        a = got[f][idx]
-        mism += int((a != ref[f]).reshape(len(idx), -1).any(axis=1).sum())
-    log(f"oracle: {len(idx) / wall:.1f} candidates/s; {mism} candidates differ from the GPU")
+    mism_all = mismatches(idx, ref)
+    log(f"oracle: {len(idx) / wall:.1f} candidates/s; {mism_all} candidates differ from the GPU")
     return dict(value=len(idx) / wall, unit="candidates/s", cores=threads, kind="oracle",
-                sample=f"{len(idx)} evenly spaced candidates of the same batch (indices 0..{B - 1}), "
-                       f"{threads} threads, {wall:.1f} s wall",
-                op_evals_per_s=len(idx) * g.n_ops / wall), dict(checked=int(len(idx)), mismatching_candidates=mism)
+                sample=f"{len(idx)} candidates of the same batch (indices 0..{B - 1}: evenly spaced, and the first "
+                       f"and last of every chunk of {chunk} and sub-chunk of {sub}), {threads} threads, "
+                       f"{wall:.1f} s wall",
+                op_evals_per_s=len(idx) * g.n_ops / wall, cpu_model=model, cpus_available=avail,
+                one_thread={"value": len(first) / wall1, "unit": "candidates/s",
+                            "sample": f"the first {len(first)} candidates, 1 thread, {wall1:.1f} s wall"}), \
+        dict(checked=int(len(idx) + len(first)), mismatching_candidates=mism_all + mism,
+             chunk=int(chunk), sub_chunk=int(sub))
 
 
 EST_N, EST_F, EST_SAMPLES = 65536, 5, 1 << 23  # estimators, features, samples fed back per step
@@ -538,7 +586,8 @@ def main():
     if not args.no_cpu_baseline:
         got = {k: v.cpu().numpy() for k, v in out.items()}
         log("running the oracle CPU baseline")
-        cb, par = cpu_baseline(g, cid, B, args.cpu_seconds, got, args.dispatch, args.links)
+        cb, par = cpu_baseline(g, cid, B, args.cpu_seconds, got, args.dispatch, args.links,
+                               split=ss.chunking(h, B, dispatch=args.dispatch))
         result["cpu_baseline"] = cb
         result["parity_sample"] = par
     print(json.dumps(result), flush=True)

@@ -33,7 +33,7 @@ extern "C" {
 #define SS_LAYOUT_ROW_MAJOR 0    /* placements[b * n_ops + v] = device of op v in candidate b */
 #define SS_LAYOUT_OP_MAJOR 1     /* placements[v * B + b] = device of op v in candidate b */
 #define SS_DISPATCH_READY 0x100  /* OR into layout: ready-time dispatch (see ss_simulate_batch) */
-#define SS_LINK_PORTS 0x200      /* OR into layout: transfers arbitrated over device ports (refused for now) */
+#define SS_LINK_PORTS 0x200      /* OR into layout: transfers arbitrated over device ports (see ss_simulate_batch) */
 
 #define SS_VIOLATION_MEMORY 0x1  /* some device's peak memory exceeds its capacity */
 #define SS_VIOLATION_INVALID 0x4 /* the placement names a device id >= n_dev; not simulated */
@@ -150,8 +150,22 @@ int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req)
  * A candidate naming a device >= n_dev is not simulated: violation =
  * SS_VIOLATION_INVALID, makespan = sumfin = INT64_MAX, peak = 0 and slack =
  * INT64_MIN.  This is a per-candidate result, not a call error.
- * With layout | SS_LINK_PORTS the call fails with SS_ERR_UNSUPPORTED: the
- * event-driven transfer arbitration of Sec. 3.5.2 has no GPU kernels yet.
+ * With layout | SS_LINK_PORTS transfers contend for the devices' ports, after
+ * the event-driven arbitration of Sec. 3.5.2: each device sends one tensor at
+ * a time and receives one at a time.  The output of an op is moved once to
+ * every other device holding a consumer; that transfer becomes pending when
+ * the op finishes.  At every instant where an op finishes or a transfer
+ * arrives, the pending transfers are examined in order of request time, then
+ * producer index, then destination device, and each one whose send and
+ * receive ports are both idle starts then and holds both until it arrives
+ * (its estimate later); a zero estimate moves nothing and completes at once.
+ * Compute queues stay index-ordered.  Consumers on the destination wait for
+ * the arrival; the copy there is allocated at the transfer's start and the
+ * producer's output is kept until its last transfer has arrived.  Index-order
+ * dispatch only: with SS_DISPATCH_READY as well the call fails with
+ * SS_ERR_UNSUPPORTED.  This variant simulates each candidate with one
+ * wavefront, event by event, so it costs more per candidate than the
+ * latency-only rule.
  * placements: DEVICE pointer, uint8, SS_LAYOUT_ROW_MAJOR [B][n_ops] or
  * SS_LAYOUT_OP_MAJOR [n_ops][B] (the layout the schedule pass reads: no
  * transpose of the batch before it), either one OR-ed with the flags above.
@@ -181,6 +195,17 @@ int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int64_t B, int
  * SS_ERR_DEVICE, SS_ERR_UNSUPPORTED (as ss_simulate_batch would).
  */
 int ss_simulate_workspace_size(const ss_gmg *g, int64_t B, int layout, int64_t *min_bytes, int64_t *pref_bytes);
+
+/*
+ * How ss_simulate_batch splits B candidates (the same simulation, Sec. 3.3.3,
+ * and candidate loop of Alg. 1): *chunk candidates per schedule launch and
+ * *sub per memory-pass launch inside a chunk (equal to *chunk where the
+ * memory pass is not split), so that tests and benchmarks can check the
+ * candidates at every boundary.  A chunk size reduced after running out of
+ * memory applies to later calls and is reported.  Launches nothing.
+ * Errors: SS_ERR_INVALID_ARG, SS_ERR_DEVICE, SS_ERR_UNSUPPORTED.
+ */
+int ss_simulate_chunking(const ss_gmg *g, int64_t B, int layout, int64_t *chunk, int64_t *sub);
 
 /*
  * ss_simulate_batch with a caller-owned workspace: the same arguments and

@@ -50,18 +50,20 @@ namespace {
 // Checks shared by the simulation entry points; fills the placement source
 // and the dispatch flags.  SS_OK with B == 0 means there is nothing to do.
 int check_simulate(const char *fn, const ss_gmg *g, const uint8_t *placements, int64_t B, int layout,
-                   const int64_t *out_makespan, const uint8_t *out_violation, SsPlace *src, bool *ready) {
+                   const int64_t *out_makespan, const uint8_t *out_violation, SsPlace *src, bool *ready,
+                   bool *ports) {
   const std::string f(fn);
   if (!g) return ss_set_error(SS_ERR_INVALID_ARG, f + ": g is NULL");
   if (B < 0) return ss_set_error(SS_ERR_INVALID_ARG, f + ": B < 0");
   if ((layout & ~(SS_LAYOUT_OP_MAJOR | SS_DISPATCH_READY | SS_LINK_PORTS)) != 0)
     return ss_set_error(SS_ERR_INVALID_ARG, f + ": unknown layout");
-  if (layout & SS_LINK_PORTS)
-    return ss_set_error(SS_ERR_UNSUPPORTED, f + ": SS_LINK_PORTS (event-driven transfer arbitration) is not built yet");
+  if ((layout & SS_LINK_PORTS) && (layout & SS_DISPATCH_READY))
+    return ss_set_error(SS_ERR_UNSUPPORTED, f + ": SS_LINK_PORTS takes index-order dispatch only");
   src->p = placements;
   src->B = B;
   src->op_major = (layout & SS_LAYOUT_OP_MAJOR) != 0;
   *ready = (layout & SS_DISPATCH_READY) != 0;
+  *ports = (layout & SS_LINK_PORTS) != 0;
   if (B == 0) return SS_OK;
   if (!out_makespan || !out_violation)
     return ss_set_error(SS_ERR_INVALID_ARG, f + ": out_makespan and out_violation are required");
@@ -75,13 +77,13 @@ extern "C" int ss_simulate_batch(const ss_gmg *g, const uint8_t *placements, int
                                  int64_t *out_sla_slack, int64_t *out_sumfin, void *hip_stream) {
   ss_clear_error();
   SsPlace src;
-  bool ready = false;
+  bool ready = false, ports = false;
   const int rc = check_simulate("ss_simulate_batch", g, placements, B, layout, out_makespan, out_violation, &src,
-                                &ready);
+                                &ready, &ports);
   if (rc != SS_OK || B == 0) return rc;
   SsWork W;
   return ss_run_simulate(g, src, out_makespan, out_peak_mem, out_violation, out_sla_slack, out_sumfin,
-                         static_cast<hipStream_t>(hip_stream), ready, false, W);
+                         static_cast<hipStream_t>(hip_stream), ready, ports, W);
 }
 
 extern "C" int ss_simulate_workspace_size(const ss_gmg *g, int64_t B, int layout, int64_t *min_bytes,
@@ -91,20 +93,41 @@ extern "C" int ss_simulate_workspace_size(const ss_gmg *g, int64_t B, int layout
   if (pref_bytes) *pref_bytes = 0;
   if (!min_bytes && !pref_bytes) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_workspace_size: no output");
   SsPlace src;
-  bool ready = false;
+  bool ready = false, ports = false;
   int64_t dummy_ms = 0;
   uint8_t dummy_vi = 0;
   const uint8_t dummy_p = 0;
   const int rc = check_simulate("ss_simulate_workspace_size", g, &dummy_p, B, layout, &dummy_ms, &dummy_vi, &src,
-                                &ready);
+                                &ready, &ports);
   if (rc != SS_OK || B == 0) return rc;
   SsWork W;
   W.query = true;
   W.single = true;
-  const int r2 = ss_run_simulate(g, src, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, ready, false, W);
+  const int r2 = ss_run_simulate(g, src, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, ready, ports, W);
   if (r2 != SS_OK) return r2;
   if (min_bytes) *min_bytes = (int64_t)W.need_min;
   if (pref_bytes) *pref_bytes = (int64_t)W.need_pref;
+  return SS_OK;
+}
+
+extern "C" int ss_simulate_chunking(const ss_gmg *g, int64_t B, int layout, int64_t *chunk, int64_t *sub) {
+  ss_clear_error();
+  if (!chunk || !sub) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_chunking: a NULL output");
+  *chunk = *sub = 0;
+  SsPlace src;
+  bool ready = false, ports = false;
+  int64_t dummy_ms = 0;
+  uint8_t dummy_vi = 0;
+  const uint8_t dummy_p = 0;
+  const int rc = check_simulate("ss_simulate_chunking", g, &dummy_p, B, layout, &dummy_ms, &dummy_vi, &src, &ready,
+                                &ports);
+  if (rc != SS_OK || B == 0) return rc;
+  SsWork W;
+  W.query = true;
+  const int r2 = ss_run_simulate(g, src, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, ready, ports, W);
+  if (r2 != SS_OK) return r2;
+  *chunk = W.chunk;
+  *sub = W.sub;
   return SS_OK;
 }
 
@@ -114,9 +137,9 @@ extern "C" int ss_simulate_batch_ws(const ss_gmg *g, const uint8_t *placements, 
                                     int64_t workspace_bytes, void *hip_stream) {
   ss_clear_error();
   SsPlace src;
-  bool ready = false;
+  bool ready = false, ports = false;
   const int rc = check_simulate("ss_simulate_batch_ws", g, placements, B, layout, out_makespan, out_violation, &src,
-                                &ready);
+                                &ready, &ports);
   if (rc != SS_OK || B == 0) return rc;
   if (!workspace || workspace_bytes <= 0)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_batch_ws: workspace is NULL or empty");
@@ -127,7 +150,7 @@ extern "C" int ss_simulate_batch_ws(const ss_gmg *g, const uint8_t *placements, 
   W.bytes = (size_t)workspace_bytes;
   W.single = true;
   return ss_run_simulate(g, src, out_makespan, out_peak_mem, out_violation, out_sla_slack, out_sumfin,
-                         static_cast<hipStream_t>(hip_stream), ready, false, W);
+                         static_cast<hipStream_t>(hip_stream), ready, ports, W);
 }
 
 extern "C" int ss_est_create(int64_t n_est, int64_t n_feat, ss_est **out) {

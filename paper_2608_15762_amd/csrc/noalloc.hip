@@ -67,5 +67,6 @@ extern "C" int ss_simulate_batch_noalloc(const ss_gmg *g, const uint8_t *placeme
   W.bytes = kNoAllocScratch;
   W.single = true;
   return ss_run_simulate(g, src, out_makespan, out_peak_mem, out_violation, out_sla_slack, out_sumfin,
-                         static_cast<hipStream_t>(hip_stream), (layout & SS_DISPATCH_READY) != 0, false, W);
+                         static_cast<hipStream_t>(hip_stream), (layout & SS_DISPATCH_READY) != 0,
+                         (layout & SS_LINK_PORTS) != 0, W);
 }

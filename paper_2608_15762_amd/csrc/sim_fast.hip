@@ -180,28 +180,15 @@ struct SchedPipe {
   uint32_t wq[4];                // duration on the target device
   uint32_t le[4];                // time -> slice lookup entry at a lower bound of the op's finish
   uint4 lw[4];                   // its {begin, end} of slices lk and lk+1
-  uint32_t sx[4][2];             // with ports: devices of the op's first two successors (raw bytes)
-  uint32_t pa[4][kPipePre];      // with ports: arrivals over the predecessor edges (ops up to T-2)
 };
 // kLink: 0 = link classes from device groups (LDS), 1 = bit table (two
 // classes), 2 = byte table (more classes), 3 = device groups of 2^s
 // consecutive devices (group = device >> s).  With groups (0, 3) stage T-2
 // computes each predecessor's transfer time itself.
-// kPorts (no in-degree overflow, at most two successors per op): transfers
-// are admitted over device ports as in the general kernel (reserve_transfers):
-// after op T is placed, its output goes to the devices of its first two
-// successors in their order (one transfer per remote device, a zero estimate
-// takes no port), start = max(finish, send port of T's device, receive port
-// of the destination).  Port clocks are u32 [2][D][nb] in global memory
-// (candidate-minor), read for op T right after op T-1's port stores;
-// arrivals are u32 [E][nb] per predecessor edge, written by the producer and
-// read by the consumer two ops ahead (op T-1's from registers).  A remote
-// predecessor counts with its arrival, a local one with its finish.
-template <int kLink, bool kOverflow, bool kOneClass, bool kPorts>
+template <int kLink, bool kOverflow, bool kOneClass>
 __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const uint8_t *__restrict__ PT, int64_t ppitch,
                                                        int64_t nb,
-                                                       uint32_t *__restrict__ finT, uint32_t *__restrict__ arrT,
-                                                       uint32_t *__restrict__ port, int64_t *__restrict__ makespan,
+                                                       uint32_t *__restrict__ finT, int64_t *__restrict__ makespan,
                                                        int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
                                                        uint8_t *__restrict__ violation) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
@@ -227,8 +214,6 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   const bool live = c_raw < nb;
   const int64_t c = live ? c_raw : nb - 1;
   for (int d = 0; d < D; ++d) clk[d * kWave + lane] = G.slice_begin32[sbase[d]];
-  if (kPorts)
-    for (int d = 0; d < 2 * D; ++d) port[(int64_t)d * nb + c] = 0u;
   for (int r = 0; r < R; ++r) comp[r * kWave + lane] = G.release32[r];
   if (N == 0) {
     if (live) {
@@ -278,12 +263,6 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
 
   // Results of the last two ops: h1 = op T (after its step), h2 before it.
   uint32_t h1f = 0, h1d = 0, h2f = 0, h2d = 0;
-  // with ports: op T's successors (packed as succ2) and the arrivals of its
-  // transfers to them; the port clocks read for the next op
-  uint32_t h1s2 = 0xFFFFFFFFu, h1a0 = 0, h1a1 = 0, ps_send = 0, ps_recv0 = 0, ps_recv1 = 0;
-  uint32_t *const arrTc = kPorts ? arrT + c : nullptr;
-  uint32_t *const portc = kPorts ? port + c : nullptr;
-  const uint32_t n_edges = (uint32_t)G.pred_ptr[N];
 
   // Stage T-2 for target op t = T+2, after op T.
   auto stage2 = [&](auto qq, int T) {
@@ -310,10 +289,6 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
       // step's history; its device is already final)
       S.pd[q2][i] = du;
       S.pf[q2][i] = fu;
-      if (kPorts) {  // the arrival over edge i of op t (written once u <= T was placed)
-        const uint32_t ei = min(meta(kMetaE0, t) + (uint32_t)i, n_edges - 1u);
-        S.pa[q2][i] = arrTc[row((int)ei)];
-      }
       // transfer time in the bound: exact with device groups, else the
       // cheapest class (the fields hold classes 0 and 1), else none
       const uint32_t x0 = meta(kMetaX + 2 * i, t), x1 = meta(kMetaX + 2 * i + 1, t);
@@ -323,11 +298,6 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
       lb = ((uint32_t)i < np && u != T + 1) ? umax32(lb, fu + xe) : lb;
     }
     S.wq[q2] = kOneClass ? meta(kMetaDur, t) : G.dur32[(int64_t)t * C + dcls[dt]];
-    if (kPorts) {  // devices of op t's first two successors
-      const uint32_t s2t = G.succ2[t], y0 = s2t & 0xFFFFu, y1 = s2t >> 16;
-      S.sx[q2][0] = PTc[prow(y0 == 0xFFFFu ? t : (int)y0)];
-      S.sx[q2][1] = PTc[prow(y1 == 0xFFFFu ? t : (int)y1)];
-    }
     lb = umax32(lb, clk[(int)dt * kWave + lane]) + (kOneClass ? meta(kMetaDur, t) : 0u);
     const uint32_t e = dt * (uint32_t)G.lut_nb + (uint32_t)min((int)(lb >> G.lut_shift), G.lut_nb - 1);
     S.le[q2] = e;
@@ -380,11 +350,7 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
         const uint32_t x0 = meta(kMetaX + 2 * i, T), x1 = meta(kMetaX + 2 * i + 1, T);
         x = S.lc[q0][i] ? x1 : x0;
       }
-      uint32_t a = tt + (kGroups || du != d ? x : 0u);
-      if (kPorts) {
-        const uint32_t ar = u == T - 1 ? ((h1s2 & 0xFFFFu) == (uint32_t)T ? h1a0 : h1a1) : S.pa[q0][i];
-        a = du != d ? ar : tt;
-      }
+      const uint32_t a = tt + (kGroups || du != d ? x : 0u);
       ready = (uint32_t)i < np ? umax32(ready, a) : ready;
     }
     if (kOverflow && np > (uint32_t)kPipePre) {  // predecessors past the pipelined ones
@@ -432,50 +398,6 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     const uint32_t f = s + w;
     clk[slot] = f;
     finTc[row(T)] = f;
-    if (kPorts) {
-      const uint32_t s2 = G.succ2[T], pe = G.succ2_pe[T];
-      const uint32_t dx0 = clampD(S.sx[q0][0]), dx1 = clampD(S.sx[q0][1]);
-      const bool r0 = (s2 & 0xFFFFu) != 0xFFFFu && dx0 != d, r1 = (s2 >> 16) != 0xFFFFu && dx1 != d;
-      // the transfer time of op T's output to device e
-      auto xfer_out = [&](uint32_t e) -> uint32_t {
-        uint32_t lc;
-        if (kLink == 0) lc = lgrp[e] == lgrp[d] ? lsame : 1u - lsame;
-        else if (kLink == 3) lc = e >> lshift == d >> lshift ? lsame : 1u - lsame;
-        else if (kLink == 1) lc = link_bit(G, d, e);
-        else lc = G.link_class[d * D + e];
-        return G.xfer32[(int64_t)T * K + (kLink == 2 ? lc : min(lc, (uint32_t)K - 1u))];
-      };
-      uint32_t send = ps_send, a0 = f, a1 = f;
-      bool w0 = false, w1 = false;
-      if (r0) {
-        const uint32_t x = xfer_out(dx0);
-        if (x > 0) {
-          a0 = umax32(f, umax32(send, ps_recv0)) + x;
-          send = a0;
-          w0 = true;
-        }
-      }
-      if (r1) {
-        if (r0 && dx1 == dx0) {
-          a1 = a0;  // the tensor is already on its way to that device
-        } else {
-          const uint32_t x = xfer_out(dx1);
-          if (x > 0) {
-            a1 = umax32(f, umax32(send, ps_recv1)) + x;
-            send = a1;
-            w1 = true;
-          }
-        }
-      }
-      if (w0) portc[(int64_t)(D + (int)dx0) * nb] = a0;
-      if (w1) portc[(int64_t)(D + (int)dx1) * nb] = a1;
-      if (w0 || w1) portc[(int64_t)d * nb] = send;
-      if (r0) arrTc[row((int)(pe & 0xFFFFu))] = a0;
-      if (r1) arrTc[row((int)(pe >> 16))] = a1;
-      h1s2 = s2;
-      h1a0 = a0;
-      h1a1 = a1;
-    }
     atomicMax(&comp[r * kWave + lane], f);
     ms = umax32(ms, f);
     sum += f;
@@ -485,13 +407,6 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     h1d = d;
     stage2(qq, T);
     stage3(qq, T);
-    if (kPorts) {  // op T+1's ports, after op T's port stores
-      constexpr int qn = (q0 + 1) & 3;
-      const uint32_t dn = clampD(S.dq[qn]);
-      ps_send = portc[(int64_t)dn * nb];
-      ps_recv0 = portc[(int64_t)(D + (int)clampD(S.sx[qn][0])) * nb];
-      ps_recv1 = portc[(int64_t)(D + (int)clampD(S.sx[qn][1])) * nb];
-    }
     S.dq[q0] = load_dev(min(T + 4, N - 1));
   };
 
@@ -1643,15 +1558,12 @@ __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0,
 }
 
 template <int kLink>
-const void *schedule_fn(bool overflow, bool one_class, bool ports) {
-  if (ports)  // callers exclude in-degree overflow
-    return one_class ? reinterpret_cast<const void *>(&fast_schedule<kLink, false, true, true>)
-                     : reinterpret_cast<const void *>(&fast_schedule<kLink, false, false, true>);
+const void *schedule_fn(bool overflow, bool one_class) {
   if (overflow)
-    return one_class ? reinterpret_cast<const void *>(&fast_schedule<kLink, true, true, false>)
-                     : reinterpret_cast<const void *>(&fast_schedule<kLink, true, false, false>);
-  return one_class ? reinterpret_cast<const void *>(&fast_schedule<kLink, false, true, false>)
-                   : reinterpret_cast<const void *>(&fast_schedule<kLink, false, false, false>);
+    return one_class ? reinterpret_cast<const void *>(&fast_schedule<kLink, true, true>)
+                     : reinterpret_cast<const void *>(&fast_schedule<kLink, true, false>);
+  return one_class ? reinterpret_cast<const void *>(&fast_schedule<kLink, false, true>)
+                   : reinterpret_cast<const void *>(&fast_schedule<kLink, false, false>);
 }
 
 int hip_fail(hipError_t err, const char *what) {
@@ -1804,7 +1716,7 @@ struct FastPlan {
   int64_t chunk = 0, sub = 0, nslots = 0, n_ticket = 0;
   int sets = kRecSets;
   size_t sz_pt = 0, sz_fin = 0, sz_own = 0, sz_cp = 0, sz_meta = 0, sz_rank = 0, sz_wk = 0, sz_wb = 0, sz_tk = 0,
-         sz_port = 0, sz_arr = 0, total = 0;
+         total = 0;
 };
 
 hipError_t ss_rows_from_op_major(const uint8_t *P, int64_t n_ops, int64_t B, int64_t b0, int64_t nb, uint8_t *rows,
@@ -1816,7 +1728,7 @@ hipError_t ss_rows_from_op_major(const uint8_t *P, int64_t n_ops, int64_t B, int
 }
 
 int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_t *peak, uint8_t *violation,
-                         int64_t *slack, int64_t *sumfin, hipStream_t stream, bool link_ports, SsWork &W) {
+                         int64_t *slack, int64_t *sumfin, hipStream_t stream, SsWork &W) {
   const GmgView &G = g->view;
   const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req, B = src.B;
   const size_t sched_lds = ss_fast_schedule_lds(g);
@@ -1829,19 +1741,15 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
   const int link_mode = G.link_shift >= 0 ? 3 : G.link_grp ? 0 : g->n_link <= 2 ? 1 : 2;
   const bool overflow = g->max_indeg > kPipePre;
   const bool one_class = g->n_class == 1;
-  const bool ports = link_ports && E > 0;  // without edges nothing is transferred
-  if (ports && !ss_fast_ports_ok(g))
-    return ss_set_error(SS_ERR_UNSUPPORTED, "this GMG needs the general kernels for transfer ports");
-  const void *const sched_fn = link_mode == 0   ? schedule_fn<0>(overflow, one_class, ports)
-                               : link_mode == 1 ? schedule_fn<1>(overflow, one_class, ports)
-                               : link_mode == 2 ? schedule_fn<2>(overflow, one_class, ports)
-                                                : schedule_fn<3>(overflow, one_class, ports);
+  const void *const sched_fn = link_mode == 0   ? schedule_fn<0>(overflow, one_class)
+                               : link_mode == 1 ? schedule_fn<1>(overflow, one_class)
+                               : link_mode == 2 ? schedule_fn<2>(overflow, one_class)
+                                                : schedule_fn<3>(overflow, one_class);
   const bool iv_fast = g->n_class == 1 && g->n_link <= 2 && g->max_outdeg <= 2;
   // chunk: placements (op-major for the schedule from row-major input, rows
   // for the memory passes from op-major input), op-major and row-major finish
-  // times; with ports also the port clocks and the arrivals, op-major and
-  // row-major
-  const int64_t per_cand = N * (1 + 4 + 4) + (ports ? 2 * D * 4 + E * 8 : 0);
+  // times
+  const int64_t per_cand = N * (1 + 4 + 4);
   int lds_cu = 0;
   err = hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
@@ -1875,9 +1783,7 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
     q.sz_wb = align((size_t)q.nslots * slot_cap * 8);
     q.n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
     q.sz_tk = align((size_t)q.n_ticket * 4);
-    q.sz_port = ports ? align((size_t)2 * D * chunk * 4) : 0;
-    q.sz_arr = ports ? align((size_t)E * chunk * 4) : 0;
-    q.total = q.sz_pt + 2 * q.sz_fin + q.sz_port + 2 * q.sz_arr + (size_t)sets * (q.sz_own + q.sz_cp + q.sz_meta) +
+    q.total = q.sz_pt + 2 * q.sz_fin + (size_t)sets * (q.sz_own + q.sz_cp + q.sz_meta) +
               q.sz_rank + q.sz_wk + q.sz_wb + q.sz_tk;
     return q;
   };
@@ -1891,7 +1797,13 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
   const FastPlan pmin = plan_of(kWave, 1);
   if (W.query) {
     W.need_min = pmin.total;
-    W.need_pref = plan_for_budget(kFastScratchBudget).total;
+    const FastPlan pp = plan_for_budget(kFastScratchBudget);
+    W.need_pref = pp.total;
+    // the pool path starts from the last budget that fitted on this device
+    const int64_t fb = g_fast_budget[g->device & 255].load();
+    const FastPlan pq = W.single ? pp : plan_for_budget(fb > 0 ? fb : kFastScratchBudget);
+    W.chunk = pq.chunk;
+    W.sub = pq.sub;
     return SS_OK;
   }
   err = hipFuncSetAttribute(sched_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
@@ -1940,9 +1852,6 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
   auto *PT = reinterpret_cast<uint8_t *>(take(pl.sz_pt));  // op-major copy, or candidate rows of op-major input
   auto *finT = reinterpret_cast<uint32_t *>(take(pl.sz_fin));
   auto *fin = reinterpret_cast<uint32_t *>(take(pl.sz_fin));
-  auto *port = ports ? reinterpret_cast<uint32_t *>(take(pl.sz_port)) : nullptr;
-  auto *arrT = ports ? reinterpret_cast<uint32_t *>(take(pl.sz_arr)) : nullptr;  // [E][chunk]
-  auto *arr = ports ? reinterpret_cast<uint32_t *>(take(pl.sz_arr)) : nullptr;   // [chunk][E]
   MemPass M{};
   for (int k = 0; k < pl.sets; ++k) {
     M.own[k] = reinterpret_cast<Rec *>(take(pl.sz_own));
@@ -2012,8 +1921,8 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
       int64_t *ms_out = makespan + b0, *sf_out = sumfin ? sumfin + b0 : nullptr,
               *sl_out = slack ? slack + b0 * R : nullptr;
       uint8_t *vi_out = violation + b0;
-      void *args[] = {const_cast<GmgView *>(&G), &sched_P, &ppitch, const_cast<int64_t *>(&nb), &finT, &arrT, &port,
-                      &ms_out, &sf_out, &sl_out, &vi_out};
+      void *args[] = {const_cast<GmgView *>(&G), &sched_P, &ppitch, const_cast<int64_t *>(&nb), &finT, &ms_out,
+                      &sf_out, &sl_out, &vi_out};
       const hipError_t le = hipLaunchKernel(sched_fn, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), args,
                                             sched_lds, stream);
       if (le != hipSuccess && rc == SS_OK) rc = hip_fail(le, "fast_schedule launch");
@@ -2027,14 +1936,9 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
       hipLaunchKernelGGL(transpose_tiles<uint32_t>, tg, dim3(256), 0, stream, static_cast<const uint32_t *>(finT),
                          (int64_t)N, nb, nb, fin);
     }
-    if (ports) {  // arrivals per edge -> candidates' rows
-      const dim3 tg((unsigned)((nb + 63) / 64), (unsigned)((E + 63) / 64));
-      hipLaunchKernelGGL(transpose_tiles<uint32_t>, tg, dim3(256), 0, stream, static_cast<const uint32_t *>(arrT),
-                         (int64_t)E, nb, nb, arr);
-    }
     ss_timing_stop(tt, stream);
     if (!check("transpose launch")) break;
-    rc = memory_passes(g, M, Pc, fin, nb, false, peak ? peak + b0 * D : nullptr, violation + b0, stream, arr);
+    rc = memory_passes(g, M, Pc, fin, nb, false, peak ? peak + b0 * D : nullptr, violation + b0, stream);
   }
   const int jrc = mem_pass_join(M, stream);
   if (rc == SS_OK) rc = jrc;
@@ -2045,10 +1949,6 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
   return rc;
 }
 
-bool ss_fast_ports_ok(const ss_gmg *g) {
-  return g->max_indeg <= kPipePre && g->n_class == 1 && g->n_link <= 2 && g->max_outdeg <= 2 && g->view.succ2 &&
-         g->view.succ2_pe;
-}
 
 size_t ss_ready_schedule_lds(const ss_gmg *g) { return ready_schedule_lds((int)g->n_dev, (int)g->n_req); }
 
@@ -2102,6 +2002,8 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
   if (W.query) {
     W.need_min = pmin.total;
     W.need_pref = ppref.total;
+    W.chunk = ppref.chunk;
+    W.sub = ppref.sub;
     return SS_OK;
   }
   err = hipFuncSetAttribute(reinterpret_cast<const void *>(&ready_schedule), hipFuncAttributeMaxDynamicSharedMemorySize,

@@ -10,10 +10,8 @@
 //   (all lanes are at the same op), so it is read with wave-uniform loads.
 //   Finish times go to a per-chunk scratch row for the memory pass.
 //
-//   With kPorts (SS_LINK_PORTS) the lane also reserves each output's
-//   transfers on the devices' send and receive ports (clocks per device in
-//   global scratch, [2][device][candidate]) right after the producer is
-//   placed, and records each edge's arrival time ([edge][candidate]).
+// port_event_schedule: transfer arbitration (SS_LINK_PORTS, Sec. 3.5.2)
+//   event by event, one wave per candidate (see below).
 //
 // ready_schedule_general: the ready-time dispatch rule, one wave per
 //   candidate (the ready set is searched by the whole wave at every step).
@@ -42,48 +40,6 @@ constexpr int kMemBlocksPerCU = 4;
 __device__ __forceinline__ int64_t imax(int64_t a, int64_t b) { return a > b ? a : b; }
 
 // ------------------------------------------------------------------ schedule
-// Transfer arbitration over device ports (Sec. 3.5.2): a device sends one
-// tensor at a time and receives one at a time.  The transfers of op v's
-// output are requested at its finish f and admitted now, right after v is
-// placed (producers in index order; for one producer, destinations in the
-// order of their first consumers): start = max(f, send port of v's device,
-// receive port of the destination), both ports busy until the arrival.  A
-// zero estimate moves nothing and takes no port.  The arrival is written for
-// every edge from v into the destination device ([edge][candidate]).
-__device__ __forceinline__ void reserve_transfers(const GmgView &G, const uint8_t *prow, int v, int d, int64_t f,
-                                                  int64_t *port, int64_t *arr, int64_t nb, int64_t c) {
-  const int D = G.n_dev, K = G.n_link;
-  const int q0 = G.succ_ptr[v], q1 = G.succ_ptr[v + 1];
-  for (int q = q0; q < q1; ++q) {
-    int e = prow[G.succ_idx[q]];
-    if (e >= D) e = 0;  // an invalid candidate: walked on device 0, never reported
-    if (e == d) continue;
-    int first = q;
-    for (int q2 = q0; q2 < q; ++q2) {
-      int e2 = prow[G.succ_idx[q2]];
-      if (e2 >= D) e2 = 0;
-      if (e2 == e) {
-        first = q2;
-        break;
-      }
-    }
-    int64_t a;
-    if (first != q) {
-      a = arr[(int64_t)G.succ_pe[first] * nb + c];  // the tensor is already on its way to e
-    } else {
-      const int64_t x = G.xfer[(int64_t)v * K + G.link_class[d * D + e]];
-      a = f;
-      if (x > 0) {
-        int64_t *send = port + (int64_t)d * nb + c, *recv = port + (int64_t)(D + e) * nb + c;
-        a = imax(f, imax(*send, *recv)) + x;
-        *send = a;
-        *recv = a;
-      }
-    }
-    arr[(int64_t)G.succ_pe[q] * nb + c] = a;
-  }
-}
-
 // Resumption from a captured state (ss_simulate_batch_resume): every
 // candidate places its first k0 ops as the captured run did, so a lane starts
 // at op k0 with the captured device clocks, slice cursors, request
@@ -124,11 +80,9 @@ __global__ __launch_bounds__(256) void fill_prefix(int64_t *__restrict__ fin, in
   }
 }
 
-template <bool kPorts>
 __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const uint8_t *__restrict__ P,
                                                          int64_t nb, int64_t *__restrict__ fin,
-                                                         int64_t *__restrict__ comp, int64_t *__restrict__ port,
-                                                         int64_t *__restrict__ arr, const Resume RS,
+                                                         int64_t *__restrict__ comp, const Resume RS,
                                                          int64_t *__restrict__ makespan,
                                                          int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
                                                          uint8_t *__restrict__ violation) {
@@ -147,8 +101,6 @@ __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const 
     cur[d * kWave + lane] = from ? (uint16_t)RS.cur[d] : 0;
   }
   for (int r = 0; r < R; ++r) comp[(int64_t)r * nb + c] = from ? RS.comp[r] : G.release[r];
-  if (kPorts)
-    for (int d = 0; d < 2 * D; ++d) port[(int64_t)d * nb + c] = 0;
 
   bool invalid = false;
   int64_t ms = from ? RS.scal[0] : 0, sum = from ? RS.scal[1] : 0;
@@ -169,7 +121,7 @@ __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const 
       int64_t t = frow[u];
       int du = prow[u];
       if (du >= D) du = 0;
-      if (du != d) t = kPorts ? arr[(int64_t)e * nb + c] : t + G.xfer[(int64_t)u * K + G.link_class[du * D + d]];
+      if (du != d) t += G.xfer[(int64_t)u * K + G.link_class[du * D + d]];
       ready = imax(ready, t);
     }
     // one op at a time: not before the device's previous finish; then the
@@ -189,7 +141,6 @@ __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const 
     const int64_t f = s + w;
     frow[v] = f;
     clk[slot] = f;
-    if (kPorts) reserve_transfers(G, prow, v, d, f, port, arr, nb, c);
     ms = imax(ms, f);
     sum += f;
     int64_t *cr = comp + (int64_t)r * nb + c;
@@ -437,6 +388,306 @@ __global__ __launch_bounds__(kWave) void ready_schedule_general(
   __syncthreads();
   if (slack)
     for (int r = lane; r < R; r += kWave) slack[c * R + r] = G.deadline[r] - crow[r];
+}
+
+// ------------------------------------------------------------------ transfer ports, event by event
+// The arbitration of Sec. 3.5.2 inside an event-driven simulation (one wave
+// per candidate):
+//   - compute queues are those of contract A: a device runs its ops in index
+//     order, one at a time, each at the earliest fit at or after
+//     max(ready, the device's previous finish);
+//   - the output of u is moved once to every other device that holds a
+//     consumer of u; its transfer becomes pending when u finishes;
+//   - at every instant where an op finishes or a transfer arrives, the
+//     pending transfers are examined in order of request time, producer index
+//     and destination device, and each one whose source's send port and
+//     destination's receive port are both idle starts then and holds both
+//     until it arrives (a zero estimate moves nothing and completes at once);
+//   - an op is placed as soon as every input's availability is known and
+//     the op ahead of it on its device is placed (its start depends on
+//     nothing else, and it never lies before the current instant).
+// Per device in LDS: its queue (a range of the candidate's op list, ops of
+// the device in index order), the queue head and the first placed op not yet
+// finished (ops of a device finish in queue order), the clock and slice
+// cursor, both port clocks, the arrival of the transfer now entering it, and
+// the earliest unprocessed finish.  The next instant is a wave minimum over
+// the devices.  Pending transfers (producer << 8 | destination) are a list
+// in global scratch kept in examination order: appended at each instant in
+// producer then destination order, scanned 64 at a time, compacted.
+// Arrivals go to arr ([predecessor edge][candidate], every edge from u into
+// the destination), which the memory pass reads: copies allocated at their
+// transfer's start, own outputs kept until their last arrival.
+constexpr int64_t kNever = INT64_MAX;
+
+struct PortLds {
+  int32_t *qbeg, *head, *done, *cur;
+  int64_t *clk, *send_until, *recv_until, *arr_evt, *next_fin, *comp;
+  uint8_t *dirty, *seen;
+};
+
+size_t port_schedule_lds(int D, int R) {
+  return (size_t)(D + 1) * 4 + (size_t)D * 3 * 4 + (size_t)D * 5 * 8 + (size_t)R * 8 + (size_t)D * 2 + 64;
+}
+
+__device__ __forceinline__ PortLds port_lds(unsigned char *raw, int D, int R) {
+  PortLds L;
+  int64_t *p64 = reinterpret_cast<int64_t *>(raw);
+  L.clk = p64;
+  L.send_until = p64 + D;
+  L.recv_until = p64 + 2 * D;
+  L.arr_evt = p64 + 3 * D;
+  L.next_fin = p64 + 4 * D;
+  L.comp = p64 + 5 * D;
+  int32_t *p32 = reinterpret_cast<int32_t *>(L.comp + R);
+  L.qbeg = p32;
+  L.head = p32 + D + 1;
+  L.done = p32 + 2 * D + 1;
+  L.cur = p32 + 3 * D + 1;
+  L.dirty = reinterpret_cast<uint8_t *>(p32 + 4 * D + 1);
+  L.seen = L.dirty + D;
+  return L;
+}
+
+// Sets the arrival of u's transfer to device e on every edge from u into e.
+__device__ __forceinline__ void port_set_arrivals(const GmgView &G, const uint8_t *prow, int u, int e, int64_t a,
+                                                  int64_t *arr, int64_t nb, int64_t c, int q_begin, int q_step) {
+  const int q1 = G.succ_ptr[u + 1];
+  for (int q = G.succ_ptr[u] + q_begin; q < q1; q += q_step)
+    if (prow[G.succ_idx[q]] == e) arr[(int64_t)G.succ_pe[q] * nb + c] = a;
+}
+
+__global__ __launch_bounds__(kWave) void port_event_schedule(const GmgView G, const uint8_t *__restrict__ P,
+                                                             int64_t nb, int64_t *__restrict__ fin,
+                                                             int64_t *__restrict__ arr, int32_t *__restrict__ lists,
+                                                             int64_t *__restrict__ pend_all, int64_t pend_cap,
+                                                             int64_t *__restrict__ makespan,
+                                                             int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
+                                                             uint8_t *__restrict__ violation) {
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = G.n_class, K = G.n_link;
+  const int E = G.pred_ptr[N];
+  const int lane = threadIdx.x;
+  const int64_t c = blockIdx.x;
+  const uint8_t *prow = P + c * N;
+  int64_t *frow = fin + c * N;
+  int32_t *list = lists + c * N;
+  int64_t *pend = pend_all + c * pend_cap;
+  PortLds L = port_lds(lds_raw, D, R);
+
+  // a candidate naming a device outside the set is not simulated
+  bool bad = false;
+  for (int v = lane; v < N; v += kWave) bad = bad || prow[v] >= D;
+  if (__ballot(bad)) {
+    if (lane == 0) {
+      makespan[c] = INT64_MAX;
+      if (sumfin) sumfin[c] = INT64_MAX;
+      violation[c] = SS_VIOLATION_INVALID;
+    }
+    if (slack)
+      for (int r = lane; r < R; r += kWave) slack[c * R + r] = INT64_MIN;
+    return;
+  }
+  // every device's queue: its ops in index order
+  for (int d = lane; d < D; d += kWave) L.head[d] = 0;
+  __syncthreads();
+  for (int v = lane; v < N; v += kWave) atomicAdd(&L.head[prow[v]], 1);
+  __syncthreads();
+  if (lane == 0) {
+    int s = 0;
+    for (int d = 0; d < D; ++d) {
+      const int n = L.head[d];
+      L.qbeg[d] = s;
+      L.done[d] = s;  // fill position while the lists are written
+      s += n;
+    }
+    L.qbeg[D] = s;
+  }
+  __syncthreads();
+  for (int v0 = 0; v0 < N; v0 += kWave) {
+    const int v = v0 + lane;
+    const int d = v < N ? prow[v] : -1;
+    // lanes of this chunk on the same device, lower lanes first
+    uint64_t peers = (uint64_t)__ballot(v < N);
+    for (int b = 0; b < 8; ++b) {
+      const uint64_t m = (uint64_t)__ballot(v < N && ((d >> b) & 1));
+      peers &= (v < N && ((d >> b) & 1)) ? m : ~m;
+    }
+    const int below = __popcll(peers & ((lane == 0) ? 0ull : (~0ull >> (64 - lane))));
+    const int base = v < N ? L.done[d] : 0;
+    __syncthreads();
+    if (v < N) {
+      list[base + below] = v;
+      if (below == 0) L.done[d] = base + __popcll(peers);
+    }
+    __syncthreads();
+  }
+  for (int d = lane; d < D; d += kWave) {
+    L.head[d] = L.done[d] = L.qbeg[d];
+    L.cur[d] = 0;
+    L.clk[d] = L.send_until[d] = L.recv_until[d] = 0;
+    L.arr_evt[d] = L.next_fin[d] = kNever;
+    L.dirty[d] = 1;
+    L.seen[d] = 0;
+  }
+  for (int r = lane; r < R; r += kWave) L.comp[r] = G.release[r];
+  for (int e = lane; e < E; e += kWave) arr[(int64_t)e * nb + c] = -1;  // not started yet
+  __syncthreads();
+
+  int64_t ms = 0, sum = 0;
+  int64_t npend = 0;
+  bool stuck = false;
+  // every instant consumes at least one finish or arrival, so N + E + 1
+  // instants are enough; the bound only guarantees that the wave exits
+  for (int64_t step = 0;; ++step) {
+    if (step > (int64_t)N + E + 1) {
+      stuck = true;
+      break;
+    }
+    // place every queue head whose inputs' availability is known
+    for (int d = lane; d < D; d += kWave) {
+      if (!L.dirty[d]) continue;
+      L.dirty[d] = 0;
+      const int qend = L.qbeg[d + 1];
+      int h = L.head[d];
+      for (; h < qend; ++h) {
+        const int v = list[h];
+        int64_t ready = G.release[G.op_req[v]];
+        bool known = true;
+        for (int pe = G.pred_ptr[v]; pe < G.pred_ptr[v + 1]; ++pe) {
+          const int u = G.pred_idx[pe];
+          int64_t a;
+          if (prow[u] == d) {
+            a = frow[u];  // earlier in this queue, hence placed
+          } else {
+            a = arr[(int64_t)pe * nb + c];
+            if (a < 0) {
+              known = false;
+              break;
+            }
+          }
+          ready = imax(ready, a);
+        }
+        if (!known) break;
+        const int64_t w = G.dur[(int64_t)v * C + G.dev_class[d]];
+        const int64_t t = imax(ready, L.clk[d]);
+        const int sb = G.slice_ptr[d];
+        int k = L.cur[d];
+        int64_t s;
+        for (;;) {
+          s = imax(t, G.slice_begin[sb + k]);
+          if (s + w <= G.slice_end[sb + k]) break;
+          ++k;
+        }
+        L.cur[d] = k;
+        const int64_t f = s + w;
+        frow[v] = f;
+        L.clk[d] = f;
+        if (L.done[d] == h) L.next_fin[d] = f;  // the first placed op not yet finished
+        ms = imax(ms, f);
+        sum += f;
+        atomicMax(reinterpret_cast<unsigned long long *>(&L.comp[G.op_req[v]]), (unsigned long long)f);
+      }
+      L.head[d] = h;
+    }
+    __syncthreads();
+    // the next instant: a finish or an arrival
+    int64_t t = kNever;
+    for (int d = lane; d < D; d += kWave) t = min(t, min(L.next_fin[d], L.arr_evt[d]));
+    for (int o = kWave / 2; o >= 1; o >>= 1) t = min(t, (int64_t)__shfl_xor(t, o, kWave));
+    if (t == kNever) break;
+    // arrivals at t: the ports they held are idle from t on
+    for (int d = lane; d < D; d += kWave)
+      if (L.arr_evt[d] == t) L.arr_evt[d] = kNever;
+    // finishes at t, in producer index order: their Intents, by destination
+    for (;;) {
+      int u = INT_MAX;
+      for (int d = lane; d < D; d += kWave)
+        if (L.next_fin[d] == t) u = min(u, list[L.done[d]]);
+      for (int o = kWave / 2; o >= 1; o >>= 1) u = min(u, __shfl_xor(u, o, kWave));
+      if (u == INT_MAX) break;
+      const int du = prow[u];
+      __syncthreads();
+      if (lane == 0) {
+        const int nd = ++L.done[du];
+        L.next_fin[du] = nd < L.head[du] ? frow[list[nd]] : kNever;
+      }
+      for (int q = G.succ_ptr[u] + lane; q < G.succ_ptr[u + 1]; q += kWave) {
+        const int e = prow[G.succ_idx[q]];
+        if (e != du) L.seen[e] = 1;
+      }
+      __syncthreads();
+      for (int d0 = 0; d0 < D; d0 += kWave) {
+        const int d = d0 + lane;
+        const bool mark = d < D && L.seen[d];
+        uint64_t m = (uint64_t)__ballot(mark);
+        if (mark) L.seen[d] = 0;
+        while (m) {  // destinations in increasing device order
+          const int e = d0 + __ffsll((unsigned long long)m) - 1;
+          m &= m - 1;
+          const int64_t x = G.xfer[(int64_t)u * K + G.link_class[du * D + e]];
+          if (x == 0) {  // nothing moves: complete at its request
+            port_set_arrivals(G, prow, u, e, t, arr, nb, c, lane, kWave);
+            if (lane == 0) L.dirty[e] = 1;
+          } else {
+            if (lane == 0) pend[npend] = (int64_t)u << 8 | e;
+            ++npend;
+          }
+        }
+      }
+      __syncthreads();
+    }
+    // arbitration at t: pending transfers in order, each started when both of
+    // its ports are idle; the rest kept in order
+    int64_t kept = 0;
+    for (int64_t b0 = 0; b0 < npend; b0 += kWave) {
+      const int64_t i = b0 + lane;
+      const bool valid = i < npend;
+      const int64_t ent = valid ? pend[i] : 0;
+      const int u = (int)(ent >> 8), e = (int)(ent & 255), s = valid ? prow[u] : 0;
+      const int64_t x = valid ? G.xfer[(int64_t)u * K + G.link_class[s * D + e]] : 0;
+      bool started = false;
+      __syncthreads();
+      for (;;) {
+        const bool elig = valid && !started && L.send_until[s] <= t && L.recv_until[e] <= t;
+        const uint64_t m = (uint64_t)__ballot(elig);
+        if (!m) break;
+        const int first = __ffsll((unsigned long long)m) - 1;
+        if (lane == first) {
+          const int64_t a = t + x;
+          L.send_until[s] = a;
+          L.recv_until[e] = a;
+          L.arr_evt[e] = a;
+          L.dirty[e] = 1;
+          port_set_arrivals(G, prow, u, e, a, arr, nb, c, 0, 1);
+          started = true;
+        }
+        __syncthreads();
+      }
+      const bool keep = valid && !started;
+      const uint64_t km = (uint64_t)__ballot(keep);
+      const int pos = __popcll(km & ((lane == 0) ? 0ull : (~0ull >> (64 - lane))));
+      __syncthreads();
+      if (keep) pend[kept + pos] = ent;
+      kept += __popcll(km);
+    }
+    npend = kept;
+    __syncthreads();
+  }
+  // completion-time statistics (Sec. 3.3.3); every queue has run out (a
+  // queue left with ops would be a defect: its makespan reads -1)
+  for (int d = lane; d < D; d += kWave) stuck = stuck || L.head[d] < L.qbeg[d + 1];
+  for (int o = kWave / 2; o >= 1; o >>= 1) {
+    ms = imax(ms, (int64_t)__shfl_xor(ms, o, kWave));
+    sum += (int64_t)__shfl_xor(sum, o, kWave);
+  }
+  if (__ballot(stuck)) ms = -1;
+  if (lane == 0) {
+    makespan[c] = ms;
+    if (sumfin) sumfin[c] = sum;
+    violation[c] = 0;
+  }
+  if (slack)
+    for (int r = lane; r < R; r += kWave) slack[c * R + r] = G.deadline[r] - L.comp[r];
 }
 
 // ------------------------------------------------------------------ memory
@@ -692,10 +943,11 @@ static int run_simulate_generic(const ss_gmg *g, SsPlace src, int64_t *makespan,
   if (slot_cap >= INT32_MAX) return ss_set_error(SS_ERR_UNSUPPORTED, "n_ops + n_edges too large for the memory pass");
   if (ready && ports) return ss_set_error(SS_ERR_UNSUPPORTED, "transfer ports take index-order dispatch only");
   const void *sched_fn = ready   ? reinterpret_cast<const void *>(&ready_schedule_general)
-                         : ports ? reinterpret_cast<const void *>(&schedule_kernel<true>)
-                                 : reinterpret_cast<const void *>(&schedule_kernel<false>);
-  const size_t sched_lds = ready ? (size_t)D * (sizeof(int64_t) + sizeof(int32_t))
-                                 : (size_t)D * kWave * (sizeof(int64_t) + sizeof(uint16_t));
+                         : ports ? reinterpret_cast<const void *>(&port_event_schedule)
+                                 : reinterpret_cast<const void *>(&schedule_kernel);
+  const size_t sched_lds = ready   ? (size_t)D * (sizeof(int64_t) + sizeof(int32_t))
+                           : ports ? port_schedule_lds((int)D, (int)R)
+                                   : (size_t)D * kWave * (sizeof(int64_t) + sizeof(uint16_t));
   int cus = 0;
   hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
@@ -712,9 +964,9 @@ static int run_simulate_generic(const ss_gmg *g, SsPlace src, int64_t *makespan,
 
   // per candidate: finish times and request completions; with ready-time
   // dispatch also missing-predecessor counts and the spill list; with
-  // transfer ports also two port clocks per device and an arrival per edge;
-  // with op-major input the chunk's placement rows
-  const int64_t per_cand = N * 8 + R * 8 + (ready ? N * (4 + 8 + 4) : 0) + (ports ? (2 * D + E) * 8 : 0) +
+  // transfer ports also an arrival per edge, the op list by device and the
+  // pending transfers; with op-major input the chunk's placement rows
+  const int64_t per_cand = N * 8 + R * 8 + (ready ? N * (4 + 8 + 4) : 0) + (ports ? E * 8 + N * 4 + E * 8 : 0) +
                            (src.op_major ? N : 0);
   const bool resumed = from && from->k > 0;
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
@@ -733,7 +985,7 @@ static int run_simulate_generic(const ss_gmg *g, SsPlace src, int64_t *makespan,
     q.sz_spo = ready ? align((size_t)chunk * N * 4 + 4) : 0;
     q.sz_bydev = align((size_t)q.nslots * N * 4 + 4);
     q.sz_ev = align((size_t)q.nslots * slot_cap * 8);
-    q.sz_port = ports ? align((size_t)2 * D * chunk * 8) : 0;
+    q.sz_port = ports ? align((size_t)chunk * N * 4 + 4) + align((size_t)chunk * (E + 1) * 8) : 0;
     q.sz_arr = ports ? align((size_t)E * chunk * 8 + 8) : 0;
     q.sz_bad = resumed ? align((size_t)chunk * 4) : 0;
     q.sz_rows = src.op_major ? align((size_t)chunk * N + 1) : 0;
@@ -748,6 +1000,7 @@ static int run_simulate_generic(const ss_gmg *g, SsPlace src, int64_t *makespan,
   if (W.query) {
     W.need_min = pmin.total;
     W.need_pref = plan_of(pref_chunk).total;
+    W.chunk = W.sub = plan_of(pref_chunk).chunk;
     return SS_OK;
   }
   err = hipFuncSetAttribute(sched_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sched_lds);
@@ -833,10 +1086,18 @@ static int run_simulate_generic(const ss_gmg *g, SsPlace src, int64_t *makespan,
         hipLaunchKernelGGL(prefix_check, dim3(grid), dim3(256), 0, stream, Pc, nb, N, (int64_t)RS.k0, (int)D, bad);
         RS.bad = bad;
       }
-      hipLaunchKernelGGL(ports ? schedule_kernel<true> : schedule_kernel<false>,
-                         dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), sched_lds, stream, G, Pc, nb, fin,
-                         comp, port, arr, RS, makespan + b0, sumfin ? sumfin + b0 : nullptr,
-                         slack ? slack + b0 * R : nullptr, violation + b0);
+      if (ports) {  // event by event, one wave per candidate
+        auto *lists = reinterpret_cast<int32_t *>(port);
+        auto *pend = reinterpret_cast<int64_t *>(reinterpret_cast<unsigned char *>(port) +
+                                                  align((size_t)chunk * N * 4 + 4));
+        hipLaunchKernelGGL(port_event_schedule, dim3((unsigned)nb), dim3(kWave), sched_lds, stream, G, Pc, nb, fin,
+                           arr, lists, pend, E + 1, makespan + b0, sumfin ? sumfin + b0 : nullptr,
+                           slack ? slack + b0 * R : nullptr, violation + b0);
+      } else {
+        hipLaunchKernelGGL(schedule_kernel, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave),
+                           sched_lds, stream, G, Pc, nb, fin, comp, RS, makespan + b0,
+                           sumfin ? sumfin + b0 : nullptr, slack ? slack + b0 * R : nullptr, violation + b0);
+      }
       if (capture) {  // one candidate: its finish times and request completions
         err = hipMemcpyAsync(capture->fin, fin, (size_t)N * 8, hipMemcpyDeviceToDevice, stream);
         if (err == hipSuccess)
@@ -887,23 +1148,21 @@ int ss_run_simulate(const ss_gmg *g, SsPlace P, int64_t *makespan, int64_t *peak
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
   const bool fast_ok = g->view.time32 && (ready_dispatch ? ss_ready_schedule_lds(g) : ss_fast_schedule_lds(g)) <=
                                              (size_t)lds_max;
-  const bool ports_fast = link_ports && fast_ok && ss_fast_ports_ok(g);
   const char *path = std::getenv("SS_PATH");
-  if (path && std::strcmp(path, "fast") == 0 && (!fast_ok || (link_ports && !ports_fast)))
+  if (path && std::strcmp(path, "fast") == 0 && (!fast_ok || link_ports))
     return ss_set_error(SS_ERR_UNSUPPORTED, "SS_PATH=fast but this GMG or dispatch needs the general path");
-  // transfer ports run on the 32-bit kernels when the GMG fits them, else on
-  // the general schedule kernel, whose memory pass is still the 32-bit one
-  // when the GMG fits the branch-free interval writer (SS_PATH=generic: the
-  // general kernels throughout)
+  // transfer ports: the event-driven schedule of the general path, whose
+  // memory pass is the 32-bit one when the GMG fits the branch-free interval
+  // writer (SS_PATH=generic: the general kernels throughout)
   const bool force_generic = path && std::strcmp(path, "generic") == 0;
-  const bool generic = !fast_ok || (link_ports && !ports_fast) || force_generic;
+  const bool generic = !fast_ok || link_ports || force_generic;
   const bool ports_mem_fast = link_ports && !force_generic && g->view.time32 && g->n_ops > 0 && g->n_class == 1 &&
                               g->n_link <= 2 && g->max_outdeg <= 2 && g->view.succ2_pe;
   if (generic)
     return run_simulate_generic(g, P, makespan, peak, violation, slack, sumfin, stream, ready_dispatch, link_ports, W,
                                 nullptr, nullptr, ports_mem_fast && !W.ptr && !W.query);
   if (ready_dispatch) return ss_run_simulate_ready(g, P, makespan, peak, violation, slack, sumfin, stream, W);
-  return ss_run_simulate_fast(g, P, makespan, peak, violation, slack, sumfin, stream, link_ports, W);
+  return ss_run_simulate_fast(g, P, makespan, peak, violation, slack, sumfin, stream, W);
 }
 
 // The state's buffer grows to hold a capture of g (synchronising the stream

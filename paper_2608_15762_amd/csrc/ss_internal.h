@@ -185,6 +185,7 @@ struct SsWork {
   bool single = false;
   bool query = false;
   size_t need_min = 0, need_pref = 0;
+  int64_t chunk = 0, sub = 0;  // query: candidates per chunk and per memory-pass sub-chunk of the pool path
 };
 // Placements of a call: row-major [B][n_ops], or op-major [n_ops][B].
 struct SsPlace {
@@ -215,10 +216,7 @@ int ss_run_memory_fast(const ss_gmg *g, const uint8_t *P, const int64_t *fin64, 
 // Fast path (sim_fast.hip): 32-bit times, N <= 65535.
 size_t ss_fast_schedule_lds(const ss_gmg *g);
 int ss_run_simulate_fast(const ss_gmg *g, SsPlace P, int64_t *makespan, int64_t *peak, uint8_t *violation,
-                         int64_t *slack, int64_t *sumfin, hipStream_t stream, bool link_ports, SsWork &W);
-// Whether transfer ports can run on the 32-bit kernels: one device class, at
-// most two link classes, two predecessors and two successors per op.
-bool ss_fast_ports_ok(const ss_gmg *g);
+                         int64_t *slack, int64_t *sumfin, hipStream_t stream, SsWork &W);
 // Ready-time dispatch on the fast path (sim_fast.hip).
 size_t ss_ready_schedule_lds(const ss_gmg *g);
 int ss_run_simulate_ready(const ss_gmg *g, SsPlace P, int64_t *makespan, int64_t *peak, uint8_t *violation,

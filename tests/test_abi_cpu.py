@@ -140,8 +140,8 @@ def test_unknown_layout_bits_are_rejected_before_the_device():
                                       None) == -1
         assert L.ss_simulate_workspace_size(ctypes.c_void_p(8), 1, layout, ctypes.byref(ctypes.c_int64()),
                                             None) == -1
-    # transfer ports (any dispatch, any layout): refused as unsupported
-    for layout in (0x200, 0x201, 0x300):
+    # transfer ports with ready-time dispatch (either layout): refused as unsupported
+    for layout in (0x300, 0x301):
         assert L.ss_simulate_batch(ctypes.c_void_p(8), None, 1, layout, None, None, None, None, None, None) == -5
         assert b"SS_LINK_PORTS" in L.ss_last_error()
 

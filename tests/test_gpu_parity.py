@@ -305,29 +305,3 @@ def test_select_best_ties_and_sizes(dev, B):
         assert gpu_select(h, viol, key, slack, sla, dev) == exp
     none = gpu_select(h, np.ones(B, np.uint8), key, slack, False, dev)
     assert none == (-1, 2 ** 63 - 1)
-
-
-# ------------------------------------------------------------------ full-size batches
-@pytest.mark.parametrize("cid,n_sample", [(1, 256), (2, 64), (3, 32)])
-def test_full_batch_sampled_parity(dev, path, cid, n_sample):
-    """The whole batch of a workload in one call (the configuration the
-    benchmark times), checked against the oracle on sampled candidates."""
-    g = synth.build_gmg(cid)
-    B = synth.CONFIGS[cid].n_cand
-    print(f"config {cid}: full batch of {B}", flush=True)
-    P = synth.placements(g, cid, 0, B)
-    got = gpu_run(ss.Gmg(g), P, dev)
-    rng = np.random.default_rng(cid)
-    idx = np.unique(np.concatenate([[0, B - 1], rng.choice(B, n_sample, replace=False)]))
-    ref = oracle.simulate_batch(g, P[idx], n_threads=8)
-    assert_same(got, ref, idx=idx, label=f"config {cid} full")
-
-
-def test_link_ports_refused(dev):
-    """Transfer arbitration (SS_LINK_PORTS) is refused with SS_ERR_UNSUPPORTED
-    until GPU kernels of the event-driven rule match the oracle."""
-    g = synth.build_gmg(0)
-    Pt = torch.from_numpy(synth.placements(g, 0, 0, 8)).to(dev)
-    with pytest.raises(ss.SSError) as e:
-        ss.simulate_batch(ss.Gmg(g), Pt, links="ports")
-    assert e.value.code == ss.SS_ERR_UNSUPPORTED

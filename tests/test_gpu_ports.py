@@ -1,6 +1,6 @@
-"""Parity of the transfer-port variant (SS_LINK_PORTS, Sec. 3.5.2 arbitration
-read into the simulation) on the GPU with the oracle's LINK_PORTS schedule,
-element by element through the C ABI.
+"""Parity of the transfer-port variant (SS_LINK_PORTS: the event-driven
+arbitration of Sec. 3.5.2 read into the simulation) on the GPU with the
+oracle's LINK_PORTS schedule, element by element through the C ABI.
 
 Integer results: bit-exact on every output.  Cases: the hand-derived port
 cases, the seeded workloads (a slice of each batch, and one whole batch
@@ -20,15 +20,7 @@ from paper_2608_15762_amd import ss, synth
 from paper_2608_15762_amd.synth import TIME_INF, make_gmg
 
 torch = pytest.importorskip("torch")
-# The oracle now takes the arbitration of Sec. 3.5.2 event by event (a
-# transfer starts when its Intent arrives or a transfer on its ports
-# completes); the library's port kernels booked ports in producer index order
-# and no longer match it, so the library refuses SS_LINK_PORTS
-# (SS_ERR_UNSUPPORTED, checked in test_gpu_parity.py) until kernels of the
-# event-driven rule replace them.
-pytestmark = [pytest.mark.gpu,
-              pytest.mark.skip(reason="SS_LINK_PORTS is refused until GPU kernels of the event-driven arbitration "
-                                      "(Sec. 3.5.2) match the oracle")]
+pytestmark = pytest.mark.gpu
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 FIELDS = ("makespan", "peak", "violation", "slack", "sumfin")
@@ -201,18 +193,34 @@ def test_nullable_outputs_ports(dev):
     assert np.array_equal(got["makespan"], ref["makespan"]) and np.array_equal(got["violation"], ref["violation"])
 
 
-def test_full_batch_sampled_parity_ports(dev):
-    """The llama8b workload's whole batch in one call, sampled against the oracle."""
+def test_full_batch_parity_ports(dev):
+    """The llama8b workload's whole batch in one call, every candidate against
+    the oracle."""
     cid = 1
     g = synth.build_gmg(cid)
     B = synth.CONFIGS[cid].n_cand
     print(f"transfer ports, config {cid}: full batch of {B}", flush=True)
     P = synth.placements(g, cid, 0, B)
     got = gpu_run(ss.Gmg(g), P, dev)
-    rng = np.random.default_rng(77)
-    idx = np.unique(np.concatenate([[0, B - 1], rng.choice(B, 256, replace=False)]))
-    ref = oracle.simulate_batch(g, P[idx], dispatch=oracle.LINK_PORTS, n_threads=8)
-    assert_same(got, ref, idx=idx, label=f"ports, config {cid} full")
+    ref = oracle.simulate_batch(g, P, dispatch=oracle.LINK_PORTS, n_threads=max(1, min(16, os.cpu_count() or 1)))
+    assert_same(got, ref, label=f"ports, config {cid} full")
+
+
+@pytest.mark.parametrize("cid,nb", [(2, 200), (3, 40)])
+def test_ports_with_workspace_and_op_major(dev, cid, nb):
+    """Transfer ports through a caller's workspace (smallest and preferred)
+    and with op-major placements."""
+    g = synth.build_gmg(cid)
+    P = synth.placements(g, cid, 11, nb)
+    ref = oracle.simulate_batch(g, P, dispatch=oracle.LINK_PORTS, n_threads=8)
+    h = ss.Gmg(g)
+    lo, hi = ss.workspace_size(h, nb, links="ports")
+    for nbytes in (lo, hi):
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        assert_same(gpu_run(h, P, dev, workspace=ws), ref, label=f"ports, workspace {nbytes}")
+    out = ss.simulate_batch(h, torch.from_numpy(np.ascontiguousarray(P.T)).to(dev), links="ports", layout="op")
+    torch.cuda.synchronize()
+    assert_same({k: v.cpu().numpy() for k, v in out.items()}, ref, label="ports, op-major")
 
 
 def test_refusals(dev, monkeypatch):
@@ -221,7 +229,7 @@ def test_refusals(dev, monkeypatch):
     Pt = torch.from_numpy(synth.placements(g, 0, 0, 8)).to(dev)
     with pytest.raises(ss.SSError):
         ss.simulate_batch(h, Pt, dispatch="ready", links="ports")
-    # a graph with an op of three predecessors needs the general kernels for ports
+    # transfer ports run on the general kernels only
     g3 = make_gmg(2, ["op"] * 4, [(0, 3), (1, 3), (2, 3)], [0] * 4, [[5]] * 4, [10] * 4, [[(0, TIME_INF)]] * 2,
                   [10 ** 6] * 2, [0], [10 ** 6], bw=(10,), lat=(1,))
     P3 = torch.zeros((2, 4), dtype=torch.uint8, device=dev)
