@@ -41,7 +41,7 @@ class _Gmg(ctypes.Structure):
                 ("n_link", ctypes.c_int64), ("n_req", ctypes.c_int64)] + \
                [(n, ctypes.c_void_p) for n in ("pred_ptr", "pred_idx", "op_req", "dur", "out_bytes", "dev_class",
                                                "link_class", "bw", "lat", "slice_ptr", "slice_begin", "slice_end",
-                                               "cap", "release", "deadline")]
+                                               "cap", "release", "deadline", "done_fin", "issue_at")]
 
 
 _P = ctypes.c_void_p
@@ -76,12 +76,16 @@ class OracleGmg:
             self._keep[name] = a
             return a.ctypes.data
 
+        def opt(name):  # optional snapshot arrays: NULL when absent
+            return arr(name, np.int64) if getattr(g, name, None) is not None else None
+
         self.c = _Gmg(g.n_ops, g.n_dev, g.n_class, g.n_link, g.n_req,
                       arr("pred_ptr", np.int32), arr("pred_idx", np.int32), arr("op_req", np.int32),
                       arr("dur", np.int64), arr("out_bytes", np.int64), arr("dev_class", np.int32),
                       arr("link_class", np.uint8), arr("bw", np.int64), arr("lat", np.int64),
                       arr("slice_ptr", np.int64), arr("slice_begin", np.int64), arr("slice_end", np.int64),
-                      arr("cap", np.int64), arr("release", np.int64), arr("deadline", np.int64))
+                      arr("cap", np.int64), arr("release", np.int64), arr("deadline", np.int64),
+                      opt("done_fin"), opt("issue_at"))
 
 
 def _og(g):
@@ -103,6 +107,8 @@ def simulate_one(g, placement, dispatch: int = INDEX_ORDER) -> dict:
     rc = _get().sso_simulate_one(ctypes.byref(og.c), p.ctypes.data, dispatch, st.ctypes.data, fin.ctypes.data,
                                  ms.ctypes.data, peak.ctypes.data, viol.ctypes.data, slack.ctypes.data,
                                  sf.ctypes.data)
+    if rc == -3:
+        raise ValueError("a snapshot (done_fin, issue_at) takes index-order dispatch only")
     if rc != 0:
         raise MemoryError("oracle allocation failed")
     return dict(st=st, fin=fin, makespan=int(ms[0]), peak=peak, violation=int(viol[0]), slack=slack,
@@ -146,6 +152,8 @@ def simulate_batch(g, placements, dispatch: int = INDEX_ORDER, n_threads: int = 
             t.start()
         for t in ths:
             t.join()
+    if -3 in errors:
+        raise ValueError("a snapshot (done_fin, issue_at) takes index-order dispatch only")
     if errors:
         raise MemoryError("oracle allocation failed")
     return out

@@ -30,7 +30,13 @@
  *     transfer's start (the producer's finish; the receive buffer exists
  *     before the data moves, Sec. 3.5.2) until its last consumer there
  *     finishes; outputs without consumers stay resident; intervals are
- *     half-open; a device violates when its peak exceeds its capacity.
+ *     half-open; a device violates when its peak exceeds its capacity;
+ *   - a snapshot of a running schedule (Sec. 3.2 scheduling metadata: the
+ *     issued and done timestamps; Sec. 3.3.2 builds the simulator from it):
+ *     a done op is not simulated, it finished at its recorded time on its
+ *     device; an op does not start before it was issued, and the transfer of
+ *     an output to a device does not start before the first consumer there
+ *     was issued (its Intent exists only from then on).
  *
  * Parity: pinned by closed forms, bounds, brute force and hand-worked cases in
  * the CPU test-suite (no printed worked example exists in the paper).
@@ -112,17 +118,60 @@ static int build_succ(const sso_gmg *g, succ_csr *s) {
 
 static void free_succ(succ_csr *s) { free(s->ptr); free(s->idx); }
 
+/* ---------------------------------------------------------------- snapshots */
+
+static int64_t issue_time(const sso_gmg *g, int64_t v) { return g->issue_at ? g->issue_at[v] : 0; }
+
+static int is_done(const sso_gmg *g, int64_t v) { return g->done_fin && g->done_fin[v] >= 0; }
+
+/* Earliest start of the transfer of u's output to device e: the first issue
+ * time among u's consumers on e (the Intent of the first one issued), never
+ * before u finishes (the caller takes the later of the two). */
+static int64_t transfer_floor(const sso_gmg *g, const succ_csr *sc, const uint8_t *place, int64_t u, int64_t e) {
+  int64_t f = INT64_MAX;
+  for (int64_t q = sc->ptr[u]; q < sc->ptr[u + 1]; ++q) {
+    const int64_t x = sc->idx[q];
+    if (place[x] == e && issue_time(g, x) < f) f = issue_time(g, x);
+  }
+  return f == INT64_MAX ? 0 : f;
+}
+
+/* Arrival on device e of u's output (u on another device): its transfer
+ * starts once u has finished and the first consumer on e has been issued. */
+static int64_t transfer_arrival(const sso_gmg *g, const succ_csr *sc, const uint8_t *place, const int64_t *fin,
+                                int64_t u, int64_t e) {
+  const int64_t floor_ = transfer_floor(g, sc, place, u, e);
+  const int64_t start = fin[u] > floor_ ? fin[u] : floor_;
+  return start + transfer_time(g, u, place[u], e);
+}
+
 /* ---------------------------------------------------------------- schedules */
 
 /* Contract A: ops in index order; each starts at the earliest fit at or after
- * max(ready, the device's previous finish); one op at a time per device. */
-static void schedule_index_order(const sso_gmg *g, const uint8_t *place, int64_t *clock, int64_t *st,
-                                 int64_t *fin) {
+ * max(ready, the device's previous finish); one op at a time per device.  In
+ * a snapshot a done op is not placed: it finished at its recorded time and
+ * its device is free from then on; ready times also wait for the op's issue
+ * and for transfers that start no earlier than their first consumer's issue. */
+static void schedule_index_order(const sso_gmg *g, const uint8_t *place, const succ_csr *sc, int64_t *clock,
+                                 int64_t *st, int64_t *fin) {
   for (int64_t d = 0; d < g->n_dev; ++d) clock[d] = 0;
   for (int64_t v = 0; v < g->n_ops; ++v) {
     const int64_t d = place[v];
     const int64_t w = op_duration(g, v, d);
-    const int64_t ready = ready_time(g, place, fin, v);
+    if (is_done(g, v)) {
+      fin[v] = g->done_fin[v];
+      st[v] = fin[v] - w;
+      if (fin[v] > clock[d]) clock[d] = fin[v];
+      continue;
+    }
+    int64_t ready = g->release[g->op_req[v]];
+    if (ready < 0) ready = 0;
+    if (issue_time(g, v) > ready) ready = issue_time(g, v);
+    for (int64_t e = g->pred_ptr[v]; e < g->pred_ptr[v + 1]; ++e) {
+      const int64_t u = g->pred_idx[e];
+      const int64_t arrive = place[u] == d ? fin[u] : transfer_arrival(g, sc, place, fin, u, d);
+      if (arrive > ready) ready = arrive;
+    }
     const int64_t t = ready > clock[d] ? ready : clock[d];
     st[v] = earliest_fit(g, d, t, w);
     fin[v] = st[v] + w;
@@ -419,14 +468,15 @@ static int64_t residency_intervals(const sso_gmg *g, const uint8_t *place, const
       free_at = fin[v];
       for (int64_t e = s0; e < s1; ++e) {
         const int64_t x = sc->idx[e], dx = place[x];
-        const int64_t t = (dx == d) ? fin[x] : xa ? xa[e] : fin[v] + transfer_time(g, v, d, dx);
+        const int64_t t = (dx == d) ? fin[x] : xa ? xa[e] : transfer_arrival(g, sc, place, fin, v, dx);
         if (t > free_at) free_at = t;
       }
     }
     iv[n++] = (interval){d, st[v], free_at, b};
     /* one remote copy per destination device, from the transfer's start (v's
-     * finish, or the admitted start with arbitrated ports) until the last
-     * consumer on that device finishes */
+     * finish, not before the first consumer there was issued; with arbitrated
+     * ports the admitted start) until the last consumer on that device
+     * finishes */
     for (int64_t e = s0; e < s1; ++e) {
       const int64_t dx = place[sc->idx[e]];
       if (dx == d) continue;
@@ -437,7 +487,8 @@ static int64_t residency_intervals(const sso_gmg *g, const uint8_t *place, const
       int64_t last = 0;
       for (int64_t e2 = s0; e2 < s1; ++e2)
         if (place[sc->idx[e2]] == dx && fin[sc->idx[e2]] > last) last = fin[sc->idx[e2]];
-      iv[n++] = (interval){dx, xs ? xs[e] : fin[v], last, b};
+      const int64_t floor_ = transfer_floor(g, sc, place, v, dx);
+      iv[n++] = (interval){dx, xs ? xs[e] : fin[v] > floor_ ? fin[v] : floor_, last, b};
     }
   }
   *out = iv;
@@ -516,12 +567,13 @@ static int simulate_with(const sso_gmg *g, const succ_csr *sc, const uint8_t *pl
     if (slack) for (int64_t r = 0; r < R; ++r) slack[r] = INT64_MIN;
     return 0;
   }
+  if ((g->done_fin || g->issue_at) && dispatch != SSO_INDEX_ORDER) return -3;
   if (dispatch == SSO_READY_ORDER) {
     if (schedule_ready_order(g, place, sc, clock, st, fin) != 0) return -1;
   } else if (ports) {
     if (schedule_index_order_ports(g, place, sc, clock, st, fin, wb->xs, wb->xa, 0, 0) != 0) return -1;
   } else {
-    schedule_index_order(g, place, clock, st, fin);
+    schedule_index_order(g, place, sc, clock, st, fin);
   }
   /* completion-time statistics (Sec. 3.3.3): makespan from t0 = 0, per-request
    * completion (its release when it has no ops) against its deadline, and the

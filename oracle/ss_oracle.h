@@ -39,6 +39,17 @@ typedef struct {
   const int64_t *cap;        /* [n_dev] */
   const int64_t *release;    /* [n_req] */
   const int64_t *deadline;   /* [n_req] */
+  /* A snapshot of a running schedule (Sec. 3.2 scheduling metadata), both
+   * optional (NULL: none), index-order dispatch only:
+   *   done_fin[n_ops]  -1, or the recorded completion time of an op that is
+   *                    done: it is not simulated, it finished then on its
+   *                    device (free from then on); its output counts from
+   *                    that time minus its estimate;
+   *   issue_at[n_ops]  the time an op was issued: it does not start earlier,
+   *                    and a transfer to it does not start before the first
+   *                    of its destination's consumers was issued. */
+  const int64_t *done_fin;
+  const int64_t *issue_at;
 } sso_gmg;
 
 /* dispatch rules */
@@ -47,7 +58,8 @@ typedef struct {
 #define SSO_LINK_PORTS 2   /* index order; transfers arbitrated event by event over per-device send and receive ports */
 
 /* One candidate.  st/fin (length n_ops) and peak (n_dev), slack (n_req) may be
- * NULL.  Returns 0, or -1 on allocation failure. */
+ * NULL.  Returns 0, -1 on allocation failure, -3 for a snapshot (done_fin or
+ * issue_at) with another dispatch than SSO_INDEX_ORDER. */
 int sso_simulate_one(const sso_gmg *g, const uint8_t *place, int dispatch, int64_t *st, int64_t *fin,
                      int64_t *makespan, int64_t *peak, uint8_t *violation, int64_t *slack, int64_t *sumfin);
 

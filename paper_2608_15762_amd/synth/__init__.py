@@ -272,6 +272,10 @@ class Gmg:
     kinds: list = field(default_factory=list)
     tenant_of: np.ndarray | None = None
     name: str = ""
+    # a snapshot of a running schedule (optional): recorded completion time of
+    # each done op (-1: not done), issue time of each op
+    done_fin: np.ndarray | None = None   # int64 [N]
+    issue_at: np.ndarray | None = None   # int64 [N]
 
     @property
     def n_edges(self) -> int:
