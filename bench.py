@@ -51,6 +51,8 @@ def parse():
                          "host-to-device copy and simulation overlapped; reported beside value, not as it)")
     ap.add_argument("--batch-cap", type=int, default=400, help="incremental loop: ops per batch")
     ap.add_argument("--budget", type=int, default=1600, help="incremental loop: issued-op budget")
+    ap.add_argument("--no-prefix-reuse", action="store_true",
+                    help="incremental loop: simulate every round's whole graph (no resume from the last capture)")
     return ap.parse_args()
 
 
@@ -366,26 +368,42 @@ def estimator_main(args):
     print(json.dumps(result), flush=True)
 
 
-def sched_run(S, g, synth, key, record=None, max_rounds=None):
-    """One scheduling run: rounds until every op is issued or done, the executor
-    feeding back completions whenever a round issues nothing.  Returns
-    (rounds, issued rounds)."""
-    rounds = issued_rounds = step = 0
-    while max_rounds is None or rounds < max_rounds:
-        st, batch, p = S.round()
+def sched_run(S, g, synth, key, record=None, max_rounds=None, osch=None, deadline=None):
+    """One scheduling run: rounds until every op is issued or done.  Rounds
+    come at the stand-in executor's completion times: after a round that
+    issues nothing, the next completion is fed back and the clock moves to it.
+    With `record`, each round's (status, batch, partition, size of its
+    snapshot graph) is appended (the size is read from the scheduler's state,
+    outside what a caller needs).  `osch`: S is the oracle's scheduler.  Stops
+    early at `max_rounds` or at the perf_counter `deadline`.  Returns (rounds,
+    issued rounds)."""
+    X = synth.Executor(g, key)
+    rounds = issued_rounds = 0
+    now = 0
+    succ_open = None
+    if record is not None:
+        preds = [g.pred_idx[g.pred_ptr[v]:g.pred_ptr[v + 1]] for v in range(g.n_ops)]
+    while (max_rounds is None or rounds < max_rounds) and (deadline is None or time.perf_counter() < deadline):
+        if record is not None:
+            state = S.state()[0] if osch is None else S.state
+            done = state == 2
+            succ_open = np.zeros(g.n_ops, bool)
+            for v in np.nonzero(~done)[0]:
+                succ_open[preds[v]] = True
+            graph = int((state == 1).sum() + (done & succ_open).sum())
+        st, batch, p = S.round(now)
         rounds += 1
         if record is not None:
-            record.append((st, tuple(batch), p))
+            record.append((st, tuple(batch), p, graph + len(batch)))
         if st == 0:
             issued_rounds += 1
+            X.issue(batch, (S.state()[1] if osch is None else S.place)[batch], now)
             continue
-        state, place = S.state()
-        issued = np.nonzero(state == 1)[0]
-        if len(issued) == 0:
+        ev = X.next_completion()
+        if ev is None:
             break
-        for v in synth.completion_feedback(issued, key, step):
-            S.complete(v)
-        step += 1
+        now, v = ev
+        S.complete(v, now)
     return rounds, issued_rounds
 
 
@@ -406,18 +424,19 @@ def sched_main(args):
     log(f"incremental loop on {cfg.name}: N={g.n_ops} partitions={len(part)} cap={args.batch_cap} "
         f"budget={args.budget}")
     copy_gbs = copy_bandwidth(torch, dev)
+    reuse = not args.no_prefix_reuse
+    gpu_rec = []
     for i in range(args.warmup):
-        S = ss.Scheduler(g, part, prio, args.budget, args.batch_cap)
-        sched_run(S, g, synth, cid)
+        S = ss.Scheduler(g, part, prio, args.budget, args.batch_cap, prefix_reuse=reuse)
+        sched_run(S, g, synth, cid, record=gpu_rec if i == 0 else None)
         S.free()
         log(f"warmup run {i + 1}/{args.warmup} done")
     ss.kernel_timing(True)
     rounds = issued = 0
-    gpu_rec = []
     t0 = time.perf_counter()
     for i in range(args.steps):
-        S = ss.Scheduler(g, part, prio, args.budget, args.batch_cap)
-        r, ir = sched_run(S, g, synth, cid, record=gpu_rec if i == 0 else None)
+        S = ss.Scheduler(g, part, prio, args.budget, args.batch_cap, prefix_reuse=reuse)
+        r, ir = sched_run(S, g, synth, cid)
         S.free()
         rounds += r
         issued += ir
@@ -430,18 +449,19 @@ def sched_main(args):
         n, ms = ss.kernel_time(k)
         kernels[name] = dict(launches=n, total_ms=round(ms, 3), avg_ms=round(ms / max(n, 1), 4))
     ss.kernel_timing(False)
+    if not gpu_rec:  # no warmup: record one more run, untimed
+        S = ss.Scheduler(g, part, prio, args.budget, args.batch_cap, prefix_reuse=reuse)
+        sched_run(S, g, synth, cid, record=gpu_rec)
+        S.free()
     # algorithmic bytes of the simulations: per candidate its placement row of
-    # the round's graph and its outputs (makespan, violation, slack, sumfin)
+    # the round's snapshot graph and its outputs (makespan, violation, slack, sumfin)
     per_run, n_ops_sim = 0, 0
     dom = max((k for k in kernels if k != "select"), key=lambda k: kernels[k]["total_ms"])
     D, R = g.n_dev, g.n_req
-    # the round graphs of the first run: done + issued + batch ops at each issuing round
-    n_sched = 0
-    for st, batch, p in gpu_rec:
-        if st == 0:
-            n_sched += len(batch)
-            per_run += len(part) * (n_sched + 8 + 1 + 8 * R + 8)
-            n_ops_sim += len(part) * n_sched
+    graphs = [n for st, batch, p, n in gpu_rec if st in (0, 3)]
+    for n in graphs:
+        per_run += len(part) * (n + 8 + 1 + 8 * R + 8)
+        n_ops_sim += len(part) * n
     alg_bytes = per_run * args.steps
     achieved = alg_bytes / max(kernels[dom]["launches"], 1) / (kernels[dom]["avg_ms"] * 1e-3) / 1e9
     result = {
@@ -451,7 +471,9 @@ def sched_main(args):
         "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
         "config": {"workload": f"{cfg.name}-incremental", "n_ops": g.n_ops, "partitions": len(part),
                    "batch_cap": args.batch_cap, "issue_budget": args.budget, "rounds_per_run": rounds // args.steps,
-                   "issuing_rounds_per_run": issued // args.steps},
+                   "issuing_rounds_per_run": issued // args.steps, "prefix_reuse": reuse,
+                   "snapshot_ops_mean": round(float(np.mean(graphs)), 1) if graphs else 0,
+                   "snapshot_ops_max": int(max(graphs)) if graphs else 0},
         "simulated_op_evals_per_s": round(n_ops_sim * args.steps / elapsed, 1),
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 4), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 7), "traffic": None,
@@ -466,20 +488,8 @@ def sched_main(args):
         O = osch.Scheduler(g, part, prio, args.budget, args.batch_cap)
         rec = []
         t0 = time.perf_counter()
-        n_issuing = 0
-        step = 0
-        while time.perf_counter() - t0 < args.cpu_seconds:
-            st, batch, p = O.round()
-            rec.append((st, tuple(batch), p))
-            if st == 0:
-                n_issuing += 1
-                continue
-            issued_ops = np.nonzero(O.state == osch.ISSUED)[0]
-            if len(issued_ops) == 0:
-                break
-            for v in synth.completion_feedback(issued_ops, cid, step):
-                O.complete(v)
-            step += 1
+        sched_run(O, g, synth, cid, record=rec, osch=osch, deadline=t0 + args.cpu_seconds)
+        n_issuing = sum(1 for x in rec if x[0] == 0)
         wall = time.perf_counter() - t0
         mism = sum(1 for a, b in zip(rec, gpu_rec) if a != b)
         result["cpu_baseline"] = {"value": round(n_issuing / wall, 3), "unit": "rounds/s", "cores": 1,

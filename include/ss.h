@@ -73,11 +73,32 @@ typedef struct ss_gmg ss_gmg;
  *   release[R], deadline[R]  per-request arrival (>= 0) and absolute SLA
  *                  deadline (|deadline| < 2^62).
  *
+ * The state of a running schedule (Sec. 3.2 scheduling metadata: the issued
+ * and done timestamps of the ops; Sec. 3.3.2 builds the simulator from it),
+ * all optional (NULL / 0: a plan from an idle start):
+ *   done_fin[N]    -1, or the recorded completion time (>= 0) of an op that
+ *                  is done.  A done op is not simulated: it finished then on
+ *                  the device its candidate names, which is free from then
+ *                  on; its output counts from that time minus its estimate.
+ *                  A done op's predecessors must be done and have finished
+ *                  strictly earlier.
+ *   issue_at[N]    the time (>= 0) each op was issued: it starts no earlier,
+ *                  and the transfer of an output to a device starts no
+ *                  earlier than the first issue time among its consumers on
+ *                  that device (its Intent exists from then on).  A done op
+ *                  must finish strictly after its issue time.
+ *   t_now          the snapshot's timestamp (>= 0): peak memory is taken over
+ *                  the times at or after it (every residency interval clipped
+ *                  to [t_now, inf)).
+ * A GMG with any of them simulates under index-order dispatch with latency-
+ * only transfers (SS_DISPATCH_READY and SS_LINK_PORTS: SS_ERR_UNSUPPORTED).
+ *
  * The loader also rejects snapshots whose time horizon could overflow:
- * H = max_d last-slice start + max_r release + sum_v max_c dur[v][c]
- *     + sum_v (outdeg(v) + 1) * max_k (lat[k] + ceil(out_bytes[v] / bw[k]))
- * must stay below 2^62, N * H below 2^63, and sum_v out_bytes[v] * (D + 1)
- * below 2^63.
+ * H = T + sum_v max_c dur[v][c]
+ *     + sum_v (outdeg(v) + 1) * max_k (lat[k] + ceil(out_bytes[v] / bw[k])),
+ * with T the largest of the last-slice starts, releases, issue times, done
+ * times and t_now, must stay below 2^62, N * H below 2^63, and
+ * sum_v out_bytes[v] * (D + 1) below 2^63.
  */
 typedef struct ss_gmg_desc {
   int64_t n_ops, n_edges, n_dev, n_class, n_link, n_req;
@@ -96,6 +117,9 @@ typedef struct ss_gmg_desc {
   const int64_t *cap;
   const int64_t *release;
   const int64_t *deadline;
+  const int64_t *done_fin; /* nullable */
+  const int64_t *issue_at; /* nullable */
+  int64_t t_now;
 } ss_gmg_desc;
 
 /*
@@ -123,7 +147,9 @@ int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req)
  *     finish) at which it fits entirely inside one idle slice; the ready time
  *     is the later of the request's release and, over the predecessors, their
  *     finish plus the transfer estimate when they ran on another device
- *     (Sec. 3.3.2);
+ *     (Sec. 3.3.2); with a running schedule's state (see ss_gmg_desc) done
+ *     ops keep their recorded finish, ops wait for their issue time and
+ *     transfers for their destination's first issued consumer;
  *   - memory: an op's output occupies its device from the op's start until
  *     its last local consumer finishes and its last outgoing transfer has
  *     arrived (forever if it has no consumer); each (output, remote device)
@@ -265,9 +291,11 @@ int ss_state_info(const ss_state *st, int64_t *n_ops);
  * on the same arguments when `from` was captured from a simulation of a GMG
  * whose first k ops (and their predecessors, requests, durations, sizes) are
  * g's first k ops and whose placement of them is every candidate's (the
- * caller's contract; the library checks k <= n_ops and the device and request
- * counts).  Each candidate's schedule is walked from op k only; the memory
- * pass covers all ops.  from may be NULL or empty (a full simulation).
+ * caller's contract, which with issue times also asks that ops k.. be issued
+ * no earlier than ops ..k-1, as in the incremental loop, so that no later
+ * consumer moves an earlier transfer; the library checks k <= n_ops and the
+ * device and request counts).  Each candidate's schedule is walked from op k
+ * only; the memory pass covers all ops.  from may be NULL or empty (a full simulation).
  * Placements of the first k ops are still checked against n_dev
  * (SS_VIOLATION_INVALID).  Asynchronous on hip_stream.  Errors:
  * SS_ERR_INVALID_ARG, SS_ERR_OOM, SS_ERR_DEVICE, SS_ERR_UNSUPPORTED.
@@ -372,22 +400,28 @@ int ss_est_predict(const double *coef, int64_t n_est, int64_t n_feat, const int3
 /*
  * Incremental simulation-based scheduling (Alg. 1, Sec. 3.4).  A scheduler
  * holds the GMG of a whole run (every op that will be scheduled) with a state
- * per op, and keeps the two frontiers of Sec. 3.4.1: the scheduled frontier
- * (issued or done ops with an unscheduled successor, whose outputs stay on
- * their devices as checkpoints) and the unscheduled frontier (unscheduled ops
- * whose predecessors are all issued or done).
+ * per op (unscheduled, issued, done) and its scheduling metadata (Sec. 3.2:
+ * the time it was issued, the time it completed), and keeps the two
+ * frontiers of Sec. 3.4.1: the scheduled frontier (issued or done ops with an
+ * unscheduled successor, whose outputs stay on their devices as checkpoints)
+ * and the unscheduled frontier (unscheduled ops whose predecessors are all
+ * issued or done).
  *
  * ss_sched_desc (HOST pointers, copied by ss_sched_create):
- *   gmg            the run's GMG; the loader's rules apply (ss_gmg_load).
+ *   gmg            the run's GMG; the loader's rules apply (ss_gmg_load); it
+ *                  holds no running state (done_fin, issue_at NULL, t_now 0):
+ *                  the scheduler keeps that.
  *   n_part, part_dev[n_part][n_ops]  the pre-defined partitions (Sec. 3.4.2):
  *                  partition p places op v on device part_dev[p][v] (< n_dev).
  *   priority[n_req] request priority, smaller first (for instance the
  *                  deadline); ties go to the lower op index.
  *   issue_budget   Alg. 1's budget on issued (not yet done) ops, >= 1.
  *   batch_cap      the batch cap of CollectConnectedGraph, >= 1.
- *   flags          0 or SS_SELECT_REQUIRE_SLA (feasibility also requires every
- *                  request's slack >= 0).
+ *   flags          SS_SELECT_REQUIRE_SLA (feasibility also requires every
+ *                  request's slack >= 0) and SS_SCHED_NO_PREFIX_REUSE (every
+ *                  round simulates its whole graph; for measurement), or 0.
  */
+#define SS_SCHED_NO_PREFIX_REUSE 0x2
 #define SS_OP_UNSCHEDULED 0
 #define SS_OP_ISSUED 1
 #define SS_OP_DONE 2
@@ -416,35 +450,41 @@ int ss_sched_create(const ss_sched_desc *desc, ss_sched **out);
 void ss_sched_free(ss_sched *s);
 
 /*
- * One round of Alg. 1.  Returns at once (SS_ROUND_BUDGET, SS_ROUND_IDLE) when
- * the issued ops reach the budget or the unscheduled frontier is empty.
- * Otherwise: the highest-priority op of the unscheduled frontier; its batch,
- * collected by repeatedly adding the lowest-index unscheduled successor of a
- * batch op whose predecessors are all issued, done or in the batch, up to
- * batch_cap ops; one candidate per partition, simulated together on the GPU
- * (ss_simulate_batch, index-order dispatch) over the graph of the scheduled
- * ops in the order they were issued (the device queues' order) followed by
- * the batch in index order, with the estimated durations; the feasible
- * candidate with the smallest sum of finish times (ties to the lower
- * partition) is written back and the batch marked issued.
+ * One round of Alg. 1 at time `now` (>= the previous round's, < 2^62).
+ * Returns at once (SS_ROUND_BUDGET, SS_ROUND_IDLE) when the issued ops reach
+ * the budget or the unscheduled frontier is empty.  Otherwise: the
+ * highest-priority op of the unscheduled frontier; its batch, collected by
+ * repeatedly adding the lowest-index unscheduled successor of a batch op
+ * whose predecessors are all issued, done or in the batch, up to batch_cap
+ * ops; one candidate per partition, simulated together on the GPU
+ * (ss_simulate_batch, index-order dispatch) over the snapshot (Sec. 3.3.2):
+ * in the order they were issued (the device queues' order), the issued ops
+ * that are not done and the done ops whose output still feeds an op to run,
+ * then the batch in index order issued at `now`; done ops keep their
+ * recorded completion, the others take their estimates and start no earlier
+ * than their issue (see ss_gmg_desc), and memory is checked from `now` on;
+ * the feasible candidate with the smallest sum of finish times (ties to the
+ * lower partition) is written back and the batch marked issued at `now`.
  * out_ops (HOST, >= batch_cap entries) receives the batch in index order and
  * *out_n its size (also for SS_ROUND_INFEASIBLE, 0 otherwise); *out_part the
  * partition (-1 unless issued); *out_status an SS_ROUND_* value.  The call
  * runs its GPU work on hip_stream and synchronises it before returning.
  * Errors: SS_ERR_INVALID_ARG, SS_ERR_OOM, SS_ERR_DEVICE.
  */
-int ss_sched_round(ss_sched *s, int *out_status, int64_t *out_ops, int64_t *out_n, int64_t *out_part,
-                   void *hip_stream);
+int ss_sched_round(ss_sched *s, int64_t now, int *out_status, int64_t *out_ops, int64_t *out_n,
+                   int64_t *out_part, void *hip_stream);
 
-/* Executor feedback: issued op `op` is done and no longer counts against the
- * issue budget (its place in the simulated history is unchanged; measured
- * times refine the estimators, ss_est_*).  Errors: SS_ERR_INVALID_ARG (op not
- * issued). */
-int ss_sched_complete(ss_sched *s, int64_t op);
+/* Executor feedback: issued op `op` completed at time t_done, which must be
+ * later than its issue and than every predecessor's completion (each
+ * predecessor reported first), and below 2^62.  It no longer counts against
+ * the issue budget; its recorded completion enters the next snapshots while
+ * an op to run still reads its output.  Errors: SS_ERR_INVALID_ARG. */
+int ss_sched_complete(ss_sched *s, int64_t op, int64_t t_done);
 
-/* Current state (SS_OP_*) and device of every op, HOST arrays of n_ops
- * entries; either may be NULL.  The device of an unscheduled op is 0. */
-int ss_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place);
+/* Current state (SS_OP_*), device, issue time and completion time (-1 until
+ * then) of every op, HOST arrays of n_ops entries; any may be NULL.  The
+ * device of an unscheduled op is 0. */
+int ss_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place, int64_t *issue_t, int64_t *done_t);
 
 /*
  * The library takes every device buffer (staged GMGs, scratch, scheduler and

@@ -41,7 +41,8 @@ class _Gmg(ctypes.Structure):
                 ("n_link", ctypes.c_int64), ("n_req", ctypes.c_int64)] + \
                [(n, ctypes.c_void_p) for n in ("pred_ptr", "pred_idx", "op_req", "dur", "out_bytes", "dev_class",
                                                "link_class", "bw", "lat", "slice_ptr", "slice_begin", "slice_end",
-                                               "cap", "release", "deadline", "done_fin", "issue_at")]
+                                               "cap", "release", "deadline", "done_fin", "issue_at")] + \
+               [("t_now", ctypes.c_int64)]
 
 
 _P = ctypes.c_void_p
@@ -85,7 +86,7 @@ class OracleGmg:
                       arr("link_class", np.uint8), arr("bw", np.int64), arr("lat", np.int64),
                       arr("slice_ptr", np.int64), arr("slice_begin", np.int64), arr("slice_end", np.int64),
                       arr("cap", np.int64), arr("release", np.int64), arr("deadline", np.int64),
-                      opt("done_fin"), opt("issue_at"))
+                      opt("done_fin"), opt("issue_at"), int(getattr(g, "t_now", 0) or 0))
 
 
 def _og(g):

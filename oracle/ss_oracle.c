@@ -36,7 +36,9 @@
  *     a done op is not simulated, it finished at its recorded time on its
  *     device; an op does not start before it was issued, and the transfer of
  *     an output to a device does not start before the first consumer there
- *     was issued (its Intent exists only from then on).
+ *     was issued (its Intent exists only from then on); the peak is that of
+ *     the memory held at or after the snapshot's timestamp (every residency
+ *     interval clipped to [t_now, inf)).
  *
  * Parity: pinned by closed forms, bounds, brute force and hand-worked cases in
  * the CPU test-suite (no printed worked example exists in the paper).
@@ -449,6 +451,14 @@ static int schedule_ready_order(const sso_gmg *g, const uint8_t *place, const su
 
 typedef struct { int64_t dev, lo, hi, bytes; } interval;
 
+/* The part of an interval at or after t0 (empty, [t0, t0), when it ended
+ * before): memory is counted from the snapshot's timestamp on. */
+static interval clip(interval iv, int64_t t0) {
+  if (iv.lo < t0) iv.lo = t0;
+  if (iv.hi < t0) iv.hi = t0;
+  return iv;
+}
+
 /* Residency intervals of one scheduled candidate (see the memory reading in
  * the file header).  Returns the count, or -1 on allocation failure. */
 static int64_t residency_intervals(const sso_gmg *g, const uint8_t *place, const succ_csr *sc, const int64_t *st,
@@ -472,7 +482,7 @@ static int64_t residency_intervals(const sso_gmg *g, const uint8_t *place, const
         if (t > free_at) free_at = t;
       }
     }
-    iv[n++] = (interval){d, st[v], free_at, b};
+    iv[n++] = clip((interval){d, st[v], free_at, b}, g->t_now);
     /* one remote copy per destination device, from the transfer's start (v's
      * finish, not before the first consumer there was issued; with arbitrated
      * ports the admitted start) until the last consumer on that device
@@ -488,7 +498,7 @@ static int64_t residency_intervals(const sso_gmg *g, const uint8_t *place, const
       for (int64_t e2 = s0; e2 < s1; ++e2)
         if (place[sc->idx[e2]] == dx && fin[sc->idx[e2]] > last) last = fin[sc->idx[e2]];
       const int64_t floor_ = transfer_floor(g, sc, place, v, dx);
-      iv[n++] = (interval){dx, xs ? xs[e] : fin[v] > floor_ ? fin[v] : floor_, last, b};
+      iv[n++] = clip((interval){dx, xs ? xs[e] : fin[v] > floor_ ? fin[v] : floor_, last, b}, g->t_now);
     }
   }
   *out = iv;

@@ -47,9 +47,12 @@ typedef struct {
    *                    that time minus its estimate;
    *   issue_at[n_ops]  the time an op was issued: it does not start earlier,
    *                    and a transfer to it does not start before the first
-   *                    of its destination's consumers was issued. */
+   *                    of its destination's consumers was issued.
+   * t_now is the snapshot's timestamp: peak memory is taken over times at or
+   * after it (0 without a snapshot, where every residency starts at >= 0). */
   const int64_t *done_fin;
   const int64_t *issue_at;
+  int64_t t_now;
 } sso_gmg;
 
 /* dispatch rules */

@@ -292,7 +292,11 @@ extern "C" int ss_sched_create(const ss_sched_desc *d, ss_sched **out) {
   if (d->gmg->n_req > 0 && !d->priority) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: priority is NULL");
   if (d->issue_budget < 1 || d->batch_cap < 1)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: issue_budget and batch_cap must be >= 1");
-  if (d->flags & ~SS_SELECT_REQUIRE_SLA) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: unknown flags");
+  if (d->flags & ~(SS_SELECT_REQUIRE_SLA | SS_SCHED_NO_PREFIX_REUSE))
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: unknown flags");
+  if (d->gmg->done_fin || d->gmg->issue_at || d->gmg->t_now != 0)
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: the run's GMG holds no running state (the scheduler "
+                                            "keeps it)");
   const int64_t N = d->gmg->n_ops, D = d->gmg->n_dev;
   if (N < 0 || D < 1) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: bad GMG sizes");
   if (d->n_part > (int64_t(1) << 40) / std::max<int64_t>(N, 1))
@@ -306,24 +310,25 @@ extern "C" void ss_sched_free(ss_sched *s) {
   if (s) ss_run_sched_free(s);
 }
 
-extern "C" int ss_sched_round(ss_sched *s, int *out_status, int64_t *out_ops, int64_t *out_n, int64_t *out_part,
-                              void *hip_stream) {
+extern "C" int ss_sched_round(ss_sched *s, int64_t now, int *out_status, int64_t *out_ops, int64_t *out_n,
+                              int64_t *out_part, void *hip_stream) {
   ss_clear_error();
   if (!s || !out_status || !out_ops || !out_n || !out_part)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_round: NULL argument");
-  return ss_run_sched_round(s, out_status, out_ops, out_n, out_part, static_cast<hipStream_t>(hip_stream));
+  if (now < 0 || now >= ((int64_t)1 << 62)) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_round: now out of range");
+  return ss_run_sched_round(s, now, out_status, out_ops, out_n, out_part, static_cast<hipStream_t>(hip_stream));
 }
 
-extern "C" int ss_sched_complete(ss_sched *s, int64_t op) {
+extern "C" int ss_sched_complete(ss_sched *s, int64_t op, int64_t t_done) {
   ss_clear_error();
   if (!s) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_complete: s is NULL");
-  return ss_run_sched_complete(s, op);
+  return ss_run_sched_complete(s, op, t_done);
 }
 
-extern "C" int ss_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place) {
+extern "C" int ss_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place, int64_t *issue_t, int64_t *done_t) {
   ss_clear_error();
   if (!s) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_state: s is NULL");
-  ss_run_sched_state(s, state, place);
+  ss_run_sched_state(s, state, place, issue_t, done_t);
   return SS_OK;
 }
 

@@ -344,6 +344,29 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
         return bad("deadline magnitude must be below 2^62");
       max_rel = std::max<i128>(max_rel, d->release[r]);
     }
+    // a running schedule's state: done ops (their predecessors done and
+    // finished strictly earlier, themselves strictly after their issue),
+    // issue times, the snapshot's timestamp; the latest of them bounds the
+    // horizon's start like a release
+    const bool snapshot = d->done_fin || d->issue_at || d->t_now != 0;
+    if (d->t_now < 0 || d->t_now >= kTimeLimit) return bad("t_now must be in [0, 2^62)");
+    max_rel = std::max<i128>(max_rel, d->t_now);
+    for (int64_t v = 0; v < N; ++v) {
+      if (d->issue_at) {
+        if (d->issue_at[v] < 0 || d->issue_at[v] >= kTimeLimit) return bad("issue times must be in [0, 2^62)");
+        max_rel = std::max<i128>(max_rel, d->issue_at[v]);
+      }
+      if (!d->done_fin || d->done_fin[v] == -1) continue;
+      const int64_t f = d->done_fin[v];
+      if (f < 0 || f >= kTimeLimit) return bad("done_fin must be -1 (not done) or in [0, 2^62)");
+      if (d->issue_at && f <= d->issue_at[v]) return bad("a done op must finish after its issue time");
+      for (int64_t e = d->pred_ptr[v]; e < d->pred_ptr[v + 1]; ++e) {
+        const int64_t fu = d->done_fin[d->pred_idx[e]];
+        if (fu < 0) return bad("a done op's predecessors must be done");
+        if (fu >= f) return bad("a done op must finish after its predecessors");
+      }
+      max_rel = std::max<i128>(max_rel, f);
+    }
 
     // ------------------------------------------- precompute + overflow bound
     std::vector<int64_t> xfer((size_t)N * K);
@@ -381,7 +404,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     // 32-bit time path: every time the simulation can produce is <= horizon
     int64_t max_bytes = 0;
     for (int64_t v = 0; v < N; ++v) max_bytes = std::max(max_bytes, d->out_bytes[v]);
-    const bool time32 = horizon < (i128)UINT32_MAX && N <= 65535 && E <= 65535 && max_slices <= 65535 &&
+    const bool time32 = !snapshot && horizon < (i128)UINT32_MAX && N <= 65535 && E <= 65535 && max_slices <= 65535 &&
                         max_bytes <= (int64_t)UINT32_MAX;
     std::vector<uint32_t> dur32, xfer32, sb32, se32, rel32, meta, lbits, bytes32, succ2, succ2_pe, lutk, lutw;
     std::vector<uint8_t> lgrp;
@@ -530,6 +553,8 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     const size_t o_rel = pk.add(d->release, R * sizeof(int64_t));
     const size_t o_dl = pk.add(d->deadline, R * sizeof(int64_t));
     const size_t o_link = pk.add(d->link_class, D * D);
+    const size_t o_done = d->done_fin ? pk.add(d->done_fin, N * sizeof(int64_t)) : 0;
+    const size_t o_issue = d->issue_at ? pk.add(d->issue_at, N * sizeof(int64_t)) : 0;
     const size_t o_dur32 = pk.add(dur32), o_xfer32 = pk.add(xfer32), o_sb32 = pk.add(sb32), o_se32 = pk.add(se32),
                  o_rel32 = pk.add(rel32), o_meta = pk.add(meta), o_lbits = pk.add(lbits), o_b32 = pk.add(bytes32),
                  o_succ2 = pk.add(succ2), o_succ2_pe = pk.add(succ2_pe), o_lutk = pk.add(lutk), o_lutw = pk.add(lutw), o_lgrp = pk.add(lgrp),
@@ -583,6 +608,9 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     V.release = reinterpret_cast<const int64_t *>(base + o_rel);
     V.deadline = reinterpret_cast<const int64_t *>(base + o_dl);
     V.link_class = reinterpret_cast<const uint8_t *>(base + o_link);
+    V.done_fin = d->done_fin ? reinterpret_cast<const int64_t *>(base + o_done) : nullptr;
+    V.issue_at = d->issue_at ? reinterpret_cast<const int64_t *>(base + o_issue) : nullptr;
+    V.t_now = d->t_now;
     V.time32 = time32 ? 1 : 0;
     V.dur32 = reinterpret_cast<const uint32_t *>(base + o_dur32);
     V.xfer32 = reinterpret_cast<const uint32_t *>(base + o_xfer32);
@@ -614,6 +642,7 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     g->n_req = R;
     g->max_slices = max_slices;
     g->horizon = (int64_t)horizon;
+    g->snapshot = snapshot;
     for (int64_t v = 0; v < N; ++v) g->max_indeg = std::max<int64_t>(g->max_indeg, d->pred_ptr[v + 1] - d->pred_ptr[v]);
     g->max_outdeg = max_outdeg;
     *out = g;

@@ -4,18 +4,27 @@
 // call on the GPU, selection by ss_select_best, write-back.
 //
 // Host-side state, per op: unscheduled / issued / done, the device chosen for
-// it, and the number of its predecessors still unscheduled (it is on the
-// unscheduled frontier when that count is zero).  The frontier is kept
-// ordered by (request priority, op), so the highest-priority op is its first
-// element.
+// it, its issue and completion times (the scheduling metadata of Sec. 3.2),
+// the number of its predecessors still unscheduled (it is on the unscheduled
+// frontier when that count is zero) and of its successors not done.  The
+// frontier is kept ordered by (request priority, op), so the highest-priority
+// op is its first element.
 //
-// A round's simulated graph holds the scheduled ops in the order they were
-// issued (the order of the device queues), then the batch in index order: a
-// topological order in which all candidates place the ops before the batch
-// alike, so under index-order dispatch those ops have the same schedule in
-// every candidate and the candidates' finish-time sums differ by the batch's
-// alone.  Later rounds only extend the order.  Durations are the estimates;
-// completion feedback changes an op's state, not the simulated history.
+// A round at time `now` simulates the snapshot (Sec. 3.3.2): the issued ops
+// that are not done and the done ops whose output still feeds an op to run,
+// in the order they were issued, then the batch in index order, issued at
+// `now`.  Done ops keep their recorded completion; the rest is simulated with
+// the estimates, no op before its issue; memory is checked from `now` on.
+// The ops before the batch precede it in every device queue and were issued
+// no later, so they have one schedule in every candidate and the candidates'
+// finish-time sums differ by the batch's alone.  A done op with no successor
+// left to run is out of every later snapshot, so the graph is bounded by the
+// issue budget, the checkpoints and one batch.
+//
+// Prefix reuse: the chosen candidate's state after its round's graph is
+// captured; while no completion arrives, the next round's graph is that graph
+// followed by a new batch (the batch just issued joins the issued ops, the
+// done ops still in play stay), so every candidate resumes after it.
 #include <algorithm>
 #include <new>
 #include <queue>
@@ -35,7 +44,13 @@ struct ss_sched {
   int flags = 0;
   int device = 0;
   std::vector<uint8_t> state, place;
-  std::vector<int32_t> issue_order;  // scheduled ops in the order they were issued
+  std::vector<int64_t> issue_t, done_t;  // -1 until issued / done
+  int64_t now = 0;                       // time of the latest round
+  // ops that can still be in a snapshot (issued, or done with a successor not
+  // done), in the order they were issued; a done op leaves for good once its
+  // last successor is done
+  std::vector<int32_t> issue_order;
+  std::vector<int32_t> open_succ;  // successors not done
   std::vector<int32_t> missing;  // unscheduled predecessors
   std::vector<uint8_t> rows;     // host candidate rows of the current round (kept: no new pages each round)
   std::set<std::pair<int64_t, int32_t>> frontier;
@@ -46,6 +61,8 @@ struct ss_sched {
   // the chosen candidate's simulation state after the scheduled ops (the
   // prefix of the next round), and a second state to capture the next one in
   ss_state *prefix = nullptr, *next = nullptr;
+  bool prefix_ok = false;  // no completion since prefix was captured
+  bool reuse = true;       // prefix reuse enabled
 
 };
 
@@ -141,6 +158,10 @@ int ss_run_sched_create(const ss_sched_desc *d, ss_sched **out) {
     s->flags = d->flags;
     s->state.assign((size_t)s->N, SS_OP_UNSCHEDULED);
     s->place.assign((size_t)s->N, 0);
+    s->issue_t.assign((size_t)s->N, -1);
+    s->done_t.assign((size_t)s->N, -1);
+    s->open_succ.assign((size_t)s->N, 0);
+    s->reuse = !(d->flags & SS_SCHED_NO_PREFIX_REUSE);
     s->missing.assign((size_t)s->N, 0);
     s->succ_ptr.assign((size_t)s->N + 1, 0);
     s->succ_idx.assign((size_t)s->E, 0);
@@ -148,6 +169,7 @@ int ss_run_sched_create(const ss_sched_desc *d, ss_sched **out) {
       s->missing[v] = s->pred_ptr[v + 1] - s->pred_ptr[v];
       for (int32_t e = s->pred_ptr[v]; e < s->pred_ptr[v + 1]; ++e) ++s->succ_ptr[s->pred_idx[e] + 1];
     }
+    for (int64_t v = 0; v < s->N; ++v) s->open_succ[v] = s->succ_ptr[v + 1];
     for (int64_t v = 0; v < s->N; ++v) s->succ_ptr[v + 1] += s->succ_ptr[v];
     std::vector<int32_t> fill(s->succ_ptr.begin(), s->succ_ptr.end() - 1);
     for (int64_t v = 0; v < s->N; ++v)
@@ -189,9 +211,12 @@ void ss_run_sched_free(ss_sched *s) {
   delete s;
 }
 
-int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, int64_t *part, hipStream_t stream) {
+int ss_run_sched_round(ss_sched *s, int64_t now, int *status, int64_t *ops, int64_t *n_ops, int64_t *part,
+                       hipStream_t stream) {
   *n_ops = 0;
   *part = -1;
+  if (now < s->now) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_round: rounds come at non-decreasing times");
+  s->now = now;
   if (s->n_issued >= s->budget) {
     *status = SS_ROUND_BUDGET;
     return SS_OK;
@@ -205,6 +230,11 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
   std::vector<int32_t> order;
   try {
     batch = collect(s, op);
+    // the snapshot's ops: done ops whose every successor is done leave for good
+    size_t w = 0;
+    for (const int32_t v : s->issue_order)
+      if (s->state[v] == SS_OP_ISSUED || s->open_succ[v] > 0) s->issue_order[w++] = v;
+    s->issue_order.resize(w);
     order = s->issue_order;
     order.insert(order.end(), batch.begin(), batch.end());
     s->issue_order.reserve(order.size());  // the write-back cannot fail half-way
@@ -213,21 +243,25 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
   }
   const int64_t Ns = (int64_t)order.size(), nb = (int64_t)batch.size(), npre = Ns - nb, P = s->P;
 
-  // the round's graph: the scheduled ops and the batch, renumbered
+  // the round's graph: the snapshot's ops and the batch, renumbered; a done
+  // op's predecessors outside the snapshot are dropped (it is not simulated)
   std::vector<int32_t> newid((size_t)s->N, -1), sp_ptr(1, 0), sp_idx, sreq((size_t)Ns);
   sp_idx.reserve(s->pred_idx.size());
   sp_ptr.reserve((size_t)Ns + 1);
-  std::vector<int64_t> sdur((size_t)(Ns * s->C)), sbytes((size_t)Ns);
+  std::vector<int64_t> sdur((size_t)(Ns * s->C)), sbytes((size_t)Ns), sdone((size_t)Ns), sissue((size_t)Ns);
   for (int64_t i = 0; i < Ns; ++i) newid[order[i]] = (int32_t)i;
   for (int64_t i = 0; i < Ns; ++i) {
     const int32_t v = order[i];
     const size_t first = sp_idx.size();
-    for (int32_t e = s->pred_ptr[v]; e < s->pred_ptr[v + 1]; ++e) sp_idx.push_back(newid[s->pred_idx[e]]);
+    for (int32_t e = s->pred_ptr[v]; e < s->pred_ptr[v + 1]; ++e)
+      if (newid[s->pred_idx[e]] >= 0) sp_idx.push_back(newid[s->pred_idx[e]]);
     std::sort(sp_idx.begin() + (std::ptrdiff_t)first, sp_idx.end());
     sp_ptr.push_back((int32_t)sp_idx.size());
     sreq[i] = s->op_req[v];
     for (int64_t c = 0; c < s->C; ++c) sdur[i * s->C + c] = s->dur[v * s->C + c];
     sbytes[i] = s->out_bytes[v];
+    sdone[i] = s->state[v] == SS_OP_DONE ? s->done_t[v] : -1;
+    sissue[i] = i < npre ? s->issue_t[v] : now;
   }
   ss_gmg_desc gd{};
   gd.n_ops = Ns;
@@ -251,8 +285,11 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
   gd.cap = s->cap.data();
   gd.release = s->release.data();
   gd.deadline = s->deadline.data();
+  gd.done_fin = sdone.data();
+  gd.issue_at = sissue.data();
+  gd.t_now = now;
 
-  // candidate b = partition b: the scheduled ops where they are, the batch by the partition
+  // candidate b = partition b: the snapshot's ops where they are, the batch by the partition
   try {
     if (s->rows.size() < (size_t)(P * Ns)) s->rows.resize((size_t)(P * Ns));
   } catch (const std::bad_alloc &) {
@@ -274,7 +311,7 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
   const size_t need = sz_rows + 2 * sz_ms + sz_vi + sz_sl + sz_best;
   hipError_t err = hipSuccess;
   if (need > s->dev_bytes) {
-    const size_t grow = std::max(need, 2 * s->dev_bytes);  // rounds' graphs grow: few reallocations
+    const size_t grow = std::max(need, 2 * s->dev_bytes);  // few reallocations as graphs vary
     if (s->dev_buf) {
       (void)hipStreamSynchronize(stream);
       ss_pool_free(s->dev_buf, stream);
@@ -298,21 +335,22 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
   int64_t best[2] = {-1, 0};
   err = hipMemcpyAsync(d_rows, rows.data(), (size_t)(P * Ns), hipMemcpyHostToDevice, stream);
   if (err == hipSuccess) {
-    // every candidate resumes after the scheduled ops (the prefix state holds
-    // them when the previous issuing round captured; else all ops are walked)
+    // every candidate resumes after the snapshot's ops when the state
+    // captured at the last issuing round still describes them
     int64_t k = 0;
     (void)ss_state_info(s->prefix, &k);
-    const ss_state *from = k == npre ? s->prefix : nullptr;
+    const ss_state *from = s->reuse && s->prefix_ok && k == npre ? s->prefix : nullptr;
     rc = ss_simulate_batch_resume(g, from, d_rows, P, d_ms, nullptr, d_vi, d_sl, d_sum, stream);
     if (rc == SS_OK)
       rc = ss_select_best(g, d_vi, d_sum, d_sl, P, s->flags & SS_SELECT_REQUIRE_SLA, d_best, stream);
     if (rc == SS_OK) err = hipMemcpyAsync(best, d_best, sizeof(best), hipMemcpyDeviceToHost, stream);
     if (rc == SS_OK && err == hipSuccess) err = hipStreamSynchronize(stream);
-    if (rc == SS_OK && err == hipSuccess && best[0] >= 0) {
+    if (rc == SS_OK && err == hipSuccess && best[0] >= 0 && s->reuse) {
       // the chosen candidate's schedule once more, captured for the next round
       rc = ss_state_capture(g, from, d_rows + best[0] * Ns, s->next, stream);
       if (rc == SS_OK) err = hipStreamSynchronize(stream);
       if (rc == SS_OK && err == hipSuccess) std::swap(s->prefix, s->next);
+      s->prefix_ok = rc == SS_OK && err == hipSuccess;
     }
   }
   ss_gmg_free(g);
@@ -325,22 +363,39 @@ int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, i
     *status = SS_ROUND_INFEASIBLE;
     return SS_OK;
   }
-  for (int64_t i = 0; i < nb; ++i) mark_issued(s, batch[i], s->part[best[0] * s->N + batch[i]]);
+  for (int64_t i = 0; i < nb; ++i) {
+    mark_issued(s, batch[i], s->part[best[0] * s->N + batch[i]]);
+    s->issue_t[batch[i]] = now;
+  }
   s->issue_order.insert(s->issue_order.end(), batch.begin(), batch.end());
   *part = best[0];
   *status = SS_ROUND_ISSUED;
   return SS_OK;
 }
 
-int ss_run_sched_complete(ss_sched *s, int64_t op) {
+int ss_run_sched_complete(ss_sched *s, int64_t op, int64_t t_done) {
   if (op < 0 || op >= s->N || s->state[op] != SS_OP_ISSUED)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_complete: op is not issued");
+  if (t_done <= s->issue_t[op])
+    return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_complete: completion not after the op's issue");
+  if (t_done >= ((int64_t)1 << 62)) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_complete: time >= 2^62");
+  for (int32_t e = s->pred_ptr[op]; e < s->pred_ptr[op + 1]; ++e) {
+    const int32_t u = s->pred_idx[e];
+    if (s->state[u] != SS_OP_DONE || s->done_t[u] >= t_done)
+      return ss_set_error(SS_ERR_INVALID_ARG,
+                          "ss_sched_complete: completion before a predecessor's completion");
+  }
   s->state[op] = SS_OP_DONE;
+  s->done_t[op] = t_done;
   --s->n_issued;
+  for (int32_t e = s->pred_ptr[op]; e < s->pred_ptr[op + 1]; ++e) --s->open_succ[s->pred_idx[e]];
+  s->prefix_ok = false;
   return SS_OK;
 }
 
-void ss_run_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place) {
+void ss_run_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place, int64_t *issue_t, int64_t *done_t) {
   if (state) std::copy(s->state.begin(), s->state.end(), state);
   if (place) std::copy(s->place.begin(), s->place.end(), place);
+  if (issue_t) std::copy(s->issue_t.begin(), s->issue_t.end(), issue_t);
+  if (done_t) std::copy(s->done_t.begin(), s->done_t.end(), done_t);
 }

@@ -8,7 +8,11 @@
 //   [device][lane], so the 64 lanes of a wave hit 64 distinct banks whatever
 //   device each one touches.  Op-indexed GMG data is the same for every lane
 //   (all lanes are at the same op), so it is read with wave-uniform loads.
-//   Finish times go to a per-chunk scratch row for the memory pass.
+//   Finish times go to a per-chunk scratch row for the memory pass.  With a
+//   running schedule's state in the GMG (Sec. 3.2, 3.3.2) a done op keeps its
+//   recorded finish and frees its device from then on, an op waits for its
+//   issue time, and a transfer for the first issue among its destination's
+//   consumers (xfer_floor).
 //
 // port_event_schedule: transfer arbitration (SS_LINK_PORTS, Sec. 3.5.2)
 //   event by event, one wave per candidate (see below).
@@ -38,6 +42,19 @@ constexpr int64_t kFinBudget = int64_t(16) << 30; // bytes of finish-time scratc
 constexpr int kMemBlocksPerCU = 4;
 
 __device__ __forceinline__ int64_t imax(int64_t a, int64_t b) { return a > b ? a : b; }
+
+// Running schedule (GMG issue times given): the transfer of u's output to
+// device e starts no earlier than the first issue time among u's consumers
+// placed on e, the moment its Intent exists.  0 when none is there.
+__device__ int64_t xfer_floor(const GmgView &G, const uint8_t *prow, int u, int e) {
+  int64_t f = INT64_MAX;
+  const int q1 = G.succ_ptr[u + 1];
+  for (int q = G.succ_ptr[u]; q < q1; ++q) {
+    const int x = G.succ_idx[q];
+    if (prow[x] == e && G.issue_at[x] < f) f = G.issue_at[x];
+  }
+  return f == INT64_MAX ? 0 : f;
+}
 
 // ------------------------------------------------------------------ schedule
 // Resumption from a captured state (ss_simulate_batch_resume): every
@@ -111,36 +128,50 @@ __global__ __launch_bounds__(kWave) void schedule_kernel(const GmgView G, const 
       invalid = true;
       d = 0;
     }
-    const int64_t w = G.dur[(int64_t)v * C + G.dev_class[d]];
     const int r = G.op_req[v];
-    // ready: release, and every predecessor's finish plus its transfer
-    int64_t ready = G.release[r];
-    const int e1 = G.pred_ptr[v + 1];
-    for (int e = G.pred_ptr[v]; e < e1; ++e) {
-      const int u = G.pred_idx[e];
-      int64_t t = frow[u];
-      int du = prow[u];
-      if (du >= D) du = 0;
-      if (du != d) t += G.xfer[(int64_t)u * K + G.link_class[du * D + d]];
-      ready = imax(ready, t);
-    }
-    // one op at a time: not before the device's previous finish; then the
-    // first idle slice that holds [s, s + w) (the cursor only moves forward)
     const int slot = d * kWave + lane;
-    const int64_t t = imax(ready, clk[slot]);
-    const int sbase = G.slice_ptr[d];
-    int k = cur[slot];
-    int64_t s;
-    for (;;) {
-      const int64_t a = G.slice_begin[sbase + k], e = G.slice_end[sbase + k];
-      s = imax(t, a);
-      if (s + w <= e) break;
-      ++k;
+    const int64_t done = G.done_fin ? G.done_fin[v] : -1;
+    int64_t f;
+    if (done >= 0) {
+      // done (running schedule): it finished at its recorded time; the
+      // device is free from then on
+      f = done;
+      clk[slot] = imax(clk[slot], f);
+    } else {
+      const int64_t w = G.dur[(int64_t)v * C + G.dev_class[d]];
+      // ready: release (and issue time), and every predecessor's finish plus
+      // its transfer (started no earlier than the transfer's Intent)
+      int64_t ready = G.release[r];
+      if (G.issue_at) ready = imax(ready, G.issue_at[v]);
+      const int e1 = G.pred_ptr[v + 1];
+      for (int e = G.pred_ptr[v]; e < e1; ++e) {
+        const int u = G.pred_idx[e];
+        int64_t t = frow[u];
+        int du = prow[u];
+        if (du >= D) du = 0;
+        if (du != d) {
+          if (G.issue_at) t = imax(t, xfer_floor(G, prow, u, d));
+          t += G.xfer[(int64_t)u * K + G.link_class[du * D + d]];
+        }
+        ready = imax(ready, t);
+      }
+      // one op at a time: not before the device's previous finish; then the
+      // first idle slice that holds [s, s + w) (the cursor only moves forward)
+      const int64_t t = imax(ready, clk[slot]);
+      const int sbase = G.slice_ptr[d];
+      int k = cur[slot];
+      int64_t s;
+      for (;;) {
+        const int64_t a = G.slice_begin[sbase + k], e = G.slice_end[sbase + k];
+        s = imax(t, a);
+        if (s + w <= e) break;
+        ++k;
+      }
+      cur[slot] = (uint16_t)k;
+      f = s + w;
+      clk[slot] = f;
     }
-    cur[slot] = (uint16_t)k;
-    const int64_t f = s + w;
     frow[v] = f;
-    clk[slot] = f;
     ms = imax(ms, f);
     sum += f;
     int64_t *cr = comp + (int64_t)r * nb + c;
@@ -702,16 +733,22 @@ __global__ __launch_bounds__(kWave) void port_event_schedule(const GmgView G, co
 // order and finish order agree under index-order dispatch).  kPorts: arrivals
 // come from the port reservations (arr, [edge][candidate]); a copy is
 // allocated at its transfer's start = arrival - estimate.
+// A running schedule's state in the GMG (index order, latency transfers):
+// transfers start no earlier than xfer_floor; with done ops, whose recorded
+// finishes need not follow index order, the last consumer is the one with the
+// latest (finish, index); every time is clipped to t_now, from which on the
+// peak is taken (t_now = 0 otherwise, where no time is negative).
 template <bool kWrite, bool kReady, bool kPorts, class KP, class VP>
 __device__ int op_events(const GmgView &G, const uint8_t *prow, const int64_t *frow, int y, int e, KP keys,
                          VP vals, int w, const int64_t *arr, int64_t nb, int64_t c) {
   const int C = G.n_class, K = G.n_link, D = G.n_dev;
+  const int64_t T0 = G.t_now;
   int n = 0;
   const int64_t fy = frow[y];
   const int64_t by = G.out_bytes[y];
   if (by > 0) {
     if (kWrite) {
-      keys[w] = 2 * (fy - G.dur[(int64_t)y * C + G.dev_class[e]]) + 1;
+      keys[w] = 2 * imax(fy - G.dur[(int64_t)y * C + G.dev_class[e]], T0) + 1;
       vals[w] = by;
     }
     ++n;
@@ -722,12 +759,18 @@ __device__ int op_events(const GmgView &G, const uint8_t *prow, const int64_t *f
         for (int q = x0; q < x1; ++q) {
           const int x = G.succ_idx[q];
           const int dx = prow[x];
-          const int64_t t = (dx == e)  ? frow[x]
-                            : kPorts ? arr[(int64_t)G.succ_pe[q] * nb + c]
-                                     : fy + G.xfer[(int64_t)y * K + G.link_class[e * D + dx]];
+          int64_t t;
+          if (dx == e) {
+            t = frow[x];
+          } else if (kPorts) {
+            t = arr[(int64_t)G.succ_pe[q] * nb + c];
+          } else {
+            t = G.issue_at ? imax(fy, xfer_floor(G, prow, y, dx)) : fy;
+            t += G.xfer[(int64_t)y * K + G.link_class[e * D + dx]];
+          }
           F = imax(F, t);
         }
-        keys[w + n] = 2 * F;
+        keys[w + n] = 2 * imax(F, T0);
         vals[w + n] = -by;
       }
       ++n;
@@ -741,7 +784,15 @@ __device__ int op_events(const GmgView &G, const uint8_t *prow, const int64_t *f
     if (bu == 0) continue;
     bool last = true;  // no consumer of u on e after y?
     const int s0 = G.succ_ptr[u];
-    if (kReady) {  // one op at a time on e: finishes there are distinct
+    if (!kReady && !kPorts && G.done_fin) {
+      for (int s = s0; s < G.succ_ptr[u + 1]; ++s) {
+        const int x = G.succ_idx[s];
+        if (x != y && prow[x] == e && (frow[x] > fy || (frow[x] == fy && x > y))) {
+          last = false;
+          break;
+        }
+      }
+    } else if (kReady) {  // one op at a time on e: finishes there are distinct
       for (int s = s0; s < G.succ_ptr[u + 1]; ++s) {
         const int x = G.succ_idx[s];
         if (prow[x] == e && frow[x] > fy) {
@@ -761,11 +812,14 @@ __device__ int op_events(const GmgView &G, const uint8_t *prow, const int64_t *f
     }
     if (!last) continue;
     if (kWrite) {
-      const int64_t t0 = kPorts ? arr[(int64_t)q * nb + c] - G.xfer[(int64_t)u * K + G.link_class[prow[u] * D + e]]
-                                : frow[u];
-      keys[w + n] = 2 * t0 + 1;
+      int64_t t0;
+      if (kPorts)
+        t0 = arr[(int64_t)q * nb + c] - G.xfer[(int64_t)u * K + G.link_class[prow[u] * D + e]];
+      else
+        t0 = G.issue_at ? imax(frow[u], xfer_floor(G, prow, u, e)) : frow[u];
+      keys[w + n] = 2 * imax(t0, T0) + 1;
       vals[w + n] = bu;
-      keys[w + n + 1] = 2 * fy;
+      keys[w + n + 1] = 2 * imax(fy, T0);
       vals[w + n + 1] = -bu;
     }
     n += 2;
@@ -1139,10 +1193,16 @@ static int run_simulate_generic(const ss_gmg *g, SsPlace src, int64_t *makespan,
 
 // Path choice: the 32-bit fast path when the loader enabled it and its LDS
 // state fits; SS_PATH=generic or SS_PATH=fast in the environment forces one
-// (fast is still refused when the GMG does not qualify).
+// (fast is still refused when the GMG does not qualify).  A GMG holding a
+// running schedule's state never qualifies: the loader keeps it off the 32-bit
+// tables, so it takes schedule_kernel and memory_kernel.
 int ss_run_simulate(const ss_gmg *g, SsPlace P, int64_t *makespan, int64_t *peak, uint8_t *violation,
                     int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch, bool link_ports,
                     SsWork &W) {
+  if (g->snapshot && (ready_dispatch || link_ports))
+    return ss_set_error(SS_ERR_UNSUPPORTED,
+                        "a running schedule's state (done_fin, issue_at, t_now) takes index-order dispatch and "
+                        "latency-only transfers");
   int lds_max = 0;
   hipError_t err = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");

@@ -22,6 +22,10 @@ struct GmgView {
   const int64_t *slice_begin, *slice_end;
   const int64_t *cap, *release, *deadline;
   const uint8_t *link_class;  // [D][D]
+  // a running schedule's state (null / 0 without one): recorded finish of
+  // done ops (-1: not done), issue times, the snapshot's timestamp
+  const int64_t *done_fin, *issue_at;
+  int64_t t_now;
   // 32-bit copies of every time quantity, present when the loader proved the
   // whole time horizon (all starts, finishes, frees and finite slice bounds)
   // stays below 2^32 - 1, there are at most 65535 ops, 65535 edges and 65535
@@ -86,6 +90,7 @@ struct ss_gmg {
   int64_t horizon = 0;     // loader's upper bound on every simulated time
   int64_t max_indeg = 0;   // largest predecessor count of any op
   int64_t max_outdeg = 0;  // largest successor count of any op
+  bool snapshot = false;   // done_fin, issue_at or t_now given (general index-order path only)
   void *dev_mem = nullptr;
   // second stream of the memory passes (the peak evaluation of one sub-chunk
   // overlaps the interval pass of the next): the device's (ss_device_aux)
@@ -168,9 +173,10 @@ void ss_timing_stop(SsTimingRec *rec, hipStream_t stream);
 // Incremental scheduling loop (sched.cpp).  Arguments are already checked.
 int ss_run_sched_create(const ss_sched_desc *d, ss_sched **out);
 void ss_run_sched_free(ss_sched *s);
-int ss_run_sched_round(ss_sched *s, int *status, int64_t *ops, int64_t *n_ops, int64_t *part, hipStream_t stream);
-int ss_run_sched_complete(ss_sched *s, int64_t op);
-void ss_run_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place);
+int ss_run_sched_round(ss_sched *s, int64_t now, int *status, int64_t *ops, int64_t *n_ops, int64_t *part,
+                       hipStream_t stream);
+int ss_run_sched_complete(ss_sched *s, int64_t op, int64_t t_done);
+void ss_run_sched_state(const ss_sched *s, uint8_t *state, uint8_t *place, int64_t *issue_t, int64_t *done_t);
 
 // Where a simulation call takes its scratch (device memory beyond its inputs
 // and outputs) from: the device's pool (ptr null), or a caller's workspace of

@@ -29,6 +29,7 @@ LINKS = {"latency": 0, "ports": SS_LINK_PORTS}
 SS_VIOLATION_MEMORY = 0x1
 SS_VIOLATION_INVALID = 0x4
 SS_SELECT_REQUIRE_SLA = 0x1
+SS_SCHED_NO_PREFIX_REUSE = 0x2
 EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "ss_select_best", "ss_kernel_timing",
             "ss_kernel_time", "ss_last_error", "ss_est_create", "ss_est_free", "ss_est_add", "ss_est_solve",
             "ss_est_predict", "ss_sched_create", "ss_sched_free", "ss_sched_round", "ss_sched_complete",
@@ -58,7 +59,8 @@ class _Desc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in ("n_ops", "n_edges", "n_dev", "n_class", "n_link", "n_req")] + \
                [(n, ctypes.c_void_p) for n in ("pred_ptr", "pred_idx", "op_req", "dur", "out_bytes", "dev_class",
                                                "link_class", "bw", "lat", "slice_ptr", "slice_begin", "slice_end",
-                                               "cap", "release", "deadline")]
+                                               "cap", "release", "deadline", "done_fin", "issue_at")] + \
+               [("t_now", ctypes.c_int64)]
 
 
 def lib():
@@ -107,11 +109,11 @@ def lib():
             L.ss_sched_create.restype = ctypes.c_int
             L.ss_sched_free.argtypes = [P]
             L.ss_sched_free.restype = None
-            L.ss_sched_round.argtypes = [P, P, P, P, P, P]
+            L.ss_sched_round.argtypes = [P, I64, P, P, P, P, P]
             L.ss_sched_round.restype = ctypes.c_int
-            L.ss_sched_complete.argtypes = [P, I64]
+            L.ss_sched_complete.argtypes = [P, I64, I64]
             L.ss_sched_complete.restype = ctypes.c_int
-            L.ss_sched_state.argtypes = [P, P, P]
+            L.ss_sched_state.argtypes = [P, P, P, P, P]
             L.ss_sched_state.restype = ctypes.c_int
             L.ss_state_create.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
             L.ss_state_create.restype = ctypes.c_int
@@ -152,12 +154,16 @@ def _gmg_desc(g, keep):
         keep[name] = a
         return a.ctypes.data
 
+    def opt(name):  # the running schedule's state: NULL when absent
+        return arr(name, np.int64) if getattr(g, name, None) is not None else None
+
     return _Desc(int(g.n_ops), int(g.pred_ptr[-1]), int(g.n_dev), int(g.n_class), int(g.n_link), int(g.n_req),
                  arr("pred_ptr", np.int32), arr("pred_idx", np.int32), arr("op_req", np.int32),
                  arr("dur", np.int64), arr("out_bytes", np.int64), arr("dev_class", np.int32),
                  arr("link_class", np.uint8), arr("bw", np.int64), arr("lat", np.int64),
                  arr("slice_ptr", np.int64), arr("slice_begin", np.int64), arr("slice_end", np.int64),
-                 arr("cap", np.int64), arr("release", np.int64), arr("deadline", np.int64))
+                 arr("cap", np.int64), arr("release", np.int64), arr("deadline", np.int64),
+                 opt("done_fin"), opt("issue_at"), int(getattr(g, "t_now", 0) or 0))
 
 
 class Gmg:
@@ -198,36 +204,39 @@ class Scheduler:
     """The incremental scheduling loop of Alg. 1 (ss_sched_*) over a run's GMG,
     its pre-defined partitions part_dev[n_part][n_ops] and request priorities."""
 
-    def __init__(self, g, part_dev, priority, budget, cap, require_sla=False):
+    def __init__(self, g, part_dev, priority, budget, cap, require_sla=False, prefix_reuse=True):
         keep = {}
         desc = _gmg_desc(g, keep)
         part = np.ascontiguousarray(part_dev, np.uint8)
         prio = np.ascontiguousarray(priority, np.int64)
         assert part.ndim == 2 and part.shape[1] == g.n_ops and prio.shape == (g.n_req,)
+        flags = (SS_SELECT_REQUIRE_SLA if require_sla else 0) | (0 if prefix_reuse else SS_SCHED_NO_PREFIX_REUSE)
         d = _SchedDesc(ctypes.pointer(desc), part.shape[0], part.ctypes.data, prio.ctypes.data, int(budget),
-                       int(cap), SS_SELECT_REQUIRE_SLA if require_sla else 0)
+                       int(cap), flags)
         h = ctypes.c_void_p()
         _check(lib().ss_sched_create(ctypes.byref(d), ctypes.byref(h)))
         self.handle = h
         self.n_ops, self.cap = int(g.n_ops), int(cap)
         self._ops = np.zeros(max(1, int(cap)), np.int64)
 
-    def round(self, stream=None):
-        """(status, batch ops, partition or -1)."""
+    def round(self, now, stream=None):
+        """One round at time `now`: (status, batch ops, partition or -1)."""
         st, n, p = ctypes.c_int(), ctypes.c_int64(), ctypes.c_int64()
-        _check(lib().ss_sched_round(self.handle, ctypes.byref(st), self._ops.ctypes.data, ctypes.byref(n),
-                                    ctypes.byref(p), _stream_ptr(stream)))
+        _check(lib().ss_sched_round(self.handle, int(now), ctypes.byref(st), self._ops.ctypes.data,
+                                    ctypes.byref(n), ctypes.byref(p), _stream_ptr(stream)))
         return st.value, self._ops[:n.value].tolist(), p.value
 
-    def complete(self, op):
-        _check(lib().ss_sched_complete(self.handle, int(op)))
+    def complete(self, op, t_done):
+        _check(lib().ss_sched_complete(self.handle, int(op), int(t_done)))
 
     def state(self):
-        """(state[n_ops] of SS_OP_*, place[n_ops])."""
+        """(state[n_ops] of SS_OP_*, place[n_ops], issue time[n_ops], completion time[n_ops])."""
         st = np.zeros(self.n_ops, np.uint8)
         pl = np.zeros(self.n_ops, np.uint8)
-        _check(lib().ss_sched_state(self.handle, st.ctypes.data, pl.ctypes.data))
-        return st, pl
+        it = np.zeros(self.n_ops, np.int64)
+        dt = np.zeros(self.n_ops, np.int64)
+        _check(lib().ss_sched_state(self.handle, st.ctypes.data, pl.ctypes.data, it.ctypes.data, dt.ctypes.data))
+        return st, pl, it, dt
 
     def free(self):
         if self.handle:

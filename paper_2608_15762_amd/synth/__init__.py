@@ -31,7 +31,9 @@ Units: times are int64 microseconds, sizes int64 bytes.
 """
 from __future__ import annotations
 
+import copy
 import ctypes
+import heapq
 import math
 import os
 import subprocess
@@ -273,9 +275,10 @@ class Gmg:
     tenant_of: np.ndarray | None = None
     name: str = ""
     # a snapshot of a running schedule (optional): recorded completion time of
-    # each done op (-1: not done), issue time of each op
+    # each done op (-1: not done), issue time of each op, the snapshot's time
     done_fin: np.ndarray | None = None   # int64 [N]
     issue_at: np.ndarray | None = None   # int64 [N]
+    t_now: int = 0
 
     @property
     def n_edges(self) -> int:
@@ -498,14 +501,79 @@ def partition_table(g: Gmg, cid: int) -> np.ndarray:
     return out
 
 
-def completion_feedback(issued, key: int, step: int) -> list:
-    """Executor feedback for a driver of the incremental loop: a seeded random
-    half (at least one) of the issued ops complete.  Returns those ops,
-    ascending."""
-    issued = sorted(int(v) for v in issued)
-    st = Stream(draw(key, 0x5C4ED + step))
-    order = sorted(issued, key=lambda v: (st.next(), v))
-    return sorted(order[:max(1, len(issued) // 2)])
+def random_snapshot(g: Gmg, seed: int, done_p: float = 0.5, issue_span: int = 400, t_now: int | None = None,
+                    issue: bool = True) -> Gmg:
+    """A copy of g holding a random state of a running schedule: every op an
+    issue time in [0, issue_span] (or none with issue=False); ops done with
+    probability done_p when all their predecessors are done, finishing 1-60 us
+    after the later of their issue and their predecessors' finishes; the
+    snapshot's timestamp t_now (default: drawn up to the latest finish)."""
+    st = Stream(draw(0x5A9 + seed, 2))
+    N = g.n_ops
+    iss = np.array([st.uniform_int(0, issue_span) for _ in range(N)], np.int64)
+    done = np.full(N, -1, np.int64)
+    for v in range(N):
+        preds = g.pred_idx[g.pred_ptr[v]:g.pred_ptr[v + 1]]
+        if st.unit() < done_p and all(done[u] >= 0 for u in preds):
+            t = max([int(iss[v]) if issue else 0] + [int(done[u]) for u in preds])
+            done[v] = t + st.uniform_int(1, 60)
+    h = copy.deepcopy(g)
+    h.done_fin = done
+    h.issue_at = iss if issue else None
+    h.t_now = int(st.uniform_int(0, int(max(done.max(), 0)) + 1)) if t_now is None else int(t_now)
+    return h
+
+
+class Executor:
+    """Stand-in for the cluster that runs what the incremental loop issues
+    (Sec. 3.5), reporting completions with their times.  An issued op runs
+    once its predecessors have completed: it completes at the later of its
+    issue time and its predecessors' completions, plus its duration estimate
+    on its device's class scaled by a seeded factor in [0.75, 1.25] (at least
+    1 us).  Completions come out in time order, ties to the lower op."""
+
+    def __init__(self, g: Gmg, key: int):
+        self.g = g
+        self.key = key
+        N = g.n_ops
+        self.issue_t = np.full(N, -1, np.int64)
+        self.dev = np.zeros(N, np.int64)
+        self.done_t = np.full(N, -1, np.int64)
+        self.waiting = np.zeros(N, np.int64)  # predecessors not yet completed
+        self.succ = [[] for _ in range(N)]
+        for v in range(N):
+            for u in g.pred_idx[g.pred_ptr[v]:g.pred_ptr[v + 1]]:
+                self.succ[int(u)].append(v)
+            self.waiting[v] = g.pred_ptr[v + 1] - g.pred_ptr[v]
+        self.events = []  # heap of (completion time, op)
+
+    def _start(self, v):
+        g = self.g
+        preds = g.pred_idx[g.pred_ptr[v]:g.pred_ptr[v + 1]]
+        t = max([int(self.issue_t[v])] + [int(self.done_t[u]) for u in preds])
+        w = int(g.dur[v, g.dev_class[self.dev[v]]])
+        f = Stream(draw(self.key, 0xE7EC + v)).unit()
+        heapq.heappush(self.events, (t + max(1, int(round(w * (0.75 + 0.5 * f)))), v))
+
+    def issue(self, ops, devs, t: int):
+        for v, d in zip(ops, devs):
+            v = int(v)
+            self.issue_t[v] = t
+            self.dev[v] = int(d)
+            if self.waiting[v] == 0:
+                self._start(v)
+
+    def next_completion(self):
+        """(time, op) of the next completion, or None when nothing runs."""
+        if not self.events:
+            return None
+        t, v = heapq.heappop(self.events)
+        self.done_t[v] = t
+        for x in self.succ[v]:
+            self.waiting[x] -= 1
+            if self.waiting[x] == 0 and self.issue_t[x] >= 0:
+                self._start(x)
+        return t, v
 
 
 def request_priority(g: Gmg) -> np.ndarray:

@@ -99,6 +99,36 @@ def test_loader_rejects_malformed_snapshot(name):
     assert load_rc(g) == -2, name
 
 
+def snap(done=(-1, -1, -1), issue=(0, 0, 0), t_now=0):
+    g = good()
+    g.done_fin = np.asarray(done, np.int64)
+    g.issue_at = None if issue is None else np.asarray(issue, np.int64)
+    g.t_now = t_now
+    return g
+
+
+def test_valid_running_schedule_passes_validation():
+    for g in (snap(), snap((10, 20, -1), (0, 5, 30), 25), snap((10, -1, -1), None, 7)):
+        assert load_rc(g) in (0, -4)
+
+
+BAD_SNAPSHOTS = {
+    "done_pred_not_done": snap((-1, 20, -1)),
+    "done_before_pred": snap((20, 20, -1)),
+    "done_at_issue": snap((10, -1, -1), (10, 0, 0)),
+    "done_below_minus_one": snap((-2, -1, -1)),
+    "negative_issue": snap(issue=(0, -1, 0)),
+    "negative_t_now": snap(t_now=-1),
+    "huge_done": snap((1 << 62, -1, -1)),
+    "huge_issue": snap(issue=(0, 1 << 62, 0)),
+}
+
+
+@pytest.mark.parametrize("name", sorted(BAD_SNAPSHOTS))
+def test_loader_rejects_malformed_running_schedule(name):
+    assert load_rc(BAD_SNAPSHOTS[name]) == -2, name
+
+
 def test_loader_rejects_too_many_devices():
     g = synth.random_gmg(0, n_ops=4, n_dev=3)
     g.n_dev = 256
@@ -126,6 +156,7 @@ def test_binding_constants_match_the_header():
     assert c["SS_LINK_PORTS"] & (c["SS_DISPATCH_READY"] | c["SS_LAYOUT_ROW_MAJOR"]) == 0
     assert c["SS_VIOLATION_MEMORY"] == ss.SS_VIOLATION_MEMORY and c["SS_VIOLATION_INVALID"] == ss.SS_VIOLATION_INVALID
     assert c["SS_SELECT_REQUIRE_SLA"] == ss.SS_SELECT_REQUIRE_SLA
+    assert c["SS_SCHED_NO_PREFIX_REUSE"] == ss.SS_SCHED_NO_PREFIX_REUSE
     for code, name in ss.ERRORS.items():
         assert c[name] == code
 
@@ -183,13 +214,18 @@ def test_scheduler_arguments_are_checked_before_the_device():
     part = synth.partition_table(g, 0)
     prio = synth.request_priority(g)
     for n_part, budget, cap, flags, bad_dev in [(0, 4, 4, 0, False), (3, 0, 4, 0, False), (3, 4, 0, 0, False),
-                                                (3, 4, 4, 2, False), (3, 4, 4, 0, True)]:
+                                                (3, 4, 4, 4, False), (3, 4, 4, 0, True)]:
         pd = part.copy()
         if bad_dev:
             pd[1, 5] = g.n_dev
         d = ss._SchedDesc(ctypes.pointer(desc), n_part, pd.ctypes.data, prio.ctypes.data, budget, cap, flags)
         assert L.ss_sched_create(ctypes.byref(d), ctypes.byref(h)) == -1
-    assert L.ss_sched_round(None, None, None, None, None, None) == -1
-    assert L.ss_sched_complete(None, 0) == -1
-    assert L.ss_sched_state(None, None, None) == -1
+    g.done_fin = np.full(g.n_ops, -1, np.int64)  # the run's GMG holds no running state
+    desc2 = ss._gmg_desc(g, keep)
+    d = ss._SchedDesc(ctypes.pointer(desc2), 3, part.ctypes.data, prio.ctypes.data, 4, 4, 0)
+    assert L.ss_sched_create(ctypes.byref(d), ctypes.byref(h)) == -1
+    assert b"running state" in L.ss_last_error()
+    assert L.ss_sched_round(None, 0, None, None, None, None, None) == -1
+    assert L.ss_sched_complete(None, 0, 1) == -1
+    assert L.ss_sched_state(None, None, None, None, None) == -1
     L.ss_sched_free(None)

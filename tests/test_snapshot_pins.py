@@ -149,3 +149,48 @@ def test_later_issue_never_finishes_earlier(gi):
         iss2[rng.integers(0, g.n_ops)] += int(rng.integers(1, 5000))
         hi = oracle.simulate_one(with_snapshot(g, issue=iss2), p)
         assert (hi["fin"] >= lo["fin"]).all()
+
+
+def test_peak_counts_memory_from_the_snapshot_time():
+    # d0 only.  op0 done at 10 (estimate 10, 7 B), read by op1 done at 20 (3 B,
+    # no consumer: kept); op2 issued at 50 (4 B).  Residencies: op0 [0, 20),
+    # op1 [10, inf), op2 [50, inf).  From t = 0 the peak is 7 + 3 = 10 (at 10);
+    # from t_now = 30, op0 is gone and the peak is 3 + 4 = 7 (at 50).
+    g = make_gmg(1, ["op"] * 3, [(0, 1)], [0] * 3, [[10], [10], [5]], [7, 3, 4], [[(0, TIME_INF)]], [100], [0],
+                 [500])
+    s = with_snapshot(g, done=[10, 20, -1], issue=[0, 0, 50])
+    p = np.zeros(3, np.uint8)
+    assert oracle.simulate_one(s, p)["peak"].tolist() == [10]
+    s.t_now = 30
+    out = oracle.simulate_one(s, p)
+    assert out["peak"].tolist() == [7] and out["fin"].tolist() == [10, 20, 55]
+    s.t_now = 10  # op0 still held at 10 (half-open [0, 20)): 10 again
+    assert oracle.simulate_one(s, p)["peak"].tolist() == [10]
+    s.t_now = 20  # op0 freed at 20 before anything else counts: 3, then 7 at 50
+    assert oracle.simulate_one(s, p)["peak"].tolist() == [7]
+
+
+@pytest.mark.parametrize("gi", range(len(GRAPHS)))
+def test_snapshot_time_clips_only_the_peak(gi):
+    """The snapshot time changes no schedule; the peak does not grow with it;
+    beyond every finite residency end what remains is the outputs without
+    consumers, on their devices."""
+    g = random_gmg(1000 + gi, **GRAPHS[gi])
+    rng = np.random.default_rng(70 + gi)
+    has_succ = np.zeros(g.n_ops, bool)
+    has_succ[g.pred_idx] = True
+    for b in range(8):
+        p = rng.integers(0, g.n_dev, g.n_ops).astype(np.uint8)
+        base = oracle.simulate_one(g, p)
+        prev = base["peak"]
+        for t in sorted(rng.integers(0, int(base["makespan"]) + 1, 4).tolist()) + [1 << 40]:
+            h = copy.deepcopy(g)
+            h.t_now = t
+            out = oracle.simulate_one(h, p)
+            for f in ("st", "fin", "makespan", "slack", "sumfin"):
+                assert np.array_equal(np.asarray(out[f]), np.asarray(base[f])), f
+            assert (out["peak"] <= prev).all()
+            prev = out["peak"]
+        kept = np.zeros(g.n_dev, np.int64)
+        np.add.at(kept, p[~has_succ], g.out_bytes[~has_succ])
+        assert prev.tolist() == kept.tolist()
