@@ -24,8 +24,8 @@ if ROOT not in sys.path:
 METRIC = "candidate placements simulated/sec (+ op-evals/sec, % HBM roofline), 1 GPU"
 HBM_PEAK_GBS = 8000.0
 COPY_BYTES = 1 << 31  # device-to-device copy: achievable bandwidth, and the counter calibration kernel
-# Measured HBM traffic of the kernels (rocprofv3 FETCH_SIZE / WRITE_SIZE, scaled by
-# the copy kernel's readings), valid while the kernel sources hash as recorded there.
+# Measured HBM traffic of the kernels (rocprofv3 read requests by size and
+# WRITE_SIZE), valid while the kernel sources hash as recorded there.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_16tenant-50kop-128dev.md")
 KERNEL_SOURCES = ("paper_2608_15762_amd/csrc/sim_fast.hip", "paper_2608_15762_amd/csrc/gmg_load.cpp")
 
@@ -51,8 +51,9 @@ def parse():
                          "host-to-device copy and simulation overlapped; reported beside value, not as it)")
     ap.add_argument("--batch-cap", type=int, default=400, help="incremental loop: ops per batch")
     ap.add_argument("--budget", type=int, default=1600, help="incremental loop: issued-op budget")
-    ap.add_argument("--no-prefix-reuse", action="store_true",
-                    help="incremental loop: simulate every round's whole graph (no resume from the last capture)")
+    ap.add_argument("--prefix-reuse", action="store_true",
+                    help="incremental loop: resume candidates from the last issuing round's capture while no "
+                         "completion came in between")
     return ap.parse_args()
 
 
@@ -380,21 +381,19 @@ def sched_run(S, g, synth, key, record=None, max_rounds=None, osch=None, deadlin
     X = synth.Executor(g, key)
     rounds = issued_rounds = 0
     now = 0
-    succ_open = None
     if record is not None:
-        preds = [g.pred_idx[g.pred_ptr[v]:g.pred_ptr[v + 1]] for v in range(g.n_ops)]
+        dst = np.repeat(np.arange(g.n_ops), np.diff(g.pred_ptr))  # consumer of each edge
     while (max_rounds is None or rounds < max_rounds) and (deadline is None or time.perf_counter() < deadline):
-        if record is not None:
-            state = S.state()[0] if osch is None else S.state
-            done = state == 2
-            succ_open = np.zeros(g.n_ops, bool)
-            for v in np.nonzero(~done)[0]:
-                succ_open[preds[v]] = True
-            graph = int((state == 1).sum() + (done & succ_open).sum())
         st, batch, p = S.round(now)
         rounds += 1
         if record is not None:
-            record.append((st, tuple(batch), p, graph + len(batch)))
+            graph = 0
+            if st in (0, 3):  # the snapshot's ops: issued, and done ones feeding an op not done
+                state = S.state()[0] if osch is None else S.state
+                done = state == 2
+                open_ = np.bincount(g.pred_idx, weights=~done[dst], minlength=g.n_ops) > 0
+                graph = int((state == 1).sum() + (done & open_).sum()) + (len(batch) if st == 3 else 0)
+            record.append((st, tuple(batch), p, graph))
         if st == 0:
             issued_rounds += 1
             X.issue(batch, (S.state()[1] if osch is None else S.place)[batch], now)
@@ -424,7 +423,7 @@ def sched_main(args):
     log(f"incremental loop on {cfg.name}: N={g.n_ops} partitions={len(part)} cap={args.batch_cap} "
         f"budget={args.budget}")
     copy_gbs = copy_bandwidth(torch, dev)
-    reuse = not args.no_prefix_reuse
+    reuse = args.prefix_reuse
     gpu_rec = []
     for i in range(args.warmup):
         S = ss.Scheduler(g, part, prio, args.budget, args.batch_cap, prefix_reuse=reuse)

@@ -418,10 +418,15 @@ int ss_est_predict(const double *coef, int64_t n_est, int64_t n_feat, const int3
  *   issue_budget   Alg. 1's budget on issued (not yet done) ops, >= 1.
  *   batch_cap      the batch cap of CollectConnectedGraph, >= 1.
  *   flags          SS_SELECT_REQUIRE_SLA (feasibility also requires every
- *                  request's slack >= 0) and SS_SCHED_NO_PREFIX_REUSE (every
- *                  round simulates its whole graph; for measurement), or 0.
+ *                  request's slack >= 0) and SS_SCHED_PREFIX_REUSE (each
+ *                  issuing round captures the chosen candidate's state, and
+ *                  the next round resumes every candidate from it when no
+ *                  completion came in between; same decisions, and slower
+ *                  on the measured workloads: the candidates of a round run
+ *                  in parallel lanes, so the capture's extra serial walk
+ *                  costs more than the walk it saves), or 0.
  */
-#define SS_SCHED_NO_PREFIX_REUSE 0x2
+#define SS_SCHED_PREFIX_REUSE 0x2
 #define SS_OP_UNSCHEDULED 0
 #define SS_OP_ISSUED 1
 #define SS_OP_DONE 2

@@ -292,7 +292,7 @@ extern "C" int ss_sched_create(const ss_sched_desc *d, ss_sched **out) {
   if (d->gmg->n_req > 0 && !d->priority) return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: priority is NULL");
   if (d->issue_budget < 1 || d->batch_cap < 1)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: issue_budget and batch_cap must be >= 1");
-  if (d->flags & ~(SS_SELECT_REQUIRE_SLA | SS_SCHED_NO_PREFIX_REUSE))
+  if (d->flags & ~(SS_SELECT_REQUIRE_SLA | SS_SCHED_PREFIX_REUSE))
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: unknown flags");
   if (d->gmg->done_fin || d->gmg->issue_at || d->gmg->t_now != 0)
     return ss_set_error(SS_ERR_INVALID_ARG, "ss_sched_create: the run's GMG holds no running state (the scheduler "

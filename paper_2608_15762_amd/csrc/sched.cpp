@@ -21,10 +21,12 @@
 // left to run is out of every later snapshot, so the graph is bounded by the
 // issue budget, the checkpoints and one batch.
 //
-// Prefix reuse: the chosen candidate's state after its round's graph is
-// captured; while no completion arrives, the next round's graph is that graph
-// followed by a new batch (the batch just issued joins the issued ops, the
-// done ops still in play stay), so every candidate resumes after it.
+// Prefix reuse (SS_SCHED_PREFIX_REUSE): the chosen candidate's state after
+// its round's graph is captured; while no completion arrives, the next
+// round's graph is that graph followed by a new batch (the batch just issued
+// joins the issued ops, the done ops still in play stay), so every candidate
+// resumes after it.  Off by default: the candidates run in parallel lanes, so
+// the capture's serial walk costs more than the walk each lane saves.
 #include <algorithm>
 #include <new>
 #include <queue>
@@ -62,7 +64,7 @@ struct ss_sched {
   // prefix of the next round), and a second state to capture the next one in
   ss_state *prefix = nullptr, *next = nullptr;
   bool prefix_ok = false;  // no completion since prefix was captured
-  bool reuse = true;       // prefix reuse enabled
+  bool reuse = false;      // prefix reuse enabled (SS_SCHED_PREFIX_REUSE)
 
 };
 
@@ -161,7 +163,7 @@ int ss_run_sched_create(const ss_sched_desc *d, ss_sched **out) {
     s->issue_t.assign((size_t)s->N, -1);
     s->done_t.assign((size_t)s->N, -1);
     s->open_succ.assign((size_t)s->N, 0);
-    s->reuse = !(d->flags & SS_SCHED_NO_PREFIX_REUSE);
+    s->reuse = (d->flags & SS_SCHED_PREFIX_REUSE) != 0;
     s->missing.assign((size_t)s->N, 0);
     s->succ_ptr.assign((size_t)s->N + 1, 0);
     s->succ_idx.assign((size_t)s->E, 0);

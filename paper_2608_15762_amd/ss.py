@@ -29,7 +29,7 @@ LINKS = {"latency": 0, "ports": SS_LINK_PORTS}
 SS_VIOLATION_MEMORY = 0x1
 SS_VIOLATION_INVALID = 0x4
 SS_SELECT_REQUIRE_SLA = 0x1
-SS_SCHED_NO_PREFIX_REUSE = 0x2
+SS_SCHED_PREFIX_REUSE = 0x2
 EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "ss_select_best", "ss_kernel_timing",
             "ss_kernel_time", "ss_last_error", "ss_est_create", "ss_est_free", "ss_est_add", "ss_est_solve",
             "ss_est_predict", "ss_sched_create", "ss_sched_free", "ss_sched_round", "ss_sched_complete",
@@ -204,13 +204,13 @@ class Scheduler:
     """The incremental scheduling loop of Alg. 1 (ss_sched_*) over a run's GMG,
     its pre-defined partitions part_dev[n_part][n_ops] and request priorities."""
 
-    def __init__(self, g, part_dev, priority, budget, cap, require_sla=False, prefix_reuse=True):
+    def __init__(self, g, part_dev, priority, budget, cap, require_sla=False, prefix_reuse=False):
         keep = {}
         desc = _gmg_desc(g, keep)
         part = np.ascontiguousarray(part_dev, np.uint8)
         prio = np.ascontiguousarray(priority, np.int64)
         assert part.ndim == 2 and part.shape[1] == g.n_ops and prio.shape == (g.n_req,)
-        flags = (SS_SELECT_REQUIRE_SLA if require_sla else 0) | (0 if prefix_reuse else SS_SCHED_NO_PREFIX_REUSE)
+        flags = (SS_SELECT_REQUIRE_SLA if require_sla else 0) | (SS_SCHED_PREFIX_REUSE if prefix_reuse else 0)
         d = _SchedDesc(ctypes.pointer(desc), part.shape[0], part.ctypes.data, prio.ctypes.data, int(budget),
                        int(cap), flags)
         h = ctypes.c_void_p()

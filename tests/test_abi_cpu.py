@@ -156,7 +156,7 @@ def test_binding_constants_match_the_header():
     assert c["SS_LINK_PORTS"] & (c["SS_DISPATCH_READY"] | c["SS_LAYOUT_ROW_MAJOR"]) == 0
     assert c["SS_VIOLATION_MEMORY"] == ss.SS_VIOLATION_MEMORY and c["SS_VIOLATION_INVALID"] == ss.SS_VIOLATION_INVALID
     assert c["SS_SELECT_REQUIRE_SLA"] == ss.SS_SELECT_REQUIRE_SLA
-    assert c["SS_SCHED_NO_PREFIX_REUSE"] == ss.SS_SCHED_NO_PREFIX_REUSE
+    assert c["SS_SCHED_PREFIX_REUSE"] == ss.SS_SCHED_PREFIX_REUSE
     for code, name in ss.ERRORS.items():
         assert c[name] == code
 

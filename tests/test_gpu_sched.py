@@ -24,7 +24,7 @@ def dev():
     return torch.device("cuda:0")
 
 
-def drive_both(g, part, prio, budget, cap, key, require_sla=False, max_rounds=10_000, prefix_reuse=True):
+def drive_both(g, part, prio, budget, cap, key, require_sla=False, max_rounds=10_000, prefix_reuse=False):
     """Drive the library and the oracle through the same run, fed by the
     stand-in executor (completions with times), comparing every round."""
     O = osch.Scheduler(g, part, prio, budget, cap, require_sla)
@@ -55,11 +55,13 @@ def drive_both(g, part, prio, budget, cap, key, require_sla=False, max_rounds=10
         L.free()
 
 
-@pytest.mark.parametrize("cid,budget,cap", [(0, 8, 5), (1, 64, 40), (2, 600, 150), (2, 300, 400)])
-def test_workload_runs_match_the_oracle(dev, cid, budget, cap):
-    print(f"incremental loop, workload {cid}, budget {budget}, cap {cap}", flush=True)
+@pytest.mark.parametrize("cid,budget,cap,reuse", [(0, 8, 5, False), (1, 64, 40, True), (2, 600, 150, False),
+                                                  (2, 300, 400, True)])
+def test_workload_runs_match_the_oracle(dev, cid, budget, cap, reuse):
+    print(f"incremental loop, workload {cid}, budget {budget}, cap {cap}, prefix reuse {reuse}", flush=True)
     g = synth.build_gmg(cid)
-    rounds = drive_both(g, synth.partition_table(g, cid), synth.request_priority(g), budget, cap, key=cid)
+    rounds = drive_both(g, synth.partition_table(g, cid), synth.request_priority(g), budget, cap, key=cid,
+                        prefix_reuse=reuse)
     assert rounds > 2
 
 
@@ -70,7 +72,8 @@ def test_random_runs_match_the_oracle(dev, seed):
     rng = np.random.default_rng(seed)
     part = rng.integers(0, g.n_dev, (1 + 3 * seed, g.n_ops)).astype(np.uint8)
     prio = rng.integers(0, 4, g.n_req)
-    drive_both(g, part, prio, budget=5 + 3 * seed, cap=1 + 4 * seed, key=seed, require_sla=(seed % 2 == 1))
+    drive_both(g, part, prio, budget=5 + 3 * seed, cap=1 + 4 * seed, key=seed, require_sla=(seed % 2 == 1),
+               prefix_reuse=(seed % 3 == 0))
 
 
 def test_prefix_reuse_changes_no_decision(dev):
