@@ -53,7 +53,8 @@ def _get():
     global _lib
     with _lock:
         if _lib is None:
-            lib = ctypes.CDLL(build())
+            # SS_ORACLE_LIB: another build of the same source (the sanitizer run)
+            lib = ctypes.CDLL(os.environ.get("SS_ORACLE_LIB") or build())
             lib.sso_simulate_one.argtypes = [ctypes.POINTER(_Gmg), _P, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P]
             lib.sso_simulate_batch.argtypes = [ctypes.POINTER(_Gmg), _P, _I64, ctypes.c_int, _P, _P, _P, _P, _P]
             lib.sso_peak_sweep.argtypes = [ctypes.POINTER(_Gmg), _P, _P, _P, _P]

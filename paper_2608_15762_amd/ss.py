@@ -68,9 +68,11 @@ def lib():
     global _lib
     with _lock:
         if _lib is None:
-            if not os.path.exists(LIB_PATH):
-                raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2608_15762_amd/build.py")
-            L = ctypes.CDLL(LIB_PATH)
+            # SS_LIBRARY: another build of the same sources (the host sanitizer run)
+            path = os.environ.get("SS_LIBRARY") or LIB_PATH
+            if not os.path.exists(path):
+                raise RuntimeError(f"{path} is missing: build it with paper_2608_15762_amd/build.py")
+            L = ctypes.CDLL(path)
             P, I64 = ctypes.c_void_p, ctypes.c_int64
             L.ss_gmg_load.argtypes = [ctypes.POINTER(_Desc), ctypes.POINTER(ctypes.c_void_p)]
             L.ss_gmg_load.restype = ctypes.c_int

@@ -601,7 +601,8 @@ def _get_lib():
     global _lib
     with _lib_lock:
         if _lib is None:
-            lib = ctypes.CDLL(build_lib())
+            # SS_SYNTH_LIB: another build of the same source (the sanitizer run)
+            lib = ctypes.CDLL(os.environ.get("SS_SYNTH_LIB") or build_lib())
             lib.synth_placements.restype = ctypes.c_int
             lib.synth_placements.argtypes = [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                              ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
