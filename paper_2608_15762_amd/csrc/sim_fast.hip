@@ -47,6 +47,8 @@
 //                 ranks and fast_peaks as above.
 #include <atomic>
 #include <climits>
+#include <cstdlib>
+#include <cstring>
 
 #include "ss_internal.h"
 
@@ -482,10 +484,12 @@ __global__ __launch_bounds__(kWave) void ready_schedule(const GmgView G, const u
                                                         uint32_t *__restrict__ fin, uint16_t *__restrict__ rank,
                                                         uint16_t *__restrict__ missing, uint64_t *__restrict__ spill,
                                                         int64_t *__restrict__ makespan, int64_t *__restrict__ sumfin,
-                                                        int64_t *__restrict__ slack, uint8_t *__restrict__ violation) {
+                                                        int64_t *__restrict__ slack, uint8_t *__restrict__ violation,
+                                                        const uint32_t *__restrict__ only) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = G.n_class;
   const int lane = threadIdx.x;
+  if (only && only[blockIdx.x] == 0) return;  // candidates the lane kernel has already placed
   uint32_t *clk = reinterpret_cast<uint32_t *>(lds_raw);  // [D]
   uint32_t *comp = clk + D;                               // [R]
   uint32_t *cnt = comp + R;                               // [D] ops dispatched per device
@@ -655,6 +659,224 @@ __global__ __launch_bounds__(kWave) void ready_schedule(const GmgView G, const u
 }
 
 size_t ready_schedule_lds(int D, int R) { return (size_t)(3 * D + R + 1 + D) * 4; }
+
+// The same rule with one lane per candidate (64 candidates per wave): the
+// ready set is a lane's own, kLaneSlots keys in registers; device clocks in
+// LDS [device][lane]; ranks per device and request completions in global
+// scratch [device or request][candidate]; finish times and ranks in the
+// candidate rows the memory pass reads.  An op is ready when none of its
+// predecessors' finish times is still unset (the rows start cleared), so no
+// per-op counters are kept.  A candidate whose ready set outgrows the slots
+// is flagged (ovf) and handed to ready_schedule, which redoes it whole; a
+// placement naming a device >= D is walked on device 0 and reported invalid.
+constexpr int kLaneSlots = 32;
+constexpr uint32_t kFinUnset = 0xFFFFFFFFu;  // above every finish (the horizon is below 2^32 - 1)
+
+// kPacked (0, 2 or 4): with at most two successors per op (succ2) and at most
+// kPacked predecessors, an op's successors and their predecessors, requests
+// and releases come from the packed per-op fields, all loaded unconditionally
+// (indices clamped, results discarded when unused) so that a step waits for
+// three levels of dependent loads; 0 walks the CSR lists.
+template <int kPacked>
+__global__ __launch_bounds__(kWave) void ready_lanes(const GmgView G, const uint8_t *__restrict__ P, int64_t nb,
+                                                     uint32_t *__restrict__ fin, uint16_t *__restrict__ rank,
+                                                     uint16_t *__restrict__ cnt, uint32_t *__restrict__ comp,
+                                                     uint32_t *__restrict__ ovf, int64_t *__restrict__ makespan,
+                                                     int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
+                                                     uint8_t *__restrict__ violation) {
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  uint32_t *clk = reinterpret_cast<uint32_t *>(lds_raw);  // [D][64]
+  const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = G.n_class;
+  const int lane = threadIdx.x;
+  const int64_t c0 = (int64_t)blockIdx.x * kWave, c = c0 + lane;
+  const int rows = (int)min<int64_t>(kWave, nb - c0);
+  for (int r = 0; r < rows; ++r) {  // the wave clears its candidates' finish rows, coalesced
+    uint32_t *fr = fin + (c0 + r) * N;
+    for (int v = lane; v < N; v += kWave) fr[v] = kFinUnset;
+  }
+  for (int d = 0; d < D; ++d) clk[d * kWave + lane] = 0;
+  const bool act = c < nb;
+  if (act) {
+    for (int d = 0; d < D; ++d) cnt[(int64_t)d * nb + c] = 0;
+    for (int r = 0; r < R; ++r) comp[(int64_t)r * nb + c] = G.release32[r];
+  }
+  __syncthreads();  // every row cleared before a lane reads its own
+  if (!act) return;
+  const uint8_t *prow = P + c * N;
+  uint32_t *frow = fin + c * N;
+  uint16_t *rrow = rank + c * N;
+  const int64_t ms_ = G.meta_stride;
+  const uint32_t *m_req = G.op_meta + kMetaReq * ms_, *m_rel = G.op_meta + kMetaRel * ms_,
+                 *m_p01 = G.op_meta + kMetaP01 * ms_, *m_p23 = G.op_meta + kMetaP23 * ms_;
+  constexpr uint64_t kNone = ~0ull;
+  uint64_t slot[kLaneSlots];
+#pragma unroll
+  for (int k = 0; k < kLaneSlots; ++k) slot[k] = kNone;
+  int sp = 0;
+  uint64_t sk = G.n_src > 0 ? G.src_keys[0] : kNone;  // the next source's key, loaded a step ahead
+  bool bad = false, over = false;
+  uint32_t ms = 0;
+  uint64_t sum = 0;
+  // a ready key for successor x of v (finish f) when none of x's
+  // predecessors is unset, else kNone
+  auto ready_key = [&](int x, int v, uint32_t f, int dx, uint32_t rel, int np, const int *pu) -> uint64_t {
+    uint32_t rx = rel;
+    bool ok = true;
+#pragma unroll
+    for (int i = 0; i < (kPacked ? kPacked : 1); ++i) {
+      const bool use = i < np;
+      const int u = use ? pu[i] : v;  // loads from a valid op either way
+      uint32_t t = u == v ? f : frow[u];
+      int du = prow[u];
+      if (du >= D) du = 0;
+      if (du != dx) t += xfer_of(G, u, du, dx);
+      ok &= !use || frow[u] != kFinUnset || u == v;
+      if (use) rx = umax32(rx, t);
+    }
+    return ok ? ((uint64_t)rx << 16 | (uint64_t)x) : kNone;
+  };
+  auto insert = [&](uint64_t nk) {
+    bool placed = false;
+#pragma unroll
+    for (int k = 0; k < kLaneSlots; ++k)
+      if (!placed && slot[k] == kNone) {
+        slot[k] = nk;
+        placed = true;
+      }
+    over |= !placed;
+  };
+  for (int step = 0; step < N && !over; ++step) {
+    uint64_t my = slot[0];
+#pragma unroll
+    for (int k = 1; k < kLaneSlots; ++k) my = slot[k] < my ? slot[k] : my;
+    uint64_t key;
+    if (sk < my) {
+      key = sk;
+      ++sp;
+      sk = sp < G.n_src ? G.src_keys[sp] : kNone;
+    } else {
+      key = my;
+      bool done = false;
+#pragma unroll
+      for (int k = 0; k < kLaneSlots; ++k)
+        if (!done && slot[k] == my) {
+          slot[k] = kNone;
+          done = true;
+        }
+    }
+    if (key == kNone) {  // nothing ready before every op ran: only after a lost key
+      over = true;
+      break;
+    }
+    const int v = (int)(key & 0xFFFFu);
+    const uint32_t ready = (uint32_t)(key >> 16);
+    // the successors' fields, requested before the placement needs them
+    uint32_t s2 = 0, xs[2] = {0, 0}, xreq[2], xrel[2], xp01[2], xp23[2];
+    int xd[2];
+    if (kPacked) {
+      s2 = G.succ2[v];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const uint32_t x = (s2 >> (16 * i)) & 0xFFFFu;
+        xs[i] = x == 0xFFFFu ? 0u : x;
+        xreq[i] = m_req[xs[i]];
+        xrel[i] = m_rel[xs[i]];
+        xp01[i] = m_p01[xs[i]];
+        xp23[i] = kPacked > 2 ? m_p23[xs[i]] : 0xFFFFFFFFu;
+        xd[i] = prow[xs[i]];
+      }
+    }
+    int d = prow[v];
+    if (d >= D) {
+      bad = true;
+      d = 0;
+    }
+    const uint32_t w = C == 1 ? G.dur32[v] : G.dur32[(int64_t)v * C + G.dev_class[d]];
+    uint32_t s = umax32(ready, clk[d * kWave + lane]);
+    {  // the first idle slice that holds [s', s' + w) with s' >= s
+      const uint32_t e = (uint32_t)d * (uint32_t)G.lut_nb + (uint32_t)min((int)((s + w) >> G.lut_shift), G.lut_nb - 1);
+      const uint4 lw = G.lut_w[e];
+      const uint32_t t0 = umax32(s, lw.x), t1 = umax32(s, lw.z);
+      if (t0 + w <= lw.y) {
+        s = t0;
+      } else if (t1 + w <= lw.w) {
+        s = t1;
+      } else {
+        const int sb = G.slice_ptr[d];
+        for (int k = (int)G.lut_k[e] + 2;; ++k) {
+          const uint32_t t = umax32(s, G.slice_begin32[sb + k]);
+          if (t + w <= G.slice_end32[sb + k]) {
+            s = t;
+            break;
+          }
+        }
+      }
+    }
+    const uint32_t f = s + w;
+    clk[d * kWave + lane] = f;
+    uint16_t *cd = cnt + (int64_t)d * nb + c;
+    const uint16_t rk = *cd;
+    *cd = (uint16_t)(rk + 1);
+    rrow[v] = rk;
+    frow[v] = f;
+    uint32_t *cr = comp + (int64_t)(m_req[v] & 0xFFFFu) * nb + c;
+    *cr = umax32(*cr, f);
+    ms = umax32(ms, f);
+    sum += f;
+    // successors whose last unset predecessor this was become ready
+    if (kPacked) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        if (((s2 >> (16 * i)) & 0xFFFFu) != 0xFFFFu) {
+          int dx = xd[i];
+          if (dx >= D) dx = 0;
+          const int pu[4] = {(int)(xp01[i] & 0xFFFFu), (int)(xp01[i] >> 16), (int)(xp23[i] & 0xFFFFu),
+                             (int)(xp23[i] >> 16)};
+          const uint64_t nk = ready_key((int)xs[i], v, f, dx, xrel[i], (int)(xreq[i] >> 16), pu);
+          if (nk != kNone) insert(nk);
+        }
+      }
+    } else {
+      const int q1 = G.succ_ptr[v + 1];
+      for (int q = G.succ_ptr[v]; q < q1; ++q) {
+        const int x = G.succ_idx[q];
+        int dx = prow[x];
+        if (dx >= D) dx = 0;
+        uint32_t rx = G.release32[G.op_req[x]];
+        bool ok = true;
+        const int e1 = G.pred_ptr[x + 1];
+        for (int e = G.pred_ptr[x]; e < e1; ++e) {
+          const int u = G.pred_idx[e];
+          uint32_t t = u == v ? f : frow[u];
+          if (t == kFinUnset) {
+            ok = false;
+            break;
+          }
+          int du = prow[u];
+          if (du >= D) du = 0;
+          if (du != dx) t += xfer_of(G, u, du, dx);
+          rx = umax32(rx, t);
+        }
+        if (ok) insert((uint64_t)rx << 16 | (uint64_t)x);
+      }
+    }
+  }
+  ovf[c] = over ? 1u : 0u;
+  if (over) return;  // ready_schedule writes this candidate's outputs
+  if (bad) {
+    makespan[c] = INT64_MAX;
+    if (sumfin) sumfin[c] = INT64_MAX;
+    if (slack)
+      for (int r = 0; r < R; ++r) slack[c * R + r] = INT64_MIN;
+    violation[c] = SS_VIOLATION_INVALID;
+    return;
+  }
+  makespan[c] = ms;
+  if (sumfin) sumfin[c] = (int64_t)sum;
+  violation[c] = 0;
+  if (slack)
+    for (int r = 0; r < R; ++r) slack[c * R + r] = G.deadline[r] - (int64_t)comp[(int64_t)r * nb + c];
+}
 
 // ------------------------------------------------------------------ memory
 // Residency intervals (Sec. 3.3.2) are written by fast_intervals into
@@ -1969,9 +2191,14 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
   const int64_t slot_cap = N + E + 1;
   const int sets = W.single ? 1 : kRecSets;
   auto align = [](size_t x) { return (x + 255) & ~size_t(255); };
+  // one lane per candidate (ready_lanes) unless SS_READY=wave; its per-device
+  // ranks and per-request completions, and the flags of the candidates it
+  // hands to ready_schedule
+  const char *rmode = std::getenv("SS_READY");
+  const bool lanes = !(rmode && std::strcmp(rmode, "wave") == 0);
   struct Plan {
     int64_t chunk, sub, nslots, n_ticket;
-    size_t sz_fin, sz_rank, sz_miss, sz_spill, sz_rows, sz_own, sz_cp, sz_meta, sz_wk, sz_wb, sz_tk, total;
+    size_t sz_fin, sz_rank, sz_miss, sz_spill, sz_rows, sz_own, sz_cp, sz_meta, sz_wk, sz_wb, sz_tk, sz_lane, total;
   };
   auto plan_of = [&](int64_t chunk, int64_t sub_cap) {
     Plan q{};
@@ -1992,12 +2219,16 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
     q.sz_wb = align((size_t)q.nslots * slot_cap * 8);
     q.n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
     q.sz_tk = align((size_t)q.n_ticket * 4);
+    q.sz_lane = lanes ? align((size_t)chunk * D * 2) + align((size_t)chunk * R * 4 + 4) + align((size_t)chunk * 4) : 0;
     q.total = q.sz_fin + q.sz_rank + q.sz_miss + q.sz_spill + q.sz_rows +
-              (size_t)sets * (q.sz_own + q.sz_cp + q.sz_meta) + q.sz_wk + q.sz_wb + q.sz_tk;
+              (size_t)sets * (q.sz_own + q.sz_cp + q.sz_meta) + q.sz_wk + q.sz_wb + q.sz_tk + q.sz_lane;
     return q;
   };
   const int64_t sub_pref = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
-  const Plan ppref = plan_of(kScratchBudget / std::max<int64_t>(1, per_cand), sub_pref);
+  // the lane kernel keeps one wave per 64 candidates resident: large chunks
+  // (the fast path's budget, halved while it does not fit) fill the chip
+  const int64_t budget0 = lanes ? kFastScratchBudget : kScratchBudget;
+  const Plan ppref = plan_of(budget0 / std::max<int64_t>(1, per_cand), sub_pref);
   const Plan pmin = plan_of(1, 1);
   if (W.query) {
     W.need_min = pmin.total;
@@ -2009,6 +2240,15 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
   err = hipFuncSetAttribute(reinterpret_cast<const void *>(&ready_schedule), hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)lds);
   if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
+  const size_t lane_lds = (size_t)D * kWave * 4;
+  const int packed = G.succ2 && g->n_link <= 2 ? (g->max_indeg <= 2 ? 2 : g->max_indeg <= 4 ? 4 : 0) : 0;
+  const void *lane_fn = packed == 2   ? reinterpret_cast<const void *>(&ready_lanes<2>)
+                        : packed == 4 ? reinterpret_cast<const void *>(&ready_lanes<4>)
+                                      : reinterpret_cast<const void *>(&ready_lanes<0>);
+  if (lanes) {
+    err = hipFuncSetAttribute(lane_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lane_lds);
+    if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
+  }
   Plan pl = ppref;
   SsScratch scr;
   void *scratch = nullptr;
@@ -2028,7 +2268,11 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
     }
     scratch = W.ptr;
   } else {
-    err = ss_scratch_get(g->device, g->pool, pl.total, stream, &scr);
+    for (int64_t budget = budget0;; budget /= 2) {
+      pl = plan_of(budget / std::max<int64_t>(1, per_cand), sub_pref);
+      err = ss_scratch_get(g->device, g->pool, pl.total, stream, &scr);
+      if (err != hipErrorOutOfMemory || budget <= kScratchBudget / 4 || pl.chunk <= 1) break;
+    }
     if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
     scratch = scr.p;
   }
@@ -2044,6 +2288,13 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
   auto *miss = reinterpret_cast<uint16_t *>(take(pl.sz_miss));
   auto *spill = reinterpret_cast<uint64_t *>(take(pl.sz_spill));
   auto *rows = reinterpret_cast<uint8_t *>(take(pl.sz_rows));
+  uint16_t *lcnt = nullptr;
+  uint32_t *lcomp = nullptr, *lovf = nullptr;
+  if (lanes) {
+    lcnt = reinterpret_cast<uint16_t *>(take(align((size_t)chunk * D * 2)));
+    lcomp = reinterpret_cast<uint32_t *>(take(align((size_t)chunk * R * 4 + 4)));
+    lovf = reinterpret_cast<uint32_t *>(take(align((size_t)chunk * 4)));
+  }
   MemPass M{};
   for (int k = 0; k < sets; ++k) {
     M.own[k] = reinterpret_cast<Rec *>(take(pl.sz_own));
@@ -2082,9 +2333,25 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
       Pc = rows;
     }
     SsTimingRec *ts = ss_timing_start(SS_KERNEL_SCHEDULE, stream);
+    if (lanes) {
+      int64_t *ms_out = makespan + b0, *sf_out = sumfin ? sumfin + b0 : nullptr,
+              *sl_out = slack ? slack + b0 * R : nullptr;
+      uint8_t *vi_out = violation + b0;
+      const uint8_t *pc = Pc;
+      int64_t nbv = nb;
+      void *args[] = {const_cast<GmgView *>(&G), &pc, &nbv, &fin, &rank, &lcnt, &lcomp, &lovf, &ms_out, &sf_out,
+                      &sl_out, &vi_out};
+      err = hipLaunchKernel(lane_fn, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), args, lane_lds, stream);
+      if (err == hipSuccess) err = hipGetLastError();
+      if (err != hipSuccess) {
+        rc = hip_fail(err, "ready_lanes launch");
+        break;
+      }
+    }
+    // the candidates ready_lanes flagged (all of them without it), one wave each
     hipLaunchKernelGGL(ready_schedule, dim3((unsigned)nb), dim3(kWave), lds, stream, G, Pc, fin, rank, miss, spill,
                        makespan + b0, sumfin ? sumfin + b0 : nullptr, slack ? slack + b0 * R : nullptr,
-                       violation + b0);
+                       violation + b0, static_cast<const uint32_t *>(lovf));
     ss_timing_stop(ts, stream);
     err = hipGetLastError();
     if (err != hipSuccess) {
