@@ -105,11 +105,18 @@ __global__ __launch_bounds__(256) void transpose_tiles(const T *__restrict__ in,
 // Byte matrices whose sizes and input pitch are multiples of 4 (and 4-byte
 // aligned input): 128 x 128 tiles moved as 4-byte words on both sides. A word
 // read holds 4 columns of one row; a word written packs 4 rows of one column,
-// gathered byte by byte from LDS (row pitch 33 words).
+// gathered byte by byte from LDS (row pitch 33 words).  Workgroups go to the
+// 8 XCDs round-robin by launch order, each XCD with its own L2; tiles are
+// renumbered so that each XCD takes consecutive tiles of a row band, whose
+// row segments share the 128-byte lines they straddle (the row pitch need
+// not be a multiple of 128), and a line is fetched once instead of twice.
 __global__ __launch_bounds__(256) void transpose_u8_words(const uint8_t *__restrict__ in, int64_t rows, int64_t cols,
                                                           int64_t pitch, uint8_t *__restrict__ out) {
   __shared__ uint32_t tile[128 * 33];
-  const int64_t c0 = (int64_t)blockIdx.x * 128, r0 = (int64_t)blockIdx.y * 128;
+  const uint32_t gx = gridDim.x, total = gx * gridDim.y, L = blockIdx.y * gx + blockIdx.x;
+  const uint32_t xcd = L % 8u, per = total / 8u, extra = total % 8u;
+  const uint32_t Lr = xcd * per + min(xcd, extra) + L / 8u;  // a bijection of [0, total)
+  const int64_t c0 = (int64_t)(Lr % gx) * 128, r0 = (int64_t)(Lr / gx) * 128;
   const int w = threadIdx.x & 31, i0 = threadIdx.x >> 5;
   const bool col_in = c0 + 4 * w < cols;
 #pragma unroll
@@ -661,9 +668,9 @@ __global__ __launch_bounds__(kWave) void ready_schedule(const GmgView G, const u
 size_t ready_schedule_lds(int D, int R) { return (size_t)(3 * D + R + 1 + D) * 4; }
 
 // The same rule with one lane per candidate (64 candidates per wave): the
-// ready set is a lane's own, kLaneSlots keys in registers; device clocks in
-// LDS [device][lane]; ranks per device and request completions in global
-// scratch [device or request][candidate]; finish times and ranks in the
+// ready set is a lane's own, kLaneSlots keys in registers; device clocks and
+// request completions in LDS [device or request][lane]; ranks per device in
+// global scratch [device][candidate]; finish times and ranks in the
 // candidate rows the memory pass reads.  An op is ready when none of its
 // predecessors' finish times is still unset (the rows start cleared), so no
 // per-op counters are kept.  A candidate whose ready set outgrows the slots
@@ -680,13 +687,13 @@ constexpr uint32_t kFinUnset = 0xFFFFFFFFu;  // above every finish (the horizon 
 template <int kPacked>
 __global__ __launch_bounds__(kWave) void ready_lanes(const GmgView G, const uint8_t *__restrict__ P, int64_t nb,
                                                      uint32_t *__restrict__ fin, uint16_t *__restrict__ rank,
-                                                     uint16_t *__restrict__ cnt, uint32_t *__restrict__ comp,
-                                                     uint32_t *__restrict__ ovf, int64_t *__restrict__ makespan,
-                                                     int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
-                                                     uint8_t *__restrict__ violation) {
+                                                     uint16_t *__restrict__ cnt, uint32_t *__restrict__ ovf,
+                                                     int64_t *__restrict__ makespan, int64_t *__restrict__ sumfin,
+                                                     int64_t *__restrict__ slack, uint8_t *__restrict__ violation) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
-  uint32_t *clk = reinterpret_cast<uint32_t *>(lds_raw);  // [D][64]
   const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = G.n_class;
+  uint32_t *clk = reinterpret_cast<uint32_t *>(lds_raw);  // [D][64]
+  uint32_t *comp = clk + (size_t)D * kWave;                // [R][64]
   const int lane = threadIdx.x;
   const int64_t c0 = (int64_t)blockIdx.x * kWave, c = c0 + lane;
   const int rows = (int)min<int64_t>(kWave, nb - c0);
@@ -695,11 +702,10 @@ __global__ __launch_bounds__(kWave) void ready_lanes(const GmgView G, const uint
     for (int v = lane; v < N; v += kWave) fr[v] = kFinUnset;
   }
   for (int d = 0; d < D; ++d) clk[d * kWave + lane] = 0;
+  for (int r = 0; r < R; ++r) comp[r * kWave + lane] = G.release32[r];
   const bool act = c < nb;
-  if (act) {
+  if (act)
     for (int d = 0; d < D; ++d) cnt[(int64_t)d * nb + c] = 0;
-    for (int r = 0; r < R; ++r) comp[(int64_t)r * nb + c] = G.release32[r];
-  }
   __syncthreads();  // every row cleared before a lane reads its own
   if (!act) return;
   const uint8_t *prow = P + c * N;
@@ -819,7 +825,7 @@ __global__ __launch_bounds__(kWave) void ready_lanes(const GmgView G, const uint
     *cd = (uint16_t)(rk + 1);
     rrow[v] = rk;
     frow[v] = f;
-    uint32_t *cr = comp + (int64_t)(m_req[v] & 0xFFFFu) * nb + c;
+    uint32_t *cr = comp + (m_req[v] & 0xFFFFu) * kWave + lane;
     *cr = umax32(*cr, f);
     ms = umax32(ms, f);
     sum += f;
@@ -875,7 +881,7 @@ __global__ __launch_bounds__(kWave) void ready_lanes(const GmgView G, const uint
   if (sumfin) sumfin[c] = (int64_t)sum;
   violation[c] = 0;
   if (slack)
-    for (int r = 0; r < R; ++r) slack[c * R + r] = G.deadline[r] - (int64_t)comp[(int64_t)r * nb + c];
+    for (int r = 0; r < R; ++r) slack[c * R + r] = G.deadline[r] - (int64_t)comp[r * kWave + lane];
 }
 
 // ------------------------------------------------------------------ memory
@@ -2195,7 +2201,12 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
   // ranks and per-request completions, and the flags of the candidates it
   // hands to ready_schedule
   const char *rmode = std::getenv("SS_READY");
-  const bool lanes = !(rmode && std::strcmp(rmode, "wave") == 0);
+  const bool lanes_env = !(rmode && std::strcmp(rmode, "wave") == 0);
+  const size_t lane_lds = (size_t)(D + R) * kWave * 4;
+  int lds_blk = 0;
+  err = hipDeviceGetAttribute(&lds_blk, hipDeviceAttributeMaxSharedMemoryPerBlock, g->device);
+  if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
+  const bool lanes = lanes_env && lane_lds <= (size_t)lds_blk;  // else one wave per candidate throughout
   struct Plan {
     int64_t chunk, sub, nslots, n_ticket;
     size_t sz_fin, sz_rank, sz_miss, sz_spill, sz_rows, sz_own, sz_cp, sz_meta, sz_wk, sz_wb, sz_tk, sz_lane, total;
@@ -2219,7 +2230,7 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
     q.sz_wb = align((size_t)q.nslots * slot_cap * 8);
     q.n_ticket = (B + chunk - 1) / chunk * ((chunk + sub - 1) / sub);
     q.sz_tk = align((size_t)q.n_ticket * 4);
-    q.sz_lane = lanes ? align((size_t)chunk * D * 2) + align((size_t)chunk * R * 4 + 4) + align((size_t)chunk * 4) : 0;
+    q.sz_lane = lanes ? align((size_t)chunk * D * 2) + align((size_t)chunk * 4) : 0;
     q.total = q.sz_fin + q.sz_rank + q.sz_miss + q.sz_spill + q.sz_rows +
               (size_t)sets * (q.sz_own + q.sz_cp + q.sz_meta) + q.sz_wk + q.sz_wb + q.sz_tk + q.sz_lane;
     return q;
@@ -2240,7 +2251,6 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
   err = hipFuncSetAttribute(reinterpret_cast<const void *>(&ready_schedule), hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)lds);
   if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
-  const size_t lane_lds = (size_t)D * kWave * 4;
   const int packed = G.succ2 && g->n_link <= 2 ? (g->max_indeg <= 2 ? 2 : g->max_indeg <= 4 ? 4 : 0) : 0;
   const void *lane_fn = packed == 2   ? reinterpret_cast<const void *>(&ready_lanes<2>)
                         : packed == 4 ? reinterpret_cast<const void *>(&ready_lanes<4>)
@@ -2289,10 +2299,9 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
   auto *spill = reinterpret_cast<uint64_t *>(take(pl.sz_spill));
   auto *rows = reinterpret_cast<uint8_t *>(take(pl.sz_rows));
   uint16_t *lcnt = nullptr;
-  uint32_t *lcomp = nullptr, *lovf = nullptr;
+  uint32_t *lovf = nullptr;
   if (lanes) {
     lcnt = reinterpret_cast<uint16_t *>(take(align((size_t)chunk * D * 2)));
-    lcomp = reinterpret_cast<uint32_t *>(take(align((size_t)chunk * R * 4 + 4)));
     lovf = reinterpret_cast<uint32_t *>(take(align((size_t)chunk * 4)));
   }
   MemPass M{};
@@ -2339,8 +2348,8 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
       uint8_t *vi_out = violation + b0;
       const uint8_t *pc = Pc;
       int64_t nbv = nb;
-      void *args[] = {const_cast<GmgView *>(&G), &pc, &nbv, &fin, &rank, &lcnt, &lcomp, &lovf, &ms_out, &sf_out,
-                      &sl_out, &vi_out};
+      void *args[] = {const_cast<GmgView *>(&G), &pc, &nbv, &fin, &rank, &lcnt, &lovf, &ms_out, &sf_out, &sl_out,
+                      &vi_out};
       err = hipLaunchKernel(lane_fn, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), args, lane_lds, stream);
       if (err == hipSuccess) err = hipGetLastError();
       if (err != hipSuccess) {
