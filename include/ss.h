@@ -200,7 +200,10 @@ int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req)
  * It takes stream-ordered scratch on hip_stream, for the duration of the
  * work, from the library's memory pool for g's device, which keeps that
  * memory for later calls (for a fixed workload, calls after the first
- * allocate no device memory; see ss_release_cached_memory).  A caller that
+ * allocate no device memory; see ss_release_cached_memory).  Its chunk sizes
+ * follow the memory the device has free at the call; when the pool runs
+ * short, the call waits for hip_stream's earlier work, returns its idle
+ * memory to the driver and retries once, then halves its chunks.  A caller that
  * must own that memory passes it to ss_simulate_batch_ws instead (sized with
  * ss_simulate_workspace_size).  B = 0 is a no-op.  Results are bit-identical
  * to a sequential CPU evaluation of the same rules.
@@ -227,8 +230,9 @@ int ss_simulate_workspace_size(const ss_gmg *g, int64_t B, int layout, int64_t *
  * and candidate loop of Alg. 1): *chunk candidates per schedule launch and
  * *sub per memory-pass launch inside a chunk (equal to *chunk where the
  * memory pass is not split), so that tests and benchmarks can check the
- * candidates at every boundary.  A chunk size reduced after running out of
- * memory applies to later calls and is reported.  Launches nothing.
+ * candidates at every boundary.  The sizes follow the memory the device has
+ * free at the time of the query, as a call's would (a call that then runs
+ * out of memory halves its chunks).  Launches nothing.
  * Errors: SS_ERR_INVALID_ARG, SS_ERR_DEVICE, SS_ERR_UNSUPPORTED.
  */
 int ss_simulate_chunking(const ss_gmg *g, int64_t B, int layout, int64_t *chunk, int64_t *sub);

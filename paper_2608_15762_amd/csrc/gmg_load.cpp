@@ -158,6 +158,27 @@ hipError_t ss_pool_malloc(void **p, size_t bytes, hipMemPool_t pool, hipStream_t
   return e;
 }
 
+int64_t ss_scratch_budget(int device, hipMemPool_t pool, int64_t cap) {
+  size_t free_b = 0, total_b = 0;
+  if (hipMemGetInfo(&free_b, &total_b) != hipSuccess) {
+    (void)hipGetLastError();
+    return cap;
+  }
+  uint64_t reserved = 0, used = 0;
+  if (pool && (hipMemPoolGetAttribute(pool, hipMemPoolAttrReservedMemCurrent, &reserved) != hipSuccess ||
+               hipMemPoolGetAttribute(pool, hipMemPoolAttrUsedMemCurrent, &used) != hipSuccess)) {
+    (void)hipGetLastError();
+    reserved = used = 0;
+  }
+  size_t idle = 0;
+  if (device >= 0 && device < kMaxDevices) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    for (const IdleScratch &b : g_idle[device]) idle += b.bytes;
+  }
+  const uint64_t avail = (uint64_t)free_b + (reserved > used ? reserved - used : 0) + idle;
+  return std::min<int64_t>(cap, (int64_t)(avail / 4 * 3));
+}
+
 hipError_t ss_scratch_get(int device, hipMemPool_t pool, size_t bytes, hipStream_t stream, SsScratch *s) {
   s->p = nullptr;
   s->bytes = 0;

@@ -58,10 +58,9 @@ constexpr int kWave = 64;
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per chunk
 // index-order 32-bit path: larger chunks (fewer pipeline fills and drains of
-// the memory passes), halved while the scratch does not fit; later calls on
-// the device start from the last budget that fitted
+// the memory passes), within the memory the call can get (ss_scratch_budget)
+// and halved while the scratch does not fit
 constexpr int64_t kFastScratchBudget = int64_t(96) << 30;
-std::atomic<int64_t> g_fast_budget[256];  // 0: not tried yet
 constexpr int64_t kRecordBudget = int64_t(32) << 30;   // sizes the sub-chunks (record bytes of about two sets)
 constexpr int kPeakBlocksPerCU = 8;  // fast_peaks holds about 19.5 KB of LDS
 
@@ -2027,9 +2026,8 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
     W.need_min = pmin.total;
     const FastPlan pp = plan_for_budget(kFastScratchBudget);
     W.need_pref = pp.total;
-    // the pool path starts from the last budget that fitted on this device
-    const int64_t fb = g_fast_budget[g->device & 255].load();
-    const FastPlan pq = W.single ? pp : plan_for_budget(fb > 0 ? fb : kFastScratchBudget);
+    // the pool path starts from the budget the device's memory allows now
+    const FastPlan pq = W.single ? pp : plan_for_budget(ss_scratch_budget(g->device, g->pool, kFastScratchBudget));
     W.chunk = pq.chunk;
     W.sub = pq.sub;
     return SS_OK;
@@ -2059,14 +2057,11 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
   } else {
     // the largest chunk within the scratch budget; when its scratch does not
     // fit in the device's free memory, half the budget (down to one round)
-    std::atomic<int64_t> &fitted = g_fast_budget[g->device & 255];
-    int64_t budget = fitted.load();
-    for (budget = budget > 0 ? budget : kFastScratchBudget;; budget /= 2) {
+    for (int64_t budget = ss_scratch_budget(g->device, g->pool, kFastScratchBudget);; budget /= 2) {
       pl = plan_for_budget(budget);
       err = ss_scratch_get(g->device, g->pool, pl.total, stream, &scr);
       if (err != hipErrorOutOfMemory || pl.chunk <= std::min<int64_t>(round, B)) break;
     }
-    if (err == hipSuccess && pl.chunk < B) fitted.store(budget);  // a budget that bounded the chunk and fitted
     if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
     scratch = scr.p;
   }
@@ -2238,14 +2233,18 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
   const int64_t sub_pref = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
   // the lane kernel keeps one wave per 64 candidates resident: large chunks
   // (the fast path's budget, halved while it does not fit) fill the chip
-  const int64_t budget0 = lanes ? kFastScratchBudget : kScratchBudget;
-  const Plan ppref = plan_of(budget0 / std::max<int64_t>(1, per_cand), sub_pref);
+  // (the preferred layout for a caller's workspace; the pool path starts
+  // from what the device's memory allows now)
+  const int64_t budget_pref = lanes ? kFastScratchBudget : kScratchBudget;
+  const int64_t budget0 = lanes ? ss_scratch_budget(g->device, g->pool, budget_pref) : budget_pref;
+  const Plan ppref = plan_of(budget_pref / std::max<int64_t>(1, per_cand), sub_pref);
   const Plan pmin = plan_of(1, 1);
   if (W.query) {
     W.need_min = pmin.total;
     W.need_pref = ppref.total;
-    W.chunk = ppref.chunk;
-    W.sub = ppref.sub;
+    const Plan pq = W.single ? ppref : plan_of(budget0 / std::max<int64_t>(1, per_cand), sub_pref);
+    W.chunk = pq.chunk;
+    W.sub = pq.sub;
     return SS_OK;
   }
   err = hipFuncSetAttribute(reinterpret_cast<const void *>(&ready_schedule), hipFuncAttributeMaxDynamicSharedMemorySize,
