@@ -101,6 +101,58 @@ __global__ __launch_bounds__(256) void transpose_tiles(const T *__restrict__ in,
   }
 }
 
+// 32-bit matrices whose row and column counts and pitch are multiples of 4
+// (16-byte aligned buffers): a workgroup takes a strip of 64 columns and walks
+// kStripTiles tiles of 64 rows down it, each tile read and written as 16-byte
+// vectors through LDS (a wave moves four 256-byte row segments per access).
+// The next tile's loads are in flight while the current one is written out,
+// and the output segments of consecutive tiles, which share the lines where a
+// row's segments meet, are written by the same workgroup.
+constexpr int kStripTiles = 16;
+__global__ __launch_bounds__(256) void transpose_u32_strips(const uint32_t *__restrict__ in, int64_t rows,
+                                                            int64_t cols, int64_t pitch, uint32_t *__restrict__ out) {
+  __shared__ uint32_t tile[64][65];
+  const int64_t c0 = (int64_t)blockIdx.x * 64, rb = (int64_t)blockIdx.y * (64 * kStripTiles);
+  const int t = threadIdx.x, sub = t & 15, grp = t >> 4;
+  // read side: rows grp + 16j of the tile, columns 4 sub .. 4 sub + 3;
+  // write side: columns grp + 16j of the tile (output rows), rows 4 sub .. 4 sub + 3
+  const bool col_in = c0 + 4 * sub < cols;
+  auto load = [&](int64_t r0, uint4 (&v)[4]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t r = r0 + grp + 16 * j;
+      v[j] = (col_in && r < rows) ? *reinterpret_cast<const uint4 *>(in + r * pitch + c0 + 4 * sub)
+                                  : uint4{0u, 0u, 0u, 0u};
+    }
+  };
+  const int64_t left = (rows - rb + 63) / 64;  // >= 1: the grid covers the rows
+  const int ntile = left < kStripTiles ? (int)left : kStripTiles;
+  uint4 v[4];
+  load(rb, v);
+  for (int k = 0; k < ntile; ++k) {
+    const int64_t r0 = rb + (int64_t)k * 64;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t *row = tile[grp + 16 * j] + 4 * sub;
+      row[0] = v[j].x;
+      row[1] = v[j].y;
+      row[2] = v[j].z;
+      row[3] = v[j].w;
+    }
+    __syncthreads();
+    if (k + 1 < ntile) load(r0 + 64, v);
+    const int64_t r = r0 + 4 * sub;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int oc = grp + 16 * j;
+      if (c0 + oc < cols && r < rows)
+        *reinterpret_cast<uint4 *>(out + (c0 + oc) * rows + r) =
+            uint4{tile[4 * sub][oc], tile[4 * sub + 1][oc], tile[4 * sub + 2][oc], tile[4 * sub + 3][oc]};
+    }
+    __syncthreads();
+  }
+}
+
 // Byte matrices whose sizes and input pitch are multiples of 4 (and 4-byte
 // aligned input): 128 x 128 tiles moved as 4-byte words on both sides. A word
 // read holds 4 columns of one row; a word written packs 4 rows of one column,
@@ -1007,15 +1059,17 @@ struct IvSucc {  // device, finish and rank of the first two successors (with po
   uint32_t dx0, dx1, fx0, fx1, rx0, rx1, ax0, ax1;
 };
 
-// Store staging.  A 64-byte line of a bucket holds the records of positions
-// 4L .. 4L+3.  A destination's records of one chunk have consecutive
-// positions [first, last], and with index ranks no later chunk writes below
-// them, so line L of a bucket [start, end) is complete once position
-// min(4L+3, end-1) has been produced.  A record's role:
-//   open   its line began in an earlier chunk: staged in LDS; the record that
-//          completes the line (close) queues it for a cooperative write
-//   direct its line lies inside this chunk's run and is complete: stored
-//   tail   its line begins in this chunk and is not complete: staged
+// Store staging of the own records.  A block of a bucket holds the records
+// of positions 2L, 2L+1.  A device's own records of one chunk have
+// consecutive positions [first, last], and with index ranks no later chunk
+// writes below them, so block L of a bucket [start, end) is complete once
+// position min(2L+1, end-1) has been produced.  A record's role:
+//   open   its block began in an earlier chunk: staged in LDS; the record
+//          that completes the block (close) queues it for a cooperative write
+//   direct its block lies inside this chunk's run and is complete: stored
+//   tail   its block begins in this chunk and is not complete: staged
+// Copies are stored directly: staging them as well (a block per destination
+// device) cost more occupancy than it saved.
 constexpr int kRoleNone = 0, kRoleDirect = 1, kRoleOpen = 2, kRoleClose = 6, kRoleTail = 8;
 
 template <int kShift>
@@ -1030,10 +1084,9 @@ __device__ __forceinline__ int line_role(int p, int first, int last, int end) {
   return done ? kRoleDirect : kRoleTail;
 }
 
-// Staged blocks: own records and copies in 32-byte pairs (a smaller stage
-// leaves more waves per CU, which this kernel needs).
+// Staged blocks: own records in 32-byte pairs (a smaller stage leaves more
+// waves per CU, which this kernel needs).
 constexpr int kOwnShift = 1, kOwnRecs = 1 << kOwnShift;
-constexpr int kCpShift = 1, kCpRecs = 1 << kCpShift;
 
 // kGivenRanks: the rank table already holds every op's rank on its device
 // (dispatch order), pass A only counts.  kShiftLinks (with kFast): link
@@ -1051,22 +1104,19 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
                                                         const uint8_t *__restrict__ violation,
                                                         const uint32_t *__restrict__ arr) {
   // LDS (dynamic, sized by the device count): bucket offsets and fill
-  // pointers; with staged stores (kFast with index ranks) also the open line of
-  // every device's own bucket and the queue of complete lines
+  // pointers; with staged stores (kFast with index ranks) also the open block
+  // of every device's own bucket and the queue of complete blocks
   constexpr bool kStage = kFast && !kGivenRanks;
   extern __shared__ __align__(16) unsigned char iv_lds[];
   const int Dv = G.n_dev;
   Rec *obuf = reinterpret_cast<Rec *>(iv_lds);                           // [D][kOwnRecs]
-  Rec *cbuf = obuf + (kStage ? kOwnRecs * Dv : 0);                       // [D][kCpRecs]
-  int *own_off = reinterpret_cast<int *>(cbuf + (kStage ? kCpRecs * Dv : 0));  // [D+1]
+  int *own_off = reinterpret_cast<int *>(obuf + (kStage ? kOwnRecs * Dv : 0));  // [D+1]
   int *cp_off = own_off + Dv + 1;                                          // [D+1]
   int *cfill = cp_off + Dv + 1;                                            // [D] next copy slot
   int *base = cfill + Dv;  // [D] ops counted so far; with staging then the next own position
   int *nocopy = base + Dv;                                                 // [64]
-  uint32_t *fq = reinterpret_cast<uint32_t *>(nocopy + kWave);  // [64] own lines to write
-  uint32_t *fc = fq + kWave;                                    // [128] copy blocks to write
-  int &fqn = *reinterpret_cast<int *>(fc + 2 * kWave);
-  int &fcn = *(&fqn + 1);
+  uint32_t *fq = reinterpret_cast<uint32_t *>(nocopy + kWave);  // [64] own blocks to write
+  int &fqn = *reinterpret_cast<int *>(fq + kWave);
   const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops], K = G.n_link;
   const int lane = threadIdx.x;
   const int64_t j = blockIdx.x, c = j0 + j;
@@ -1119,7 +1169,7 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
   }
   if (kStage) {
     for (int d = lane; d < D; d += kWave) base[d] = own_off[d];
-    if (lane == 0) fqn = fcn = 0;
+    if (lane == 0) fqn = 0;
   }
   __syncthreads();  // also orders the rank-table stores before the loads below
   if (!kFast) {
@@ -1194,10 +1244,8 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       const bool c0 = act && has0 && !loc0 && a.b != 0;
       const bool c1 = act && has1 && !loc1 && !same && a.b != 0;
       int *const f0 = c0 ? &cfill[sc.dx0] : &nocopy[lane], *const f1 = c1 ? &cfill[sc.dx1] : &nocopy[lane];
-      int qo = 0, q0 = 0, q1 = 0;
-      if (kStage) {  // first position of each destination's run in this chunk
-        q0 = *f0;
-        q1 = *f1;
+      int qo = 0;
+      if (kStage) {  // first position of the device's own run in this chunk
         qo = base[d];  // d is valid in every lane (inactive lanes repeat the last op)
         atomicAdd(&base[d], act ? 1 : 0);
       }
@@ -1211,34 +1259,26 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       const uint32_t st0 = kPorts ? T0 - X0 : a.f, st1 = kPorts ? T1 - X1 : a.f;  // transfer starts
       const Rec r0 = Rec{st0, hi0, a.b, (uint32_t)max((int)ra0 - 3, 0) << 16 | (ry0 + 1)};
       const Rec r1 = Rec{st1, sc.fx1, a.b, (uint32_t)max((int)sc.rx1 - 3, 0) << 16 | (sc.rx1 + 1)};
-      const uint32_t dx0 = sc.dx0, dx1 = sc.dx1;
       sc = load_succ(an, vn);  // the next chunk's successors, in flight during the stores
       if (!kStage) {
         own[act ? po : N] = ro;
         cp[c0 ? s0 : E] = r0;
         cp[c1 ? s1 : E] = r1;
       } else {
+        if (c0) cp[s0] = r0;
+        if (c1) cp[s1] = r1;
         wave_lds_fence();
-        // each destination's positions in this chunk form one run [first, last]
+        // the device's positions in this chunk form one run [first, last]
         const int eo = base[d] - 1, bo = own_off[d + 1];
-        const int e0 = *f0 - 1, e1 = *f1 - 1;
         const int ko = act ? line_role<kOwnShift>(po, qo, eo, bo) : kRoleNone;
-        const int k0 = c0 ? line_role<kCpShift>(s0, q0, e0, INT_MAX) : kRoleNone;
-        const int k1 = c1 ? line_role<kCpShift>(s1, q1, e1, INT_MAX) : kRoleNone;
-        // blocks complete inside this chunk: stored directly
+        // a block complete inside this chunk: stored directly
         if (ko == kRoleDirect) own[po] = ro;
-        if (k0 == kRoleDirect) cp[s0] = r0;
-        if (k1 == kRoleDirect) cp[s1] = r1;
         // the block open since earlier chunks: staged, and queued once complete
         if (ko & kRoleOpen) obuf[d * kOwnRecs + (po & (kOwnRecs - 1))] = ro;
-        if (k0 & kRoleOpen) cbuf[dx0 * kCpRecs + (s0 & (kCpRecs - 1))] = r0;
-        if (k1 & kRoleOpen) cbuf[dx1 * kCpRecs + (s1 & (kCpRecs - 1))] = r1;
         if (ko == kRoleClose) fq[atomicAdd(&fqn, 1)] = d << 20 | (uint32_t)(po >> kOwnShift);
-        if (k0 == kRoleClose) fc[atomicAdd(&fcn, 1)] = dx0 << 20 | (uint32_t)(s0 >> kCpShift);
-        if (k1 == kRoleClose) fc[atomicAdd(&fcn, 1)] = dx1 << 20 | (uint32_t)(s1 >> kCpShift);
         wave_lds_fence();
         // write the queued blocks, adjacent lanes to adjacent records
-        const int nq = fqn, nc = fcn;
+        const int nq = fqn;
         for (int qb = 0; qb < nq; qb += kWave / kOwnRecs) {
           const int qi = qb + (lane >> kOwnShift), part = lane & (kOwnRecs - 1);
           if (qi < nq) {  // bounds and record read together; a slot outside the bucket goes to the spare
@@ -1249,31 +1289,12 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
             own[((pos >= lo) & (pos < hi)) ? pos : N] = r;
           }
         }
-        for (int qb = 0; qb < nc; qb += kWave / kCpRecs) {
-          const int qi = qb + (lane >> kCpShift), part = lane & (kCpRecs - 1);
-          if (qi < nc) {
-            const uint32_t ent = fc[qi];
-            const int dv = (int)(ent >> 20), pos = (int)(ent & 0xFFFFFu) * kCpRecs + part;
-            const int lo = cp_off[dv];
-            const Rec r = cbuf[dv * kCpRecs + part];
-            cp[pos >= lo ? pos : E] = r;
-          }
-        }
         wave_lds_fence();
         // a block begun in this chunk but not complete: staged for later chunks
         if (ko == kRoleTail) obuf[d * kOwnRecs + (po & (kOwnRecs - 1))] = ro;
-        if (k0 == kRoleTail) cbuf[dx0 * kCpRecs + (s0 & (kCpRecs - 1))] = r0;
-        if (k1 == kRoleTail) cbuf[dx1 * kCpRecs + (s1 & (kCpRecs - 1))] = r1;
-        if (lane == 0) fqn = fcn = 0;
+        if (lane == 0) fqn = 0;
       }
       a = an;
-    }
-    if (kStage) {  // copy blocks still open (a bucket ends short of its reserve)
-      wave_lds_fence();
-      for (int e = lane; e < D; e += kWave) {
-        const int end = cfill[e], lo = max(end & ~(kCpRecs - 1), cp_off[e]);
-        for (int pos = lo; pos < end; ++pos) cp[pos] = cbuf[e * kCpRecs + (pos & (kCpRecs - 1))];
-      }
     }
   }
   wave_lds_fence();
@@ -1860,8 +1881,7 @@ int mem_pass_join(MemPass &M, hipStream_t stream) {
 // Dynamic LDS of fast_intervals: per-device offsets and fill pointers, and
 // with staged stores the open blocks of every device's buckets.
 size_t intervals_lds(int D, bool stage) {
-  return (stage ? (size_t)D * (kOwnRecs + kCpRecs) * sizeof(Rec) : 0) +
-         (size_t)(4 * D + 2 + 4 * kWave + 2) * sizeof(int);
+  return (stage ? (size_t)D * kOwnRecs * sizeof(Rec) : 0) + (size_t)(4 * D + 2 + 2 * kWave + 1) * sizeof(int);
 }
 
 // Residency intervals, then peaks, for the nb candidates of one chunk (their
@@ -2155,9 +2175,15 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
     SsTimingRec *tt = nullptr;
     tt = ss_timing_start(SS_KERNEL_TRANSPOSE, stream);
     if (N > 0) {  // op-major -> candidates' rows for the memory passes
-      const dim3 tg((unsigned)((nb + 63) / 64), (unsigned)((N + 63) / 64));
-      hipLaunchKernelGGL(transpose_tiles<uint32_t>, tg, dim3(256), 0, stream, static_cast<const uint32_t *>(finT),
-                         (int64_t)N, nb, nb, fin);
+      if (N % 4 == 0 && nb % 4 == 0) {  // scratch buffers are 256-byte aligned
+        const dim3 tg((unsigned)((nb + 63) / 64), (unsigned)((N + 64 * kStripTiles - 1) / (64 * kStripTiles)));
+        hipLaunchKernelGGL(transpose_u32_strips, tg, dim3(256), 0, stream, static_cast<const uint32_t *>(finT),
+                           (int64_t)N, nb, nb, fin);
+      } else {
+        const dim3 tg((unsigned)((nb + 63) / 64), (unsigned)((N + 63) / 64));
+        hipLaunchKernelGGL(transpose_tiles<uint32_t>, tg, dim3(256), 0, stream, static_cast<const uint32_t *>(finT),
+                           (int64_t)N, nb, nb, fin);
+      }
     }
     ss_timing_stop(tt, stream);
     if (!check("transpose launch")) break;
