@@ -200,9 +200,12 @@ int ss_gmg_info(const ss_gmg *g, int64_t *n_ops, int64_t *n_dev, int64_t *n_req)
  * It takes stream-ordered scratch on hip_stream, for the duration of the
  * work, from the library's memory pool for g's device, which keeps that
  * memory for later calls (for a fixed workload, calls after the first
- * allocate no device memory; see ss_release_cached_memory).  Its chunk sizes
- * follow the memory the device has free at the call; when the pool runs
- * short, the call waits for hip_stream's earlier work, returns its idle
+ * allocate no device memory; see ss_release_cached_memory).  With index-order
+ * dispatch its scratch is at most the preferred workspace
+ * (ss_simulate_workspace_size) and at most seven eighths of the memory the
+ * call can get at its start (free device memory, the pool's unused memory and
+ * idle blocks); smaller memory means smaller chunks.  When the pool runs
+ * short anyway, the call waits for hip_stream's earlier work, returns its idle
  * memory to the driver and retries once, then halves its chunks.  A caller that
  * must own that memory passes it to ss_simulate_batch_ws instead (sized with
  * ss_simulate_workspace_size).  B = 0 is a no-op.  Results are bit-identical

@@ -158,7 +158,7 @@ hipError_t ss_pool_malloc(void **p, size_t bytes, hipMemPool_t pool, hipStream_t
   return e;
 }
 
-int64_t ss_scratch_budget(int device, hipMemPool_t pool, int64_t cap) {
+int64_t ss_scratch_budget(int device, hipMemPool_t pool, int64_t cap, int eighths) {
   size_t free_b = 0, total_b = 0;
   if (hipMemGetInfo(&free_b, &total_b) != hipSuccess) {
     (void)hipGetLastError();
@@ -176,7 +176,7 @@ int64_t ss_scratch_budget(int device, hipMemPool_t pool, int64_t cap) {
     for (const IdleScratch &b : g_idle[device]) idle += b.bytes;
   }
   const uint64_t avail = (uint64_t)free_b + (reserved > used ? reserved - used : 0) + idle;
-  return std::min<int64_t>(cap, (int64_t)(avail / 4 * 3));
+  return std::min<int64_t>(cap, (int64_t)(avail / 8 * (uint64_t)eighths));
 }
 
 hipError_t ss_scratch_get(int device, hipMemPool_t pool, size_t bytes, hipStream_t stream, SsScratch *s) {

@@ -49,6 +49,7 @@
 #include <climits>
 #include <cstdlib>
 #include <cstring>
+#include <type_traits>
 
 #include "ss_internal.h"
 
@@ -57,9 +58,10 @@ namespace {
 constexpr int kWave = 64;
 constexpr uint32_t kInf32 = 0xFFFFFFFFu;
 constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per chunk
-// index-order 32-bit path: larger chunks (fewer pipeline fills and drains of
-// the memory passes), within the memory the call can get (ss_scratch_budget)
-// and halved while the scratch does not fit
+// index-order 32-bit path: the chunk buffers of its preferred layout (larger
+// chunks mean fewer pipeline fills and drains of the memory passes); the
+// whole layout, record sets included, is then fitted to the memory the call
+// can get (ss_scratch_budget) and halved while it does not fit
 constexpr int64_t kFastScratchBudget = int64_t(96) << 30;
 constexpr int64_t kRecordBudget = int64_t(32) << 30;   // sizes the sub-chunks (record bytes of about two sets)
 constexpr int kPeakBlocksPerCU = 8;  // fast_peaks holds about 19.5 KB of LDS
@@ -1068,8 +1070,10 @@ struct IvSucc {  // device, finish and rank of the first two successors (with po
 //          that completes the block (close) queues it for a cooperative write
 //   direct its block lies inside this chunk's run and is complete: stored
 //   tail   its block begins in this chunk and is not complete: staged
-// Copies are stored directly: staging them as well (a block per destination
-// device) cost more occupancy than it saved.
+// Copies (kStageCp) are staged the same way, a block per destination device,
+// when the pass runs alone; beside the peak pass on a second stream they are
+// stored directly, since there the LDS of their blocks costs more occupancy
+// than the whole blocks save.
 constexpr int kRoleNone = 0, kRoleDirect = 1, kRoleOpen = 2, kRoleClose = 6, kRoleTail = 8;
 
 template <int kShift>
@@ -1084,9 +1088,10 @@ __device__ __forceinline__ int line_role(int p, int first, int last, int end) {
   return done ? kRoleDirect : kRoleTail;
 }
 
-// Staged blocks: own records in 32-byte pairs (a smaller stage leaves more
-// waves per CU, which this kernel needs).
+// Staged blocks: records in 32-byte pairs (a smaller stage leaves more waves
+// per CU, which this kernel needs).
 constexpr int kOwnShift = 1, kOwnRecs = 1 << kOwnShift;
+constexpr int kCpShift = 1, kCpRecs = 1 << kCpShift;
 
 // kGivenRanks: the rank table already holds every op's rank on its device
 // (dispatch order), pass A only counts.  kShiftLinks (with kFast): link
@@ -1096,7 +1101,7 @@ constexpr int kOwnShift = 1, kOwnRecs = 1 << kOwnShift;
 // holds every candidate's arrival per predecessor edge (rows of E, like fin):
 // an own output is kept until its last remote arrival, a copy is allocated at
 // its transfer's start (arrival minus estimate).
-template <bool kFast, bool kGivenRanks, bool kShiftLinks, bool kPorts>
+template <bool kFast, bool kGivenRanks, bool kShiftLinks, bool kPorts, bool kStageCp>
 __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const uint8_t *__restrict__ P,
                                                         const uint32_t *__restrict__ fin, int64_t j0,
                                                         Rec *__restrict__ own_all, Rec *__restrict__ cp_all,
@@ -1105,18 +1110,23 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
                                                         const uint32_t *__restrict__ arr) {
   // LDS (dynamic, sized by the device count): bucket offsets and fill
   // pointers; with staged stores (kFast with index ranks) also the open block
-  // of every device's own bucket and the queue of complete blocks
+  // of every device's own bucket (and copy bucket) and the queues of complete
+  // blocks
   constexpr bool kStage = kFast && !kGivenRanks;
+  constexpr bool kCpSt = kStage && kStageCp;
   extern __shared__ __align__(16) unsigned char iv_lds[];
   const int Dv = G.n_dev;
   Rec *obuf = reinterpret_cast<Rec *>(iv_lds);                           // [D][kOwnRecs]
-  int *own_off = reinterpret_cast<int *>(obuf + (kStage ? kOwnRecs * Dv : 0));  // [D+1]
+  Rec *cbuf = obuf + (kStage ? kOwnRecs * Dv : 0);                       // [D][kCpRecs]
+  int *own_off = reinterpret_cast<int *>(cbuf + (kCpSt ? kCpRecs * Dv : 0));  // [D+1]
   int *cp_off = own_off + Dv + 1;                                          // [D+1]
   int *cfill = cp_off + Dv + 1;                                            // [D] next copy slot
   int *base = cfill + Dv;  // [D] ops counted so far; with staging then the next own position
   int *nocopy = base + Dv;                                                 // [64]
   uint32_t *fq = reinterpret_cast<uint32_t *>(nocopy + kWave);  // [64] own blocks to write
-  int &fqn = *reinterpret_cast<int *>(fq + kWave);
+  uint32_t *fc = fq + kWave;                                    // [128] copy blocks to write
+  int &fqn = *reinterpret_cast<int *>(fc + (kCpSt ? 2 * kWave : 0));
+  int &fcn = *(&fqn + 1);
   const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops], K = G.n_link;
   const int lane = threadIdx.x;
   const int64_t j = blockIdx.x, c = j0 + j;
@@ -1169,7 +1179,7 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
   }
   if (kStage) {
     for (int d = lane; d < D; d += kWave) base[d] = own_off[d];
-    if (lane == 0) fqn = 0;
+    if (lane == 0) fqn = fcn = 0;
   }
   __syncthreads();  // also orders the rank-table stores before the loads below
   if (!kFast) {
@@ -1244,8 +1254,12 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       const bool c0 = act && has0 && !loc0 && a.b != 0;
       const bool c1 = act && has1 && !loc1 && !same && a.b != 0;
       int *const f0 = c0 ? &cfill[sc.dx0] : &nocopy[lane], *const f1 = c1 ? &cfill[sc.dx1] : &nocopy[lane];
-      int qo = 0;
-      if (kStage) {  // first position of the device's own run in this chunk
+      int qo = 0, q0 = 0, q1 = 0;
+      if (kStage) {  // first position of each destination's run in this chunk
+        if (kCpSt) {
+          q0 = *f0;
+          q1 = *f1;
+        }
         qo = base[d];  // d is valid in every lane (inactive lanes repeat the last op)
         atomicAdd(&base[d], act ? 1 : 0);
       }
@@ -1259,23 +1273,38 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       const uint32_t st0 = kPorts ? T0 - X0 : a.f, st1 = kPorts ? T1 - X1 : a.f;  // transfer starts
       const Rec r0 = Rec{st0, hi0, a.b, (uint32_t)max((int)ra0 - 3, 0) << 16 | (ry0 + 1)};
       const Rec r1 = Rec{st1, sc.fx1, a.b, (uint32_t)max((int)sc.rx1 - 3, 0) << 16 | (sc.rx1 + 1)};
+      const uint32_t dx0 = sc.dx0, dx1 = sc.dx1;
       sc = load_succ(an, vn);  // the next chunk's successors, in flight during the stores
       if (!kStage) {
         own[act ? po : N] = ro;
         cp[c0 ? s0 : E] = r0;
         cp[c1 ? s1 : E] = r1;
       } else {
-        if (c0) cp[s0] = r0;
-        if (c1) cp[s1] = r1;
+        if (!kCpSt) {
+          if (c0) cp[s0] = r0;
+          if (c1) cp[s1] = r1;
+        }
         wave_lds_fence();
-        // the device's positions in this chunk form one run [first, last]
+        // each destination's positions in this chunk form one run [first, last]
         const int eo = base[d] - 1, bo = own_off[d + 1];
         const int ko = act ? line_role<kOwnShift>(po, qo, eo, bo) : kRoleNone;
-        // a block complete inside this chunk: stored directly
+        int k0 = kRoleNone, k1 = kRoleNone;
+        if (kCpSt) {
+          const int e0 = *f0 - 1, e1 = *f1 - 1;
+          k0 = c0 ? line_role<kCpShift>(s0, q0, e0, INT_MAX) : kRoleNone;
+          k1 = c1 ? line_role<kCpShift>(s1, q1, e1, INT_MAX) : kRoleNone;
+        }
+        // blocks complete inside this chunk: stored directly
         if (ko == kRoleDirect) own[po] = ro;
+        if (k0 == kRoleDirect) cp[s0] = r0;
+        if (k1 == kRoleDirect) cp[s1] = r1;
         // the block open since earlier chunks: staged, and queued once complete
         if (ko & kRoleOpen) obuf[d * kOwnRecs + (po & (kOwnRecs - 1))] = ro;
+        if (k0 & kRoleOpen) cbuf[dx0 * kCpRecs + (s0 & (kCpRecs - 1))] = r0;
+        if (k1 & kRoleOpen) cbuf[dx1 * kCpRecs + (s1 & (kCpRecs - 1))] = r1;
         if (ko == kRoleClose) fq[atomicAdd(&fqn, 1)] = d << 20 | (uint32_t)(po >> kOwnShift);
+        if (k0 == kRoleClose) fc[atomicAdd(&fcn, 1)] = dx0 << 20 | (uint32_t)(s0 >> kCpShift);
+        if (k1 == kRoleClose) fc[atomicAdd(&fcn, 1)] = dx1 << 20 | (uint32_t)(s1 >> kCpShift);
         wave_lds_fence();
         // write the queued blocks, adjacent lanes to adjacent records
         const int nq = fqn;
@@ -1289,12 +1318,34 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
             own[((pos >= lo) & (pos < hi)) ? pos : N] = r;
           }
         }
+        if (kCpSt) {
+          const int nc = fcn;
+          for (int qb = 0; qb < nc; qb += kWave / kCpRecs) {
+            const int qi = qb + (lane >> kCpShift), part = lane & (kCpRecs - 1);
+            if (qi < nc) {
+              const uint32_t ent = fc[qi];
+              const int dv = (int)(ent >> 20), pos = (int)(ent & 0xFFFFFu) * kCpRecs + part;
+              const int lo = cp_off[dv];
+              const Rec r = cbuf[dv * kCpRecs + part];
+              cp[pos >= lo ? pos : E] = r;
+            }
+          }
+        }
         wave_lds_fence();
         // a block begun in this chunk but not complete: staged for later chunks
         if (ko == kRoleTail) obuf[d * kOwnRecs + (po & (kOwnRecs - 1))] = ro;
-        if (lane == 0) fqn = 0;
+        if (k0 == kRoleTail) cbuf[dx0 * kCpRecs + (s0 & (kCpRecs - 1))] = r0;
+        if (k1 == kRoleTail) cbuf[dx1 * kCpRecs + (s1 & (kCpRecs - 1))] = r1;
+        if (lane == 0) fqn = fcn = 0;
       }
       a = an;
+    }
+    if (kCpSt) {  // copy blocks still open (a bucket ends short of its reserve)
+      wave_lds_fence();
+      for (int e = lane; e < D; e += kWave) {
+        const int end = cfill[e], lo = max(end & ~(kCpRecs - 1), cp_off[e]);
+        for (int pos = lo; pos < end; ++pos) cp[pos] = cbuf[e * kCpRecs + (pos & (kCpRecs - 1))];
+      }
     }
   }
   wave_lds_fence();
@@ -1880,8 +1931,9 @@ int mem_pass_join(MemPass &M, hipStream_t stream) {
 
 // Dynamic LDS of fast_intervals: per-device offsets and fill pointers, and
 // with staged stores the open blocks of every device's buckets.
-size_t intervals_lds(int D, bool stage) {
-  return (stage ? (size_t)D * kOwnRecs * sizeof(Rec) : 0) + (size_t)(4 * D + 2 + 2 * kWave + 1) * sizeof(int);
+size_t intervals_lds(int D, bool stage, bool stage_cp) {
+  return (stage ? (size_t)D * kOwnRecs * sizeof(Rec) : 0) + (stage_cp ? (size_t)D * kCpRecs * sizeof(Rec) : 0) +
+         (size_t)(4 * D + 2 + 2 * kWave + (stage_cp ? 2 * kWave : 0) + 2) * sizeof(int);
 }
 
 // Residency intervals, then peaks, for the nb candidates of one chunk (their
@@ -1904,23 +1956,30 @@ int memory_passes(const ss_gmg *g, MemPass &M, const uint8_t *Pc, const uint32_t
     if (arr && (!M.iv_fast || given_ranks))
       return ss_set_error(SS_ERR_UNSUPPORTED, "port arrivals need the branch-free interval writer");
     const bool shift = G.link_shift >= 0;
+    // copy records staged when this pass runs alone (one stream)
+    const bool scp = M.single;
+    auto staged = [&](auto shift_c, auto ports_c) -> const void * {
+      constexpr bool kS = decltype(shift_c)::value, kP = decltype(ports_c)::value;
+      return scp ? reinterpret_cast<const void *>(&fast_intervals<true, false, kS, kP, true>)
+                 : reinterpret_cast<const void *>(&fast_intervals<true, false, kS, kP, false>);
+    };
+    using T_ = std::true_type;
+    using F_ = std::false_type;
     const void *fn =
-        arr ? (shift ? reinterpret_cast<const void *>(&fast_intervals<true, false, true, true>)
-                     : reinterpret_cast<const void *>(&fast_intervals<true, false, false, true>))
+        arr ? (shift ? staged(T_(), T_()) : staged(F_(), T_()))
         : M.iv_fast
-            ? (given_ranks ? (shift ? reinterpret_cast<const void *>(&fast_intervals<true, true, true, false>)
-                                    : reinterpret_cast<const void *>(&fast_intervals<true, true, false, false>))
-                           : (shift ? reinterpret_cast<const void *>(&fast_intervals<true, false, true, false>)
-                                    : reinterpret_cast<const void *>(&fast_intervals<true, false, false, false>)))
-            : (given_ranks ? reinterpret_cast<const void *>(&fast_intervals<false, true, false, false>)
-                           : reinterpret_cast<const void *>(&fast_intervals<false, false, false, false>));
+            ? (given_ranks ? (shift ? reinterpret_cast<const void *>(&fast_intervals<true, true, true, false, false>)
+                                    : reinterpret_cast<const void *>(&fast_intervals<true, true, false, false, false>))
+                           : (shift ? staged(T_(), F_()) : staged(F_(), F_())))
+            : (given_ranks ? reinterpret_cast<const void *>(&fast_intervals<false, true, false, false, false>)
+                           : reinterpret_cast<const void *>(&fast_intervals<false, false, false, false, false>));
     const uint8_t *vi = violation;
     Rec *own = M.own[set], *cp = M.cp[set];
     int32_t *meta = M.meta[set];
     void *args[] = {const_cast<GmgView *>(&G), const_cast<uint8_t **>(&Pc), const_cast<uint32_t **>(&fin),
                     &j0, &own, &cp, &meta, &rank, &vi, const_cast<uint32_t **>(&arr)};
     // the branch-free writer with index ranks stages its stores
-    const size_t lds = intervals_lds((int)g->n_dev, M.iv_fast && !given_ranks);
+    const size_t lds = intervals_lds((int)g->n_dev, M.iv_fast && !given_ranks, M.iv_fast && !given_ranks && scp);
     err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (err != hipSuccess) return hip_fail(err, "hipFuncSetAttribute");
     SsTimingRec *ti = ss_timing_start(SS_KERNEL_INTERVALS, stream);
@@ -2041,13 +2100,37 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
     chunk = std::min<int64_t>(chunk, int64_t(65535) * 64);  // transpose grids index 64-candidate tiles in y
     return plan_of(chunk, std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand)));
   };
-  const FastPlan pmin = plan_of(kWave, 1);
+  const FastPlan pmin = plan_of(kWave, 1), pref = plan_for_budget(kFastScratchBudget);
+  // the largest layout within `bytes`: the preferred chunk with sub-chunks as
+  // large as fit (down to a sixteenth of the chunk), else smaller chunks (by
+  // whole rounds, then halves), down to the smallest layout
+  auto plan_fit = [&](int64_t bytes) {
+    if ((int64_t)pref.total <= bytes) return pref;
+    int64_t chunk = pref.chunk;
+    for (;;) {
+      const int64_t lo0 = chunk > kWave ? std::max<int64_t>(1, std::min<int64_t>(pref.sub, chunk / 16)) : 1;
+      if ((int64_t)plan_of(chunk, lo0).total <= bytes) {
+        int64_t lo = lo0, hi = std::max<int64_t>(lo0, pref.sub);  // the largest sub-chunk cap that fits
+        while (lo < hi) {
+          const int64_t mid = lo + (hi - lo + 1) / 2;
+          if ((int64_t)plan_of(chunk, mid).total <= bytes)
+            lo = mid;
+          else
+            hi = mid - 1;
+        }
+        return plan_of(chunk, lo);
+      }
+      if (chunk <= kWave) return plan_of(chunk, 1);
+      chunk = chunk > round ? chunk - round : std::max<int64_t>(kWave, chunk / 2 / kWave * kWave);
+    }
+  };
+  // the pool path's budget: up to the preferred layout, within seven eighths
+  // of the memory the call can get now
+  auto pool_budget = [&] { return ss_scratch_budget(g->device, g->pool, (int64_t)pref.total, 7); };
   if (W.query) {
     W.need_min = pmin.total;
-    const FastPlan pp = plan_for_budget(kFastScratchBudget);
-    W.need_pref = pp.total;
-    // the pool path starts from the budget the device's memory allows now
-    const FastPlan pq = W.single ? pp : plan_for_budget(ss_scratch_budget(g->device, g->pool, kFastScratchBudget));
+    W.need_pref = pref.total;
+    const FastPlan pq = W.single ? pref : plan_fit(pool_budget());
     W.chunk = pq.chunk;
     W.sub = pq.sub;
     return SS_OK;
@@ -2062,25 +2145,15 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
       return ss_set_error(SS_ERR_INVALID_ARG, "workspace of " + std::to_string(W.bytes) +
                                                    " bytes is smaller than this call's minimum of " +
                                                    std::to_string(pmin.total));
-    pl = plan_for_budget(kFastScratchBudget);
-    int64_t chunk = pl.chunk, sub_cap = pl.sub;
-    while (pl.total > W.bytes) {
-      if (sub_cap > 1 && plan_of(chunk, 1).total <= W.bytes) {
-        sub_cap = std::max<int64_t>(1, sub_cap / 2);  // fewer records first
-      } else {
-        chunk = std::max<int64_t>(kWave, (chunk / 2) / kWave * kWave);
-        sub_cap = std::min(sub_cap, chunk);
-      }
-      pl = plan_of(chunk, sub_cap);
-    }
+    pl = plan_fit((int64_t)W.bytes);
     scratch = W.ptr;
   } else {
-    // the largest chunk within the scratch budget; when its scratch does not
-    // fit in the device's free memory, half the budget (down to one round)
-    for (int64_t budget = ss_scratch_budget(g->device, g->pool, kFastScratchBudget);; budget /= 2) {
-      pl = plan_for_budget(budget);
+    // the largest layout within the budget; while its scratch cannot be
+    // had, half the budget (down to the smallest layout)
+    for (int64_t budget = pool_budget();; budget /= 2) {
+      pl = plan_fit(budget);
       err = ss_scratch_get(g->device, g->pool, pl.total, stream, &scr);
-      if (err != hipErrorOutOfMemory || pl.chunk <= std::min<int64_t>(round, B)) break;
+      if (err != hipErrorOutOfMemory || pl.total <= pmin.total) break;
     }
     if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
     scratch = scr.p;

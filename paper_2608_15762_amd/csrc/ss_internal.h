@@ -137,12 +137,12 @@ struct SsScratch {
   size_t bytes = 0;
 };
 hipError_t ss_scratch_get(int device, hipMemPool_t pool, size_t bytes, hipStream_t stream, SsScratch *s);
-// A scratch budget for one call: `cap`, or three quarters of the memory the
-// call could get (the device's free memory, the pool's reserved but unused
-// memory and the device's idle scratch blocks) when that is less.  Taken at
-// each call, so a budget cut by memory that others held grows back once
-// they release it.
-int64_t ss_scratch_budget(int device, hipMemPool_t pool, int64_t cap);
+// A scratch budget for one call: `cap`, or `eighths` eighths of the memory
+// the call could get (the device's free memory, the pool's reserved but
+// unused memory and the device's idle scratch blocks) when that is less.
+// Taken at each call, so a budget cut by memory that others held grows back
+// once they release it.
+int64_t ss_scratch_budget(int device, hipMemPool_t pool, int64_t cap, int eighths = 6);
 hipError_t ss_scratch_put(int device, SsScratch *s, hipStream_t stream);
 // A buffer from the device's pool, ready for use on any stream when it returns
 // (allocated on `stream`, which is synchronised), and its release.
