@@ -142,3 +142,32 @@ def test_workspace_reused_across_calls_and_sizes(dev):
         P = synth.placements(g, 3, b0, nb)
         ref = oracle.simulate_batch(g, P, n_threads=8)
         assert_same(run(h, P, dev, workspace=ws), ref, f"{nb} candidates")
+
+
+def test_pool_scratch_fits_the_memory_left(dev):
+    """With most of the device's memory held by the caller, a call sizes its
+    own scratch to what is left: ss_simulate_chunking reports smaller
+    memory-pass sub-chunks than with the memory free, and the results, computed
+    in those smaller pieces, still equal the oracle's."""
+    g = synth.build_gmg(3)
+    h = ss.Gmg(g)
+    nb = 8192
+    P = synth.placements(g, 3, 0, nb)
+    ref = oracle.simulate_batch(g, P, n_threads=8)
+    ss.release_cached_memory()
+    torch.cuda.empty_cache()
+    roomy = ss.chunking(h, nb)
+    _, pref = ss.workspace_size(h, nb)
+    free, _ = torch.cuda.mem_get_info()
+    left = pref // 2 + 3 * g.n_ops * nb  # about half the preferred scratch, plus the test's own tensors
+    print(f"roomy chunking {roomy}, preferred scratch {pref / 1e9:.2f} GB, holding {(free - left) / 1e9:.1f} GB",
+          flush=True)
+    hold = torch.empty(free - left, dtype=torch.uint8, device=dev)
+    try:
+        tight = ss.chunking(h, nb)
+        print(f"tight chunking {tight}", flush=True)
+        assert tight[0] <= roomy[0] and tight[1] < roomy[1], (roomy, tight)
+        assert_same(run(h, P, dev), ref, "scratch fitted to the memory left")
+    finally:
+        del hold
+        torch.cuda.empty_cache()
