@@ -444,6 +444,18 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     int64_t max_outdeg = 0;
     for (int64_t v = 0; v < N; ++v) max_outdeg = std::max<int64_t>(max_outdeg, outdeg[v]);
     const int64_t lwords = (D + 31) / 32;
+    // 32-bit byte sums in the peak pass: with every size divided by their
+    // common power of two, what can be live on one device at once (each output
+    // and at most one copy per consumer edge) sums below 2^32
+    int32_t pshift = 0, pnarrow = 0;
+    if (time32) {
+      uint64_t any_bits = 0;
+      for (int64_t v = 0; v < N; ++v) any_bits |= (uint64_t)d->out_bytes[v];
+      pshift = any_bits ? __builtin_ctzll(any_bits) : 0;
+      i128 total = 0;
+      for (int64_t v = 0; v < N; ++v) total += (i128)(d->out_bytes[v] >> pshift) * (1 + outdeg[v]);
+      pnarrow = total < ((i128)1 << 32) ? 1 : 0;
+    }
     const int64_t meta_stride = std::max<int64_t>(128, (N + 63) / 64 * 64 + 64);  // two blocks of 64 past any op
     if (time32) {
       meta.assign((size_t)kOpMetaFields * meta_stride, 0);
@@ -643,6 +655,8 @@ extern "C" int ss_gmg_load(const ss_gmg_desc *d, ss_gmg **out) {
     V.link_bits = lbits.empty() ? nullptr : reinterpret_cast<const uint32_t *>(base + o_lbits);
     V.link_words = (int32_t)lwords;
     V.bytes32 = reinterpret_cast<const uint32_t *>(base + o_b32);
+    V.peak_shift = pshift;
+    V.peak_narrow = pnarrow;
     V.succ2 = succ2.empty() ? nullptr : reinterpret_cast<const uint32_t *>(base + o_succ2);
     V.succ2_pe = succ2_pe.empty() ? nullptr : reinterpret_cast<const uint32_t *>(base + o_succ2_pe);
     V.link_grp = lgrp.empty() ? nullptr : reinterpret_cast<const uint8_t *>(base + o_lgrp);

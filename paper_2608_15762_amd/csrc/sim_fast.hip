@@ -64,7 +64,7 @@ constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per c
 // can get (ss_scratch_budget) and halved while it does not fit
 constexpr int64_t kFastScratchBudget = int64_t(96) << 30;
 constexpr int64_t kRecordBudget = int64_t(32) << 30;   // sizes the sub-chunks (record bytes of about two sets)
-constexpr int kPeakBlocksPerCU = 8;  // fast_peaks holds about 19.5 KB of LDS
+constexpr int kPeakBlocksPerCU = 8;  // fast_peaks: 228 registers, 12 or 16 KB of LDS per wave
 
 __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
 __device__ __forceinline__ int64_t imax64(int64_t a, int64_t b) { return a > b ? a : b; }
@@ -1556,13 +1556,16 @@ constexpr int kAggCap = 512;   // own allocations per device for the aggregate m
 constexpr int kAggCopies = 1024;
 constexpr int kHardCap = 128;  // events of hard gaps per device
 
+// Per-gap byte sums: int64 in general; u32 when the loader proved that every
+// byte that can be live on one device at once sums below 2^32 once all sizes
+// are divided by their common power of two (GmgView::peak_narrow): the sums
+// are then exact modulo 2^32 and every value compared lies in [0, 2^32).
+template <class Acc>
 struct AggLds {
   uint32_t S[kAggCap];        // own starts
-  uint32_t ob[kAggCap];       // own bytes
-  int64_t dg[kAggCap + 1];    // per gap: copies allocated (+ own_{g-1}), then L[g]
-  int64_t fg[kAggCap + 1];    // per gap: freed bytes
+  Acc dg[kAggCap + 1];        // per gap: copies allocated (+ own_{g-1}), then L[g]
+  Acc fg[kAggCap + 1];        // per gap: freed bytes, then the live bytes at the gap's start
   uint32_t cg[kAggCopies];    // per copy: allocation gap << 16 | free gap
-  uint16_t og[kAggCap];       // per own allocation: free gap (0xFFFF: never freed)
   uint8_t hard[kAggCap + 1];
   uint32_t ht[kHardCap], hb[kHardCap], hx[kHardCap];  // collected events: time, bytes, gap << 1 | is_alloc
   int hn;
@@ -1594,22 +1597,46 @@ __device__ __forceinline__ void load_cp(Rec (&rc)[kCpPre], const DevSpan &s, int
   for (int q = 0; q < kCpPre; ++q) rc[q] = s.cp[min(q * kWave + lane, max(s.nc - 1, 0))];
 }
 
+__device__ __forceinline__ void lds_add(uint32_t *p, uint32_t v) { atomicAdd(p, v); }
+__device__ __forceinline__ void lds_add(int64_t *p, int64_t v) {
+  atomicAdd(reinterpret_cast<unsigned long long *>(p), (unsigned long long)v);
+}
+__device__ __forceinline__ uint32_t wave_max_acc(uint32_t x) {
+  for (int o = kWave / 2; o >= 1; o >>= 1) x = umax32(x, (uint32_t)__shfl_xor((int)x, o, kWave));
+  return x;
+}
+__device__ __forceinline__ int64_t wave_max_acc(int64_t x) {
+  for (int o = kWave / 2; o >= 1; o >>= 1) x = imax64(x, __shfl_xor(x, o, kWave));
+  return x;
+}
+__device__ __forceinline__ uint32_t wave_scan_acc(uint32_t x, int lane) {
+  return (uint32_t)wave_incl_scan32((int)x, lane);  // modulo 2^32
+}
+__device__ __forceinline__ int64_t wave_scan_acc(int64_t x, int lane) { return wave_incl_scan64(x, lane); }
+
 // Peak of one device whose records the caller loaded into ro and rc (it fits
 // the LDS arrays: agg_fits).  Once a record array has been used for the last
 // time it is refilled with the records of the next device (nxt, when pf), so
-// those loads overlap the rest of this device's work.  Returns -1 if the hard
-// events overflow (the caller then uses device_peak).
+// those loads overlap the rest of this device's work; the own sizes (and
+// the gaps of the own frees) stay in registers past that.  Sizes are divided
+// by 2^sh (kNarrow).  Returns -1 if the hard events overflow (the caller then
+// uses device_peak).
+template <bool kNarrow>
 __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (&rc)[kCpPre], const DevSpan &nxt,
-                                   bool pf, AggLds &A, int lane) {
+                                   bool pf, AggLds<typename std::conditional<kNarrow, uint32_t, int64_t>::type> &A,
+                                   int lane, int sh) {
+  using Acc = typename std::conditional<kNarrow, uint32_t, int64_t>::type;
   const int m = cur.m, nc = cur.nc;
-  // own k: start, bytes, and its allocation as the opening value of gap k + 1
+  auto size_of = [&](uint32_t z) -> uint32_t { return kNarrow ? z >> sh : z; };
+  // own k: start, and its allocation as the opening value of gap k + 1
+  uint32_t obr[kOwnPer];  // size of own k = q * 64 + lane
 #pragma unroll
   for (int q = 0; q < kOwnPer; ++q) {
     const int k = q * kWave + lane;
+    obr[q] = size_of(ro[q].z);
     if (k < m) {
       A.S[k] = ro[q].x;
-      A.ob[k] = ro[q].z;
-      A.dg[k + 1] = (int64_t)ro[q].z;
+      A.dg[k + 1] = (Acc)obr[q];
     }
     if (k <= m) {
       A.fg[k] = 0;
@@ -1621,9 +1648,6 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
     A.hn = 0;
   }
   wave_lds_fence();
-  auto add64 = [](int64_t *p, int64_t v) {
-    atomicAdd(reinterpret_cast<unsigned long long *>(p), (unsigned long long)v);
-  };
   // copies: allocation gap (window probes, four rows at a time), free gap exact
 #pragma unroll
   for (int q0 = 0; q0 < kCpPer; q0 += 4) {
@@ -1644,14 +1668,17 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
           if (!ok[q]) g[q] = gap_search<true>(A.S, m, r.x);
           const int gf = min((int)(r.w & 0xFFFFu), m);
           A.cg[i] = (uint32_t)g[q] << 16 | (uint32_t)gf;
-          add64(&A.dg[g[q]], (int64_t)r.z);
-          add64(&A.fg[gf], (int64_t)r.z);
+          lds_add(&A.dg[g[q]], (Acc)size_of(r.z));
+          lds_add(&A.fg[gf], (Acc)size_of(r.z));
         }
       }
     }
   }
   if (pf) load_cp(rc, nxt, lane);
-  // own frees: exact gap or window probes
+  // own frees: exact gap or window probes; the gap is kept (0xFFFF: never freed)
+  uint32_t ogr[kOwnPer / 2];  // u16 pairs: free gap of own q * 64 + lane in half q & 1 of word q / 2
+#pragma unroll
+  for (int q = 0; q < kOwnPer / 2; ++q) ogr[q] = 0xFFFFFFFFu;
 #pragma unroll
   for (int q0 = 0; q0 < kOwnPer; q0 += 4) {
     if (q0 * kWave < m) {
@@ -1669,12 +1696,11 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
         const int k = (q0 + q) * kWave + lane;
         if (k < m) {
           const Rec r = ro[q0 + q];
-          if (r.y == kInf32) {
-            A.og[k] = 0xFFFFu;
-          } else {
+          if (r.y != kInf32) {
             if (!ok[q]) g[q] = gap_search<false>(A.S, m, r.y);
-            A.og[k] = (uint16_t)g[q];
-            add64(&A.fg[g[q]], (int64_t)r.z);
+            const int half = 16 * ((q0 + q) & 1);
+            ogr[(q0 + q) >> 1] = (ogr[(q0 + q) >> 1] & ~(0xFFFFu << half)) | (uint32_t)g[q] << half;
+            lds_add(&A.fg[g[q]], (Acc)obr[q0 + q]);
           }
         }
       }
@@ -1682,13 +1708,13 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
   }
   if (pf) load_own(ro, nxt, lane);
   wave_lds_fence();
-  // L[g] = prefix of dg; P0 at own allocations, exact values of copy-only gaps.
-  // Every loop below runs a fixed number of rows (m < kAggCap, nc <= kAggCopies)
-  // with clamped, unconditional LDS loads, so that each row's loads overlap.
+  // L[g] = prefix of dg - fg.  Every loop below runs a fixed number of rows
+  // (m < kAggCap, nc <= kAggCopies) with clamped, unconditional LDS loads, so
+  // that each row's loads overlap.
   {
     const int n = m + 1, per = (n + kWave - 1) / kWave, lo = lane * per;
-    int64_t v[kOwnPer];
-    int64_t sacc = 0;
+    Acc v[kOwnPer];
+    Acc sacc = 0;
 #pragma unroll
     for (int t = 0; t < kOwnPer; ++t) {
       const int g = min(lo + t, n - 1);
@@ -1696,7 +1722,7 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
       if (t >= per || lo + t >= n) v[t] = 0;
       sacc += v[t];
     }
-    int64_t run = wave_incl_scan64(sacc, lane) - sacc;
+    Acc run = wave_scan_acc(sacc, lane) - sacc;
 #pragma unroll
     for (int t = 0; t < kOwnPer; ++t) {
       run += v[t];
@@ -1704,23 +1730,29 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
     }
   }
   wave_lds_fence();
-  int64_t best = 0;
-  int64_t bound[kOwnPer];  // per gap of this lane: L + frees when the gap holds copies and frees, else -1
+  // P0 at own allocations, exact values of copy-only gaps; the live bytes at
+  // each gap's start (after own g - 1) replace its frees in fg
+  Acc best = 0;
+  Acc bound[kOwnPer];  // per gap of this lane: L + frees when the gap holds copies and frees, else 0
 #pragma unroll
   for (int q = 0; q < kOwnPer; ++q) {
     const int g = q * kWave + lane, gc = min(g, m), gp = max(gc - 1, 0);
-    const int64_t L = A.dg[gc], F = A.fg[gc];
-    const int64_t prev = gc > 0 ? A.dg[gp] + (int64_t)A.ob[gp] : 0;
-    const int64_t obg = (int64_t)A.ob[min(gc, max(m - 1, 0))];
-    const int64_t copies = L - prev + F;
-    bound[q] = -1;
+    // size of own g - 1: the previous lane's, or lane 63's of the row before
+    const uint32_t up = (uint32_t)__shfl_up((int)obr[q], 1, kWave);
+    const uint32_t wrap = q > 0 ? (uint32_t)__shfl((int)obr[q > 0 ? q - 1 : 0], kWave - 1, kWave) : 0u;
+    const uint32_t ob_prev = lane > 0 ? up : wrap;
+    const Acc L = A.dg[gc], F = A.fg[gc];
+    const Acc prev = gc > 0 ? A.dg[gp] + (Acc)ob_prev : (Acc)0;
+    const Acc copies = L - prev + F;
+    bound[q] = 0;
     if (g <= m) {
-      if (g < m) best = imax64(best, L + obg);
-      if (copies > 0 && F == 0) best = imax64(best, L);  // copies only: all of them precede own g
+      if (g < m) best = best > L + (Acc)obr[q] ? best : L + (Acc)obr[q];
+      if (copies > 0 && F == 0) best = best > L ? best : L;  // copies only: all of them precede own g
       if (copies > 0 && F > 0) bound[q] = L + F;
+      A.fg[g] = prev;
     }
   }
-  for (int o = kWave / 2; o >= 1; o >>= 1) best = imax64(best, __shfl_xor(best, o, kWave));
+  best = wave_max_acc(best);
   bool any = false;
 #pragma unroll
   for (int q = 0; q < kOwnPer; ++q) {
@@ -1729,7 +1761,8 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
       any = true;
     }
   }
-  if (!__any(any)) return best;
+  auto widen = [&](Acc x) -> int64_t { return kNarrow ? (int64_t)x << sh : (int64_t)x; };
+  if (!__any(any)) return widen(best);
   wave_lds_fence();
   // collect the events of the hard gaps
   auto push = [&](uint32_t t, uint32_t b, uint32_t x) {
@@ -1757,17 +1790,17 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
         const int i = (q0 + q) * kWave + lane;
         if (i < nc && (ha[q] || hf[q])) {
           const Rec r = cur.cp[i];
-          if (ha[q]) push(r.x, r.z, (gg[q] >> 16) << 1 | 1u);
-          if (hf[q]) push(r.y, r.z, (gg[q] & 0xFFFFu) << 1);
+          if (ha[q]) push(r.x, size_of(r.z), (gg[q] >> 16) << 1 | 1u);
+          if (hf[q]) push(r.y, size_of(r.z), (gg[q] & 0xFFFFu) << 1);
         }
       }
     }
   }
 #pragma unroll
   for (int q = 0; q < kOwnPer; ++q) {
-    const int k = q * kWave + lane, kc = min(k, max(m - 1, 0));
-    const uint32_t gf = A.og[kc];
-    if (k < m && gf != 0xFFFFu && A.hard[gf]) push(cur.own[k].y, A.ob[k], gf << 1);
+    const int k = q * kWave + lane;
+    const uint32_t gf = (ogr[q >> 1] >> (16 * (q & 1))) & 0xFFFFu;
+    if (k < m && gf != 0xFFFFu && A.hard[gf]) push(cur.own[k].y, obr[q], gf << 1);
   }
   wave_lds_fence();
   const int hn = A.hn;
@@ -1779,33 +1812,33 @@ __device__ int64_t device_peak_agg(const DevSpan &cur, Rec (&ro)[kOwnPer], Rec (
     if (!(x & 1u)) continue;
     const int g = (int)(x >> 1);
     const uint32_t t = A.ht[e];
-    int64_t live = g > 0 ? A.dg[g - 1] + (int64_t)A.ob[g - 1] : 0;
+    Acc live = A.fg[g];
     for (int z = 0; z < hn; ++z) {
       const uint32_t xz = A.hx[z];
       if ((int)(xz >> 1) != g) continue;
       const uint32_t tz = A.ht[z];
       if (xz & 1u) {
-        if (tz < t || (tz == t && z <= e)) live += A.hb[z];
+        if (tz < t || (tz == t && z <= e)) live += (Acc)A.hb[z];
       } else if (tz <= t) {
-        live -= A.hb[z];
+        live -= (Acc)A.hb[z];
       }
     }
-    best = imax64(best, live);
+    best = best > live ? best : live;
   }
-  for (int o = kWave / 2; o >= 1; o >>= 1) best = imax64(best, __shfl_xor(best, o, kWave));
-  return best;
+  return widen(wave_max_acc(best));
 }
 
 // Blocks take candidates from a ticket counter (zero at launch) rather than
 // in a fixed stride: a block that starts late, or shares its CU with another
 // kernel's waves, takes fewer candidates instead of holding up the launch.
+template <bool kNarrow>
 __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0, int64_t nj,
                                                     const Rec *__restrict__ own_all, const Rec *__restrict__ cp_all,
                                                     const int32_t *__restrict__ meta, uint32_t *__restrict__ wk_all,
                                                     int64_t *__restrict__ wb_all, int64_t slot_cap,
                                                     uint32_t *__restrict__ ticket, int64_t *__restrict__ peak,
                                                     uint8_t *__restrict__ violation) {
-  __shared__ AggLds s_agg;
+  __shared__ AggLds<typename std::conditional<kNarrow, uint32_t, int64_t>::type> s_agg;
   const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops];
   const int lane = threadIdx.x;
   uint32_t *g_ak = wk_all + (int64_t)blockIdx.x * 2 * (slot_cap + 2);
@@ -1841,7 +1874,7 @@ __global__ __launch_bounds__(kWave) void fast_peaks(const GmgView G, int64_t j0,
       const bool pf = e + 1 < D && agg_fits(nxt);
       int64_t pk = 0;
       if (cur.m + cur.nc > 0 && agg_fits(cur)) {
-        pk = device_peak_agg(cur, ro, rc, nxt, pf, s_agg, lane);
+        pk = device_peak_agg<kNarrow>(cur, ro, rc, nxt, pf, s_agg, lane, G.peak_shift);
       } else if (pf) {
         load_own(ro, nxt, lane);
         load_cp(rc, nxt, lane);
@@ -1995,7 +2028,8 @@ int memory_passes(const ss_gmg *g, MemPass &M, const uint8_t *Pc, const uint32_t
     }
     if (M.it >= M.n_ticket) return ss_set_error(SS_ERR_DEVICE, "memory passes: more peak launches than counters");
     SsTimingRec *tm = ss_timing_start(SS_KERNEL_MEMORY, ps);
-    hipLaunchKernelGGL(fast_peaks, dim3((unsigned)std::min<int64_t>(nj, M.nslots)), dim3(kWave), 0, ps, G, j0, nj,
+    hipLaunchKernelGGL(G.peak_narrow ? fast_peaks<true> : fast_peaks<false>,
+                       dim3((unsigned)std::min<int64_t>(nj, M.nslots)), dim3(kWave), 0, ps, G, j0, nj,
                        static_cast<const Rec *>(own), static_cast<const Rec *>(cp),
                        static_cast<const int32_t *>(meta), M.wk, M.wb, M.slot_cap, M.ticket + M.it, peak, violation);
     ss_timing_stop(tm, ps);

@@ -51,6 +51,10 @@ struct GmgView {
   // 2^s devices), else -1
   int32_t link_shift;
   const uint32_t *bytes32;  // out_bytes as u32
+  // the peak pass's byte sums: sizes divided by 2^peak_shift (their common
+  // power of two) sum below 2^32 over every output and one copy per consumer
+  // edge (peak_narrow), so 32-bit sums are exact
+  int32_t peak_shift, peak_narrow;
   // first two successors of each op as u16 (0xFFFF: none), when no op has more
   const uint32_t *succ2;
   // with succ2 and fewer than 65,535 edges: the predecessor-edge index of each

@@ -270,6 +270,36 @@ def test_horizon_beyond_32_bits_takes_general_path(dev, monkeypatch):
         gpu_run(h, P, dev)
 
 
+@pytest.mark.parametrize("dispatch", ["index", "ready"])
+@pytest.mark.parametrize("case", ["wide", "scaled"])
+def test_byte_sums_beyond_32_bits(dev, monkeypatch, case, dispatch):
+    """Output sizes near 2^31 on the 32-bit time path.  "wide": odd sizes, so
+    no common power of two divides them and their sums pass 2^32 (the peak
+    pass keeps 64-bit sums); "scaled": multiples of 2^20 whose sums pass 2^32
+    but whose sums divided by 2^20 do not (32-bit sums of the scaled sizes).
+    Capacities at each device's 90th-percentile peak leave some candidates
+    feasible and make others overflow."""
+    g = synth.random_gmg(40 + (case == "scaled"), n_ops=300, n_dev=6, n_req=3, n_slices=3, n_link=2)
+    st = synth.Stream(41)
+    if case == "wide":
+        ob = [2 * st.uniform_int(1 << 29, (1 << 30) - 1) + 1 for _ in range(g.n_ops)]
+    else:
+        ob = [st.uniform_int(1, 1 << 11) << 20 for _ in range(g.n_ops)]
+    g.out_bytes = np.asarray(ob, np.int64)
+    g.bw = np.asarray([1 << 20, 1 << 21], np.int64)  # transfers of about a millisecond keep times in 32 bits
+    st2 = synth.Stream(43)
+    P = np.array([[st2.uniform_int(0, g.n_dev - 1) for _ in range(g.n_ops)] for _ in range(200)], np.uint8)
+    mode = oracle.INDEX_ORDER if dispatch == "index" else oracle.READY_ORDER
+    g.cap = np.full(g.n_dev, 1 << 62, np.int64)
+    roomy = oracle.simulate_batch(g, P, dispatch=mode)
+    assert roomy["peak"].max() > (1 << 32)
+    g.cap = np.percentile(roomy["peak"], 90, axis=0).astype(np.int64)
+    ref = oracle.simulate_batch(g, P, dispatch=mode)
+    assert 0 < (ref["violation"] == 1).sum() < len(P)
+    monkeypatch.setenv("SS_PATH", "fast")  # the 32-bit path must take this GMG
+    assert_same(gpu_run(ss.Gmg(g), P, dev, dispatch=dispatch), ref, label=f"byte sums beyond 2^32 ({case}, {dispatch})")
+
+
 # ------------------------------------------------------------------ selection
 def gpu_select(h, viol, key, slack, require_sla, dev):
     out = ss.select_best(h, torch.from_numpy(viol).to(dev), torch.from_numpy(key).to(dev),
