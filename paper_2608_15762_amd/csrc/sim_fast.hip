@@ -64,7 +64,7 @@ constexpr int64_t kScratchBudget = int64_t(32) << 30;  // schedule scratch per c
 // can get (ss_scratch_budget) and halved while it does not fit
 constexpr int64_t kFastScratchBudget = int64_t(96) << 30;
 constexpr int64_t kRecordBudget = int64_t(32) << 30;   // sizes the sub-chunks (record bytes of about two sets)
-constexpr int kPeakBlocksPerCU = 8;  // fast_peaks: 228 registers, 12 or 16 KB of LDS per wave
+constexpr int kPeakBlocksPerCU = 8;  // fast_peaks: 2 waves per SIMD (198 or 224 registers)
 
 __device__ __forceinline__ uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
 __device__ __forceinline__ int64_t imax64(int64_t a, int64_t b) { return a > b ? a : b; }
@@ -1609,8 +1609,12 @@ __device__ __forceinline__ int64_t wave_max_acc(int64_t x) {
   for (int o = kWave / 2; o >= 1; o >>= 1) x = imax64(x, __shfl_xor(x, o, kWave));
   return x;
 }
-__device__ __forceinline__ uint32_t wave_scan_acc(uint32_t x, int lane) {
-  return (uint32_t)wave_incl_scan32((int)x, lane);  // modulo 2^32
+__device__ __forceinline__ uint32_t wave_scan_acc(uint32_t x, int lane) {  // modulo 2^32
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t y = (uint32_t)__shfl_up((int)x, o, kWave);
+    if (lane >= o) x += y;
+  }
+  return x;
 }
 __device__ __forceinline__ int64_t wave_scan_acc(int64_t x, int lane) { return wave_incl_scan64(x, lane); }
 
