@@ -2369,17 +2369,39 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
   };
   const int64_t sub_pref = std::max<int64_t>(1, kRecordBudget / std::max<int64_t>(1, rec_per_cand));
   // the lane kernel keeps one wave per 64 candidates resident: large chunks
-  // (the fast path's budget, halved while it does not fit) fill the chip
-  // (the preferred layout for a caller's workspace; the pool path starts
-  // from what the device's memory allows now)
+  // (the fast path's chunk budget) fill the chip.  That is the preferred
+  // layout (a caller's workspace of that size gets it); the pool path fits
+  // the whole layout, record sets included, to seven eighths of the memory
+  // the call can get now: sub-chunks shrink first (down to a sixteenth of the
+  // chunk), then the chunk halves.
   const int64_t budget_pref = lanes ? kFastScratchBudget : kScratchBudget;
-  const int64_t budget0 = lanes ? ss_scratch_budget(g->device, g->pool, budget_pref) : budget_pref;
   const Plan ppref = plan_of(budget_pref / std::max<int64_t>(1, per_cand), sub_pref);
   const Plan pmin = plan_of(1, 1);
+  auto plan_fit = [&](int64_t bytes) {
+    if ((int64_t)ppref.total <= bytes) return ppref;
+    int64_t chunk = ppref.chunk;
+    for (;;) {
+      const int64_t lo0 = chunk > kWave ? std::max<int64_t>(1, std::min<int64_t>(ppref.sub, chunk / 16)) : 1;
+      if ((int64_t)plan_of(chunk, lo0).total <= bytes) {
+        int64_t lo = lo0, hi = std::max<int64_t>(lo0, ppref.sub);  // the largest sub-chunk cap that fits
+        while (lo < hi) {
+          const int64_t mid = lo + (hi - lo + 1) / 2;
+          if ((int64_t)plan_of(chunk, mid).total <= bytes)
+            lo = mid;
+          else
+            hi = mid - 1;
+        }
+        return plan_of(chunk, lo);
+      }
+      if (chunk <= 1) return pmin;
+      chunk = chunk > kWave ? chunk / 2 / kWave * kWave : chunk / 2;
+    }
+  };
+  const int64_t budget0 = ss_scratch_budget(g->device, g->pool, (int64_t)ppref.total, 7);
   if (W.query) {
     W.need_min = pmin.total;
     W.need_pref = ppref.total;
-    const Plan pq = W.single ? ppref : plan_of(budget0 / std::max<int64_t>(1, per_cand), sub_pref);
+    const Plan pq = W.single ? ppref : plan_fit(budget0);
     W.chunk = pq.chunk;
     W.sub = pq.sub;
     return SS_OK;
@@ -2403,21 +2425,13 @@ int ss_run_simulate_ready(const ss_gmg *g, SsPlace src, int64_t *makespan, int64
       return ss_set_error(SS_ERR_INVALID_ARG, "workspace of " + std::to_string(W.bytes) +
                                                    " bytes is smaller than this call's minimum of " +
                                                    std::to_string(pmin.total));
-    int64_t chunk = pl.chunk, sub_cap = pl.sub;
-    while (pl.total > W.bytes) {
-      if (sub_cap > 1 && plan_of(chunk, 1).total <= W.bytes) sub_cap = std::max<int64_t>(1, sub_cap / 2);
-      else {
-        chunk = std::max<int64_t>(1, chunk / 2);
-        sub_cap = std::min(sub_cap, chunk);
-      }
-      pl = plan_of(chunk, sub_cap);
-    }
+    pl = plan_fit((int64_t)W.bytes);
     scratch = W.ptr;
   } else {
     for (int64_t budget = budget0;; budget /= 2) {
-      pl = plan_of(budget / std::max<int64_t>(1, per_cand), sub_pref);
+      pl = plan_fit(budget);
       err = ss_scratch_get(g->device, g->pool, pl.total, stream, &scr);
-      if (err != hipErrorOutOfMemory || budget <= kScratchBudget / 4 || pl.chunk <= 1) break;
+      if (err != hipErrorOutOfMemory || pl.total <= pmin.total) break;
     }
     if (err != hipSuccess) return hip_fail(err, "allocating the simulation scratch");
     scratch = scr.p;

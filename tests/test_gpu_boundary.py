@@ -144,7 +144,8 @@ def test_workspace_reused_across_calls_and_sizes(dev):
         assert_same(run(h, P, dev, workspace=ws), ref, f"{nb} candidates")
 
 
-def test_pool_scratch_fits_the_memory_left(dev):
+@pytest.mark.parametrize("dispatch", ["index", "ready"])
+def test_pool_scratch_fits_the_memory_left(dev, dispatch):
     """With most of the device's memory held by the caller, a call sizes its
     own scratch to what is left: ss_simulate_chunking reports smaller
     memory-pass sub-chunks than with the memory free, and the results, computed
@@ -153,21 +154,22 @@ def test_pool_scratch_fits_the_memory_left(dev):
     h = ss.Gmg(g)
     nb = 8192
     P = synth.placements(g, 3, 0, nb)
-    ref = oracle.simulate_batch(g, P, n_threads=8)
+    mode = oracle.INDEX_ORDER if dispatch == "index" else oracle.READY_ORDER
+    ref = oracle.simulate_batch(g, P, dispatch=mode, n_threads=8)
     ss.release_cached_memory()
     torch.cuda.empty_cache()
-    roomy = ss.chunking(h, nb)
-    _, pref = ss.workspace_size(h, nb)
+    roomy = ss.chunking(h, nb, dispatch=dispatch)
+    _, pref = ss.workspace_size(h, nb, dispatch=dispatch)
     free, _ = torch.cuda.mem_get_info()
     left = pref // 2 + 3 * g.n_ops * nb  # about half the preferred scratch, plus the test's own tensors
     print(f"roomy chunking {roomy}, preferred scratch {pref / 1e9:.2f} GB, holding {(free - left) / 1e9:.1f} GB",
           flush=True)
     hold = torch.empty(free - left, dtype=torch.uint8, device=dev)
     try:
-        tight = ss.chunking(h, nb)
+        tight = ss.chunking(h, nb, dispatch=dispatch)
         print(f"tight chunking {tight}", flush=True)
         assert tight[0] <= roomy[0] and tight[1] < roomy[1], (roomy, tight)
-        assert_same(run(h, P, dev), ref, "scratch fitted to the memory left")
+        assert_same(run(h, P, dev, dispatch=dispatch), ref, f"scratch fitted to the memory left ({dispatch})")
     finally:
         del hold
         torch.cuda.empty_cache()
