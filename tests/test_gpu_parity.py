@@ -271,20 +271,26 @@ def test_horizon_beyond_32_bits_takes_general_path(dev, monkeypatch):
 
 
 @pytest.mark.parametrize("dispatch", ["index", "ready"])
-@pytest.mark.parametrize("case", ["wide", "scaled"])
+@pytest.mark.parametrize("case", ["wide", "scaled", "scaled_small", "mixed"])
 def test_byte_sums_beyond_32_bits(dev, monkeypatch, case, dispatch):
     """Output sizes near 2^31 on the 32-bit time path.  "wide": odd sizes, so
     no common power of two divides them and their sums pass 2^32 (the peak
     pass keeps 64-bit sums); "scaled": multiples of 2^20 whose sums pass 2^32
-    but whose sums divided by 2^20 do not (32-bit sums of the scaled sizes).
+    but whose sums divided by 2^20 do not (32-bit sums of the scaled sizes);
+    "scaled_small": multiples of 2^11 whose raw sums stay below 2^32 too;
+    "mixed": zero sizes beside sizes of 2^31 - 1 (64-bit sums).
     Capacities at each device's 90th-percentile peak leave some candidates
     feasible and make others overflow."""
     g = synth.random_gmg(40 + (case == "scaled"), n_ops=300, n_dev=6, n_req=3, n_slices=3, n_link=2)
     st = synth.Stream(41)
     if case == "wide":
         ob = [2 * st.uniform_int(1 << 29, (1 << 30) - 1) + 1 for _ in range(g.n_ops)]
-    else:
+    elif case == "scaled":
         ob = [st.uniform_int(1, 1 << 11) << 20 for _ in range(g.n_ops)]
+    elif case == "scaled_small":
+        ob = [st.uniform_int(1, 1 << 10) << 11 for _ in range(g.n_ops)]
+    else:
+        ob = [0 if st.uniform_int(0, 2) == 0 else (1 << 31) - 1 for _ in range(g.n_ops)]
     g.out_bytes = np.asarray(ob, np.int64)
     g.bw = np.asarray([1 << 20, 1 << 21], np.int64)  # transfers of about a millisecond keep times in 32 bits
     st2 = synth.Stream(43)
@@ -292,7 +298,7 @@ def test_byte_sums_beyond_32_bits(dev, monkeypatch, case, dispatch):
     mode = oracle.INDEX_ORDER if dispatch == "index" else oracle.READY_ORDER
     g.cap = np.full(g.n_dev, 1 << 62, np.int64)
     roomy = oracle.simulate_batch(g, P, dispatch=mode)
-    assert roomy["peak"].max() > (1 << 32)
+    assert case == "scaled_small" or roomy["peak"].max() > (1 << 32)
     g.cap = np.percentile(roomy["peak"], 90, axis=0).astype(np.int64)
     ref = oracle.simulate_batch(g, P, dispatch=mode)
     assert 0 < (ref["violation"] == 1).sum() < len(P)
