@@ -220,16 +220,20 @@ class Scheduler:
         self.handle = h
         self.n_ops, self.cap = int(g.n_ops), int(cap)
         self._ops = np.zeros(max(1, int(cap)), np.int64)
+        # reused per call: a run makes one round and one completion call per op
+        self._st, self._n, self._p = ctypes.c_int(), ctypes.c_int64(), ctypes.c_int64()
+        self._args = (ctypes.byref(self._st), self._ops.ctypes.data, ctypes.byref(self._n), ctypes.byref(self._p))
+        self._round, self._complete = lib().ss_sched_round, lib().ss_sched_complete
 
     def round(self, now, stream=None):
         """One round at time `now`: (status, batch ops, partition or -1)."""
-        st, n, p = ctypes.c_int(), ctypes.c_int64(), ctypes.c_int64()
-        _check(lib().ss_sched_round(self.handle, int(now), ctypes.byref(st), self._ops.ctypes.data,
-                                    ctypes.byref(n), ctypes.byref(p), _stream_ptr(stream)))
-        return st.value, self._ops[:n.value].tolist(), p.value
+        st, ops, n, p = self._args
+        _check(self._round(self.handle, int(now), st, ops, n, p, _stream_ptr(stream)))
+        k = self._n.value
+        return self._st.value, (self._ops[:k].tolist() if k else []), self._p.value
 
     def complete(self, op, t_done):
-        _check(lib().ss_sched_complete(self.handle, int(op), int(t_done)))
+        _check(self._complete(self.handle, int(op), int(t_done)))
 
     def state(self):
         """(state[n_ops] of SS_OP_*, place[n_ops], issue time[n_ops], completion time[n_ops])."""

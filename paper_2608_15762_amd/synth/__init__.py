@@ -63,6 +63,21 @@ def draw(key: int, n: int) -> int:
     return mix((key + (n + 1) * GAMMA) & M64)
 
 
+def mix_np(z: np.ndarray) -> np.ndarray:
+    """mix over a uint64 array (multiplications wrap modulo 2^64, as in mix)."""
+    z = np.asarray(z, np.uint64)
+    with np.errstate(over="ignore"):
+        z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+        z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+    return z ^ (z >> np.uint64(31))
+
+
+def draw_np(key, n: np.ndarray) -> np.ndarray:
+    """draw(key, n) for every n of an array (key an int or a uint64 array)."""
+    with np.errstate(over="ignore"):
+        return mix_np(np.asarray(key, np.uint64) + (np.asarray(n, np.uint64) + np.uint64(1)) * np.uint64(GAMMA))
+
+
 def below(x: int, n: int) -> int:
     """floor(x * n / 2^64): maps a 64-bit draw to [0, n)."""
     return (int(x) * int(n)) >> 64
@@ -536,29 +551,36 @@ class Executor:
         self.g = g
         self.key = key
         N = g.n_ops
-        self.issue_t = np.full(N, -1, np.int64)
-        self.dev = np.zeros(N, np.int64)
-        self.done_t = np.full(N, -1, np.int64)
-        self.waiting = np.zeros(N, np.int64)  # predecessors not yet completed
+        # plain lists: the loop runs once per completion
+        pp = np.asarray(g.pred_ptr).tolist()
+        pi = np.asarray(g.pred_idx).tolist()
+        self.preds = [pi[pp[v]:pp[v + 1]] for v in range(N)]
         self.succ = [[] for _ in range(N)]
         for v in range(N):
-            for u in g.pred_idx[g.pred_ptr[v]:g.pred_ptr[v + 1]]:
-                self.succ[int(u)].append(v)
-            self.waiting[v] = g.pred_ptr[v + 1] - g.pred_ptr[v]
+            for u in self.preds[v]:
+                self.succ[u].append(v)
+        self.waiting = [len(p) for p in self.preds]  # predecessors not yet completed
+        self.dur = np.asarray(g.dur).tolist()
+        self.dev_class = np.asarray(g.dev_class).tolist()
+        self.issue_t = [-1] * N
+        self.dev = [0] * N
+        self.done_t = [-1] * N
         self.events = []  # heap of (completion time, op)
+        # op v's factor: the first unit() of Stream(draw(key, 0xE7EC + v)), for all ops at once
+        x = draw_np(draw_np(key & M64, np.arange(N, dtype=np.uint64) + np.uint64(0xE7EC)), np.zeros(N, np.uint64))
+        self.factor = (((x >> np.uint64(11)) + np.uint64(1)).astype(np.float64) * (1.0 / (1 << 53))).tolist()
 
     def _start(self, v):
-        g = self.g
-        preds = g.pred_idx[g.pred_ptr[v]:g.pred_ptr[v + 1]]
-        t = max([int(self.issue_t[v])] + [int(self.done_t[u]) for u in preds])
-        w = int(g.dur[v, g.dev_class[self.dev[v]]])
-        f = Stream(draw(self.key, 0xE7EC + v)).unit()
-        heapq.heappush(self.events, (t + max(1, int(round(w * (0.75 + 0.5 * f)))), v))
+        t = self.issue_t[v]
+        for u in self.preds[v]:
+            t = max(t, self.done_t[u])
+        w = self.dur[v][self.dev_class[self.dev[v]]]
+        heapq.heappush(self.events, (t + max(1, int(round(w * (0.75 + 0.5 * self.factor[v])))), v))
 
     def issue(self, ops, devs, t: int):
         for v, d in zip(ops, devs):
             v = int(v)
-            self.issue_t[v] = t
+            self.issue_t[v] = int(t)
             self.dev[v] = int(d)
             if self.waiting[v] == 0:
                 self._start(v)
