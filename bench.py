@@ -507,7 +507,7 @@ def main():
         return sched_main(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the candidate batch shards "
-              "across GPUs by contiguous ranges but no multi-GPU run is part of this build.", file=sys.stderr)
+              "across GPUs by contiguous ranges, but this benchmark runs on one GPU only.", file=sys.stderr)
         sys.exit(2)
     import torch
 

@@ -26,7 +26,7 @@ extern "C" {
 #define SS_ERR_INVALID_GMG (-2)  /* the snapshot breaks a rule listed under ss_gmg_desc */
 #define SS_ERR_OOM (-3)          /* host or device allocation failed */
 #define SS_ERR_DEVICE (-4)       /* a HIP call or kernel launch failed */
-#define SS_ERR_UNSUPPORTED (-5)  /* valid input beyond this build's limits (see ss_gmg_desc) */
+#define SS_ERR_UNSUPPORTED (-5)  /* valid input beyond the library's limits (see ss_gmg_desc) */
 
 #define SS_TIME_INF INT64_MAX    /* end of a device's last (open) idle slice */
 
