@@ -211,13 +211,14 @@ __device__ __forceinline__ uint32_t xfer_of(const GmgView &G, int u, int du, int
 }
 
 // Software pipeline of the schedule, for target op T (one lane per candidate):
-//   T-4  load the op's device from the op-major placements;
-//   T-3  load finish time and device of its first kPipePre predecessors when
-//        they are op T-4 or older (op-major finish times written earlier by
-//        this lane);
-//   T-2  resolve each predecessor: ops T-3 and T-2 from a two-deep register
-//        history (op T-1's device is already loaded), the rest from the T-3
-//        loads, kept for step T; gather the link class of each predecessor
+//   T-4  load the op's device from the op-major placements, and the finish
+//        time and device of its first kPipePre predecessors when they are op
+//        T-5 or older (op-major finish times written earlier by this lane;
+//        two steps pass before they are used, which covers the latency of
+//        rows far back that have left the cache);
+//   T-2  resolve each predecessor: ops T-4, T-3 and T-2 from a three-deep
+//        register history (op T-1's device is already loaded), the rest from
+//        the T-4 loads, kept for step T; gather the link class of each predecessor
 //        transfer, the op's duration on its device, and the device's current
 //        slice end plus the next slice's bounds;
 //   T    ready time (only a predecessor T-1 still comes from the history),
@@ -323,8 +324,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     for (int i = 0; i < kPipePre; ++i) S.pf[q][i] = S.pd[q][i] = S.lc[q][i] = 0;
   }
 
-  // Results of the last two ops: h1 = op T (after its step), h2 before it.
-  uint32_t h1f = 0, h1d = 0, h2f = 0, h2d = 0;
+  // Results of the last three ops: h1 = op T (after its step), h2 and h3 before it.
+  uint32_t h1f = 0, h1d = 0, h2f = 0, h2d = 0, h3f = 0, h3d = 0;
 
   // Stage T-2 for target op t = T+2, after op T.
   auto stage2 = [&](auto qq, int T) {
@@ -339,14 +340,18 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
 #pragma unroll
     for (int i = 0; i < kPipePre; ++i) {
       const int u = (int)pred_of(p01, i);
-      const uint32_t du = u == T + 1 ? clampD(S.dq[q1]) : u == T ? h1d : u == T - 1 ? h2d : clampD(S.pd[q2][i]);
+      const uint32_t du = u == T + 1 ? clampD(S.dq[q1])
+                          : u == T   ? h1d
+                          : u == T - 1 ? h2d
+                          : u == T - 2 ? h3d
+                                       : clampD(S.pd[q2][i]);
       uint32_t lc;
       if (kLink == 0) lc = (uint32_t)lgrp[du] == gdt ? lsame : 1u - lsame;
       else if (kLink == 3) lc = du >> lshift == gdt ? lsame : 1u - lsame;
       else if (kLink == 1) lc = link_bit(G, du, dt);  // zero with one class
       else lc = G.link_class[du * D + dt];
       S.lc[q2][i] = lc;
-      const uint32_t fu = u == T ? h1f : u == T - 1 ? h2f : S.pf[q2][i];
+      const uint32_t fu = u == T ? h1f : u == T - 1 ? h2f : u == T - 2 ? h3f : S.pf[q2][i];
       // resolved for the step (a predecessor T+1 takes its finish from the
       // step's history; its device is already final)
       S.pd[q2][i] = du;
@@ -365,11 +370,11 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     S.le[q2] = e;
     S.lw[q2] = G.lut_w[e];
   };
-  // Stage T-3 for target op t = T+3: predecessors u <= T-1 (the others are
+  // Stage T-4 for target op t = T+4: predecessors u <= T-1 (the others are
   // forwarded from the register history when op t runs).
   auto stage3 = [&](auto qq, int T) {
-    constexpr int q3 = (decltype(qq)::value + 3) & 3;
-    const int t = min(T + 3, N - 1);
+    constexpr int q3 = decltype(qq)::value;
+    const int t = min(T + 4, N - 1);
     const uint32_t p01 = meta(kMetaP01, t);
 #pragma unroll
     for (int i = 0; i < kPipePre; ++i) {
@@ -384,7 +389,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   uint64_t sum = 0;
   stage2(std::integral_constant<int, 2>(), -2);
   stage2(std::integral_constant<int, 3>(), -1);
-  stage3(std::integral_constant<int, 3>(), -1);  // op 2: every predecessor comes from the history
+  stage3(std::integral_constant<int, 2>(), -2);  // ops 2 and 3: every predecessor comes from the history
+  stage3(std::integral_constant<int, 3>(), -1);
 
   auto step = [&](auto qq, int T) {
     constexpr int q0 = decltype(qq)::value;
@@ -463,6 +469,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     atomicMax(&comp[r * kWave + lane], f);
     ms = umax32(ms, f);
     sum += f;
+    h3f = h2f;
+    h3d = h2d;
     h2f = h1f;
     h2d = h1d;
     h1f = f;
