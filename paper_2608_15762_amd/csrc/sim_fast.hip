@@ -16,8 +16,8 @@
 // then per sub-chunk of candidates:
 //   fast_intervals one wave per candidate, lanes = consecutive ops (coalesced
 //                 row reads).  Pass A ranks every op among the ops of its
-//                 device (lanes sharing a device from one ballot per bit of
-//                 the device id) into a rank table and counts per device.
+//                 device (lanes sharing a device from a 64-bit lane mask per
+//                 device in LDS) into a rank table and counts per device.
 //                 Pass B writes every residency interval (Sec. 3.3.2) into a
 //                 per-device bucket: own outputs at their rank (so a device's
 //                 own intervals are start-sorted), one copy per (output,
@@ -1037,17 +1037,6 @@ __device__ void op_intervals(const GmgView &G, const uint8_t *prow, const uint32
   }
 }
 
-// Lanes whose key equals this lane's key, among the active lanes: one ballot
-// per key bit (keys below 2^nbits, nbits wave-uniform).
-__device__ __forceinline__ uint64_t same_key_lanes(int key, bool active, int nbits) {
-  uint64_t peers = (uint64_t)__ballot(active);
-  for (int b = 0; b < nbits; ++b) {
-    const uint64_t m = (uint64_t)__ballot((key >> b) & 1);
-    peers &= ((key >> b) & 1) ? m : ~m;
-  }
-  return peers;
-}
-
 // Per-candidate bucket geometry written by fast_intervals, read by fast_peaks.
 __device__ __forceinline__ int meta_stride(int D) { return 3 * (D + 1); }
 
@@ -1135,6 +1124,10 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
   uint32_t *fc = fq + kWave;                                    // [128] copy blocks to write
   int &fqn = *reinterpret_cast<int *>(fc + (kCpSt ? 2 * kWave : 0));
   int &fcn = *(&fqn + 1);
+  // pass A's masks of the lanes on each device: on the own-record stage (not
+  // used before pass B), else past the end
+  uint64_t *dmask = kStage ? reinterpret_cast<uint64_t *>(obuf)
+                           : reinterpret_cast<uint64_t *>((reinterpret_cast<uintptr_t>(&fcn + 1) + 7) & ~uintptr_t(7));
   const int D = G.n_dev, N = G.n_ops, E = G.pred_ptr[G.n_ops], K = G.n_link;
   const int lane = threadIdx.x;
   const int64_t j = blockIdx.x, c = j0 + j;
@@ -1149,10 +1142,10 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
   for (int d = lane; d < D; d += kWave) {
     cfill[d] = 0;
     base[d] = 0;
+    dmask[d] = 0;
   }
   wave_lds_fence();
   {
-    const int dbits = 32 - __builtin_clz((unsigned)max(D - 1, 1));  // bits of a device id
     int vn = min(lane, N - 1);
     uint32_t dn = N > 0 ? prow[vn] : 0, in = N > 0 ? indeg_f[vn] : 0;
     for (int v0 = 0; v0 < N; v0 += kWave) {
@@ -1163,9 +1156,18 @@ __global__ __launch_bounds__(kWave) void fast_intervals(const GmgView G, const u
       dn = prow[vn];
       in = indeg_f[vn];
       if (!kGivenRanks) {  // rank = ops of d so far + lower lanes of this chunk on d
-        const uint64_t peers = same_key_lanes(d, act, dbits);
-        if (act) rk[v] = (uint16_t)(base[d] + __builtin_amdgcn_mbcnt_hi((uint32_t)(peers >> 32),
-                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u)));
+        // the lanes on d: each lane sets its bit in d's mask, reads the mask
+        // back once every lane has, and clears it once every lane has read
+        // (a wave's LDS operations complete in order)
+        if (act) atomicOr(reinterpret_cast<unsigned long long *>(&dmask[d]), 1ull << lane);
+        wave_lds_fence();
+        const uint64_t peers = act ? dmask[d] : 0ull;
+        wave_lds_fence();
+        if (act) {
+          dmask[d] = 0;
+          rk[v] = (uint16_t)(base[d] + __builtin_amdgcn_mbcnt_hi((uint32_t)(peers >> 32),
+                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u)));
+        }
       }
       if (act) {  // counts: the order of these adds does not matter
         atomicAdd(&base[d], 1);
@@ -1978,7 +1980,8 @@ int mem_pass_join(MemPass &M, hipStream_t stream) {
 // with staged stores the open blocks of every device's buckets.
 size_t intervals_lds(int D, bool stage, bool stage_cp) {
   return (stage ? (size_t)D * kOwnRecs * sizeof(Rec) : 0) + (stage_cp ? (size_t)D * kCpRecs * sizeof(Rec) : 0) +
-         (size_t)(4 * D + 2 + 2 * kWave + (stage_cp ? 2 * kWave : 0) + 2) * sizeof(int);
+         (size_t)(4 * D + 2 + 2 * kWave + (stage_cp ? 2 * kWave : 0) + 2) * sizeof(int) +
+         (stage ? 0 : (size_t)D * 8 + 8);  // lane masks per device (on the own-record stage when staged)
 }
 
 // Residency intervals, then peaks, for the nb candidates of one chunk (their
