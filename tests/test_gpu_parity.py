@@ -154,6 +154,35 @@ def test_device_group_links(dev, path, case):
     assert_same(got, ref, label=f"device groups {case}")
 
 
+def test_predecessor_distances(dev, path):
+    """Predecessors 1 to 7 ops back, in pairs and alone.  The schedule takes
+    the nearest predecessors of an op from its register history and older
+    ones from rows it loaded steps before, so every distance meets each of
+    those paths (and the slices, with gaps, make the lookups do work)."""
+    n = 300
+    st = synth.Stream(9001)
+    edges = []
+    for v in range(1, n):
+        a = v - (1 + (v * 5) % 7)
+        b = v - (1 + (v // 7) % 7)
+        ps = {p for p in (a, b) if p >= 0}
+        if v % 11 == 0:
+            ps = {max(a, 0)}
+        edges += [(p, v) for p in sorted(ps)]
+    dur = [[st.uniform_int(1, 40)] for _ in range(n)]
+    out_b = [st.uniform_int(0, 900) for _ in range(n)]
+    slices = [[(0, 300 + 50 * d), (400 + 70 * d, 2000), (2100, TIME_INF)] for d in range(4)]
+    g = make_gmg(4, ["op"] * n, edges, [v % 2 for v in range(n)], dur, out_b, slices, [4200] * 4, [0, 25],
+                 [4000, 5000], bw=[7], lat=[3])
+    assert np.diff(g.pred_ptr).max() <= 2  # both predecessors go through the pipeline
+    P = np.array([[st.uniform_int(0, 3) for _ in range(n)] for _ in range(96)], np.uint8)
+    P[0] = 0
+    P[1] = np.arange(n) % 4
+    P[2] = (np.arange(n) // 5) % 4
+    ref = oracle.simulate_batch(g, P)
+    assert_same(gpu_run(ss.Gmg(g), P, dev), ref, label="predecessor distances")
+
+
 def test_scratch_reuse_across_streams(dev):
     """Calls on two streams with no host synchronisation between them: the
     smaller call on the second stream takes the first call's idle scratch
