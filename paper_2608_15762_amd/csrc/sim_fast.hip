@@ -10,9 +10,12 @@
 //                 slice that holds an op comes from a per-device time ->
 //                 slice lookup taken two ops ahead at a lower bound of the
 //                 op's finish.  The next ops' devices, predecessor values,
-//                 link classes and lookups are already in flight (a four-
-//                 stage software pipeline).  Finish times are written op-major.
-//   transpose     finish times back to candidate rows
+//                 link classes and lookups are already in flight (a
+//                 software pipeline).  Finish times are written op-major
+//                 (the schedule's own reads) and, eight ops at a time from an
+//                 LDS tile, into each candidate's row for the memory passes.
+//   transpose     finish times to candidate rows instead, when the row tile
+//                 would cost the schedule a wave per CU (or N % 4 != 0)
 // then per sub-chunk of candidates:
 //   fast_intervals one wave per candidate, lanes = consecutive ops (coalesced
 //                 row reads).  Pass A ranks every op among the ops of its
@@ -232,6 +235,7 @@ __device__ __forceinline__ uint32_t xfer_of(const GmgView &G, int u, int du, int
 // no branch around a memory operation and the compiler can keep the loads of
 // later stages in flight while op T waits only for its own.
 constexpr int kPipePre = 2;  // predecessors handled by the pipeline; more go through the CSR
+constexpr int kRowOps = 8;   // finish times a lane gathers in LDS before it writes them to its own row
 constexpr int kWindowStep = 32;  // ops per advance of the op-field window
 
 struct SchedPipe {
@@ -253,7 +257,7 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
                                                        int64_t nb,
                                                        uint32_t *__restrict__ finT, int64_t *__restrict__ makespan,
                                                        int64_t *__restrict__ sumfin, int64_t *__restrict__ slack,
-                                                       uint8_t *__restrict__ violation) {
+                                                       uint8_t *__restrict__ violation, uint32_t *__restrict__ finR) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   const int D = G.n_dev, N = G.n_ops, R = G.n_req, C = kOneClass ? 1 : G.n_class, K = G.n_link;
   const int lane = threadIdx.x;
@@ -262,6 +266,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   int32_t *sbase = reinterpret_cast<int32_t *>(comp + (size_t)R * kWave);  // [D+1] slice ranges of the devices
   int32_t *dcls = sbase + D + 1;                                          // [D] device class
   uint8_t *lgrp = reinterpret_cast<uint8_t *>(dcls + D);                  // [D] link group (kLink 0)
+  // with finR: the last kRowOps finish times of each lane, [op mod kRowOps][lane]
+  uint32_t *tile = reinterpret_cast<uint32_t *>(lgrp + (D + 3) / 4 * 4);
   for (int d = lane; d <= D; d += kWave) {
     sbase[d] = G.slice_ptr[d];
     if (d < D) dcls[d] = G.dev_class[d];
@@ -310,6 +316,7 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   const uint64_t nbu = (uint64_t)(uint32_t)nb;  // a chunk holds fewer than 2^32 candidates
   const uint8_t *const PTc = PT + c;
   uint32_t *const finTc = finT + c;
+  uint32_t *const finRc = finR ? finR + (uint64_t)(uint32_t)c * (uint32_t)N : nullptr;
   const uint64_t ppu = (uint64_t)ppitch;  // placement rows: the caller's op-major pitch, or the chunk's
   auto row = [&](int t) -> uint64_t { return (uint64_t)(uint32_t)t * nbu; };
   auto prow = [&](int t) -> uint64_t { return (uint64_t)(uint32_t)t * ppu; };
@@ -466,6 +473,15 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     const uint32_t f = s + w;
     clk[slot] = f;
     finTc[row(T)] = f;
+    if (finRc) {  // the candidate's own row, kRowOps finish times at a time
+      tile[(T & (kRowOps - 1)) * kWave + lane] = f;
+      if ((T & (kRowOps - 1)) == kRowOps - 1) {
+        const int b = T - (kRowOps - 1);
+        uint4 *dst = reinterpret_cast<uint4 *>(finRc + b);
+        dst[0] = make_uint4(tile[0 * kWave + lane], tile[1 * kWave + lane], tile[2 * kWave + lane], tile[3 * kWave + lane]);
+        dst[1] = make_uint4(tile[4 * kWave + lane], tile[5 * kWave + lane], tile[6 * kWave + lane], tile[7 * kWave + lane]);
+      }
+    }
     atomicMax(&comp[r * kWave + lane], f);
     ms = umax32(ms, f);
     sum += f;
@@ -509,6 +525,8 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
       if (T + 3 < N) step(std::integral_constant<int, 3>(), T + 3);
     }
   }
+  if (finRc)  // the last N mod kRowOps finish times
+    for (int k = 0; k < (N & (kRowOps - 1)); ++k) finRc[(N & ~(kRowOps - 1)) + k] = tile[k * kWave + lane];
   if (!live) return;
   if (invalid) {
     makespan[c] = INT64_MAX;
@@ -2065,6 +2083,11 @@ size_t ss_fast_schedule_lds(const ss_gmg *g) {
          (size_t)(g->n_dev + 3) / 4 * 4;
 }
 
+namespace {
+// with the row tile of a schedule that writes the candidates' finish rows
+size_t schedule_lds_rows(const ss_gmg *g) { return ss_fast_schedule_lds(g) + (size_t)kRowOps * kWave * 4; }
+}  // namespace
+
 // Scratch of one fast-path call, laid out for a chunk of `chunk` candidates
 // and memory-pass sub-chunks of `sub`.
 struct FastPlan {
@@ -2086,10 +2109,17 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
                          int64_t *slack, int64_t *sumfin, hipStream_t stream, SsWork &W) {
   const GmgView &G = g->view;
   const int64_t N = g->n_ops, E = g->n_edges, D = g->n_dev, R = g->n_req, B = src.B;
-  const size_t sched_lds = ss_fast_schedule_lds(g);
   int cus = 0;
   hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
+  int lds_cu = 0;
+  err = hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, g->device);
+  if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
+  // the schedule writes the candidates' finish-time rows itself (no
+  // transpose) when its row tile leaves as many waves per CU as without it
+  const bool sched_rows = N > 0 && N % 4 == 0 &&
+                          lds_cu / (int64_t)schedule_lds_rows(g) == lds_cu / (int64_t)ss_fast_schedule_lds(g);
+  const size_t sched_lds = sched_rows ? schedule_lds_rows(g) : ss_fast_schedule_lds(g);
   // kernel variant: link classes from device groups, a bit table or (more
   // than two classes) xfer32; in-degrees above the pipelined count go
   // through the predecessor CSR
@@ -2105,9 +2135,6 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
   // for the memory passes from op-major input), op-major and row-major finish
   // times
   const int64_t per_cand = N * (1 + 4 + 4);
-  int lds_cu = 0;
-  err = hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, g->device);
-  if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
   // A schedule launch is best a whole number of rounds of the waves the chip
   // holds at once (every wave runs about as long as any other).
   const int64_t round =
@@ -2286,17 +2313,17 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
       int64_t *ms_out = makespan + b0, *sf_out = sumfin ? sumfin + b0 : nullptr,
               *sl_out = slack ? slack + b0 * R : nullptr;
       uint8_t *vi_out = violation + b0;
+      uint32_t *rows_out = sched_rows ? fin : nullptr;
       void *args[] = {const_cast<GmgView *>(&G), &sched_P, &ppitch, const_cast<int64_t *>(&nb), &finT, &ms_out,
-                      &sf_out, &sl_out, &vi_out};
+                      &sf_out, &sl_out, &vi_out, &rows_out};
       const hipError_t le = hipLaunchKernel(sched_fn, dim3((unsigned)((nb + kWave - 1) / kWave)), dim3(kWave), args,
                                             sched_lds, stream);
       if (le != hipSuccess && rc == SS_OK) rc = hip_fail(le, "fast_schedule launch");
     }
     ss_timing_stop(ts, stream);
     if (!check("fast_schedule launch")) break;
-    SsTimingRec *tt = nullptr;
-    tt = ss_timing_start(SS_KERNEL_TRANSPOSE, stream);
-    if (N > 0) {  // op-major -> candidates' rows for the memory passes
+    if (N > 0 && !sched_rows) {  // op-major -> candidates' rows for the memory passes
+      SsTimingRec *tt = ss_timing_start(SS_KERNEL_TRANSPOSE, stream);
       if (N % 4 == 0 && nb % 4 == 0) {  // scratch buffers are 256-byte aligned
         const dim3 tg((unsigned)((nb + 63) / 64), (unsigned)((N + 64 * kStripTiles - 1) / (64 * kStripTiles)));
         hipLaunchKernelGGL(transpose_u32_strips, tg, dim3(256), 0, stream, static_cast<const uint32_t *>(finT),
@@ -2306,9 +2333,9 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
         hipLaunchKernelGGL(transpose_tiles<uint32_t>, tg, dim3(256), 0, stream, static_cast<const uint32_t *>(finT),
                            (int64_t)N, nb, nb, fin);
       }
+      ss_timing_stop(tt, stream);
+      if (!check("transpose launch")) break;
     }
-    ss_timing_stop(tt, stream);
-    if (!check("transpose launch")) break;
     rc = memory_passes(g, M, Pc, fin, nb, false, peak ? peak + b0 * D : nullptr, violation + b0, stream);
   }
   const int jrc = mem_pass_join(M, stream);
