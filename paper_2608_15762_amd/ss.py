@@ -296,7 +296,8 @@ def simulate_batch_into(g: Gmg, placements, makespan, violation, peak=None, slac
     dispatch: "index" (every device serves its ops in index order) or "ready"
     (earliest ready time first, SS_DISPATCH_READY).
     links: "latency" (a transfer takes its estimate from the producer's
-    finish) or "ports" (SS_LINK_PORTS, refused by the library for now).
+    finish) or "ports" (SS_LINK_PORTS: transfers arbitrated event by event
+    over each device's send and receive port; index-order dispatch only).
     workspace: None (the library's pool) or a device tensor whose memory
     becomes the call's scratch (ss_simulate_batch_ws)."""
     B, flags = _layout(g, placements, layout, dispatch, links)
