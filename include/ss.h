@@ -241,6 +241,19 @@ int ss_simulate_workspace_size(const ss_gmg *g, int64_t B, int layout, int64_t *
 int ss_simulate_chunking(const ss_gmg *g, int64_t B, int layout, int64_t *chunk, int64_t *sub);
 
 /*
+ * The width in bits of the integers a ss_simulate_batch call on g with these
+ * flags computes its simulated times in (Sec. 3.3.2-3.3.3; the results are
+ * the same either way): 32 when the loader proved that every time of the GMG
+ * fits in 32 bits and the call takes the 32-bit kernels (index-order or
+ * ready-time dispatch; byte sums are then 32-bit too when their bound allows
+ * it, else 64-bit), 64 on the general path (a GMG beyond 32 bits, a running
+ * schedule's state, SS_LINK_PORTS, or SS_PATH=generic in the environment).
+ * Launches nothing.  Errors: SS_ERR_INVALID_ARG (g or bits NULL, an unknown
+ * flag), SS_ERR_DEVICE, SS_ERR_UNSUPPORTED (as ss_simulate_batch would).
+ */
+int ss_simulate_time_bits(const ss_gmg *g, int layout, int *bits);
+
+/*
  * ss_simulate_batch with a caller-owned workspace: the same arguments and
  * results, plus `workspace`, a DEVICE buffer of workspace_bytes (256-byte
  * aligned, at least ss_simulate_workspace_size's min_bytes) that the call

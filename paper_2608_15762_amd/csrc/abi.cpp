@@ -131,6 +131,19 @@ extern "C" int ss_simulate_chunking(const ss_gmg *g, int64_t B, int layout, int6
   return SS_OK;
 }
 
+extern "C" int ss_simulate_time_bits(const ss_gmg *g, int layout, int *bits) {
+  ss_clear_error();
+  if (!bits) return ss_set_error(SS_ERR_INVALID_ARG, "ss_simulate_time_bits: bits is NULL");
+  *bits = 0;
+  SsPlace src;
+  bool ready = false, ports = false;
+  const int rc = check_simulate("ss_simulate_time_bits", g, nullptr, 0, layout, nullptr, nullptr, &src, &ready, &ports);
+  if (rc != SS_OK) return rc;
+  const int rd = check_device(g);
+  if (rd != SS_OK) return rd;
+  return ss_simulate_time_bits_of(g, ready, ports, bits);
+}
+
 extern "C" int ss_simulate_batch_ws(const ss_gmg *g, const uint8_t *placements, int64_t B, int layout,
                                     int64_t *out_makespan, int64_t *out_peak_mem, uint8_t *out_violation,
                                     int64_t *out_sla_slack, int64_t *out_sumfin, void *workspace,

@@ -1196,9 +1196,10 @@ static int run_simulate_generic(const ss_gmg *g, SsPlace src, int64_t *makespan,
 // (fast is still refused when the GMG does not qualify).  A GMG holding a
 // running schedule's state never qualifies: the loader keeps it off the 32-bit
 // tables, so it takes schedule_kernel and memory_kernel.
-int ss_run_simulate(const ss_gmg *g, SsPlace P, int64_t *makespan, int64_t *peak, uint8_t *violation,
-                    int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch, bool link_ports,
-                    SsWork &W) {
+// The kernels a call takes: the general int64 ones (generic), and with
+// transfer ports whether the memory pass is the 32-bit one.
+static int simulate_route(const ss_gmg *g, bool ready_dispatch, bool link_ports, bool *generic,
+                          bool *ports_mem_fast) {
   if (g->snapshot && (ready_dispatch || link_ports))
     return ss_set_error(SS_ERR_UNSUPPORTED,
                         "a running schedule's state (done_fin, issue_at, t_now) takes index-order dispatch and "
@@ -1215,9 +1216,25 @@ int ss_run_simulate(const ss_gmg *g, SsPlace P, int64_t *makespan, int64_t *peak
   // memory pass is the 32-bit one when the GMG fits the branch-free interval
   // writer (SS_PATH=generic: the general kernels throughout)
   const bool force_generic = path && std::strcmp(path, "generic") == 0;
-  const bool generic = !fast_ok || link_ports || force_generic;
-  const bool ports_mem_fast = link_ports && !force_generic && g->view.time32 && g->n_ops > 0 && g->n_class == 1 &&
-                              g->n_link <= 2 && g->max_outdeg <= 2 && g->view.succ2_pe;
+  *generic = !fast_ok || link_ports || force_generic;
+  *ports_mem_fast = link_ports && !force_generic && g->view.time32 && g->n_ops > 0 && g->n_class == 1 &&
+                    g->n_link <= 2 && g->max_outdeg <= 2 && g->view.succ2_pe;
+  return SS_OK;
+}
+
+int ss_simulate_time_bits_of(const ss_gmg *g, bool ready_dispatch, bool link_ports, int *bits) {
+  bool generic = false, ports_mem_fast = false;
+  const int rc = simulate_route(g, ready_dispatch, link_ports, &generic, &ports_mem_fast);
+  if (rc == SS_OK) *bits = generic ? 64 : 32;
+  return rc;
+}
+
+int ss_run_simulate(const ss_gmg *g, SsPlace P, int64_t *makespan, int64_t *peak, uint8_t *violation,
+                    int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch, bool link_ports,
+                    SsWork &W) {
+  bool generic = false, ports_mem_fast = false;
+  const int route = simulate_route(g, ready_dispatch, link_ports, &generic, &ports_mem_fast);
+  if (route != SS_OK) return route;
   if (generic)
     return run_simulate_generic(g, P, makespan, peak, violation, slack, sumfin, stream, ready_dispatch, link_ports, W,
                                 nullptr, nullptr, ports_mem_fast && !W.ptr && !W.query);

@@ -211,6 +211,9 @@ struct SsPlace {
 };
 
 // Kernel drivers (simulate.hip / select.hip).  Arguments are already checked.
+// The width of the integers (32 or 64) the simulation of a call with these
+// flags computes its times in.
+int ss_simulate_time_bits_of(const ss_gmg *g, bool ready_dispatch, bool link_ports, int *bits);
 int ss_run_simulate(const ss_gmg *g, SsPlace P, int64_t *makespan, int64_t *peak, uint8_t *violation,
                     int64_t *slack, int64_t *sumfin, hipStream_t stream, bool ready_dispatch, bool link_ports,
                     SsWork &W);

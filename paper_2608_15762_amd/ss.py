@@ -35,7 +35,7 @@ EXPORTED = ("ss_gmg_load", "ss_gmg_free", "ss_gmg_info", "ss_simulate_batch", "s
             "ss_est_predict", "ss_sched_create", "ss_sched_free", "ss_sched_round", "ss_sched_complete",
             "ss_sched_state", "ss_state_create", "ss_state_free", "ss_state_info", "ss_simulate_batch_resume",
             "ss_state_capture", "ss_release_cached_memory", "ss_simulate_workspace_size", "ss_simulate_batch_ws",
-            "ss_simulate_batch_noalloc", "ss_simulate_chunking")
+            "ss_simulate_batch_noalloc", "ss_simulate_chunking", "ss_simulate_time_bits")
 SS_OP_UNSCHEDULED, SS_OP_ISSUED, SS_OP_DONE = 0, 1, 2
 SS_ROUND_ISSUED, SS_ROUND_BUDGET, SS_ROUND_IDLE, SS_ROUND_INFEASIBLE = 0, 1, 2, 3
 SS_KERNEL_SCHEDULE, SS_KERNEL_MEMORY, SS_KERNEL_SELECT, SS_KERNEL_INTERVALS, SS_KERNEL_TRANSPOSE = 0, 1, 2, 3, 4
@@ -89,6 +89,8 @@ def lib():
             L.ss_simulate_batch_noalloc.restype = ctypes.c_int
             L.ss_simulate_chunking.argtypes = [P, I64, ctypes.c_int, P, P]
             L.ss_simulate_chunking.restype = ctypes.c_int
+            L.ss_simulate_time_bits.argtypes = [P, ctypes.c_int, P]
+            L.ss_simulate_time_bits.restype = ctypes.c_int
             L.ss_select_best.argtypes = [P, P, P, P, I64, ctypes.c_int, P, P]
             L.ss_select_best.restype = ctypes.c_int
             L.ss_kernel_timing.argtypes = [ctypes.c_int]
@@ -286,6 +288,15 @@ def chunking(g: Gmg, B: int, layout="row", dispatch="index") -> tuple[int, int]:
     _check(lib().ss_simulate_chunking(g.handle, B, LAYOUTS[layout] | DISPATCH[dispatch], ctypes.byref(c),
                                       ctypes.byref(s_)))
     return c.value, s_.value
+
+
+def time_bits(g: Gmg, dispatch="index", links="latency") -> int:
+    """ss_simulate_time_bits: 32 or 64, the width of the integers a
+    simulation of g with this dispatch rule and link model computes its
+    times in."""
+    b = ctypes.c_int()
+    _check(lib().ss_simulate_time_bits(g.handle, DISPATCH[dispatch] | LINKS[links], ctypes.byref(b)))
+    return b.value
 
 
 def simulate_batch_into(g: Gmg, placements, makespan, violation, peak=None, slack=None, sumfin=None,

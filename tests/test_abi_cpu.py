@@ -177,6 +177,18 @@ def test_unknown_layout_bits_are_rejected_before_the_device():
         assert b"SS_LINK_PORTS" in L.ss_last_error()
 
 
+def test_time_bits_checks_arguments_first():
+    L = ss.lib()
+    b = ctypes.c_int(9)
+    assert L.ss_simulate_time_bits(None, 0, ctypes.byref(b)) == -1 and b.value == 0
+    # a non-null dummy handle is never dereferenced: the argument and flag checks come first
+    assert L.ss_simulate_time_bits(ctypes.c_void_p(8), 0, None) == -1
+    for layout in (2, 0x400, 0x80):
+        assert L.ss_simulate_time_bits(ctypes.c_void_p(8), layout, ctypes.byref(b)) == -1
+        assert b"layout" in L.ss_last_error()
+    assert L.ss_simulate_time_bits(ctypes.c_void_p(8), 0x300, ctypes.byref(b)) == -5
+
+
 def test_workspace_entry_points_check_arguments_first():
     L = ss.lib()
     lo = ctypes.c_int64(7)

@@ -173,3 +173,21 @@ def test_pool_scratch_fits_the_memory_left(dev, dispatch):
     finally:
         del hold
         torch.cuda.empty_cache()
+
+
+def test_time_bits_follow_the_path(dev, monkeypatch):
+    """ss_simulate_time_bits names the integers the call computes its times
+    in: 32 on the 32-bit kernels, 64 on the general path."""
+    monkeypatch.delenv("SS_PATH", raising=False)
+    h = ss.Gmg(synth.build_gmg(4))
+    assert ss.time_bits(h) == 32
+    assert ss.time_bits(h, dispatch="ready") == 32
+    assert ss.time_bits(h, links="ports") == 64
+    monkeypatch.setenv("SS_PATH", "generic")
+    assert ss.time_bits(h) == 64
+    monkeypatch.delenv("SS_PATH")
+    g = random_gmg(11, n_ops=90, n_dev=4, n_req=2, n_slices=4, n_link=2, cap_scale=2000)
+    shift = 1 << 33  # slices beyond 2^32 us: the loader keeps the GMG off the 32-bit tables
+    g.slice_begin = g.slice_begin + shift
+    g.slice_end = np.where(g.slice_end == synth.TIME_INF, synth.TIME_INF, g.slice_end + shift)
+    assert ss.time_bits(ss.Gmg(g)) == 64
