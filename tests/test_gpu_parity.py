@@ -343,14 +343,26 @@ def gpu_select(h, viol, key, slack, require_sla, dev):
     return tuple(out.cpu().tolist())
 
 
-def test_select_best_on_tight_memory_workload(dev):
+@pytest.mark.parametrize("batch", ["own", "uniform"])
+def test_select_best_on_tight_memory_workload(dev, batch):
+    """The tight-memory workload's own candidates (a balanced base with a few
+    ops moved: about 1% violate) and uniform random placements over its 64
+    devices (about a quarter violate), simulated and then selected with both
+    keys, with and without the SLA condition."""
     g = synth.build_gmg(3)
     h = ss.Gmg(g)
-    P = synth.placements(g, 3, 0, 2000)
+    if batch == "own":
+        P = synth.placements(g, 3, 0, 2000)
+    else:
+        words = synth.draw_np(3003, np.arange(600 * g.n_ops)).reshape(600, g.n_ops)
+        P = (words % np.uint64(g.n_dev)).astype(np.uint8)
     got = gpu_run(h, P, dev)
     ref = oracle.simulate_batch(g, P, n_threads=8)
-    assert_same(got, ref, label="config 3 x 2000")
-    assert 0 < (ref["violation"] == 1).sum() < 2000
+    assert_same(got, ref, label=f"config 3, {batch} candidates")
+    n_viol = int((ref["violation"] == 1).sum())
+    assert 0 < n_viol < len(P)
+    if batch == "uniform":
+        assert n_viol > len(P) // 10
     for key in ("sumfin", "makespan"):
         for sla in (False, True):
             exp = oracle.select_best(ref["violation"], ref[key], ref["slack"], sla)
