@@ -12,10 +12,10 @@
 //                 op's finish.  The next ops' devices, predecessor values,
 //                 link classes and lookups are already in flight (a
 //                 software pipeline).  Finish times are written op-major
-//                 (the schedule's own reads) and, eight ops at a time from an
-//                 LDS tile, into each candidate's row for the memory passes.
-//   transpose     finish times to candidate rows instead, when the row tile
-//                 would cost the schedule a wave per CU (or N % 4 != 0)
+//                 (the schedule's own reads) and, eight ops at a time from
+//                 registers, into each candidate's row for the memory passes.
+//   transpose     finish times to candidate rows instead when N % 4 != 0
+//                 (rows not 16-byte aligned)
 // then per sub-chunk of candidates:
 //   fast_intervals one wave per candidate, lanes = consecutive ops (coalesced
 //                 row reads).  Pass A ranks every op among the ops of its
@@ -235,7 +235,7 @@ __device__ __forceinline__ uint32_t xfer_of(const GmgView &G, int u, int du, int
 // no branch around a memory operation and the compiler can keep the loads of
 // later stages in flight while op T waits only for its own.
 constexpr int kPipePre = 2;  // predecessors handled by the pipeline; more go through the CSR
-constexpr int kRowOps = 8;   // finish times a lane gathers in LDS before it writes them to its own row
+constexpr int kRowOps = 8;   // finish times a lane gathers in registers before it writes them to its own row
 constexpr int kWindowStep = 32;  // ops per advance of the op-field window
 
 struct SchedPipe {
@@ -266,8 +266,6 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
   int32_t *sbase = reinterpret_cast<int32_t *>(comp + (size_t)R * kWave);  // [D+1] slice ranges of the devices
   int32_t *dcls = sbase + D + 1;                                          // [D] device class
   uint8_t *lgrp = reinterpret_cast<uint8_t *>(dcls + D);                  // [D] link group (kLink 0)
-  // with finR: the last kRowOps finish times of each lane, [op mod kRowOps][lane]
-  uint32_t *tile = reinterpret_cast<uint32_t *>(lgrp + (D + 3) / 4 * 4);
   for (int d = lane; d <= D; d += kWave) {
     sbase[d] = G.slice_ptr[d];
     if (d < D) dcls[d] = G.dev_class[d];
@@ -331,6 +329,10 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     for (int i = 0; i < kPipePre; ++i) S.pf[q][i] = S.pd[q][i] = S.lc[q][i] = 0;
   }
 
+  // with finR: the lane's finish times of ops 8k .. 8k+7 (op T in slot T mod 8)
+  uint32_t rb[kRowOps];
+#pragma unroll
+  for (int k = 0; k < kRowOps; ++k) rb[k] = 0;
   // Results of the last three ops: h1 = op T (after its step), h2 and h3 before it.
   uint32_t h1f = 0, h1d = 0, h2f = 0, h2d = 0, h3f = 0, h3d = 0;
 
@@ -474,12 +476,15 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
     clk[slot] = f;
     finTc[row(T)] = f;
     if (finRc) {  // the candidate's own row, kRowOps finish times at a time
-      tile[(T & (kRowOps - 1)) * kWave + lane] = f;
-      if ((T & (kRowOps - 1)) == kRowOps - 1) {
-        const int b = T - (kRowOps - 1);
-        uint4 *dst = reinterpret_cast<uint4 *>(finRc + b);
-        dst[0] = make_uint4(tile[0 * kWave + lane], tile[1 * kWave + lane], tile[2 * kWave + lane], tile[3 * kWave + lane]);
-        dst[1] = make_uint4(tile[4 * kWave + lane], tile[5 * kWave + lane], tile[6 * kWave + lane], tile[7 * kWave + lane]);
+      // T mod 4 is q0 (steps come four to a block that starts at a multiple
+      // of 4), so the slot is q0 or q0 + 4 by the wave-uniform bit T & 4
+      const bool hi = (T & 4) != 0;
+      rb[q0] = hi ? rb[q0] : f;
+      rb[q0 + 4] = hi ? f : rb[q0 + 4];
+      if (q0 == 3 && hi) {
+        uint4 *dst = reinterpret_cast<uint4 *>(finRc + (T - (kRowOps - 1)));
+        dst[0] = make_uint4(rb[0], rb[1], rb[2], rb[3]);
+        dst[1] = make_uint4(rb[4], rb[5], rb[6], rb[7]);
       }
     }
     atomicMax(&comp[r * kWave + lane], f);
@@ -525,8 +530,11 @@ __global__ __launch_bounds__(kWave) void fast_schedule(const GmgView G, const ui
       if (T + 3 < N) step(std::integral_constant<int, 3>(), T + 3);
     }
   }
-  if (finRc)  // the last N mod kRowOps finish times
-    for (int k = 0; k < (N & (kRowOps - 1)); ++k) finRc[(N & ~(kRowOps - 1)) + k] = tile[k * kWave + lane];
+  if (finRc) {  // the last N mod kRowOps finish times
+#pragma unroll
+    for (int k = 0; k < kRowOps; ++k)
+      if (k < (N & (kRowOps - 1))) finRc[(N & ~(kRowOps - 1)) + k] = rb[k];
+  }
   if (!live) return;
   if (invalid) {
     makespan[c] = INT64_MAX;
@@ -2083,10 +2091,6 @@ size_t ss_fast_schedule_lds(const ss_gmg *g) {
          (size_t)(g->n_dev + 3) / 4 * 4;
 }
 
-namespace {
-// with the row tile of a schedule that writes the candidates' finish rows
-size_t schedule_lds_rows(const ss_gmg *g) { return ss_fast_schedule_lds(g) + (size_t)kRowOps * kWave * 4; }
-}  // namespace
 
 // Scratch of one fast-path call, laid out for a chunk of `chunk` candidates
 // and memory-pass sub-chunks of `sub`.
@@ -2116,10 +2120,9 @@ int ss_run_simulate_fast(const ss_gmg *g, SsPlace src, int64_t *makespan, int64_
   err = hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, g->device);
   if (err != hipSuccess) return hip_fail(err, "hipDeviceGetAttribute");
   // the schedule writes the candidates' finish-time rows itself (no
-  // transpose) when its row tile leaves as many waves per CU as without it
-  const bool sched_rows = N > 0 && N % 4 == 0 &&
-                          lds_cu / (int64_t)schedule_lds_rows(g) == lds_cu / (int64_t)ss_fast_schedule_lds(g);
-  const size_t sched_lds = sched_rows ? schedule_lds_rows(g) : ss_fast_schedule_lds(g);
+  // transpose) when each row is 16-byte aligned
+  const bool sched_rows = N > 0 && N % 4 == 0;
+  const size_t sched_lds = ss_fast_schedule_lds(g);
   // kernel variant: link classes from device groups, a bit table or (more
   // than two classes) xfer32; in-degrees above the pipelined count go
   // through the predecessor CSR
